@@ -1,0 +1,201 @@
+"""ctypes wrapper of the plain CPU oracle (pporacle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the package smoke check
+and by the bench's CPU-baseline leg.  The product path never imports it.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(_HERE, "pporacle.c")
+LIB = os.path.join(_HERE, "libpporacle.so")
+
+OK, E_ARG, E_TREE, E_RANGE, E_OVERFLOW, E_NOMEM = 0, -1, -2, -3, -4, -5
+F_NO_REFINE = 2
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with the host C compiler (no GPU code)."""
+    if force or not os.path.exists(LIB) or \
+            os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra",
+                        "-shared", "-fPIC", "-pthread", "-o", tmp, SRC],
+                       check=True)
+        os.replace(tmp, LIB)
+    return LIB
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build(force=False)
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32, i64, u32, u64 = (ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32,
+                              ctypes.c_uint64)
+        L.ppo_preorder.argtypes = [i32, P, P, P]
+        L.ppo_rooted_dp.argtypes = [i32, P, P, i32, P, P]
+        L.ppo_marginal.argtypes = [i32, i32, P, P, P, P, i32, P, P]
+        L.ppo_objective.argtypes = [i32, i32, P, P, P, P, P]
+        L.ppo_orders.argtypes = [i32, i32, u64, P, P]
+        L.ppo_num_starts.argtypes = [i32, i32]
+        L.ppo_num_starts.restype = i32
+        L.ppo_splitmix64_stream.argtypes = [u64, i32, P]
+        L.ppo_splitmix64_stream.restype = None
+        L.ppo_plan.argtypes = [i32, i32, P, P, P, P, P, i32, i32, u64, P, u32,
+                               i32, P, P, P, P, P, P, P, P]
+        for f in (L.ppo_preorder, L.ppo_rooted_dp, L.ppo_marginal,
+                  L.ppo_objective, L.ppo_orders, L.ppo_plan):
+            f.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle returned {code}")
+        self.code = code
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise OracleError(rc)
+
+
+def preorder(parent):
+    parent = _c(parent, np.int32)
+    n = parent.shape[0]
+    order = np.empty(n, np.int32)
+    nxt = np.empty(n, np.int32)
+    _check(lib().ppo_preorder(n, _p(parent), _p(order), _p(nxt)))
+    return order, nxt
+
+
+def rooted_dp(parent, profit, k):
+    parent = _c(parent, np.int32)
+    profit = _c(profit, np.int64)
+    n = parent.shape[0]
+    sel = np.zeros(n, np.uint8)
+    val = np.zeros(1, np.int64)
+    _check(lib().ppo_rooted_dp(n, _p(parent), _p(profit), int(k), _p(sel),
+                               _p(val)))
+    return sel, int(val[0])
+
+
+def marginal(demand, recompute_cost, fetch_cost, target, h):
+    demand = _c(demand, np.int64)
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    target = _c(target, np.uint8)
+    m, n = demand.shape
+    prof = np.zeros(n, np.int64)
+    g = np.zeros(1, np.int64)
+    _check(lib().ppo_marginal(n, m, _p(demand), _p(w), _p(f), _p(target),
+                              int(h), _p(prof), _p(g)))
+    return prof, int(g[0])
+
+
+def objective(demand, recompute_cost, fetch_cost, target) -> int:
+    demand = _c(demand, np.int64)
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    target = _c(target, np.uint8)
+    m, n = demand.shape
+    out = np.zeros(1, np.int64)
+    _check(lib().ppo_objective(n, m, _p(demand), _p(w), _p(f), _p(target),
+                               _p(out)))
+    return int(out[0])
+
+
+def num_starts(m: int, n_starts: int) -> int:
+    return int(lib().ppo_num_starts(m, n_starts))
+
+
+def orders(m, n_starts, order_seed, standalone):
+    st = _c(standalone, np.int64)
+    S = num_starts(m, n_starts)
+    out = np.zeros((S, m), np.int32)
+    _check(lib().ppo_orders(m, n_starts, ctypes.c_uint64(order_seed & (2**64 - 1)),
+                            _p(st), _p(out)))
+    return out
+
+
+def splitmix64_stream(seed: int, count: int) -> list[int]:
+    out = np.zeros(count, np.uint64)
+    lib().ppo_splitmix64_stream(ctypes.c_uint64(seed), count, _p(out))
+    return [int(x) for x in out]
+
+
+@dataclass
+class PlanResult:
+    target: np.ndarray          # uint8 [m][n]
+    objective: int
+    standalone: np.ndarray      # int64 [m]
+    orders: np.ndarray          # int32 [S][m]
+    start_objective: np.ndarray
+    start_sweeps: np.ndarray
+    start_accepts: np.ndarray
+    best_start: int
+    updates: int
+    dp_cells: int
+
+
+def plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=1,
+         max_rounds=0, order_seed=0, orders_in=None, flags=0, threads=1
+         ) -> PlanResult:
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.int64)
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    cap = _c(cap, np.int32)
+    m, n = demand.shape
+    S = num_starts(m, n_starts)
+    if orders_in is not None:
+        orders_in = _c(orders_in, np.int32)
+    tgt = np.zeros((m, n), np.uint8)
+    obj = np.zeros(1, np.int64)
+    st = np.zeros(m, np.int64)
+    ords = np.zeros((S, m), np.int32)
+    so = np.zeros(S, np.int64)
+    ss = np.zeros(S, np.int32)
+    sa = np.zeros(S, np.int32)
+    info = np.zeros(4, np.int64)
+    _check(lib().ppo_plan(n, m, _p(parent), _p(demand), _p(w), _p(f), _p(cap),
+                          int(n_starts), int(max_rounds),
+                          ctypes.c_uint64(order_seed & (2**64 - 1)),
+                          _p(orders_in), int(flags), int(threads), _p(tgt),
+                          _p(obj), _p(st), _p(ords), _p(so), _p(ss), _p(sa),
+                          _p(info)))
+    return PlanResult(target=tgt, objective=int(obj[0]), standalone=st,
+                      orders=ords, start_objective=so, start_sweeps=ss,
+                      start_accepts=sa, best_start=int(info[0]),
+                      updates=int(info[1]), dp_cells=int(info[2]))
+
+
+def plan_instance(inst, **kw) -> PlanResult:
+    """Plan a `workloads.Instance` with its own start/round/seed settings."""
+    args = dict(n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+                order_seed=inst.order_seed)
+    args.update(kw)
+    return plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                inst.cap, **args)

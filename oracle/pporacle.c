@@ -1,0 +1,753 @@
+/*
+ * pporacle.c -- plain CPU oracle of the PrefixPlace planner hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the tests, the package's smoke check and the bench's
+ * CPU-baseline leg use it.  It shares no code, header, table or helper with
+ * the HIP implementation.
+ *
+ * Everything here is the plain definition from the paper, in int64, with no
+ * blocking, fusion or incremental state:
+ *   - savings q_{m<-h}(b)                           Eq. (5), Sec. III-C
+ *   - objective F_pair(T), max over the empty set 0  Eq. (6), Sec. III-C
+ *   - worker marginal p_h(b) and v_m^{(-h)}(b)       Eq. (7), Proposition 1
+ *   - rooted-tree DP D[i,j] and its backtrack        Eq. (9), Theorem 1, Algorithm 1 (RootedDP)
+ *   - WorkerGreedy, coordinate refinement,
+ *     order-diverse starts, best-candidate return   Sec. IV-B/IV-C, Theorem 3, Algorithm 1 (PrefixPlace)
+ *
+ * Readings of points the paper leaves open (numbered as in the design notes):
+ *   R1  DP ties: take b_i only if strictly better; skip wins ties.
+ *   R2  preorder: roots, then children, in increasing node id.
+ *   R3  parent = -1 attaches to the no-cost dummy root; forests allowed.
+ *   R4  integer costs, so the refinement tolerance is 0 (strictly greater).
+ *   R5  the greedy pass adopts every DP result.
+ *   R6  standalone score of worker h = RootedDP value of p_h against the
+ *       empty placement; order 0 sorts by (score desc, worker id asc).
+ *   R7  order 1 = reverse of order 0; orders >= 2 are Fisher-Yates shuffles
+ *       driven by SplitMix64 seeded with order_seed + start index.
+ *   R8  n_starts > 0 overrides the paper's default start set; n_starts = 0
+ *       selects it (M <= 5: all M! orders, lexicographic; else 8 starts).
+ *   R9  max_rounds counts refinement sweeps including the last
+ *       non-improving one; 0 = until a sweep accepts nothing.
+ *   R10 ties between starts go to the earliest start.
+ *   R11 fetch_cost[h][h][*] is ignored (q_{h<-h} = w_h).
+ *   R13 capacity above n is capped to n.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <pthread.h>
+
+enum {
+    PPO_OK = 0,
+    PPO_E_ARG = -1,
+    PPO_E_TREE = -2,
+    PPO_E_RANGE = -3,
+    PPO_E_OVERFLOW = -4,
+    PPO_E_NOMEM = -5
+};
+
+enum { PPO_F_NO_REFINE = 2u };
+
+static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+
+/* ---------------------------------------------------------------- tree -- */
+
+/* Canonical preorder (R2, R3).  order[i] = node at 0-based position i;
+ * nextpos[i] = first position after the subtree of order[i] (Sec. IV-A:
+ * next(i), here 0-based).  Returns PPO_E_TREE if a parent is out of range,
+ * a node is its own parent, or some node never reaches a root (a cycle). */
+static int preorder(int32_t n, const int32_t *parent, int32_t *order,
+                    int32_t *nextpos)
+{
+    for (int32_t v = 0; v < n; v++) {
+        if (parent[v] < -1 || parent[v] >= n || parent[v] == v)
+            return PPO_E_TREE;
+    }
+    /* children lists, in increasing id because v is scanned upward */
+    int32_t *nchild = calloc((size_t)n + 1, sizeof(int32_t));
+    int32_t *start = malloc(((size_t)n + 1) * sizeof(int32_t));
+    int32_t *kids = malloc((size_t)n * sizeof(int32_t));
+    int32_t *fill = malloc(((size_t)n + 1) * sizeof(int32_t));
+    int32_t *stack = malloc((size_t)n * sizeof(int32_t));
+    int32_t *posof = malloc((size_t)n * sizeof(int32_t));
+    if (!nchild || !start || !kids || !fill || !stack || !posof) {
+        free(nchild); free(start); free(kids); free(fill); free(stack); free(posof);
+        return PPO_E_NOMEM;
+    }
+    /* slot n collects the roots (children of the dummy root) */
+    for (int32_t v = 0; v < n; v++)
+        nchild[parent[v] < 0 ? n : parent[v]]++;
+    start[0] = 0;
+    for (int32_t u = 0; u < n; u++)
+        start[u + 1] = start[u] + nchild[u];
+    /* roots occupy [start[n], start[n] + nchild[n]) */
+    for (int32_t u = 0; u <= n; u++)
+        fill[u] = start[u];
+    for (int32_t v = 0; v < n; v++) {
+        int32_t u = parent[v] < 0 ? n : parent[v];
+        kids[fill[u]++] = v;
+    }
+    int32_t top = 0, pos = 0;
+    for (int32_t r = nchild[n] - 1; r >= 0; r--)
+        stack[top++] = kids[start[n] + r];
+    while (top > 0) {
+        int32_t v = stack[--top];
+        posof[v] = pos;
+        order[pos++] = v;
+        for (int32_t c = nchild[v] - 1; c >= 0; c--)
+            stack[top++] = kids[start[v] + c];
+    }
+    int rc = PPO_OK;
+    if (pos != n) {
+        rc = PPO_E_TREE; /* nodes on a cycle are never reached from a root */
+    } else {
+        /* subtree sizes, accumulated in reverse preorder */
+        int32_t *size = stack; /* reuse */
+        for (int32_t i = 0; i < n; i++)
+            size[i] = 1;
+        for (int32_t i = n - 1; i >= 0; i--) {
+            int32_t v = order[i];
+            if (parent[v] >= 0)
+                size[posof[parent[v]]] += size[i];
+        }
+        for (int32_t i = 0; i < n; i++)
+            nextpos[i] = i + size[i];
+    }
+    free(nchild); free(start); free(kids); free(fill); free(stack); free(posof);
+    return rc;
+}
+
+/* ----------------------------------------------------------- RootedDP -- */
+
+/* Eq. (9) with 1-based preorder positions i = 1..n, nxt(i) = next(i):
+ *   D[i][j] = max(D[next(i)][j], p(b_i) + D[i+1][j-1]),
+ *   D[n+1][j] = 0, D[i][0] = 0.
+ * The whole (n+2) x (k'+1) table is kept (Theorem 1: O(nk) memory), and the
+ * backtrack compares table values (R1: take only if strictly better).
+ * profit_pos[i-1] is p(b_i); sel_pos[i-1] is set to 1 for chosen b_i. */
+static int rooted_dp_pos(int32_t n, const int32_t *nextpos,
+                         const int64_t *profit_pos, int32_t k,
+                         uint8_t *sel_pos, int64_t *value)
+{
+    int64_t kk = k < n ? k : n; /* R13 */
+    memset(sel_pos, 0, (size_t)n);
+    if (kk <= 0) {
+        *value = 0;
+        return PPO_OK;
+    }
+    size_t W = (size_t)kk + 1;
+    int64_t *D = calloc(((size_t)n + 2) * W, sizeof(int64_t));
+    if (!D)
+        return PPO_E_NOMEM;
+#define CELL(i, j) D[(size_t)(i) * W + (size_t)(j)]
+    for (int64_t i = n; i >= 1; i--) {
+        int64_t nx = (int64_t)nextpos[i - 1] + 1; /* 1-based next(i) */
+        int64_t p = profit_pos[i - 1];
+        for (int64_t j = 1; j <= kk; j++) {
+            int64_t s = CELL(nx, j);          /* skip b_i and its subtree */
+            int64_t t = p + CELL(i + 1, j - 1); /* take b_i */
+            CELL(i, j) = max64(s, t);
+        }
+    }
+    *value = CELL(1, kk);
+    int64_t i = 1, j = kk;
+    while (i <= n && j > 0) {
+        int64_t nx = (int64_t)nextpos[i - 1] + 1;
+        int64_t s = CELL(nx, j);
+        int64_t t = profit_pos[i - 1] + CELL(i + 1, j - 1);
+        if (t > s) {
+            sel_pos[i - 1] = 1;
+            i += 1;
+            j -= 1;
+        } else {
+            i = nx;
+        }
+    }
+#undef CELL
+    free(D);
+    return PPO_OK;
+}
+
+/* ------------------------------------------------------------ savings -- */
+
+/* Eq. (5): q_{m<-h}(b) = w_m(b) if h == m, else [w_m(b) - f_{m<-h}(b)]_+.
+ * fetch is laid out [src=h][dst=m][b]. */
+static int64_t q_save(int32_t n, int32_t m, const int64_t *w, const int64_t *f,
+                      int32_t h, int32_t req, int32_t b)
+{
+    int64_t wm = w[(size_t)req * n + b];
+    if (h == req)
+        return wm;
+    int64_t fh = f[((size_t)h * m + req) * n + b];
+    return max64(wm - fh, 0);
+}
+
+/* Eq. (6): G(T) = sum_b sum_m Lambda_m(b) * max({q_{m<-h}(b) : b in T_h} u {0}). */
+static int64_t objective_full(int32_t n, int32_t m, const int64_t *lam,
+                              const int64_t *w, const int64_t *f,
+                              const uint8_t *tgt)
+{
+    int64_t g = 0;
+    for (int32_t b = 0; b < n; b++) {
+        for (int32_t r = 0; r < m; r++) {
+            int64_t best = 0;
+            for (int32_t h = 0; h < m; h++)
+                if (tgt[(size_t)h * n + b])
+                    best = max64(best, q_save(n, m, w, f, h, r, b));
+            g += lam[(size_t)r * n + b] * best;
+        }
+    }
+    return g;
+}
+
+/* Eq. (7) / Proposition 1: with every worker but h fixed,
+ *   v_m(b) = max({q_{m<-l}(b) : l != h, b in T_l} u {0}),
+ *   p_h(b) = sum_m Lambda_m(b) [q_{m<-h}(b) - v_m(b)]_+,
+ * and G(T_{-h}) = sum_{m,b} Lambda_m(b) v_m(b). */
+static void marginal_full(int32_t n, int32_t m, const int64_t *lam,
+                          const int64_t *w, const int64_t *f,
+                          const uint8_t *tgt, int32_t h, int64_t *profit,
+                          int64_t *g_without)
+{
+    int64_t g = 0;
+    for (int32_t b = 0; b < n; b++) {
+        int64_t p = 0;
+        for (int32_t r = 0; r < m; r++) {
+            int64_t v = 0;
+            for (int32_t l = 0; l < m; l++)
+                if (l != h && tgt[(size_t)l * n + b])
+                    v = max64(v, q_save(n, m, w, f, l, r, b));
+            int64_t L = lam[(size_t)r * n + b];
+            p += L * max64(q_save(n, m, w, f, h, r, b) - v, 0);
+            g += L * v;
+        }
+        profit[b] = p;
+    }
+    if (g_without)
+        *g_without = g;
+}
+
+/* --------------------------------------------------------- validation -- */
+
+static int validate(int32_t n, int32_t m, const int32_t *parent,
+                    const int64_t *lam, const int64_t *w, const int64_t *f,
+                    const int32_t *cap)
+{
+    if (n < 1 || m < 1 || m > 255 || !parent || !lam || !w || !f || !cap)
+        return PPO_E_ARG;
+    for (int32_t v = 0; v < n; v++)
+        if (parent[v] < -1 || parent[v] >= n || parent[v] == v)
+            return PPO_E_TREE;
+    size_t mn = (size_t)m * n;
+    for (size_t x = 0; x < mn; x++)
+        if (lam[x] < 0 || w[x] < 0)
+            return PPO_E_RANGE;
+    for (size_t x = 0; x < mn * (size_t)m; x++)
+        if (f[x] < 0)
+            return PPO_E_RANGE;
+    for (int32_t r = 0; r < m; r++)
+        if (cap[r] < 0)
+            return PPO_E_RANGE;
+    /* every p, D and G value is at most sum Lambda * w; it must fit int64 */
+    unsigned __int128 tot = 0;
+    for (size_t x = 0; x < mn; x++) {
+        tot += (unsigned __int128)(uint64_t)lam[x] * (uint64_t)w[x];
+        if (tot > (unsigned __int128)INT64_MAX)
+            return PPO_E_OVERFLOW;
+    }
+    return PPO_OK;
+}
+
+/* Value checks shared by the entry points that take no tree. */
+static int validate_values(int32_t n, int32_t m, const int64_t *lam,
+                           const int64_t *w, const int64_t *f)
+{
+    size_t mn = (size_t)m * n;
+    for (size_t x = 0; x < mn; x++)
+        if (lam[x] < 0 || w[x] < 0)
+            return PPO_E_RANGE;
+    for (size_t x = 0; x < mn * (size_t)m; x++)
+        if (f[x] < 0)
+            return PPO_E_RANGE;
+    unsigned __int128 tot = 0;
+    for (size_t x = 0; x < mn; x++) {
+        tot += (unsigned __int128)(uint64_t)lam[x] * (uint64_t)w[x];
+        if (tot > (unsigned __int128)INT64_MAX)
+            return PPO_E_OVERFLOW;
+    }
+    return PPO_OK;
+}
+
+/* ------------------------------------------------------------- orders -- */
+
+/* SplitMix64 (Steele, Lea & Flood, OOPSLA 2014), in the published form. */
+static uint64_t splitmix64(uint64_t *x)
+{
+    uint64_t z = (*x += 0x9e3779b97f4a7c15ULL);
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+
+/* Lexicographic successor of a permutation; returns 0 after the last one. */
+static int next_perm(int32_t *a, int32_t m)
+{
+    int32_t i = m - 2;
+    while (i >= 0 && a[i] >= a[i + 1])
+        i--;
+    if (i < 0)
+        return 0;
+    int32_t j = m - 1;
+    while (a[j] <= a[i])
+        j--;
+    int32_t t = a[i]; a[i] = a[j]; a[j] = t;
+    for (int32_t l = i + 1, r = m - 1; l < r; l++, r--) {
+        t = a[l]; a[l] = a[r]; a[r] = t;
+    }
+    return 1;
+}
+
+static int64_t factorial(int32_t m)
+{
+    int64_t f = 1;
+    for (int32_t i = 2; i <= m; i++)
+        f *= i;
+    return f;
+}
+
+/* Number of starts the options select (R8). */
+int32_t ppo_num_starts(int32_t m, int32_t n_starts)
+{
+    if (n_starts > 0)
+        return n_starts;
+    if (m <= 5)
+        return (int32_t)factorial(m);
+    return 8;
+}
+
+/* Start orders (Sec. IV-C; R6-R8).  standalone[h] is worker h's score. */
+int ppo_orders(int32_t m, int32_t n_starts, uint64_t order_seed,
+               const int64_t *standalone, int32_t *orders)
+{
+    if (m < 1 || m > 255 || n_starts < 0 || !standalone || !orders)
+        return PPO_E_ARG;
+    int32_t S = ppo_num_starts(m, n_starts);
+    if (n_starts == 0 && m <= 5) {
+        int32_t *a = orders;
+        for (int32_t h = 0; h < m; h++)
+            a[h] = h;
+        for (int32_t s = 1; s < S; s++) {
+            memcpy(orders + (size_t)s * m, orders + (size_t)(s - 1) * m,
+                   (size_t)m * sizeof(int32_t));
+            next_perm(orders + (size_t)s * m, m);
+        }
+        return PPO_OK;
+    }
+    /* order 0: score descending, then id ascending (selection sort) */
+    int32_t *o0 = orders;
+    for (int32_t h = 0; h < m; h++)
+        o0[h] = h;
+    for (int32_t a = 0; a < m; a++) {
+        int32_t best = a;
+        for (int32_t c = a + 1; c < m; c++) {
+            int64_t sc = standalone[o0[c]], sb = standalone[o0[best]];
+            if (sc > sb || (sc == sb && o0[c] < o0[best]))
+                best = c;
+        }
+        int32_t t = o0[a]; o0[a] = o0[best]; o0[best] = t;
+    }
+    for (int32_t s = 1; s < S; s++) {
+        int32_t *o = orders + (size_t)s * m;
+        if (s == 1) {
+            for (int32_t h = 0; h < m; h++)
+                o[h] = o0[m - 1 - h];
+        } else {
+            uint64_t x = order_seed + (uint64_t)s;
+            for (int32_t h = 0; h < m; h++)
+                o[h] = h;
+            for (int32_t i = m - 1; i >= 1; i--) {
+                int32_t j = (int32_t)(splitmix64(&x) % (uint64_t)(i + 1));
+                int32_t t = o[i]; o[i] = o[j]; o[j] = t;
+            }
+        }
+    }
+    return PPO_OK;
+}
+
+/* Raw SplitMix64 stream, exported so tests can pin it to published values. */
+void ppo_splitmix64_stream(uint64_t seed, int32_t count, uint64_t *out)
+{
+    uint64_t x = seed;
+    for (int32_t i = 0; i < count; i++)
+        out[i] = splitmix64(&x);
+}
+
+/* ----------------------------------------------------- per-kernel ABI -- */
+
+int ppo_preorder(int32_t n, const int32_t *parent, int32_t *order,
+                 int32_t *nextpos)
+{
+    if (n < 1 || !parent || !order || !nextpos)
+        return PPO_E_ARG;
+    return preorder(n, parent, order, nextpos);
+}
+
+/* One exact rooted-tree solve in caller ids (Theorem 1). */
+int ppo_rooted_dp(int32_t n, const int32_t *parent, const int64_t *profit,
+                  int32_t k, uint8_t *selected, int64_t *value)
+{
+    if (n < 1 || !parent || !profit || !selected || !value || k < 0)
+        return PPO_E_ARG;
+    for (int32_t b = 0; b < n; b++)
+        if (profit[b] < 0)
+            return PPO_E_RANGE;
+    int32_t *order = malloc((size_t)n * sizeof(int32_t));
+    int32_t *nextpos = malloc((size_t)n * sizeof(int32_t));
+    int64_t *pp = malloc((size_t)n * sizeof(int64_t));
+    uint8_t *sp = malloc((size_t)n);
+    int rc = PPO_E_NOMEM;
+    if (order && nextpos && pp && sp) {
+        rc = preorder(n, parent, order, nextpos);
+        if (rc == PPO_OK) {
+            /* sum of profits must fit int64 */
+            unsigned __int128 tot = 0;
+            for (int32_t b = 0; b < n; b++)
+                tot += (uint64_t)profit[b];
+            if (tot > (unsigned __int128)INT64_MAX)
+                rc = PPO_E_OVERFLOW;
+        }
+        if (rc == PPO_OK) {
+            for (int32_t i = 0; i < n; i++)
+                pp[i] = profit[order[i]];
+            int64_t val = 0;
+            rc = rooted_dp_pos(n, nextpos, pp, k, sp, &val);
+            if (rc == PPO_OK) {
+                for (int32_t i = 0; i < n; i++)
+                    selected[order[i]] = sp[i];
+                *value = val;
+            }
+        }
+    }
+    free(order); free(nextpos); free(pp); free(sp);
+    return rc;
+}
+
+int ppo_marginal(int32_t n, int32_t m, const int64_t *demand,
+                 const int64_t *recompute_cost, const int64_t *fetch_cost,
+                 const uint8_t *target, int32_t h, int64_t *profit,
+                 int64_t *g_without_h)
+{
+    if (n < 1 || m < 1 || m > 255 || !demand || !recompute_cost ||
+        !fetch_cost || !target || !profit || h < 0 || h >= m)
+        return PPO_E_ARG;
+    int rc = validate_values(n, m, demand, recompute_cost, fetch_cost);
+    if (rc != PPO_OK)
+        return rc;
+    marginal_full(n, m, demand, recompute_cost, fetch_cost, target, h, profit,
+                  g_without_h);
+    return PPO_OK;
+}
+
+int ppo_objective(int32_t n, int32_t m, const int64_t *demand,
+                  const int64_t *recompute_cost, const int64_t *fetch_cost,
+                  const uint8_t *target, int64_t *objective)
+{
+    if (n < 1 || m < 1 || m > 255 || !demand || !recompute_cost ||
+        !fetch_cost || !target || !objective)
+        return PPO_E_ARG;
+    int rc = validate_values(n, m, demand, recompute_cost, fetch_cost);
+    if (rc != PPO_OK)
+        return rc;
+    *objective = objective_full(n, m, demand, recompute_cost, fetch_cost,
+                                target);
+    return PPO_OK;
+}
+
+/* --------------------------------------------------------------- plan -- */
+
+typedef struct {
+    int32_t n, m;
+    const int64_t *lam, *w, *f;
+    const int32_t *cap;
+    const int32_t *order, *nextpos;
+    int32_t max_rounds;
+    uint32_t flags;
+} plan_in;
+
+/* one worker update: p = marginal(h, T) with T_h treated as empty, then
+ * RootedDP(p, k_h); writes the chosen set into cand (caller ids). */
+static int worker_update(const plan_in *in, const uint8_t *tgt, int32_t h,
+                         int64_t *profit, int64_t *pp, uint8_t *sp,
+                         uint8_t *cand, int64_t *dpval)
+{
+    int32_t n = in->n;
+    marginal_full(n, in->m, in->lam, in->w, in->f, tgt, h, profit, NULL);
+    for (int32_t i = 0; i < n; i++)
+        pp[i] = profit[in->order[i]];
+    int rc = rooted_dp_pos(n, in->nextpos, pp, in->cap[h], sp, dpval);
+    if (rc != PPO_OK)
+        return rc;
+    for (int32_t i = 0; i < n; i++)
+        cand[in->order[i]] = sp[i];
+    return PPO_OK;
+}
+
+/* Algorithm 1, one start: WorkerGreedy in the fixed order, then coordinate
+ * refinement sweeps that accept only strict improvements of G (R4, R5, R9). */
+static int run_start(const plan_in *in, const int32_t *pi, uint8_t *tgt,
+                     int64_t *obj, int32_t *sweeps, int32_t *accepts)
+{
+    int32_t n = in->n, m = in->m;
+    int64_t *profit = malloc((size_t)n * sizeof(int64_t));
+    int64_t *pp = malloc((size_t)n * sizeof(int64_t));
+    uint8_t *sp = malloc((size_t)n);
+    uint8_t *cand = malloc((size_t)n);
+    uint8_t *old = malloc((size_t)n);
+    int rc = PPO_E_NOMEM;
+    if (!profit || !pp || !sp || !cand || !old)
+        goto out;
+    memset(tgt, 0, (size_t)m * n);
+    int64_t v;
+    for (int32_t a = 0; a < m; a++) {  /* greedy pass: always adopt */
+        int32_t h = pi[a];
+        rc = worker_update(in, tgt, h, profit, pp, sp, cand, &v);
+        if (rc != PPO_OK)
+            goto out;
+        memcpy(tgt + (size_t)h * n, cand, (size_t)n);
+    }
+    int32_t r = 0, acc = 0;
+    if (!(in->flags & PPO_F_NO_REFINE)) {
+        int improved;
+        do {
+            improved = 0;
+            for (int32_t a = 0; a < m; a++) {
+                int32_t h = pi[a];
+                int64_t g_old = objective_full(n, m, in->lam, in->w, in->f, tgt);
+                uint8_t *th = tgt + (size_t)h * n;
+                memcpy(old, th, (size_t)n);
+                memset(th, 0, (size_t)n);
+                rc = worker_update(in, tgt, h, profit, pp, sp, cand, &v);
+                if (rc != PPO_OK)
+                    goto out;
+                memcpy(th, cand, (size_t)n);
+                int64_t g_new = objective_full(n, m, in->lam, in->w, in->f, tgt);
+                if (g_new > g_old) {
+                    improved = 1;
+                    acc++;
+                } else {
+                    memcpy(th, old, (size_t)n);
+                }
+            }
+            r++;
+        } while (improved && !(in->max_rounds > 0 && r == in->max_rounds));
+    }
+    *obj = objective_full(n, m, in->lam, in->w, in->f, tgt);
+    *sweeps = r;
+    *accepts = acc;
+    rc = PPO_OK;
+out:
+    free(profit); free(pp); free(sp); free(cand); free(old);
+    return rc;
+}
+
+typedef struct {
+    const plan_in *in;
+    int32_t S;
+    const int32_t *orders;
+    uint8_t *tgts;        /* [S][m][n] */
+    int64_t *obj;
+    int32_t *sweeps, *accepts;
+    int *rcs;
+    /* standalone phase */
+    int64_t *standalone;
+    int phase;
+    int32_t next_job;
+    pthread_mutex_t mu;
+} plan_work;
+
+static int32_t take_job(plan_work *pw, int32_t limit)
+{
+    pthread_mutex_lock(&pw->mu);
+    int32_t j = pw->next_job < limit ? pw->next_job++ : -1;
+    pthread_mutex_unlock(&pw->mu);
+    return j;
+}
+
+static void *plan_worker(void *arg)
+{
+    plan_work *pw = arg;
+    const plan_in *in = pw->in;
+    int32_t n = in->n, m = in->m;
+    if (pw->phase == 0) {
+        /* R6: standalone score = DP value of p_h against the empty placement */
+        uint8_t *empty = calloc((size_t)m * n, 1);
+        int64_t *profit = malloc((size_t)n * sizeof(int64_t));
+        int64_t *pp = malloc((size_t)n * sizeof(int64_t));
+        uint8_t *sp = malloc((size_t)n);
+        uint8_t *cand = malloc((size_t)n);
+        int32_t h;
+        while ((h = take_job(pw, m)) >= 0) {
+            if (!empty || !profit || !pp || !sp || !cand) {
+                pw->rcs[h] = PPO_E_NOMEM;
+                continue;
+            }
+            pw->rcs[h] = worker_update(in, empty, h, profit, pp, sp, cand,
+                                       &pw->standalone[h]);
+        }
+        free(empty); free(profit); free(pp); free(sp); free(cand);
+    } else {
+        int32_t s;
+        while ((s = take_job(pw, pw->S)) >= 0)
+            pw->rcs[s] = run_start(in, pw->orders + (size_t)s * m,
+                                   pw->tgts + (size_t)s * m * n, &pw->obj[s],
+                                   &pw->sweeps[s], &pw->accepts[s]);
+    }
+    return NULL;
+}
+
+static int run_phase(plan_work *pw, int phase, int32_t jobs, int32_t threads)
+{
+    pw->phase = phase;
+    pw->next_job = 0;
+    int32_t T = threads < 1 ? 1 : threads;
+    if (T > jobs)
+        T = jobs;
+    pthread_t *tid = malloc((size_t)T * sizeof(pthread_t));
+    if (!tid)
+        return PPO_E_NOMEM;
+    int32_t started = 0;
+    for (int32_t t = 0; t < T; t++) {
+        if (pthread_create(&tid[t], NULL, plan_worker, pw) != 0)
+            break;
+        started++;
+    }
+    if (started == 0)
+        plan_worker(pw);
+    for (int32_t t = 0; t < started; t++)
+        pthread_join(tid[t], NULL);
+    free(tid);
+    for (int32_t j = 0; j < jobs; j++)
+        if (pw->rcs[j] != PPO_OK)
+            return pw->rcs[j];
+    return PPO_OK;
+}
+
+/* The whole planner (Algorithm 1 with the readings above).
+ *   target[m][n]          out: the returned placement, caller ids
+ *   objective             out: G of the returned placement
+ *   standalone_out[m]     optional out: standalone scores (R6)
+ *   orders_out[S][m]      optional out: the start orders used
+ *   start_objective[S], start_sweeps[S], start_accepts[S]: optional outs
+ *   info[4] (int64)       optional out: best start, executed worker updates,
+ *                         executed DP cells (sum of n * min(k_h, n) over
+ *                         updates), number of starts S. */
+int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
+             const int64_t *recompute_cost, const int64_t *fetch_cost,
+             const int32_t *cap, int32_t n_starts, int32_t max_rounds,
+             uint64_t order_seed, const int32_t *orders_in, uint32_t flags,
+             int32_t threads, uint8_t *target, int64_t *objective,
+             int64_t *standalone_out, int32_t *orders_out,
+             int64_t *start_objective, int32_t *start_sweeps,
+             int32_t *start_accepts, int64_t *info)
+{
+    int rc = validate(n, m, parent, demand, recompute_cost, fetch_cost, cap);
+    if (rc != PPO_OK)
+        return rc;
+    if (n_starts < 0 || max_rounds < 0 || !target || !objective)
+        return PPO_E_ARG;
+    int32_t S = ppo_num_starts(m, n_starts);
+    if (orders_in) {
+        if (n_starts < 1)
+            return PPO_E_ARG;
+        for (int32_t s = 0; s < S; s++) {
+            /* each explicit order must be a permutation of 0..m-1 */
+            uint8_t seen[256] = {0};
+            for (int32_t a = 0; a < m; a++) {
+                int32_t h = orders_in[(size_t)s * m + a];
+                if (h < 0 || h >= m || seen[h])
+                    return PPO_E_ARG;
+                seen[h] = 1;
+            }
+        }
+    }
+    int32_t *order = malloc((size_t)n * sizeof(int32_t));
+    int32_t *nextpos = malloc((size_t)n * sizeof(int32_t));
+    int32_t *orders = malloc((size_t)S * m * sizeof(int32_t));
+    int64_t *standalone = malloc((size_t)m * sizeof(int64_t));
+    uint8_t *tgts = malloc((size_t)S * m * n);
+    int64_t *obj = malloc((size_t)S * sizeof(int64_t));
+    int32_t *sw = malloc((size_t)S * sizeof(int32_t));
+    int32_t *ac = malloc((size_t)S * sizeof(int32_t));
+    int *rcs = malloc((size_t)(S > m ? S : m) * sizeof(int));
+    rc = PPO_E_NOMEM;
+    if (!order || !nextpos || !orders || !standalone || !tgts || !obj ||
+        !sw || !ac || !rcs)
+        goto out;
+    rc = preorder(n, parent, order, nextpos);
+    if (rc != PPO_OK)
+        goto out;
+    plan_in in = {n, m, demand, recompute_cost, fetch_cost, cap, order,
+                  nextpos, max_rounds, flags};
+    plan_work pw;
+    memset(&pw, 0, sizeof pw);
+    pw.in = &in;
+    pw.S = S;
+    pw.tgts = tgts;
+    pw.obj = obj;
+    pw.sweeps = sw;
+    pw.accepts = ac;
+    pw.rcs = rcs;
+    pw.standalone = standalone;
+    pthread_mutex_init(&pw.mu, NULL);
+    rc = run_phase(&pw, 0, m, threads);
+    if (rc == PPO_OK) {
+        if (orders_in)
+            memcpy(orders, orders_in, (size_t)S * m * sizeof(int32_t));
+        else
+            rc = ppo_orders(m, n_starts, order_seed, standalone, orders);
+    }
+    if (rc == PPO_OK) {
+        pw.orders = orders;
+        rc = run_phase(&pw, 1, S, threads);
+    }
+    pthread_mutex_destroy(&pw.mu);
+    if (rc != PPO_OK)
+        goto out;
+    /* Algorithm 1: return the best candidate; R10: earliest start on ties */
+    int32_t best = 0;
+    for (int32_t s = 1; s < S; s++)
+        if (obj[s] > obj[best])
+            best = s;
+    memcpy(target, tgts + (size_t)best * m * n, (size_t)m * n);
+    *objective = obj[best];
+    int64_t updates = m, cells = 0;
+    for (int32_t h = 0; h < m; h++)
+        cells += (int64_t)n * (cap[h] < n ? cap[h] : n);
+    int64_t cells_per_pass = cells;
+    for (int32_t s = 0; s < S; s++) {
+        updates += (int64_t)m * (1 + sw[s]);
+        cells += cells_per_pass * (1 + sw[s]);
+    }
+    if (standalone_out)
+        memcpy(standalone_out, standalone, (size_t)m * sizeof(int64_t));
+    if (orders_out)
+        memcpy(orders_out, orders, (size_t)S * m * sizeof(int32_t));
+    if (start_objective)
+        memcpy(start_objective, obj, (size_t)S * sizeof(int64_t));
+    if (start_sweeps)
+        memcpy(start_sweeps, sw, (size_t)S * sizeof(int32_t));
+    if (start_accepts)
+        memcpy(start_accepts, ac, (size_t)S * sizeof(int32_t));
+    if (info) {
+        info[0] = best;
+        info[1] = updates;
+        info[2] = cells;
+        info[3] = S;
+    }
+    rc = PPO_OK;
+out:
+    free(order); free(nextpos); free(orders); free(standalone); free(tgts);
+    free(obj); free(sw); free(ac); free(rcs);
+    return rc;
+}

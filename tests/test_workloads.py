@@ -1,0 +1,56 @@
+"""Checks of the seeded input generator (no planner arithmetic involved)."""
+
+import numpy as np
+import pytest
+
+from paper_2608_01655_amd import workloads as W
+
+
+def test_chunk_fetch_constants():
+    """36,864 B/token x 512 tokens = 18,874,368 B ("18.9 MB", Sec. I); at
+    1.5 Gb/s that is about 100.7 ms (Fig. 1 caption)."""
+    assert W.CHUNK_BYTES == 18_874_368
+    assert int(W.fetch_us_for_gbps(1.5)) == 100_663
+    assert abs(int(W.fetch_us_for_gbps(1.5)) - 100_700) < 100
+
+
+@pytest.mark.parametrize("name", ["tiny", "tree2k", "rag10k"])
+def test_small_workloads_shape(name):
+    inst = W.make_workload(name)
+    n, m = inst.n, inst.m
+    assert inst.demand.shape == (m, n)
+    assert inst.fetch_cost.shape == (m, m, n)
+    # preorder labels: every parent precedes its child
+    assert np.all(inst.parent[1:] < np.arange(1, n))
+    assert inst.parent[0] == -1
+    # demand of a node = sum of its children's plus its own leaf requests
+    child_sum = np.zeros_like(inst.demand)
+    for v in range(1, n):
+        child_sum[:, inst.parent[v]] += inst.demand[:, v]
+    has_child = np.zeros(n, bool)
+    has_child[inst.parent[1:]] = True
+    assert np.all(inst.demand[:, has_child] == child_sum[:, has_child])
+    assert np.all(inst.demand >= 0) and np.all(inst.recompute_cost > 0)
+    for h in range(m):
+        assert np.all(inst.fetch_cost[h, h] == 0)
+
+
+def test_workload_totals_and_depths():
+    for name, total, dmax in (("tiny", 10_000, 8), ("tree2k", 10 ** 6, 12),
+                              ("rag10k", 10 ** 7, 7)):
+        inst = W.make_workload(name)
+        assert int(inst.demand[:, 0].sum()) == total
+        assert int(inst.depth.max()) <= dmax
+    tiny = W.make_workload("tiny")
+    assert tiny.n == 200 and tiny.m == 2
+    assert np.all(tiny.fetch_cost[0, 1] == 100_700)
+    # h = [1.0, 2.5], a = 20,000, b = 6,000
+    d = tiny.depth.astype(np.int64)
+    assert np.array_equal(tiny.recompute_cost[0], 20_000 + 6_000 * d)
+    assert np.array_equal(tiny.recompute_cost[1], (25 * (20_000 + 6_000 * d)) // 10)
+
+
+def test_generator_is_deterministic():
+    a = W.make_workload("tree2k")
+    b = W.make_workload("tree2k")
+    assert a.checksum() == b.checksum()
