@@ -1,0 +1,183 @@
+"""Throughput of the PrefixPlace planner hot path on one MI355X.
+
+One step = one full plan (standalone scores, WorkerGreedy, coordinate
+refinement until no sweep improves, best start) of the tree50k workload
+(n = 50,000 chunks, M = 16 workers, k = 4,096 each, 8 order-diverse starts,
+source-dependent fetch costs) through the device-resident C-ABI entry point,
+inputs already in HBM.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# Algorithmic bytes per DP cell in the table formulation of Theorem 1:
+# 8 B write of D[i][j], 8 B read of the skip operand D[next(i)][j], and one
+# choice bit (row i+1 is produced the step before and held on chip).
+BYTES_PER_CELL = 16.125
+HBM_PEAK_GBS = 8000.0
+METRIC = ("full PrefixPlace plans/sec and tree-DP cells/sec "
+          "(n·k·updates/s), 1 GPU")
+# Paper context: n = 50,000, M = 16 solved in 12.29 s on one EPYC 9V74 with
+# k = 128 (Sec. V, RQ5) -- a different capacity, so not a like-for-like
+# baseline.
+PAPER_CONTEXT = "n=50,000, M=16, k=128: 12.29 s per plan on one EPYC 9V74"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(inst, cells_per_plan, threads):
+    """The oracle as it stands, on a bounded sample of the same workload:
+    the standalone pass and the greedy pass of every start (no refinement
+    sweeps), timed on the host cores."""
+    import oracle
+
+    oracle.lib()
+    t0 = time.perf_counter()
+    res = oracle.plan_instance(inst, flags=oracle.F_NO_REFINE, threads=threads)
+    dt = time.perf_counter() - t0
+    cps = res.dp_cells / dt
+    return {
+        "value": cps / cells_per_plan,
+        "unit": "plans/s",
+        "cells_per_s": cps,
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"{inst.name}: standalone + greedy pass of all "
+                   f"{inst.n_starts} starts ({res.updates} worker updates, "
+                   f"{res.dp_cells:.3e} DP cells) in {dt:.1f} s; plans/s = "
+                   f"cells/s / cells of one full plan"),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="tree50k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on exactly one GPU: the planner's starts would "
+              "shard across GPUs with one exchange of (objective, start) "
+              "pairs, which this build does not run", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_01655_amd import binding as B
+    from paper_2608_01655_amd import workloads as W
+
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2608_01655_amd import build
+
+        build.build()
+    inst = W.make_workload(args.workload)
+    log(f"[bench] workload {inst.name}: n={inst.n} m={inst.m} "
+        f"k={int(inst.cap.min())}..{int(inst.cap.max())} S={inst.n_starts}")
+    dev = torch.device("cuda:0")
+    lam = torch.from_numpy(inst.demand).to(dev)
+    w = torch.from_numpy(inst.recompute_cost).to(dev)
+    f = torch.from_numpy(inst.fetch_cost).to(dev)
+    tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+    ctx = B.Context(0)
+
+    def step(flags=0):
+        return ctx.pp_plan_device(inst.parent, lam, w, f, inst.cap, tgt,
+                                  n_starts=inst.n_starts,
+                                  max_rounds=inst.max_rounds,
+                                  order_seed=inst.order_seed, flags=flags)
+
+    for i in range(args.warmup):
+        p = step()
+        log(f"[bench] warmup {i}: objective {p.objective}")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plans = []
+    for i in range(args.steps):
+        plans.append(step(B.PP_F_TIME_KERNELS))
+        log(f"[bench] step {i}: objective {plans[-1].objective} "
+            f"dp {plans[-1].dp_kernel_ms:.1f} ms")
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    p = plans[-1]
+    objectives = {q.objective for q in plans}
+    gold_ok = None
+    gold_path = os.path.join(ROOT, "tests", "golden", "plans.json")
+    if os.path.exists(gold_path):
+        with open(gold_path) as fh:
+            gold = json.load(fh).get(inst.name)
+        if gold:
+            gold_ok = objectives == {gold["objective"]}
+    cells = p.dp_cells
+    plans_per_s = args.steps / dt
+    cells_per_s = cells * args.steps / dt
+    dp_ms = sum(q.dp_kernel_ms for q in plans)
+    launches = sum(q.dp_launches for q in plans)
+    bytes_per_launch = cells * args.steps * BYTES_PER_CELL / launches
+    avg_launch_s = dp_ms / launches / 1e3
+    achieved = bytes_per_launch / avg_launch_s / 1e9
+    out = {
+        "metric": METRIC,
+        "value": plans_per_s,
+        "unit": "plans/s",
+        "dp_cells_per_s": cells_per_s,
+        "dp_cells_per_s_frac_hbm_roofline": cells_per_s * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
+        "plans_per_s_frac_hbm_roofline": cells_per_s * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": inst.name, "n": inst.n, "workers": inst.m,
+            "k": [int(x) for x in sorted(set(inst.cap.tolist()))],
+            "starts": inst.n_starts, "max_rounds": inst.max_rounds,
+            "updates_per_plan": p.updates, "dp_cells_per_plan": cells,
+            "sweeps_per_start": p.start_sweeps.tolist(),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_dp (rooted-tree DP sweep)",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "bytes_per_cell": BYTES_PER_CELL,
+            "dp_launches_per_plan": launches // args.steps,
+            "avg_launch_ms": avg_launch_s * 1e3,
+            "dp_cells_per_s_in_kernel": cells * args.steps / (dp_ms / 1e3),
+            "dp_share_of_plan_time": dp_ms / 1e3 / dt,
+        },
+        "parity_vs_golden": gold_ok,
+        "paper_context": PAPER_CONTEXT,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        threads = max(1, min(8, os.cpu_count() or 1))
+        out["cpu_baseline"] = cpu_baseline(inst, cells, threads)
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

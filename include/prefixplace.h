@@ -1,0 +1,184 @@
+/*
+ * prefixplace.h -- C ABI of the MI355X (gfx950) PrefixPlace planner hot path.
+ *
+ * PrefixPlace (arXiv 2608.01655) assigns every LLM-serving worker a
+ * prefix-complete (parent-closed) set of KV-cache chunks under a per-worker
+ * chunk budget, maximising the materialisation cost saved per epoch.
+ *
+ * Problem (Eq. 8): maximise F_pair(T) (Eq. 6) over T = (T_1..T_M) with
+ * |T_m| <= k_m and every T_m parent-closed, where requester m saves
+ *   q_{m<-h}(b) = w_m(b)                     if h == m,
+ *                 max(w_m(b) - f_{m<-h}(b), 0) otherwise      (Eq. 5)
+ * on chunk b when holder h is its best resident copy.  Each worker update
+ * computes the exact marginals p_h(b) of Proposition 1 (Eq. 7) and solves
+ * the rooted-tree knapsack of Eq. 9 / Theorem 1 exactly; updates run as
+ * WorkerGreedy (Theorem 3) followed by coordinate refinement over
+ * order-diverse starts (Sec. IV-C, Algorithm 1).
+ *
+ * Conventions shared by every entry point
+ *   - Integers only: demand is requests per epoch, costs are integer
+ *     microseconds, every value/objective is int64 (request * us).  Results
+ *     are exact and deterministic.
+ *   - Node ids are the caller's labels 0..n-1.  parent[v] = -1 attaches v to
+ *     the implicit no-cost dummy root (Sec. III-A), so forests are allowed.
+ *   - Host arrays are C-contiguous, caller-owned, read or written only during
+ *     the call; the library keeps no pointer after returning.
+ *   - On any error the outputs are left unmodified, a negative PP_E_* code is
+ *     returned and pp_last_error() describes it.  No C++ exception crosses
+ *     this ABI.  Inputs are validated before any device work.
+ *   - Tie rules (deterministic):
+ *       DP ties keep the skip branch (a node is taken only if strictly
+ *       better), so among optimal sets the one whose 0/1 vector in canonical
+ *       preorder (roots, then children, by increasing id) is
+ *       lexicographically smallest is returned;
+ *       a refinement replacement is accepted only if it strictly raises the
+ *       objective (integer costs: tolerance 0);
+ *       ties between starts go to the lowest start index.
+ *   - Start orders: start 0 sorts workers by standalone score (the optimum
+ *     of the worker's own rooted-tree problem against an empty placement)
+ *     descending, ties by lower worker id; start 1 is its reverse; start
+ *     s >= 2 is a Fisher-Yates shuffle of 0..m-1 driven by SplitMix64
+ *     seeded with order_seed + s (j = next() mod (i+1), for i = m-1..1).
+ *   - All GPU entry points run on the current HIP device.
+ */
+#ifndef PREFIXPLACE_H
+#define PREFIXPLACE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PP_ABI_VERSION 1
+
+enum {
+    PP_OK = 0,
+    PP_E_ARG = -1,      /* null pointer, n < 1, m < 1 or m > 255, bad option */
+    PP_E_TREE = -2,     /* parent out of range, self-parent, or a cycle */
+    PP_E_RANGE = -3,    /* negative demand, cost, capacity or profit */
+    PP_E_OVERFLOW = -4, /* sum over (m,b) of demand*recompute exceeds INT64_MAX */
+    PP_E_NOMEM = -5,    /* host or device allocation failed */
+    PP_E_DEVICE = -6,   /* HIP error, no device, or a device-side stall */
+    PP_E_UNSUPPORTED = -7 /* a shape beyond a documented limit (see below) */
+};
+
+enum {
+    PP_F_VALIDATE_ONLY = 1u, /* validate and build the tree layout, no GPU work */
+    PP_F_NO_REFINE = 2u,     /* greedy pass only (Theorem 3's WorkerGreedy) */
+    PP_F_TIME_KERNELS = 4u   /* time every DP-sweep launch with HIP events */
+};
+
+/* Planner options.  Passing NULL selects
+ * {n_starts = 8, max_rounds = 0, order_seed = 0, orders = NULL, flags = 0}. */
+typedef struct {
+    int32_t n_starts;       /* >= 1: number of starts; 0: the paper's default
+                               set (m <= 5: all m! orders in lexicographic
+                               order; otherwise 8 starts) */
+    int32_t max_rounds;     /* cap on refinement sweeps, counting the final
+                               non-improving one; 0 = until a sweep accepts
+                               nothing */
+    uint64_t order_seed;    /* seeds the shuffled starts (index >= 2) */
+    const int32_t *orders;  /* optional [n_starts][m] explicit worker orders
+                               (host); NULL = generate as described above */
+    uint32_t flags;         /* PP_F_* */
+} pp_options;
+
+/* Optional statistics.  Pointer fields may be NULL; arrays indexed by start
+ * must hold pp_num_starts(m, n_starts) entries. */
+typedef struct {
+    int32_t best_start;        /* out: start whose placement is returned */
+    int32_t n_starts;          /* out: number of starts run */
+    int64_t updates;           /* out: worker updates executed (standalone +
+                                  greedy + every sweep) */
+    int64_t dp_cells;          /* out: sum over updates of n * min(k_h, n) */
+    int64_t *start_objective;  /* out [S]: objective of each start */
+    int32_t *start_sweeps;     /* out [S]: refinement sweeps per start */
+    int32_t *start_accepts;    /* out [S]: accepted replacements per start */
+    int64_t *standalone;       /* out [m]: standalone score per worker */
+    int32_t *orders;           /* out [S][m]: start orders used */
+    double dp_kernel_ms;       /* out with PP_F_TIME_KERNELS: summed duration
+                                  of the DP-sweep launches */
+    int32_t dp_launches;       /* out with PP_F_TIME_KERNELS */
+} pp_stats;
+
+/* Number of starts the options select (see pp_options.n_starts). */
+int32_t pp_num_starts(int32_t m, int32_t n_starts);
+
+/* Full planner (Algorithm 1 with exact rooted-tree updates; Eq. 8).
+ *   parent          [n]      host; -1 = child of the dummy root
+ *   demand          [m][n]   host; Lambda_m(b) >= 0 (Sec. III-A)
+ *   recompute_cost  [m][n]   host; w_m(b) >= 0 us
+ *   fetch_cost      [m][m][n] host; fetch_cost[src][dst][b] = f_{dst<-src}(b)
+ *                            >= 0 us; the src == dst plane is ignored.  A
+ *                            requester-side cost f_m(b) is given by repeating
+ *                            it over src (this reproduces Eq. 4 exactly).
+ *   cap             [m]      host; k_m >= 0 chunks (values above n act as n)
+ *   opt                      NULL or options
+ *   target          [m][n]   host out: 1 iff b is in T_m; each row is
+ *                            parent-closed with at most cap[m] ones
+ *   objective                host out: F_pair(T) in request * us
+ *   stats                    NULL or statistics
+ * Limits: the tree's nesting of pending subtree boundaries (at most its
+ * depth) must not exceed 255, else PP_E_UNSUPPORTED. */
+int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
+            const int64_t *recompute_cost, const int64_t *fetch_cost,
+            const int32_t *cap, const pp_options *opt, uint8_t *target,
+            int64_t *objective, pp_stats *stats);
+
+/* One exact rooted-tree solve (Eq. 9, Theorem 1) on the GPU.
+ *   parent [n] host, profit [n] host (>= 0, sum <= INT64_MAX), k >= 0;
+ *   selected [n] host out (0/1, parent-closed, at most min(k, n) ones);
+ *   value host out = max total profit. */
+int pp_rooted_dp(int32_t n, const int32_t *parent, const int64_t *profit,
+                 int32_t k, uint8_t *selected, int64_t *value);
+
+/* Exact marginals of worker h against the other workers' current sets
+ * (Proposition 1, Eq. 7), on the GPU.
+ *   target [m][n] host: current placement (row h is ignored);
+ *   profit [n] host out: p_h(b);
+ *   g_without_h host out (may be NULL): F_pair with T_h emptied. */
+int pp_marginal(int32_t n, int32_t m, const int64_t *demand,
+                const int64_t *recompute_cost, const int64_t *fetch_cost,
+                const uint8_t *target, int32_t h, int64_t *profit,
+                int64_t *g_without_h);
+
+/* F_pair(T) of Eq. 6 for an arbitrary placement (target [m][n] host), on
+ * the GPU. */
+int pp_objective(int32_t n, int32_t m, const int64_t *demand,
+                 const int64_t *recompute_cost, const int64_t *fetch_cost,
+                 const uint8_t *target, int64_t *objective);
+
+/* Start orders (Sec. IV-C) from standalone scores [m]; host only.
+ * orders [pp_num_starts(m, n_starts)][m] host out. */
+int pp_orders(int32_t m, int32_t n_starts, uint64_t order_seed,
+              const int64_t *standalone, int32_t *orders);
+
+/* Reusable GPU context: keeps device buffers between calls.  A context is
+ * used by one thread at a time; separate contexts may run concurrently. */
+typedef struct pp_ctx pp_ctx;
+int pp_ctx_create(pp_ctx **ctx, int device);
+void pp_ctx_destroy(pp_ctx *ctx);
+
+/* pp_plan with device-resident inputs and output, on `hip_stream`
+ * (a hipStream_t; NULL = the null stream).  demand_dev, recompute_dev,
+ * fetch_dev are device pointers in caller ids, laid out as in pp_plan;
+ * target_dev [m][n] device out.  parent, cap and the options stay on the
+ * host.  The call returns after the plan has finished on the stream. */
+int pp_plan_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
+                   const int64_t *demand_dev, const int64_t *recompute_dev,
+                   const int64_t *fetch_dev, const int32_t *cap,
+                   const pp_options *opt, uint8_t *target_dev,
+                   int64_t *objective, pp_stats *stats, void *hip_stream);
+
+/* Description of the last error on the calling thread; valid until the
+ * next pp_* call on that thread. */
+const char *pp_last_error(void);
+
+int pp_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PREFIXPLACE_H */

@@ -1,0 +1,1006 @@
+// pp_host.cpp -- host side of the PrefixPlace planner: input validation,
+// canonical preorder and DP-sweep metadata, start orders, the update loop
+// of Algorithm 1 (standalone scores, WorkerGreedy, coordinate refinement,
+// best start) and the C ABI of include/prefixplace.h.
+//
+// Every step of a worker update runs in the gfx950 kernels of
+// pp_kernels.hip; this file only prepares layouts and sequences launches.
+
+#include "prefixplace.h"
+#include "pp_internal.h"
+
+#include <algorithm>
+#include <climits>
+#include <cstdlib>
+#include <cstring>
+#include <memory>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace pp;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define PP_HIP(expr)                                                      \
+  do {                                                                    \
+    hipError_t e_ = (expr);                                               \
+    if (e_ != hipSuccess)                                                 \
+      return fail(PP_E_DEVICE, std::string(#expr) + ": " +                \
+                                   hipGetErrorString(e_));                \
+  } while (0)
+
+#define PP_TRY(expr)            \
+  do {                          \
+    int rc_ = (expr);           \
+    if (rc_ != PP_OK) return rc_; \
+  } while (0)
+
+// ------------------------------------------------------------ buffers ---
+
+struct DevBuf {
+  void* p = nullptr;
+  size_t cap = 0;
+  // Grow to at least `bytes`; zero the new memory when `zero`.
+  int ensure(size_t bytes, bool zero = false) {
+    if (bytes == 0) bytes = 64;
+    if (bytes <= cap) return PP_OK;
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    cap = 0;
+    if (hipMalloc(&p, bytes) != hipSuccess)
+      return fail(PP_E_NOMEM, "device allocation of " + std::to_string(bytes) +
+                                  " bytes failed");
+    cap = bytes;
+    if (zero && hipMemset(p, 0, bytes) != hipSuccess)
+      return fail(PP_E_DEVICE, "hipMemset failed");
+    return PP_OK;
+  }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    cap = 0;
+  }
+  template <class T>
+  T* as() const { return static_cast<T*>(p); }
+};
+
+// --------------------------------------------------------------- tree ---
+
+// Canonical preorder (roots, then children, in increasing id) and the DP
+// sweep's per-step metadata.  `order[pos]` is the caller id at 0-based
+// position pos, `nextpos[pos]` the first position after its subtree.
+struct TreeLayout {
+  int32_t n = 0;
+  std::vector<int32_t> order, nextpos;
+  std::vector<uint32_t> meta;
+  int32_t slots = 0;    // LDS stack rows the sweep needs
+  bool identity = true; // caller ids are already in preorder
+};
+
+int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
+  for (int32_t v = 0; v < n; ++v) {
+    const int32_t p = parent[v];
+    if (p < -1 || p >= n || p == v)
+      return fail(PP_E_TREE, "parent[" + std::to_string(v) + "] = " +
+                                 std::to_string(p) + " is out of range or self");
+  }
+  // children in increasing id via counting sort on the parent (roots under
+  // the dummy index n)
+  std::vector<int32_t> head(n + 2, 0), kids(n);
+  for (int32_t v = 0; v < n; ++v) head[(parent[v] < 0 ? n : parent[v]) + 1]++;
+  for (int32_t u = 0; u <= n; ++u) head[u + 1] += head[u];
+  {
+    std::vector<int32_t> fill(head.begin(), head.end() - 1);
+    for (int32_t v = 0; v < n; ++v) kids[fill[parent[v] < 0 ? n : parent[v]]++] = v;
+  }
+  t.n = n;
+  t.order.assign(n, 0);
+  t.nextpos.assign(n, 0);
+  std::vector<int32_t> stack;
+  stack.reserve(n);
+  for (int32_t k = head[n + 1] - 1; k >= head[n]; --k) stack.push_back(kids[k]);
+  int32_t pos = 0;
+  std::vector<int32_t> posof(n, -1);
+  while (!stack.empty()) {
+    const int32_t v = stack.back();
+    stack.pop_back();
+    posof[v] = pos;
+    t.order[pos++] = v;
+    for (int32_t k = head[v + 1] - 1; k >= head[v]; --k) stack.push_back(kids[k]);
+  }
+  if (pos != n) return fail(PP_E_TREE, "parent[] contains a cycle");
+  std::vector<int32_t> size(n, 1);
+  for (int32_t q = n - 1; q >= 0; --q) {
+    const int32_t p = parent[t.order[q]];
+    if (p >= 0) size[posof[p]] += size[q];
+  }
+  t.identity = true;
+  for (int32_t q = 0; q < n; ++q) {
+    t.nextpos[q] = q + size[q];
+    if (t.order[q] != q) t.identity = false;
+  }
+  // DP metadata.  Rows are 1-based positions i; nx(i) = next(i).  Row r is
+  // a far skip target if r = next(a) for some a with r != a+1, r != n+1;
+  // the smallest such a is its last reader.  Pending targets nest like the
+  // subtrees that end at them, so they live on a stack of LDS slots.
+  auto nx = [&](int32_t i) { return t.nextpos[i - 1] + 1; };
+  std::vector<int32_t> last_user(n + 2, INT32_MAX), slot_of(n + 2, -1);
+  for (int32_t a = n; a >= 1; --a) {
+    const int32_t r = nx(a);
+    if (r != a + 1 && r != n + 1) last_user[r] = a;  // descending: ends at min
+  }
+  t.meta.assign(n, 0);
+  int32_t top = 0, high = 0;
+  for (int32_t i = n; i >= 1; --i) {
+    const int32_t s = n - i;
+    const int32_t r = nx(i);
+    uint32_t mw = 0;
+    if (r == i + 1) mw |= kMetaLeaf;
+    if (r != i + 1 && r != n + 1 && last_user[r] == i) {
+      if (slot_of[r] != top - 1) return fail(PP_E_DEVICE, "internal: stack order");
+      --top;
+    }
+    uint32_t store = kSlotNone;
+    if (last_user[i] != INT32_MAX) {
+      if (top >= kMaxSlots)
+        return fail(PP_E_UNSUPPORTED,
+                    "tree needs more than 254 pending subtree boundaries");
+      slot_of[i] = top++;
+      high = std::max(high, top);
+      store = (uint32_t)slot_of[i];
+    }
+    uint32_t pf = kSlotNone;
+    if (i > 1) {
+      const int32_t r2 = nx(i - 1);
+      if (r2 != i) pf = (r2 == n + 1) ? kSlotZero : (uint32_t)slot_of[r2];
+    }
+    t.meta[s] = mw | (store << 8) | (pf << 16);
+  }
+  t.slots = high;
+  return PP_OK;
+}
+
+// ------------------------------------------------------------- orders ---
+
+uint64_t splitmix64_next(uint64_t& state) {
+  uint64_t z = (state += 0x9e3779b97f4a7c15ull);
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+int32_t num_starts(int32_t m, int32_t n_starts) {
+  if (n_starts > 0) return n_starts;
+  if (m <= 5) {
+    int32_t f = 1;
+    for (int32_t k = 2; k <= m; ++k) f *= k;
+    return f;
+  }
+  return 8;
+}
+
+void make_orders(int32_t m, int32_t n_starts, uint64_t seed,
+                 const int64_t* score, int32_t* out) {
+  const int32_t S = num_starts(m, n_starts);
+  if (n_starts == 0 && m <= 5) {  // every order, lexicographic
+    std::vector<int32_t> p(m);
+    for (int32_t h = 0; h < m; ++h) p[h] = h;
+    for (int32_t s = 0; s < S; ++s) {
+      std::copy(p.begin(), p.end(), out + (size_t)s * m);
+      std::next_permutation(p.begin(), p.end());
+    }
+    return;
+  }
+  std::vector<int32_t> base(m);
+  for (int32_t h = 0; h < m; ++h) base[h] = h;
+  std::stable_sort(base.begin(), base.end(), [&](int32_t a, int32_t b) {
+    return score[a] > score[b];  // stable: equal scores keep id order
+  });
+  for (int32_t s = 0; s < S; ++s) {
+    int32_t* o = out + (size_t)s * m;
+    if (s == 0) {
+      std::copy(base.begin(), base.end(), o);
+    } else if (s == 1) {
+      std::reverse_copy(base.begin(), base.end(), o);
+    } else {
+      uint64_t st = seed + (uint64_t)s;
+      for (int32_t h = 0; h < m; ++h) o[h] = h;
+      for (int32_t i = m - 1; i >= 1; --i) {
+        const int32_t j = (int32_t)(splitmix64_next(st) % (uint64_t)(i + 1));
+        std::swap(o[i], o[j]);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ context ---
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  return (v && *v) ? std::atoi(v) : dflt;
+}
+
+}  // namespace
+
+struct pp_ctx {
+  int device = 0;
+  hipStream_t own = nullptr;
+  // problem, preorder layout
+  DevBuf lam, w, f, nextpos, meta, order;
+  // uploads for host-pointer entry points (caller order)
+  DevBuf up_lam, up_w, up_f, up_u8;
+  // per-slot state
+  DevBuf tgt, v1, v2, h1, profit, sel, bits, ring, cs;
+  DevBuf partial, flag;
+  uint32_t epoch = 0;
+  std::vector<hipEvent_t> events;
+  ~pp_ctx() {
+    for (DevBuf* b : {&lam, &w, &f, &nextpos, &meta, &order, &up_lam, &up_w,
+                      &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
+                      &ring, &cs, &partial, &flag})
+      b->release();
+    for (hipEvent_t e : events) (void)hipEventDestroy(e);
+    if (own) (void)hipStreamDestroy(own);
+  }
+};
+
+namespace {
+
+int select_device(pp_ctx* c) {
+  PP_HIP(hipSetDevice(c->device));
+  return PP_OK;
+}
+
+int npad_of(int32_t n) { return (n + 63) / 64 * 64; }
+
+// Allocate per-slot buffers for `slots` chains of up to `kmax` cells.
+int ensure_slots(pp_ctx* c, DevState& d, int32_t slots, int32_t kmax,
+                 int cells) {
+  const size_t n = (size_t)d.n, m = (size_t)d.m, npad = (size_t)d.npad;
+  const int32_t stages = std::max(1, (kmax + 64 * cells - 1) / (64 * cells));
+  PP_TRY(c->tgt.ensure(slots * m * n));
+  PP_TRY(c->v1.ensure(slots * m * n * 8));
+  PP_TRY(c->v2.ensure(slots * m * n * 8));
+  PP_TRY(c->h1.ensure(slots * m * n));
+  PP_TRY(c->profit.ensure(slots * n * 8));
+  PP_TRY(c->sel.ensure(slots * npad));
+  PP_TRY(c->bits.ensure((size_t)slots * stages * cells * npad * 8));
+  // ring words carry a launch tag; fresh memory is zeroed so that no stale
+  // word can ever carry a live tag (tags start at 1)
+  PP_TRY(c->ring.ensure((size_t)slots * stages * n * 16, true));
+  PP_TRY(c->cs.ensure(slots * sizeof(ChainState)));
+  d.tgt = c->tgt.as<uint8_t>();
+  d.v1 = c->v1.as<int64_t>();
+  d.v2 = c->v2.as<int64_t>();
+  d.h1 = c->h1.as<uint8_t>();
+  d.profit = c->profit.as<int64_t>();
+  d.sel = c->sel.as<uint8_t>();
+  d.bits = c->bits.as<uint64_t>();
+  d.ring = c->ring.as<uint64_t>();
+  d.cs = c->cs.as<ChainState>();
+  d.stages = stages;
+  d.cells = cells;
+  return PP_OK;
+}
+
+ChainSet chain_set(const std::vector<int32_t>& slots,
+                   const std::vector<int32_t>& workers,
+                   const std::vector<int32_t>& kprime, size_t lo, size_t hi) {
+  ChainSet s;
+  std::memset(&s, 0, sizeof s);
+  s.count = (int32_t)(hi - lo);
+  for (size_t k = lo; k < hi; ++k) {
+    s.slot[k - lo] = slots[k];
+    s.worker[k - lo] = workers[k];
+    s.kprime[k - lo] = kprime[k];
+  }
+  return s;
+}
+
+struct Timer {
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> marks;
+  size_t used = 0;
+};
+
+int timer_mark(pp_ctx* c, Timer& t, bool start, hipStream_t st) {
+  if (!t.on) return PP_OK;
+  if (start) {
+    while (c->events.size() < 2 * (t.used + 1)) {
+      hipEvent_t e;
+      PP_HIP(hipEventCreate(&e));
+      c->events.push_back(e);
+    }
+    t.marks.push_back({c->events[2 * t.used], c->events[2 * t.used + 1]});
+    PP_HIP(hipEventRecord(t.marks.back().first, st));
+  } else {
+    PP_HIP(hipEventRecord(t.marks.back().second, st));
+    ++t.used;
+  }
+  return PP_OK;
+}
+
+struct Engine {
+  pp_ctx* c;
+  DevState d;
+  int32_t slots_lds;
+  int resident;       // DP blocks resident at once
+  uint32_t spin_limit;
+  hipStream_t st;
+  Timer timer;
+
+  // One DP sweep over the chains of `set` (kprime >= 1 each), split into
+  // launches whose stages all fit on the device at once.
+  int dp(const ChainSet& in, int store_bits) {
+    const int cellsw = 64 * d.cells;
+    int32_t k = 0;
+    while (k < in.count) {
+      ChainSet s;
+      std::memset(&s, 0, sizeof s);
+      int32_t blocks = 0;
+      while (k < in.count) {
+        const int32_t g = (in.kprime[k] + cellsw - 1) / cellsw;
+        if (s.count > 0 && blocks + g > resident) break;
+        s.slot[s.count] = in.slot[k];
+        s.worker[s.count] = in.worker[k];
+        s.kprime[s.count] = in.kprime[k];
+        s.base[s.count] = blocks;
+        blocks += g;
+        ++s.count;
+        ++k;
+      }
+      s.base[s.count] = blocks;
+      if (blocks > resident)
+        return fail(PP_E_UNSUPPORTED,
+                    "capacity needs more DP stages than the device holds");
+      if (++c->epoch == 0) ++c->epoch;  // tag 0 marks never-written words
+      PP_TRY(timer_mark(c, timer, true, st));
+      PP_HIP(launch_dp(s, d, c->epoch, spin_limit, store_bits, slots_lds, st));
+      PP_TRY(timer_mark(c, timer, false, st));
+    }
+    return PP_OK;
+  }
+
+  // One worker update (gains, DP sweep, accept + backtrack, commit) for
+  // every chain of `set`.
+  int update(const ChainSet& set, int mode) {
+    if (set.count == 0) return PP_OK;
+    PP_HIP(launch_gains(set, d, st));
+    PP_TRY(dp(set, 1));
+    PP_HIP(launch_backtrack(set, d, mode, st));
+    PP_HIP(launch_commit(set, d, st));
+    return PP_OK;
+  }
+};
+
+int choose_cells(int32_t total_stage_cells_c1, int dev, int32_t slots_lds) {
+  const int forced = env_int("PP_DP_CELLS", 0);
+  if (forced == 1 || forced == 2 || forced == 4 || forced == 8) return forced;
+  // fewest cells per lane whose stages of one update all fit at once
+  for (int c : {1, 2, 4, 8}) {
+    const int res = dp_resident_blocks(c, slots_lds, dev);
+    if (res > 0 && (total_stage_cells_c1 + c - 1) / c <= res) return c;
+  }
+  return 8;
+}
+
+struct PlanResult {
+  std::vector<int64_t> start_obj, standalone;
+  std::vector<int32_t> sweeps, accepts, orders;
+  int32_t best = 0, S = 0;
+  int64_t updates = 0, cells = 0;
+  double dp_ms = 0.0;
+  int32_t dp_launches = 0;
+};
+
+// Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
+int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
+             const pp_options& o, hipStream_t st, PlanResult& res) {
+  const int32_t n = t.n;
+  const int32_t S = num_starts(m, o.n_starts);
+  res.S = S;
+  std::vector<int32_t> kp(m);
+  int32_t kmax = 0;
+  int64_t cells_pass = 0;
+  for (int32_t h = 0; h < m; ++h) {
+    kp[h] = std::min(cap[h], n);
+    kmax = std::max(kmax, kp[h]);
+    cells_pass += (int64_t)n * kp[h];
+  }
+  const int32_t slots = std::max(m, S);
+  Engine e;
+  e.c = c;
+  e.st = st;
+  e.slots_lds = std::max(1, t.slots);
+  e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 26);
+  e.timer.on = (o.flags & PP_F_TIME_KERNELS) != 0;
+  DevState& d = e.d;
+  d = DevState{};
+  d.n = n;
+  d.m = m;
+  d.npad = npad_of(n);
+  d.lam = c->lam.as<int64_t>();
+  d.w = c->w.as<int64_t>();
+  d.f = c->f.as<int64_t>();
+  d.nextpos = c->nextpos.as<int32_t>();
+  d.meta = c->meta.as<uint32_t>();
+  // widest single launch: every start's update at once
+  int64_t stage64 = 0;
+  {
+    std::vector<int32_t> ks(kp.begin(), kp.end());
+    std::sort(ks.rbegin(), ks.rend());
+    for (int32_t k = 0; k < std::min<int32_t>(S, kMaxChains); ++k)
+      stage64 += (ks[k % m] + 63) / 64;
+  }
+  const int cells = choose_cells((int32_t)std::min<int64_t>(stage64, INT32_MAX),
+                                 c->device, e.slots_lds);
+  e.resident = dp_resident_blocks(cells, e.slots_lds, c->device);
+  if (e.resident <= 0)
+    return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident (LDS stack of " +
+                                      std::to_string(e.slots_lds) + " rows)");
+  PP_TRY(ensure_slots(c, d, slots, kmax, cells));
+
+  // --- standalone scores: each worker against the empty placement
+  res.standalone.assign(m, 0);
+  std::vector<ChainState> hs(slots);
+  for (int32_t lo = 0; lo < m; lo += kMaxChains) {
+    const int32_t hi = std::min(m, lo + kMaxChains);
+    std::vector<int32_t> sl, wk, kk;
+    for (int32_t h = lo; h < hi; ++h) {
+      sl.push_back(h);
+      wk.push_back(h);
+      kk.push_back(kp[h]);
+    }
+    ChainSet all = chain_set(sl, wk, kk, 0, sl.size());
+    PP_HIP(launch_init_slots(all, d, 1, st));
+    PP_HIP(launch_gains(all, d, st));
+    std::vector<int32_t> sl2, wk2, kk2;
+    for (size_t q = 0; q < sl.size(); ++q)
+      if (kk[q] > 0) {
+        sl2.push_back(sl[q]);
+        wk2.push_back(wk[q]);
+        kk2.push_back(kk[q]);
+      }
+    if (!sl2.empty()) PP_TRY(e.dp(chain_set(sl2, wk2, kk2, 0, sl2.size()), 0));
+  }
+  PP_HIP(hipMemcpyAsync(hs.data(), d.cs, sizeof(ChainState) * m,
+                        hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  for (int32_t h = 0; h < m; ++h) {
+    if (hs[h].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+    res.standalone[h] = kp[h] > 0 ? hs[h].dpval : 0;
+  }
+
+  // --- start orders
+  res.orders.assign((size_t)S * m, 0);
+  if (o.orders)
+    std::memcpy(res.orders.data(), o.orders, sizeof(int32_t) * S * m);
+  else
+    make_orders(m, o.n_starts, o.order_seed, res.standalone.data(),
+                res.orders.data());
+
+  // --- starts: WorkerGreedy then refinement sweeps, all starts together
+  res.sweeps.assign(S, 0);
+  res.accepts.assign(S, 0);
+  res.start_obj.assign(S, 0);
+  for (int32_t lo = 0; lo < S; lo += kMaxChains) {
+    const int32_t hi = std::min(S, lo + kMaxChains);
+    std::vector<int32_t> active;
+    for (int32_t s = lo; s < hi; ++s) active.push_back(s);
+    {
+      std::vector<int32_t> sl(active), wk(active.size(), 0), kk(active.size(), 0);
+      PP_HIP(launch_init_slots(chain_set(sl, wk, kk, 0, sl.size()), d, 1, st));
+    }
+    auto position_set = [&](const std::vector<int32_t>& act, int32_t a) {
+      std::vector<int32_t> sl, wk, kk;
+      for (int32_t s : act) {
+        const int32_t h = res.orders[(size_t)s * m + a];
+        if (kp[h] == 0) continue;  // empty set: never changes the placement
+        sl.push_back(s);
+        wk.push_back(h);
+        kk.push_back(kp[h]);
+      }
+      return chain_set(sl, wk, kk, 0, sl.size());
+    };
+    for (int32_t a = 0; a < m; ++a)
+      PP_TRY(e.update(position_set(active, a), kModeGreedy));
+    if (!(o.flags & PP_F_NO_REFINE)) {
+      while (!active.empty()) {
+        {
+          std::vector<int32_t> wk(active.size(), 0), kk(active.size(), 0);
+          PP_HIP(launch_reset_round(chain_set(active, wk, kk, 0, active.size()),
+                                    d, st));
+        }
+        for (int32_t a = 0; a < m; ++a)
+          PP_TRY(e.update(position_set(active, a), kModeRefine));
+        std::vector<ChainState> cur(active.size());
+        for (size_t q = 0; q < active.size(); ++q)
+          PP_HIP(hipMemcpyAsync(&cur[q], d.cs + active[q], sizeof(ChainState),
+                                hipMemcpyDeviceToHost, st));
+        PP_HIP(hipStreamSynchronize(st));
+        std::vector<int32_t> next;
+        for (size_t q = 0; q < active.size(); ++q) {
+          const int32_t s = active[q];
+          if (cur[q].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+          res.sweeps[s] += 1;
+          const bool capped = o.max_rounds > 0 && res.sweeps[s] >= o.max_rounds;
+          if (cur[q].improved && !capped) next.push_back(s);
+        }
+        active.swap(next);
+      }
+    }
+    std::vector<int32_t> sl, wk, kk;
+    for (int32_t s = lo; s < hi; ++s) {
+      sl.push_back(s);
+      wk.push_back(0);
+      kk.push_back(0);
+    }
+    ChainSet all = chain_set(sl, wk, kk, 0, sl.size());
+    PP_HIP(launch_objective(all, d, st));
+    std::vector<ChainState> fin(hi - lo);
+    PP_HIP(hipMemcpyAsync(fin.data(), d.cs + lo, sizeof(ChainState) * (hi - lo),
+                          hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    for (int32_t s = lo; s < hi; ++s) {
+      if (fin[s - lo].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+      res.start_obj[s] = fin[s - lo].obj;
+      res.accepts[s] = fin[s - lo].accepts;
+    }
+  }
+  res.best = 0;
+  for (int32_t s = 1; s < S; ++s)
+    if (res.start_obj[s] > res.start_obj[res.best]) res.best = s;
+  res.updates = m;
+  res.cells = cells_pass;
+  for (int32_t s = 0; s < S; ++s) {
+    res.updates += (int64_t)m * (1 + res.sweeps[s]);
+    res.cells += cells_pass * (1 + res.sweeps[s]);
+  }
+  if (e.timer.on) {
+    float tot = 0.f;
+    for (auto& mk : e.timer.marks) {
+      float ms = 0.f;
+      PP_HIP(hipEventElapsedTime(&ms, mk.first, mk.second));
+      tot += ms;
+    }
+    res.dp_ms = tot;
+    res.dp_launches = (int32_t)e.timer.marks.size();
+  }
+  return PP_OK;
+}
+
+// ---------------------------------------------------------- validation --
+
+int check_options(int32_t m, const pp_options& o) {
+  if (o.n_starts < 0 || o.max_rounds < 0)
+    return fail(PP_E_ARG, "n_starts and max_rounds must be >= 0");
+  if (o.orders) {
+    if (o.n_starts < 1)
+      return fail(PP_E_ARG, "explicit orders need n_starts >= 1");
+    for (int32_t s = 0; s < o.n_starts; ++s) {
+      std::vector<char> seen(m, 0);
+      for (int32_t a = 0; a < m; ++a) {
+        const int32_t h = o.orders[(size_t)s * m + a];
+        if (h < 0 || h >= m || seen[h])
+          return fail(PP_E_ARG, "orders[" + std::to_string(s) +
+                                    "] is not a permutation of 0..m-1");
+        seen[h] = 1;
+      }
+    }
+  }
+  return PP_OK;
+}
+
+int check_values(int32_t n, int32_t m, const int64_t* lam, const int64_t* w,
+                 const int64_t* f) {
+  const size_t mn = (size_t)m * n;
+  for (size_t x = 0; x < mn; ++x)
+    if (lam[x] < 0 || w[x] < 0)
+      return fail(PP_E_RANGE, "negative demand or recompute cost");
+  for (size_t x = 0; x < mn * (size_t)m; ++x)
+    if (f[x] < 0) return fail(PP_E_RANGE, "negative fetch cost");
+  unsigned __int128 tot = 0;
+  for (size_t x = 0; x < mn; ++x) {
+    tot += (unsigned __int128)(uint64_t)lam[x] * (uint64_t)w[x];
+    if (tot > (unsigned __int128)INT64_MAX)
+      return fail(PP_E_OVERFLOW, "sum of demand * recompute cost exceeds INT64_MAX");
+  }
+  return PP_OK;
+}
+
+int check_common(int32_t n, int32_t m, const void* a, const void* b,
+                 const void* c2, const void* d2) {
+  if (n < 1) return fail(PP_E_ARG, "n must be >= 1");
+  if (m < 1 || m > 255) return fail(PP_E_ARG, "m must be in 1..255");
+  if (!a || !b || !c2 || !d2) return fail(PP_E_ARG, "null pointer argument");
+  return PP_OK;
+}
+
+pp_options default_options() {
+  pp_options o;
+  o.n_starts = 8;
+  o.max_rounds = 0;
+  o.order_seed = 0;
+  o.orders = nullptr;
+  o.flags = 0;
+  return o;
+}
+
+// Per-thread default context for the host-pointer entry points.
+pp_ctx* thread_ctx(int& rc) {
+  thread_local std::unique_ptr<pp_ctx> ctx;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    rc = fail(PP_E_DEVICE, "no HIP device");
+    return nullptr;
+  }
+  if (!ctx || ctx->device != dev) {
+    ctx.reset();
+    pp_ctx* c = nullptr;
+    rc = pp_ctx_create(&c, dev);
+    if (rc != PP_OK) return nullptr;
+    ctx.reset(c);
+  }
+  rc = PP_OK;
+  return ctx.get();
+}
+
+// Upload the tree layout and (already gathered or identity) inputs.
+int upload_tree(pp_ctx* c, const TreeLayout& t, hipStream_t st) {
+  const size_t n = (size_t)t.n;
+  PP_TRY(c->nextpos.ensure(n * 4));
+  PP_TRY(c->meta.ensure(n * 4));
+  PP_TRY(c->order.ensure(n * 4));
+  PP_HIP(hipMemcpyAsync(c->nextpos.p, t.nextpos.data(), n * 4,
+                        hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->meta.p, t.meta.data(), n * 4, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->order.p, t.order.data(), n * 4, hipMemcpyHostToDevice, st));
+  return PP_OK;
+}
+
+// Device inputs in caller ids -> context buffers in preorder.
+int layout_inputs(pp_ctx* c, const TreeLayout& t, int32_t m,
+                  const int64_t* lam, const int64_t* w, const int64_t* f,
+                  hipStream_t st) {
+  const size_t n = (size_t)t.n;
+  PP_TRY(c->lam.ensure(m * n * 8));
+  PP_TRY(c->w.ensure(m * n * 8));
+  PP_TRY(c->f.ensure((size_t)m * m * n * 8));
+  const int32_t* ord = c->order.as<int32_t>();
+  PP_HIP(launch_gather(lam, c->lam.as<int64_t>(), m, t.n, ord, st));
+  PP_HIP(launch_gather(w, c->w.as<int64_t>(), m, t.n, ord, st));
+  PP_HIP(launch_gather(f, c->f.as<int64_t>(), m * m, t.n, ord, st));
+  return PP_OK;
+}
+
+void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
+  if (!stats) return;
+  stats->best_start = r.best;
+  stats->n_starts = r.S;
+  stats->updates = r.updates;
+  stats->dp_cells = r.cells;
+  if (stats->start_objective)
+    std::copy(r.start_obj.begin(), r.start_obj.end(), stats->start_objective);
+  if (stats->start_sweeps)
+    std::copy(r.sweeps.begin(), r.sweeps.end(), stats->start_sweeps);
+  if (stats->start_accepts)
+    std::copy(r.accepts.begin(), r.accepts.end(), stats->start_accepts);
+  if (stats->standalone)
+    std::copy(r.standalone.begin(), r.standalone.end(), stats->standalone);
+  if (stats->orders) std::copy(r.orders.begin(), r.orders.end(), stats->orders);
+  stats->dp_kernel_ms = r.dp_ms;
+  stats->dp_launches = r.dp_launches;
+  (void)m;
+}
+
+template <class F>
+int guarded(F&& fn) {
+  try {
+    return fn();
+  } catch (const std::bad_alloc&) {
+    return fail(PP_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(PP_E_DEVICE, "unexpected internal exception");
+  }
+}
+
+}  // namespace
+
+// ================================================================ C ABI ===
+
+extern "C" {
+
+int pp_abi_version(void) { return PP_ABI_VERSION; }
+
+const char* pp_last_error(void) { return g_err.c_str(); }
+
+int32_t pp_num_starts(int32_t m, int32_t n_starts) {
+  return num_starts(m, n_starts);
+}
+
+int pp_orders(int32_t m, int32_t n_starts, uint64_t order_seed,
+              const int64_t* standalone, int32_t* orders) {
+  g_err.clear();
+  if (m < 1 || m > 255 || n_starts < 0 || !standalone || !orders)
+    return fail(PP_E_ARG, "bad arguments to pp_orders");
+  return guarded([&] {
+    make_orders(m, n_starts, order_seed, standalone, orders);
+    return PP_OK;
+  });
+}
+
+int pp_ctx_create(pp_ctx** ctx, int device) {
+  g_err.clear();
+  if (!ctx) return fail(PP_E_ARG, "null ctx");
+  return guarded([&]() -> int {
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || count < 1)
+      return fail(PP_E_DEVICE, "no HIP device");
+    if (device < 0 || device >= count) return fail(PP_E_ARG, "bad device index");
+    std::unique_ptr<pp_ctx> c(new pp_ctx);
+    c->device = device;
+    PP_TRY(select_device(c.get()));
+    PP_HIP(hipStreamCreateWithFlags(&c->own, hipStreamNonBlocking));
+    *ctx = c.release();
+    return PP_OK;
+  });
+}
+
+void pp_ctx_destroy(pp_ctx* ctx) {
+  if (!ctx) return;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  delete ctx;
+}
+
+int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
+                   const int64_t* demand_dev, const int64_t* recompute_dev,
+                   const int64_t* fetch_dev, const int32_t* cap,
+                   const pp_options* opt, uint8_t* target_dev,
+                   int64_t* objective, pp_stats* stats, void* hip_stream) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (!ctx) return fail(PP_E_ARG, "null ctx");
+    PP_TRY(check_common(n, m, parent, demand_dev, recompute_dev, fetch_dev));
+    if (!cap || !target_dev || !objective) return fail(PP_E_ARG, "null pointer argument");
+    const pp_options o = opt ? *opt : default_options();
+    PP_TRY(check_options(m, o));
+    for (int32_t h = 0; h < m; ++h)
+      if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    PP_TRY(select_device(ctx));
+    hipStream_t st = (hipStream_t)hip_stream;
+    // value checks on the device: negatives, and sum of lam*w added exactly
+    PP_TRY(ctx->partial.ensure(1024 * 8));
+    PP_TRY(ctx->flag.ensure(64));
+    PP_HIP(hipMemsetAsync(ctx->flag.p, 0, 4, st));
+    int32_t nb = 0;
+    PP_HIP(launch_validate(demand_dev, recompute_dev, fetch_dev, n, m,
+                           ctx->partial.as<uint64_t>(), ctx->flag.as<int32_t>(),
+                           &nb, st));
+    std::vector<uint64_t> part(nb);
+    int32_t neg = 0;
+    PP_HIP(hipMemcpyAsync(part.data(), ctx->partial.p, 8 * nb, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipMemcpyAsync(&neg, ctx->flag.p, 4, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    if (neg) return fail(PP_E_RANGE, "negative demand or cost");
+    unsigned __int128 tot = 0;
+    for (uint64_t v : part) tot += v;
+    if (tot > (unsigned __int128)INT64_MAX)
+      return fail(PP_E_OVERFLOW, "sum of demand * recompute cost exceeds INT64_MAX");
+    PP_TRY(upload_tree(ctx, t, st));
+    PP_TRY(layout_inputs(ctx, t, m, demand_dev, recompute_dev, fetch_dev, st));
+    PlanResult r;
+    PP_TRY(run_plan(ctx, t, m, cap, o, st, r));
+    // best start's placement back to caller ids
+    const size_t mn = (size_t)m * n;
+    PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.best * mn,
+                             target_dev, m, n, ctx->order.as<int32_t>(), st));
+    PP_HIP(hipStreamSynchronize(st));
+    *objective = r.start_obj[r.best];
+    fill_stats(stats, r, m);
+    return PP_OK;
+  });
+}
+
+int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
+            const int64_t* recompute_cost, const int64_t* fetch_cost,
+            const int32_t* cap, const pp_options* opt, uint8_t* target,
+            int64_t* objective, pp_stats* stats) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
+    if (!cap || !target || !objective) return fail(PP_E_ARG, "null pointer argument");
+    const pp_options o = opt ? *opt : default_options();
+    PP_TRY(check_options(m, o));
+    for (int32_t h = 0; h < m; ++h)
+      if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
+    PP_TRY(check_values(n, m, demand, recompute_cost, fetch_cost));
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    int rc = PP_OK;
+    pp_ctx* c = thread_ctx(rc);
+    if (!c) return rc;
+    hipStream_t st = c->own;
+    const size_t mn = (size_t)m * n;
+    PP_TRY(c->up_lam.ensure(mn * 8));
+    PP_TRY(c->up_w.ensure(mn * 8));
+    PP_TRY(c->up_f.ensure(mn * m * 8));
+    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
+    PP_TRY(upload_tree(c, t, st));
+    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
+                         c->up_f.as<int64_t>(), st));
+    PlanResult r;
+    PP_TRY(run_plan(c, t, m, cap, o, st, r));
+    std::vector<uint8_t> pre(mn);
+    PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.best * mn,
+                          mn, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    for (int32_t h = 0; h < m; ++h)
+      for (int32_t q = 0; q < n; ++q)
+        target[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
+    *objective = r.start_obj[r.best];
+    fill_stats(stats, r, m);
+    return PP_OK;
+  });
+}
+
+int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
+                 int32_t k, uint8_t* selected, int64_t* value) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (n < 1) return fail(PP_E_ARG, "n must be >= 1");
+    if (!parent || !profit || !selected || !value)
+      return fail(PP_E_ARG, "null pointer argument");
+    if (k < 0) return fail(PP_E_RANGE, "negative capacity");
+    unsigned __int128 tot = 0;
+    for (int32_t b = 0; b < n; ++b) {
+      if (profit[b] < 0) return fail(PP_E_RANGE, "negative profit");
+      tot += (uint64_t)profit[b];
+    }
+    if (tot > (unsigned __int128)INT64_MAX)
+      return fail(PP_E_OVERFLOW, "sum of profits exceeds INT64_MAX");
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    const int32_t kp = std::min(k, n);
+    if (kp == 0) {
+      std::memset(selected, 0, n);
+      *value = 0;
+      return PP_OK;
+    }
+    int rc = PP_OK;
+    pp_ctx* c = thread_ctx(rc);
+    if (!c) return rc;
+    hipStream_t st = c->own;
+    PP_TRY(upload_tree(c, t, st));
+    DevState d{};
+    d.n = n;
+    d.m = 1;
+    d.npad = npad_of(n);
+    d.nextpos = c->nextpos.as<int32_t>();
+    d.meta = c->meta.as<uint32_t>();
+    const int32_t slots_lds = std::max(1, t.slots);
+    const int cells = choose_cells((kp + 63) / 64, c->device, slots_lds);
+    PP_TRY(ensure_slots(c, d, 1, kp, cells));
+    PP_TRY(c->up_lam.ensure((size_t)n * 8));
+    PP_HIP(hipMemcpyAsync(c->up_lam.p, profit, (size_t)n * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(launch_gather(c->up_lam.as<int64_t>(), d.profit, 1, n,
+                         c->order.as<int32_t>(), st));
+    std::vector<int32_t> sl{0}, wk{0}, kk{kp};
+    ChainSet set = chain_set(sl, wk, kk, 0, 1);
+    Engine e;
+    e.c = c;
+    e.d = d;
+    e.st = st;
+    e.slots_lds = slots_lds;
+    e.resident = dp_resident_blocks(cells, slots_lds, c->device);
+    e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 26);
+    if (e.resident <= 0) return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident");
+    ChainState z{};
+    PP_HIP(hipMemcpyAsync(d.cs, &z, sizeof z, hipMemcpyHostToDevice, st));
+    PP_TRY(e.dp(set, 1));
+    PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
+    std::vector<uint8_t> pre(n);
+    ChainState out{};
+    PP_HIP(hipMemcpyAsync(pre.data(), d.sel, n, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    if (out.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+    for (int32_t q = 0; q < n; ++q) selected[t.order[q]] = pre[q];
+    *value = out.dpval;
+    return PP_OK;
+  });
+}
+
+// pp_marginal / pp_objective: chunks need no tree, so positions = ids.
+static int marginal_or_objective(int32_t n, int32_t m, const int64_t* demand,
+                                 const int64_t* recompute_cost,
+                                 const int64_t* fetch_cost, const uint8_t* target,
+                                 int32_t h, int64_t* profit, int64_t* gwo,
+                                 int64_t* objective) {
+  PP_TRY(check_common(n, m, demand, recompute_cost, fetch_cost, target));
+  PP_TRY(check_values(n, m, demand, recompute_cost, fetch_cost));
+  int rc = PP_OK;
+  pp_ctx* c = thread_ctx(rc);
+  if (!c) return rc;
+  hipStream_t st = c->own;
+  const size_t mn = (size_t)m * n;
+  PP_TRY(c->lam.ensure(mn * 8));
+  PP_TRY(c->w.ensure(mn * 8));
+  PP_TRY(c->f.ensure(mn * m * 8));
+  PP_HIP(hipMemcpyAsync(c->lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
+  DevState d{};
+  d.n = n;
+  d.m = m;
+  d.npad = npad_of(n);
+  d.lam = c->lam.as<int64_t>();
+  d.w = c->w.as<int64_t>();
+  d.f = c->f.as<int64_t>();
+  PP_TRY(ensure_slots(c, d, 1, 1, 1));
+  std::vector<int32_t> sl{0}, wk{h}, kk{0};
+  ChainSet set = chain_set(sl, wk, kk, 0, 1);
+  PP_HIP(launch_init_slots(set, d, 0, st));
+  PP_HIP(hipMemcpyAsync(d.tgt, target, mn, hipMemcpyHostToDevice, st));
+  PP_HIP(launch_holder_build(set, d, st));
+  ChainState out{};
+  if (profit) {
+    PP_HIP(launch_gains(set, d, st));
+    PP_HIP(hipMemcpyAsync(profit, d.profit, (size_t)n * 8, hipMemcpyDeviceToHost, st));
+  } else {
+    PP_HIP(launch_objective(set, d, st));
+  }
+  PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  if (gwo) *gwo = out.gwo;
+  if (objective) *objective = out.obj;
+  return PP_OK;
+}
+
+int pp_marginal(int32_t n, int32_t m, const int64_t* demand,
+                const int64_t* recompute_cost, const int64_t* fetch_cost,
+                const uint8_t* target, int32_t h, int64_t* profit,
+                int64_t* g_without_h) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (!profit) return fail(PP_E_ARG, "null profit");
+    if (m >= 1 && (h < 0 || h >= m)) return fail(PP_E_ARG, "h out of range");
+    std::vector<int64_t> tmp(n > 0 ? n : 1);
+    int64_t g = 0;
+    PP_TRY(marginal_or_objective(n, m, demand, recompute_cost, fetch_cost,
+                                 target, h, tmp.data(), &g, nullptr));
+    std::copy(tmp.begin(), tmp.begin() + n, profit);
+    if (g_without_h) *g_without_h = g;
+    return PP_OK;
+  });
+}
+
+int pp_objective(int32_t n, int32_t m, const int64_t* demand,
+                 const int64_t* recompute_cost, const int64_t* fetch_cost,
+                 const uint8_t* target, int64_t* objective) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (!objective) return fail(PP_E_ARG, "null objective");
+    int64_t v = 0;
+    PP_TRY(marginal_or_objective(n, m, demand, recompute_cost, fetch_cost,
+                                 target, 0, nullptr, nullptr, &v));
+    *objective = v;
+    return PP_OK;
+  });
+}
+
+}  // extern "C"

@@ -1,0 +1,108 @@
+// pp_internal.h -- shared declarations between the host driver (pp_host.cpp)
+// and the gfx950 kernels (pp_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pp {
+
+// Chains (one worker update each) handled by a single launch.
+constexpr int kMaxChains = 64;
+// "no holder" marker of the top-1 holder state (workers are < 255).
+constexpr uint8_t kNoHolder = 255;
+
+// Per-step metadata of the DP sweep, one uint32 per step s (row i = n - s in
+// the paper's 1-based preorder positions):
+//   bit 0       1: the skip operand D[next(i)][*] is the previous row
+//                  (next(i) = i + 1, b_i is a leaf); 0: it is the operand
+//                  prefetched during step s-1.
+//   bits 8..15  stack slot that row i is saved to (kSlotNone: not saved).
+//               A row is saved iff it is next(a) for some a < i - 1.
+//   bits 16..23 slot to prefetch as the skip operand of step s+1
+//               (kSlotNone: none; kSlotZero: next(i-1) = n+1, the zero row).
+constexpr uint32_t kMetaLeaf = 1u;
+constexpr uint32_t kSlotNone = 0xFFu;
+constexpr uint32_t kSlotZero = 0xFEu;
+constexpr int kMaxSlots = 254;
+
+enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
+
+// Scalars of one chain slot, updated on the device.
+struct ChainState {
+  int64_t dpval;     // D[1][k'] of the last DP sweep
+  int64_t inc;       // sum of p_h over the incumbent T_h (refinement test)
+  int64_t gwo;       // G(T_-h): objective with T_h emptied
+  int64_t obj;       // objective of the chain's placement
+  int32_t accept;    // last update adopted its DP result
+  int32_t improved;  // some update of the current sweep was accepted
+  int32_t accepts;   // accepted refinement replacements so far
+  int32_t status;    // nonzero: a device-side wait gave up
+};
+
+// The chains of one launch, passed by value as a kernel argument.
+struct ChainSet {
+  int32_t count;
+  int32_t slot[kMaxChains];    // state slot of the chain
+  int32_t worker[kMaxChains];  // worker h being updated
+  int32_t kprime[kMaxChains];  // min(k_h, n)
+  int32_t base[kMaxChains + 1];  // DP: first block of each chain's stages
+};
+
+// Device-resident problem and per-slot state of a context.
+struct DevState {
+  int32_t n, m;
+  int32_t npad;             // n rounded up to a multiple of 64
+  const int64_t* lam;       // [m][n]     demand, preorder positions
+  const int64_t* w;         // [m][n]     recompute cost, preorder
+  const int64_t* f;         // [m][m][n]  fetch cost [src][dst][pos]
+  const int32_t* nextpos;   // [n]        0-based first position after subtree
+  const uint32_t* meta;     // [n]        per-step DP metadata
+  uint8_t* tgt;             // [slots][m][n] placement, preorder
+  int64_t* v1;              // [slots][m][n] best holder saving
+  int64_t* v2;              // [slots][m][n] best saving among other holders
+  uint8_t* h1;              // [slots][m][n] holder giving v1
+  int64_t* profit;          // [slots][n]    marginal profits p_h, preorder
+  uint8_t* sel;             // [slots][npad] backtracked selection, preorder
+  uint64_t* bits;           // [slots][stages][cells][npad] DP choice bits
+  uint64_t* ring;           // [slots][stages][n][2] stage boundary values
+  ChainState* cs;           // [slots]
+  int32_t stages;           // stage stride of bits / ring
+  int32_t cells;            // cells per lane of the DP sweep
+};
+
+// Host-side launchers (pp_kernels.hip).  All enqueue on `st`.
+hipError_t launch_gather(const int64_t* src, int64_t* dst, int32_t rows,
+                         int32_t n, const int32_t* order, hipStream_t st);
+hipError_t launch_gather_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
+                            int32_t n, const int32_t* order, hipStream_t st);
+hipError_t launch_scatter_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
+                             int32_t n, const int32_t* order, hipStream_t st);
+hipError_t launch_scatter_i64(const int64_t* src, int64_t* dst, int32_t n,
+                              const int32_t* order, hipStream_t st);
+hipError_t launch_validate(const int64_t* lam, const int64_t* w,
+                           const int64_t* f, int32_t n, int32_t m,
+                           uint64_t* partial, int32_t* neg, int32_t* nblocks,
+                           hipStream_t st);
+hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
+                             int clear_tgt, hipStream_t st);
+hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
+                               hipStream_t st);
+hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st);
+hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
+                     uint32_t spin_limit, int store_bits, int32_t slots_lds,
+                     hipStream_t st);
+hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
+                            hipStream_t st);
+hipError_t launch_commit(const ChainSet& set, const DevState& d, hipStream_t st);
+hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
+                              hipStream_t st);
+hipError_t launch_objective(const ChainSet& set, const DevState& d,
+                            hipStream_t st);
+
+// Blocks of the DP sweep that can be resident at once for `cells` cells
+// per lane and `slots_lds` stack slots (0 if unsupported).
+int dp_resident_blocks(int cells, int32_t slots_lds, int device);
+size_t dp_lds_bytes(int cells, int32_t slots_lds);
+
+}  // namespace pp

@@ -1,0 +1,668 @@
+// pp_kernels.hip -- gfx950 kernels of the PrefixPlace worker update.
+//
+// One worker update (Algorithm 1, PrefixPlace procedure) is four launches
+// over every active chain (a chain is one start's current update, or one
+// standalone solve):
+//   k_gains      exact marginals p_h(b) (Eq. 7, Proposition 1) from the
+//                top-2 holder state, plus the incumbent's value for the
+//                strict-improvement test (Sec. IV-C)
+//   k_dp<C>      the rooted-tree DP sweep of Eq. 9 (Theorem 1), pipelined
+//                over the capacity axis: one wave64 "stage" owns 64*C
+//                consecutive cells j; rows are swept n..1 with no barrier
+//   k_backtrack  the acceptance decision and the backtrack (Theorem 1's
+//                "at most n states"), one wave per chain
+//   k_commit     adopt T'_h and refresh the top-2 holder state on the chunks
+//                whose membership changed
+// plus the objective F_pair (Eq. 6) and small layout helpers.
+//
+// Integers only (int64 values, int32 indices); no floating point anywhere.
+
+#include "pp_internal.h"
+
+namespace pp {
+
+namespace {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ int64_t imax(int64_t a, int64_t b) {
+  return a > b ? a : b;
+}
+
+// Eq. 5: saving of requester `r` when its copy of chunk `i` comes from
+// holder `h` (fetch plane is [src][dst][pos]).
+__device__ __forceinline__ int64_t saving(const DevState& d, int h, int r,
+                                          int64_t i) {
+  const int64_t wr = d.w[(int64_t)r * d.n + i];
+  if (h == r) return wr;
+  return imax(wr - d.f[((int64_t)h * d.m + r) * d.n + i], 0);
+}
+
+// Top-2 holder state of chunk i for every requester, from slot s's
+// placement: v1 = best saving over holders, h1 = its holder (lowest id on
+// ties), v2 = best saving over holders other than h1 (0 if none).  The
+// leave-one-out value of Eq. 7 is then v2 if h1 == h else v1.
+__device__ void refresh_holders(const DevState& d, int64_t s, int64_t i) {
+  const int64_t mn = (int64_t)d.m * d.n;
+  const uint8_t* t = d.tgt + s * mn;
+  for (int r = 0; r < d.m; ++r) {
+    int64_t b1 = 0, b2 = 0;
+    int hb = kNoHolder;
+    for (int l = 0; l < d.m; ++l) {
+      if (!t[(int64_t)l * d.n + i]) continue;
+      const int64_t q = saving(d, l, r, i);
+      if (hb == kNoHolder || q > b1) {
+        b2 = (hb == kNoHolder) ? b2 : b1;
+        b1 = q;
+        hb = l;
+      } else if (q > b2) {
+        b2 = q;
+      }
+    }
+    const int64_t o = s * mn + (int64_t)r * d.n + i;
+    d.v1[o] = b1;
+    d.v2[o] = b2;
+    d.h1[o] = (uint8_t)hb;
+  }
+}
+
+__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
+__device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
+  const uint32_t lo = readlane_u32((uint32_t)(uint64_t)v, lane);
+  const uint32_t hi = readlane_u32((uint32_t)((uint64_t)v >> 32), lane);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Lane l receives v from lane l-1 (DPP wave_shr:1); lane 0 receives `in0`.
+__device__ __forceinline__ int64_t shift_up(int64_t v, int64_t in0) {
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)(uint64_t)in0,
+                                             (int)(uint32_t)(uint64_t)v,
+                                             0x138, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(
+      (int)(uint32_t)((uint64_t)in0 >> 32), (int)(uint32_t)((uint64_t)v >> 32),
+      0x138, 0xF, 0xF, false);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__device__ __forceinline__ uint64_t ld_agent(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void st_agent(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Sum over a 256-thread block, returned in thread 0.
+__device__ int64_t block_sum(int64_t v) {
+  __shared__ int64_t part[256 / kWave];
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, kWave);
+  const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+  if (lane == 0) part[wv] = v;
+  __syncthreads();
+  int64_t t = 0;
+  if (threadIdx.x == 0)
+    for (int k = 0; k < (int)(blockDim.x / kWave); ++k) t += part[k];
+  __syncthreads();
+  return t;
+}
+
+// ------------------------------------------------------------ helpers ---
+
+__global__ void k_gather(const int64_t* __restrict__ src, int64_t* __restrict__ dst,
+                         int32_t n, const int32_t* __restrict__ order) {
+  const int64_t row = blockIdx.y;
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[row * n + i] = src[row * n + order[i]];
+}
+
+__global__ void k_gather_u8(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                            int32_t n, const int32_t* __restrict__ order) {
+  const int64_t row = blockIdx.y;
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[row * n + i] = src[row * n + order[i]];
+}
+
+__global__ void k_scatter_u8(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                             int32_t n, const int32_t* __restrict__ order) {
+  const int64_t row = blockIdx.y;
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[row * n + order[i]] = src[row * n + i];
+}
+
+__global__ void k_scatter_i64(const int64_t* __restrict__ src, int64_t* __restrict__ dst,
+                              int32_t n, const int32_t* __restrict__ order) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[order[i]] = src[i];
+}
+
+// Value checks of device-resident inputs: negatives are flagged, and each
+// block's sum of lam*w is returned (saturated to UINT64_MAX on overflow) for
+// the host to add exactly.
+__global__ void k_validate(const int64_t* __restrict__ lam, const int64_t* __restrict__ w,
+                           const int64_t* __restrict__ f, int64_t mn, int64_t mmn,
+                           uint64_t* partial, int32_t* neg) {
+  uint64_t acc = 0;
+  bool ovf = false, bad = false;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mmn;
+       x += (int64_t)gridDim.x * blockDim.x) {
+    if (f[x] < 0) bad = true;
+    if (x < mn) {
+      const int64_t a = lam[x], b = w[x];
+      if (a < 0 || b < 0) {
+        bad = true;
+        continue;
+      }
+      uint64_t prod;
+      if (__builtin_mul_overflow((uint64_t)a, (uint64_t)b, &prod) ||
+          prod > (uint64_t)INT64_MAX || acc + prod > (uint64_t)INT64_MAX)
+        ovf = true;
+      else
+        acc += prod;
+    }
+  }
+  if (bad) atomicOr(neg, 1);
+  // block sum with saturation: each term is <= INT64_MAX, so two fit u64
+  __shared__ uint64_t part[256];
+  part[threadIdx.x] = ovf ? UINT64_MAX : acc;
+  __syncthreads();
+  for (int o = blockDim.x / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      const uint64_t a = part[threadIdx.x], b = part[threadIdx.x + o];
+      part[threadIdx.x] = (a > (uint64_t)INT64_MAX || b > (uint64_t)INT64_MAX ||
+                           a + b > (uint64_t)INT64_MAX) ? UINT64_MAX : a + b;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) partial[blockIdx.x] = part[0];
+}
+
+// Reset chain slots: empty placement (optional), zero holder state and
+// chain scalars.
+__global__ void k_init_slots(ChainSet set, DevState d, int clear_tgt) {
+  const int ci = blockIdx.y;
+  const int64_t s = set.slot[ci];
+  const int64_t mn = (int64_t)d.m * d.n;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+       x += (int64_t)gridDim.x * blockDim.x) {
+    if (clear_tgt) d.tgt[s * mn + x] = 0;
+    d.v1[s * mn + x] = 0;
+    d.v2[s * mn + x] = 0;
+    d.h1[s * mn + x] = kNoHolder;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ChainState z = {};
+    d.cs[s] = z;
+  }
+}
+
+__global__ void k_holder_build(ChainSet set, DevState d) {
+  const int ci = blockIdx.y;
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < d.n) refresh_holders(d, set.slot[ci], i);
+}
+
+// ------------------------------------------------------------- gains ----
+
+// p_h(b) = sum_m Lambda_m(b) [q_{m<-h}(b) - v_m^{(-h)}(b)]_+  (Eq. 7) for
+// every preorder position, written to the chain's profit row; also the
+// incumbent's value sum_{b in T_h} p_h(b) and G(T_-h) = sum Lambda v^{(-h)}.
+__global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
+  const int ci = blockIdx.y;
+  const int64_t s = set.slot[ci];
+  const int h = set.worker[ci];
+  const int64_t n = d.n;
+  const int64_t mn = (int64_t)d.m * n;
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  int64_t p = 0, g = 0, held = 0;
+  if (i < n) {
+    for (int r = 0; r < d.m; ++r) {
+      const int64_t o = s * mn + (int64_t)r * n + i;
+      const int64_t vmh = (d.h1[o] == h) ? d.v2[o] : d.v1[o];
+      const int64_t L = d.lam[(int64_t)r * n + i];
+      p += L * imax(saving(d, h, r, i) - vmh, 0);
+      g += L * vmh;
+    }
+    d.profit[s * n + i] = p;
+    held = d.tgt[s * mn + (int64_t)h * n + i] ? p : 0;
+  }
+  const int64_t sh = block_sum(held);
+  const int64_t sg = block_sum(g);
+  if (threadIdx.x == 0) {
+    if (sh) atomicAdd((unsigned long long*)&d.cs[s].inc, (unsigned long long)sh);
+    if (sg) atomicAdd((unsigned long long*)&d.cs[s].gwo, (unsigned long long)sg);
+  }
+}
+
+// ------------------------------------------------------------ DP sweep --
+
+// Eq. 9, rows i = n..1 (step s = n - i), cells j = 1..k':
+//   D[i][j] = max(D[next(i)][j], p(b_i) + D[i+1][j-1]),  D[n+1][*] = 0,
+//   D[*][0] = 0;  choice bit = (take > skip)  (ties keep the skip branch).
+//
+// Layout: a chain's k' cells are split over G stages; stage g is one wave64
+// block owning cells j = g*64*C + l*C + c + 1 (lane l, c < C).  Row i+1
+// stays in registers; the take operand D[i+1][j-1] comes from the left
+// neighbour by a DPP lane shift, and for lane 0 from stage g-1 through a
+// per-step ring in global memory whose 64-bit words carry a launch tag in
+// their high half (relaxed agent-scope atomics; no fences).  Rows that are
+// a later skip target are saved in an LDS stack of `slots` rows; because
+// subtrees nest, the pending targets form a stack no deeper than the tree,
+// so every skip operand is on chip.  Choice bits are one ballot per cell
+// column per step, gathered 64 steps at a time and written coalesced as
+// bits[slot][g][c][step].  No per-row launch, barrier or HBM row traffic.
+template <int C>
+__global__ void __launch_bounds__(64)
+k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
+     int store_bits) {
+  extern __shared__ int64_t stk[];  // [slots][C][64]
+  const int lane = threadIdx.x;
+  const int blk = blockIdx.x;
+  if (blk >= set.base[set.count]) return;
+  int ci = 0;
+  while (ci + 1 < set.count && set.base[ci + 1] <= blk) ++ci;
+  const int64_t slot = set.slot[ci];
+  const int kp = set.kprime[ci];
+  const int g = blk - set.base[ci];
+  const int G = set.base[ci + 1] - set.base[ci];
+  const int n = d.n;
+  const int64_t* __restrict__ prof = d.profit + slot * n;
+  const uint32_t* __restrict__ meta = d.meta;
+  uint64_t* bits = d.bits + (slot * d.stages + g) * (int64_t)C * d.npad;
+  uint64_t* ring_out = d.ring + (slot * d.stages + g) * (int64_t)n * 2;
+  const uint64_t* ring_in = (g > 0) ? ring_out - (int64_t)n * 2 : nullptr;
+  const uint64_t tag = (uint64_t)epoch << 32;
+
+  int64_t x[C], pre[C];
+  uint64_t acc[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    x[c] = 0;
+    pre[c] = 0;
+    acc[c] = 0;
+  }
+  uint32_t mv = 0;
+  int64_t pv = 0;
+  int64_t bv = 0;          // ring batch: entry bbase + lane
+  int bbase = 0, bavail = 0;
+  uint32_t spins = 0;
+  bool failed = false;
+
+  for (int s = 0; s < n; ++s) {
+    const int r = s & 63;
+    if (r == 0) {
+      const int idx = s + lane;
+      mv = idx < n ? meta[idx] : 0u;
+      pv = idx < n ? prof[n - 1 - idx] : 0;
+    }
+    const uint32_t ms = readlane_u32(mv, r);
+    const int64_t ps = readlane_i64(pv, r);
+    // D[i+1][first cell - 1]: 0 for stage 0 and for the zero row n+1
+    int64_t bnd = 0;
+    if (g > 0 && s > 0) {
+      const int e = s - 1;
+      if (e >= bbase + bavail) {
+        bbase = e;
+        for (;;) {
+          const int idx = bbase + lane;
+          bool ok = false;
+          if (idx <= n - 2) {
+            const uint64_t w0 = ld_agent(ring_in + 2 * (int64_t)idx);
+            const uint64_t w1 = ld_agent(ring_in + 2 * (int64_t)idx + 1);
+            ok = (w0 & 0xFFFFFFFF00000000ull) == tag &&
+                 (w1 & 0xFFFFFFFF00000000ull) == tag;
+            bv = (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
+          }
+          const uint64_t vm = __builtin_amdgcn_ballot_w64(ok);
+          bavail = (vm == ~0ull) ? 64 : __builtin_ctzll(~vm);
+          if (bavail > 0) break;
+          if (++spins > spin_limit) {
+            failed = true;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+        if (failed) break;
+      }
+      bnd = readlane_i64(bv, e - bbase);
+    }
+    const int64_t left = shift_up(x[C - 1], bnd);
+    const bool mine = lane == r;  // this lane keeps step s's choice words
+    int64_t y[C];
+    if (ms & kMetaLeaf) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const int64_t t = ps + (c == 0 ? left : x[c - 1]);
+        const bool tk = t > x[c];
+        y[c] = tk ? t : x[c];
+        const uint64_t bm = __builtin_amdgcn_ballot_w64(tk);
+        acc[c] = mine ? bm : acc[c];
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const int64_t t = ps + (c == 0 ? left : x[c - 1]);
+        const bool tk = t > pre[c];
+        y[c] = tk ? t : pre[c];
+        const uint64_t bm = __builtin_amdgcn_ballot_w64(tk);
+        acc[c] = mine ? bm : acc[c];
+      }
+    }
+    const uint32_t sslot = (ms >> 8) & 0xFFu;
+    if (sslot != kSlotNone) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) stk[(sslot * C + c) * kWave + lane] = y[c];
+    }
+    if (g + 1 < G && lane == kWave - 1) {
+      const uint64_t v = (uint64_t)y[C - 1];
+      st_agent(ring_out + 2 * (int64_t)s, tag | (v & 0xFFFFFFFFull));
+      st_agent(ring_out + 2 * (int64_t)s + 1, tag | (v >> 32));
+    }
+    const uint32_t pslot = (ms >> 16) & 0xFFu;
+    if (pslot == kSlotZero) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) pre[c] = 0;
+    } else if (pslot != kSlotNone) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) pre[c] = stk[(pslot * C + c) * kWave + lane];
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) x[c] = y[c];
+    if (store_bits && (r == 63 || s == n - 1)) {
+      const int idx = (s & ~63) + lane;
+      if (idx < n) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) bits[(int64_t)c * d.npad + idx] = acc[c];
+      }
+    }
+  }
+  if (failed) {
+    if (lane == 0) __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  // D[1][k'] sits in stage (k'-1)/(64C), lane ((k'-1) mod 64C)/C, cell c.
+  const int jj = kp - 1;
+  if (jj / (kWave * C) == g) {
+    const int rem = jj % (kWave * C);
+    const int ln = rem / C, cc = rem % C;
+    if (lane == ln) {
+      int64_t v = 0;
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+        if (c == cc) v = x[c];
+      d.cs[slot].dpval = v;
+    }
+  }
+}
+
+// ----------------------------------------------------------- backtrack --
+
+// Acceptance (greedy: always; refinement: DP value > incumbent value, which
+// by Proposition 1 is G(T_-h, T'_h) > G(T)) and, when accepted, the walk
+// from (i=1, j=k'): take b_i if its choice bit is set (i+1, j-1), else jump
+// to next(i).  The wave loads a window of 64 rows (their next() and the
+// choice words of the current stage) at once and walks it with lane reads,
+// so memory latency is paid per window rather than per step.
+template <int C>
+__global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
+                                                  int mode) {
+  const int ci = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int64_t slot = set.slot[ci];
+  const int kp = set.kprime[ci];
+  const int n = d.n;
+  ChainState* st = d.cs + slot;
+  const int64_t dpval = st->dpval, inc = st->inc;
+  const bool accept = (mode == kModeGreedy) || (dpval > inc);
+  if (lane == 0) {
+    st->accept = accept ? 1 : 0;
+    st->inc = 0;
+    if (mode == kModeRefine && accept) {
+      st->improved = 1;
+      st->accepts += 1;
+    }
+  }
+  if (!accept) return;
+  uint8_t* sel = d.sel + slot * d.npad;
+  uint32_t* sel4 = (uint32_t*)sel;
+  for (int q = lane; q < d.npad / 4; q += kWave) sel4[q] = 0;
+  __threadfence_block();
+  __syncthreads();
+  int pos = 0, j = kp;
+  while (pos < n && j > 0) {
+    const int g = (j - 1) / (kWave * C);
+    const uint64_t* bw = d.bits + (slot * d.stages + g) * (int64_t)C * d.npad;
+    const int pos0 = pos;
+    const int q = pos0 + lane;
+    uint64_t w[C];
+    int nx = n;
+#pragma unroll
+    for (int c = 0; c < C; ++c) w[c] = 0;
+    if (q < n) {
+      const int s = n - 1 - q;
+#pragma unroll
+      for (int c = 0; c < C; ++c) w[c] = bw[(int64_t)c * d.npad + s];
+      nx = d.nextpos[q];
+    }
+    const int jlo = g * kWave * C + 1;
+    uint64_t takes = 0;
+    for (;;) {
+      const int r = pos - pos0;
+      if (r >= kWave || pos >= n || j < jlo) break;
+      const int rem = j - jlo;
+      const int ln = rem / C, cc = rem % C;
+      uint64_t word = 0;
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        const uint64_t wc = (uint64_t)readlane_i64((int64_t)w[c], r);
+        if (c == cc) word = wc;
+      }
+      if ((word >> ln) & 1ull) {
+        takes |= 1ull << r;
+        ++pos;
+        --j;
+      } else {
+        pos = (int)readlane_u32((uint32_t)nx, r);
+      }
+    }
+    if ((takes >> lane) & 1ull) sel[pos0 + lane] = 1;
+  }
+}
+
+// -------------------------------------------------------------- commit --
+
+// Adopt T'_h where accepted: write the new membership and refresh the top-2
+// holder state of every chunk whose membership changed (O(M^2) each).
+__global__ void __launch_bounds__(256) k_commit(ChainSet set, DevState d) {
+  const int ci = blockIdx.y;
+  const int64_t s = set.slot[ci];
+  if (!d.cs[s].accept) return;
+  const int h = set.worker[ci];
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= d.n) return;
+  const int64_t mn = (int64_t)d.m * d.n;
+  uint8_t* th = d.tgt + s * mn + (int64_t)h * d.n;
+  const uint8_t nv = d.sel[s * d.npad + i];
+  if (nv == th[i]) return;
+  th[i] = nv;
+  refresh_holders(d, s, i);
+}
+
+// Start of a refinement sweep: no replacement accepted yet.
+__global__ void k_reset_round(ChainSet set, DevState d) {
+  const int ci = threadIdx.x;
+  if (ci < set.count) d.cs[set.slot[ci]].improved = 0;
+}
+
+// ----------------------------------------------------------- objective --
+
+// F_pair(T) = sum_{m,b} Lambda_m(b) * v1_m(b)   (Eq. 6)
+__global__ void __launch_bounds__(256) k_objective(ChainSet set, DevState d) {
+  const int ci = blockIdx.y;
+  const int64_t s = set.slot[ci];
+  const int64_t mn = (int64_t)d.m * d.n;
+  int64_t acc = 0;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+       x += (int64_t)gridDim.x * blockDim.x)
+    acc += d.lam[x] * d.v1[s * mn + x];
+  const int64_t t = block_sum(acc);
+  if (threadIdx.x == 0 && t)
+    atomicAdd((unsigned long long*)&d.cs[s].obj, (unsigned long long)t);
+}
+
+inline dim3 grid1(int64_t work, int bs, int rows) {
+  int64_t b = (work + bs - 1) / bs;
+  if (b < 1) b = 1;
+  return dim3((unsigned)b, (unsigned)rows);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------- launchers ---
+
+hipError_t launch_gather(const int64_t* src, int64_t* dst, int32_t rows,
+                         int32_t n, const int32_t* order, hipStream_t st) {
+  hipLaunchKernelGGL(k_gather, grid1(n, 256, rows), dim3(256), 0, st, src, dst,
+                     n, order);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
+                            int32_t n, const int32_t* order, hipStream_t st) {
+  hipLaunchKernelGGL(k_gather_u8, grid1(n, 256, rows), dim3(256), 0, st, src,
+                     dst, n, order);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
+                             int32_t n, const int32_t* order, hipStream_t st) {
+  hipLaunchKernelGGL(k_scatter_u8, grid1(n, 256, rows), dim3(256), 0, st, src,
+                     dst, n, order);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_i64(const int64_t* src, int64_t* dst, int32_t n,
+                              const int32_t* order, hipStream_t st) {
+  hipLaunchKernelGGL(k_scatter_i64, grid1(n, 256, 1), dim3(256), 0, st, src,
+                     dst, n, order);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const int64_t* lam, const int64_t* w,
+                           const int64_t* f, int32_t n, int32_t m,
+                           uint64_t* partial, int32_t* neg, int32_t* nblocks,
+                           hipStream_t st) {
+  const int64_t mn = (int64_t)m * n, mmn = mn * m;
+  int64_t b = (mmn + 255) / 256;
+  if (b > 1024) b = 1024;
+  *nblocks = (int32_t)b;
+  hipLaunchKernelGGL(k_validate, dim3((unsigned)b), dim3(256), 0, st, lam, w,
+                     f, mn, mmn, partial, neg);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
+                             int clear_tgt, hipStream_t st) {
+  int64_t mn = (int64_t)d.m * d.n;
+  int64_t b = (mn + 255) / 256;
+  if (b > 2048) b = 2048;
+  hipLaunchKernelGGL(k_init_slots, dim3((unsigned)b, set.count), dim3(256), 0,
+                     st, set, d, clear_tgt);
+  return hipGetLastError();
+}
+
+hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
+                               hipStream_t st) {
+  hipLaunchKernelGGL(k_holder_build, grid1(d.n, 256, set.count), dim3(256), 0,
+                     st, set, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) {
+  hipLaunchKernelGGL(k_gains, grid1(d.n, 256, set.count), dim3(256), 0, st,
+                     set, d);
+  return hipGetLastError();
+}
+
+size_t dp_lds_bytes(int cells, int32_t slots_lds) {
+  return (size_t)(slots_lds > 0 ? slots_lds : 1) * cells * kWave * sizeof(int64_t);
+}
+
+template <int C>
+static hipError_t dp_launch_c(const ChainSet& set, const DevState& d,
+                              uint32_t epoch, uint32_t spin_limit,
+                              int store_bits, int32_t slots_lds,
+                              hipStream_t st) {
+  const size_t lds = dp_lds_bytes(C, slots_lds);
+  hipLaunchKernelGGL(k_dp<C>, dim3((unsigned)set.base[set.count]), dim3(kWave),
+                     lds, st, set, d, epoch, spin_limit, store_bits);
+  return hipGetLastError();
+}
+
+hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
+                     uint32_t spin_limit, int store_bits, int32_t slots_lds,
+                     hipStream_t st) {
+  switch (d.cells) {
+    case 1: return dp_launch_c<1>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 2: return dp_launch_c<2>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 4: return dp_launch_c<4>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 8: return dp_launch_c<8>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+int dp_resident_blocks(int cells, int32_t slots_lds, int device) {
+  int per_cu = 0, cus = 0;
+  const size_t lds = dp_lds_bytes(cells, slots_lds);
+  hipError_t e = hipErrorInvalidValue;
+  switch (cells) {
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1>, kWave, lds); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2>, kWave, lds); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4>, kWave, lds); break;
+    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<8>, kWave, lds); break;
+    default: return 0;
+  }
+  if (e != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
+    return 0;
+  return per_cu * cus;
+}
+
+hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
+                            hipStream_t st) {
+  switch (d.cells) {
+    case 1: hipLaunchKernelGGL(k_backtrack<1>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
+    case 2: hipLaunchKernelGGL(k_backtrack<2>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
+    case 4: hipLaunchKernelGGL(k_backtrack<4>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
+    case 8: hipLaunchKernelGGL(k_backtrack<8>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const ChainSet& set, const DevState& d, hipStream_t st) {
+  hipLaunchKernelGGL(k_commit, grid1(d.n, 256, set.count), dim3(256), 0, st,
+                     set, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(k_reset_round, dim3(1), dim3(kMaxChains), 0, st, set, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_objective(const ChainSet& set, const DevState& d,
+                            hipStream_t st) {
+  int64_t mn = (int64_t)d.m * d.n;
+  int64_t b = (mn + 255) / 256;
+  if (b > 1024) b = 1024;
+  hipLaunchKernelGGL(k_objective, dim3((unsigned)b, set.count), dim3(256), 0,
+                     st, set, d);
+  return hipGetLastError();
+}
+
+}  // namespace pp

@@ -1,0 +1,127 @@
+"""Boundary checks that need no GPU: the C-ABI library loads, exports every
+function include/prefixplace.h declares, and validates inputs (through
+PP_F_VALIDATE_ONLY) before any device work."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_01655_amd import binding as B
+from paper_2608_01655_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2608_01655_amd import build
+
+        build.build()
+    return B.lib()
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "prefixplace.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"\b(pp_[a-z_]+)\s*\(", src)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared_functions()
+    assert "pp_plan" in names and "pp_rooted_dp" in names
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(L, name), name
+    assert B.pp_abi_version() == 1
+
+
+def _validate(inst, **kw):
+    args = dict(n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+                order_seed=inst.order_seed, flags=B.PP_F_VALIDATE_ONLY)
+    args.update(kw)
+    return B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                     inst.fetch_cost, inst.cap, **args)
+
+
+def test_validate_only_accepts_good_input(L):
+    inst = W.make_workload("tiny")
+    p = _validate(inst)
+    assert p.target.sum() == 0  # outputs untouched
+
+
+def _expect(code, fn):
+    with pytest.raises(B.PPError) as e:
+        fn()
+    assert e.value.code == code
+    assert B.pp_last_error()
+
+
+def test_validation_errors(L):
+    rng = np.random.default_rng(0)
+    inst = W.random_instance(10, 3, rng)
+    bad = inst.parent.copy()
+    bad[3] = 3
+    _expect(B.PP_E_TREE, lambda: B.pp_plan(bad, inst.demand, inst.recompute_cost,
+                                           inst.fetch_cost, inst.cap,
+                                           flags=B.PP_F_VALIDATE_ONLY))
+    cyc = np.array([1, 2, 0, -1, -1, -1, -1, -1, -1, -1], np.int32)
+    _expect(B.PP_E_TREE, lambda: B.pp_plan(cyc, inst.demand, inst.recompute_cost,
+                                           inst.fetch_cost, inst.cap,
+                                           flags=B.PP_F_VALIDATE_ONLY))
+    oob = inst.parent.copy()
+    oob[5] = 10
+    _expect(B.PP_E_TREE, lambda: _validate_with(inst, parent=oob))
+    d = inst.demand.copy()
+    d[1, 1] = -1
+    _expect(B.PP_E_RANGE, lambda: _validate_with(inst, demand=d))
+    f = inst.fetch_cost.copy()
+    f[2, 0, 4] = -3
+    _expect(B.PP_E_RANGE, lambda: _validate_with(inst, fetch=f))
+    c = inst.cap.copy()
+    c[0] = -1
+    _expect(B.PP_E_RANGE, lambda: _validate_with(inst, cap=c))
+    big = np.full_like(inst.demand, 2 ** 31)
+    _expect(B.PP_E_OVERFLOW, lambda: _validate_with(inst, demand=big, w=big))
+    _expect(B.PP_E_ARG, lambda: _validate(inst, n_starts=-1))
+    _expect(B.PP_E_ARG, lambda: _validate(inst, n_starts=1,
+                                          orders=np.array([[0, 1, 1]], np.int32)))
+    _expect(B.PP_E_ARG, lambda: _validate(inst, n_starts=0,
+                                          orders=np.array([[0, 1, 2]], np.int32)))
+
+
+def _validate_with(inst, parent=None, demand=None, w=None, fetch=None, cap=None):
+    return B.pp_plan(inst.parent if parent is None else parent,
+                     inst.demand if demand is None else demand,
+                     inst.recompute_cost if w is None else w,
+                     inst.fetch_cost if fetch is None else fetch,
+                     inst.cap if cap is None else cap,
+                     flags=B.PP_F_VALIDATE_ONLY)
+
+
+def test_bad_sizes_rejected(L):
+    P = ctypes.c_void_p
+    z = np.zeros(4, np.int64)
+    for n, m in ((0, 1), (1, 0), (1, 256)):
+        rc = L.pp_plan(n, m, z.ctypes.data_as(P), z.ctypes.data_as(P),
+                       z.ctypes.data_as(P), z.ctypes.data_as(P),
+                       z.ctypes.data_as(P), None, z.ctypes.data_as(P),
+                       z.ctypes.data_as(P), None)
+        assert rc == B.PP_E_ARG
+    rc = L.pp_plan(1, 1, None, None, None, None, None, None, None, None, None)
+    assert rc == B.PP_E_ARG
+
+
+def test_orders_match_oracle(L, oracle_mod):
+    rng = np.random.default_rng(5)
+    for m in (1, 2, 3, 5, 6, 9, 16):
+        st = rng.integers(0, 5, size=m).astype(np.int64)  # ties
+        for S in (0, 1, 2, 8, 11):
+            seed = int(rng.integers(0, 2 ** 63))
+            assert B.pp_num_starts(m, S) == oracle_mod.num_starts(m, S)
+            np.testing.assert_array_equal(B.pp_orders(m, S, seed, st),
+                                          oracle_mod.orders(m, S, seed, st))

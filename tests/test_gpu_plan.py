@@ -1,0 +1,172 @@
+"""GPU parity of the whole planner (Algorithm 1) against the CPU oracle:
+identical placements, objective, per-start objectives, sweep and accept
+counts, standalone scores, orders and work counters -- bit-exact."""
+
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+from paper_2608_01655_amd import binding as B
+from paper_2608_01655_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "plans.json")
+
+
+@pytest.fixture(autouse=True)
+def _say_case(request):
+    print(f"\n[case] {request.node.name}", flush=True)
+    yield
+
+
+def _same(gpu, ora):
+    assert gpu.objective == ora.objective
+    np.testing.assert_array_equal(gpu.standalone, ora.standalone)
+    np.testing.assert_array_equal(gpu.orders, ora.orders)
+    np.testing.assert_array_equal(gpu.start_objective, ora.start_objective)
+    np.testing.assert_array_equal(gpu.start_sweeps, ora.start_sweeps)
+    np.testing.assert_array_equal(gpu.start_accepts, ora.start_accepts)
+    assert gpu.best_start == ora.best_start
+    assert gpu.updates == ora.updates
+    assert gpu.dp_cells == ora.dp_cells
+    np.testing.assert_array_equal(gpu.target, ora.target)
+
+
+def _plan_both(oracle_mod, inst, **kw):
+    args = dict(n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+                order_seed=inst.order_seed)
+    args.update(kw)
+    g = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                  inst.fetch_cost, inst.cap, **args)
+    orders = args.pop("orders", None)
+    o = oracle_mod.plan_instance(inst, orders_in=orders, threads=8, **args)
+    return g, o
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_plan_random(oracle_mod, seed):
+    rng = np.random.default_rng(seed)
+    m = int(rng.integers(1, 7))
+    n = int(rng.integers(1, 300))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, 200, n + 2])),
+                             source_dependent=bool(seed % 4),
+                             value_range=int(rng.choice([5, 100, 10 ** 5])))
+    g, o = _plan_both(oracle_mod, inst, n_starts=int(rng.integers(0, 5)),
+                      max_rounds=int(rng.integers(0, 4)),
+                      order_seed=int(rng.integers(0, 2 ** 62)))
+    _same(g, o)
+
+
+def test_plan_flags_and_explicit_orders(oracle_mod):
+    rng = np.random.default_rng(11)
+    inst = W.random_instance(150, 4, rng, kmax=60)
+    g, o = _plan_both(oracle_mod, inst, n_starts=3, flags=B.PP_F_NO_REFINE)
+    _same(g, o)
+    orders = np.array([[3, 2, 1, 0], [1, 3, 0, 2]], np.int32)
+    g, o = _plan_both(oracle_mod, inst, n_starts=2, orders=orders)
+    _same(g, o)
+
+
+@pytest.mark.parametrize("name", ["tiny", "tree2k", "rag10k"])
+def test_plan_small_workloads_live(oracle_mod, name):
+    inst = W.make_workload(name)
+    g, o = _plan_both(oracle_mod, inst)
+    _same(g, o)
+
+
+def _golden(name):
+    with open(GOLDEN) as fh:
+        return json.load(fh)[name]
+
+
+def _check_golden(inst, gold, plan, target):
+    assert inst.checksum() == gold["input_sha256"]
+    assert plan.objective == gold["objective"]
+    assert plan.best_start == gold["best_start"]
+    assert plan.standalone.tolist() == gold["standalone"]
+    assert plan.orders.tolist() == gold["orders"]
+    assert plan.start_objective.tolist() == gold["start_objective"]
+    assert plan.start_sweeps.tolist() == gold["start_sweeps"]
+    assert plan.start_accepts.tolist() == gold["start_accepts"]
+    assert plan.updates == gold["updates"]
+    assert plan.dp_cells == gold["dp_cells"]
+    rows = [hashlib.sha256(np.ascontiguousarray(target[h]).tobytes()).hexdigest()
+            for h in range(inst.m)]
+    assert rows == gold["target_row_sha256"]
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_plan_workloads_golden(name):
+    """All five workloads at full size against the oracle's stored plans."""
+    inst = W.make_workload(name)
+    gold = _golden(name)
+    p = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                  inst.fetch_cost, inst.cap, n_starts=inst.n_starts,
+                  max_rounds=inst.max_rounds, order_seed=inst.order_seed)
+    _check_golden(inst, gold, p, p.target)
+
+
+@pytest.mark.parametrize("name", ["rag10k", "tree50k"])
+def test_plan_device_path_golden(name):
+    """The device-resident entry point (the one the bench times) on torch
+    tensors, with kernel timing on."""
+    import torch
+
+    inst = W.make_workload(name)
+    gold = _golden(name)
+    dev = torch.device("cuda:0")
+    lam = torch.from_numpy(inst.demand).to(dev)
+    w = torch.from_numpy(inst.recompute_cost).to(dev)
+    f = torch.from_numpy(inst.fetch_cost).to(dev)
+    tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+    ctx = B.Context(0)
+    for rep in range(2):  # a warm context must give the same answer
+        p = ctx.pp_plan_device(inst.parent, lam, w, f, inst.cap, tgt,
+                               n_starts=inst.n_starts,
+                               max_rounds=inst.max_rounds,
+                               order_seed=inst.order_seed,
+                               flags=B.PP_F_TIME_KERNELS)
+        _check_golden(inst, gold, p, tgt.cpu().numpy())
+        assert p.dp_launches > 0 and p.dp_kernel_ms > 0
+    ctx.close()
+
+
+def test_plan_is_deterministic():
+    inst = W.make_workload("tree2k")
+    a = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                  inst.cap, n_starts=4, order_seed=2)
+    for cells in ("1", "4"):
+        os.environ["PP_DP_CELLS"] = cells
+        try:
+            b = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                          inst.fetch_cost, inst.cap, n_starts=4, order_seed=2)
+        finally:
+            del os.environ["PP_DP_CELLS"]
+        assert a.objective == b.objective
+        np.testing.assert_array_equal(a.target, b.target)
+        np.testing.assert_array_equal(a.start_objective, b.start_objective)
+
+
+def test_stall_guard_reports_device_error(monkeypatch):
+    """A tiny spin limit on the sweep's bounded stage-to-stage wait, forced
+    from the host: the call either completes correctly or reports
+    PP_E_DEVICE -- every kernel still exits normally."""
+    inst = W.make_workload("tree2k")
+    ref = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                    inst.fetch_cost, inst.cap, n_starts=2)
+    monkeypatch.setenv("PP_SPIN_LIMIT", "0")
+    try:
+        p = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, n_starts=2)
+        assert p.objective == ref.objective
+    except B.PPError as e:
+        assert e.code == B.PP_E_DEVICE
+    monkeypatch.delenv("PP_SPIN_LIMIT")
+    p = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                  inst.fetch_cost, inst.cap, n_starts=2)
+    assert p.objective == ref.objective
