@@ -137,32 +137,37 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
     const int32_t r = nx(a);
     if (r != a + 1 && r != n + 1) last_user[r] = a;  // descending: ends at min
   }
-  t.meta.assign(n, 0);
+  std::vector<int32_t> store(n, -1), pref(n, -1);  // pref: -1 none, -2 zero row
   int32_t top = 0, high = 0;
   for (int32_t i = n; i >= 1; --i) {
     const int32_t s = n - i;
     const int32_t r = nx(i);
-    uint32_t mw = 0;
-    if (r == i + 1) mw |= kMetaLeaf;
     if (r != i + 1 && r != n + 1 && last_user[r] == i) {
       if (slot_of[r] != top - 1) return fail(PP_E_DEVICE, "internal: stack order");
       --top;
     }
-    uint32_t store = kSlotNone;
     if (last_user[i] != INT32_MAX) {
       if (top >= kMaxSlots)
         return fail(PP_E_UNSUPPORTED,
                     "tree needs more than 254 pending subtree boundaries");
       slot_of[i] = top++;
       high = std::max(high, top);
-      store = (uint32_t)slot_of[i];
+      store[s] = slot_of[i];
     }
-    uint32_t pf = kSlotNone;
     if (i > 1) {
       const int32_t r2 = nx(i - 1);
-      if (r2 != i) pf = (r2 == n + 1) ? kSlotZero : (uint32_t)slot_of[r2];
+      if (r2 != i) pref[s] = (r2 == n + 1) ? -2 : slot_of[r2];
     }
-    t.meta[s] = mw | (store << 8) | (pf << 16);
+  }
+  // row `high` is a write sink, row `high + 1` the zero row
+  const uint32_t sink = (uint32_t)high, zero = (uint32_t)high + 1;
+  t.meta.assign(n, 0);
+  for (int32_t s = 0; s < n; ++s) {
+    const int32_t i = n - s;
+    uint32_t mw = (nx(i) == i + 1) ? kMetaLeaf : 0u;
+    mw |= (store[s] >= 0 ? (uint32_t)store[s] : sink) << 8;
+    mw |= (pref[s] >= 0 ? (uint32_t)pref[s] : (pref[s] == -2 ? zero : sink)) << 16;
+    t.meta[s] = mw;
   }
   t.slots = high;
   return PP_OK;
@@ -419,7 +424,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   Engine e;
   e.c = c;
   e.st = st;
-  e.slots_lds = std::max(1, t.slots);
+  e.slots_lds = t.slots;
   e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 26);
   e.timer.on = (o.flags & PP_F_TIME_KERNELS) != 0;
   DevState& d = e.d;
@@ -892,7 +897,7 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     d.npad = npad_of(n);
     d.nextpos = c->nextpos.as<int32_t>();
     d.meta = c->meta.as<uint32_t>();
-    const int32_t slots_lds = std::max(1, t.slots);
+    const int32_t slots_lds = t.slots;
     const int cells = choose_cells((kp + 63) / 64, c->device, slots_lds);
     PP_TRY(ensure_slots(c, d, 1, kp, cells));
     PP_TRY(c->up_lam.ensure((size_t)n * 8));

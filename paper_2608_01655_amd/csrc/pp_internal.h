@@ -13,17 +13,18 @@ constexpr int kMaxChains = 64;
 constexpr uint8_t kNoHolder = 255;
 
 // Per-step metadata of the DP sweep, one uint32 per step s (row i = n - s in
-// the paper's 1-based preorder positions):
+// the paper's 1-based preorder positions).  With H = rows of the LDS stack
+// (the deepest nesting of pending skip targets), row H is a write sink and
+// row H+1 the all-zero row:
 //   bit 0       1: the skip operand D[next(i)][*] is the previous row
-//                  (next(i) = i + 1, b_i is a leaf); 0: it is the operand
+//                  (next(i) = i + 1, b_i is a leaf); 0: it is the row
 //                  prefetched during step s-1.
-//   bits 8..15  stack slot that row i is saved to (kSlotNone: not saved).
-//               A row is saved iff it is next(a) for some a < i - 1.
-//   bits 16..23 slot to prefetch as the skip operand of step s+1
-//               (kSlotNone: none; kSlotZero: next(i-1) = n+1, the zero row).
+//   bits 8..15  LDS row that row i is saved to: its stack slot when some
+//               a < i-1 has next(a) = i, else the sink.
+//   bits 16..23 LDS row prefetched as the skip operand of step s+1: the
+//               stack slot of next(i-1), the zero row when next(i-1) = n+1,
+//               or the sink when b_{i-1} is a leaf (unused read).
 constexpr uint32_t kMetaLeaf = 1u;
-constexpr uint32_t kSlotNone = 0xFFu;
-constexpr uint32_t kSlotZero = 0xFEu;
 constexpr int kMaxSlots = 254;
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };

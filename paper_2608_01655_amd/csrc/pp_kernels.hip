@@ -244,20 +244,31 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
 //
 // Layout: a chain's k' cells are split over G stages; stage g is one wave64
 // block owning cells j = g*64*C + l*C + c + 1 (lane l, c < C).  Row i+1
-// stays in registers; the take operand D[i+1][j-1] comes from the left
-// neighbour by a DPP lane shift, and for lane 0 from stage g-1 through a
-// per-step ring in global memory whose 64-bit words carry a launch tag in
-// their high half (relaxed agent-scope atomics; no fences).  Rows that are
-// a later skip target are saved in an LDS stack of `slots` rows; because
-// subtrees nest, the pending targets form a stack no deeper than the tree,
-// so every skip operand is on chip.  Choice bits are one ballot per cell
-// column per step, gathered 64 steps at a time and written coalesced as
-// bits[slot][g][c][step].  No per-row launch, barrier or HBM row traffic.
+// stays in registers.  The take operand D[i+1][j-1] comes from the left
+// neighbour lane by a DPP shift; lane 0 gets it from stage g-1, whose last
+// cell of every row is published through a per-step ring in global memory.
+// Ring words carry a launch tag in their high half (relaxed agent-scope
+// atomics, no fences): a consumer validates each word by its tag.
+//
+// Rows that a later row skips to (next(a) for some a < i-1) are kept in an
+// LDS stack: pending targets nest like the subtrees that end at them, so at
+// most "tree depth" rows are live and every skip operand is on chip.  The
+// step body is branch-free: every step stores its row (to a sink row when
+// it is not a target) and prefetches the next step's skip operand (from the
+// zero row when next(i-1) = n+1); a leaf's skip operand is row i+1 itself.
+//
+// Steps run in batches of kBatch: per batch, each lane loads one step's
+// metadata and profit, the stage's ring input for the batch is prefetched
+// one batch ahead and validated at the batch boundary, and the choice bits
+// (one ballot per cell column per step) and ring output are written back
+// with one coalesced store each.  No per-row launch, barrier or HBM row.
+constexpr int kBatch = 32;
+
 template <int C>
 __global__ void __launch_bounds__(64)
 k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
-     int store_bits) {
-  extern __shared__ int64_t stk[];  // [slots][C][64]
+     int store_bits, int32_t slots) {
+  extern __shared__ int64_t stk[];  // [slots + 2][C][64]
   const int lane = threadIdx.x;
   const int blk = blockIdx.x;
   if (blk >= set.base[set.count]) return;
@@ -274,6 +285,40 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   uint64_t* ring_out = d.ring + (slot * d.stages + g) * (int64_t)n * 2;
   const uint64_t* ring_in = (g > 0) ? ring_out - (int64_t)n * 2 : nullptr;
   const uint64_t tag = (uint64_t)epoch << 32;
+  constexpr int kRow = C * kWave;  // int64 per LDS row
+  // the zero row (index slots + 1) is read but never written
+#pragma unroll
+  for (int c = 0; c < C; ++c) stk[(slots + 1) * kRow + c * kWave + lane] = 0;
+
+  // Ring input of the batch starting at step s0: lane u < kBatch holds
+  // D[row of step s0+u-1][first cell - 1], i.e. entry s0+u-1 of stage g-1.
+  auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
+    const int e = s0 - 1 + lane;
+    w0 = tag;
+    w1 = tag;
+    if (ring_in && lane < kBatch && e >= 0 && e <= n - 2) {
+      w0 = ld_agent(ring_in + 2 * (int64_t)e);
+      w1 = ld_agent(ring_in + 2 * (int64_t)e + 1);
+    }
+  };
+  auto ring_ok = [&](uint64_t w0, uint64_t w1) {
+    const bool ok = (w0 & 0xFFFFFFFF00000000ull) == tag &&
+                    (w1 & 0xFFFFFFFF00000000ull) == tag;
+    return __builtin_amdgcn_ballot_w64(ok) == ~0ull;
+  };
+  uint32_t spins = 0;
+  bool failed = false;
+  // wait until the ring words of the batch at s0 are all valid
+  auto ring_wait = [&](int s0, uint64_t& w0, uint64_t& w1) {
+    while (!ring_ok(w0, w1)) {
+      if (++spins > spin_limit) {
+        failed = true;
+        return;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      ring_load(s0, w0, w1);
+    }
+  };
 
   int64_t x[C], pre[C];
   uint64_t acc[C];
@@ -283,99 +328,68 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     pre[c] = 0;
     acc[c] = 0;
   }
-  uint32_t mv = 0;
-  int64_t pv = 0;
-  int64_t bv = 0;          // ring batch: entry bbase + lane
-  int bbase = 0, bavail = 0;
-  uint32_t spins = 0;
-  bool failed = false;
+  uint64_t bo = 0;  // ring output of the batch: lane u <- step s0+u
+  // first batch
+  uint32_t mv = lane < n ? meta[lane] : 0u;
+  int64_t pv = lane < n ? prof[n - 1 - lane] : 0;
+  uint64_t rw0, rw1;
+  ring_load(0, rw0, rw1);
+  ring_wait(0, rw0, rw1);
+  int64_t bv = (int64_t)((rw1 << 32) | (rw0 & 0xFFFFFFFFull));
 
-  for (int s = 0; s < n; ++s) {
-    const int r = s & 63;
-    if (r == 0) {
-      const int idx = s + lane;
-      mv = idx < n ? meta[idx] : 0u;
-      pv = idx < n ? prof[n - 1 - idx] : 0;
-    }
-    const uint32_t ms = readlane_u32(mv, r);
-    const int64_t ps = readlane_i64(pv, r);
-    // D[i+1][first cell - 1]: 0 for stage 0 and for the zero row n+1
-    int64_t bnd = 0;
-    if (g > 0 && s > 0) {
-      const int e = s - 1;
-      if (e >= bbase + bavail) {
-        bbase = e;
-        for (;;) {
-          const int idx = bbase + lane;
-          bool ok = false;
-          if (idx <= n - 2) {
-            const uint64_t w0 = ld_agent(ring_in + 2 * (int64_t)idx);
-            const uint64_t w1 = ld_agent(ring_in + 2 * (int64_t)idx + 1);
-            ok = (w0 & 0xFFFFFFFF00000000ull) == tag &&
-                 (w1 & 0xFFFFFFFF00000000ull) == tag;
-            bv = (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
-          }
-          const uint64_t vm = __builtin_amdgcn_ballot_w64(ok);
-          bavail = (vm == ~0ull) ? 64 : __builtin_ctzll(~vm);
-          if (bavail > 0) break;
-          if (++spins > spin_limit) {
-            failed = true;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(2);
-        }
-        if (failed) break;
-      }
-      bnd = readlane_i64(bv, e - bbase);
-    }
-    const int64_t left = shift_up(x[C - 1], bnd);
-    const bool mine = lane == r;  // this lane keeps step s's choice words
-    int64_t y[C];
-    if (ms & kMetaLeaf) {
+  for (int s0 = 0; s0 < n && !failed; s0 += kBatch) {
+    const int cnt = min(kBatch, n - s0);
+    const int s1 = s0 + kBatch;
+    // next batch: metadata, profits and ring input, consumed after the loop
+    const int nidx = s1 + lane;
+    const uint32_t mv_n = (lane < kBatch && nidx < n) ? meta[nidx] : 0u;
+    const int64_t pv_n = (lane < kBatch && nidx < n) ? prof[n - 1 - nidx] : 0;
+    uint64_t nw0 = tag, nw1 = tag;
+    if (s1 < n) ring_load(s1, nw0, nw1);
+
+    for (int u = 0; u < cnt; ++u) {
+      const uint32_t ms = readlane_u32(mv, u);
+      const int64_t ps = readlane_i64(pv, u);
+      const int64_t bnd = readlane_i64(bv, u);
+      const int64_t left = shift_up(x[C - 1], bnd);
+      const bool leaf = (ms & kMetaLeaf) != 0;
+      const bool mine = lane == u;
+      int64_t y[C];
 #pragma unroll
       for (int c = 0; c < C; ++c) {
+        const int64_t sk = leaf ? x[c] : pre[c];
         const int64_t t = ps + (c == 0 ? left : x[c - 1]);
-        const bool tk = t > x[c];
-        y[c] = tk ? t : x[c];
+        const bool tk = t > sk;
+        y[c] = tk ? t : sk;
         const uint64_t bm = __builtin_amdgcn_ballot_w64(tk);
         acc[c] = mine ? bm : acc[c];
       }
-    } else {
+      const int sb = (int)((ms >> 8) & 0xFFu) * kRow;
+#pragma unroll
+      for (int c = 0; c < C; ++c) stk[sb + c * kWave + lane] = y[c];
+      const int64_t y63 = readlane_i64(y[C - 1], kWave - 1);
+      bo = mine ? (uint64_t)y63 : bo;
+      const int pb = (int)((ms >> 16) & 0xFFu) * kRow;
 #pragma unroll
       for (int c = 0; c < C; ++c) {
-        const int64_t t = ps + (c == 0 ? left : x[c - 1]);
-        const bool tk = t > pre[c];
-        y[c] = tk ? t : pre[c];
-        const uint64_t bm = __builtin_amdgcn_ballot_w64(tk);
-        acc[c] = mine ? bm : acc[c];
+        pre[c] = stk[pb + c * kWave + lane];
+        x[c] = y[c];
       }
     }
-    const uint32_t sslot = (ms >> 8) & 0xFFu;
-    if (sslot != kSlotNone) {
+    const int idx = s0 + lane;
+    if (store_bits && lane < cnt) {
 #pragma unroll
-      for (int c = 0; c < C; ++c) stk[(sslot * C + c) * kWave + lane] = y[c];
+      for (int c = 0; c < C; ++c) bits[(int64_t)c * d.npad + idx] = acc[c];
     }
-    if (g + 1 < G && lane == kWave - 1) {
-      const uint64_t v = (uint64_t)y[C - 1];
-      st_agent(ring_out + 2 * (int64_t)s, tag | (v & 0xFFFFFFFFull));
-      st_agent(ring_out + 2 * (int64_t)s + 1, tag | (v >> 32));
+    if (g + 1 < G && lane < cnt) {
+      st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
+      st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
     }
-    const uint32_t pslot = (ms >> 16) & 0xFFu;
-    if (pslot == kSlotZero) {
-#pragma unroll
-      for (int c = 0; c < C; ++c) pre[c] = 0;
-    } else if (pslot != kSlotNone) {
-#pragma unroll
-      for (int c = 0; c < C; ++c) pre[c] = stk[(pslot * C + c) * kWave + lane];
-    }
-#pragma unroll
-    for (int c = 0; c < C; ++c) x[c] = y[c];
-    if (store_bits && (r == 63 || s == n - 1)) {
-      const int idx = (s & ~63) + lane;
-      if (idx < n) {
-#pragma unroll
-        for (int c = 0; c < C; ++c) bits[(int64_t)c * d.npad + idx] = acc[c];
-      }
+    mv = mv_n;
+    pv = pv_n;
+    if (s1 < n) {
+      ring_wait(s1, nw0, nw1);
+      bv = (int64_t)((nw1 << 32) | (nw0 & 0xFFFFFFFFull));
     }
   }
   if (failed) {
@@ -588,7 +602,8 @@ hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) 
 }
 
 size_t dp_lds_bytes(int cells, int32_t slots_lds) {
-  return (size_t)(slots_lds > 0 ? slots_lds : 1) * cells * kWave * sizeof(int64_t);
+  // stack rows plus the sink row and the zero row
+  return (size_t)(slots_lds + 2) * cells * kWave * sizeof(int64_t);
 }
 
 template <int C>
@@ -598,7 +613,7 @@ static hipError_t dp_launch_c(const ChainSet& set, const DevState& d,
                               hipStream_t st) {
   const size_t lds = dp_lds_bytes(C, slots_lds);
   hipLaunchKernelGGL(k_dp<C>, dim3((unsigned)set.base[set.count]), dim3(kWave),
-                     lds, st, set, d, epoch, spin_limit, store_bits);
+                     lds, st, set, d, epoch, spin_limit, store_bits, slots_lds);
   return hipGetLastError();
 }
 
