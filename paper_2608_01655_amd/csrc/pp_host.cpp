@@ -161,13 +161,17 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
   }
   // row `high` is a write sink, row `high + 1` the zero row
   const uint32_t sink = (uint32_t)high, zero = (uint32_t)high + 1;
-  t.meta.assign(n, 0);
+  const int32_t nsteps = (n + kDpBatch - 1) / kDpBatch * kDpBatch;
+  const int32_t pad = nsteps - n;
+  // leading dummy steps: leaf (skip operand = previous all-zero row), rows
+  // stored to and prefetched from the sink
+  t.meta.assign(nsteps, kMetaLeaf | (sink << 8) | (sink << 16));
   for (int32_t s = 0; s < n; ++s) {
     const int32_t i = n - s;
     uint32_t mw = (nx(i) == i + 1) ? kMetaLeaf : 0u;
     mw |= (store[s] >= 0 ? (uint32_t)store[s] : sink) << 8;
     mw |= (pref[s] >= 0 ? (uint32_t)pref[s] : (pref[s] == -2 ? zero : sink)) << 16;
-    t.meta[s] = mw;
+    t.meta[pad + s] = mw;
   }
   t.slots = high;
   return PP_OK;
@@ -280,7 +284,7 @@ int ensure_slots(pp_ctx* c, DevState& d, int32_t slots, int32_t kmax,
   PP_TRY(c->bits.ensure((size_t)slots * stages * cells * npad * 8));
   // ring words carry a launch tag; fresh memory is zeroed so that no stale
   // word can ever carry a live tag (tags start at 1)
-  PP_TRY(c->ring.ensure((size_t)slots * stages * n * 16, true));
+  PP_TRY(c->ring.ensure((size_t)slots * stages * npad * 16, true));
   PP_TRY(c->cs.ensure(slots * sizeof(ChainState)));
   d.tgt = c->tgt.as<uint8_t>();
   d.v1 = c->v1.as<int64_t>();
@@ -389,8 +393,10 @@ struct Engine {
 int choose_cells(int32_t total_stage_cells_c1, int dev, int32_t slots_lds) {
   const int forced = env_int("PP_DP_CELLS", 0);
   if (forced == 1 || forced == 2 || forced == 4 || forced == 8) return forced;
-  // fewest cells per lane whose stages of one update all fit at once
-  for (int c : {1, 2, 4, 8}) {
+  // Two cells per lane cost the same step latency as one (the row
+  // recurrence, not issue, bounds a step), so start from two; take the
+  // fewest cells per lane whose stages of one update all fit at once.
+  for (int c : {2, 4, 8}) {
     const int res = dp_resident_blocks(c, slots_lds, dev);
     if (res > 0 && (total_stage_cells_c1 + c - 1) / c <= res) return c;
   }
@@ -662,11 +668,12 @@ pp_ctx* thread_ctx(int& rc) {
 int upload_tree(pp_ctx* c, const TreeLayout& t, hipStream_t st) {
   const size_t n = (size_t)t.n;
   PP_TRY(c->nextpos.ensure(n * 4));
-  PP_TRY(c->meta.ensure(n * 4));
+  PP_TRY(c->meta.ensure(t.meta.size() * 4));
   PP_TRY(c->order.ensure(n * 4));
   PP_HIP(hipMemcpyAsync(c->nextpos.p, t.nextpos.data(), n * 4,
                         hipMemcpyHostToDevice, st));
-  PP_HIP(hipMemcpyAsync(c->meta.p, t.meta.data(), n * 4, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->meta.p, t.meta.data(), t.meta.size() * 4,
+                        hipMemcpyHostToDevice, st));
   PP_HIP(hipMemcpyAsync(c->order.p, t.order.data(), n * 4, hipMemcpyHostToDevice, st));
   return PP_OK;
 }

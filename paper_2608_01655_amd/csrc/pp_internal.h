@@ -26,6 +26,10 @@ constexpr uint8_t kNoHolder = 255;
 //               or the sink when b_{i-1} is a leaf (unused read).
 constexpr uint32_t kMetaLeaf = 1u;
 constexpr int kMaxSlots = 254;
+// The sweep runs steps in batches of kDpBatch; the step count is padded up
+// to a multiple of it with leading dummy steps (leaf, profit 0, sink rows),
+// so step s of the tree is padded step s + pad, pad = nsteps - n.
+constexpr int kDpBatch = 32;
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
 

@@ -76,15 +76,23 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+typedef int pp_int2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ pp_int2 split64(int64_t v) {
+  return __builtin_bit_cast(pp_int2, v);
+}
+
+__device__ __forceinline__ int64_t join64(pp_int2 v) {
+  return __builtin_bit_cast(int64_t, v);
+}
+
 // Lane l receives v from lane l-1 (DPP wave_shr:1); lane 0 receives `in0`.
 __device__ __forceinline__ int64_t shift_up(int64_t v, int64_t in0) {
-  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)(uint64_t)in0,
-                                             (int)(uint32_t)(uint64_t)v,
-                                             0x138, 0xF, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(
-      (int)(uint32_t)((uint64_t)in0 >> 32), (int)(uint32_t)((uint64_t)v >> 32),
-      0x138, 0xF, 0xF, false);
-  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+  const pp_int2 s = split64(v), o = split64(in0);
+  pp_int2 r;
+  r.x = __builtin_amdgcn_update_dpp(o.x, s.x, 0x138, 0xF, 0xF, false);
+  r.y = __builtin_amdgcn_update_dpp(o.y, s.y, 0x138, 0xF, 0xF, false);
+  return join64(r);
 }
 
 __device__ __forceinline__ uint64_t ld_agent(const uint64_t* p) {
@@ -238,7 +246,21 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
 
 // ------------------------------------------------------------ DP sweep --
 
-// Eq. 9, rows i = n..1 (step s = n - i), cells j = 1..k':
+// v_writelane_b32 (not exposed as a clang builtin): lane `lane` of the
+// result is `val`, every other lane keeps `old`.
+extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
+    "llvm.amdgcn.writelane.i32");
+
+__device__ __forceinline__ uint64_t writelane_u64(uint64_t old, uint64_t val,
+                                                  int lane) {
+  const uint32_t lo = (uint32_t)pp_writelane_i32((int)(uint32_t)val, lane,
+                                                 (int)(uint32_t)old);
+  const uint32_t hi = (uint32_t)pp_writelane_i32((int)(uint32_t)(val >> 32),
+                                                 lane, (int)(uint32_t)(old >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Eq. 9, rows i = n..1, cells j = 1..k':
 //   D[i][j] = max(D[next(i)][j], p(b_i) + D[i+1][j-1]),  D[n+1][*] = 0,
 //   D[*][0] = 0;  choice bit = (take > skip)  (ties keep the skip branch).
 //
@@ -257,18 +279,30 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
 // it is not a target) and prefetches the next step's skip operand (from the
 // zero row when next(i-1) = n+1); a leaf's skip operand is row i+1 itself.
 //
-// Steps run in batches of kBatch: per batch, each lane loads one step's
-// metadata and profit, the stage's ring input for the batch is prefetched
-// one batch ahead and validated at the batch boundary, and the choice bits
-// (one ballot per cell column per step) and ring output are written back
-// with one coalesced store each.  No per-row launch, barrier or HBM row.
-constexpr int kBatch = 32;
+// Steps run in batches of kBatch, fully unrolled.  The step count is padded
+// up to a multiple of kBatch with leading dummy steps (profit 0, leaf, rows
+// stay all-zero, so they change nothing).  Per batch each lane stages one
+// step's {profit, boundary value} record in LDS, read back per step with one
+// broadcast 16-byte load; the ring input is prefetched one batch ahead and
+// validated at the batch boundary; the choice bits (one ballot per cell
+// column per step, gathered with v_writelane) and the ring output are
+// written back with one coalesced store each.  No per-row launch, barrier
+// or HBM row traffic.
+constexpr int kBatch = kDpBatch;
+
+struct __attribute__((aligned(16))) StepRec {
+  int64_t p;    // profit of the step's node
+  int64_t bnd;  // D[i+1][first cell - 1] from stage g-1 (0 for stage 0)
+};
 
 template <int C>
 __global__ void __launch_bounds__(64)
 k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
      int store_bits, int32_t slots) {
-  extern __shared__ int64_t stk[];  // [slots + 2][C][64]
+  extern __shared__ int64_t lds[];
+  constexpr int kRow = C * kWave;  // int64 per LDS row
+  int64_t* stk = lds;              // [slots + 2][C][64]
+  StepRec* rec = (StepRec*)(lds + (slots + 2) * kRow);  // [kBatch]
   const int lane = threadIdx.x;
   const int blk = blockIdx.x;
   if (blk >= set.base[set.count]) return;
@@ -279,24 +313,24 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const int g = blk - set.base[ci];
   const int G = set.base[ci + 1] - set.base[ci];
   const int n = d.n;
+  const int nsteps = (n + kBatch - 1) / kBatch * kBatch;
+  const int pad = nsteps - n;  // leading dummy steps
+  const int64_t stride = (int64_t)d.npad;  // steps per stage row of bits/ring
   const int64_t* __restrict__ prof = d.profit + slot * n;
-  const uint32_t* __restrict__ meta = d.meta;
-  uint64_t* bits = d.bits + (slot * d.stages + g) * (int64_t)C * d.npad;
-  uint64_t* ring_out = d.ring + (slot * d.stages + g) * (int64_t)n * 2;
-  const uint64_t* ring_in = (g > 0) ? ring_out - (int64_t)n * 2 : nullptr;
+  const uint32_t* __restrict__ meta = d.meta;  // [nsteps], padded
+  uint64_t* bits = d.bits + (slot * d.stages + g) * (int64_t)C * stride;
+  uint64_t* ring_out = d.ring + (slot * d.stages + g) * stride * 2;
+  const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
   const uint64_t tag = (uint64_t)epoch << 32;
-  constexpr int kRow = C * kWave;  // int64 per LDS row
-  // the zero row (index slots + 1) is read but never written
 #pragma unroll
   for (int c = 0; c < C; ++c) stk[(slots + 1) * kRow + c * kWave + lane] = 0;
 
-  // Ring input of the batch starting at step s0: lane u < kBatch holds
-  // D[row of step s0+u-1][first cell - 1], i.e. entry s0+u-1 of stage g-1.
+  // ring input of the batch at s0: lane u < kBatch <- entry s0+u-1
   auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
     const int e = s0 - 1 + lane;
     w0 = tag;
     w1 = tag;
-    if (ring_in && lane < kBatch && e >= 0 && e <= n - 2) {
+    if (ring_in && lane < kBatch && e >= 0) {
       w0 = ld_agent(ring_in + 2 * (int64_t)e);
       w1 = ld_agent(ring_in + 2 * (int64_t)e + 1);
     }
@@ -308,7 +342,6 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   };
   uint32_t spins = 0;
   bool failed = false;
-  // wait until the ring words of the batch at s0 are all valid
   auto ring_wait = [&](int s0, uint64_t& w0, uint64_t& w1) {
     while (!ring_ok(w0, w1)) {
       if (++spins > spin_limit) {
@@ -318,6 +351,11 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       __builtin_amdgcn_s_sleep(2);
       ring_load(s0, w0, w1);
     }
+  };
+  // profit of padded step t (0 for the leading dummy steps)
+  auto profit_at = [&](int t) -> int64_t {
+    const int s = t - pad;
+    return (lane < kBatch && s >= 0 && s < n) ? prof[n - 1 - s] : 0;
   };
 
   int64_t x[C], pre[C];
@@ -329,65 +367,81 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     acc[c] = 0;
   }
   uint64_t bo = 0;  // ring output of the batch: lane u <- step s0+u
-  // first batch
-  uint32_t mv = lane < n ? meta[lane] : 0u;
-  int64_t pv = lane < n ? prof[n - 1 - lane] : 0;
+  uint32_t mv = lane < kBatch ? meta[lane] : 0u;
+  int64_t pv = profit_at(lane);
   uint64_t rw0, rw1;
   ring_load(0, rw0, rw1);
   ring_wait(0, rw0, rw1);
   int64_t bv = (int64_t)((rw1 << 32) | (rw0 & 0xFFFFFFFFull));
 
-  for (int s0 = 0; s0 < n && !failed; s0 += kBatch) {
-    const int cnt = min(kBatch, n - s0);
+  for (int s0 = 0; s0 < nsteps && !failed; s0 += kBatch) {
     const int s1 = s0 + kBatch;
+    if (lane < kBatch) {
+      StepRec r;
+      r.p = pv;
+      r.bnd = bv;
+      rec[lane] = r;
+    }
     // next batch: metadata, profits and ring input, consumed after the loop
-    const int nidx = s1 + lane;
-    const uint32_t mv_n = (lane < kBatch && nidx < n) ? meta[nidx] : 0u;
-    const int64_t pv_n = (lane < kBatch && nidx < n) ? prof[n - 1 - nidx] : 0;
+    const uint32_t mv_n = (lane < kBatch && s1 < nsteps) ? meta[s1 + lane] : 0u;
+    const int64_t pv_n = profit_at(s1 + lane);
     uint64_t nw0 = tag, nw1 = tag;
-    if (s1 < n) ring_load(s1, nw0, nw1);
+    if (s1 < nsteps) ring_load(s1, nw0, nw1);
 
-    for (int u = 0; u < cnt; ++u) {
-      const uint32_t ms = readlane_u32(mv, u);
-      const int64_t ps = readlane_i64(pv, u);
-      const int64_t bnd = readlane_i64(bv, u);
-      const int64_t left = shift_up(x[C - 1], bnd);
+    // Software pipeline: the records of steps u+1 and u+2 and the meta
+    // word of step u+1 are in flight while step u computes, and the skip
+    // operand of step u+1 is read at the top of step u.  That read may
+    // precede step u's own store: a non-leaf step's skip row was produced
+    // at least two steps earlier and sits in a slot no later push reuses
+    // while it is pending, and a leaf's skip operand is the row in
+    // registers.
+    StepRec rq[3];
+    rq[0] = rec[0];
+    rq[1] = rec[1];
+    uint32_t ms_next = readlane_u32(mv, 0);
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (u + 2 < kBatch) rq[(u + 2) % 3] = rec[u + 2];
+      const uint32_t ms = ms_next;
+      if (u + 1 < kBatch) ms_next = readlane_u32(mv, u + 1);
+      const int pb = (int)((ms >> 16) & 0xFFu) * kRow;
+      int64_t pnext[C];
+#pragma unroll
+      for (int c = 0; c < C; ++c) pnext[c] = stk[pb + c * kWave + lane];
+      const StepRec cur = rq[u % 3];
+      const int64_t left = shift_up(x[C - 1], cur.bnd);
       const bool leaf = (ms & kMetaLeaf) != 0;
-      const bool mine = lane == u;
       int64_t y[C];
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         const int64_t sk = leaf ? x[c] : pre[c];
-        const int64_t t = ps + (c == 0 ? left : x[c - 1]);
+        const int64_t t = cur.p + (c == 0 ? left : x[c - 1]);
         const bool tk = t > sk;
         y[c] = tk ? t : sk;
-        const uint64_t bm = __builtin_amdgcn_ballot_w64(tk);
-        acc[c] = mine ? bm : acc[c];
+        acc[c] = writelane_u64(acc[c], __builtin_amdgcn_ballot_w64(tk), u);
       }
       const int sb = (int)((ms >> 8) & 0xFFu) * kRow;
 #pragma unroll
       for (int c = 0; c < C; ++c) stk[sb + c * kWave + lane] = y[c];
-      const int64_t y63 = readlane_i64(y[C - 1], kWave - 1);
-      bo = mine ? (uint64_t)y63 : bo;
-      const int pb = (int)((ms >> 16) & 0xFFu) * kRow;
+      bo = writelane_u64(bo, (uint64_t)readlane_i64(y[C - 1], kWave - 1), u);
 #pragma unroll
       for (int c = 0; c < C; ++c) {
-        pre[c] = stk[pb + c * kWave + lane];
+        pre[c] = pnext[c];
         x[c] = y[c];
       }
     }
     const int idx = s0 + lane;
-    if (store_bits && lane < cnt) {
+    if (store_bits && lane < kBatch) {
 #pragma unroll
-      for (int c = 0; c < C; ++c) bits[(int64_t)c * d.npad + idx] = acc[c];
+      for (int c = 0; c < C; ++c) bits[(int64_t)c * stride + idx] = acc[c];
     }
-    if (g + 1 < G && lane < cnt) {
+    if (g + 1 < G && lane < kBatch) {
       st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
       st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
     }
     mv = mv_n;
     pv = pv_n;
-    if (s1 < n) {
+    if (s1 < nsteps) {
       ring_wait(s1, nw0, nw1);
       bv = (int64_t)((nw1 << 32) | (nw0 & 0xFFFFFFFFull));
     }
@@ -455,8 +509,9 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     int nx = n;
 #pragma unroll
     for (int c = 0; c < C; ++c) w[c] = 0;
+    const int pad = (n + kDpBatch - 1) / kDpBatch * kDpBatch - n;
     if (q < n) {
-      const int s = n - 1 - q;
+      const int s = n - 1 - q + pad;  // padded step of row q
 #pragma unroll
       for (int c = 0; c < C; ++c) w[c] = bw[(int64_t)c * d.npad + s];
       nx = d.nextpos[q];
@@ -602,8 +657,9 @@ hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) 
 }
 
 size_t dp_lds_bytes(int cells, int32_t slots_lds) {
-  // stack rows plus the sink row and the zero row
-  return (size_t)(slots_lds + 2) * cells * kWave * sizeof(int64_t);
+  // stack rows plus the sink row and the zero row, then the step records
+  return (size_t)(slots_lds + 2) * cells * kWave * sizeof(int64_t) +
+         kBatch * sizeof(StepRec);
 }
 
 template <int C>
