@@ -119,8 +119,10 @@ int32_t pp_num_starts(int32_t m, int32_t n_starts);
  *                            parent-closed with at most cap[m] ones
  *   objective                host out: F_pair(T) in request * us
  *   stats                    NULL or statistics
- * Limits: the tree's nesting of pending subtree boundaries (at most its
- * depth) must not exceed 255, else PP_E_UNSUPPORTED. */
+ * Limits: the DP sweep keeps pending skip-target rows in LDS; their number
+ * (at most the tree depth; 11 and 14 on the benchmark trees) must not exceed
+ * 254, and the rows must fit one compute unit's LDS (about 280 rows at one
+ * cell per lane), else PP_E_UNSUPPORTED. */
 int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
             const int64_t *recompute_cost, const int64_t *fetch_cost,
             const int32_t *cap, const pp_options *opt, uint8_t *target,
@@ -170,6 +172,21 @@ int pp_plan_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
                    const int64_t *fetch_dev, const int32_t *cap,
                    const pp_options *opt, uint8_t *target_dev,
                    int64_t *objective, pp_stats *stats, void *hip_stream);
+
+/* Host only, for inspection and CPU-side checks of the DP sweep's step
+ * schedule: for the tree `parent` and `cells` (1, 2 or 4) DP cells per
+ * lane, writes the per-step metadata of the sweep (`meta`, may be NULL to
+ * query the size; 2 * nsteps words, nsteps = n padded up to a multiple of 32
+ * with leading dummy steps) and the number of LDS stack rows H.  Rows hold
+ * 64*cells int64 in the order [H stack rows | zero row | sink row].  Per
+ * step: word 0 = byte offset of the row the step's DP row is written to
+ * (its stack slot when a later row skips to it, else the sink); word 1 =
+ * byte offset of the row read as the next step's skip operand (Eq. 9's
+ * D[next(i)][*]), plus 256 when the next step's node is a leaf (its skip
+ * operand is then the previous row and the read is unused).  The first
+ * step's node is always a leaf. */
+int pp_sweep_layout(int32_t n, const int32_t *parent, int32_t cells,
+                    uint32_t *meta, int32_t *nsteps, int32_t *slots);
 
 /* Description of the last error on the calling thread; valid until the
  * next pp_* call on that thread. */

@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
         L.pp_marginal.argtypes = [i32, i32, _P, _P, _P, _P, i32, _P, _P]
         L.pp_objective.argtypes = [i32, i32, _P, _P, _P, _P, _P]
         L.pp_orders.argtypes = [i32, i32, u64, _P, _P]
+        L.pp_sweep_layout.argtypes = [i32, _P, i32, _P, _P, _P]
+        L.pp_sweep_layout.restype = ctypes.c_int
         L.pp_ctx_create.argtypes = [ctypes.POINTER(_P), ctypes.c_int]
         L.pp_ctx_destroy.argtypes = [_P]
         L.pp_ctx_destroy.restype = None
@@ -219,6 +221,19 @@ def pp_orders(m, n_starts, order_seed, standalone):
     _check(lib().pp_orders(m, n_starts, int(order_seed) & (2 ** 64 - 1),
                            _p(st), _p(out)))
     return out
+
+
+def pp_sweep_layout(parent, cells):
+    """Per-step metadata of the DP sweep for a tree (host only)."""
+    parent = _c(parent, np.int32)
+    n = parent.shape[0]
+    ns, sl = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().pp_sweep_layout(n, _p(parent), int(cells), None,
+                                 ctypes.byref(ns), ctypes.byref(sl)))
+    meta = np.zeros((ns.value, 2), np.uint32)
+    _check(lib().pp_sweep_layout(n, _p(parent), int(cells), _p(meta),
+                                 ctypes.byref(ns), ctypes.byref(sl)))
+    return meta, sl.value
 
 
 class Context:

@@ -80,7 +80,11 @@ struct DevBuf {
 struct TreeLayout {
   int32_t n = 0;
   std::vector<int32_t> order, nextpos;
-  std::vector<uint32_t> meta;
+  // per padded DP step: leaf flag, stack slot the row is kept in (-1: not a
+  // skip target), and the padded step whose row is the next step's skip
+  // operand (-1: the next step is a leaf or there is none, -2: zero row)
+  std::vector<uint8_t> leaf;
+  std::vector<int32_t> store, src;
   int32_t slots = 0;    // LDS stack rows the sweep needs
   bool identity = true; // caller ids are already in preorder
 };
@@ -137,11 +141,16 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
     const int32_t r = nx(a);
     if (r != a + 1 && r != n + 1) last_user[r] = a;  // descending: ends at min
   }
-  std::vector<int32_t> store(n, -1), pref(n, -1);  // pref: -1 none, -2 zero row
+  const int32_t nsteps = (n + kDpBatch - 1) / kDpBatch * kDpBatch;
+  const int32_t pad = nsteps - n;
+  t.leaf.assign(nsteps, 1);
+  t.store.assign(nsteps, -1);
+  t.src.assign(nsteps, -2);
   int32_t top = 0, high = 0;
   for (int32_t i = n; i >= 1; --i) {
-    const int32_t s = n - i;
+    const int32_t s = pad + n - i;  // padded step of row i
     const int32_t r = nx(i);
+    t.leaf[s] = (r == i + 1) ? 1 : 0;
     if (r != i + 1 && r != n + 1 && last_user[r] == i) {
       if (slot_of[r] != top - 1) return fail(PP_E_DEVICE, "internal: stack order");
       --top;
@@ -152,30 +161,37 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
                     "tree needs more than 254 pending subtree boundaries");
       slot_of[i] = top++;
       high = std::max(high, top);
-      store[s] = slot_of[i];
+      t.store[s] = slot_of[i];
     }
+    t.src[s] = -1;
     if (i > 1) {
       const int32_t r2 = nx(i - 1);
-      if (r2 != i) pref[s] = (r2 == n + 1) ? -2 : slot_of[r2];
+      if (r2 != i) t.src[s] = (r2 == n + 1) ? -2 : pad + n - r2;
     }
-  }
-  // row `high` is a write sink, row `high + 1` the zero row
-  const uint32_t sink = (uint32_t)high, zero = (uint32_t)high + 1;
-  const int32_t nsteps = (n + kDpBatch - 1) / kDpBatch * kDpBatch;
-  const int32_t pad = nsteps - n;
-  // leading dummy steps: leaf (skip operand = previous all-zero row), rows
-  // stored to and prefetched from the sink
-  t.meta.assign(nsteps, kMetaLeaf | (sink << 8) | (sink << 16));
-  for (int32_t s = 0; s < n; ++s) {
-    const int32_t i = n - s;
-    uint32_t mw = (nx(i) == i + 1) ? kMetaLeaf : 0u;
-    mw |= (store[s] >= 0 ? (uint32_t)store[s] : sink) << 8;
-    mw |= (pref[s] >= 0 ? (uint32_t)pref[s] : (pref[s] == -2 ? zero : sink)) << 16;
-    t.meta[pad + s] = mw;
   }
   t.slots = high;
   return PP_OK;
 }
+
+// DP-sweep metadata for `cells` cells per lane (layout in pp_internal.h):
+// two words per padded step.
+std::vector<uint32_t> encode_meta(const TreeLayout& t, int cells) {
+  const int64_t row = (int64_t)cells * 64 * 8;  // bytes per LDS stack row
+  const int64_t zero = (int64_t)t.slots * row, sink = zero + row;
+  const int32_t nsteps = (int32_t)t.leaf.size();
+  std::vector<uint32_t> meta(2 * (size_t)nsteps);
+  for (int32_t s = 0; s < nsteps; ++s) {
+    const int32_t r = t.src[s];
+    const int64_t st = t.store[s] >= 0 ? (int64_t)t.store[s] * row : sink;
+    const int64_t pf = r >= 0 ? (int64_t)t.store[r] * row : zero;
+    const bool next_leaf = s + 1 < nsteps && t.leaf[s + 1];
+    meta[2 * (size_t)s] = (uint32_t)st;
+    meta[2 * (size_t)s + 1] = (uint32_t)pf | (next_leaf ? kLeafByte : 0u);
+  }
+  return meta;
+}
+
+int upload_meta(pp_ctx* c, const TreeLayout& t, int cells, hipStream_t st);
 
 // ------------------------------------------------------------- orders ---
 
@@ -250,6 +266,7 @@ struct pp_ctx {
   DevBuf tgt, v1, v2, h1, profit, sel, bits, ring, cs;
   DevBuf partial, flag;
   uint32_t epoch = 0;
+  std::vector<uint32_t> meta_host;  // source of the last metadata upload
   std::vector<hipEvent_t> events;
   ~pp_ctx() {
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &meta, &order, &up_lam, &up_w,
@@ -343,12 +360,15 @@ struct Engine {
   int32_t slots_lds;
   int resident;       // DP blocks resident at once
   uint32_t spin_limit;
+  int fmax = 0;  // every DP value < 2^62: max via v_max_f64
   hipStream_t st;
   Timer timer;
 
   // One DP sweep over the chains of `set` (kprime >= 1 each), split into
   // launches whose stages all fit on the device at once.
   int dp(const ChainSet& in, int store_bits) {
+    if (!d.meta || !d.profit || !d.bits || !d.ring || !d.cs)
+      return fail(PP_E_DEVICE, "internal: DP sweep buffers are not set");
     const int cellsw = 64 * d.cells;
     int32_t k = 0;
     while (k < in.count) {
@@ -372,7 +392,8 @@ struct Engine {
                     "capacity needs more DP stages than the device holds");
       if (++c->epoch == 0) ++c->epoch;  // tag 0 marks never-written words
       PP_TRY(timer_mark(c, timer, true, st));
-      PP_HIP(launch_dp(s, d, c->epoch, spin_limit, store_bits, slots_lds, st));
+      PP_HIP(launch_dp(s, d, c->epoch, spin_limit, store_bits, slots_lds, fmax,
+                       st));
       PP_TRY(timer_mark(c, timer, false, st));
     }
     return PP_OK;
@@ -390,17 +411,40 @@ struct Engine {
   }
 };
 
+// Cells per lane for a launch whose chains need `total_stage_cells_c1`
+// stages at one cell per lane.  A stage is one wave; alone on its SIMD its
+// row step takes about 61 / 77 / 125 ns at 1 / 2 / 4 cells per lane (it is
+// bound by the wave's instruction issue).  When stages outnumber SIMDs they
+// share the SIMDs' vector units, so the estimate is scaled by the waves per
+// SIMD (about three quarters of a step's instructions are vector ops).
+// Only widths whose stages all fit on the device at once are considered; if
+// none fits, the width with the most resident blocks is used and launches
+// are split.
 int choose_cells(int32_t total_stage_cells_c1, int dev, int32_t slots_lds) {
   const int forced = env_int("PP_DP_CELLS", 0);
-  if (forced == 1 || forced == 2 || forced == 4 || forced == 8) return forced;
-  // Two cells per lane cost the same step latency as one (the row
-  // recurrence, not issue, bounds a step), so start from two; take the
-  // fewest cells per lane whose stages of one update all fit at once.
-  for (int c : {2, 4, 8}) {
-    const int res = dp_resident_blocks(c, slots_lds, dev);
-    if (res > 0 && (total_stage_cells_c1 + c - 1) / c <= res) return c;
+  if (forced == 1 || forced == 2 || forced == 4) return forced;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 256;
+  const double simds = 4.0 * cus;
+  const struct { int c; double ns; } widths[] = {{1, 61.0}, {2, 77.0}, {4, 125.0}};
+  int best = 0, most = 2, most_res = 0;
+  double best_cost = 0.0;
+  for (const auto& w : widths) {
+    const int res = dp_resident_blocks(w.c, slots_lds, dev);
+    const int32_t stages = (total_stage_cells_c1 + w.c - 1) / w.c;
+    if (res > most_res) {
+      most = w.c;
+      most_res = res;
+    }
+    if (res <= 0 || stages > res) continue;
+    const double cost = w.ns * std::max(1.0, 0.75 * stages / simds);
+    if (best == 0 || cost < best_cost) {
+      best = w.c;
+      best_cost = cost;
+    }
   }
-  return 8;
+  return best ? best : most;
 }
 
 struct PlanResult {
@@ -414,7 +458,8 @@ struct PlanResult {
 
 // Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
 int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
-             const pp_options& o, hipStream_t st, PlanResult& res) {
+             const pp_options& o, bool fmax_ok, hipStream_t st,
+             PlanResult& res) {
   const int32_t n = t.n;
   const int32_t S = num_starts(m, o.n_starts);
   res.S = S;
@@ -431,7 +476,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   e.c = c;
   e.st = st;
   e.slots_lds = t.slots;
-  e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 26);
+  e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 22);
   e.timer.on = (o.flags & PP_F_TIME_KERNELS) != 0;
   DevState& d = e.d;
   d = DevState{};
@@ -442,7 +487,6 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   d.w = c->w.as<int64_t>();
   d.f = c->f.as<int64_t>();
   d.nextpos = c->nextpos.as<int32_t>();
-  d.meta = c->meta.as<uint32_t>();
   // widest single launch: every start's update at once
   int64_t stage64 = 0;
   {
@@ -457,7 +501,10 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   if (e.resident <= 0)
     return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident (LDS stack of " +
                                       std::to_string(e.slots_lds) + " rows)");
+  e.fmax = fmax_ok && env_int("PP_DP_NO_FMAX", 0) == 0;
   PP_TRY(ensure_slots(c, d, slots, kmax, cells));
+  PP_TRY(upload_meta(c, t, cells, st));
+  d.meta = c->meta.as<uint32_t>();  // upload_meta may have (re)allocated it
 
   // --- standalone scores: each worker against the empty placement
   res.standalone.assign(m, 0);
@@ -611,7 +658,7 @@ int check_options(int32_t m, const pp_options& o) {
 }
 
 int check_values(int32_t n, int32_t m, const int64_t* lam, const int64_t* w,
-                 const int64_t* f) {
+                 const int64_t* f, unsigned __int128* total = nullptr) {
   const size_t mn = (size_t)m * n;
   for (size_t x = 0; x < mn; ++x)
     if (lam[x] < 0 || w[x] < 0)
@@ -624,8 +671,13 @@ int check_values(int32_t n, int32_t m, const int64_t* lam, const int64_t* w,
     if (tot > (unsigned __int128)INT64_MAX)
       return fail(PP_E_OVERFLOW, "sum of demand * recompute cost exceeds INT64_MAX");
   }
+  if (total) *total = tot;
   return PP_OK;
 }
+
+// Every marginal, DP value and objective is at most sum Lambda*w; below
+// 2^62 the sweep may take its maximum with v_max_f64 on the bit patterns.
+constexpr unsigned __int128 kFmaxBound = (unsigned __int128)1 << 62;
 
 int check_common(int32_t n, int32_t m, const void* a, const void* b,
                  const void* c2, const void* d2) {
@@ -668,13 +720,36 @@ pp_ctx* thread_ctx(int& rc) {
 int upload_tree(pp_ctx* c, const TreeLayout& t, hipStream_t st) {
   const size_t n = (size_t)t.n;
   PP_TRY(c->nextpos.ensure(n * 4));
-  PP_TRY(c->meta.ensure(t.meta.size() * 4));
+
   PP_TRY(c->order.ensure(n * 4));
   PP_HIP(hipMemcpyAsync(c->nextpos.p, t.nextpos.data(), n * 4,
                         hipMemcpyHostToDevice, st));
-  PP_HIP(hipMemcpyAsync(c->meta.p, t.meta.data(), t.meta.size() * 4,
-                        hipMemcpyHostToDevice, st));
+
   PP_HIP(hipMemcpyAsync(c->order.p, t.order.data(), n * 4, hipMemcpyHostToDevice, st));
+  return PP_OK;
+}
+
+// Every LDS row the metadata names must lie inside the sweep's LDS layout.
+int check_meta(const TreeLayout& t, const std::vector<uint32_t>& meta,
+               int cells) {
+  if (t.leaf.empty() || !t.leaf[0])
+    return fail(PP_E_DEVICE, "internal: the first DP step must be a leaf");
+  const int64_t row = (int64_t)cells * 64 * 8;  // bytes
+  for (size_t q = 0; q < meta.size(); q += 2) {
+    const int64_t st = meta[q], pf = meta[q + 1] & ~kLeafByte;
+    if (st % row != 0 || st / row > t.slots + 1 || pf % row != 0 ||
+        pf / row > t.slots)
+      return fail(PP_E_DEVICE, "internal: DP step metadata out of range");
+  }
+  return PP_OK;
+}
+
+int upload_meta(pp_ctx* c, const TreeLayout& t, int cells, hipStream_t st) {
+  c->meta_host = encode_meta(t, cells);
+  PP_TRY(check_meta(t, c->meta_host, cells));
+  PP_TRY(c->meta.ensure(c->meta_host.size() * 4));
+  PP_HIP(hipMemcpyAsync(c->meta.p, c->meta_host.data(), c->meta_host.size() * 4,
+                        hipMemcpyHostToDevice, st));
   return PP_OK;
 }
 
@@ -749,6 +824,25 @@ int pp_orders(int32_t m, int32_t n_starts, uint64_t order_seed,
   });
 }
 
+int pp_sweep_layout(int32_t n, const int32_t* parent, int32_t cells,
+                    uint32_t* meta, int32_t* nsteps, int32_t* slots) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (n < 1 || !parent || !nsteps || !slots)
+      return fail(PP_E_ARG, "bad arguments to pp_sweep_layout");
+    if (cells != 1 && cells != 2 && cells != 4)
+      return fail(PP_E_ARG, "cells must be 1, 2 or 4");
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    const std::vector<uint32_t> mv = encode_meta(t, cells);
+    PP_TRY(check_meta(t, mv, cells));
+    if (meta) std::copy(mv.begin(), mv.end(), meta);
+    *nsteps = (int32_t)(mv.size() / 2);
+    *slots = t.slots;
+    return PP_OK;
+  });
+}
+
 int pp_ctx_create(pp_ctx** ctx, int device) {
   g_err.clear();
   if (!ctx) return fail(PP_E_ARG, "null ctx");
@@ -813,7 +907,7 @@ int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     PP_TRY(upload_tree(ctx, t, st));
     PP_TRY(layout_inputs(ctx, t, m, demand_dev, recompute_dev, fetch_dev, st));
     PlanResult r;
-    PP_TRY(run_plan(ctx, t, m, cap, o, st, r));
+    PP_TRY(run_plan(ctx, t, m, cap, o, tot < kFmaxBound, st, r));
     // best start's placement back to caller ids
     const size_t mn = (size_t)m * n;
     PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.best * mn,
@@ -837,7 +931,8 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
     PP_TRY(check_options(m, o));
     for (int32_t h = 0; h < m; ++h)
       if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
-    PP_TRY(check_values(n, m, demand, recompute_cost, fetch_cost));
+    unsigned __int128 tot = 0;
+    PP_TRY(check_values(n, m, demand, recompute_cost, fetch_cost, &tot));
     TreeLayout t;
     PP_TRY(build_tree(n, parent, t));
     if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
@@ -856,7 +951,7 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
     PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
                          c->up_f.as<int64_t>(), st));
     PlanResult r;
-    PP_TRY(run_plan(c, t, m, cap, o, st, r));
+    PP_TRY(run_plan(c, t, m, cap, o, tot < kFmaxBound, st, r));
     std::vector<uint8_t> pre(mn);
     PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.best * mn,
                           mn, hipMemcpyDeviceToHost, st));
@@ -903,10 +998,11 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     d.m = 1;
     d.npad = npad_of(n);
     d.nextpos = c->nextpos.as<int32_t>();
-    d.meta = c->meta.as<uint32_t>();
     const int32_t slots_lds = t.slots;
     const int cells = choose_cells((kp + 63) / 64, c->device, slots_lds);
     PP_TRY(ensure_slots(c, d, 1, kp, cells));
+    PP_TRY(upload_meta(c, t, cells, st));
+    d.meta = c->meta.as<uint32_t>();  // upload_meta may have (re)allocated it
     PP_TRY(c->up_lam.ensure((size_t)n * 8));
     PP_HIP(hipMemcpyAsync(c->up_lam.p, profit, (size_t)n * 8, hipMemcpyHostToDevice, st));
     PP_HIP(launch_gather(c->up_lam.as<int64_t>(), d.profit, 1, n,
@@ -919,7 +1015,8 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     e.st = st;
     e.slots_lds = slots_lds;
     e.resident = dp_resident_blocks(cells, slots_lds, c->device);
-    e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 26);
+    e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 22);
+    e.fmax = tot < kFmaxBound && env_int("PP_DP_NO_FMAX", 0) == 0;
     if (e.resident <= 0) return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident");
     ChainState z{};
     PP_HIP(hipMemcpyAsync(d.cs, &z, sizeof z, hipMemcpyHostToDevice, st));

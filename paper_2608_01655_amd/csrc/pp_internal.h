@@ -12,23 +12,25 @@ constexpr int kMaxChains = 64;
 // "no holder" marker of the top-1 holder state (workers are < 255).
 constexpr uint8_t kNoHolder = 255;
 
-// Per-step metadata of the DP sweep, one uint32 per step s (row i = n - s in
-// the paper's 1-based preorder positions).  With H = rows of the LDS stack
-// (the deepest nesting of pending skip targets), row H is a write sink and
-// row H+1 the all-zero row:
-//   bit 0       1: the skip operand D[next(i)][*] is the previous row
-//                  (next(i) = i + 1, b_i is a leaf); 0: it is the row
-//                  prefetched during step s-1.
-//   bits 8..15  LDS row that row i is saved to: its stack slot when some
-//               a < i-1 has next(a) = i, else the sink.
-//   bits 16..23 LDS row prefetched as the skip operand of step s+1: the
-//               stack slot of next(i-1), the zero row when next(i-1) = n+1,
-//               or the sink when b_{i-1} is a leaf (unused read).
-constexpr uint32_t kMetaLeaf = 1u;
+// Per-step metadata of the DP sweep: two uint32 per padded step (see
+// kDpBatch), encoded for a given cells-per-lane width C.  LDS stack rows
+// hold 64*C int64 (512*C bytes): rows [0, H) are the stack of pending skip
+// targets, row H is the all-zero row and row H+1 a write sink.
+//   word 0: byte offset of the row that row i is stored to: its stack slot
+//           if it is a later skip target (next(a) = i for some a < i-1),
+//           else the sink row.
+//   word 1: byte offset of the row prefetched as the skip operand of the
+//           next step (row i-1): the stack slot of next(i-1), or the zero
+//           row when next(i-1) = n+1; plus kLeafByte when b_{i-1} is a leaf,
+//           whose skip operand D[next(i-1)][*] = D[i][*] is the row in
+//           registers -- the prefetched row is then unused, so the shifted
+//           (still in-bounds) address is harmless.  Offsets are multiples of
+//           512, so kLeafByte never collides.  Padded step 0 is a leaf.
+constexpr uint32_t kLeafByte = 256u;
 constexpr int kMaxSlots = 254;
 // The sweep runs steps in batches of kDpBatch; the step count is padded up
-// to a multiple of it with leading dummy steps (leaf, profit 0, sink rows),
-// so step s of the tree is padded step s + pad, pad = nsteps - n.
+// to a multiple of it with leading dummy steps (leaf, profit 0), so step s
+// of the tree is padded step s + pad, pad = nsteps - n.
 constexpr int kDpBatch = 32;
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
@@ -96,7 +98,7 @@ hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
 hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st);
 hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      uint32_t spin_limit, int store_bits, int32_t slots_lds,
-                     hipStream_t st);
+                     int fmax, hipStream_t st);
 hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
                             hipStream_t st);
 hipError_t launch_commit(const ChainSet& set, const DevState& d, hipStream_t st);

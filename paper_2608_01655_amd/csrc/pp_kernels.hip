@@ -17,6 +17,8 @@
 //
 // Integers only (int64 values, int32 indices); no floating point anywhere.
 
+#include <utility>
+
 #include "pp_internal.h"
 
 namespace pp {
@@ -260,6 +262,18 @@ __device__ __forceinline__ uint64_t writelane_u64(uint64_t old, uint64_t val,
   return ((uint64_t)hi << 32) | lo;
 }
 
+// Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
+// such bit patterns are finite non-negative doubles (denormals included,
+// which the kernel's FP64 mode preserves), and IEEE 754 orders them exactly
+// as the integers they encode, so the result is the larger integer.
+__device__ __forceinline__ int64_t max_nonneg_f64(int64_t a, int64_t b) {
+  double r;
+  asm("v_max_f64 %0, %1, %2"
+      : "=v"(r)
+      : "v"(__builtin_bit_cast(double, a)), "v"(__builtin_bit_cast(double, b)));
+  return __builtin_bit_cast(int64_t, r);
+}
+
 // Eq. 9, rows i = n..1, cells j = 1..k':
 //   D[i][j] = max(D[next(i)][j], p(b_i) + D[i+1][j-1]),  D[n+1][*] = 0,
 //   D[*][0] = 0;  choice bit = (take > skip)  (ties keep the skip branch).
@@ -272,38 +286,55 @@ __device__ __forceinline__ uint64_t writelane_u64(uint64_t old, uint64_t val,
 // Ring words carry a launch tag in their high half (relaxed agent-scope
 // atomics, no fences): a consumer validates each word by its tag.
 //
-// Rows that a later row skips to (next(a) for some a < i-1) are kept in an
-// LDS stack: pending targets nest like the subtrees that end at them, so at
-// most "tree depth" rows are live and every skip operand is on chip.  The
-// step body is branch-free: every step stores its row (to a sink row when
-// it is not a target) and prefetches the next step's skip operand (from the
-// zero row when next(i-1) = n+1); a leaf's skip operand is row i+1 itself.
+// Rows that a later row skips to (next(a) for some a < i-1) are written to
+// an LDS stack slot at their own step (other rows to a sink row, so the
+// store needs no branch): pending targets nest like the subtrees that end
+// at them, so at most "tree depth" are pending and every skip operand is on
+// chip.  A step reads the next step's skip operand (a
+// stack slot, or the all-zero row when next(i-1) = n+1) at its top, a full
+// step before use: that row was produced at least two steps earlier and no
+// push reuses its slot while it is pending.  A leaf's skip operand is the
+// row in registers.  Each step also writes its last cell column to a small
+// history, from which the ring output is gathered every kProd steps.
 //
-// Steps run in batches of kBatch, fully unrolled.  The step count is padded
-// up to a multiple of kBatch with leading dummy steps (profit 0, leaf, rows
-// stay all-zero, so they change nothing).  Per batch each lane stages one
-// step's {profit, boundary value} record in LDS, read back per step with one
-// broadcast 16-byte load; the ring input is prefetched one batch ahead and
+// Steps run in batches of kBatch, unrolled at compile time; the step count
+// is padded up to a multiple of kBatch with leading dummy steps (profit 0,
+// leaf, rows stay all-zero).  Per batch each lane stages one step's
+// {profit, boundary value} record in LDS, read back per step with one
+// broadcast load; the ring input is prefetched one batch ahead and
 // validated at the batch boundary; the choice bits (one ballot per cell
 // column per step, gathered with v_writelane) and the ring output are
-// written back with one coalesced store each.  No per-row launch, barrier
-// or HBM row traffic.
+// written with one coalesced store each.  No per-row launch, barrier or
+// HBM row traffic.
 constexpr int kBatch = kDpBatch;
+constexpr int kProd = 16;  // steps per gather of the ring output
 
 struct __attribute__((aligned(16))) StepRec {
   int64_t p;    // profit of the step's node
   int64_t bnd;  // D[i+1][first cell - 1] from stage g-1 (0 for stage 0)
 };
 
-template <int C>
+template <int U>
+using IC = std::integral_constant<int, U>;
+
+template <class F, int... U>
+__device__ __forceinline__ void unroll_steps(F&& f, std::integer_sequence<int, U...>) {
+  (f(IC<U>{}), ...);
+}
+
+template <int C, bool FMAX>
 __global__ void __launch_bounds__(64)
 k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
      int store_bits, int32_t slots) {
   extern __shared__ int64_t lds[];
-  constexpr int kRow = C * kWave;  // int64 per LDS row
-  int64_t* stk = lds;              // [slots + 2][C][64]
-  StepRec* rec = (StepRec*)(lds + (slots + 2) * kRow);  // [kBatch]
+  constexpr int kRow = C * kWave;              // int64 per stack row
+  // step records first (small immediate offsets), then the stack rows, the
+  // zero row and the sink row, then the last-column history
+  StepRec* rec = (StepRec*)lds;                            // [kBatch]
+  int64_t* stk = lds + kBatch * 2;                         // [slots + 2][C][64]
+  int64_t* hist = stk + (slots + 2) * kRow;                // [kProd][64]
   const int lane = threadIdx.x;
+  char* lane_bytes = (char*)stk + lane * 8;
   const int blk = blockIdx.x;
   if (blk >= set.base[set.count]) return;
   int ci = 0;
@@ -317,13 +348,14 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const int pad = nsteps - n;  // leading dummy steps
   const int64_t stride = (int64_t)d.npad;  // steps per stage row of bits/ring
   const int64_t* __restrict__ prof = d.profit + slot * n;
-  const uint32_t* __restrict__ meta = d.meta;  // [nsteps], padded
+  const uint2* __restrict__ meta = (const uint2*)d.meta;  // [nsteps], padded
   uint64_t* bits = d.bits + (slot * d.stages + g) * (int64_t)C * stride;
   uint64_t* ring_out = d.ring + (slot * d.stages + g) * stride * 2;
   const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
   const uint64_t tag = (uint64_t)epoch << 32;
+  const bool produce = g + 1 < G;
 #pragma unroll
-  for (int c = 0; c < C; ++c) stk[(slots + 1) * kRow + c * kWave + lane] = 0;
+  for (int c = 0; c < C; ++c) stk[slots * kRow + c * kWave + lane] = 0;
 
   // ring input of the batch at s0: lane u < kBatch <- entry s0+u-1
   auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
@@ -366,14 +398,20 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     pre[c] = 0;
     acc[c] = 0;
   }
-  uint64_t bo = 0;  // ring output of the batch: lane u <- step s0+u
-  uint32_t mv = lane < kBatch ? meta[lane] : 0u;
+  // history column rotated by step, so gathering lane 63's cells reads 16
+  // different banks: step u's value of lane l sits at column (l + u) mod 64
+  int hw[kProd];
+#pragma unroll
+  for (int q = 0; q < kProd; ++q) hw[q] = q * kWave + ((lane + q) & (kWave - 1));
+  const int hr = (lane % kProd) * kWave + ((kWave - 1 + lane % kProd) & (kWave - 1));
+  uint2 mv = lane < kBatch ? meta[lane] : make_uint2(0u, 0u);
   int64_t pv = profit_at(lane);
   uint64_t rw0, rw1;
   ring_load(0, rw0, rw1);
   ring_wait(0, rw0, rw1);
   int64_t bv = (int64_t)((rw1 << 32) | (rw0 & 0xFFFFFFFFull));
 
+  uint32_t pf_prev = kLeafByte;  // padded step 0 is a dummy step or row n: leaves
   for (int s0 = 0; s0 < nsteps && !failed; s0 += kBatch) {
     const int s1 = s0 + kBatch;
     if (lane < kBatch) {
@@ -383,59 +421,73 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       rec[lane] = r;
     }
     // next batch: metadata, profits and ring input, consumed after the loop
-    const uint32_t mv_n = (lane < kBatch && s1 < nsteps) ? meta[s1 + lane] : 0u;
+    const uint2 mv_n = (lane < kBatch && s1 < nsteps) ? meta[s1 + lane] : make_uint2(0u, 0u);
     const int64_t pv_n = profit_at(s1 + lane);
     uint64_t nw0 = tag, nw1 = tag;
     if (s1 < nsteps) ring_load(s1, nw0, nw1);
 
-    // Software pipeline: the records of steps u+1 and u+2 and the meta
-    // word of step u+1 are in flight while step u computes, and the skip
-    // operand of step u+1 is read at the top of step u.  That read may
-    // precede step u's own store: a non-leaf step's skip row was produced
-    // at least two steps earlier and sits in a slot no later push reuses
-    // while it is pending, and a leaf's skip operand is the row in
-    // registers.
     StepRec rq[3];
     rq[0] = rec[0];
     rq[1] = rec[1];
-    uint32_t ms_next = readlane_u32(mv, 0);
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      if (u + 2 < kBatch) rq[(u + 2) % 3] = rec[u + 2];
-      const uint32_t ms = ms_next;
-      if (u + 1 < kBatch) ms_next = readlane_u32(mv, u + 1);
-      const int pb = (int)((ms >> 16) & 0xFFu) * kRow;
+    uint32_t st_next = readlane_u32(mv.x, 0), pf_next = readlane_u32(mv.y, 0);
+    // pf_prev: word 1 of the previous step, whose kLeafByte flags this step
+    int64_t gath[kBatch / kProd];  // lane 63's last cells, gathered per kProd
+    auto step = [&](auto uc) {
+      constexpr int u = decltype(uc)::value;
+      if constexpr (u + 2 < kBatch) rq[(u + 2) % 3] = rec[u + 2];
+      const uint32_t st_off = st_next, pf = pf_next;
+      if constexpr (u + 1 < kBatch) {
+        st_next = readlane_u32(mv.x, u + 1);
+        pf_next = readlane_u32(mv.y, u + 1);
+      }
+      // skip operand of step u+1: a stack slot or the zero row (byte offset
+      // in pf, plus kLeafByte when step u+1 is a leaf -- its read is then
+      // unused, so the shifted address does no harm)
+      const int64_t* prow = (const int64_t*)(lane_bytes + pf);
       int64_t pnext[C];
 #pragma unroll
-      for (int c = 0; c < C; ++c) pnext[c] = stk[pb + c * kWave + lane];
+      for (int c = 0; c < C; ++c) pnext[c] = prow[c * kWave];
       const StepRec cur = rq[u % 3];
       const int64_t left = shift_up(x[C - 1], cur.bnd);
-      const bool leaf = (ms & kMetaLeaf) != 0;
+      const bool leaf = (pf_prev & kLeafByte) != 0;
+      pf_prev = pf;
       int64_t y[C];
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         const int64_t sk = leaf ? x[c] : pre[c];
         const int64_t t = cur.p + (c == 0 ? left : x[c - 1]);
         const bool tk = t > sk;
-        y[c] = tk ? t : sk;
+        if constexpr (FMAX)
+          y[c] = max_nonneg_f64(sk, t);
+        else
+          y[c] = tk ? t : sk;
         acc[c] = writelane_u64(acc[c], __builtin_amdgcn_ballot_w64(tk), u);
       }
-      const int sb = (int)((ms >> 8) & 0xFFu) * kRow;
+      // the row goes to its stack slot if it is a later skip target, else
+      // to the sink row
+      int64_t* srow = (int64_t*)(lane_bytes + st_off);
 #pragma unroll
-      for (int c = 0; c < C; ++c) stk[sb + c * kWave + lane] = y[c];
-      bo = writelane_u64(bo, (uint64_t)readlane_i64(y[C - 1], kWave - 1), u);
+      for (int c = 0; c < C; ++c) srow[c * kWave] = y[c];
+      hist[hw[u % kProd]] = y[C - 1];
+      if constexpr (u % kProd == kProd - 1) gath[u / kProd] = hist[hr];
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         pre[c] = pnext[c];
         x[c] = y[c];
       }
-    }
+    };
+    unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
     const int idx = s0 + lane;
     if (store_bits && lane < kBatch) {
 #pragma unroll
       for (int c = 0; c < C; ++c) bits[(int64_t)c * stride + idx] = acc[c];
     }
-    if (g + 1 < G && lane < kBatch) {
+    if (produce && lane < kBatch) {
+      int64_t v = gath[0];
+#pragma unroll
+      for (int q = 1; q < kBatch / kProd; ++q)
+        if (lane >= q * kProd) v = gath[q];
+      const uint64_t bo = (uint64_t)v;
       st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
       st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
     }
@@ -657,30 +709,35 @@ hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) 
 }
 
 size_t dp_lds_bytes(int cells, int32_t slots_lds) {
-  // stack rows plus the sink row and the zero row, then the step records
-  return (size_t)(slots_lds + 2) * cells * kWave * sizeof(int64_t) +
-         kBatch * sizeof(StepRec);
+  // step records, stack rows, the zero row and the sink row, the
+  // last-column history
+  return kBatch * sizeof(StepRec) +
+         (size_t)(slots_lds + 2) * cells * kWave * sizeof(int64_t) +
+         (size_t)kProd * kWave * sizeof(int64_t);
 }
 
-template <int C>
+template <int C, bool FMAX>
 static hipError_t dp_launch_c(const ChainSet& set, const DevState& d,
                               uint32_t epoch, uint32_t spin_limit,
                               int store_bits, int32_t slots_lds,
                               hipStream_t st) {
   const size_t lds = dp_lds_bytes(C, slots_lds);
-  hipLaunchKernelGGL(k_dp<C>, dim3((unsigned)set.base[set.count]), dim3(kWave),
-                     lds, st, set, d, epoch, spin_limit, store_bits, slots_lds);
+  hipLaunchKernelGGL((k_dp<C, FMAX>), dim3((unsigned)set.base[set.count]),
+                     dim3(kWave), lds, st, set, d, epoch, spin_limit,
+                     store_bits, slots_lds);
   return hipGetLastError();
 }
 
 hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      uint32_t spin_limit, int store_bits, int32_t slots_lds,
-                     hipStream_t st) {
-  switch (d.cells) {
-    case 1: return dp_launch_c<1>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
-    case 2: return dp_launch_c<2>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
-    case 4: return dp_launch_c<4>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
-    case 8: return dp_launch_c<8>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+                     int fmax, hipStream_t st) {
+  switch (d.cells * 2 + (fmax ? 1 : 0)) {
+    case 2: return dp_launch_c<1, false>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 3: return dp_launch_c<1, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 4: return dp_launch_c<2, false>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 5: return dp_launch_c<2, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 8: return dp_launch_c<4, false>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+    case 9: return dp_launch_c<4, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -690,10 +747,9 @@ int dp_resident_blocks(int cells, int32_t slots_lds, int device) {
   const size_t lds = dp_lds_bytes(cells, slots_lds);
   hipError_t e = hipErrorInvalidValue;
   switch (cells) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1>, kWave, lds); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2>, kWave, lds); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4>, kWave, lds); break;
-    case 8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<8>, kWave, lds); break;
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1, false>, kWave, lds); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2, false>, kWave, lds); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4, false>, kWave, lds); break;
     default: return 0;
   }
   if (e != hipSuccess) return 0;
@@ -708,7 +764,6 @@ hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
     case 1: hipLaunchKernelGGL(k_backtrack<1>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
     case 2: hipLaunchKernelGGL(k_backtrack<2>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
     case 4: hipLaunchKernelGGL(k_backtrack<4>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
-    case 8: hipLaunchKernelGGL(k_backtrack<8>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

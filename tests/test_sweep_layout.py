@@ -1,0 +1,124 @@
+"""CPU check of the DP sweep's step schedule (no GPU).
+
+The library exports, per tree, the metadata its gfx950 sweep follows: which
+steps are leaves, which rows are kept in which LDS stack slot, and which row
+each step's skip operand is read from.  This test replays that schedule on
+whole DP rows with numpy -- target rows written to their slots at their own
+step, the next step's skip row read before the current step writes -- and
+requires the replay to reproduce the oracle's rooted-tree optimum and
+selection (Eq. 9, Theorem 1, tie rule R1).  A wrong slot, a slot reused
+while pending, or a read issued too early would give a different value or
+set.
+"""
+
+import numpy as np
+import pytest
+
+from paper_2608_01655_amd import binding as B
+from paper_2608_01655_amd import workloads as W
+from tests import bruteforce as bf
+
+BATCH = 32
+
+
+def replay(parent, profit, k, cells):
+    meta, slots = B.pp_sweep_layout(parent, cells)
+    n = len(parent)
+    kk = min(k, n)
+    order = bf.canonical_preorder(parent)
+    nsteps = meta.shape[0]
+    assert nsteps % BATCH == 0 and nsteps - n < BATCH
+    pad = nsteps - n
+    row = 64 * cells * 8  # bytes per LDS row
+    rows = np.zeros((slots + 2, kk + 1), dtype=object)  # stack, zero, sink
+    x = np.zeros(kk + 1, dtype=object)
+    pre = np.zeros(kk + 1, dtype=object)
+    bits = np.zeros((nsteps, kk + 1), dtype=bool)
+    leaf_next = True                             # padded step 0 is a leaf
+    for s in range(nsteps):
+        st, pf = int(meta[s][0]), int(meta[s][1])
+        leaf = leaf_next
+        leaf_next = bool(pf & 256)               # flags step s+1
+        if not leaf_next:                        # the row is used: exact
+            assert pf % row == 0
+        pf_used = pf & ~256
+        assert pf_used % row == 0 and pf_used // row <= slots
+        assert st % row == 0 and st // row <= slots + 1 and st // row != slots
+        pnext = rows[pf_used // row].copy()      # read before this step writes
+        sk = x if leaf else pre
+        p = int(profit[order[n - 1 - (s - pad)]]) if s >= pad else 0
+        t = np.empty(kk + 1, dtype=object)
+        t[0] = -1
+        t[1:] = x[:-1] + p
+        take = t > sk
+        take[0] = False
+        y = np.where(take, t, sk)
+        y[0] = 0
+        bits[s] = take
+        rows[st // row] = y                      # its slot, or the sink
+        assert all(v == 0 for v in rows[slots])  # the zero row stays zero
+        pre, x = pnext, y
+    # backtrack over the recorded choice bits, in preorder positions
+    nextpos = np.empty(n, np.int64)
+    pos_of = {v: i for i, v in enumerate(order)}
+    size = np.ones(n, np.int64)
+    for v in reversed(order):
+        if parent[v] >= 0:
+            size[pos_of[parent[v]]] += size[pos_of[v]]
+    nextpos[:] = np.arange(n) + size
+    sel = np.zeros(n, np.uint8)
+    q, j = 0, kk
+    while q < n and j > 0:
+        if bits[n - 1 - q + pad][j]:
+            sel[order[q]] = 1
+            q, j = q + 1, j - 1
+        else:
+            q = int(nextpos[q])
+    return int(x[kk]) if kk > 0 else 0, sel
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import os
+
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2608_01655_amd import build
+
+        build.build()
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_replayed_schedule_matches_oracle(oracle_mod, seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 260))
+    parent = W.random_forest(n, rng, p_root=float(rng.choice([0.0, 0.1, 0.4])))
+    profit = rng.integers(0, int(rng.choice([3, 50, 10 ** 6])), size=n)
+    k = int(rng.integers(0, n + 3))
+    cells = int(rng.choice([1, 2, 4]))
+    val, sel = replay(parent, profit, k, cells)
+    osel, oval = oracle_mod.rooted_dp(parent, profit, k)
+    assert val == oval
+    np.testing.assert_array_equal(sel, osel)
+
+
+def test_replayed_schedule_deep_and_wide(oracle_mod):
+    rng = np.random.default_rng(9)
+    comb = np.array([-1] + list(range(0, 199)) + list(range(0, 200)), np.int32)
+    path = np.arange(-1, 299, dtype=np.int32)
+    star = np.array([-1] + [0] * 299, np.int32)
+    for parent in (comb, path, star):
+        profit = rng.integers(0, 20, size=parent.shape[0])
+        for k in (1, 70, parent.shape[0]):
+            val, sel = replay(parent, profit, k, 2)
+            osel, oval = oracle_mod.rooted_dp(parent, profit, k)
+            assert val == oval
+            np.testing.assert_array_equal(sel, osel)
+
+
+def test_layout_of_benchmark_trees():
+    """Stack depth of the benchmark trees stays small (LDS-resident)."""
+    for name, limit in (("tree50k", 16), ("chat50k", 20), ("rag10k", 10)):
+        inst = W.make_workload(name)
+        meta, slots = B.pp_sweep_layout(inst.parent, 2)
+        assert slots <= limit
+        assert meta.shape[0] == (inst.n + 31) // 32 * 32
