@@ -12,8 +12,10 @@ inputs already in HBM.  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,9 +34,61 @@ METRIC = ("full PrefixPlace plans/sec and tree-DP cells/sec "
 # baseline.
 PAPER_CONTEXT = "n=50,000, M=16, k=128: 12.29 s per plan on one EPYC 9V74"
 
+# HBM traffic of the DP sweep as measured by hardware counters (FETCH_SIZE
+# and WRITE_SIZE per dispatch, each scaled by what the same counter reads for
+# a device copy of known size).  The summary records a digest of the sources
+# that decide the kernel and its launch; a different digest means the
+# counters describe another kernel and the figure is not reported.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_dp_hbm_traffic.md")
+KERNEL_SOURCES = ("paper_2608_01655_amd/csrc/pp_kernels.hip",
+                  "paper_2608_01655_amd/csrc/pp_internal.h",
+                  "paper_2608_01655_amd/csrc/pp_host.cpp")
+
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_sources_digest():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per DP-sweep launch from the committed counter summary, or
+    None if there is none for this workload and these kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    for m in re.finditer(r"<!-- traffic (\{.*?\}) -->", text):
+        rec = json.loads(m.group(1))
+        if rec.get("workload") == workload and \
+                rec.get("sources_sha256") == kernel_sources_digest():
+            return float(rec["bytes_per_launch"])
+    return None
+
+
+def copy_probe(mib):
+    """A device-to-device copy of known size, for calibrating the HBM byte
+    counters (run under rocprofv3 --pmc)."""
+    import torch
+
+    n = mib * 2 ** 20 // 8
+    a = torch.arange(n, dtype=torch.int64, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    ok = bool(torch.equal(a, b))
+    print(json.dumps({"copy_bytes": n * 8, "copies": 3, "equal": ok}),
+          flush=True)
+    return 0 if ok else 1
 
 
 def cpu_baseline(inst, cells_per_plan, threads):
@@ -69,7 +123,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="tree50k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device (counter "
+                         "calibration) and exit")
     args = ap.parse_args()
+    if args.copy_probe:
+        sys.exit(copy_probe(args.copy_probe))
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: the planner's starts would "
               "shard across GPUs with one exchange of (objective, start) "
@@ -161,7 +220,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": measured_traffic(inst.name),
             "bytes_per_cell": BYTES_PER_CELL,
             "dp_launches_per_plan": launches // args.steps,
             "avg_launch_ms": avg_launch_s * 1e3,
