@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 1
+#define PP_ABI_VERSION 2
 
 enum {
     PP_OK = 0,
@@ -176,15 +176,17 @@ int pp_plan_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
 /* Host only, for inspection and CPU-side checks of the DP sweep's step
  * schedule: for the tree `parent` and `cells` (1, 2 or 4) DP cells per
  * lane, writes the per-step metadata of the sweep (`meta`, may be NULL to
- * query the size; 2 * nsteps words, nsteps = n padded up to a multiple of 32
- * with leading dummy steps) and the number of LDS stack rows H.  Rows hold
- * 64*cells int64 in the order [H stack rows | zero row | sink row].  Per
- * step: word 0 = byte offset of the row the step's DP row is written to
- * (its stack slot when a later row skips to it, else the sink); word 1 =
- * byte offset of the row read as the next step's skip operand (Eq. 9's
- * D[next(i)][*]), plus 256 when the next step's node is a leaf (its skip
- * operand is then the previous row and the read is unused).  The first
- * step's node is always a leaf. */
+ * query the size; 4 * nsteps words, nsteps = n padded up to a multiple of 32
+ * with leading dummy steps; step s handles preorder row n - (s - pad), pad =
+ * nsteps - n) and the number of LDS stack rows H.  Rows hold 64*cells int64
+ * in the order [H stack rows | zero row | sink row].  Per step: word 0 =
+ * byte offset of the row the step's DP row is written to (its stack slot
+ * when a later row skips to it, else the sink); word 1 = byte offset of the
+ * row read as the next step's skip operand (Eq. 9's D[next(i)][*]: a stack
+ * slot, or the zero row when that next() is past the end or the next node is
+ * a leaf); words 2 and 3 = 0xFFFFFFFF when the step's own node is a leaf
+ * (its skip operand is then the previous row), else 0.  The first step's
+ * node is always a leaf. */
 int pp_sweep_layout(int32_t n, const int32_t *parent, int32_t cells,
                     uint32_t *meta, int32_t *nsteps, int32_t *slots);
 

@@ -230,7 +230,7 @@ def pp_sweep_layout(parent, cells):
     ns, sl = ctypes.c_int32(0), ctypes.c_int32(0)
     _check(lib().pp_sweep_layout(n, _p(parent), int(cells), None,
                                  ctypes.byref(ns), ctypes.byref(sl)))
-    meta = np.zeros((ns.value, 2), np.uint32)
+    meta = np.zeros((ns.value, 4), np.uint32)
     _check(lib().pp_sweep_layout(n, _p(parent), int(cells), _p(meta),
                                  ctypes.byref(ns), ctypes.byref(sl)))
     return meta, sl.value

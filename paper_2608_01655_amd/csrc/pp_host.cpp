@@ -174,19 +174,22 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
 }
 
 // DP-sweep metadata for `cells` cells per lane (layout in pp_internal.h):
-// two words per padded step.
+// kMetaWords words per padded step.
 std::vector<uint32_t> encode_meta(const TreeLayout& t, int cells) {
   const int64_t row = (int64_t)cells * 64 * 8;  // bytes per LDS stack row
   const int64_t zero = (int64_t)t.slots * row, sink = zero + row;
   const int32_t nsteps = (int32_t)t.leaf.size();
-  std::vector<uint32_t> meta(2 * (size_t)nsteps);
+  std::vector<uint32_t> meta(kMetaWords * (size_t)nsteps);
   for (int32_t s = 0; s < nsteps; ++s) {
     const int32_t r = t.src[s];
     const int64_t st = t.store[s] >= 0 ? (int64_t)t.store[s] * row : sink;
     const int64_t pf = r >= 0 ? (int64_t)t.store[r] * row : zero;
-    const bool next_leaf = s + 1 < nsteps && t.leaf[s + 1];
-    meta[2 * (size_t)s] = (uint32_t)st;
-    meta[2 * (size_t)s + 1] = (uint32_t)pf | (next_leaf ? kLeafByte : 0u);
+    const uint32_t leaf = t.leaf[s] ? 0xFFFFFFFFu : 0u;
+    uint32_t* w = meta.data() + kMetaWords * (size_t)s;
+    w[0] = (uint32_t)st;
+    w[1] = (uint32_t)pf;
+    w[2] = leaf;
+    w[3] = leaf;
   }
   return meta;
 }
@@ -297,7 +300,7 @@ int ensure_slots(pp_ctx* c, DevState& d, int32_t slots, int32_t kmax,
   PP_TRY(c->v2.ensure(slots * m * n * 8));
   PP_TRY(c->h1.ensure(slots * m * n));
   PP_TRY(c->profit.ensure(slots * n * 8));
-  PP_TRY(c->sel.ensure(slots * npad));
+  PP_TRY(c->sel.ensure(slots * (npad / 8)));
   PP_TRY(c->bits.ensure((size_t)slots * stages * cells * npad * 8));
   // ring words carry a launch tag; fresh memory is zeroed so that no stale
   // word can ever carry a live tag (tags start at 1)
@@ -308,7 +311,7 @@ int ensure_slots(pp_ctx* c, DevState& d, int32_t slots, int32_t kmax,
   d.v2 = c->v2.as<int64_t>();
   d.h1 = c->h1.as<uint8_t>();
   d.profit = c->profit.as<int64_t>();
-  d.sel = c->sel.as<uint8_t>();
+  d.sel = c->sel.as<uint32_t>();
   d.bits = c->bits.as<uint64_t>();
   d.ring = c->ring.as<uint64_t>();
   d.cs = c->cs.as<ChainState>();
@@ -735,10 +738,16 @@ int check_meta(const TreeLayout& t, const std::vector<uint32_t>& meta,
   if (t.leaf.empty() || !t.leaf[0])
     return fail(PP_E_DEVICE, "internal: the first DP step must be a leaf");
   const int64_t row = (int64_t)cells * 64 * 8;  // bytes
-  for (size_t q = 0; q < meta.size(); q += 2) {
-    const int64_t st = meta[q], pf = meta[q + 1] & ~kLeafByte;
-    if (st % row != 0 || st / row > t.slots + 1 || pf % row != 0 ||
-        pf / row > t.slots)
+  if (meta.size() != kMetaWords * t.leaf.size() || meta[2] != 0xFFFFFFFFu)
+    return fail(PP_E_DEVICE, "internal: DP step metadata malformed");
+  for (size_t q = 0; q < meta.size(); q += kMetaWords) {
+    const int64_t st = meta[q], pf = meta[q + 1];
+    // stores go to a stack slot or the sink, never to the zero row; reads
+    // come from a stack slot or the zero row
+    if (st % row != 0 || st / row > t.slots + 1 || st / row == t.slots ||
+        pf % row != 0 || pf / row > t.slots ||
+        (meta[q + 2] != 0u && meta[q + 2] != 0xFFFFFFFFu) ||
+        meta[q + 3] != meta[q + 2])
       return fail(PP_E_DEVICE, "internal: DP step metadata out of range");
   }
   return PP_OK;
@@ -837,7 +846,7 @@ int pp_sweep_layout(int32_t n, const int32_t* parent, int32_t cells,
     const std::vector<uint32_t> mv = encode_meta(t, cells);
     PP_TRY(check_meta(t, mv, cells));
     if (meta) std::copy(mv.begin(), mv.end(), meta);
-    *nsteps = (int32_t)(mv.size() / 2);
+    *nsteps = (int32_t)(mv.size() / kMetaWords);
     *slots = t.slots;
     return PP_OK;
   });
@@ -1022,13 +1031,13 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     PP_HIP(hipMemcpyAsync(d.cs, &z, sizeof z, hipMemcpyHostToDevice, st));
     PP_TRY(e.dp(set, 1));
     PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
-    std::vector<uint8_t> pre(n);
+    std::vector<uint32_t> pre(d.npad / 32);
     ChainState out{};
-    PP_HIP(hipMemcpyAsync(pre.data(), d.sel, n, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipMemcpyAsync(pre.data(), d.sel, pre.size() * 4, hipMemcpyDeviceToHost, st));
     PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
     PP_HIP(hipStreamSynchronize(st));
     if (out.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
-    for (int32_t q = 0; q < n; ++q) selected[t.order[q]] = pre[q];
+    for (int32_t q = 0; q < n; ++q) selected[t.order[q]] = (pre[q / 32] >> (q % 32)) & 1u;
     *value = out.dpval;
     return PP_OK;
   });

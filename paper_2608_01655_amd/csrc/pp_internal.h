@@ -12,7 +12,7 @@ constexpr int kMaxChains = 64;
 // "no holder" marker of the top-1 holder state (workers are < 255).
 constexpr uint8_t kNoHolder = 255;
 
-// Per-step metadata of the DP sweep: two uint32 per padded step (see
+// Per-step metadata of the DP sweep: four uint32 per padded step (see
 // kDpBatch), encoded for a given cells-per-lane width C.  LDS stack rows
 // hold 64*C int64 (512*C bytes): rows [0, H) are the stack of pending skip
 // targets, row H is the all-zero row and row H+1 a write sink.
@@ -21,12 +21,12 @@ constexpr uint8_t kNoHolder = 255;
 //           else the sink row.
 //   word 1: byte offset of the row prefetched as the skip operand of the
 //           next step (row i-1): the stack slot of next(i-1), or the zero
-//           row when next(i-1) = n+1; plus kLeafByte when b_{i-1} is a leaf,
-//           whose skip operand D[next(i-1)][*] = D[i][*] is the row in
-//           registers -- the prefetched row is then unused, so the shifted
-//           (still in-bounds) address is harmless.  Offsets are multiples of
-//           512, so kLeafByte never collides.  Padded step 0 is a leaf.
-constexpr uint32_t kLeafByte = 256u;
+//           row when next(i-1) = n+1 or b_{i-1} is a leaf (whose skip
+//           operand D[next(i-1)][*] = D[i][*] is the row in registers).
+//   words 2, 3: the lane mask selecting the row in registers as the skip
+//           operand: all ones when b_i is a leaf, else zero.  Padded step 0
+//           is a leaf.
+constexpr int kMetaWords = 4;
 constexpr int kMaxSlots = 254;
 // The sweep runs steps in batches of kDpBatch; the step count is padded up
 // to a multiple of it with leading dummy steps (leaf, profit 0), so step s
@@ -64,14 +64,18 @@ struct DevState {
   const int64_t* w;         // [m][n]     recompute cost, preorder
   const int64_t* f;         // [m][m][n]  fetch cost [src][dst][pos]
   const int32_t* nextpos;   // [n]        0-based first position after subtree
-  const uint32_t* meta;     // [n]        per-step DP metadata
+  const uint32_t* meta;     // [nsteps][4] per-step DP metadata
   uint8_t* tgt;             // [slots][m][n] placement, preorder
   int64_t* v1;              // [slots][m][n] best holder saving
   int64_t* v2;              // [slots][m][n] best saving among other holders
   uint8_t* h1;              // [slots][m][n] holder giving v1
   int64_t* profit;          // [slots][n]    marginal profits p_h, preorder
-  uint8_t* sel;             // [slots][npad] backtracked selection, preorder
-  uint64_t* bits;           // [slots][stages][cells][npad] DP choice bits
+  uint32_t* sel;            // [slots][npad/32] backtracked selection bitmap:
+                            //   position q is bit q%32 of word q/32
+  uint64_t* bits;           // [slots][stages][cells][npad] DP choice bits:
+                            //   as uint32 words [2*npad] per (stage, cell),
+                            //   word 64*b + l = lane l's cell over sweep
+                            //   batch b, bit 31-u = step 32*b + u
   uint64_t* ring;           // [slots][stages][n][2] stage boundary values
   ChainState* cs;           // [slots]
   int32_t stages;           // stage stride of bits / ring

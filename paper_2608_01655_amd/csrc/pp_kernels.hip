@@ -72,13 +72,9 @@ __device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
-__device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
-  const uint32_t lo = readlane_u32((uint32_t)(uint64_t)v, lane);
-  const uint32_t hi = readlane_u32((uint32_t)((uint64_t)v >> 32), lane);
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
 typedef int pp_int2 __attribute__((ext_vector_type(2)));
+typedef int64_t pp_i64x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t pp_u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ pp_int2 split64(int64_t v) {
   return __builtin_bit_cast(pp_int2, v);
@@ -248,18 +244,27 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
 
 // ------------------------------------------------------------ DP sweep --
 
-// v_writelane_b32 (not exposed as a clang builtin): lane `lane` of the
-// result is `val`, every other lane keeps `old`.
-extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
-    "llvm.amdgcn.writelane.i32");
+// Bitwise select: bits of `a` where `mask` is set, else bits of `b` (one
+// v_bfi_b32 per half; the sweep's masks are all ones or all zeros).
+__device__ __forceinline__ int64_t select_bits(uint32_t mask, int64_t a,
+                                               int64_t b) {
+  const pp_int2 av = split64(a), bv = split64(b);
+  pp_int2 r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r.x) : "v"(mask), "v"(av.x), "v"(bv.x));
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r.y) : "v"(mask), "v"(av.y), "v"(bv.y));
+  return join64(r);
+}
 
-__device__ __forceinline__ uint64_t writelane_u64(uint64_t old, uint64_t val,
-                                                  int lane) {
-  const uint32_t lo = (uint32_t)pp_writelane_i32((int)(uint32_t)val, lane,
-                                                 (int)(uint32_t)old);
-  const uint32_t hi = (uint32_t)pp_writelane_i32((int)(uint32_t)(val >> 32),
-                                                 lane, (int)(uint32_t)(old >> 32));
-  return ((uint64_t)hi << 32) | lo;
+// acc * 2 + (t > sk): the lane's choice bit of this step shifted into its
+// 32-step word (the compare's lane mask is the add's carry-in).
+__device__ __forceinline__ uint32_t shift_in_gt(int64_t t, int64_t sk,
+                                                uint32_t acc) {
+  uint32_t r;
+  asm("v_cmp_gt_i64 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
+      : "=v"(r)
+      : "v"(t), "v"(sk), "v"(acc)
+      : "vcc");
+  return r;
 }
 
 // Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
@@ -290,28 +295,35 @@ __device__ __forceinline__ int64_t max_nonneg_f64(int64_t a, int64_t b) {
 // an LDS stack slot at their own step (other rows to a sink row, so the
 // store needs no branch): pending targets nest like the subtrees that end
 // at them, so at most "tree depth" are pending and every skip operand is on
-// chip.  A step reads the next step's skip operand (a
-// stack slot, or the all-zero row when next(i-1) = n+1) at its top, a full
-// step before use: that row was produced at least two steps earlier and no
-// push reuses its slot while it is pending.  A leaf's skip operand is the
-// row in registers.  Each step also writes its last cell column to a small
-// history, from which the ring output is gathered every kProd steps.
+// chip.  A step reads the next step's skip operand (a stack slot, or the
+// all-zero row) at its top, a full step before use: that row was produced
+// at least two steps earlier and no push reuses its slot while it is
+// pending.  A leaf's skip operand is the row in registers, chosen per step
+// by a uniform lane mask from the metadata.  Each step also writes its last
+// cell column to a small history, from which the ring output is gathered
+// every kProd steps.
 //
 // Steps run in batches of kBatch, unrolled at compile time; the step count
 // is padded up to a multiple of kBatch with leading dummy steps (profit 0,
-// leaf, rows stay all-zero).  Per batch each lane stages one step's
-// {profit, boundary value} record in LDS, read back per step with one
-// broadcast load; the ring input is prefetched one batch ahead and
-// validated at the batch boundary; the choice bits (one ballot per cell
-// column per step, gathered with v_writelane) and the ring output are
-// written with one coalesced store each.  No per-row launch, barrier or
-// HBM row traffic.
+// leaf, rows stay all-zero).  Per batch each lane stages one step's record
+// -- profit, boundary value and the step's metadata words -- in LDS, read
+// back per step with two broadcast loads; the metadata, profits and ring
+// input of the next batch are loaded one batch ahead (the ring input is
+// validated at the batch boundary).
+// Each lane shifts its cells' choice bits into one 32-bit word per cell per
+// batch (bit 31-u = step u), stored with one coalesced store per cell; the
+// ring output also leaves with one store per batch.  No per-row launch,
+// barrier or HBM row traffic.
 constexpr int kBatch = kDpBatch;
 constexpr int kProd = 16;  // steps per gather of the ring output
 
 struct __attribute__((aligned(16))) StepRec {
-  int64_t p;    // profit of the step's node
-  int64_t bnd;  // D[i+1][first cell - 1] from stage g-1 (0 for stage 0)
+  int64_t p;      // profit of the step's node
+  int64_t bnd;    // D[i+1][first cell - 1] from stage g-1 (0 for stage 0)
+  uint32_t st;    // byte offset of the row this step is stored to
+  uint32_t pf;    // byte offset of the next step's skip row
+  uint32_t leaf;  // all ones when the step's node is a leaf, else zero
+  uint32_t pad;
 };
 
 template <int U>
@@ -331,7 +343,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // step records first (small immediate offsets), then the stack rows, the
   // zero row and the sink row, then the last-column history
   StepRec* rec = (StepRec*)lds;                            // [kBatch]
-  int64_t* stk = lds + kBatch * 2;                         // [slots + 2][C][64]
+  int64_t* stk = lds + kBatch * (sizeof(StepRec) / 8);     // [slots + 2][C][64]
   int64_t* hist = stk + (slots + 2) * kRow;                // [kProd][64]
   const int lane = threadIdx.x;
   char* lane_bytes = (char*)stk + lane * 8;
@@ -346,10 +358,11 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const int n = d.n;
   const int nsteps = (n + kBatch - 1) / kBatch * kBatch;
   const int pad = nsteps - n;  // leading dummy steps
-  const int64_t stride = (int64_t)d.npad;  // steps per stage row of bits/ring
+  const int64_t stride = (int64_t)d.npad;  // steps per stage row of the ring
+  const int64_t cstride = 2 * stride;      // choice words per (stage, cell)
   const int64_t* __restrict__ prof = d.profit + slot * n;
-  const uint2* __restrict__ meta = (const uint2*)d.meta;  // [nsteps], padded
-  uint64_t* bits = d.bits + (slot * d.stages + g) * (int64_t)C * stride;
+  const uint4* __restrict__ meta = (const uint4*)d.meta;  // [nsteps], padded
+  uint32_t* bits = (uint32_t*)d.bits + (slot * d.stages + g) * (int64_t)C * cstride;
   uint64_t* ring_out = d.ring + (slot * d.stages + g) * stride * 2;
   const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
   const uint64_t tag = (uint64_t)epoch << 32;
@@ -391,7 +404,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   };
 
   int64_t x[C], pre[C];
-  uint64_t acc[C];
+  uint32_t acc[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     x[c] = 0;
@@ -404,68 +417,68 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
 #pragma unroll
   for (int q = 0; q < kProd; ++q) hw[q] = q * kWave + ((lane + q) & (kWave - 1));
   const int hr = (lane % kProd) * kWave + ((kWave - 1 + lane % kProd) & (kWave - 1));
-  uint2 mv = lane < kBatch ? meta[lane] : make_uint2(0u, 0u);
+  auto meta_at = [&](int t) -> uint4 {
+    return (lane < kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
+  };
   int64_t pv = profit_at(lane);
+  uint4 mv = meta_at(lane);
   uint64_t rw0, rw1;
   ring_load(0, rw0, rw1);
   ring_wait(0, rw0, rw1);
   int64_t bv = (int64_t)((rw1 << 32) | (rw0 & 0xFFFFFFFFull));
 
-  uint32_t pf_prev = kLeafByte;  // padded step 0 is a dummy step or row n: leaves
   for (int s0 = 0; s0 < nsteps && !failed; s0 += kBatch) {
     const int s1 = s0 + kBatch;
     if (lane < kBatch) {
       StepRec r;
       r.p = pv;
       r.bnd = bv;
+      r.st = mv.x;
+      r.pf = mv.y;
+      r.leaf = mv.z;
+      r.pad = 0;
       rec[lane] = r;
     }
     // next batch: metadata, profits and ring input, consumed after the loop
-    const uint2 mv_n = (lane < kBatch && s1 < nsteps) ? meta[s1 + lane] : make_uint2(0u, 0u);
     const int64_t pv_n = profit_at(s1 + lane);
+    const uint4 mv_n = meta_at(s1 + lane);
     uint64_t nw0 = tag, nw1 = tag;
     if (s1 < nsteps) ring_load(s1, nw0, nw1);
 
-    StepRec rq[3];
-    rq[0] = rec[0];
-    rq[1] = rec[1];
-    uint32_t st_next = readlane_u32(mv.x, 0), pf_next = readlane_u32(mv.y, 0);
-    // pf_prev: word 1 of the previous step, whose kLeafByte flags this step
+    // records of steps u, u+1, u+2 in flight: {p, bnd} and {st, pf, leaf}
+    pp_i64x2 rv[3];
+    pp_u32x4 rm[3];
+    auto rec_load = [&](int t, int q) {
+      rv[q] = *(const pp_i64x2*)&rec[t];
+      rm[q] = *(const pp_u32x4*)&rec[t].st;
+    };
+    rec_load(0, 0);
+    rec_load(1, 1);
     int64_t gath[kBatch / kProd];  // lane 63's last cells, gathered per kProd
     auto step = [&](auto uc) {
       constexpr int u = decltype(uc)::value;
-      if constexpr (u + 2 < kBatch) rq[(u + 2) % 3] = rec[u + 2];
-      const uint32_t st_off = st_next, pf = pf_next;
-      if constexpr (u + 1 < kBatch) {
-        st_next = readlane_u32(mv.x, u + 1);
-        pf_next = readlane_u32(mv.y, u + 1);
-      }
-      // skip operand of step u+1: a stack slot or the zero row (byte offset
-      // in pf, plus kLeafByte when step u+1 is a leaf -- its read is then
-      // unused, so the shifted address does no harm)
-      const int64_t* prow = (const int64_t*)(lane_bytes + pf);
+      if constexpr (u + 2 < kBatch) rec_load(u + 2, (u + 2) % 3);
+      const int64_t cur_p = rv[u % 3].x, cur_bnd = rv[u % 3].y;
+      const uint32_t cur_st = rm[u % 3].x, cur_pf = rm[u % 3].y, cur_leaf = rm[u % 3].z;
+      const int64_t* prow = (const int64_t*)(lane_bytes + cur_pf);
       int64_t pnext[C];
 #pragma unroll
       for (int c = 0; c < C; ++c) pnext[c] = prow[c * kWave];
-      const StepRec cur = rq[u % 3];
-      const int64_t left = shift_up(x[C - 1], cur.bnd);
-      const bool leaf = (pf_prev & kLeafByte) != 0;
-      pf_prev = pf;
+      const int64_t left = shift_up(x[C - 1], cur_bnd);
       int64_t y[C];
 #pragma unroll
       for (int c = 0; c < C; ++c) {
-        const int64_t sk = leaf ? x[c] : pre[c];
-        const int64_t t = cur.p + (c == 0 ? left : x[c - 1]);
-        const bool tk = t > sk;
+        const int64_t sk = select_bits(cur_leaf, x[c], pre[c]);
+        const int64_t t = cur_p + (c == 0 ? left : x[c - 1]);
+        acc[c] = shift_in_gt(t, sk, acc[c]);
         if constexpr (FMAX)
           y[c] = max_nonneg_f64(sk, t);
         else
-          y[c] = tk ? t : sk;
-        acc[c] = writelane_u64(acc[c], __builtin_amdgcn_ballot_w64(tk), u);
+          y[c] = t > sk ? t : sk;
       }
       // the row goes to its stack slot if it is a later skip target, else
       // to the sink row
-      int64_t* srow = (int64_t*)(lane_bytes + st_off);
+      int64_t* srow = (int64_t*)(lane_bytes + cur_st);
 #pragma unroll
       for (int c = 0; c < C; ++c) srow[c * kWave] = y[c];
       hist[hw[u % kProd]] = y[C - 1];
@@ -477,10 +490,10 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       }
     };
     unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
-    const int idx = s0 + lane;
-    if (store_bits && lane < kBatch) {
+    if (store_bits) {
+      const int64_t wi = (int64_t)(s0 / kBatch) * kWave + lane;
 #pragma unroll
-      for (int c = 0; c < C; ++c) bits[(int64_t)c * stride + idx] = acc[c];
+      for (int c = 0; c < C; ++c) bits[c * cstride + wi] = acc[c];
     }
     if (produce && lane < kBatch) {
       int64_t v = gath[0];
@@ -488,11 +501,12 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       for (int q = 1; q < kBatch / kProd; ++q)
         if (lane >= q * kProd) v = gath[q];
       const uint64_t bo = (uint64_t)v;
+      const int idx = s0 + lane;
       st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
       st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
     }
-    mv = mv_n;
     pv = pv_n;
+    mv = mv_n;
     if (s1 < nsteps) {
       ring_wait(s1, nw0, nw1);
       bv = (int64_t)((nw1 << 32) | (nw0 & 0xFFFFFFFFull));
@@ -520,15 +534,73 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
 
 // ----------------------------------------------------------- backtrack --
 
+// v_writelane_b32 (not exposed as a clang builtin): lane `lane` of the
+// result is `val`, every other lane keeps `old`.
+extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
+    "llvm.amdgcn.writelane.i32");
+
+// The walk inside one 32-row window for one cell per lane, in scalar code:
+// row q = wlo + r, column word W = lane `rem` of `wc` (bit r = choice of row
+// q), next(q) = lane r of `nx`.  A set bit takes b_q (q+1, rem-1) and marks
+// bit r of `tm`; a clear bit jumps to next(q).  Runs while q stays in
+// [wlo, wlo + lim) and rem >= 0.  The entry state must satisfy both; every
+// step raises q (next(q) > q), so the loop ends within lim steps.
+__device__ __forceinline__ void walk_window_c1(uint32_t& q, int& rem, uint32_t& tm,
+                                               uint32_t wlo, uint32_t lim,
+                                               uint32_t wc, uint32_t nx) {
+  uint32_t r, w, nq, bm, qp;
+  asm volatile(
+      "1:\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "v_readlane_b32 %[w], %[wc], %[rem]\n\t"
+      "v_readlane_b32 %[nq], %[nx], %[r]\n\t"
+      "s_lshl_b32 %[bm], 1, %[r]\n\t"
+      "s_add_u32 %[qp], %[q], 1\n\t"
+      "s_and_b32 %[w], %[w], %[bm]\n\t"      // SCC = take
+      "s_cselect_b32 %[q], %[qp], %[nq]\n\t"
+      "s_cselect_b32 %[bm], %[bm], 0\n\t"
+      "s_subb_u32 %[rem], %[rem], 0\n\t"     // rem -= take
+      "s_or_b32 %[tm], %[tm], %[bm]\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "s_cmp_lt_u32 %[r], %[lim]\n\t"
+      "s_cselect_b32 %[r], %[rem], -1\n\t"
+      "s_cmp_ge_i32 %[r], 0\n\t"
+      "s_cbranch_scc1 1b"
+      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [r] "=&s"(r), [w] "=&s"(w),
+        [nq] "=&s"(nq), [bm] "=&s"(bm), [qp] "=&s"(qp)
+      : [wlo] "s"(wlo), [lim] "s"(lim), [wc] "v"(wc), [nx] "v"(nx)
+      : "scc");
+}
+
 // Acceptance (greedy: always; refinement: DP value > incumbent value, which
 // by Proposition 1 is G(T_-h, T'_h) > G(T)) and, when accepted, the walk
 // from (i=1, j=k'): take b_i if its choice bit is set (i+1, j-1), else jump
-// to next(i).  The wave loads a window of 64 rows (their next() and the
-// choice words of the current stage) at once and walks it with lane reads,
-// so memory latency is paid per window rather than per step.
+// to next(i).
+//
+// A choice word of one sweep batch holds 32 consecutive rows -- a window,
+// row q at bit q mod 32 (the padded step count is a multiple of 32) -- of
+// one cell column, so the walk tests bits of one scalar word per (window,
+// column) and reads next(q) from one register per window.  Rows are staged
+// in super-windows of 512: the words of the current stage and next() of the
+// 512 rows go to LDS, and the next super-window of the same stage is loaded
+// from memory into registers while this one is walked (rows only increase
+// along the walk).  The walk keeps the current window in registers (lane l:
+// the words of its cell columns; lanes 0..31: next() of the window's rows)
+// and reads the following window from LDS ahead of use.  When j leaves the
+// stage, the words are reloaded for the stage below.  Taken rows are
+// gathered per window and written as a bitmap.
 template <int C>
 __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
                                                   int mode) {
+  constexpr int kWin = kDpBatch;        // rows per choice word
+  constexpr int kSwWin = 16;            // windows per super-window
+  constexpr int kSw = kWin * kSwWin;    // rows per super-window
+  constexpr int kNx = kSw / kWave;      // next() registers per lane
+  constexpr int kW = C * kSwWin;        // choice-word registers per lane
+  constexpr int kStage = kWave * C;     // cells per stage
+  static_assert(kWin == 32, "choice words hold 32 steps");
+  __shared__ uint32_t s_words[kSwWin][C][kWave];
+  __shared__ int s_nx[kSw];
   const int ci = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t slot = set.slot[ci];
@@ -546,51 +618,158 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     }
   }
   if (!accept) return;
-  uint8_t* sel = d.sel + slot * d.npad;
-  uint32_t* sel4 = (uint32_t*)sel;
-  for (int q = lane; q < d.npad / 4; q += kWave) sel4[q] = 0;
-  __threadfence_block();
+  const int nwords = d.npad / 32;
+  uint32_t* selw = d.sel + slot * nwords;
+  for (int q = lane; q < nwords; q += kWave) selw[q] = 0;
+  if (kp <= 0) return;
+
+  const int nwin = (n + kWin - 1) / kWin;  // windows = sweep batches
+  const int64_t cstride = 2 * (int64_t)d.npad;
+  const uint32_t* bw = (const uint32_t*)d.bits + slot * d.stages * (int64_t)C * cstride;
+
+  // window wq = rows [32 wq, 32 wq + 32) = sweep batch nwin-1-wq.  Rows
+  // past the end are never walked; their loads are clamped into range.
+  auto load_words = [&](int sw, int g, uint32_t (&w)[kW]) {
+    const uint32_t* base = bw + (int64_t)g * C * cstride + lane;
+#pragma unroll
+    for (int k = 0; k < kSwWin; ++k) {
+      const int b = max(nwin - 1 - (sw * kSwWin + k), 0);
+#pragma unroll
+      for (int c = 0; c < C; ++c) w[c * kSwWin + k] = base[c * cstride + (int64_t)b * kWave];
+    }
+  };
+  auto load_next = [&](int sw, int (&nx)[kNx]) {
+#pragma unroll
+    for (int t = 0; t < kNx; ++t)
+      nx[t] = d.nextpos[min(sw * kSw + t * kWave + lane, n - 1)];
+  };
+  auto words_to_lds = [&](const uint32_t (&w)[kW]) {
+#pragma unroll
+    for (int k = 0; k < kSwWin; ++k)
+#pragma unroll
+      for (int c = 0; c < C; ++c) s_words[k][c][lane] = w[c * kSwWin + k];
+  };
+  auto next_to_lds = [&](const int (&nx)[kNx]) {
+#pragma unroll
+    for (int t = 0; t < kNx; ++t) s_nx[t * kWave + lane] = nx[t];
+  };
+  // window k of the staged super-window: lane l's words, and next() of row
+  // 32k + (l mod 32)
+  auto read_win = [&](int k, uint32_t (&w)[C], int& nx) {
+#pragma unroll
+    for (int c = 0; c < C; ++c) w[c] = s_words[k][c][lane];
+    nx = s_nx[k * kWin + lane % kWin];
+  };
+
+  // take masks: lane (window mod 64) of tw holds that window's mask; tw
+  // covers windows [64 tblk, 64 tblk + 64)
+  uint32_t tw = 0;
+  int tblk = 0;
+  int cur_win = 0;
+  uint32_t tm = 0;
+  auto move_to = [&](int win) {
+    if (win == cur_win) return;
+    if ((cur_win >> 6) != tblk) {
+      const int idx = tblk * kWave + lane;
+      if (idx < nwords) selw[idx] = tw;
+      tw = 0;
+      tblk = cur_win >> 6;
+    }
+    tw = (uint32_t)pp_writelane_i32((int)tm, cur_win & (kWave - 1), (int)tw);
+    tm = 0;
+    cur_win = win;
+  };
+
+  int q = 0, j = kp;
+  int g = (j - 1) / kStage;
+  int sw = 0;
+  uint32_t wb[kW];
+  int nb[kNx];
+  load_words(0, g, wb);
+  load_next(0, nb);
+  words_to_lds(wb);
+  next_to_lds(nb);
   __syncthreads();
-  int pos = 0, j = kp;
-  while (pos < n && j > 0) {
-    const int g = (j - 1) / (kWave * C);
-    const uint64_t* bw = d.bits + (slot * d.stages + g) * (int64_t)C * d.npad;
-    const int pos0 = pos;
-    const int q = pos0 + lane;
-    uint64_t w[C];
-    int nx = n;
-#pragma unroll
-    for (int c = 0; c < C; ++c) w[c] = 0;
-    const int pad = (n + kDpBatch - 1) / kDpBatch * kDpBatch - n;
-    if (q < n) {
-      const int s = n - 1 - q + pad;  // padded step of row q
-#pragma unroll
-      for (int c = 0; c < C; ++c) w[c] = bw[(int64_t)c * d.npad + s];
-      nx = d.nextpos[q];
-    }
-    const int jlo = g * kWave * C + 1;
-    uint64_t takes = 0;
+  bool done = false;
+  while (!done) {
+    // the next super-window of this stage, in flight while this one is walked
+    load_words(sw + 1, g, wb);
+    load_next(sw + 1, nb);
+    const int q_lo = sw * kSw;
+    const int jlo = g * kStage + 1;
+    int wk = (q - q_lo) / kWin;
+    move_to(q / kWin);
+    uint32_t wc[C], wn[C];
+    int nxc, nxn;
+    read_win(wk, wc, nxc);
+    read_win(min(wk + 1, kSwWin - 1), wn, nxn);
+    int rem = j - jlo;  // cell of j within the stage
     for (;;) {
-      const int r = pos - pos0;
-      if (r >= kWave || pos >= n || j < jlo) break;
-      const int rem = j - jlo;
-      const int ln = rem / C, cc = rem % C;
-      uint64_t word = 0;
-#pragma unroll
-      for (int c = 0; c < C; ++c) {
-        const uint64_t wc = (uint64_t)readlane_i64((int64_t)w[c], r);
-        if (c == cc) word = wc;
-      }
-      if ((word >> ln) & 1ull) {
-        takes |= 1ull << r;
-        ++pos;
-        --j;
+      // walk inside the window: rows [wlo, wlo + lim), lim <= 32
+      const uint32_t wlo = (uint32_t)(q_lo + wk * kWin);
+      const uint32_t lim = (uint32_t)min(kWin, n - (int)wlo);
+      uint32_t uq = (uint32_t)q;
+      uint32_t t = tm;
+      if constexpr (C == 1) {
+        walk_window_c1(uq, rem, t, wlo, lim, wc[0], (uint32_t)nxc);
       } else {
-        pos = (int)readlane_u32((uint32_t)nx, r);
+        for (;;) {
+          const uint32_t r = uq - wlo;
+          uint32_t wsel = wc[0];
+#pragma unroll
+          for (int c = 1; c < C; ++c)
+            if (rem % C == c) wsel = wc[c];
+          const uint32_t W = readlane_u32(wsel, rem / C);
+          const uint32_t nq = readlane_u32((uint32_t)nxc, r);
+          const uint32_t bm = 1u << r;
+          const bool tk = (W & bm) != 0u;  // take b_q, else skip its subtree
+          t |= tk ? bm : 0u;
+          uq = tk ? uq + 1u : nq;
+          rem -= tk ? 1 : 0;
+          if (!(uq - wlo < lim && rem >= 0)) break;
+        }
       }
+      tm = t;
+      q = (int)uq;
+      j = jlo + rem;
+      if (j == 0 || q >= n) {
+        done = true;
+        break;
+      }
+      const int nw = (q - q_lo) / kWin;
+      move_to(q / kWin);
+      if (rem < 0 || nw >= kSwWin) break;  // left the stage or super-window
+      if (nw == wk + 1) {
+#pragma unroll
+        for (int c = 0; c < C; ++c) wc[c] = wn[c];
+        nxc = nxn;
+      } else {
+        read_win(nw, wc, nxc);
+      }
+      wk = nw;
+      read_win(min(wk + 1, kSwWin - 1), wn, nxn);
     }
-    if ((takes >> lane) & 1ull) sel[pos0 + lane] = 1;
+    if (done) break;
+    const int sw_n = q / kSw, g_n = (j - 1) / kStage;
+    if (g_n == g && sw_n == sw + 1) {
+      // the prefetched super-window
+    } else if (g_n == g) {
+      load_words(sw_n, g_n, wb);
+      load_next(sw_n, nb);
+    } else {
+      load_words(sw_n, g_n, wb);
+      if (sw_n != sw) load_next(sw_n, nb);
+    }
+    __syncthreads();
+    words_to_lds(wb);
+    if (sw_n != sw) next_to_lds(nb);
+    __syncthreads();
+    sw = sw_n;
+    g = g_n;
   }
+  move_to(-1);
+  const int idx = tblk * kWave + lane;
+  if (idx < nwords) selw[idx] = tw;
 }
 
 // -------------------------------------------------------------- commit --
@@ -606,7 +785,7 @@ __global__ void __launch_bounds__(256) k_commit(ChainSet set, DevState d) {
   if (i >= d.n) return;
   const int64_t mn = (int64_t)d.m * d.n;
   uint8_t* th = d.tgt + s * mn + (int64_t)h * d.n;
-  const uint8_t nv = d.sel[s * d.npad + i];
+  const uint8_t nv = (uint8_t)((d.sel[s * (d.npad / 32) + i / 32] >> (i % 32)) & 1u);
   if (nv == th[i]) return;
   th[i] = nv;
   refresh_holders(d, s, i);

@@ -1,8 +1,8 @@
 """CPU check of the DP sweep's step schedule (no GPU).
 
 The library exports, per tree, the metadata its gfx950 sweep follows: which
-steps are leaves, which rows are kept in which LDS stack slot, and which row
-each step's skip operand is read from.  This test replays that schedule on
+steps are leaves (a lane mask per step), which rows are kept in which LDS
+stack slot, and which row each step's skip operand is read from.  This test replays that schedule on
 whole DP rows with numpy -- target rows written to their slots at their own
 step, the next step's skip row read before the current step writes -- and
 requires the replay to reproduce the oracle's rooted-tree optimum and
@@ -34,17 +34,15 @@ def replay(parent, profit, k, cells):
     x = np.zeros(kk + 1, dtype=object)
     pre = np.zeros(kk + 1, dtype=object)
     bits = np.zeros((nsteps, kk + 1), dtype=bool)
-    leaf_next = True                             # padded step 0 is a leaf
     for s in range(nsteps):
-        st, pf = int(meta[s][0]), int(meta[s][1])
-        leaf = leaf_next
-        leaf_next = bool(pf & 256)               # flags step s+1
-        if not leaf_next:                        # the row is used: exact
-            assert pf % row == 0
-        pf_used = pf & ~256
-        assert pf_used % row == 0 and pf_used // row <= slots
+        st, pf, m2, m3 = (int(v) for v in meta[s])
+        assert m2 in (0, 0xFFFFFFFF) and m3 == m2
+        leaf = m2 != 0
+        if s == 0:
+            assert leaf                           # padded step 0 is a leaf
+        assert pf % row == 0 and pf // row <= slots
         assert st % row == 0 and st // row <= slots + 1 and st // row != slots
-        pnext = rows[pf_used // row].copy()      # read before this step writes
+        pnext = rows[pf // row].copy()           # read before this step writes
         sk = x if leaf else pre
         p = int(profit[order[n - 1 - (s - pad)]]) if s >= pad else 0
         t = np.empty(kk + 1, dtype=object)
