@@ -181,12 +181,13 @@ int pp_plan_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
  * nsteps - n) and the number of LDS stack rows H.  Rows hold 64*cells int64
  * in the order [H stack rows | zero row | sink row].  Per step: word 0 =
  * byte offset of the row the step's DP row is written to (its stack slot
- * when a later row skips to it, else the sink); word 1 = byte offset of the
- * row read as the next step's skip operand (Eq. 9's D[next(i)][*]: a stack
- * slot, or the zero row when that next() is past the end or the next node is
- * a leaf); words 2 and 3 = 0xFFFFFFFF when the step's own node is a leaf
- * (its skip operand is then the previous row), else 0.  The first step's
- * node is always a leaf. */
+ * when a row more than two rows back skips to it, else the sink); word 1 =
+ * byte offset of the row read as the next step's skip operand (Eq. 9's
+ * D[next(i)][*]: a stack slot, or the zero row when that next() is past the
+ * end or the operand is one of the two previous rows); word 2 = 0xFFFFFFFF
+ * when the step's node is a leaf (skip operand: the previous row), else 0;
+ * word 3 = 0xFFFFFFFF when its subtree has two nodes (skip operand: the row
+ * before the previous one), else 0.  The first step's node is a leaf. */
 int pp_sweep_layout(int32_t n, const int32_t *parent, int32_t cells,
                     uint32_t *meta, int32_t *nsteps, int32_t *slots);
 

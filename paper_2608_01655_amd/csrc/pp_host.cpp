@@ -16,6 +16,8 @@
 #include <memory>
 #include <new>
 #include <string>
+#include <map>
+#include <set>
 #include <vector>
 
 using namespace pp;
@@ -80,9 +82,9 @@ struct DevBuf {
 struct TreeLayout {
   int32_t n = 0;
   std::vector<int32_t> order, nextpos;
-  // per padded DP step: leaf flag, stack slot the row is kept in (-1: not a
-  // skip target), and the padded step whose row is the next step's skip
-  // operand (-1: the next step is a leaf or there is none, -2: zero row)
+  // per padded DP step: leaf flag (next(i) = i+1), the LDS slot the row is
+  // stored to (-1: a sink row), and the slot holding the next step's skip
+  // operand (-1: the zero row, or the next step is a leaf)
   std::vector<uint8_t> leaf;
   std::vector<int32_t> store, src;
   int32_t slots = 0;    // LDS stack rows the sweep needs
@@ -131,42 +133,69 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
     t.nextpos[q] = q + size[q];
     if (t.order[q] != q) t.identity = false;
   }
-  // DP metadata.  Rows are 1-based positions i; nx(i) = next(i).  Row r is
-  // a far skip target if r = next(a) for some a with r != a+1, r != n+1;
-  // the smallest such a is its last reader.  Pending targets nest like the
-  // subtrees that end at them, so they live on a stack of LDS slots.
+  // DP metadata.  Rows are 1-based positions i; nx(i) = next(i); row i is
+  // produced at padded step pad + n - i.  A row r = next(a) with r != a+1
+  // (a is no leaf) and r != n+1 is a far target: it is stored to an LDS
+  // slot at its own step, and a reader a reads it right after the store two
+  // steps before its own.  Every other row is stored to a sink row (step
+  // mod the sink row count).  Every few steps (the sink row count, at most
+  // kDpGatherMax) the stage gathers its last cell column from the rows those
+  // steps were stored to, so a slot becomes free after its last reader (the
+  // smallest a) has read it and after the gather of its group.
   auto nx = [&](int32_t i) { return t.nextpos[i - 1] + 1; };
+  auto far = [&](int32_t a, int32_t r) { return r != a + 1 && r != n + 1; };
   std::vector<int32_t> last_user(n + 2, INT32_MAX), slot_of(n + 2, -1);
   for (int32_t a = n; a >= 1; --a) {
     const int32_t r = nx(a);
-    if (r != a + 1 && r != n + 1) last_user[r] = a;  // descending: ends at min
+    if (far(a, r)) last_user[r] = a;  // descending: ends at min
   }
   const int32_t nsteps = (n + kDpBatch - 1) / kDpBatch * kDpBatch;
   const int32_t pad = nsteps - n;
   t.leaf.assign(nsteps, 1);
   t.store.assign(nsteps, -1);
-  t.src.assign(nsteps, -2);
-  int32_t top = 0, high = 0;
+  t.src.assign(nsteps, -1);
+  // free slots (lowest first) and slots waiting for their release step
+  std::set<int32_t> free_slots;
+  std::multimap<int32_t, int32_t> releases;  // step -> slot
+  int32_t high = 0;
   for (int32_t i = n; i >= 1; --i) {
     const int32_t s = pad + n - i;  // padded step of row i
+    for (auto it = releases.begin(); it != releases.end() && it->first <= s;
+         it = releases.erase(it))
+      free_slots.insert(it->second);
     const int32_t r = nx(i);
     t.leaf[s] = (r == i + 1) ? 1 : 0;
-    if (r != i + 1 && r != n + 1 && last_user[r] == i) {
-      if (slot_of[r] != top - 1) return fail(PP_E_DEVICE, "internal: stack order");
-      --top;
+    if (far(i, r) && last_user[r] == i) {
+      // read at step s-2; written at step s(r), gathered at the end of its
+      // group
+      const int32_t sr = pad + n - r;
+      const int32_t after_gather = (sr / kDpGatherMax + 1) * kDpGatherMax;
+      const int32_t at = std::max(s, after_gather);
+      if (at <= s)
+        free_slots.insert(slot_of[r]);
+      else
+        releases.emplace(at, slot_of[r]);
     }
     if (last_user[i] != INT32_MAX) {
-      if (top >= kMaxSlots)
-        return fail(PP_E_UNSUPPORTED,
-                    "tree needs more than 254 pending subtree boundaries");
-      slot_of[i] = top++;
-      high = std::max(high, top);
-      t.store[s] = slot_of[i];
+      int32_t k;
+      if (!free_slots.empty()) {
+        k = *free_slots.begin();
+        free_slots.erase(free_slots.begin());
+      } else {
+        if (high >= kMaxSlots)
+          return fail(PP_E_UNSUPPORTED,
+                      "tree needs more than 254 pending subtree boundaries");
+        k = high++;
+      }
+      slot_of[i] = k;
+      t.store[s] = k;
     }
-    t.src[s] = -1;
     if (i > 1) {
       const int32_t r2 = nx(i - 1);
-      if (r2 != i) t.src[s] = (r2 == n + 1) ? -2 : pad + n - r2;
+      if (far(i - 1, r2)) {
+        if (slot_of[r2] < 0) return fail(PP_E_DEVICE, "internal: far row without a slot");
+        t.src[s] = slot_of[r2];
+      }
     }
   }
   t.slots = high;
@@ -176,20 +205,17 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
 // DP-sweep metadata for `cells` cells per lane (layout in pp_internal.h):
 // kMetaWords words per padded step.
 std::vector<uint32_t> encode_meta(const TreeLayout& t, int cells) {
-  const int64_t row = (int64_t)cells * 64 * 8;  // bytes per LDS stack row
-  const int64_t zero = (int64_t)t.slots * row, sink = zero + row;
+  const int64_t row = dp_row_stride(cells);  // bytes per LDS row
+  const int64_t zero = (int64_t)t.slots * row, sink0 = zero + row;
   const int32_t nsteps = (int32_t)t.leaf.size();
   std::vector<uint32_t> meta(kMetaWords * (size_t)nsteps);
   for (int32_t s = 0; s < nsteps; ++s) {
-    const int32_t r = t.src[s];
-    const int64_t st = t.store[s] >= 0 ? (int64_t)t.store[s] * row : sink;
-    const int64_t pf = r >= 0 ? (int64_t)t.store[r] * row : zero;
-    const uint32_t leaf = t.leaf[s] ? 0xFFFFFFFFu : 0u;
     uint32_t* w = meta.data() + kMetaWords * (size_t)s;
-    w[0] = (uint32_t)st;
-    w[1] = (uint32_t)pf;
-    w[2] = leaf;
-    w[3] = leaf;
+    w[0] = (uint32_t)(t.store[s] >= 0 ? t.store[s] * row
+                                      : sink0 + (s % dp_sink_rows(cells)) * row);
+    w[1] = (uint32_t)(t.src[s] >= 0 ? t.src[s] * row : zero);
+    w[2] = t.leaf[s] ? 0xFFFFFFFFu : 0u;
+    w[3] = 0u;
   }
   return meta;
 }
@@ -430,7 +456,7 @@ int choose_cells(int32_t total_stage_cells_c1, int dev, int32_t slots_lds) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     cus = 256;
   const double simds = 4.0 * cus;
-  const struct { int c; double ns; } widths[] = {{1, 61.0}, {2, 77.0}, {4, 125.0}};
+  const struct { int c; double ns; } widths[] = {{1, 47.0}, {2, 61.0}, {4, 103.0}};
   int best = 0, most = 2, most_res = 0;
   double best_cost = 0.0;
   for (const auto& w : widths) {
@@ -737,17 +763,18 @@ int check_meta(const TreeLayout& t, const std::vector<uint32_t>& meta,
                int cells) {
   if (t.leaf.empty() || !t.leaf[0])
     return fail(PP_E_DEVICE, "internal: the first DP step must be a leaf");
-  const int64_t row = (int64_t)cells * 64 * 8;  // bytes
+  const int64_t row = dp_row_stride(cells);
   if (meta.size() != kMetaWords * t.leaf.size() || meta[2] != 0xFFFFFFFFu)
     return fail(PP_E_DEVICE, "internal: DP step metadata malformed");
+  const int64_t h = t.slots;
   for (size_t q = 0; q < meta.size(); q += kMetaWords) {
     const int64_t st = meta[q], pf = meta[q + 1];
-    // stores go to a stack slot or the sink, never to the zero row; reads
-    // come from a stack slot or the zero row
-    if (st % row != 0 || st / row > t.slots + 1 || st / row == t.slots ||
-        pf % row != 0 || pf / row > t.slots ||
-        (meta[q + 2] != 0u && meta[q + 2] != 0xFFFFFFFFu) ||
-        meta[q + 3] != meta[q + 2])
+    // stores go to a slot or a sink row, never to the zero row; reads come
+    // from a slot or the zero row
+    const bool st_ok = st % row == 0 && (st / row < h ||
+                                         (st / row > h && st / row <= h + dp_sink_rows(cells)));
+    if (!st_ok || pf % row != 0 || pf / row > h ||
+        (meta[q + 2] != 0u && meta[q + 2] != 0xFFFFFFFFu) || meta[q + 3] != 0u)
       return fail(PP_E_DEVICE, "internal: DP step metadata out of range");
   }
   return PP_OK;

@@ -13,20 +13,28 @@ constexpr int kMaxChains = 64;
 constexpr uint8_t kNoHolder = 255;
 
 // Per-step metadata of the DP sweep: four uint32 per padded step (see
-// kDpBatch), encoded for a given cells-per-lane width C.  LDS stack rows
-// hold 64*C int64 (512*C bytes): rows [0, H) are the stack of pending skip
-// targets, row H is the all-zero row and row H+1 a write sink.
-//   word 0: byte offset of the row that row i is stored to: its stack slot
-//           if it is a later skip target (next(a) = i for some a < i-1),
-//           else the sink row.
-//   word 1: byte offset of the row prefetched as the skip operand of the
-//           next step (row i-1): the stack slot of next(i-1), or the zero
-//           row when next(i-1) = n+1 or b_{i-1} is a leaf (whose skip
-//           operand D[next(i-1)][*] = D[i][*] is the row in registers).
-//   words 2, 3: the lane mask selecting the row in registers as the skip
-//           operand: all ones when b_i is a leaf, else zero.  Padded step 0
-//           is a leaf.
+// kDpBatch), encoded for a given cells-per-lane width C.  LDS rows hold
+// 64*C int64 at a stride of dp_row_stride(C) bytes: H slot rows for far
+// skip targets, the all-zero row, then dp_sink_rows(C) sink rows.
+//   word 0: byte offset of the row that row i is stored to: its slot if it
+//           is a far skip target (next(a) = i for some a < i-1), else sink
+//           row (step mod dp_sink_rows(C)).
+//   word 1: byte offset of the row read as the skip operand of the next
+//           step (row i-1): the slot of next(i-1), or the zero row when
+//           next(i-1) = n+1 or b_{i-1} is a leaf (whose skip operand, the
+//           previous row, is in registers).
+//   word 2: all ones when b_i is a leaf, else zero.
+//   word 3: zero.
+// Padded step 0 is a leaf.
 constexpr int kMetaWords = 4;
+// Sink rows (also the steps per gather of a stage's last cell column): 16
+// at one cell per lane, 4 for wider rows to keep more stages resident.
+// Slot reuse waits for the gather of a 16-step group, which covers both.
+constexpr int kDpGatherMax = 16;
+constexpr int dp_sink_rows(int cells) { return cells == 1 ? 16 : 4; }
+// LDS row stride: 64*C int64 plus 8 bytes, so that lane 63 of consecutive
+// rows falls in different banks.
+constexpr int64_t dp_row_stride(int cells) { return (int64_t)cells * 64 * 8 + 8; }
 constexpr int kMaxSlots = 254;
 // The sweep runs steps in batches of kDpBatch; the step count is padded up
 // to a multiple of it with leading dummy steps (leaf, profit 0), so step s

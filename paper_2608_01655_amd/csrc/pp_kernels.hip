@@ -75,6 +75,7 @@ __device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
 typedef int pp_int2 __attribute__((ext_vector_type(2)));
 typedef int64_t pp_i64x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t pp_u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t pp_u32x3 __attribute__((ext_vector_type(3)));
 
 __device__ __forceinline__ pp_int2 split64(int64_t v) {
   return __builtin_bit_cast(pp_int2, v);
@@ -289,33 +290,31 @@ __device__ __forceinline__ int64_t max_nonneg_f64(int64_t a, int64_t b) {
 // neighbour lane by a DPP shift; lane 0 gets it from stage g-1, whose last
 // cell of every row is published through a per-step ring in global memory.
 // Ring words carry a launch tag in their high half (relaxed agent-scope
-// atomics, no fences): a consumer validates each word by its tag.
+// atomics, no fences): a consumer validates each word by its tag.  A stage
+// loads its input two batches ahead, so in steady state it runs two
+// batches behind its producer and finds the words there.
 //
-// Rows that a later row skips to (next(a) for some a < i-1) are written to
-// an LDS stack slot at their own step (other rows to a sink row, so the
-// store needs no branch): pending targets nest like the subtrees that end
-// at them, so at most "tree depth" are pending and every skip operand is on
-// chip.  A step reads the next step's skip operand (a stack slot, or the
-// all-zero row) at its top, a full step before use: that row was produced
-// at least two steps earlier and no push reuses its slot while it is
-// pending.  A leaf's skip operand is the row in registers, chosen per step
-// by a uniform lane mask from the metadata.  Each step also writes its last
-// cell column to a small history, from which the ring output is gathered
-// every kProd steps.
+// Rows that a later row skips to (next(a) = i for some non-leaf a, i !=
+// n+1) are stored to an LDS slot at their own step, other rows to one of a
+// few sink rows (step mod their count), so the store needs no branch.
+// Right after its store a step reads the skip operand of the step two
+// ahead (a slot, or the all-zero row): that row is produced at this step at
+// the latest.  A leaf's skip operand is the previous row, in registers,
+// chosen per step by a uniform lane mask from the metadata.  After every
+// group of sink-row-count steps the stage gathers its last cell column of
+// those steps from the rows they were stored to (a slot is reused only
+// after that gather) for the ring in global memory.
 //
 // Steps run in batches of kBatch, unrolled at compile time; the step count
 // is padded up to a multiple of kBatch with leading dummy steps (profit 0,
 // leaf, rows stay all-zero).  Per batch each lane stages one step's record
 // -- profit, boundary value and the step's metadata words -- in LDS, read
-// back per step with two broadcast loads; the metadata, profits and ring
-// input of the next batch are loaded one batch ahead (the ring input is
-// validated at the batch boundary).
-// Each lane shifts its cells' choice bits into one 32-bit word per cell per
-// batch (bit 31-u = step u), stored with one coalesced store per cell; the
-// ring output also leaves with one store per batch.  No per-row launch,
-// barrier or HBM row traffic.
+// back per step with two broadcast loads.  Each lane shifts its cells'
+// choice bits into one 32-bit word per cell per batch (bit 31-u = step u),
+// stored with one coalesced store per cell; the stage ring output also
+// leaves with one store per batch.  No per-row launch, barrier or HBM row
+// traffic.
 constexpr int kBatch = kDpBatch;
-constexpr int kProd = 16;  // steps per gather of the ring output
 
 struct __attribute__((aligned(16))) StepRec {
   int64_t p;      // profit of the step's node
@@ -339,14 +338,15 @@ __global__ void __launch_bounds__(64)
 k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
      int store_bits, int32_t slots) {
   extern __shared__ int64_t lds[];
-  constexpr int kRow = C * kWave;              // int64 per stack row
-  // step records first (small immediate offsets), then the stack rows, the
-  // zero row and the sink row, then the last-column history
-  StepRec* rec = (StepRec*)lds;                            // [kBatch]
-  int64_t* stk = lds + kBatch * (sizeof(StepRec) / 8);     // [slots + 2][C][64]
-  int64_t* hist = stk + (slots + 2) * kRow;                // [kProd][64]
+  constexpr int kStride = (int)dp_row_stride(C);  // bytes per LDS row
+  constexpr int kProd = dp_sink_rows(C);  // steps per gather of the last column
+  static_assert(kBatch % kProd == 0 && kProd <= kDpGatherMax, "gather groups");
+  // step records first (small immediate offsets), then the rows: the slots,
+  // the zero row and the sink rows
+  StepRec* rec = (StepRec*)lds;                                // [kBatch + 1]
+  char* rows = (char*)(rec + kBatch + 1);
   const int lane = threadIdx.x;
-  char* lane_bytes = (char*)stk + lane * 8;
+  char* lane_bytes = rows + lane * 8;
   const int blk = blockIdx.x;
   if (blk >= set.base[set.count]) return;
   int ci = 0;
@@ -367,15 +367,16 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
   const uint64_t tag = (uint64_t)epoch << 32;
   const bool produce = g + 1 < G;
+  const int zero_off = slots * kStride;
 #pragma unroll
-  for (int c = 0; c < C; ++c) stk[slots * kRow + c * kWave + lane] = 0;
+  for (int c = 0; c < C; ++c) *(int64_t*)(lane_bytes + zero_off + c * kWave * 8) = 0;
 
   // ring input of the batch at s0: lane u < kBatch <- entry s0+u-1
   auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
     const int e = s0 - 1 + lane;
     w0 = tag;
     w1 = tag;
-    if (ring_in && lane < kBatch && e >= 0) {
+    if (ring_in && lane < kBatch && e >= 0 && s0 < nsteps) {
       w0 = ld_agent(ring_in + 2 * (int64_t)e);
       w1 = ld_agent(ring_in + 2 * (int64_t)e + 1);
     }
@@ -402,34 +403,31 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     const int s = t - pad;
     return (lane < kBatch && s >= 0 && s < n) ? prof[n - 1 - s] : 0;
   };
+  // lane kBatch carries the first step of the following batch, whose word 0
+  // names the skip row the batch's last step reads ahead
+  auto meta_at = [&](int t) -> uint4 {
+    return (lane <= kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
+  };
 
-  int64_t x[C], pre[C];
+  // x: the previous row D[i+1]; pre[u % 2]: the far skip row of step u,
+  // read two steps ahead (padded steps 0 and 1 need none: step 0 is a leaf,
+  // and a non-leaf step 1 skips to D[n+1], the zero row)
+  int64_t x[C], pre[2][C];
   uint32_t acc[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) {
     x[c] = 0;
-    pre[c] = 0;
+    pre[0][c] = 0;
+    pre[1][c] = 0;
     acc[c] = 0;
   }
-  // history column rotated by step, so gathering lane 63's cells reads 16
-  // different banks: step u's value of lane l sits at column (l + u) mod 64
-  int hw[kProd];
-#pragma unroll
-  for (int q = 0; q < kProd; ++q) hw[q] = q * kWave + ((lane + q) & (kWave - 1));
-  const int hr = (lane % kProd) * kWave + ((kWave - 1 + lane % kProd) & (kWave - 1));
-  auto meta_at = [&](int t) -> uint4 {
-    return (lane < kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
-  };
-  int64_t pv = profit_at(lane);
-  uint4 mv = meta_at(lane);
-  uint64_t rw0, rw1;
-  ring_load(0, rw0, rw1);
-  ring_wait(0, rw0, rw1);
-  int64_t bv = (int64_t)((rw1 << 32) | (rw0 & 0xFFFFFFFFull));
-
-  for (int s0 = 0; s0 < nsteps && !failed; s0 += kBatch) {
-    const int s1 = s0 + kBatch;
-    if (lane < kBatch) {
+  // gather: lane u < kBatch reads the last cell (lane 63, cell C-1) of the
+  // row step u was stored to
+  constexpr int kLastCell = (C - 1) * kWave * 8 + (kWave - 1) * 8;
+  // stage the records of the batch at s0 (profits, boundary values and
+  // metadata already in registers); returns the lane's gather address
+  auto stage = [&](int64_t pv, int64_t bv, uint4 mv) -> const char* {
+    if (lane <= kBatch) {
       StepRec r;
       r.p = pv;
       r.bnd = bv;
@@ -439,36 +437,58 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       r.pad = 0;
       rec[lane] = r;
     }
-    // next batch: metadata, profits and ring input, consumed after the loop
+    return rows + mv.x + kLastCell;
+  };
+  auto join = [&](uint64_t w0, uint64_t w1) {
+    return (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
+  };
+  // ring words in flight: the set for batch t is loaded during batch t-2 and
+  // validated at the end of batch t-1.  The batch loop is unrolled twice so
+  // that the two sets keep their registers (no copies of pending loads).
+  uint64_t ra0, ra1, rb0, rb1;
+  const char* gath_addr;
+  {
+    uint64_t w0, w1;
+    ring_load(0, w0, w1);
+    ring_wait(0, w0, w1);
+    gath_addr = stage(profit_at(lane), join(w0, w1), meta_at(lane));
+  }
+  ring_load(kBatch, rb0, rb1);  // batch 1
+
+  // one batch at s0: `nw` receives the ring words of batch s0+2B, `vw`
+  // holds those of batch s0+B (validated at the end)
+  auto batch = [&](int s0, uint64_t& nw0, uint64_t& nw1, uint64_t& vw0,
+                   uint64_t& vw1) {
+    const int s1 = s0 + kBatch;
+    // the next batch's profits and metadata, staged at the end of this one
     const int64_t pv_n = profit_at(s1 + lane);
     const uint4 mv_n = meta_at(s1 + lane);
-    uint64_t nw0 = tag, nw1 = tag;
-    if (s1 < nsteps) ring_load(s1, nw0, nw1);
+    ring_load(s1 + kBatch, nw0, nw1);
 
-    // records of steps u, u+1, u+2 in flight: {p, bnd} and {st, pf, leaf}
-    pp_i64x2 rv[3];
-    pp_u32x4 rm[3];
+    // records of steps u..u+3 in flight: {p, bnd} and {st, pf, leaf} (the
+    // record of step kBatch is the next batch's first: only its pf is used;
+    // the unused pad word is not loaded, so no loaded register is dead)
+    constexpr int kRq = 4;
+    pp_i64x2 rv[kRq];
+    pp_u32x3 rm[kRq];
     auto rec_load = [&](int t, int q) {
       rv[q] = *(const pp_i64x2*)&rec[t];
-      rm[q] = *(const pp_u32x4*)&rec[t].st;
+      rm[q] = *(const pp_u32x3*)&rec[t].st;
     };
     rec_load(0, 0);
     rec_load(1, 1);
-    int64_t gath[kBatch / kProd];  // lane 63's last cells, gathered per kProd
+    rec_load(2, 2);
+    int64_t gath[kBatch / kProd];  // lane u: last cell of step u's row
     auto step = [&](auto uc) {
       constexpr int u = decltype(uc)::value;
-      if constexpr (u + 2 < kBatch) rec_load(u + 2, (u + 2) % 3);
-      const int64_t cur_p = rv[u % 3].x, cur_bnd = rv[u % 3].y;
-      const uint32_t cur_st = rm[u % 3].x, cur_pf = rm[u % 3].y, cur_leaf = rm[u % 3].z;
-      const int64_t* prow = (const int64_t*)(lane_bytes + cur_pf);
-      int64_t pnext[C];
-#pragma unroll
-      for (int c = 0; c < C; ++c) pnext[c] = prow[c * kWave];
+      if constexpr (u + 3 <= kBatch) rec_load(u + 3, (u + 3) % kRq);
+      const int64_t cur_p = rv[u % kRq].x, cur_bnd = rv[u % kRq].y;
+      const uint32_t cur_st = rm[u % kRq].x, cur_leaf = rm[u % kRq].z;
       const int64_t left = shift_up(x[C - 1], cur_bnd);
       int64_t y[C];
 #pragma unroll
       for (int c = 0; c < C; ++c) {
-        const int64_t sk = select_bits(cur_leaf, x[c], pre[c]);
+        const int64_t sk = select_bits(cur_leaf, x[c], pre[u % 2][c]);
         const int64_t t = cur_p + (c == 0 ? left : x[c - 1]);
         acc[c] = shift_in_gt(t, sk, acc[c]);
         if constexpr (FMAX)
@@ -476,18 +496,21 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         else
           y[c] = t > sk ? t : sk;
       }
-      // the row goes to its stack slot if it is a later skip target, else
-      // to the sink row
-      int64_t* srow = (int64_t*)(lane_bytes + cur_st);
+      // the row goes to its slot if it is a later skip target, else to a
+      // sink row
 #pragma unroll
-      for (int c = 0; c < C; ++c) srow[c * kWave] = y[c];
-      hist[hw[u % kProd]] = y[C - 1];
-      if constexpr (u % kProd == kProd - 1) gath[u / kProd] = hist[hr];
+      for (int c = 0; c < C; ++c)
+        *(int64_t*)(lane_bytes + cur_st + c * kWave * 8) = y[c];
+      // skip row of step u+2 (word 1 of step u+1), read after this store:
+      // it is row i-2's next(), produced at this step at the latest
+      {
+        const char* prow = lane_bytes + rm[(u + 1) % kRq].y;
 #pragma unroll
-      for (int c = 0; c < C; ++c) {
-        pre[c] = pnext[c];
-        x[c] = y[c];
+        for (int c = 0; c < C; ++c) pre[u % 2][c] = *(const int64_t*)(prow + c * kWave * 8);
       }
+      if constexpr (u % kProd == kProd - 1) gath[u / kProd] = *(const int64_t*)gath_addr;
+#pragma unroll
+      for (int c = 0; c < C; ++c) x[c] = y[c];
     };
     unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
     if (store_bits) {
@@ -505,12 +528,14 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
       st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
     }
-    pv = pv_n;
-    mv = mv_n;
     if (s1 < nsteps) {
-      ring_wait(s1, nw0, nw1);
-      bv = (int64_t)((nw1 << 32) | (nw0 & 0xFFFFFFFFull));
+      ring_wait(s1, vw0, vw1);
+      gath_addr = stage(pv_n, join(vw0, vw1), mv_n);
     }
+  };
+  for (int s0 = 0; s0 < nsteps && !failed; s0 += 2 * kBatch) {
+    batch(s0, ra0, ra1, rb0, rb1);
+    if (s0 + kBatch < nsteps && !failed) batch(s0 + kBatch, rb0, rb1, ra0, ra1);
   }
   if (failed) {
     if (lane == 0) __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED,
@@ -888,11 +913,9 @@ hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) 
 }
 
 size_t dp_lds_bytes(int cells, int32_t slots_lds) {
-  // step records, stack rows, the zero row and the sink row, the
-  // last-column history
-  return kBatch * sizeof(StepRec) +
-         (size_t)(slots_lds + 2) * cells * kWave * sizeof(int64_t) +
-         (size_t)kProd * kWave * sizeof(int64_t);
+  // step records, then the slot rows, the zero row and the sink rows
+  return (kBatch + 1) * sizeof(StepRec) +
+         (size_t)(slots_lds + 1 + dp_sink_rows(cells)) * dp_row_stride(cells);
 }
 
 template <int C, bool FMAX>

@@ -1,14 +1,18 @@
 """CPU check of the DP sweep's step schedule (no GPU).
 
 The library exports, per tree, the metadata its gfx950 sweep follows: which
-steps are leaves (a lane mask per step), which rows are kept in which LDS
-stack slot, and which row each step's skip operand is read from.  This test replays that schedule on
-whole DP rows with numpy -- target rows written to their slots at their own
-step, the next step's skip row read before the current step writes -- and
+steps are leaves (a lane mask: their skip operand is the previous row, in
+registers), which LDS row each row is stored to (a slot if a later row
+skips to it, else one of a few sink rows), and which slot each other step's
+skip operand is read from.  This test replays that schedule on whole DP
+rows with numpy, in the kernel's order -- a step stores its row, then reads
+the skip row of the step two ahead; after each group of sink-row-count
+steps the rows of those steps must still be in place for the gather of the
+stage's last column -- and
 requires the replay to reproduce the oracle's rooted-tree optimum and
-selection (Eq. 9, Theorem 1, tie rule R1).  A wrong slot, a slot reused
-while pending, or a read issued too early would give a different value or
-set.
+selection (Eq. 9, Theorem 1, tie rule R1).  A wrong slot, a slot reused too
+early, or a read issued too early gives a different value or set, or fails
+the gather check.
 """
 
 import numpy as np
@@ -21,6 +25,8 @@ from tests import bruteforce as bf
 BATCH = 32
 
 
+
+
 def replay(parent, profit, k, cells):
     meta, slots = B.pp_sweep_layout(parent, cells)
     n = len(parent)
@@ -29,21 +35,23 @@ def replay(parent, profit, k, cells):
     nsteps = meta.shape[0]
     assert nsteps % BATCH == 0 and nsteps - n < BATCH
     pad = nsteps - n
-    row = 64 * cells * 8  # bytes per LDS row
-    rows = np.zeros((slots + 2, kk + 1), dtype=object)  # stack, zero, sink
+    row = 64 * cells * 8 + 8                     # LDS row stride (bytes)
+    sink = 16 if cells == 1 else 4               # sink rows = gather group
+    zero = slots                                 # slots | zero | sink rows
+    rows = np.zeros((slots + 1 + sink, kk + 1), dtype=object)
     x = np.zeros(kk + 1, dtype=object)
-    pre = np.zeros(kk + 1, dtype=object)
+    pre = [np.zeros(kk + 1, dtype=object) for _ in range(2)]
     bits = np.zeros((nsteps, kk + 1), dtype=bool)
+    group = []                                   # (row, value) of this group
     for s in range(nsteps):
         st, pf, m2, m3 = (int(v) for v in meta[s])
-        assert m2 in (0, 0xFFFFFFFF) and m3 == m2
+        assert m2 in (0, 0xFFFFFFFF) and m3 == 0
         leaf = m2 != 0
         if s == 0:
             assert leaf                           # padded step 0 is a leaf
-        assert pf % row == 0 and pf // row <= slots
-        assert st % row == 0 and st // row <= slots + 1 and st // row != slots
-        pnext = rows[pf // row].copy()           # read before this step writes
-        sk = x if leaf else pre
+        assert pf % row == 0 and pf // row <= zero
+        assert st % row == 0 and st // row != zero and st // row <= zero + sink
+        sk = x if leaf else pre[s % 2]
         p = int(profit[order[n - 1 - (s - pad)]]) if s >= pad else 0
         t = np.empty(kk + 1, dtype=object)
         t[0] = -1
@@ -53,9 +61,17 @@ def replay(parent, profit, k, cells):
         y = np.where(take, t, sk)
         y[0] = 0
         bits[s] = take
-        rows[st // row] = y                      # its slot, or the sink
-        assert all(v == 0 for v in rows[slots])  # the zero row stays zero
-        pre, x = pnext, y
+        rows[st // row] = y                      # its slot, or a sink row
+        group.append((st // row, y))
+        assert all(v == 0 for v in rows[zero])   # the zero row stays zero
+        # after the store: the skip row of step s+2 (word 1 of step s+1)
+        nxt = int(meta[s + 1][1]) if s + 1 < nsteps else zero * row
+        pre[s % 2] = rows[nxt // row].copy()
+        if s % sink == sink - 1:                 # the gather of the group:
+            for r_, v in group:                  # every row still in place
+                assert list(rows[r_]) == list(v)
+            group = []
+        x = y
     # backtrack over the recorded choice bits, in preorder positions
     nextpos = np.empty(n, np.int64)
     pos_of = {v: i for i, v in enumerate(order)}
@@ -115,7 +131,7 @@ def test_replayed_schedule_deep_and_wide(oracle_mod):
 
 def test_layout_of_benchmark_trees():
     """Stack depth of the benchmark trees stays small (LDS-resident)."""
-    for name, limit in (("tree50k", 16), ("chat50k", 20), ("rag10k", 10)):
+    for name, limit in (("tree50k", 20), ("chat50k", 24), ("rag10k", 16)):
         inst = W.make_workload(name)
         meta, slots = B.pp_sweep_layout(inst.parent, 2)
         assert slots <= limit
