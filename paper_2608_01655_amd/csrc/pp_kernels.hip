@@ -442,9 +442,10 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   auto join = [&](uint64_t w0, uint64_t w1) {
     return (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
   };
-  // ring words in flight: the set for batch t is loaded during batch t-2 and
-  // validated at the end of batch t-1.  The batch loop is unrolled twice so
-  // that the two sets keep their registers (no copies of pending loads).
+  // ring words in flight: the set for batch t is loaded at the start of
+  // batch t-2 and validated at the end of batch t-1.  The batch loop is
+  // unrolled twice so that the two sets keep their registers (no copies of
+  // pending loads).
   uint64_t ra0, ra1, rb0, rb1;
   const char* gath_addr;
   {
@@ -513,24 +514,26 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       for (int c = 0; c < C; ++c) x[c] = y[c];
     };
     unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
+    // the next batch first (its waits cover loads only), then this batch's
+    // stores, which complete during the next batch (stores count in vmcnt)
+    int64_t v = gath[0];
+#pragma unroll
+    for (int q = 1; q < kBatch / kProd; ++q)
+      if (lane >= q * kProd) v = gath[q];
+    if (s1 < nsteps) {
+      ring_wait(s1, vw0, vw1);
+      gath_addr = stage(pv_n, join(vw0, vw1), mv_n);
+    }
     if (store_bits) {
       const int64_t wi = (int64_t)(s0 / kBatch) * kWave + lane;
 #pragma unroll
       for (int c = 0; c < C; ++c) bits[c * cstride + wi] = acc[c];
     }
     if (produce && lane < kBatch) {
-      int64_t v = gath[0];
-#pragma unroll
-      for (int q = 1; q < kBatch / kProd; ++q)
-        if (lane >= q * kProd) v = gath[q];
       const uint64_t bo = (uint64_t)v;
       const int idx = s0 + lane;
       st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
       st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
-    }
-    if (s1 < nsteps) {
-      ring_wait(s1, vw0, vw1);
-      gath_addr = stage(pv_n, join(vw0, vw1), mv_n);
     }
   };
   for (int s0 = 0; s0 < nsteps && !failed; s0 += 2 * kBatch) {
