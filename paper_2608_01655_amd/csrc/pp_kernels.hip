@@ -600,6 +600,80 @@ __device__ __forceinline__ void walk_window_c1(uint32_t& q, int& rem, uint32_t& 
       : "scc");
 }
 
+// The same walk for two and four cells per lane: the column word of cell
+// index rem is lane rem/C of the cell-(rem mod C) register.
+__device__ __forceinline__ void walk_window_c2(uint32_t& q, int& rem, uint32_t& tm,
+                                               uint32_t wlo, uint32_t lim,
+                                               uint32_t wc0, uint32_t wc1,
+                                               uint32_t nx) {
+  uint32_t r, ln, w, w1, nq, bm, qp;
+  asm volatile(
+      "1:\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "s_lshr_b32 %[ln], %[rem], 1\n\t"
+      "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
+      "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
+      "v_readlane_b32 %[nq], %[nx], %[r]\n\t"
+      "s_bitcmp1_b32 %[rem], 0\n\t"
+      "s_cselect_b32 %[w], %[w1], %[w]\n\t"
+      "s_lshl_b32 %[bm], 1, %[r]\n\t"
+      "s_add_u32 %[qp], %[q], 1\n\t"
+      "s_and_b32 %[w], %[w], %[bm]\n\t"      // SCC = take
+      "s_cselect_b32 %[q], %[qp], %[nq]\n\t"
+      "s_cselect_b32 %[bm], %[bm], 0\n\t"
+      "s_subb_u32 %[rem], %[rem], 0\n\t"     // rem -= take
+      "s_or_b32 %[tm], %[tm], %[bm]\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "s_cmp_lt_u32 %[r], %[lim]\n\t"
+      "s_cselect_b32 %[r], %[rem], -1\n\t"
+      "s_cmp_ge_i32 %[r], 0\n\t"
+      "s_cbranch_scc1 1b"
+      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [r] "=&s"(r), [ln] "=&s"(ln),
+        [w] "=&s"(w), [w1] "=&s"(w1), [nq] "=&s"(nq), [bm] "=&s"(bm), [qp] "=&s"(qp)
+      : [wlo] "s"(wlo), [lim] "s"(lim), [wc0] "v"(wc0), [wc1] "v"(wc1), [nx] "v"(nx)
+      : "scc");
+}
+
+__device__ __forceinline__ void walk_window_c4(uint32_t& q, int& rem, uint32_t& tm,
+                                               uint32_t wlo, uint32_t lim,
+                                               uint32_t wc0, uint32_t wc1,
+                                               uint32_t wc2, uint32_t wc3,
+                                               uint32_t nx) {
+  uint32_t r, ln, w, w1, w2, w3, nq, bm, qp;
+  asm volatile(
+      "1:\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "s_lshr_b32 %[ln], %[rem], 2\n\t"
+      "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
+      "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
+      "v_readlane_b32 %[w2], %[wc2], %[ln]\n\t"
+      "v_readlane_b32 %[w3], %[wc3], %[ln]\n\t"
+      "v_readlane_b32 %[nq], %[nx], %[r]\n\t"
+      "s_bitcmp1_b32 %[rem], 1\n\t"          // cells 2, 3
+      "s_cselect_b32 %[w], %[w2], %[w]\n\t"
+      "s_cselect_b32 %[w1], %[w3], %[w1]\n\t"
+      "s_bitcmp1_b32 %[rem], 0\n\t"          // odd cells
+      "s_cselect_b32 %[w], %[w1], %[w]\n\t"
+      "s_lshl_b32 %[bm], 1, %[r]\n\t"
+      "s_add_u32 %[qp], %[q], 1\n\t"
+      "s_and_b32 %[w], %[w], %[bm]\n\t"      // SCC = take
+      "s_cselect_b32 %[q], %[qp], %[nq]\n\t"
+      "s_cselect_b32 %[bm], %[bm], 0\n\t"
+      "s_subb_u32 %[rem], %[rem], 0\n\t"     // rem -= take
+      "s_or_b32 %[tm], %[tm], %[bm]\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "s_cmp_lt_u32 %[r], %[lim]\n\t"
+      "s_cselect_b32 %[r], %[rem], -1\n\t"
+      "s_cmp_ge_i32 %[r], 0\n\t"
+      "s_cbranch_scc1 1b"
+      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [r] "=&s"(r), [ln] "=&s"(ln),
+        [w] "=&s"(w), [w1] "=&s"(w1), [w2] "=&s"(w2), [w3] "=&s"(w3), [nq] "=&s"(nq),
+        [bm] "=&s"(bm), [qp] "=&s"(qp)
+      : [wlo] "s"(wlo), [lim] "s"(lim), [wc0] "v"(wc0), [wc1] "v"(wc1),
+        [wc2] "v"(wc2), [wc3] "v"(wc3), [nx] "v"(nx)
+      : "scc");
+}
+
 // Acceptance (greedy: always; refinement: DP value > incumbent value, which
 // by Proposition 1 is G(T_-h, T'_h) > G(T)) and, when accepted, the walk
 // from (i=1, j=k'): take b_i if its choice bit is set (i+1, j-1), else jump
@@ -740,22 +814,11 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
       uint32_t t = tm;
       if constexpr (C == 1) {
         walk_window_c1(uq, rem, t, wlo, lim, wc[0], (uint32_t)nxc);
+      } else if constexpr (C == 2) {
+        walk_window_c2(uq, rem, t, wlo, lim, wc[0], wc[1], (uint32_t)nxc);
       } else {
-        for (;;) {
-          const uint32_t r = uq - wlo;
-          uint32_t wsel = wc[0];
-#pragma unroll
-          for (int c = 1; c < C; ++c)
-            if (rem % C == c) wsel = wc[c];
-          const uint32_t W = readlane_u32(wsel, rem / C);
-          const uint32_t nq = readlane_u32((uint32_t)nxc, r);
-          const uint32_t bm = 1u << r;
-          const bool tk = (W & bm) != 0u;  // take b_q, else skip its subtree
-          t |= tk ? bm : 0u;
-          uq = tk ? uq + 1u : nq;
-          rem -= tk ? 1 : 0;
-          if (!(uq - wlo < lim && rem >= 0)) break;
-        }
+        static_assert(C == 4, "one, two or four cells per lane");
+        walk_window_c4(uq, rem, t, wlo, lim, wc[0], wc[1], wc[2], wc[3], (uint32_t)nxc);
       }
       tm = t;
       q = (int)uq;
