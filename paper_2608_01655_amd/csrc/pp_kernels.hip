@@ -333,19 +333,36 @@ __device__ __forceinline__ void unroll_steps(F&& f, std::integer_sequence<int, U
   (f(IC<U>{}), ...);
 }
 
+// LDS bytes of the sweep's control area: two record buffers, two output
+// buffers (stage-ring values and choice words of a batch) and a flag word.
+template <int C>
+constexpr size_t dp_ctl_bytes() {
+  return 2 * (kBatch + 1) * sizeof(StepRec) + 2 * kBatch * sizeof(int64_t) +
+         2 * C * kWave * sizeof(uint32_t) + 16;
+}
+
 template <int C, bool FMAX>
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(2 * kWave)
 k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
      int store_bits, int32_t slots) {
   extern __shared__ int64_t lds[];
   constexpr int kStride = (int)dp_row_stride(C);  // bytes per LDS row
   constexpr int kProd = dp_sink_rows(C);  // steps per gather of the last column
   static_assert(kBatch % kProd == 0 && kProd <= kDpGatherMax, "gather groups");
-  // step records first (small immediate offsets), then the rows: the slots,
+  // control area first (small immediate offsets), then the rows: the slots,
   // the zero row and the sink rows
-  StepRec* rec = (StepRec*)lds;                                // [kBatch + 1]
-  char* rows = (char*)(rec + kBatch + 1);
-  const int lane = threadIdx.x;
+  StepRec* recs = (StepRec*)lds;                               // [2][kBatch + 1]
+  int64_t* outv = (int64_t*)(recs + 2 * (kBatch + 1));         // [2][kBatch]
+  uint32_t* outb = (uint32_t*)(outv + 2 * kBatch);             // [2][C][64]
+  // abort[t % 2]: set by the I/O wave between the barriers before and
+  // after batch t-1, read by both waves right after the barrier before
+  // batch t (alternating words, so a later write cannot race that read)
+  volatile int* abort_flag = (volatile int*)(outb + 2 * C * kWave);
+  char* rows = (char*)lds + dp_ctl_bytes<C>();
+  // wave 0 computes the sweep; wave 1 does every global-memory access of
+  // the batch loop, so the compute wave never waits on a memory counter
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  const int lane = threadIdx.x % kWave;
   char* lane_bytes = rows + lane * 8;
   const int blk = blockIdx.x;
   if (blk >= set.base[set.count]) return;
@@ -357,58 +374,138 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const int G = set.base[ci + 1] - set.base[ci];
   const int n = d.n;
   const int nsteps = (n + kBatch - 1) / kBatch * kBatch;
+  const int nb = nsteps / kBatch;
   const int pad = nsteps - n;  // leading dummy steps
-  const int64_t stride = (int64_t)d.npad;  // steps per stage row of the ring
-  const int64_t cstride = 2 * stride;      // choice words per (stage, cell)
-  const int64_t* __restrict__ prof = d.profit + slot * n;
-  const uint4* __restrict__ meta = (const uint4*)d.meta;  // [nsteps], padded
-  uint32_t* bits = (uint32_t*)d.bits + (slot * d.stages + g) * (int64_t)C * cstride;
-  uint64_t* ring_out = d.ring + (slot * d.stages + g) * stride * 2;
-  const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
-  const uint64_t tag = (uint64_t)epoch << 32;
-  const bool produce = g + 1 < G;
+  // Barrier between the two waves.  Only LDS is exchanged through it, so
+  // the fences order LDS alone (a wait on lgkmcnt, no wait on vmcnt).
+  auto barrier = [&]() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  };
+
+  if (wave == 1) {
+    // ---------------------------------------------------------- I/O wave
+    const int64_t stride = (int64_t)d.npad;  // steps per stage row of the ring
+    const int64_t cstride = 2 * stride;      // choice words per (stage, cell)
+    const int64_t* __restrict__ prof = d.profit + slot * n;
+    const uint4* __restrict__ meta = (const uint4*)d.meta;  // [nsteps], padded
+    uint32_t* bits = (uint32_t*)d.bits + (slot * d.stages + g) * (int64_t)C * cstride;
+    uint64_t* ring_out = d.ring + (slot * d.stages + g) * stride * 2;
+    const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
+    const uint64_t tag = (uint64_t)epoch << 32;
+    const bool produce = g + 1 < G;
+    // ring input of the batch at s0: lane u < kBatch <- entry s0+u-1
+    auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
+      const int e = s0 - 1 + lane;
+      w0 = tag;
+      w1 = tag;
+      if (ring_in && lane < kBatch && e >= 0 && s0 < nsteps) {
+        w0 = ld_agent(ring_in + 2 * (int64_t)e);
+        w1 = ld_agent(ring_in + 2 * (int64_t)e + 1);
+      }
+    };
+    auto ring_ok = [&](uint64_t w0, uint64_t w1) {
+      const bool ok = (w0 & 0xFFFFFFFF00000000ull) == tag &&
+                      (w1 & 0xFFFFFFFF00000000ull) == tag;
+      return __builtin_amdgcn_ballot_w64(ok) == ~0ull;
+    };
+    uint32_t spins = 0;
+    auto ring_wait = [&](int s0, uint64_t& w0, uint64_t& w1) -> bool {
+      while (!ring_ok(w0, w1)) {
+        if (++spins > spin_limit) return false;
+        __builtin_amdgcn_s_sleep(2);
+        ring_load(s0, w0, w1);
+      }
+      return true;
+    };
+    // profit of padded step t (0 for the leading dummy steps)
+    auto profit_at = [&](int t) -> int64_t {
+      const int s = t - pad;
+      return (lane < kBatch && s >= 0 && s < n) ? prof[n - 1 - s] : 0;
+    };
+    // lane kBatch carries the first step of the following batch, whose
+    // word 1 names the skip row the batch's last steps read ahead
+    auto meta_at = [&](int t) -> uint4 {
+      return (lane <= kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
+    };
+    auto stage = [&](int b, int64_t pv, uint64_t w0, uint64_t w1, uint4 mv) {
+      if (lane <= kBatch) {
+        StepRec r;
+        r.p = pv;
+        r.bnd = (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
+        r.st = mv.x;
+        r.pf = mv.y;
+        r.leaf = mv.z;
+        r.pad = 0;
+        recs[(b % 2) * (kBatch + 1) + lane] = r;
+      }
+    };
+    // the outputs of batch b, written by the compute wave before the barrier
+    auto store_out = [&](int b) {
+      if (store_bits) {
+        const int64_t wi = (int64_t)b * kWave + lane;
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+          bits[c * cstride + wi] = outb[((b % 2) * C + c) * kWave + lane];
+      }
+      if (produce && lane < kBatch) {
+        const uint64_t bo = (uint64_t)outv[(b % 2) * kBatch + lane];
+        const int idx = b * kBatch + lane;
+        st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
+        st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
+      }
+    };
+    if (lane == 0) {
+      abort_flag[0] = 0;
+      abort_flag[1] = 0;
+    }
+    bool ok;
+    {
+      uint64_t w0, w1;
+      ring_load(0, w0, w1);
+      ok = ring_wait(0, w0, w1);
+      stage(0, profit_at(lane), w0, w1, meta_at(lane));
+    }
+    // inputs of batch b+1, loaded during batch b-1 (ring words two batches
+    // ahead; the validation waits only on loads)
+    uint64_t a0, a1;
+    ring_load(kBatch, a0, a1);
+    int64_t pa = profit_at(kBatch + lane);
+    uint4 ma = meta_at(kBatch + lane);
+    if (!ok && lane == 0) abort_flag[0] = 1;
+    barrier();
+    bool aborted = false;
+    for (int b = 0; b < nb; ++b) {
+      if (abort_flag[b % 2]) {
+        aborted = true;
+        break;
+      }
+      if (b + 1 < nb) {
+        if (ring_wait((b + 1) * kBatch, a0, a1))
+          stage(b + 1, pa, a0, a1, ma);
+        else if (lane == 0)
+          abort_flag[(b + 1) % 2] = 1;
+        ring_load((b + 2) * kBatch, a0, a1);
+        pa = profit_at((b + 2) * kBatch + lane);
+        ma = meta_at((b + 2) * kBatch + lane);
+      }
+      if (b >= 1) store_out(b - 1);
+      barrier();
+    }
+    if (aborted) {
+      if (lane == 0) __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    store_out(nb - 1);
+    return;
+  }
+
+  // ------------------------------------------------------- compute wave
   const int zero_off = slots * kStride;
 #pragma unroll
   for (int c = 0; c < C; ++c) *(int64_t*)(lane_bytes + zero_off + c * kWave * 8) = 0;
-
-  // ring input of the batch at s0: lane u < kBatch <- entry s0+u-1
-  auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
-    const int e = s0 - 1 + lane;
-    w0 = tag;
-    w1 = tag;
-    if (ring_in && lane < kBatch && e >= 0 && s0 < nsteps) {
-      w0 = ld_agent(ring_in + 2 * (int64_t)e);
-      w1 = ld_agent(ring_in + 2 * (int64_t)e + 1);
-    }
-  };
-  auto ring_ok = [&](uint64_t w0, uint64_t w1) {
-    const bool ok = (w0 & 0xFFFFFFFF00000000ull) == tag &&
-                    (w1 & 0xFFFFFFFF00000000ull) == tag;
-    return __builtin_amdgcn_ballot_w64(ok) == ~0ull;
-  };
-  uint32_t spins = 0;
-  bool failed = false;
-  auto ring_wait = [&](int s0, uint64_t& w0, uint64_t& w1) {
-    while (!ring_ok(w0, w1)) {
-      if (++spins > spin_limit) {
-        failed = true;
-        return;
-      }
-      __builtin_amdgcn_s_sleep(2);
-      ring_load(s0, w0, w1);
-    }
-  };
-  // profit of padded step t (0 for the leading dummy steps)
-  auto profit_at = [&](int t) -> int64_t {
-    const int s = t - pad;
-    return (lane < kBatch && s >= 0 && s < n) ? prof[n - 1 - s] : 0;
-  };
-  // lane kBatch carries the first step of the following batch, whose word 0
-  // names the skip row the batch's last step reads ahead
-  auto meta_at = [&](int t) -> uint4 {
-    return (lane <= kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
-  };
-
   // x: the previous row D[i+1]; pre[u % 2]: the far skip row of step u,
   // read two steps ahead (padded steps 0 and 1 need none: step 0 is a leaf,
   // and a non-leaf step 1 skips to D[n+1], the zero row)
@@ -424,48 +521,14 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // gather: lane u < kBatch reads the last cell (lane 63, cell C-1) of the
   // row step u was stored to
   constexpr int kLastCell = (C - 1) * kWave * 8 + (kWave - 1) * 8;
-  // stage the records of the batch at s0 (profits, boundary values and
-  // metadata already in registers); returns the lane's gather address
-  auto stage = [&](int64_t pv, int64_t bv, uint4 mv) -> const char* {
-    if (lane <= kBatch) {
-      StepRec r;
-      r.p = pv;
-      r.bnd = bv;
-      r.st = mv.x;
-      r.pf = mv.y;
-      r.leaf = mv.z;
-      r.pad = 0;
-      rec[lane] = r;
-    }
-    return rows + mv.x + kLastCell;
-  };
-  auto join = [&](uint64_t w0, uint64_t w1) {
-    return (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
-  };
-  // ring words in flight: the set for batch t is loaded at the start of
-  // batch t-2 and validated at the end of batch t-1.  The batch loop is
-  // unrolled twice so that the two sets keep their registers (no copies of
-  // pending loads).
-  uint64_t ra0, ra1, rb0, rb1;
-  const char* gath_addr;
-  {
-    uint64_t w0, w1;
-    ring_load(0, w0, w1);
-    ring_wait(0, w0, w1);
-    gath_addr = stage(profit_at(lane), join(w0, w1), meta_at(lane));
-  }
-  ring_load(kBatch, rb0, rb1);  // batch 1
+  barrier();
 
-  // one batch at s0: `nw` receives the ring words of batch s0+2B, `vw`
-  // holds those of batch s0+B (validated at the end)
-  auto batch = [&](int s0, uint64_t& nw0, uint64_t& nw1, uint64_t& vw0,
-                   uint64_t& vw1) {
-    const int s1 = s0 + kBatch;
-    // the next batch's profits and metadata, staged at the end of this one
-    const int64_t pv_n = profit_at(s1 + lane);
-    const uint4 mv_n = meta_at(s1 + lane);
-    ring_load(s1 + kBatch, nw0, nw1);
-
+  // one batch; `buf` (0 or 1, a compile-time constant) selects the record
+  // and output buffers
+  auto batch = [&](auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
+    const StepRec* rec = recs + buf * (kBatch + 1);
+    const char* gath_addr = rows + (lane < kBatch ? rec[lane].st : 0u) + kLastCell;
     // records of steps u..u+3 in flight: {p, bnd} and {st, pf, leaf} (the
     // record of step kBatch is the next batch's first: only its pf is used;
     // the unused pad word is not loaded, so no loaded register is dead)
@@ -514,37 +577,32 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       for (int c = 0; c < C; ++c) x[c] = y[c];
     };
     unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
-    // the next batch first (its waits cover loads only), then this batch's
-    // stores, which complete during the next batch (stores count in vmcnt)
+    // hand the batch's outputs to the I/O wave
     int64_t v = gath[0];
 #pragma unroll
     for (int q = 1; q < kBatch / kProd; ++q)
       if (lane >= q * kProd) v = gath[q];
-    if (s1 < nsteps) {
-      ring_wait(s1, vw0, vw1);
-      gath_addr = stage(pv_n, join(vw0, vw1), mv_n);
-    }
-    if (store_bits) {
-      const int64_t wi = (int64_t)(s0 / kBatch) * kWave + lane;
+    if (lane < kBatch) outv[buf * kBatch + lane] = v;
 #pragma unroll
-      for (int c = 0; c < C; ++c) bits[c * cstride + wi] = acc[c];
-    }
-    if (produce && lane < kBatch) {
-      const uint64_t bo = (uint64_t)v;
-      const int idx = s0 + lane;
-      st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
-      st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
-    }
+    for (int c = 0; c < C; ++c) outb[(buf * C + c) * kWave + lane] = acc[c];
+    barrier();
   };
-  for (int s0 = 0; s0 < nsteps && !failed; s0 += 2 * kBatch) {
-    batch(s0, ra0, ra1, rb0, rb1);
-    if (s0 + kBatch < nsteps && !failed) batch(s0 + kBatch, rb0, rb1, ra0, ra1);
+  bool aborted = false;
+  for (int b = 0; b < nb; b += 2) {
+    if (abort_flag[0]) {
+      aborted = true;
+      break;
+    }
+    batch(IC<0>{});
+    if (b + 1 < nb) {
+      if (abort_flag[1]) {
+        aborted = true;
+        break;
+      }
+      batch(IC<1>{});
+    }
   }
-  if (failed) {
-    if (lane == 0) __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
-    return;
-  }
+  if (aborted) return;
   // D[1][k'] sits in stage (k'-1)/(64C), lane ((k'-1) mod 64C)/C, cell c.
   const int jj = kp - 1;
   if (jj / (kWave * C) == g) {
@@ -979,9 +1037,10 @@ hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) 
 }
 
 size_t dp_lds_bytes(int cells, int32_t slots_lds) {
-  // step records, then the slot rows, the zero row and the sink rows
-  return (kBatch + 1) * sizeof(StepRec) +
-         (size_t)(slots_lds + 1 + dp_sink_rows(cells)) * dp_row_stride(cells);
+  // control area, then the slot rows, the zero row and the sink rows
+  const size_t ctl = cells == 1 ? dp_ctl_bytes<1>() : cells == 2 ? dp_ctl_bytes<2>()
+                                                                 : dp_ctl_bytes<4>();
+  return ctl + (size_t)(slots_lds + 1 + dp_sink_rows(cells)) * dp_row_stride(cells);
 }
 
 template <int C, bool FMAX>
@@ -991,7 +1050,7 @@ static hipError_t dp_launch_c(const ChainSet& set, const DevState& d,
                               hipStream_t st) {
   const size_t lds = dp_lds_bytes(C, slots_lds);
   hipLaunchKernelGGL((k_dp<C, FMAX>), dim3((unsigned)set.base[set.count]),
-                     dim3(kWave), lds, st, set, d, epoch, spin_limit,
+                     dim3(2 * kWave), lds, st, set, d, epoch, spin_limit,
                      store_bits, slots_lds);
   return hipGetLastError();
 }
@@ -1015,9 +1074,9 @@ int dp_resident_blocks(int cells, int32_t slots_lds, int device) {
   const size_t lds = dp_lds_bytes(cells, slots_lds);
   hipError_t e = hipErrorInvalidValue;
   switch (cells) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1, false>, kWave, lds); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2, false>, kWave, lds); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4, false>, kWave, lds); break;
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1, false>, 2 * kWave, lds); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2, false>, 2 * kWave, lds); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4, false>, 2 * kWave, lds); break;
     default: return 0;
   }
   if (e != hipSuccess) return 0;
