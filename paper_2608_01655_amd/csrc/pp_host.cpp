@@ -456,7 +456,7 @@ int choose_cells(int32_t total_stage_cells_c1, int dev, int32_t slots_lds) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     cus = 256;
   const double simds = 4.0 * cus;
-  const struct { int c; double ns; } widths[] = {{1, 47.0}, {2, 61.0}, {4, 103.0}};
+  const struct { int c; double ns; } widths[] = {{1, 45.0}, {2, 61.0}, {4, 96.0}};
   int best = 0, most = 2, most_res = 0;
   double best_cost = 0.0;
   for (const auto& w : widths) {
@@ -770,10 +770,11 @@ int check_meta(const TreeLayout& t, const std::vector<uint32_t>& meta,
   for (size_t q = 0; q < meta.size(); q += kMetaWords) {
     const int64_t st = meta[q], pf = meta[q + 1];
     // stores go to a slot or a sink row, never to the zero row; reads come
-    // from a slot or the zero row
+    // from a slot or the zero row; the sweep packs both offsets, divided by
+    // 8, into the two 16-bit halves of one word
     const bool st_ok = st % row == 0 && (st / row < h ||
                                          (st / row > h && st / row <= h + dp_sink_rows(cells)));
-    if (!st_ok || pf % row != 0 || pf / row > h ||
+    if (!st_ok || pf % row != 0 || pf / row > h || st >= (8 << 16) || pf >= (8 << 16) ||
         (meta[q + 2] != 0u && meta[q + 2] != 0xFFFFFFFFu) || meta[q + 3] != 0u)
       return fail(PP_E_DEVICE, "internal: DP step metadata out of range");
   }

@@ -85,14 +85,6 @@ __device__ __forceinline__ int64_t join64(pp_int2 v) {
   return __builtin_bit_cast(int64_t, v);
 }
 
-// Lane l receives v from lane l-1 (DPP wave_shr:1); lane 0 receives `in0`.
-__device__ __forceinline__ int64_t shift_up(int64_t v, int64_t in0) {
-  const pp_int2 s = split64(v), o = split64(in0);
-  pp_int2 r;
-  r.x = __builtin_amdgcn_update_dpp(o.x, s.x, 0x138, 0xF, 0xF, false);
-  r.y = __builtin_amdgcn_update_dpp(o.y, s.y, 0x138, 0xF, 0xF, false);
-  return join64(r);
-}
 
 __device__ __forceinline__ uint64_t ld_agent(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -245,17 +237,6 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
 
 // ------------------------------------------------------------ DP sweep --
 
-// Bitwise select: bits of `a` where `mask` is set, else bits of `b` (one
-// v_bfi_b32 per half; the sweep's masks are all ones or all zeros).
-__device__ __forceinline__ int64_t select_bits(uint32_t mask, int64_t a,
-                                               int64_t b) {
-  const pp_int2 av = split64(a), bv = split64(b);
-  pp_int2 r;
-  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r.x) : "v"(mask), "v"(av.x), "v"(bv.x));
-  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r.y) : "v"(mask), "v"(av.y), "v"(bv.y));
-  return join64(r);
-}
-
 // acc * 2 + (t > sk): the lane's choice bit of this step shifted into its
 // 32-step word (the compare's lane mask is the add's carry-in).
 __device__ __forceinline__ uint32_t shift_in_gt(int64_t t, int64_t sk,
@@ -267,6 +248,56 @@ __device__ __forceinline__ uint32_t shift_in_gt(int64_t t, int64_t sk,
       : "vcc");
   return r;
 }
+
+// Take operands of a DP row: lanes 1..63 get r + v of lane l-1 (a 64-bit
+// add whose first operand is shifted in by DPP wave_shr:1); lane 0, whose
+// shifted operand is zero (bound_ctrl), gets r.  A DPP read of a VGPR needs
+// two wait states after the VALU write of that VGPR: take_after_bit puts
+// the previous step's choice bit (t_prev > sk_prev, shifted into acc; two
+// instructions) in front of the shift, take_first pads with s_nop.
+__device__ __forceinline__ int64_t take_after_bit(int64_t r, int64_t v, int64_t t_prev,
+                                                  int64_t sk_prev, uint32_t& acc) {
+  const pp_int2 rv = split64(r), vv = split64(v);
+  pp_int2 t;
+  asm("v_cmp_gt_i64 vcc, %3, %4\n\t"
+      "v_addc_co_u32_e32 %0, vcc, %0, %0, vcc\n\t"
+      "v_add_co_u32_dpp %1, vcc, %5, %7 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+      "v_addc_co_u32_dpp %2, vcc, %6, %8, vcc wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "+v"(acc), "=&v"(t.x), "=v"(t.y)
+      : "v"(t_prev), "v"(sk_prev), "v"(vv.x), "v"(vv.y), "v"(rv.x), "v"(rv.y)
+      : "vcc");
+  return join64(t);
+}
+
+__device__ __forceinline__ int64_t take_first(int64_t r, int64_t v) {
+  const pp_int2 rv = split64(r), vv = split64(v);
+  pp_int2 t;
+  asm("s_nop 1\n\t"
+      "v_add_co_u32_dpp %0, vcc, %2, %4 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+      "v_addc_co_u32_dpp %1, vcc, %3, %5, vcc wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+      : "=&v"(t.x), "=v"(t.y)
+      : "v"(vv.x), "v"(vv.y), "v"(rv.x), "v"(rv.y)
+      : "vcc");
+  return join64(t);
+}
+
+// LDS byte address of a row cell: base + 8 * (low or high 16-bit half of w),
+// one v_mad_u32_u16 (op_sel picks the high half).
+__device__ __forceinline__ uint32_t lds_row_lo(uint32_t w, uint32_t base) {
+  uint32_t a;
+  asm("v_mad_u32_u16 %0, %1, 8, %2" : "=v"(a) : "v"(w), "v"(base));
+  return a;
+}
+
+__device__ __forceinline__ uint32_t lds_row_hi(uint32_t w, uint32_t base) {
+  uint32_t a;
+  asm("v_mad_u32_u16 %0, %1, 8, %2 op_sel:[1,0,0,0]" : "=v"(a) : "v"(w), "v"(base));
+  return a;
+}
+
+typedef __attribute__((address_space(3))) int64_t lds_i64;
+
+__device__ __forceinline__ lds_i64* lds_at(uint32_t a) { return (lds_i64*)(size_t)a; }
 
 // Maximum of two non-negative int64 values below 2^62 with one v_max_f64:
 // such bit patterns are finite non-negative doubles (denormals included,
@@ -284,11 +315,13 @@ __device__ __forceinline__ int64_t max_nonneg_f64(int64_t a, int64_t b) {
 //   D[i][j] = max(D[next(i)][j], p(b_i) + D[i+1][j-1]),  D[n+1][*] = 0,
 //   D[*][0] = 0;  choice bit = (take > skip)  (ties keep the skip branch).
 //
-// Layout: a chain's k' cells are split over G stages; stage g is one wave64
-// block owning cells j = g*64*C + l*C + c + 1 (lane l, c < C).  Row i+1
-// stays in registers.  The take operand D[i+1][j-1] comes from the left
-// neighbour lane by a DPP shift; lane 0 gets it from stage g-1, whose last
-// cell of every row is published through a per-step ring in global memory.
+// Layout: a chain's k' cells are split over G stages; stage g is a block
+// of two waves owning cells j = g*64*C + l*C + c + 1 (lane l, c < C) of
+// the compute wave.  Row i+1 stays in its registers.  The take operand
+// p + D[i+1][j-1] is one add whose D operand comes from the left neighbour
+// lane by DPP; lane 0's comes from stage g-1, whose last cell of every row
+// is published through a per-step ring in global memory, and is added to p
+// by the other wave, which does all global-memory traffic of the stage.
 // Ring words carry a launch tag in their high half (relaxed agent-scope
 // atomics, no fences): a consumer validates each word by its tag.  A stage
 // loads its input two batches ahead, so in steady state it runs two
@@ -307,22 +340,26 @@ __device__ __forceinline__ int64_t max_nonneg_f64(int64_t a, int64_t b) {
 //
 // Steps run in batches of kBatch, unrolled at compile time; the step count
 // is padded up to a multiple of kBatch with leading dummy steps (profit 0,
-// leaf, rows stay all-zero).  Per batch each lane stages one step's record
-// -- profit, boundary value and the step's metadata words -- in LDS, read
-// back per step with two broadcast loads.  Each lane shifts its cells'
+// leaf, rows stay all-zero).  Per batch the I/O wave stages each step's
+// record -- profit (plus the boundary value for lane 0), the packed row
+// offsets and the leaf mask -- in LDS, read back by the compute wave with
+// one load per step (and, for C > 1, a broadcast load of p).  The two
+// waves meet at one barrier per batch.  Each lane shifts its cells'
 // choice bits into one 32-bit word per cell per batch (bit 31-u = step u),
 // stored with one coalesced store per cell; the stage ring output also
 // leaves with one store per batch.  No per-row launch, barrier or HBM row
 // traffic.
 constexpr int kBatch = kDpBatch;
 
-struct __attribute__((aligned(16))) StepRec {
-  int64_t p;      // profit of the step's node
-  int64_t bnd;    // D[i+1][first cell - 1] from stage g-1 (0 for stage 0)
-  uint32_t st;    // byte offset of the row this step is stored to
-  uint32_t pf;    // byte offset of the next step's skip row
+// A step's record in two 16-byte views: lanes 1..63 read view 0, lane 0
+// reads view 1, with one LDS read per step.
+struct __attribute__((aligned(16))) StepView {
+  int64_t r;      // view 0: the profit p of the step's node; view 1: p plus
+                  // D[i+1][first cell - 1] from stage g-1 (0 for stage 0),
+                  // lane 0's take operand
+  uint32_t rows;  // low half: byte offset of the row this step is stored
+                  // to, high half: of the next step's skip row; both / 8
   uint32_t leaf;  // all ones when the step's node is a leaf, else zero
-  uint32_t pad;
 };
 
 template <int U>
@@ -337,7 +374,7 @@ __device__ __forceinline__ void unroll_steps(F&& f, std::integer_sequence<int, U
 // buffers (stage-ring values and choice words of a batch) and a flag word.
 template <int C>
 constexpr size_t dp_ctl_bytes() {
-  return 2 * (kBatch + 1) * sizeof(StepRec) + 2 * kBatch * sizeof(int64_t) +
+  return 2 * (kBatch + 1) * 2 * sizeof(StepView) + 2 * kBatch * sizeof(int64_t) +
          2 * C * kWave * sizeof(uint32_t) + 16;
 }
 
@@ -351,13 +388,21 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   static_assert(kBatch % kProd == 0 && kProd <= kDpGatherMax, "gather groups");
   // control area first (small immediate offsets), then the rows: the slots,
   // the zero row and the sink rows
-  StepRec* recs = (StepRec*)lds;                               // [2][kBatch + 1]
-  int64_t* outv = (int64_t*)(recs + 2 * (kBatch + 1));         // [2][kBatch]
+  StepView* recs = (StepView*)lds;                             // [2][kBatch + 1][2]
+  int64_t* outv = (int64_t*)(recs + 2 * (kBatch + 1) * 2);     // [2][kBatch]
   uint32_t* outb = (uint32_t*)(outv + 2 * kBatch);             // [2][C][64]
   // abort[t % 2]: set by the I/O wave between the barriers before and
   // after batch t-1, read by both waves right after the barrier before
   // batch t (alternating words, so a later write cannot race that read)
-  volatile int* abort_flag = (volatile int*)(outb + 2 * C * kWave);
+  int* abort_flag = (int*)(outb + 2 * C * kWave);
+  // relaxed workgroup-scope accesses (ds_read/ds_write; the barrier's
+  // fences order them)
+  auto flag_get = [&](int t) {
+    return __hip_atomic_load(abort_flag + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  };
+  auto flag_set = [&](int t, int v) {
+    __hip_atomic_store(abort_flag + t, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  };
   char* rows = (char*)lds + dp_ctl_bytes<C>();
   // wave 0 computes the sweep; wave 1 does every global-memory access of
   // the batch loop, so the compute wave never waits on a memory counter
@@ -431,14 +476,15 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     };
     auto stage = [&](int b, int64_t pv, uint64_t w0, uint64_t w1, uint4 mv) {
       if (lane <= kBatch) {
-        StepRec r;
-        r.p = pv;
-        r.bnd = (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
-        r.st = mv.x;
-        r.pf = mv.y;
-        r.leaf = mv.z;
-        r.pad = 0;
-        recs[(b % 2) * (kBatch + 1) + lane] = r;
+        const int64_t bnd = (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
+        StepView v;
+        v.r = pv;
+        v.rows = (mv.x >> 3) | ((mv.y >> 3) << 16);
+        v.leaf = mv.z;
+        StepView* dst = recs + ((b % 2) * (kBatch + 1) + lane) * 2;
+        dst[0] = v;
+        v.r = pv + bnd;  // no overflow: a feasible set's value
+        dst[1] = v;
       }
     };
     // the outputs of batch b, written by the compute wave before the barrier
@@ -457,8 +503,8 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       }
     };
     if (lane == 0) {
-      abort_flag[0] = 0;
-      abort_flag[1] = 0;
+      flag_set(0, 0);
+      flag_set(1, 0);
     }
     bool ok;
     {
@@ -473,11 +519,11 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     ring_load(kBatch, a0, a1);
     int64_t pa = profit_at(kBatch + lane);
     uint4 ma = meta_at(kBatch + lane);
-    if (!ok && lane == 0) abort_flag[0] = 1;
+    if (!ok && lane == 0) flag_set(0, 1);
     barrier();
     bool aborted = false;
     for (int b = 0; b < nb; ++b) {
-      if (abort_flag[b % 2]) {
+      if (flag_get(b % 2)) {
         aborted = true;
         break;
       }
@@ -485,7 +531,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         if (ring_wait((b + 1) * kBatch, a0, a1))
           stage(b + 1, pa, a0, a1, ma);
         else if (lane == 0)
-          abort_flag[(b + 1) % 2] = 1;
+          flag_set((b + 1) % 2, 1);
         ring_load((b + 2) * kBatch, a0, a1);
         pa = profit_at((b + 2) * kBatch + lane);
         ma = meta_at((b + 2) * kBatch + lane);
@@ -523,21 +569,31 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   constexpr int kLastCell = (C - 1) * kWave * 8 + (kWave - 1) * 8;
   barrier();
 
+  // LDS address of this lane's cell 0 in row offset 0 (rows are addressed
+  // as this plus a row's byte offset)
+  const uint32_t lane_base =
+      (uint32_t)(size_t)(__attribute__((address_space(3))) char*)lane_bytes;
+  // t, sk of the previous step, whose choice bits are shifted into acc at
+  // the start of the next step
+  int64_t tp[C], skp[C];
+
   // one batch; `buf` (0 or 1, a compile-time constant) selects the record
   // and output buffers
   auto batch = [&](auto bufc) {
     constexpr int buf = decltype(bufc)::value;
-    const StepRec* rec = recs + buf * (kBatch + 1);
-    const char* gath_addr = rows + (lane < kBatch ? rec[lane].st : 0u) + kLastCell;
-    // records of steps u..u+3 in flight: {p, bnd} and {st, pf, leaf} (the
-    // record of step kBatch is the next batch's first: only its pf is used;
-    // the unused pad word is not loaded, so no loaded register is dead)
+    const StepView* rec = recs + buf * (kBatch + 1) * 2;
+    const char* view = (const char*)rec + (lane == 0 ? sizeof(StepView) : 0);
+    const char* gath_addr =
+        rows + (lane < kBatch ? (rec[2 * lane].rows & 0xFFFFu) * 8u : 0u) + kLastCell;
+    // records of steps u..u+3 in flight (the record of step kBatch is the
+    // next batch's first: only its skip-row half is used); wider rows also
+    // read p for cells 1..C-1 (lane 0's view holds p plus the boundary)
     constexpr int kRq = 4;
-    pp_i64x2 rv[kRq];
-    pp_u32x3 rm[kRq];
+    pp_u32x4 rv[kRq];
+    int64_t pv[kRq];
     auto rec_load = [&](int t, int q) {
-      rv[q] = *(const pp_i64x2*)&rec[t];
-      rm[q] = *(const pp_u32x3*)&rec[t].st;
+      rv[q] = *(const pp_u32x4*)(view + 2 * sizeof(StepView) * t);
+      if constexpr (C > 1) pv[q] = rec[2 * t].r;
     };
     rec_load(0, 0);
     rec_load(1, 1);
@@ -546,37 +602,55 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     auto step = [&](auto uc) {
       constexpr int u = decltype(uc)::value;
       if constexpr (u + 3 <= kBatch) rec_load(u + 3, (u + 3) % kRq);
-      const int64_t cur_p = rv[u % kRq].x, cur_bnd = rv[u % kRq].y;
-      const uint32_t cur_st = rm[u % kRq].x, cur_leaf = rm[u % kRq].z;
-      const int64_t left = shift_up(x[C - 1], cur_bnd);
-      int64_t y[C];
+      const pp_u32x4 r = rv[u % kRq];
+      const int64_t r0 = (int64_t)(((uint64_t)r.y << 32) | r.x);
+      const uint64_t leaf = ((uint64_t)r.w << 32) | r.w;
+      int64_t t[C], sk[C], y[C];
+      // cell 0's take operand comes from the left lane (lane 0: r0 already
+      // holds it); the previous step's choice bits go in first
+      if constexpr (u == 0)
+        t[0] = take_first(r0, x[C - 1]);
+      else
+        t[0] = take_after_bit(r0, x[C - 1], tp[0], skp[0], acc[0]);
+#pragma unroll
+      for (int c = 1; c < C; ++c) {
+        if constexpr (u > 0) acc[c] = shift_in_gt(tp[c], skp[c], acc[c]);
+        t[c] = pv[u % kRq] + x[c - 1];
+      }
 #pragma unroll
       for (int c = 0; c < C; ++c) {
-        const int64_t sk = select_bits(cur_leaf, x[c], pre[u % 2][c]);
-        const int64_t t = cur_p + (c == 0 ? left : x[c - 1]);
-        acc[c] = shift_in_gt(t, sk, acc[c]);
+        sk[c] = (int64_t)(((uint64_t)x[c] & leaf) | ((uint64_t)pre[u % 2][c] & ~leaf));
         if constexpr (FMAX)
-          y[c] = max_nonneg_f64(sk, t);
+          y[c] = max_nonneg_f64(sk[c], t[c]);
         else
-          y[c] = t > sk ? t : sk;
+          y[c] = t[c] > sk[c] ? t[c] : sk[c];
       }
       // the row goes to its slot if it is a later skip target, else to a
       // sink row
-#pragma unroll
-      for (int c = 0; c < C; ++c)
-        *(int64_t*)(lane_bytes + cur_st + c * kWave * 8) = y[c];
-      // skip row of step u+2 (word 1 of step u+1), read after this store:
-      // it is row i-2's next(), produced at this step at the latest
       {
-        const char* prow = lane_bytes + rm[(u + 1) % kRq].y;
+        lds_i64* dst = lds_at(lds_row_lo(r.z, lane_base));
 #pragma unroll
-        for (int c = 0; c < C; ++c) pre[u % 2][c] = *(const int64_t*)(prow + c * kWave * 8);
+        for (int c = 0; c < C; ++c) dst[c * kWave] = y[c];
+      }
+      // skip row of step u+2 (high half of step u+1's rows word), read after
+      // this store: it is row i-2's next(), produced at this step at the latest
+      {
+        const lds_i64* src = lds_at(lds_row_hi(rv[(u + 1) % kRq].z, lane_base));
+#pragma unroll
+        for (int c = 0; c < C; ++c) pre[u % 2][c] = src[c * kWave];
       }
       if constexpr (u % kProd == kProd - 1) gath[u / kProd] = *(const int64_t*)gath_addr;
 #pragma unroll
-      for (int c = 0; c < C; ++c) x[c] = y[c];
+      for (int c = 0; c < C; ++c) {
+        tp[c] = t[c];
+        skp[c] = sk[c];
+        x[c] = y[c];
+      }
     };
     unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
+    // choice bits of the batch's last step
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] = shift_in_gt(tp[c], skp[c], acc[c]);
     // hand the batch's outputs to the I/O wave
     int64_t v = gath[0];
 #pragma unroll
@@ -589,13 +663,13 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   };
   bool aborted = false;
   for (int b = 0; b < nb; b += 2) {
-    if (abort_flag[0]) {
+    if (flag_get(0)) {
       aborted = true;
       break;
     }
     batch(IC<0>{});
     if (b + 1 < nb) {
-      if (abort_flag[1]) {
+      if (flag_get(1)) {
         aborted = true;
         break;
       }
