@@ -391,17 +391,26 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   StepView* recs = (StepView*)lds;                             // [2][kBatch + 1][2]
   int64_t* outv = (int64_t*)(recs + 2 * (kBatch + 1) * 2);     // [2][kBatch]
   uint32_t* outb = (uint32_t*)(outv + 2 * kBatch);             // [2][C][64]
-  // abort[t % 2]: set by the I/O wave between the barriers before and
-  // after batch t-1, read by both waves right after the barrier before
-  // batch t (alternating words, so a later write cannot race that read)
-  int* abort_flag = (int*)(outb + 2 * C * kWave);
-  // relaxed workgroup-scope accesses (ds_read/ds_write; the barrier's
-  // fences order them)
-  auto flag_get = [&](int t) {
-    return __hip_atomic_load(abort_flag + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  // Hand-off between the waves through two LDS counters: sync[kStaged] =
+  // batches whose records are staged (-1: the I/O wave gave up), sync[kDone]
+  // = batches the compute wave has finished (their outputs are in LDS and
+  // their record buffer is free; -1: it gave up).  A wave's LDS operations
+  // execute in order, so LDS data written before a counter update is in
+  // place for a wave that reads the counter and then the data; compiler
+  // fences keep that program order, and no wave waits on the LDS counter.
+  int* sync = (int*)(outb + 2 * C * kWave);
+  constexpr int kStaged = 0, kDone = 1;
+  // bound on the polls of one LDS wait (the partner wave's own waits are
+  // bounded, so this is reached only if the hand-off itself breaks)
+  constexpr uint32_t kLdsSpins = 1u << 24;
+  auto sync_load = [&](int t) {
+    return __hip_atomic_load(sync + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   };
-  auto flag_set = [&](int t, int v) {
-    __hip_atomic_store(abort_flag + t, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  auto sync_get = [&](int t) { return __builtin_amdgcn_readfirstlane(sync_load(t)); };
+  auto sync_set = [&](int t, int v) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (threadIdx.x % kWave == 0)
+      __hip_atomic_store(sync + t, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   };
   char* rows = (char*)lds + dp_ctl_bytes<C>();
   // wave 0 computes the sweep; wave 1 does every global-memory access of
@@ -421,8 +430,8 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const int nsteps = (n + kBatch - 1) / kBatch * kBatch;
   const int nb = nsteps / kBatch;
   const int pad = nsteps - n;  // leading dummy steps
-  // Barrier between the two waves.  Only LDS is exchanged through it, so
-  // the fences order LDS alone (a wait on lgkmcnt, no wait on vmcnt).
+  // Barrier between the two waves (once, after set-up).  Only LDS is
+  // exchanged through it, so the fences order LDS alone.
   auto barrier = [&]() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
@@ -440,12 +449,13 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     const uint64_t* ring_in = (g > 0) ? ring_out - stride * 2 : nullptr;
     const uint64_t tag = (uint64_t)epoch << 32;
     const bool produce = g + 1 < G;
-    // ring input of the batch at s0: lane u < kBatch <- entry s0+u-1
+    // ring input of the batch at s0: lane u <= kBatch <- entry s0+u-1 (lane
+    // kBatch: the following batch's first step, in the same producer batch)
     auto ring_load = [&](int s0, uint64_t& w0, uint64_t& w1) {
       const int e = s0 - 1 + lane;
       w0 = tag;
       w1 = tag;
-      if (ring_in && lane < kBatch && e >= 0 && s0 < nsteps) {
+      if (ring_in && lane <= kBatch && e >= 0 && s0 < nsteps) {
         w0 = ld_agent(ring_in + 2 * (int64_t)e);
         w1 = ld_agent(ring_in + 2 * (int64_t)e + 1);
       }
@@ -464,13 +474,14 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       }
       return true;
     };
-    // profit of padded step t (0 for the leading dummy steps)
+    // profit of padded step t (0 for the leading dummy steps and past the
+    // end)
     auto profit_at = [&](int t) -> int64_t {
       const int s = t - pad;
-      return (lane < kBatch && s >= 0 && s < n) ? prof[n - 1 - s] : 0;
+      return (lane <= kBatch && s >= 0 && s < n) ? prof[n - 1 - s] : 0;
     };
-    // lane kBatch carries the first step of the following batch, whose
-    // word 1 names the skip row the batch's last steps read ahead
+    // lane kBatch carries the first step of the following batch: a batch's
+    // record kBatch is the following batch's record 0
     auto meta_at = [&](int t) -> uint4 {
       return (lane <= kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
     };
@@ -487,7 +498,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         dst[1] = v;
       }
     };
-    // the outputs of batch b, written by the compute wave before the barrier
+    // the outputs of batch b, in LDS once sync[kDone] > b
     auto store_out = [&](int b) {
       if (store_bits) {
         const int64_t wi = (int64_t)b * kWave + lane;
@@ -502,10 +513,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
       }
     };
-    if (lane == 0) {
-      flag_set(0, 0);
-      flag_set(1, 0);
-    }
+    if (lane == 0) sync[kDone] = 0;
     bool ok;
     {
       uint64_t w0, w1;
@@ -519,32 +527,57 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     ring_load(kBatch, a0, a1);
     int64_t pa = profit_at(kBatch + lane);
     uint4 ma = meta_at(kBatch + lane);
-    if (!ok && lane == 0) flag_set(0, 1);
+    if (lane == 0) sync[kStaged] = ok ? 1 : -1;
     barrier();
-    bool aborted = false;
-    for (int b = 0; b < nb; ++b) {
-      if (flag_get(b % 2)) {
-        aborted = true;
+    // While the compute wave runs: publish each finished batch's outputs at
+    // once (the next stage waits on them), and stage the next batch once
+    // the compute wave has released its record buffer (batch nstage-2 done)
+    // and its ring input (loaded when the previous batch was staged) is valid.
+    int nstore = 0, nstage = 1;
+    uint32_t idle = 0;
+    while (ok && nstore < nb) {
+      const int done = sync_get(kDone);
+      if (done < 0) {
+        ok = false;
         break;
       }
-      if (b + 1 < nb) {
-        if (ring_wait((b + 1) * kBatch, a0, a1))
-          stage(b + 1, pa, a0, a1, ma);
-        else if (lane == 0)
-          flag_set((b + 1) % 2, 1);
-        ring_load((b + 2) * kBatch, a0, a1);
-        pa = profit_at((b + 2) * kBatch + lane);
-        ma = meta_at((b + 2) * kBatch + lane);
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      bool progress = false;
+      if (done > nstore) {
+        store_out(nstore);
+        ++nstore;
+        progress = true;
       }
-      if (b >= 1) store_out(b - 1);
-      barrier();
+      if (nstage < nb && done >= nstage - 1) {
+        if (ring_ok(a0, a1)) {
+          stage(nstage, pa, a0, a1, ma);
+          sync_set(kStaged, nstage + 1);
+          ++nstage;
+          ring_load(nstage * kBatch, a0, a1);
+          pa = profit_at(nstage * kBatch + lane);
+          ma = meta_at(nstage * kBatch + lane);
+          progress = true;
+        } else if (++spins > spin_limit) {
+          ok = false;
+          break;
+        } else {
+          ring_load(nstage * kBatch, a0, a1);
+        }
+      }
+      if (progress) {
+        idle = 0;
+      } else {
+        if (++idle > kLdsSpins) {
+          ok = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
     }
-    if (aborted) {
-      if (lane == 0) __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-    store_out(nb - 1);
+    if (ok) return;
+    sync_set(kStaged, -1);
+    if (lane == 0)
+      __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
 
@@ -576,32 +609,76 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // t, sk of the previous step, whose choice bits are shifted into acc at
   // the start of the next step
   int64_t tp[C], skp[C];
+  // Records of steps u..u+3 in flight, in a ring of kRq register sets that
+  // runs across batches (kRq divides kBatch): a batch's record kBatch is
+  // the next batch's record 0, and records 1 and 2 of the next batch are
+  // read from its buffer after the staged count, a few steps ahead.  Wider
+  // rows also read p for cells 1..C-1 (lane 0's view holds p plus the
+  // boundary value).
+  constexpr int kRq = 4;
+  static_assert(kBatch % kRq == 0, "record ring");
+  pp_u32x4 rv[kRq];
+  int64_t pv[kRq];
+  int staged_v;  // the staged count as loaded (made uniform where checked)
+  auto view_of = [&](int buf) {
+    return (const char*)(recs + buf * (kBatch + 1) * 2) + (lane == 0 ? sizeof(StepView) : 0);
+  };
+  auto rec_load = [&](int buf, int t) {
+    rv[t % kRq] = *(const pp_u32x4*)(view_of(buf) + 2 * sizeof(StepView) * t);
+    if constexpr (C > 1) pv[t % kRq] = recs[(buf * (kBatch + 1) + t) * 2].r;
+  };
+  staged_v = sync_load(kStaged);  // 1, or -1 if staging batch 0 failed
+  rec_load(0, 0);
+  rec_load(0, 1);
+  rec_load(0, 2);
 
-  // one batch; `buf` (0 or 1, a compile-time constant) selects the record
-  // and output buffers
-  auto batch = [&](auto bufc) {
+  // one batch; `buf` (b % 2, a compile-time constant) selects the record
+  // and output buffers.  Returns false if the I/O wave gave up.
+  auto batch = [&](auto bufc, int b) -> bool {
     constexpr int buf = decltype(bufc)::value;
+    {
+      int staged = __builtin_amdgcn_readfirstlane(staged_v);
+      if (staged < b + 1) {
+        // not staged when records 1 and 2 were read: wait, then read again
+        uint32_t polls = 0;
+        while (staged >= 0 && staged < b + 1) {
+          if (++polls > kLdsSpins) {
+            if (lane == 0)
+              __hip_atomic_store(&d.cs[slot].status, 1, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+            staged = -1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+          staged = sync_get(kStaged);
+        }
+        if (staged < b + 1) return false;
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        rec_load(buf, 1);
+        rec_load(buf, 2);
+      }
+    }
     const StepView* rec = recs + buf * (kBatch + 1) * 2;
-    const char* view = (const char*)rec + (lane == 0 ? sizeof(StepView) : 0);
-    const char* gath_addr =
-        rows + (lane < kBatch ? (rec[2 * lane].rows & 0xFFFFu) * 8u : 0u) + kLastCell;
-    // records of steps u..u+3 in flight (the record of step kBatch is the
-    // next batch's first: only its skip-row half is used); wider rows also
-    // read p for cells 1..C-1 (lane 0's view holds p plus the boundary)
-    constexpr int kRq = 4;
-    pp_u32x4 rv[kRq];
-    int64_t pv[kRq];
-    auto rec_load = [&](int t, int q) {
-      rv[q] = *(const pp_u32x4*)(view + 2 * sizeof(StepView) * t);
-      if constexpr (C > 1) pv[q] = rec[2 * t].r;
-    };
-    rec_load(0, 0);
-    rec_load(1, 1);
-    rec_load(2, 2);
+    // gather: lane u < kBatch reads the last cell of the row step u was
+    // stored to (its rows word now, the address where it is used)
+    const uint32_t gath_w = lane < kBatch ? rec[2 * lane].rows : 0u;
+    const uint32_t gath_base = lane_base - lane * 8 + kLastCell;
+    uint32_t gath_a = 0;
     int64_t gath[kBatch / kProd];  // lane u: last cell of step u's row
     auto step = [&](auto uc) {
       constexpr int u = decltype(uc)::value;
-      if constexpr (u + 3 <= kBatch) rec_load(u + 3, (u + 3) % kRq);
+      if constexpr (u + 3 < kBatch) {
+        rec_load(buf, u + 3);
+      } else if constexpr (u + 3 == kBatch) {
+        rec_load(buf, kBatch);  // = the next batch's record 0
+      } else {
+        // records 1, 2 of the next batch, after the staged count
+        if constexpr (u + 3 == kBatch + 1) {
+          staged_v = sync_load(kStaged);
+          __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        }
+        rec_load(1 - buf, u + 3 - kBatch);
+      }
       const pp_u32x4 r = rv[u % kRq];
       const int64_t r0 = (int64_t)(((uint64_t)r.y << 32) | r.x);
       const uint64_t leaf = ((uint64_t)r.w << 32) | r.w;
@@ -639,7 +716,10 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
 #pragma unroll
         for (int c = 0; c < C; ++c) pre[u % 2][c] = src[c * kWave];
       }
-      if constexpr (u % kProd == kProd - 1) gath[u / kProd] = *(const int64_t*)gath_addr;
+      if constexpr (u % kProd == kProd - 1) {
+        if constexpr (u == kProd - 1) gath_a = lds_row_lo(gath_w, gath_base);
+        gath[u / kProd] = *lds_at(gath_a);
+      }
 #pragma unroll
       for (int c = 0; c < C; ++c) {
         tp[c] = t[c];
@@ -652,31 +732,25 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[c] = shift_in_gt(tp[c], skp[c], acc[c]);
     // hand the batch's outputs to the I/O wave
+#pragma unroll
+    for (int c = 0; c < C; ++c) outb[(buf * C + c) * kWave + lane] = acc[c];
     int64_t v = gath[0];
 #pragma unroll
     for (int q = 1; q < kBatch / kProd; ++q)
       if (lane >= q * kProd) v = gath[q];
     if (lane < kBatch) outv[buf * kBatch + lane] = v;
-#pragma unroll
-    for (int c = 0; c < C; ++c) outb[(buf * C + c) * kWave + lane] = acc[c];
-    barrier();
+    sync_set(kDone, b + 1);
+    return true;
   };
-  bool aborted = false;
-  for (int b = 0; b < nb; b += 2) {
-    if (flag_get(0)) {
-      aborted = true;
-      break;
-    }
-    batch(IC<0>{});
-    if (b + 1 < nb) {
-      if (flag_get(1)) {
-        aborted = true;
-        break;
-      }
-      batch(IC<1>{});
-    }
+  bool ok = true;
+  for (int b = 0; ok && b < nb; b += 2) {
+    ok = batch(IC<0>{}, b);
+    if (ok && b + 1 < nb) ok = batch(IC<1>{}, b + 1);
   }
-  if (aborted) return;
+  if (!ok) {
+    sync_set(kDone, -1);
+    return;
+  }
   // D[1][k'] sits in stage (k'-1)/(64C), lane ((k'-1) mod 64C)/C, cell c.
   const int jj = kp - 1;
   if (jj / (kWave * C) == g) {
