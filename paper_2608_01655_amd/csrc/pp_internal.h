@@ -72,6 +72,9 @@ struct DevState {
   const int64_t* w;         // [m][n]     recompute cost, preorder
   const int64_t* f;         // [m][m][n]  fetch cost [src][dst][pos]
   const int32_t* nextpos;   // [n]        0-based first position after subtree
+  const uint32_t* chain;    // [n]        backtrack skip chain of q in its
+                            //            32-row window (bit per row)
+  const int32_t* exitr;     // [n]        first row of that chain past the window
   const uint32_t* meta;     // [nsteps][4] per-step DP metadata
   uint8_t* tgt;             // [slots][m][n] placement, preorder
   int64_t* v1;              // [slots][m][n] best holder saving

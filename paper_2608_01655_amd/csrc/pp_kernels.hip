@@ -68,9 +68,6 @@ __device__ void refresh_holders(const DevState& d, int64_t s, int64_t i) {
   }
 }
 
-__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
-  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
-}
 
 typedef int pp_int2 __attribute__((ext_vector_type(2)));
 typedef int64_t pp_i64x2 __attribute__((ext_vector_type(2)));
@@ -773,112 +770,132 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
 extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
     "llvm.amdgcn.writelane.i32");
 
-// The walk inside one 32-row window for one cell per lane, in scalar code:
-// row q = wlo + r, column word W = lane `rem` of `wc` (bit r = choice of row
-// q), next(q) = lane r of `nx`.  A set bit takes b_q (q+1, rem-1) and marks
-// bit r of `tm`; a clear bit jumps to next(q).  Runs while q stays in
-// [wlo, wlo + lim) and rem >= 0.  The entry state must satisfy both; every
-// step raises q (next(q) > q), so the loop ends within lim steps.
-__device__ __forceinline__ void walk_window_c1(uint32_t& q, int& rem, uint32_t& tm,
-                                               uint32_t wlo, uint32_t lim,
-                                               uint32_t wc, uint32_t nx) {
-  uint32_t r, w, nq, bm, qp;
-  asm volatile(
-      "1:\n\t"
-      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-      "v_readlane_b32 %[w], %[wc], %[rem]\n\t"
-      "v_readlane_b32 %[nq], %[nx], %[r]\n\t"
-      "s_lshl_b32 %[bm], 1, %[r]\n\t"
-      "s_add_u32 %[qp], %[q], 1\n\t"
-      "s_and_b32 %[w], %[w], %[bm]\n\t"      // SCC = take
-      "s_cselect_b32 %[q], %[qp], %[nq]\n\t"
-      "s_cselect_b32 %[bm], %[bm], 0\n\t"
-      "s_subb_u32 %[rem], %[rem], 0\n\t"     // rem -= take
-      "s_or_b32 %[tm], %[tm], %[bm]\n\t"
-      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-      "s_cmp_lt_u32 %[r], %[lim]\n\t"
-      "s_cselect_b32 %[r], %[rem], -1\n\t"
-      "s_cmp_ge_i32 %[r], 0\n\t"
-      "s_cbranch_scc1 1b"
-      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [r] "=&s"(r), [w] "=&s"(w),
-        [nq] "=&s"(nq), [bm] "=&s"(bm), [qp] "=&s"(qp)
-      : [wlo] "s"(wlo), [lim] "s"(lim), [wc] "v"(wc), [nx] "v"(nx)
-      : "scc");
+// The backtrack walk through one staged super-window, in scalar code.
+// Row sets of 32 consecutive rows (windows) are staged in LDS: for window k
+// and lane l, the chain mask and exit row of row q_lo + 32k + (l mod 32) at
+// ace + 256k (exit at +4), and lane l's choice word of cell c at
+// aw + 256(Ck + c).  Each pass over window wk loads those, then finds the
+// takes: the next take is the lowest set bit of (word of cell rem & chain
+// mask of q); it is recorded (bit of tm), the walk moves to the row after
+// it and to cell rem-1.  Without a set bit the walk leaves the window at
+// the chain's exit row.  When the window changes, tm goes to lane wk of tw
+// and is cleared.  The walk returns when q reaches n, when rem wraps below
+// zero (it leaves the stage), or when q leaves the super-window (wk >= 16).
+// On entry wk < 16, q lies in window wk, rem >= 0 and q < n.  Every pass
+// raises q, so each window takes at most 32 passes.
+#define PP_WALK_SW(LOADW, COLWORD)                               \
+  "10:\n\t"                                                      \
+  "s_lshl_b32 %[off], %[wk], 8\n\t"                              \
+  "v_add_u32_e32 %[va], %[off], %[ace]\n\t"                      \
+  "ds_read_b32 %[ch], %[va]\n\t"                                 \
+  "ds_read_b32 %[ex], %[va] offset:4\n\t"                        \
+  LOADW                                                          \
+  "s_lshl_b32 %[wlo], %[wk], 5\n\t"                              \
+  "s_add_u32 %[wlo], %[wlo], %[qlo]\n\t"                         \
+  "s_sub_u32 %[r], %[q], %[wlo]\n\t"                             \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
+  COLWORD                                                        \
+  "v_readlane_b32 %[m], %[ch], %[r]\n\t"                         \
+  "11:\n\t"                                                      \
+  "s_and_b32 %[m], %[m], %[w]\n\t"                               \
+  "s_cbranch_scc0 13f\n\t"                                       \
+  "s_ff1_i32_b32 %[t], %[m]\n\t"                                 \
+  "s_bitset1_b32 %[tm], %[t]\n\t"                                \
+  "s_add_u32 %[r], %[t], 1\n\t"                                  \
+  "s_sub_u32 %[rem], %[rem], 1\n\t"                              \
+  "s_cbranch_scc1 12f\n\t"                                       \
+  COLWORD                                                        \
+  "v_readlane_b32 %[m], %[ch], %[r]\n\t"                         \
+  "s_cmp_lg_u32 %[r], 32\n\t"                                    \
+  "s_cbranch_scc1 11b\n\t"                                       \
+  "12:\n\t"                                                      \
+  "s_add_u32 %[q], %[wlo], %[r]\n\t"                             \
+  "s_branch 14f\n\t"                                             \
+  "13:\n\t"                                                      \
+  "v_readlane_b32 %[q], %[ex], %[r]\n\t"                         \
+  "14:\n\t"                                                      \
+  "s_cmp_ge_u32 %[q], %[n]\n\t"                                  \
+  "s_cbranch_scc1 19f\n\t"                                       \
+  "s_sub_u32 %[r], %[q], %[qlo]\n\t"                             \
+  "s_lshr_b32 %[r], %[r], 5\n\t"                                 \
+  "s_cmp_eq_u32 %[r], %[wk]\n\t"                                 \
+  "s_cbranch_scc1 15f\n\t"                                       \
+  "s_mov_b32 m0, %[wk]\n\t"                                      \
+  "v_writelane_b32 %[tw], %[tm], m0\n\t"                        \
+  "s_mov_b32 %[tm], 0\n\t"                                       \
+  "s_mov_b32 %[wk], %[r]\n\t"                                    \
+  "15:\n\t"                                                      \
+  "s_cmp_lt_i32 %[rem], 0\n\t"                                   \
+  "s_cbranch_scc1 19f\n\t"                                       \
+  "s_cmp_lt_u32 %[wk], 16\n\t"                                   \
+  "s_cbranch_scc1 10b\n\t"                                       \
+  "19:"
+
+#define PP_WALK_OPERANDS                                                          \
+  [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [wk] "+s"(wk), [tw] "+v"(tw),      \
+      [r] "=&s"(r), [m] "=&s"(m), [w] "=&s"(w), [t] "=&s"(t), [off] "=&s"(off),   \
+      [wlo] "=&s"(wlo), [va] "=&v"(va), [ch] "=&v"(ch), [ex] "=&v"(ex)
+
+__device__ __forceinline__ void walk_sw_c1(uint32_t& q, uint32_t& rem, uint32_t& tm,
+                                           uint32_t& wk, uint32_t& tw, uint32_t qlo,
+                                           uint32_t n, uint32_t ace, uint32_t aw) {
+  uint32_t r, m, w, t, off, wlo, va, ch, ex, vb, wc0;
+  asm volatile(PP_WALK_SW("v_add_u32_e32 %[vb], %[off], %[aw]\n\t"
+                          "ds_read_b32 %[wc0], %[vb]\n\t",
+                          "v_readlane_b32 %[w], %[wc0], %[rem]\n\t")
+               : PP_WALK_OPERANDS, [vb] "=&v"(vb), [wc0] "=&v"(wc0)
+               : [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
+               : "scc", "m0");
 }
 
-// The same walk for two and four cells per lane: the column word of cell
-// index rem is lane rem/C of the cell-(rem mod C) register.
-__device__ __forceinline__ void walk_window_c2(uint32_t& q, int& rem, uint32_t& tm,
-                                               uint32_t wlo, uint32_t lim,
-                                               uint32_t wc0, uint32_t wc1,
-                                               uint32_t nx) {
-  uint32_t r, ln, w, w1, nq, bm, qp;
-  asm volatile(
-      "1:\n\t"
-      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-      "s_lshr_b32 %[ln], %[rem], 1\n\t"
-      "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
-      "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
-      "v_readlane_b32 %[nq], %[nx], %[r]\n\t"
-      "s_bitcmp1_b32 %[rem], 0\n\t"
-      "s_cselect_b32 %[w], %[w1], %[w]\n\t"
-      "s_lshl_b32 %[bm], 1, %[r]\n\t"
-      "s_add_u32 %[qp], %[q], 1\n\t"
-      "s_and_b32 %[w], %[w], %[bm]\n\t"      // SCC = take
-      "s_cselect_b32 %[q], %[qp], %[nq]\n\t"
-      "s_cselect_b32 %[bm], %[bm], 0\n\t"
-      "s_subb_u32 %[rem], %[rem], 0\n\t"     // rem -= take
-      "s_or_b32 %[tm], %[tm], %[bm]\n\t"
-      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-      "s_cmp_lt_u32 %[r], %[lim]\n\t"
-      "s_cselect_b32 %[r], %[rem], -1\n\t"
-      "s_cmp_ge_i32 %[r], 0\n\t"
-      "s_cbranch_scc1 1b"
-      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [r] "=&s"(r), [ln] "=&s"(ln),
-        [w] "=&s"(w), [w1] "=&s"(w1), [nq] "=&s"(nq), [bm] "=&s"(bm), [qp] "=&s"(qp)
-      : [wlo] "s"(wlo), [lim] "s"(lim), [wc0] "v"(wc0), [wc1] "v"(wc1), [nx] "v"(nx)
-      : "scc");
+// two and four cells per lane: cell rem is lane rem/C of word rem mod C
+__device__ __forceinline__ void walk_sw_c2(uint32_t& q, uint32_t& rem, uint32_t& tm,
+                                           uint32_t& wk, uint32_t& tw, uint32_t qlo,
+                                           uint32_t n, uint32_t ace, uint32_t aw) {
+  uint32_t r, m, w, t, off, wlo, va, ch, ex, vb, wc0, wc1, ln, w1, offw;
+  asm volatile(PP_WALK_SW("s_lshl_b32 %[offw], %[wk], 9\n\t"
+                          "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"
+                          "ds_read_b32 %[wc0], %[vb]\n\t"
+                          "ds_read_b32 %[wc1], %[vb] offset:256\n\t",
+                          "s_lshr_b32 %[ln], %[rem], 1\n\t"
+                          "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
+                          "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
+                          "s_bitcmp1_b32 %[rem], 0\n\t"
+                          "s_cselect_b32 %[w], %[w1], %[w]\n\t")
+               : PP_WALK_OPERANDS, [vb] "=&v"(vb), [wc0] "=&v"(wc0), [wc1] "=&v"(wc1),
+                 [ln] "=&s"(ln), [w1] "=&s"(w1), [offw] "=&s"(offw)
+               : [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
+               : "scc", "m0");
 }
 
-__device__ __forceinline__ void walk_window_c4(uint32_t& q, int& rem, uint32_t& tm,
-                                               uint32_t wlo, uint32_t lim,
-                                               uint32_t wc0, uint32_t wc1,
-                                               uint32_t wc2, uint32_t wc3,
-                                               uint32_t nx) {
-  uint32_t r, ln, w, w1, w2, w3, nq, bm, qp;
-  asm volatile(
-      "1:\n\t"
-      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-      "s_lshr_b32 %[ln], %[rem], 2\n\t"
-      "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
-      "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
-      "v_readlane_b32 %[w2], %[wc2], %[ln]\n\t"
-      "v_readlane_b32 %[w3], %[wc3], %[ln]\n\t"
-      "v_readlane_b32 %[nq], %[nx], %[r]\n\t"
-      "s_bitcmp1_b32 %[rem], 1\n\t"          // cells 2, 3
-      "s_cselect_b32 %[w], %[w2], %[w]\n\t"
-      "s_cselect_b32 %[w1], %[w3], %[w1]\n\t"
-      "s_bitcmp1_b32 %[rem], 0\n\t"          // odd cells
-      "s_cselect_b32 %[w], %[w1], %[w]\n\t"
-      "s_lshl_b32 %[bm], 1, %[r]\n\t"
-      "s_add_u32 %[qp], %[q], 1\n\t"
-      "s_and_b32 %[w], %[w], %[bm]\n\t"      // SCC = take
-      "s_cselect_b32 %[q], %[qp], %[nq]\n\t"
-      "s_cselect_b32 %[bm], %[bm], 0\n\t"
-      "s_subb_u32 %[rem], %[rem], 0\n\t"     // rem -= take
-      "s_or_b32 %[tm], %[tm], %[bm]\n\t"
-      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-      "s_cmp_lt_u32 %[r], %[lim]\n\t"
-      "s_cselect_b32 %[r], %[rem], -1\n\t"
-      "s_cmp_ge_i32 %[r], 0\n\t"
-      "s_cbranch_scc1 1b"
-      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [r] "=&s"(r), [ln] "=&s"(ln),
-        [w] "=&s"(w), [w1] "=&s"(w1), [w2] "=&s"(w2), [w3] "=&s"(w3), [nq] "=&s"(nq),
-        [bm] "=&s"(bm), [qp] "=&s"(qp)
-      : [wlo] "s"(wlo), [lim] "s"(lim), [wc0] "v"(wc0), [wc1] "v"(wc1),
-        [wc2] "v"(wc2), [wc3] "v"(wc3), [nx] "v"(nx)
-      : "scc");
+__device__ __forceinline__ void walk_sw_c4(uint32_t& q, uint32_t& rem, uint32_t& tm,
+                                           uint32_t& wk, uint32_t& tw, uint32_t qlo,
+                                           uint32_t n, uint32_t ace, uint32_t aw) {
+  uint32_t r, m, w, t, off, wlo, va, ch, ex, vb, wc0, wc1, wc2, wc3, ln, w1, w2, w3, offw;
+  asm volatile(PP_WALK_SW("s_lshl_b32 %[offw], %[wk], 10\n\t"
+                          "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"
+                          "ds_read_b32 %[wc0], %[vb]\n\t"
+                          "ds_read_b32 %[wc1], %[vb] offset:256\n\t"
+                          "ds_read_b32 %[wc2], %[vb] offset:512\n\t"
+                          "ds_read_b32 %[wc3], %[vb] offset:768\n\t",
+                          "s_lshr_b32 %[ln], %[rem], 2\n\t"
+                          "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
+                          "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
+                          "v_readlane_b32 %[w2], %[wc2], %[ln]\n\t"
+                          "v_readlane_b32 %[w3], %[wc3], %[ln]\n\t"
+                          "s_bitcmp1_b32 %[rem], 1\n\t"
+                          "s_cselect_b32 %[w], %[w2], %[w]\n\t"
+                          "s_cselect_b32 %[w1], %[w3], %[w1]\n\t"
+                          "s_bitcmp1_b32 %[rem], 0\n\t"
+                          "s_cselect_b32 %[w], %[w1], %[w]\n\t")
+               : PP_WALK_OPERANDS, [vb] "=&v"(vb), [wc0] "=&v"(wc0), [wc1] "=&v"(wc1),
+                 [wc2] "=&v"(wc2), [wc3] "=&v"(wc3), [ln] "=&s"(ln), [w1] "=&s"(w1),
+                 [w2] "=&s"(w2), [w3] "=&s"(w3), [offw] "=&s"(offw)
+               : [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
+               : "scc", "m0");
 }
+#undef PP_WALK_OPERANDS
+#undef PP_WALK_SW
 
 // Acceptance (greedy: always; refinement: DP value > incumbent value, which
 // by Proposition 1 is G(T_-h, T'_h) > G(T)) and, when accepted, the walk
@@ -887,28 +904,30 @@ __device__ __forceinline__ void walk_window_c4(uint32_t& q, int& rem, uint32_t& 
 //
 // A choice word of one sweep batch holds 32 consecutive rows -- a window,
 // row q at bit q mod 32 (the padded step count is a multiple of 32) -- of
-// one cell column, so the walk tests bits of one scalar word per (window,
-// column) and reads next(q) from one register per window.  Rows are staged
-// in super-windows of 512: the words of the current stage and next() of the
-// 512 rows go to LDS, and the next super-window of the same stage is loaded
-// from memory into registers while this one is walked (rows only increase
-// along the walk).  The walk keeps the current window in registers (lane l:
-// the words of its cell columns; lanes 0..31: next() of the window's rows)
-// and reads the following window from LDS ahead of use.  When j leaves the
-// stage, the words are reloaded for the stage below.  Taken rows are
-// gathered per window and written as a bitmap.
+// one cell column.  While j stays fixed the walk visits q, next(q),
+// next(next(q)), ...; the rows of that sequence inside q's window are one
+// precomputed mask, so the next take is the lowest set bit of (column word
+// & mask), and without one the walk leaves the window at the sequence's
+// precomputed exit row: the scalar walk advances per take, not per row.
+// Rows are staged in super-windows of 512: the words of the current stage
+// and the masks and exit rows of the 512 rows go to LDS, and the next
+// super-window of the same stage is loaded from memory into registers while
+// this one is walked (rows only increase along the walk).  When j leaves
+// the stage, the words are reloaded for the stage below.  Taken rows are
+// gathered per window (lane k of tw: window k of the super-window) and
+// written as a bitmap when the walk leaves the super-window.
 template <int C>
 __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
                                                   int mode) {
   constexpr int kWin = kDpBatch;        // rows per choice word
   constexpr int kSwWin = 16;            // windows per super-window
   constexpr int kSw = kWin * kSwWin;    // rows per super-window
-  constexpr int kNx = kSw / kWave;      // next() registers per lane
+  constexpr int kNx = kSw / kWave;      // chain / exit registers per lane
   constexpr int kW = C * kSwWin;        // choice-word registers per lane
   constexpr int kStage = kWave * C;     // cells per stage
-  static_assert(kWin == 32, "choice words hold 32 steps");
+  static_assert(kWin == 32 && kSwWin == 16, "the scalar walk's window layout");
   __shared__ uint32_t s_words[kSwWin][C][kWave];
-  __shared__ int s_nx[kSw];
+  __shared__ uint32_t s_ce[kSw][2];  // chain mask, exit row
   const int ci = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t slot = set.slot[ci];
@@ -946,10 +965,14 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
       for (int c = 0; c < C; ++c) w[c * kSwWin + k] = base[c * cstride + (int64_t)b * kWave];
     }
   };
-  auto load_next = [&](int sw, int (&nx)[kNx]) {
+  auto load_chain = [&](int sw, uint32_t (&ch)[kNx], int (&ex)[kNx]) {
 #pragma unroll
-    for (int t = 0; t < kNx; ++t)
-      nx[t] = d.nextpos[min(sw * kSw + t * kWave + lane, n - 1)];
+    for (int t = 0; t < kNx; ++t) {
+      // rows past the end: no take, and the walk leaves at row n
+      const int q = sw * kSw + t * kWave + lane;
+      ch[t] = q < n ? d.chain[q] : 0u;
+      ex[t] = q < n ? d.exitr[q] : n;
+    }
   };
   auto words_to_lds = [&](const uint32_t (&w)[kW]) {
 #pragma unroll
@@ -957,116 +980,79 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
 #pragma unroll
       for (int c = 0; c < C; ++c) s_words[k][c][lane] = w[c * kSwWin + k];
   };
-  auto next_to_lds = [&](const int (&nx)[kNx]) {
+  auto chain_to_lds = [&](const uint32_t (&ch)[kNx], const int (&ex)[kNx]) {
 #pragma unroll
-    for (int t = 0; t < kNx; ++t) s_nx[t * kWave + lane] = nx[t];
-  };
-  // window k of the staged super-window: lane l's words, and next() of row
-  // 32k + (l mod 32)
-  auto read_win = [&](int k, uint32_t (&w)[C], int& nx) {
-#pragma unroll
-    for (int c = 0; c < C; ++c) w[c] = s_words[k][c][lane];
-    nx = s_nx[k * kWin + lane % kWin];
-  };
-
-  // take masks: lane (window mod 64) of tw holds that window's mask; tw
-  // covers windows [64 tblk, 64 tblk + 64)
-  uint32_t tw = 0;
-  int tblk = 0;
-  int cur_win = 0;
-  uint32_t tm = 0;
-  auto move_to = [&](int win) {
-    if (win == cur_win) return;
-    if ((cur_win >> 6) != tblk) {
-      const int idx = tblk * kWave + lane;
-      if (idx < nwords) selw[idx] = tw;
-      tw = 0;
-      tblk = cur_win >> 6;
+    for (int t = 0; t < kNx; ++t) {
+      s_ce[t * kWave + lane][0] = ch[t];
+      s_ce[t * kWave + lane][1] = (uint32_t)ex[t];
     }
-    tw = (uint32_t)pp_writelane_i32((int)tm, cur_win & (kWave - 1), (int)tw);
-    tm = 0;
-    cur_win = win;
+  };
+  // LDS addresses the walk reads from: lane l's row (l mod 32) of window 0
+  // and lane l's word of window 0, cell 0
+  const uint32_t ace = (uint32_t)(size_t)(__attribute__((address_space(3))) uint32_t*)&s_ce[lane % kWin][0];
+  const uint32_t aw = (uint32_t)(size_t)(__attribute__((address_space(3))) uint32_t*)&s_words[0][0][lane];
+  // this super-window's take masks to the bitmap
+  auto store_takes = [&](int sw, uint32_t tw) {
+    const int idx = sw * kSwWin + lane;
+    if (lane < kSwWin && idx < nwords) selw[idx] = tw;
   };
 
   int q = 0, j = kp;
   int g = (j - 1) / kStage;
   int sw = 0;
   uint32_t wb[kW];
-  int nb[kNx];
+  uint32_t cb[kNx];
+  int eb[kNx];
   load_words(0, g, wb);
-  load_next(0, nb);
+  load_chain(0, cb, eb);
   words_to_lds(wb);
-  next_to_lds(nb);
+  chain_to_lds(cb, eb);
   __syncthreads();
-  bool done = false;
-  while (!done) {
+  uint32_t tw = 0, tm = 0;
+  for (;;) {
     // the next super-window of this stage, in flight while this one is walked
     load_words(sw + 1, g, wb);
-    load_next(sw + 1, nb);
-    const int q_lo = sw * kSw;
+    load_chain(sw + 1, cb, eb);
     const int jlo = g * kStage + 1;
-    int wk = (q - q_lo) / kWin;
-    move_to(q / kWin);
-    uint32_t wc[C], wn[C];
-    int nxc, nxn;
-    read_win(wk, wc, nxc);
-    read_win(min(wk + 1, kSwWin - 1), wn, nxn);
-    int rem = j - jlo;  // cell of j within the stage
-    for (;;) {
-      // walk inside the window: rows [wlo, wlo + lim), lim <= 32
-      const uint32_t wlo = (uint32_t)(q_lo + wk * kWin);
-      const uint32_t lim = (uint32_t)min(kWin, n - (int)wlo);
-      uint32_t uq = (uint32_t)q;
-      uint32_t t = tm;
-      if constexpr (C == 1) {
-        walk_window_c1(uq, rem, t, wlo, lim, wc[0], (uint32_t)nxc);
-      } else if constexpr (C == 2) {
-        walk_window_c2(uq, rem, t, wlo, lim, wc[0], wc[1], (uint32_t)nxc);
-      } else {
-        static_assert(C == 4, "one, two or four cells per lane");
-        walk_window_c4(uq, rem, t, wlo, lim, wc[0], wc[1], wc[2], wc[3], (uint32_t)nxc);
-      }
-      tm = t;
-      q = (int)uq;
-      j = jlo + rem;
-      if (j == 0 || q >= n) {
-        done = true;
-        break;
-      }
-      const int nw = (q - q_lo) / kWin;
-      move_to(q / kWin);
-      if (rem < 0 || nw >= kSwWin) break;  // left the stage or super-window
-      if (nw == wk + 1) {
-#pragma unroll
-        for (int c = 0; c < C; ++c) wc[c] = wn[c];
-        nxc = nxn;
-      } else {
-        read_win(nw, wc, nxc);
-      }
-      wk = nw;
-      read_win(min(wk + 1, kSwWin - 1), wn, nxn);
+    uint32_t uq = (uint32_t)q, urem = (uint32_t)(j - jlo);
+    uint32_t wk = (uint32_t)(q - sw * kSw) / kWin;
+    if constexpr (C == 1) {
+      walk_sw_c1(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
+    } else if constexpr (C == 2) {
+      walk_sw_c2(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
+    } else {
+      static_assert(C == 4, "one, two or four cells per lane");
+      walk_sw_c4(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
     }
-    if (done) break;
+    q = (int)uq;
+    j = jlo + (int)urem;
+    if (q >= n || j == 0) {
+      if (wk < (uint32_t)kSwWin) tw = (uint32_t)pp_writelane_i32((int)tm, (int)wk, (int)tw);
+      store_takes(sw, tw);
+      break;
+    }
+    // the walk left the stage or the super-window
     const int sw_n = q / kSw, g_n = (j - 1) / kStage;
+    if (sw_n != sw) {
+      store_takes(sw, tw);  // the last window's takes are in tw already
+      tw = 0;
+    }
     if (g_n == g && sw_n == sw + 1) {
       // the prefetched super-window
     } else if (g_n == g) {
       load_words(sw_n, g_n, wb);
-      load_next(sw_n, nb);
+      load_chain(sw_n, cb, eb);
     } else {
       load_words(sw_n, g_n, wb);
-      if (sw_n != sw) load_next(sw_n, nb);
+      if (sw_n != sw) load_chain(sw_n, cb, eb);
     }
     __syncthreads();
     words_to_lds(wb);
-    if (sw_n != sw) next_to_lds(nb);
+    if (sw_n != sw) chain_to_lds(cb, eb);
     __syncthreads();
     sw = sw_n;
     g = g_n;
   }
-  move_to(-1);
-  const int idx = tblk * kWave + lane;
-  if (idx < nwords) selw[idx] = tw;
 }
 
 // -------------------------------------------------------------- commit --
