@@ -1058,20 +1058,59 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
 // -------------------------------------------------------------- commit --
 
 // Adopt T'_h where accepted: write the new membership and refresh the top-2
-// holder state of every chunk whose membership changed (O(M^2) each).
-__global__ void __launch_bounds__(256) k_commit(ChainSet set, DevState d) {
+// holder state of every chunk whose membership changed (O(M^2) each).  A
+// block holds kCommitThreads / M chunks times M requesters (requester-major,
+// so each requester's loads are contiguous); each thread rebuilds one
+// requester's top-2 over all holders, taking worker h's membership from
+// the new selection, and the new membership is written after a barrier.
+constexpr int kCommitThreads = 256;
+
+__global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevState d) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
   if (!d.cs[s].accept) return;
   const int h = set.worker[ci];
-  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (i >= d.n) return;
-  const int64_t mn = (int64_t)d.m * d.n;
-  uint8_t* th = d.tgt + s * mn + (int64_t)h * d.n;
-  const uint8_t nv = (uint8_t)((d.sel[s * (d.npad / 32) + i / 32] >> (i % 32)) & 1u);
-  if (nv == th[i]) return;
-  th[i] = nv;
-  refresh_holders(d, s, i);
+  const int m = d.m;
+  const int64_t n = d.n;
+  const int cpb = kCommitThreads / m;  // chunks per block (m <= 255)
+  const int r = threadIdx.x / cpb;
+  const int64_t i = (int64_t)blockIdx.x * cpb + threadIdx.x % cpb;
+  const int64_t mn = (int64_t)m * n;
+  const uint8_t* t = d.tgt + s * mn;
+  uint8_t* th = d.tgt + s * mn + (int64_t)h * n;
+  bool changed = false;
+  uint8_t nv = 0;
+  if (r < m && i < n) {
+    nv = (uint8_t)((d.sel[s * (d.npad / 32) + i / 32] >> (i % 32)) & 1u);
+    changed = nv != th[i];
+  }
+  if (!__syncthreads_or(changed)) return;
+  if (changed) {
+    const int64_t wr = d.w[(int64_t)r * n + i];
+    int64_t b1 = 0, b2 = 0;
+    int hb = kNoHolder;
+#pragma unroll 8
+    for (int l = 0; l < m; ++l) {
+      const bool held = (l == h) ? nv != 0 : t[(int64_t)l * n + i] != 0;
+      const int64_t fv = (l == r) ? 0 : d.f[((int64_t)l * m + r) * n + i];
+      const int64_t q = (l == r) ? wr : imax(wr - fv, 0);
+      if (held) {
+        if (hb == kNoHolder || q > b1) {
+          b2 = (hb == kNoHolder) ? b2 : b1;
+          b1 = q;
+          hb = l;
+        } else if (q > b2) {
+          b2 = q;
+        }
+      }
+    }
+    const int64_t o = s * mn + (int64_t)r * n + i;
+    d.v1[o] = b1;
+    d.v2[o] = b2;
+    d.h1[o] = (uint8_t)hb;
+  }
+  __syncthreads();  // every requester has read the old membership row
+  if (changed && r == 0) th[i] = nv;
 }
 
 // Start of a refinement sweep: no replacement accepted yet.
@@ -1231,8 +1270,8 @@ hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
 }
 
 hipError_t launch_commit(const ChainSet& set, const DevState& d, hipStream_t st) {
-  hipLaunchKernelGGL(k_commit, grid1(d.n, 256, set.count), dim3(256), 0, st,
-                     set, d);
+  hipLaunchKernelGGL(k_commit, grid1(d.n, kCommitThreads / d.m, set.count),
+                     dim3(kCommitThreads), 0, st, set, d);
   return hipGetLastError();
 }
 
