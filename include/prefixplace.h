@@ -119,10 +119,10 @@ int32_t pp_num_starts(int32_t m, int32_t n_starts);
  *                            parent-closed with at most cap[m] ones
  *   objective                host out: F_pair(T) in request * us
  *   stats                    NULL or statistics
- * Limits: the DP sweep keeps pending skip-target rows in LDS; their number
- * (at most the tree depth; 11 and 14 on the benchmark trees) must not exceed
- * 254, and the rows must fit one compute unit's LDS (about 280 rows at one
- * cell per lane), else PP_E_UNSUPPORTED. */
+ * Limits: the DP sweep keeps pending skip-target rows in LDS slots; their
+ * number (at most the tree depth; 14 and 17 on the 50,000-chunk benchmark
+ * trees) must not exceed 254, and the rows must fit one compute unit's LDS
+ * (up to 254 slots fit at one cell per lane), else PP_E_UNSUPPORTED. */
 int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
             const int64_t *recompute_cost, const int64_t *fetch_cost,
             const int32_t *cap, const pp_options *opt, uint8_t *target,
@@ -178,16 +178,17 @@ int pp_plan_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
  * lane, writes the per-step metadata of the sweep (`meta`, may be NULL to
  * query the size; 4 * nsteps words, nsteps = n padded up to a multiple of 32
  * with leading dummy steps; step s handles preorder row n - (s - pad), pad =
- * nsteps - n) and the number of LDS stack rows H.  Rows hold 64*cells int64
- * in the order [H stack rows | zero row | sink row].  Per step: word 0 =
- * byte offset of the row the step's DP row is written to (its stack slot
- * when a row more than two rows back skips to it, else the sink); word 1 =
+ * nsteps - n) and the number of LDS slot rows H.  LDS rows hold 64*cells
+ * int64 (stride 512*cells + 8 bytes) in the order [H slot rows | zero row |
+ * sink rows: 16 at one cell per lane, else 4].  Per step: word 0 = byte
+ * offset of the row the step's DP row is stored to (its slot when a later
+ * non-leaf row skips to it, else sink row step mod the sink count); word 1 =
  * byte offset of the row read as the next step's skip operand (Eq. 9's
- * D[next(i)][*]: a stack slot, or the zero row when that next() is past the
- * end or the operand is one of the two previous rows); word 2 = 0xFFFFFFFF
- * when the step's node is a leaf (skip operand: the previous row), else 0;
- * word 3 = 0xFFFFFFFF when its subtree has two nodes (skip operand: the row
- * before the previous one), else 0.  The first step's node is a leaf. */
+ * D[next(i)][*]: a slot, or the zero row when that next() is past the end or
+ * the next step's node is a leaf), which the sweep reads right after storing
+ * the current step's row; word 2 = 0xFFFFFFFF when the step's node is a leaf
+ * (skip operand: the previous row, in registers), else 0; word 3 = 0.  The
+ * first step's node is a leaf. */
 int pp_sweep_layout(int32_t n, const int32_t *parent, int32_t cells,
                     uint32_t *meta, int32_t *nsteps, int32_t *slots);
 
