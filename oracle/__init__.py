@@ -19,6 +19,7 @@ LIB = os.path.join(_HERE, "libpporacle.so")
 
 OK, E_ARG, E_TREE, E_RANGE, E_OVERFLOW, E_NOMEM = 0, -1, -2, -3, -4, -5
 F_NO_REFINE = 2
+F_SAFEGUARDS = 8
 
 
 def build(force: bool = True) -> str:
@@ -55,9 +56,12 @@ def lib() -> ctypes.CDLL:
         L.ppo_splitmix64_stream.argtypes = [u64, i32, P]
         L.ppo_splitmix64_stream.restype = None
         L.ppo_plan.argtypes = [i32, i32, P, P, P, P, P, i32, i32, u64, P, u32,
-                               i32, P, P, P, P, P, P, P, P]
+                               i32, P, P, P, P, P, P, P, P, P]
+        L.ppo_requester_side.argtypes = [i32, i32, P]
+        L.ppo_candidates.argtypes = [i32, i32, P, P, P, P, P, P, P]
         for f in (L.ppo_preorder, L.ppo_rooted_dp, L.ppo_marginal,
-                  L.ppo_objective, L.ppo_orders, L.ppo_plan):
+                  L.ppo_objective, L.ppo_orders, L.ppo_plan,
+                  L.ppo_requester_side, L.ppo_candidates):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -127,6 +131,29 @@ def objective(demand, recompute_cost, fetch_cost, target) -> int:
     return int(out[0])
 
 
+def requester_side(fetch_cost) -> bool:
+    """Reading R14: fetch_cost[src][dst][b] equal over every src != dst."""
+    f = _c(fetch_cost, np.int64)
+    m, n = f.shape[0], f.shape[2]
+    return bool(lib().ppo_requester_side(n, m, _p(f)))
+
+
+def candidates(parent, demand, recompute_cost, fetch_cost, cap):
+    """The Independent, Popularity and LocalDedup placements (reading R15)
+    as uint8 [3][m][n] and their objectives."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.int64)
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    cap = _c(cap, np.int32)
+    m, n = demand.shape
+    tg = np.zeros((3, m, n), np.uint8)
+    objs = np.zeros(3, np.int64)
+    _check(lib().ppo_candidates(n, m, _p(parent), _p(demand), _p(w), _p(f),
+                                _p(cap), _p(tg), _p(objs)))
+    return tg, [int(x) for x in objs]
+
+
 def num_starts(m: int, n_starts: int) -> int:
     return int(lib().ppo_num_starts(m, n_starts))
 
@@ -155,9 +182,11 @@ class PlanResult:
     start_objective: np.ndarray
     start_sweeps: np.ndarray
     start_accepts: np.ndarray
-    best_start: int
+    best_start: int             # start index, or S + c for safeguard c
     updates: int
     dp_cells: int
+    safeguards_run: bool = False
+    safeguard_objective: tuple = (0, 0, 0)
 
 
 def plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=1,
@@ -179,17 +208,20 @@ def plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=1,
     so = np.zeros(S, np.int64)
     ss = np.zeros(S, np.int32)
     sa = np.zeros(S, np.int32)
-    info = np.zeros(4, np.int64)
+    info = np.zeros(5, np.int64)
+    sgo = np.zeros(3, np.int64)
     _check(lib().ppo_plan(n, m, _p(parent), _p(demand), _p(w), _p(f), _p(cap),
                           int(n_starts), int(max_rounds),
                           ctypes.c_uint64(order_seed & (2**64 - 1)),
                           _p(orders_in), int(flags), int(threads), _p(tgt),
                           _p(obj), _p(st), _p(ords), _p(so), _p(ss), _p(sa),
-                          _p(info)))
+                          _p(info), _p(sgo)))
     return PlanResult(target=tgt, objective=int(obj[0]), standalone=st,
                       orders=ords, start_objective=so, start_sweeps=ss,
                       start_accepts=sa, best_start=int(info[0]),
-                      updates=int(info[1]), dp_cells=int(info[2]))
+                      updates=int(info[1]), dp_cells=int(info[2]),
+                      safeguards_run=bool(info[4]),
+                      safeguard_objective=tuple(int(x) for x in sgo))
 
 
 def plan_instance(inst, **kw) -> PlanResult:

@@ -14,6 +14,8 @@
  *   - rooted-tree DP D[i,j] and its backtrack        Eq. (9), Theorem 1, Algorithm 1 (RootedDP)
  *   - WorkerGreedy, coordinate refinement,
  *     order-diverse starts, best-candidate return   Sec. IV-B/IV-C, Theorem 3, Algorithm 1 (PrefixPlace)
+ *   - comparator safeguards for requester-side
+ *     costs (Independent, Popularity, LocalDedup)   Sec. IV-C, Algorithm 1; Sec. V-A (comparators)
  *
  * Readings of points the paper leaves open (numbered as in the design notes):
  *   R1  DP ties: take b_i only if strictly better; skip wins ties.
@@ -32,6 +34,16 @@
  *   R10 ties between starts go to the earliest start.
  *   R11 fetch_cost[h][h][*] is ignored (q_{h<-h} = w_h).
  *   R13 capacity above n is capped to n.
+ *   R14 the safeguard candidates are added only for requester-side inputs:
+ *       fetch_cost[src][dst][b] equal over every src != dst (M = 1 counts
+ *       as requester-side); f_m(b) is that common value.
+ *   R15 Independent: RootedDP per worker with p = Lambda_m * w_m;
+ *       Popularity: p = Lambda_m; LocalDedup: workers in increasing id, each
+ *       RootedDP with p = a_m + 1{b not in U} Lambda_m [w_m - f_m]_+, U the
+ *       union of the earlier workers' sets (the requester's own saving only,
+ *       no coverage value for other requesters); capacity k_m throughout.
+ *   R16 a candidate replaces the best start only if strictly better; among
+ *       candidates the order Independent, Popularity, LocalDedup breaks ties.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -47,7 +59,7 @@ enum {
     PPO_E_NOMEM = -5
 };
 
-enum { PPO_F_NO_REFINE = 2u };
+enum { PPO_F_NO_REFINE = 2u, PPO_F_SAFEGUARDS = 8u };
 
 static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
@@ -464,6 +476,92 @@ int ppo_objective(int32_t n, int32_t m, const int64_t *demand,
     return PPO_OK;
 }
 
+/* ---------------------------------------------------------- safeguards -- */
+
+/* R14: 1 when fetch_cost[src][dst][b] is the same for every src != dst. */
+int ppo_requester_side(int32_t n, int32_t m, const int64_t *fetch_cost)
+{
+    for (int32_t dst = 0; dst < m; dst++) {
+        int32_t first = dst == 0 ? 1 : 0;
+        for (int32_t src = first + 1; src < m; src++) {
+            if (src == dst)
+                continue;
+            for (int32_t b = 0; b < n; b++)
+                if (fetch_cost[((size_t)src * m + dst) * n + b] !=
+                    fetch_cost[((size_t)first * m + dst) * n + b])
+                    return 0;
+        }
+    }
+    return 1;
+}
+
+/* The three comparator placements of Sec. IV-C (R15), each a RootedDP per
+ * worker, and their objective F (= F_pair for requester-side inputs).
+ *   targets [3][m][n] out (caller ids): Independent, Popularity, LocalDedup
+ *   objs    [3] out */
+int ppo_candidates(int32_t n, int32_t m, const int32_t *parent,
+                   const int64_t *demand, const int64_t *recompute_cost,
+                   const int64_t *fetch_cost, const int32_t *cap,
+                   uint8_t *targets, int64_t *objs)
+{
+    int rc = validate(n, m, parent, demand, recompute_cost, fetch_cost, cap);
+    if (rc != PPO_OK)
+        return rc;
+    if (!targets || !objs)
+        return PPO_E_ARG;
+    int32_t *order = malloc((size_t)n * sizeof(int32_t));
+    int32_t *nextpos = malloc((size_t)n * sizeof(int32_t));
+    int64_t *pp = malloc((size_t)n * sizeof(int64_t));
+    uint8_t *sp = malloc((size_t)n);
+    rc = PPO_E_NOMEM;
+    if (!order || !nextpos || !pp || !sp)
+        goto out;
+    rc = preorder(n, parent, order, nextpos);
+    if (rc != PPO_OK)
+        goto out;
+    memset(targets, 0, (size_t)3 * m * n);
+    for (int32_t c = 0; c < 3; c++) {
+        uint8_t *tg = targets + (size_t)c * m * n;
+        for (int32_t h = 0; h < m; h++) {
+            const int64_t *lam = demand + (size_t)h * n;
+            const int64_t *w = recompute_cost + (size_t)h * n;
+            /* f_h(b): the common off-diagonal fetch cost (R14) */
+            int32_t src = h == 0 ? 1 : 0;
+            const int64_t *f = m > 1 ? fetch_cost + ((size_t)src * m + h) * n : NULL;
+            for (int32_t i = 0; i < n; i++) {
+                int32_t b = order[i];
+                int64_t p;
+                if (c == 0) {
+                    p = lam[b] * w[b];                  /* Independent */
+                } else if (c == 1) {
+                    p = lam[b];                         /* Popularity */
+                } else if (!f) {
+                    p = lam[b] * w[b];                  /* LocalDedup, M = 1 */
+                } else {
+                    int covered = 0;                    /* b in U (earlier ids) */
+                    for (int32_t l = 0; l < h; l++)
+                        covered |= tg[(size_t)l * n + b];
+                    int64_t a = lam[b] * (w[b] < f[b] ? w[b] : f[b]);
+                    int64_t own = lam[b] * max64(w[b] - f[b], 0);
+                    p = covered ? a : a + own;          /* LocalDedup */
+                }
+                pp[i] = p;
+            }
+            int64_t v;
+            rc = rooted_dp_pos(n, nextpos, pp, cap[h], sp, &v);
+            if (rc != PPO_OK)
+                goto out;
+            for (int32_t i = 0; i < n; i++)
+                tg[(size_t)h * n + order[i]] = sp[i];
+        }
+        objs[c] = objective_full(n, m, demand, recompute_cost, fetch_cost, tg);
+    }
+    rc = PPO_OK;
+out:
+    free(order); free(nextpos); free(pp); free(sp);
+    return rc;
+}
+
 /* --------------------------------------------------------------- plan -- */
 
 typedef struct {
@@ -639,9 +737,12 @@ static int run_phase(plan_work *pw, int phase, int32_t jobs, int32_t threads)
  *   standalone_out[m]     optional out: standalone scores (R6)
  *   orders_out[S][m]      optional out: the start orders used
  *   start_objective[S], start_sweeps[S], start_accepts[S]: optional outs
- *   info[4] (int64)       optional out: best start, executed worker updates,
- *                         executed DP cells (sum of n * min(k_h, n) over
- *                         updates), number of starts S. */
+ *   info[5] (int64)       optional out: index of the returned candidate
+ *                         (start s, or S + c for safeguard c), executed
+ *                         worker updates, executed DP cells (sum of
+ *                         n * min(k_h, n) over updates), number of starts S,
+ *                         1 if the safeguard candidates were evaluated.
+ *   safeguard_obj[3]      optional out: their objectives (0 if not run). */
 int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
              const int64_t *recompute_cost, const int64_t *fetch_cost,
              const int32_t *cap, int32_t n_starts, int32_t max_rounds,
@@ -649,7 +750,7 @@ int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
              int32_t threads, uint8_t *target, int64_t *objective,
              int64_t *standalone_out, int32_t *orders_out,
              int64_t *start_objective, int32_t *start_sweeps,
-             int32_t *start_accepts, int64_t *info)
+             int32_t *start_accepts, int64_t *info, int64_t *safeguard_obj)
 {
     int rc = validate(n, m, parent, demand, recompute_cost, fetch_cost, cap);
     if (rc != PPO_OK)
@@ -676,6 +777,7 @@ int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
     int32_t *orders = malloc((size_t)S * m * sizeof(int32_t));
     int64_t *standalone = malloc((size_t)m * sizeof(int64_t));
     uint8_t *tgts = malloc((size_t)S * m * n);
+    uint8_t *cands = NULL;
     int64_t *obj = malloc((size_t)S * sizeof(int64_t));
     int32_t *sw = malloc((size_t)S * sizeof(int32_t));
     int32_t *ac = malloc((size_t)S * sizeof(int32_t));
@@ -719,8 +821,29 @@ int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
     for (int32_t s = 1; s < S; s++)
         if (obj[s] > obj[best])
             best = s;
-    memcpy(target, tgts + (size_t)best * m * n, (size_t)m * n);
-    *objective = obj[best];
+    const uint8_t *won = tgts + (size_t)best * m * n;
+    int64_t won_obj = obj[best];
+    int64_t sg_obj[3] = {0, 0, 0};
+    int sg_run = 0;
+    if ((flags & PPO_F_SAFEGUARDS) && ppo_requester_side(n, m, fetch_cost)) {
+        cands = malloc((size_t)3 * m * n);
+        rc = PPO_E_NOMEM;
+        if (!cands)
+            goto out;
+        rc = ppo_candidates(n, m, parent, demand, recompute_cost, fetch_cost,
+                            cap, cands, sg_obj);
+        if (rc != PPO_OK)
+            goto out;
+        sg_run = 1;
+        for (int32_t c = 0; c < 3; c++)  /* R16 */
+            if (sg_obj[c] > won_obj) {
+                won_obj = sg_obj[c];
+                won = cands + (size_t)c * m * n;
+                best = S + c;
+            }
+    }
+    memcpy(target, won, (size_t)m * n);
+    *objective = won_obj;
     int64_t updates = m, cells = 0;
     for (int32_t h = 0; h < m; h++)
         cells += (int64_t)n * (cap[h] < n ? cap[h] : n);
@@ -739,15 +862,22 @@ int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
         memcpy(start_sweeps, sw, (size_t)S * sizeof(int32_t));
     if (start_accepts)
         memcpy(start_accepts, ac, (size_t)S * sizeof(int32_t));
+    if (sg_run) {  /* 3M more DP updates */
+        updates += 3 * (int64_t)m;
+        cells += 3 * cells_per_pass;
+    }
     if (info) {
         info[0] = best;
         info[1] = updates;
         info[2] = cells;
         info[3] = S;
+        info[4] = sg_run;
     }
+    if (safeguard_obj)
+        memcpy(safeguard_obj, sg_obj, sizeof sg_obj);
     rc = PPO_OK;
 out:
     free(order); free(nextpos); free(orders); free(standalone); free(tgts);
-    free(obj); free(sw); free(ac); free(rcs);
+    free(obj); free(sw); free(ac); free(rcs); free(cands);
     return rc;
 }
