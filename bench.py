@@ -123,6 +123,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="tree50k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--safeguards", action="store_true",
+                    help="requester-side variant of the workload (each "
+                         "requester's fetch cost taken from one source) "
+                         "planned with the comparator safeguards")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device (counter "
                          "calibration) and exit")
@@ -146,6 +150,19 @@ def main():
 
         build.build()
     inst = W.make_workload(args.workload)
+    plan_flags = 0
+    if args.safeguards:
+        import dataclasses
+
+        f_req = inst.fetch_cost.copy()
+        for dst in range(inst.m):
+            src0 = 1 if dst == 0 else 0
+            for src in range(inst.m):
+                if src != dst and inst.m > 1:
+                    f_req[src, dst] = inst.fetch_cost[src0, dst]
+        inst = dataclasses.replace(inst, name=inst.name + "-requester-side",
+                                   fetch_cost=f_req)
+        plan_flags = B.PP_F_SAFEGUARDS
     log(f"[bench] workload {inst.name}: n={inst.n} m={inst.m} "
         f"k={int(inst.cap.min())}..{int(inst.cap.max())} S={inst.n_starts}")
     dev = torch.device("cuda:0")
@@ -159,7 +176,8 @@ def main():
         return ctx.pp_plan_device(inst.parent, lam, w, f, inst.cap, tgt,
                                   n_starts=inst.n_starts,
                                   max_rounds=inst.max_rounds,
-                                  order_seed=inst.order_seed, flags=flags)
+                                  order_seed=inst.order_seed,
+                                  flags=flags | plan_flags)
 
     for i in range(args.warmup):
         p = step()
@@ -228,6 +246,9 @@ def main():
             "dp_share_of_plan_time": dp_ms / 1e3 / dt,
         },
         "parity_vs_golden": gold_ok,
+        **({"safeguards": {"run": p.safeguards_run, "returned": p.best_start,
+                           "objectives": list(p.safeguard_objective)}}
+           if args.safeguards else {}),
         "paper_context": PAPER_CONTEXT,
     }
     if not args.no_cpu_baseline:

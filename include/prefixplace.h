@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 2
+#define PP_ABI_VERSION 3
 
 enum {
     PP_OK = 0,
@@ -66,7 +66,21 @@ enum {
 enum {
     PP_F_VALIDATE_ONLY = 1u, /* validate and build the tree layout, no GPU work */
     PP_F_NO_REFINE = 2u,     /* greedy pass only (Theorem 3's WorkerGreedy) */
-    PP_F_TIME_KERNELS = 4u   /* time every DP-sweep launch with HIP events */
+    PP_F_TIME_KERNELS = 4u,  /* time every DP-sweep launch with HIP events */
+    PP_F_SAFEGUARDS = 8u     /* comparator safeguards (Sec. IV-C, Algorithm 1):
+                                when every fetch_cost[src][dst][b], src != dst,
+                                is equal over src (requester-side costs; M = 1
+                                counts as such), also solve the Independent
+                                (p = Lambda_m w_m per worker), Popularity
+                                (p = Lambda_m) and LocalDedup (workers in
+                                increasing id, p = a_m(b) + 1{b not in U}
+                                Lambda_m [w_m - f_m]_+, U = the earlier
+                                workers' sets) placements, each a rooted-tree
+                                DP per worker, and return one of them if its
+                                objective is strictly higher than every
+                                start's (ties: Independent, Popularity,
+                                LocalDedup).  3M more DP updates.  No effect
+                                for source-dependent costs. */
 };
 
 /* Planner options.  Passing NULL selects
@@ -87,7 +101,10 @@ typedef struct {
 /* Optional statistics.  Pointer fields may be NULL; arrays indexed by start
  * must hold pp_num_starts(m, n_starts) entries. */
 typedef struct {
-    int32_t best_start;        /* out: start whose placement is returned */
+    int32_t best_start;        /* out: start whose placement is returned, or
+                                  n_starts + c when safeguard candidate c
+                                  (0 Independent, 1 Popularity, 2 LocalDedup)
+                                  is returned */
     int32_t n_starts;          /* out: number of starts run */
     int64_t updates;           /* out: worker updates executed (standalone +
                                   greedy + every sweep) */
@@ -100,6 +117,10 @@ typedef struct {
     double dp_kernel_ms;       /* out with PP_F_TIME_KERNELS: summed duration
                                   of the DP-sweep launches */
     int32_t dp_launches;       /* out with PP_F_TIME_KERNELS */
+    int32_t safeguards_run;    /* out: 1 if the PP_F_SAFEGUARDS candidates were
+                                  evaluated (requester-side costs) */
+    int64_t safeguard_objective[3]; /* out: their objectives (Independent,
+                                  Popularity, LocalDedup), 0 if not run */
 } pp_stats;
 
 /* Number of starts the options select (see pp_options.n_starts). */

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libprefixplace.so")
 
 PP_OK, PP_E_ARG, PP_E_TREE, PP_E_RANGE, PP_E_OVERFLOW = 0, -1, -2, -3, -4
 PP_E_NOMEM, PP_E_DEVICE, PP_E_UNSUPPORTED = -5, -6, -7
-PP_F_VALIDATE_ONLY, PP_F_NO_REFINE, PP_F_TIME_KERNELS = 1, 2, 4
+PP_F_VALIDATE_ONLY, PP_F_NO_REFINE, PP_F_TIME_KERNELS, PP_F_SAFEGUARDS = 1, 2, 4, 8
 
 _P = ctypes.c_void_p
 
@@ -35,7 +35,9 @@ class pp_stats(ctypes.Structure):
                 ("start_objective", _P), ("start_sweeps", _P),
                 ("start_accepts", _P), ("standalone", _P), ("orders", _P),
                 ("dp_kernel_ms", ctypes.c_double),
-                ("dp_launches", ctypes.c_int32)]
+                ("dp_launches", ctypes.c_int32),
+                ("safeguards_run", ctypes.c_int32),
+                ("safeguard_objective", ctypes.c_int64 * 3)]
 
 
 class PPError(RuntimeError):
@@ -128,6 +130,8 @@ class Plan:
     orders: np.ndarray
     dp_kernel_ms: float
     dp_launches: int
+    safeguards_run: bool = False
+    safeguard_objective: tuple = (0, 0, 0)
 
 
 def _options(m, n_starts, max_rounds, order_seed, orders, flags):
@@ -155,7 +159,10 @@ def _options(m, n_starts, max_rounds, order_seed, orders, flags):
 def _plan_from(st, arrs, target, objective):
     return Plan(target=target, objective=int(objective), best_start=st.best_start,
                 n_starts=st.n_starts, updates=st.updates, dp_cells=st.dp_cells,
-                dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches, **arrs)
+                dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches,
+                safeguards_run=bool(st.safeguards_run),
+                safeguard_objective=tuple(int(x) for x in st.safeguard_objective),
+                **arrs)
 
 
 def pp_plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=8,

@@ -494,11 +494,110 @@ int choose_cells(int32_t total_stage_cells_c1, int dev, int32_t slots_lds) {
 struct PlanResult {
   std::vector<int64_t> start_obj, standalone;
   std::vector<int32_t> sweeps, accepts, orders;
-  int32_t best = 0, S = 0;
+  int32_t best = 0, S = 0;     // best: start index, or S + c for safeguard c
+  int32_t win_slot = 0;        // slot holding the returned placement
+  int64_t win_obj = 0;         // its objective
+  bool sg_run = false;         // safeguard candidates evaluated
+  int64_t sg_obj[3] = {0, 0, 0};
   int64_t updates = 0, cells = 0;
   double dp_ms = 0.0;
   int32_t dp_launches = 0;
 };
+
+// Comparator safeguards of Sec. IV-C (Algorithm 1: the candidate set also
+// holds the Independent, Popularity and LocalDedup placements when costs are
+// requester-side).  Independent and Popularity solve every worker's DP as
+// concurrent chains in scratch slots 0..m-1 and assemble the selections into
+// their candidate slot; LocalDedup runs the workers in increasing id, each
+// against the union of the earlier ones, in its own slot.  A candidate is
+// returned only if strictly better than the best start; Independent,
+// Popularity, LocalDedup break ties in that order.
+int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
+                   int32_t slot_b, int64_t cells_pass, hipStream_t st,
+                   PlanResult& res) {
+  pp_ctx* c = e.c;
+  DevState& d = e.d;
+  const size_t mn = (size_t)m * d.n;
+  PP_TRY(c->flag.ensure(64));
+  PP_HIP(hipMemsetAsync(c->flag.p, 0, 4, st));
+  PP_HIP(launch_requester_check(d.f, d.n, m, c->flag.as<int32_t>(), st));
+  int32_t mismatch = 0;
+  PP_HIP(hipMemcpyAsync(&mismatch, c->flag.p, 4, hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  if (mismatch) return PP_OK;  // source-dependent costs: no comparators
+  // keep the best start's placement out of the scratch slots
+  PP_HIP(hipMemcpyAsync(d.tgt + (size_t)slot_b * mn, d.tgt + (size_t)res.win_slot * mn,
+                        mn, hipMemcpyDeviceToDevice, st));
+  res.win_slot = slot_b;
+  std::vector<int32_t> cand_slot = {slot_b + 1, slot_b + 2, slot_b + 3};
+  {
+    std::vector<int32_t> z(3, 0);
+    PP_HIP(launch_init_slots(chain_set(cand_slot, z, z, 0, 3), d, 1, st));
+  }
+  // Independent and Popularity: every worker's DP at once
+  std::vector<int32_t> sl, wk, kk;
+  for (int32_t h = 0; h < m; ++h)
+    if (kp[h] > 0) {
+      sl.push_back(h);
+      wk.push_back(h);
+      kk.push_back(kp[h]);
+    }
+  const int gm[2] = {kGainsIndependent, kGainsPopularity};
+  for (int q = 0; q < 2; ++q) {
+    for (size_t lo = 0; lo < sl.size(); lo += kMaxChains) {
+      const size_t hi = std::min(sl.size(), lo + (size_t)kMaxChains);
+      const ChainSet set = chain_set(sl, wk, kk, lo, hi);
+      PP_HIP(launch_init_slots(set, d, 0, st));
+      PP_HIP(launch_gains(set, d, st, gm[q]));
+      PP_TRY(e.dp(set, 1));
+      PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
+      PP_HIP(launch_assemble(set, d, cand_slot[q], st));
+    }
+  }
+  {
+    std::vector<int32_t> z(2, 0), two(cand_slot.begin(), cand_slot.begin() + 2);
+    PP_HIP(launch_holder_build(chain_set(two, z, z, 0, 2), d, st));
+  }
+  // LocalDedup: workers in increasing id, each one update in slot B+3
+  for (int32_t h = 0; h < m; ++h) {
+    if (kp[h] == 0) continue;
+    const std::vector<int32_t> s1 = {cand_slot[2]}, w1 = {h}, k1 = {kp[h]};
+    const ChainSet set = chain_set(s1, w1, k1, 0, 1);
+    PP_HIP(launch_gains(set, d, st, kGainsLocalDedup));
+    PP_TRY(e.dp(set, 1));
+    PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
+    PP_HIP(launch_commit(set, d, st));
+  }
+  {
+    std::vector<int32_t> z(3, 0);
+    PP_HIP(launch_objective(chain_set(cand_slot, z, z, 0, 3), d, st));
+  }
+  std::vector<ChainState> fin(3);
+  PP_HIP(hipMemcpyAsync(fin.data(), d.cs + cand_slot[0], sizeof(ChainState) * 3,
+                        hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  // the scratch chains' status words, in case a DP wait gave up
+  std::vector<ChainState> scr(m);
+  PP_HIP(hipMemcpyAsync(scr.data(), d.cs, sizeof(ChainState) * m,
+                        hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  for (const ChainState& x : fin)
+    if (x.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+  for (const ChainState& x : scr)
+    if (x.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+  res.sg_run = true;
+  for (int q = 0; q < 3; ++q) {
+    res.sg_obj[q] = fin[q].obj;
+    if (fin[q].obj > res.win_obj) {
+      res.win_obj = fin[q].obj;
+      res.win_slot = cand_slot[q];
+      res.best = res.S + q;
+    }
+  }
+  res.updates += 3 * (int64_t)m;
+  res.cells += 3 * cells_pass;
+  return PP_OK;
+}
 
 // Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
 int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
@@ -515,7 +614,12 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     kmax = std::max(kmax, kp[h]);
     cells_pass += (int64_t)n * kp[h];
   }
-  const int32_t slots = std::max(m, S);
+  // safeguards (requester-side inputs only): after the starts, slot B keeps
+  // the best start's placement, slots B+1..B+3 the Independent, Popularity
+  // and LocalDedup candidates, and slots 0..m-1 serve as scratch chains
+  const bool sg_asked = (o.flags & PP_F_SAFEGUARDS) != 0;
+  const int32_t slot_b = std::max(m, S);
+  const int32_t slots = slot_b + (sg_asked ? 4 : 0);
   Engine e;
   e.c = c;
   e.st = st;
@@ -662,12 +766,15 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   res.best = 0;
   for (int32_t s = 1; s < S; ++s)
     if (res.start_obj[s] > res.start_obj[res.best]) res.best = s;
+  res.win_slot = res.best;
+  res.win_obj = res.start_obj[res.best];
   res.updates = m;
   res.cells = cells_pass;
   for (int32_t s = 0; s < S; ++s) {
     res.updates += (int64_t)m * (1 + res.sweeps[s]);
     res.cells += cells_pass * (1 + res.sweeps[s]);
   }
+  if (sg_asked) PP_TRY(run_safeguards(e, m, kp, slot_b, cells_pass, st, res));
   if (e.timer.on) {
     float tot = 0.f;
     for (auto& mk : e.timer.marks) {
@@ -842,6 +949,8 @@ void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
   if (stats->orders) std::copy(r.orders.begin(), r.orders.end(), stats->orders);
   stats->dp_kernel_ms = r.dp_ms;
   stats->dp_launches = r.dp_launches;
+  stats->safeguards_run = r.sg_run ? 1 : 0;
+  for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = r.sg_obj[q];
   (void)m;
 }
 
@@ -967,10 +1076,10 @@ int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     PP_TRY(run_plan(ctx, t, m, cap, o, tot < kFmaxBound, st, r));
     // best start's placement back to caller ids
     const size_t mn = (size_t)m * n;
-    PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.best * mn,
+    PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
                              target_dev, m, n, ctx->order.as<int32_t>(), st));
     PP_HIP(hipStreamSynchronize(st));
-    *objective = r.start_obj[r.best];
+    *objective = r.win_obj;
     fill_stats(stats, r, m);
     return PP_OK;
   });
@@ -1010,13 +1119,13 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
     PlanResult r;
     PP_TRY(run_plan(c, t, m, cap, o, tot < kFmaxBound, st, r));
     std::vector<uint8_t> pre(mn);
-    PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.best * mn,
+    PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
                           mn, hipMemcpyDeviceToHost, st));
     PP_HIP(hipStreamSynchronize(st));
     for (int32_t h = 0; h < m; ++h)
       for (int32_t q = 0; q < n; ++q)
         target[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
-    *objective = r.start_obj[r.best];
+    *objective = r.win_obj;
     fill_stats(stats, r, m);
     return PP_OK;
   });

@@ -42,6 +42,14 @@ constexpr int kMaxSlots = 254;
 constexpr int kDpBatch = 32;
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
+// Profit of a worker update: the exact marginal of Eq. 7, or one of the
+// requester-side comparator profits (Sec. IV-C safeguards).
+enum GainsMode : int32_t {
+  kGainsMarginal = 0,
+  kGainsIndependent = 1,
+  kGainsPopularity = 2,
+  kGainsLocalDedup = 3
+};
 
 // Scalars of one chain slot, updated on the device.
 struct ChainState {
@@ -110,7 +118,12 @@ hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
                              int clear_tgt, hipStream_t st);
 hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
                                hipStream_t st);
-hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st);
+hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st,
+                        int gmode = kGainsMarginal);
+hipError_t launch_assemble(const ChainSet& set, const DevState& d, int32_t dst,
+                           hipStream_t st);
+hipError_t launch_requester_check(const int64_t* f, int32_t n, int32_t m,
+                                  int32_t* mismatch, hipStream_t st);
 hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      uint32_t spin_limit, int store_bits, int32_t slots_lds,
                      int fmax, hipStream_t st);

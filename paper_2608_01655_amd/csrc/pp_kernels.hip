@@ -205,13 +205,40 @@ __global__ void k_holder_build(ChainSet set, DevState d) {
 // p_h(b) = sum_m Lambda_m(b) [q_{m<-h}(b) - v_m^{(-h)}(b)]_+  (Eq. 7) for
 // every preorder position, written to the chain's profit row; also the
 // incumbent's value sum_{b in T_h} p_h(b) and G(T_-h) = sum Lambda v^{(-h)}.
-__global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d) {
+// The comparator profits of the requester-side safeguards (Sec. IV-C) use
+// the same path: Independent p = Lambda_h w_h, Popularity p = Lambda_h,
+// LocalDedup p = a_h(b) + 1{b not held by another worker} Lambda_h
+// [w_h - f_h]_+ (a_h = Lambda_h min(w_h, f_h), Eq. 2; f_h the common fetch
+// cost of requester h; with one worker p = Lambda_h w_h).
+__global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmode) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
   const int h = set.worker[ci];
   const int64_t n = d.n;
   const int64_t mn = (int64_t)d.m * n;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (gmode != kGainsMarginal) {
+    if (i >= n) return;
+    const int64_t L = d.lam[(int64_t)h * n + i], Wv = d.w[(int64_t)h * n + i];
+    int64_t p;
+    if (gmode == kGainsIndependent) {
+      p = L * Wv;
+    } else if (gmode == kGainsPopularity) {
+      p = L;
+    } else if (d.m == 1) {
+      p = L * Wv;
+    } else {
+      const int src = h == 0 ? 1 : 0;
+      const int64_t F = d.f[((int64_t)src * d.m + h) * n + i];
+      bool covered = false;
+      for (int l = 0; l < d.m; ++l)
+        if (l != h && d.tgt[s * mn + (int64_t)l * n + i]) covered = true;
+      const int64_t a = L * (Wv < F ? Wv : F);
+      p = covered ? a : a + L * imax(Wv - F, 0);
+    }
+    d.profit[s * n + i] = p;
+    return;
+  }
   int64_t p = 0, g = 0, held = 0;
   if (i < n) {
     for (int r = 0; r < d.m; ++r) {
@@ -1113,6 +1140,37 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
   if (changed && r == 0) th[i] = nv;
 }
 
+// Row h of slot `dst`'s placement := the backtracked selection of chain
+// (slot, h), for every chain of the set (the per-worker comparator
+// candidates are solved in scratch slots and assembled here).
+__global__ void k_assemble(ChainSet set, DevState d, int64_t dst) {
+  const int ci = blockIdx.y;
+  const int64_t s = set.slot[ci];
+  const int h = set.worker[ci];
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i >= d.n) return;
+  d.tgt[(dst * d.m + h) * (int64_t)d.n + i] =
+      (uint8_t)((d.sel[s * (d.npad / 32) + i / 32] >> (i % 32)) & 1u);
+}
+
+// Requester-side inputs (Sec. III-B): f[src][dst][b] is the same for every
+// src != dst.  Sets *mismatch when some entry differs.
+__global__ void k_requester_check(const int64_t* __restrict__ f, int32_t n,
+                                  int32_t m, int32_t* mismatch) {
+  const int64_t mn = (int64_t)m * n;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+       x += (int64_t)gridDim.x * blockDim.x) {
+    const int dst = (int)(x / n);
+    const int64_t b = x % n;
+    const int first = dst == 0 ? 1 : 0;
+    const int64_t ref = f[((int64_t)first * m + dst) * n + b];
+    bool diff = false;
+    for (int src = first + 1; src < m; ++src)
+      if (src != dst && f[((int64_t)src * m + dst) * n + b] != ref) diff = true;
+    if (diff) *mismatch = 1;
+  }
+}
+
 // Start of a refinement sweep: no replacement accepted yet.
 __global__ void k_reset_round(ChainSet set, DevState d) {
   const int ci = threadIdx.x;
@@ -1203,9 +1261,26 @@ hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
   return hipGetLastError();
 }
 
-hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st) {
+hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st,
+                        int gmode) {
   hipLaunchKernelGGL(k_gains, grid1(d.n, 256, set.count), dim3(256), 0, st,
-                     set, d);
+                     set, d, gmode);
+  return hipGetLastError();
+}
+
+hipError_t launch_assemble(const ChainSet& set, const DevState& d, int32_t dst,
+                           hipStream_t st) {
+  hipLaunchKernelGGL(k_assemble, grid1(d.n, 256, set.count), dim3(256), 0, st,
+                     set, d, (int64_t)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_requester_check(const int64_t* f, int32_t n, int32_t m,
+                                  int32_t* mismatch, hipStream_t st) {
+  int64_t b = ((int64_t)m * n + 255) / 256;
+  if (b > 1024) b = 1024;
+  hipLaunchKernelGGL(k_requester_check, dim3((unsigned)b), dim3(256), 0, st, f,
+                     n, m, mismatch);
   return hipGetLastError();
 }
 
