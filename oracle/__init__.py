@@ -132,7 +132,7 @@ def objective(demand, recompute_cost, fetch_cost, target) -> int:
 
 
 def requester_side(fetch_cost) -> bool:
-    """Reading R14: fetch_cost[src][dst][b] equal over every src != dst."""
+    """Reading R18: fetch_cost[src][dst][b] equal over every src != dst."""
     f = _c(fetch_cost, np.int64)
     m, n = f.shape[0], f.shape[2]
     return bool(lib().ppo_requester_side(n, m, _p(f)))

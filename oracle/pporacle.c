@@ -34,15 +34,15 @@
  *   R10 ties between starts go to the earliest start.
  *   R11 fetch_cost[h][h][*] is ignored (q_{h<-h} = w_h).
  *   R13 capacity above n is capped to n.
- *   R14 the safeguard candidates are added only for requester-side inputs:
+ *   R18 the safeguard candidates are added only for requester-side inputs:
  *       fetch_cost[src][dst][b] equal over every src != dst (M = 1 counts
  *       as requester-side); f_m(b) is that common value.
- *   R15 Independent: RootedDP per worker with p = Lambda_m * w_m;
+ *   R19 Independent: RootedDP per worker with p = Lambda_m * w_m;
  *       Popularity: p = Lambda_m; LocalDedup: workers in increasing id, each
  *       RootedDP with p = a_m + 1{b not in U} Lambda_m [w_m - f_m]_+, U the
  *       union of the earlier workers' sets (the requester's own saving only,
  *       no coverage value for other requesters); capacity k_m throughout.
- *   R16 a candidate replaces the best start only if strictly better; among
+ *   R20 a candidate replaces the best start only if strictly better; among
  *       candidates the order Independent, Popularity, LocalDedup breaks ties.
  */
 #include <stdint.h>
@@ -478,7 +478,7 @@ int ppo_objective(int32_t n, int32_t m, const int64_t *demand,
 
 /* ---------------------------------------------------------- safeguards -- */
 
-/* R14: 1 when fetch_cost[src][dst][b] is the same for every src != dst. */
+/* R18: 1 when fetch_cost[src][dst][b] is the same for every src != dst. */
 int ppo_requester_side(int32_t n, int32_t m, const int64_t *fetch_cost)
 {
     for (int32_t dst = 0; dst < m; dst++) {
@@ -495,7 +495,7 @@ int ppo_requester_side(int32_t n, int32_t m, const int64_t *fetch_cost)
     return 1;
 }
 
-/* The three comparator placements of Sec. IV-C (R15), each a RootedDP per
+/* The three comparator placements of Sec. IV-C (R19), each a RootedDP per
  * worker, and their objective F (= F_pair for requester-side inputs).
  *   targets [3][m][n] out (caller ids): Independent, Popularity, LocalDedup
  *   objs    [3] out */
@@ -525,7 +525,7 @@ int ppo_candidates(int32_t n, int32_t m, const int32_t *parent,
         for (int32_t h = 0; h < m; h++) {
             const int64_t *lam = demand + (size_t)h * n;
             const int64_t *w = recompute_cost + (size_t)h * n;
-            /* f_h(b): the common off-diagonal fetch cost (R14) */
+            /* f_h(b): the common off-diagonal fetch cost (R18) */
             int32_t src = h == 0 ? 1 : 0;
             const int64_t *f = m > 1 ? fetch_cost + ((size_t)src * m + h) * n : NULL;
             for (int32_t i = 0; i < n; i++) {
@@ -835,7 +835,7 @@ int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
         if (rc != PPO_OK)
             goto out;
         sg_run = 1;
-        for (int32_t c = 0; c < 3; c++)  /* R16 */
+        for (int32_t c = 0; c < 3; c++)  /* R20 */
             if (sg_obj[c] > won_obj) {
                 won_obj = sg_obj[c];
                 won = cands + (size_t)c * m * n;

@@ -74,7 +74,7 @@ def test_localdedup_follows_the_own_saving_definition(seed):
     tg, _ = oracle.candidates(parent, lam, w, f, cap)
     m, n = lam.shape
     built = np.zeros((m, n), np.uint8)
-    for h in range(m):  # workers in increasing id (reading R15)
+    for h in range(m):  # workers in increasing id (reading R19)
         covered = built[:h].any(axis=0)
         p = [own_gain_of_local_copy(lam, w, f_req, h, b, bool(covered[b]))
              for b in range(n)]
@@ -102,7 +102,7 @@ def test_plan_returns_the_argmax_with_starts_winning_ties(seed):
     assert sg.safeguards_run and sg.safeguard_objective == tuple(objs)
     assert sg.objective == max([plain.objective] + objs)
     assert sg.objective >= plain.objective  # never worse than the starts
-    if sg.objective == plain.objective:       # ties keep the start (R16)
+    if sg.objective == plain.objective:       # ties keep the start (R20)
         assert sg.best_start == plain.best_start
         np.testing.assert_array_equal(sg.target, plain.target)
     else:
