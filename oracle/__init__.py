@@ -59,9 +59,13 @@ def lib() -> ctypes.CDLL:
                                i32, P, P, P, P, P, P, P, P, P]
         L.ppo_requester_side.argtypes = [i32, i32, P]
         L.ppo_candidates.argtypes = [i32, i32, P, P, P, P, P, P, P]
+        L.ppo_materialization_cost.argtypes = [i32, i32, P, P, P, P, P]
+        L.ppo_replan.argtypes = [i32, i32, P, P, P, P, P, P, i64, i32, i32,
+                                 u64, u32, i32, P, P, P]
         for f in (L.ppo_preorder, L.ppo_rooted_dp, L.ppo_marginal,
                   L.ppo_objective, L.ppo_orders, L.ppo_plan,
-                  L.ppo_requester_side, L.ppo_candidates):
+                  L.ppo_requester_side, L.ppo_candidates,
+                  L.ppo_materialization_cost, L.ppo_replan):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -222,6 +226,54 @@ def plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=1,
                       updates=int(info[1]), dp_cells=int(info[2]),
                       safeguards_run=bool(info[4]),
                       safeguard_objective=tuple(int(x) for x in sgo))
+
+
+def materialization_cost(recompute_cost, fetch_cost, incumbent, proposal) -> int:
+    """Reading R21: one-time cost of the proposal's chunks that the
+    incumbent does not hold at the same worker."""
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    inc = _c(incumbent, np.uint8)
+    prop = _c(proposal, np.uint8)
+    m, n = w.shape
+    out = np.zeros(1, np.int64)
+    _check(lib().ppo_materialization_cost(n, m, _p(w), _p(f), _p(inc), _p(prop),
+                                          _p(out)))
+    return int(out[0])
+
+
+@dataclass
+class ReplanResult:
+    target: np.ndarray          # the placement to use
+    proposal: np.ndarray        # the re-optimized plan
+    adopt: bool
+    incumbent_objective: int
+    proposal_objective: int
+    materialization_cost: int
+
+
+def replan(parent, demand, recompute_cost, fetch_cost, cap, incumbent, horizon,
+           *, n_starts=1, max_rounds=0, order_seed=0, flags=0, threads=1
+           ) -> ReplanResult:
+    """Epoch re-planning (Sec. IV-D; readings R21, R22)."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.int64)
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    cap = _c(cap, np.int32)
+    inc = _c(incumbent, np.uint8)
+    m, n = demand.shape
+    tgt = np.zeros((m, n), np.uint8)
+    prop = np.zeros((m, n), np.uint8)
+    res = np.zeros(4, np.int64)
+    _check(lib().ppo_replan(n, m, _p(parent), _p(demand), _p(w), _p(f), _p(cap),
+                            _p(inc), int(horizon), int(n_starts), int(max_rounds),
+                            ctypes.c_uint64(order_seed & (2**64 - 1)), int(flags),
+                            int(threads), _p(tgt), _p(prop), _p(res)))
+    return ReplanResult(target=tgt, proposal=prop, adopt=bool(res[0]),
+                        incumbent_objective=int(res[1]),
+                        proposal_objective=int(res[2]),
+                        materialization_cost=int(res[3]))
 
 
 def plan_instance(inst, **kw) -> PlanResult:

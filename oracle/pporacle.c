@@ -16,6 +16,9 @@
  *     order-diverse starts, best-candidate return   Sec. IV-B/IV-C, Theorem 3, Algorithm 1 (PrefixPlace)
  *   - comparator safeguards for requester-side
  *     costs (Independent, Popularity, LocalDedup)   Sec. IV-C, Algorithm 1; Sec. V-A (comparators)
+ *   - epoch re-planning: adopt a re-optimized plan
+ *     only if the horizon saving exceeds the one-
+ *     time cost of materializing new chunks         Sec. IV-D; Sec. V-A (break-even requests)
  *
  * Readings of points the paper leaves open (numbered as in the design notes):
  *   R1  DP ties: take b_i only if strictly better; skip wins ties.
@@ -44,6 +47,13 @@
  *       no coverage value for other requesters); capacity k_m throughout.
  *   R20 a candidate replaces the best start only if strictly better; among
  *       candidates the order Independent, Popularity, LocalDedup breaks ties.
+ *   R21 one-time cost of the newly assigned chunks: sum over (m, b) with b
+ *       in T'_m but not in T_m of c_m(b) = min(w_m(b), min over workers h !=
+ *       m holding b in the incumbent T of f_{m<-h}(b)), under the refreshed
+ *       costs.
+ *   R22 the horizon H counts epochs; the re-optimized plan T' is adopted
+ *       iff H * (G(T') - G(T)) > that cost (exact 128-bit comparison), G
+ *       evaluated under the refreshed inputs.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -560,6 +570,114 @@ int ppo_candidates(int32_t n, int32_t m, const int32_t *parent,
 out:
     free(order); free(nextpos); free(pp); free(sp);
     return rc;
+}
+
+/* ------------------------------------------------------------ re-plan -- */
+
+int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
+             const int64_t *recompute_cost, const int64_t *fetch_cost,
+             const int32_t *cap, int32_t n_starts, int32_t max_rounds,
+             uint64_t order_seed, const int32_t *orders_in, uint32_t flags,
+             int32_t threads, uint8_t *target, int64_t *objective,
+             int64_t *standalone_out, int32_t *orders_out,
+             int64_t *start_objective, int32_t *start_sweeps,
+             int32_t *start_accepts, int64_t *info, int64_t *safeguard_obj);
+
+/* R21: one-time cost of materializing the chunks of `proposal` that the
+ * incumbent does not place at the same worker (both [m][n], caller ids). */
+static unsigned __int128 materialization_cost(int32_t n, int32_t m,
+                                              const int64_t *w,
+                                              const int64_t *f,
+                                              const uint8_t *incumbent,
+                                              const uint8_t *proposal)
+{
+    unsigned __int128 total = 0;
+    for (int32_t r = 0; r < m; r++)
+        for (int32_t b = 0; b < n; b++) {
+            if (!proposal[(size_t)r * n + b] || incumbent[(size_t)r * n + b])
+                continue;
+            int64_t c = w[(size_t)r * n + b];  /* recompute */
+            for (int32_t h = 0; h < m; h++)     /* or fetch from a holder */
+                if (h != r && incumbent[(size_t)h * n + b]) {
+                    int64_t fh = f[((size_t)h * m + r) * n + b];
+                    if (fh < c)
+                        c = fh;
+                }
+            total += (uint64_t)c;
+        }
+    return total;
+}
+
+int ppo_materialization_cost(int32_t n, int32_t m, const int64_t *recompute_cost,
+                             const int64_t *fetch_cost, const uint8_t *incumbent,
+                             const uint8_t *proposal, int64_t *cost)
+{
+    if (n < 1 || m < 1 || !recompute_cost || !fetch_cost || !incumbent ||
+        !proposal || !cost)
+        return PPO_E_ARG;
+    unsigned __int128 c = materialization_cost(n, m, recompute_cost, fetch_cost,
+                                               incumbent, proposal);
+    if (c > (unsigned __int128)INT64_MAX)
+        return PPO_E_OVERFLOW;
+    *cost = (int64_t)c;
+    return PPO_OK;
+}
+
+/* Epoch re-planning (Sec. IV-D): plan the refreshed inputs with ppo_plan's
+ * options, evaluate the incumbent under them, and adopt the new plan iff the
+ * saving over `horizon` epochs exceeds the one-time materialization cost
+ * (R21, R22).
+ *   incumbent [m][n]   the current placement (caller ids)
+ *   target    [m][n]   out: the placement to use (proposal if adopted)
+ *   proposal  [m][n]   out (may be NULL): the re-optimized plan
+ *   result[4]          out: adopt (0/1), G(incumbent), G(proposal), cost */
+int ppo_replan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
+               const int64_t *recompute_cost, const int64_t *fetch_cost,
+               const int32_t *cap, const uint8_t *incumbent, int64_t horizon,
+               int32_t n_starts, int32_t max_rounds, uint64_t order_seed,
+               uint32_t flags, int32_t threads, uint8_t *target,
+               uint8_t *proposal, int64_t *result)
+{
+    if (!incumbent || !target || !result || horizon < 0)
+        return PPO_E_ARG;
+    int rc = validate(n, m, parent, demand, recompute_cost, fetch_cost, cap);
+    if (rc != PPO_OK)
+        return rc;
+    uint8_t *prop = malloc((size_t)m * n);
+    if (!prop)
+        return PPO_E_NOMEM;
+    int64_t g_new;
+    rc = ppo_plan(n, m, parent, demand, recompute_cost, fetch_cost, cap,
+                  n_starts, max_rounds, order_seed, NULL, flags, threads, prop,
+                  &g_new, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
+    if (rc != PPO_OK) {
+        free(prop);
+        return rc;
+    }
+    int64_t g_inc = objective_full(n, m, demand, recompute_cost, fetch_cost,
+                                   incumbent);
+    unsigned __int128 cost = materialization_cost(n, m, recompute_cost,
+                                                  fetch_cost, incumbent, prop);
+    if (cost > (unsigned __int128)INT64_MAX) {
+        free(prop);
+        return PPO_E_OVERFLOW;
+    }
+    /* H * (G' - G) > cost; G' - G < 0 never adopts (cost >= 0) */
+    int adopt = 0;
+    if (g_new > g_inc) {
+        unsigned __int128 gain = (unsigned __int128)(uint64_t)(g_new - g_inc) *
+                                 (uint64_t)horizon;
+        adopt = gain > cost;
+    }
+    memcpy(target, adopt ? prop : incumbent, (size_t)m * n);
+    if (proposal)
+        memcpy(proposal, prop, (size_t)m * n);
+    result[0] = adopt;
+    result[1] = g_inc;
+    result[2] = g_new;
+    result[3] = (int64_t)cost;
+    free(prop);
+    return PPO_OK;
 }
 
 /* --------------------------------------------------------------- plan -- */

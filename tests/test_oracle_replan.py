@@ -1,0 +1,163 @@
+"""Oracle pins of the epoch re-planning rule (Sec. IV-D: evaluate the
+incumbent and a re-optimized plan under refreshed demand; adopt the new plan
+only if the saving predicted over the horizon exceeds the one-time cost of
+materializing newly assigned chunks; Sec. V-A defines break-even as that
+cost divided by the per-request gain).  CPU only.
+
+The one-time cost is rebuilt here from its definition (reading R21: each new
+(worker, chunk) pays the cheaper of recomputation and a fetch from a worker
+that already holds the chunk), and the decision (reading R22) is re-derived
+with Python integers.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_01655_amd import workloads as W
+
+
+def cost_by_definition(w, f, incumbent, proposal) -> int:
+    m, n = w.shape
+    total = 0
+    for r in range(m):
+        for b in range(n):
+            if proposal[r][b] and not incumbent[r][b]:
+                options = [int(w[r][b])]
+                options += [int(f[h][r][b]) for h in range(m)
+                            if h != r and incumbent[h][b]]
+                total += min(options)
+    return total
+
+
+def random_case(seed):
+    rng = np.random.default_rng(seed)
+    m = int(rng.integers(1, 5))
+    n = int(rng.integers(1, 60))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 15, n + 1])),
+                             source_dependent=bool(seed % 3),
+                             value_range=int(rng.choice([5, 100, 10 ** 4])))
+    inc = (rng.random((m, n)) < rng.choice([0.0, 0.2, 0.6])).astype(np.uint8)
+    return inst, inc, rng
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_materialization_cost_definition(seed):
+    inst, inc, rng = random_case(seed)
+    prop = (rng.random(inc.shape) < 0.5).astype(np.uint8)
+    want = cost_by_definition(inst.recompute_cost, inst.fetch_cost, inc, prop)
+    assert oracle.materialization_cost(inst.recompute_cost, inst.fetch_cost,
+                                       inc, prop) == want
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_replan_decision_rule(seed):
+    inst, inc, rng = random_case(seed)
+    H = int(rng.choice([0, 1, 3, 50, 10 ** 6]))
+    r = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, H, n_starts=2, max_rounds=1)
+    plan = oracle.plan(inst.parent, inst.demand, inst.recompute_cost,
+                       inst.fetch_cost, inst.cap, n_starts=2, max_rounds=1)
+    np.testing.assert_array_equal(r.proposal, plan.target)
+    assert r.proposal_objective == plan.objective
+    assert r.incumbent_objective == oracle.objective(
+        inst.demand, inst.recompute_cost, inst.fetch_cost, inc)
+    c = cost_by_definition(inst.recompute_cost, inst.fetch_cost, inc, plan.target)
+    assert r.materialization_cost == c
+    gain = H * (r.proposal_objective - r.incumbent_objective)
+    assert r.adopt == (gain > c)
+    np.testing.assert_array_equal(r.target, plan.target if r.adopt else inc)
+    if H == 0:
+        assert not r.adopt
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_break_even_threshold(seed):
+    """With a positive gain G' - G the rule switches exactly at
+    H* = floor(cost / gain) + 1 epochs."""
+    inst, _, _ = random_case(100 + seed)
+    inc = np.zeros((inst.m, inst.n), np.uint8)
+    r = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, 1)
+    gain = r.proposal_objective - r.incumbent_objective
+    if gain <= 0:
+        return
+    h_star = r.materialization_cost // gain + 1
+    below = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                          inst.fetch_cost, inst.cap, inc, h_star - 1)
+    at = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                       inst.fetch_cost, inst.cap, inc, h_star)
+    assert not below.adopt and at.adopt
+
+
+def test_incumbent_equal_to_the_plan_is_kept():
+    inst = W.make_workload("tree2k")
+    plan = oracle.plan_instance(inst, n_starts=1, max_rounds=1)
+    r = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, plan.target, 10 ** 9,
+                      n_starts=1, max_rounds=1, order_seed=inst.order_seed)
+    assert r.materialization_cost == 0
+    assert r.incumbent_objective == r.proposal_objective
+    assert not r.adopt
+    np.testing.assert_array_equal(r.target, plan.target)
+
+
+def test_empty_incumbent_pays_recomputation():
+    """With nothing resident every new chunk is recomputed: the cost is the
+    proposal's total recompute cost."""
+    inst = W.make_workload("tiny")
+    inc = np.zeros((inst.m, inst.n), np.uint8)
+    r = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, 1)
+    assert r.materialization_cost == int(np.sum(inst.recompute_cost[r.proposal == 1]))
+    assert r.incumbent_objective == 0
+
+
+def test_routing_shift_scenario():
+    """The paper's evaluation shape: plan, shift part of the routing mass,
+    re-plan; the incumbent keeps its chunks, so fetches from its holders
+    can lower the one-time cost below full recomputation."""
+    inst = W.make_workload("tree2k")
+    old = oracle.plan_instance(inst, n_starts=1, max_rounds=1)
+    rng = np.random.default_rng(4)
+    lam = inst.demand.copy()
+    lam = np.roll(lam, 1, axis=0)  # 100% routing shift: worker m gets m-1's
+    r = oracle.replan(inst.parent, lam, inst.recompute_cost, inst.fetch_cost,
+                      inst.cap, old.target, 1, n_starts=1, max_rounds=1)
+    full = int(np.sum(inst.recompute_cost[(r.proposal == 1) & (old.target == 0)]))
+    assert r.materialization_cost <= full
+    assert r.proposal_objective >= r.incumbent_objective or not r.adopt
+    _ = rng
+
+
+def test_huge_horizon_uses_exact_arithmetic():
+    inst = W.make_workload("tiny")
+    inc = np.zeros((inst.m, inst.n), np.uint8)
+    r = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, 2 ** 62)
+    assert r.adopt  # the product exceeds INT64_MAX and must not wrap
+
+
+def test_negative_horizon_is_rejected():
+    inst = W.make_workload("tiny")
+    inc = np.zeros((inst.m, inst.n), np.uint8)
+    with pytest.raises(oracle.OracleError):
+        oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, -1)
+
+
+def test_equality_keeps_the_incumbent():
+    """One chunk, one worker, Lambda = 1, w = 10: the plan stores the chunk
+    (G' = 10 per epoch against G = 0) at a one-time recompute cost of 10, so
+    one epoch only breaks even -- the rule needs strictly more (R22)."""
+    parent = np.array([-1], np.int32)
+    lam = np.array([[1]], np.int64)
+    w = np.array([[10]], np.int64)
+    f = np.zeros((1, 1, 1), np.int64)
+    cap = np.array([1], np.int32)
+    inc = np.zeros((1, 1), np.uint8)
+    one = oracle.replan(parent, lam, w, f, cap, inc, 1)
+    assert (one.proposal_objective, one.incumbent_objective,
+            one.materialization_cost) == (10, 0, 10)
+    assert not one.adopt
+    assert oracle.replan(parent, lam, w, f, cap, inc, 2).adopt
