@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 3
+#define PP_ABI_VERSION 4
 
 enum {
     PP_OK = 0,
@@ -148,6 +148,38 @@ int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
             const int64_t *recompute_cost, const int64_t *fetch_cost,
             const int32_t *cap, const pp_options *opt, uint8_t *target,
             int64_t *objective, pp_stats *stats);
+
+/* Epoch re-planning (Sec. IV-D): when demand or routing changes, plan the
+ * refreshed inputs (as pp_plan, same options), evaluate the incumbent under
+ * them, and adopt the new plan only if the saving predicted over the horizon
+ * exceeds the one-time cost of materializing the newly assigned chunks:
+ *   adopt  iff  horizon * (G(T') - G(T)) > sum over (m, b) with b in T'_m
+ *               and not in T_m of c_m(b),
+ *   c_m(b) = min(w_m(b), min over workers h != m holding b in the
+ *            incumbent of f_{m<-h}(b)),
+ * G = F_pair (Eq. 6) under the refreshed inputs; the product is compared
+ * exactly (no overflow).  Arguments as pp_plan, plus
+ *   incumbent [m][n] host: the current placement (0/1; it need not be
+ *                    parent-closed or within the new capacities)
+ *   horizon          epochs over which the gain is counted (>= 0)
+ *   target    [m][n] host out: the placement to use (T' if adopted, else a
+ *                    copy of the incumbent)
+ *   proposal  [m][n] host out, may be NULL: T'
+ *   info             out, required
+ * Errors as pp_plan; PP_E_ARG for a negative horizon or an incumbent entry
+ * other than 0 and 1, PP_E_OVERFLOW if the one-time cost exceeds INT64_MAX. */
+typedef struct {
+    int32_t adopt;                 /* 1 iff T' is adopted */
+    int64_t incumbent_objective;   /* G(T) under the refreshed inputs */
+    int64_t proposal_objective;    /* G(T') */
+    int64_t materialization_cost;  /* one-time cost of T' over T, us */
+} pp_replan_info;
+
+int pp_replan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
+              const int64_t *recompute_cost, const int64_t *fetch_cost,
+              const int32_t *cap, const uint8_t *incumbent, int64_t horizon,
+              const pp_options *opt, uint8_t *target, uint8_t *proposal,
+              pp_replan_info *info, pp_stats *stats);
 
 /* One exact rooted-tree solve (Eq. 9, Theorem 1) on the GPU.
  *   parent [n] host, profit [n] host (>= 0, sum <= INT64_MAX), k >= 0;

@@ -40,6 +40,12 @@ class pp_stats(ctypes.Structure):
                 ("safeguard_objective", ctypes.c_int64 * 3)]
 
 
+class pp_replan_info(ctypes.Structure):
+    _fields_ = [("adopt", ctypes.c_int32), ("incumbent_objective", ctypes.c_int64),
+                ("proposal_objective", ctypes.c_int64),
+                ("materialization_cost", ctypes.c_int64)]
+
+
 class PPError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"prefixplace error {code}: {msg}")
@@ -72,6 +78,8 @@ def lib() -> ctypes.CDLL:
         L.pp_num_starts.argtypes = [i32, i32]
         L.pp_num_starts.restype = i32
         L.pp_plan.argtypes = [i32, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.pp_replan.argtypes = [i32, i32, _P, _P, _P, _P, _P, _P, i64, _P, _P,
+                                _P, _P, _P]
         L.pp_rooted_dp.argtypes = [i32, _P, _P, i32, _P, _P]
         L.pp_marginal.argtypes = [i32, i32, _P, _P, _P, _P, i32, _P, _P]
         L.pp_objective.argtypes = [i32, i32, _P, _P, _P, _P, _P]
@@ -83,7 +91,7 @@ def lib() -> ctypes.CDLL:
         L.pp_ctx_destroy.restype = None
         L.pp_plan_device.argtypes = [_P, i32, i32, _P, _P, _P, _P, _P, _P, _P,
                                      _P, _P, _P]
-        for f in (L.pp_plan, L.pp_rooted_dp, L.pp_marginal, L.pp_objective,
+        for f in (L.pp_plan, L.pp_replan, L.pp_rooted_dp, L.pp_marginal, L.pp_objective,
                   L.pp_orders, L.pp_ctx_create, L.pp_plan_device):
             f.restype = ctypes.c_int
         _lib = L
@@ -183,6 +191,46 @@ def pp_plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=8,
                          ctypes.byref(st)))
     del keep
     return _plan_from(st, arrs, tgt, obj.value)
+
+
+@dataclass
+class Replan:
+    target: np.ndarray          # uint8 [m][n]: the placement to use
+    proposal: np.ndarray        # uint8 [m][n]: the re-optimized plan
+    adopt: bool
+    incumbent_objective: int
+    proposal_objective: int
+    materialization_cost: int
+    plan: Plan                  # the proposal's planner statistics
+
+
+def pp_replan(parent, demand, recompute_cost, fetch_cost, cap, incumbent,
+              horizon, *, n_starts=8, max_rounds=0, order_seed=0, orders=None,
+              flags=0) -> Replan:
+    """Epoch re-planning (see pp_replan in include/prefixplace.h)."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.int64)
+    w = _c(recompute_cost, np.int64)
+    f = _c(fetch_cost, np.int64)
+    cap = _c(cap, np.int32)
+    inc = _c(incumbent, np.uint8)
+    m, n = demand.shape
+    if inc.shape != (m, n):
+        raise ValueError(f"incumbent shape {inc.shape} != {(m, n)}")
+    o, st, arrs, keep = _options(m, n_starts, max_rounds, order_seed, orders,
+                                 flags)
+    tgt = np.zeros((m, n), np.uint8)
+    prop = np.zeros((m, n), np.uint8)
+    info = pp_replan_info()
+    _check(lib().pp_replan(n, m, _p(parent), _p(demand), _p(w), _p(f), _p(cap),
+                           _p(inc), int(horizon), ctypes.byref(o), _p(tgt),
+                           _p(prop), ctypes.byref(info), ctypes.byref(st)))
+    del keep
+    return Replan(target=tgt, proposal=prop, adopt=bool(info.adopt),
+                  incumbent_objective=int(info.incumbent_objective),
+                  proposal_objective=int(info.proposal_objective),
+                  materialization_cost=int(info.materialization_cost),
+                  plan=_plan_from(st, arrs, prop, info.proposal_objective))
 
 
 def pp_rooted_dp(parent, profit, k):

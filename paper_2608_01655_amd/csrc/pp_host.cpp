@@ -499,6 +499,7 @@ struct PlanResult {
   int64_t win_obj = 0;         // its objective
   bool sg_run = false;         // safeguard candidates evaluated
   int64_t sg_obj[3] = {0, 0, 0};
+  int32_t extra_slot = -1;     // first slot reserved for the caller
   int64_t updates = 0, cells = 0;
   double dp_ms = 0.0;
   int32_t dp_launches = 0;
@@ -602,7 +603,7 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
 // Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
 int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
              const pp_options& o, bool fmax_ok, hipStream_t st,
-             PlanResult& res) {
+             PlanResult& res, int32_t extra_slots = 0) {
   const int32_t n = t.n;
   const int32_t S = num_starts(m, o.n_starts);
   res.S = S;
@@ -619,7 +620,8 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   // and LocalDedup candidates, and slots 0..m-1 serve as scratch chains
   const bool sg_asked = (o.flags & PP_F_SAFEGUARDS) != 0;
   const int32_t slot_b = std::max(m, S);
-  const int32_t slots = slot_b + (sg_asked ? 4 : 0);
+  const int32_t slots = slot_b + (sg_asked ? 4 : 0) + extra_slots;
+  res.extra_slot = extra_slots > 0 ? slot_b + (sg_asked ? 4 : 0) : -1;
   Engine e;
   e.c = c;
   e.st = st;
@@ -1126,6 +1128,110 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
       for (int32_t q = 0; q < n; ++q)
         target[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
     *objective = r.win_obj;
+    fill_stats(stats, r, m);
+    return PP_OK;
+  });
+}
+
+int pp_replan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
+              const int64_t* recompute_cost, const int64_t* fetch_cost,
+              const int32_t* cap, const uint8_t* incumbent, int64_t horizon,
+              const pp_options* opt, uint8_t* target, uint8_t* proposal,
+              pp_replan_info* info, pp_stats* stats) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
+    if (!cap || !incumbent || !target || !info)
+      return fail(PP_E_ARG, "null pointer argument");
+    if (horizon < 0) return fail(PP_E_ARG, "horizon must be >= 0");
+    const pp_options o = opt ? *opt : default_options();
+    PP_TRY(check_options(m, o));
+    for (int32_t h = 0; h < m; ++h)
+      if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
+    const size_t mn = (size_t)m * n;
+    for (size_t x = 0; x < mn; ++x)
+      if (incumbent[x] > 1) return fail(PP_E_ARG, "incumbent entries must be 0 or 1");
+    unsigned __int128 tot = 0;
+    PP_TRY(check_values(n, m, demand, recompute_cost, fetch_cost, &tot));
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    int rc = PP_OK;
+    pp_ctx* c = thread_ctx(rc);
+    if (!c) return rc;
+    hipStream_t st = c->own;
+    PP_TRY(c->up_lam.ensure(mn * 8));
+    PP_TRY(c->up_w.ensure(mn * 8));
+    PP_TRY(c->up_f.ensure(mn * m * 8));
+    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
+    PP_TRY(upload_tree(c, t, st));
+    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
+                         c->up_f.as<int64_t>(), st));
+    // the proposal: Algorithm 1 on the refreshed inputs, one slot spare
+    PlanResult r;
+    PP_TRY(run_plan(c, t, m, cap, o, tot < kFmaxBound, st, r, 1));
+    DevState d{};
+    d.n = n;
+    d.m = m;
+    d.npad = npad_of(n);
+    d.lam = c->lam.as<int64_t>();
+    d.w = c->w.as<int64_t>();
+    d.f = c->f.as<int64_t>();
+    d.tgt = c->tgt.as<uint8_t>();
+    d.v1 = c->v1.as<int64_t>();
+    d.v2 = c->v2.as<int64_t>();
+    d.h1 = c->h1.as<uint8_t>();
+    d.cs = c->cs.as<ChainState>();
+    // the incumbent, in preorder positions, into the spare slot; its
+    // objective under the refreshed inputs (Eq. 6)
+    const int32_t xs = r.extra_slot;
+    std::vector<uint8_t> pre(mn);
+    for (int32_t h = 0; h < m; ++h)
+      for (int32_t q = 0; q < n; ++q)
+        pre[(size_t)h * n + q] = incumbent[(size_t)h * n + t.order[q]];
+    PP_HIP(hipMemcpyAsync(d.tgt + (size_t)xs * mn, pre.data(), mn,
+                          hipMemcpyHostToDevice, st));
+    const std::vector<int32_t> one = {xs}, zero = {0};
+    const ChainSet inc_set = chain_set(one, zero, zero, 0, 1);
+    PP_HIP(launch_init_slots(inc_set, d, 0, st));
+    PP_HIP(launch_holder_build(inc_set, d, st));
+    PP_HIP(launch_objective(inc_set, d, st));
+    // one-time cost of the proposal's new (worker, chunk) pairs
+    PP_TRY(c->partial.ensure(1024 * 16));
+    int32_t nb = 0;
+    PP_HIP(launch_mat_cost(d, xs, r.win_slot, c->partial.p, &nb, st));
+    std::vector<unsigned __int128> part(nb);
+    ChainState inc_cs{};
+    PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, 16 * (size_t)nb,
+                          hipMemcpyDeviceToHost, st));
+    PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState),
+                          hipMemcpyDeviceToHost, st));
+    std::vector<uint8_t> prop_pre(mn);
+    PP_HIP(hipMemcpyAsync(prop_pre.data(), d.tgt + (size_t)r.win_slot * mn, mn,
+                          hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    unsigned __int128 cost = 0;
+    for (unsigned __int128 v : part) cost += v;
+    if (cost > (unsigned __int128)INT64_MAX)
+      return fail(PP_E_OVERFLOW, "materialization cost exceeds INT64_MAX");
+    // adopt iff horizon * (G(T') - G(T)) > cost, exactly
+    const int64_t g_inc = inc_cs.obj, g_new = r.win_obj;
+    bool adopt = false;
+    if (g_new > g_inc)
+      adopt = (unsigned __int128)(uint64_t)(g_new - g_inc) * (uint64_t)horizon > cost;
+    for (int32_t h = 0; h < m; ++h)
+      for (int32_t q = 0; q < n; ++q) {
+        const size_t id = (size_t)h * n + t.order[q];
+        const uint8_t v = prop_pre[(size_t)h * n + q];
+        if (proposal) proposal[id] = v;
+        target[id] = adopt ? v : incumbent[id];
+      }
+    info->adopt = adopt ? 1 : 0;
+    info->incumbent_objective = g_inc;
+    info->proposal_objective = g_new;
+    info->materialization_cost = (int64_t)cost;
     fill_stats(stats, r, m);
     return PP_OK;
   });

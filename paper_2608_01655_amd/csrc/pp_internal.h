@@ -124,6 +124,9 @@ hipError_t launch_assemble(const ChainSet& set, const DevState& d, int32_t dst,
                            hipStream_t st);
 hipError_t launch_requester_check(const int64_t* f, int32_t n, int32_t m,
                                   int32_t* mismatch, hipStream_t st);
+// partial: at least 1024 16-byte exact sums; *nblocks receives the count
+hipError_t launch_mat_cost(const DevState& d, int32_t inc, int32_t prop,
+                           void* partial, int32_t* nblocks, hipStream_t st);
 hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      uint32_t spin_limit, int store_bits, int32_t slots_lds,
                      int fmax, hipStream_t st);

@@ -1171,6 +1171,39 @@ __global__ void k_requester_check(const int64_t* __restrict__ f, int32_t n,
   }
 }
 
+// One-time cost of the chunks slot `prop` places that slot `inc` does not
+// hold at the same worker (the re-planning rule of Sec. IV-D): each pays the
+// cheaper of recomputation and a fetch from a worker holding it in `inc`.
+// Exact per-block sums (128-bit) go to partial[blockIdx.x].
+__global__ void __launch_bounds__(256) k_mat_cost(DevState d, int64_t inc, int64_t prop,
+                                                  unsigned __int128* partial) {
+  const int64_t n = d.n, mn = (int64_t)d.m * n;
+  const uint8_t* ti = d.tgt + inc * mn;
+  const uint8_t* tp = d.tgt + prop * mn;
+  unsigned __int128 acc = 0;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+       x += (int64_t)gridDim.x * blockDim.x) {
+    if (!tp[x] || ti[x]) continue;
+    const int r = (int)(x / n);
+    const int64_t i = x % n;
+    int64_t c = d.w[x];
+    for (int h = 0; h < d.m; ++h)
+      if (h != r && ti[(int64_t)h * n + i]) {
+        const int64_t fh = d.f[((int64_t)h * d.m + r) * n + i];
+        if (fh < c) c = fh;
+      }
+    acc += (uint64_t)c;
+  }
+  __shared__ unsigned __int128 part[256];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) part[threadIdx.x] += part[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) partial[blockIdx.x] = part[0];
+}
+
 // Start of a refinement sweep: no replacement accepted yet.
 __global__ void k_reset_round(ChainSet set, DevState d) {
   const int ci = threadIdx.x;
@@ -1272,6 +1305,16 @@ hipError_t launch_assemble(const ChainSet& set, const DevState& d, int32_t dst,
                            hipStream_t st) {
   hipLaunchKernelGGL(k_assemble, grid1(d.n, 256, set.count), dim3(256), 0, st,
                      set, d, (int64_t)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_mat_cost(const DevState& d, int32_t inc, int32_t prop,
+                           void* partial, int32_t* nblocks, hipStream_t st) {
+  int64_t b = ((int64_t)d.m * d.n + 255) / 256;
+  if (b > 1024) b = 1024;
+  *nblocks = (int32_t)b;
+  hipLaunchKernelGGL(k_mat_cost, dim3((unsigned)b), dim3(256), 0, st, d,
+                     (int64_t)inc, (int64_t)prop, (unsigned __int128*)partial);
   return hipGetLastError();
 }
 

@@ -281,6 +281,60 @@ def requester_fetch(m: int, n: int, us: int) -> np.ndarray:
     return f
 
 
+def _own_demand(parent: np.ndarray, demand: np.ndarray) -> np.ndarray:
+    """Requests that end at each node: its demand minus its children's."""
+    own = demand.copy()
+    for v in range(parent.shape[0] - 1, 0, -1):
+        p = parent[v]
+        if p >= 0:
+            own[:, p] -= demand[:, v]
+    return own
+
+
+def _aggregate(parent: np.ndarray, own: np.ndarray) -> np.ndarray:
+    lam = own.copy()
+    for v in range(parent.shape[0] - 1, 0, -1):
+        p = parent[v]
+        if p >= 0:
+            lam[:, p] += lam[:, v]
+    return lam
+
+
+def shift_routing(parent: np.ndarray, demand: np.ndarray, num: int,
+                  den: int) -> np.ndarray:
+    """A routing shift between epochs: at every node, num/den of the requests
+    that end there on worker m (rounded down) move to worker (m + 1) mod M;
+    the demand is then re-aggregated along prefix paths.  num = den moves
+    all routing mass.  `parent` must be preorder-labelled."""
+    own = _own_demand(parent, demand)
+    assert np.all(own >= 0), "demand is not aggregated along prefix paths"
+    moved = (own * num) // den
+    out = own - moved + np.roll(moved, 1, axis=0)
+    return _aggregate(parent, out)
+
+
+def perturb_popularity(parent: np.ndarray, demand: np.ndarray, sigma: float,
+                       rng: np.random.Generator) -> np.ndarray:
+    """A popularity perturbation between epochs: the requests ending at each
+    node are scaled by one log-normal factor exp(sigma Z) per node (shared by
+    all workers), rounded half up, then re-aggregated along prefix paths."""
+    own = _own_demand(parent, demand)
+    assert np.all(own >= 0), "demand is not aggregated along prefix paths"
+    z = np.exp(sigma * rng.standard_normal(parent.shape[0]))
+    out = np.floor(own * z[None, :] + 0.5).astype(np.int64)
+    return _aggregate(parent, out)
+
+
+def prefix_incumbent(n: int, cap: np.ndarray) -> np.ndarray:
+    """A simple resident state for re-planning tests: worker h holds the
+    first min(cap[h], n) nodes in preorder (a prefix of the preorder is
+    closed under parents)."""
+    inc = np.zeros((cap.shape[0], n), dtype=np.uint8)
+    for h, k in enumerate(cap):
+        inc[h, :min(int(k), n)] = 1
+    return inc
+
+
 # --------------------------------------------------------------------------
 # The five benchmark workloads
 # --------------------------------------------------------------------------

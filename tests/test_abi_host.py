@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(L):
     assert len(names) >= 11
     for name in names:
         assert hasattr(L, name), name
-    assert B.pp_abi_version() == 3
+    assert B.pp_abi_version() == 4
 
 
 def _validate(inst, **kw):
@@ -125,3 +125,33 @@ def test_orders_match_oracle(L, oracle_mod):
             assert B.pp_num_starts(m, S) == oracle_mod.num_starts(m, S)
             np.testing.assert_array_equal(B.pp_orders(m, S, seed, st),
                                           oracle_mod.orders(m, S, seed, st))
+
+
+def test_replan_validation(L):
+    inst = W.make_workload("tiny")
+    inc = np.zeros((inst.m, inst.n), np.uint8)
+
+    def call(incumbent=inc, horizon=1):
+        return B.pp_replan(inst.parent, inst.demand, inst.recompute_cost,
+                           inst.fetch_cost, inst.cap, incumbent, horizon,
+                           flags=B.PP_F_VALIDATE_ONLY)
+
+    r = call()
+    assert r.target.sum() == 0 and not r.adopt  # outputs untouched
+    _expect(B.PP_E_ARG, lambda: call(horizon=-1))
+    two = inc.copy()
+    two[0, 0] = 2
+    _expect(B.PP_E_ARG, lambda: call(incumbent=two))
+    bad = inst.parent.copy()
+    bad[1] = 1
+    _expect(B.PP_E_TREE, lambda: B.pp_replan(
+        bad, inst.demand, inst.recompute_cost, inst.fetch_cost, inst.cap, inc,
+        1, flags=B.PP_F_VALIDATE_ONLY))
+    P = ctypes.c_void_p
+    z = np.zeros(64, np.int64)
+    info = B.pp_replan_info()
+    rc = L.pp_replan(2, 1, z.ctypes.data_as(P), z.ctypes.data_as(P),
+                     z.ctypes.data_as(P), z.ctypes.data_as(P),
+                     z.ctypes.data_as(P), z.ctypes.data_as(P), 1, None,
+                     z.ctypes.data_as(P), None, None, None)
+    assert rc == B.PP_E_ARG  # info is required

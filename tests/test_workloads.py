@@ -54,3 +54,27 @@ def test_generator_is_deterministic():
     a = W.make_workload("tree2k")
     b = W.make_workload("tree2k")
     assert a.checksum() == b.checksum()
+
+
+def test_routing_shift_and_popularity_perturbation():
+    inst = W.make_workload("tree2k")
+    lam = inst.demand
+    full = W.shift_routing(inst.parent, lam, 1, 1)
+    np.testing.assert_array_equal(full, np.roll(lam, 1, axis=0))
+    none = W.shift_routing(inst.parent, lam, 0, 4)
+    np.testing.assert_array_equal(none, lam)
+    for num in (1, 2):
+        part = W.shift_routing(inst.parent, lam, num, 4)
+        # requests only move between workers: per-node totals are kept
+        np.testing.assert_array_equal(part.sum(axis=0), lam.sum(axis=0))
+        assert part.min() >= 0
+    rng = np.random.default_rng(3)
+    pert = W.perturb_popularity(inst.parent, lam, 0.5, rng)
+    assert pert.min() >= 0 and pert.shape == lam.shape
+    # still aggregated along prefix paths: a node covers its children
+    for v in range(1, inst.n):
+        p = inst.parent[v]
+        if p >= 0:
+            assert np.all(pert[:, p] >= pert[:, v])
+    zero = W.perturb_popularity(inst.parent, lam, 0.0, rng)
+    np.testing.assert_array_equal(zero, lam)
