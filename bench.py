@@ -4,7 +4,9 @@ One step = one full plan (standalone scores, WorkerGreedy, coordinate
 refinement until no sweep improves, best start) of the tree50k workload
 (n = 50,000 chunks, M = 16 workers, k = 4,096 each, 8 order-diverse starts,
 source-dependent fetch costs) through the device-resident C-ABI entry point,
-inputs already in HBM.  Prints one JSON line.
+inputs already in HBM.  Prints one JSON line.  After the timed region a
+re-planning leg (a 50% routing shift of the same workload, through the
+host-array entry point) adds a "replan" object; --no-replan skips it.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
@@ -116,6 +118,49 @@ def cpu_baseline(inst, cells_per_plan, threads):
     }
 
 
+def replan_leg(B, W, inst, steps, warmup):
+    """Epoch re-planning (Sec. IV-D) after a 50% routing shift, the incumbent
+    being the first k_h preorder chunks of every worker, horizon 1,000
+    epochs: the host-array entry point, so the time includes the PCIe copies
+    of the inputs and outputs (inputs: demand, costs and incumbent; outputs:
+    target and proposal)."""
+    lam = W.shift_routing(inst.parent, inst.demand, 1, 2)
+    inc = W.prefix_incumbent(inst.n, inst.cap)
+    horizon = 1000
+
+    def call():
+        return B.pp_replan(inst.parent, lam, inst.recompute_cost,
+                           inst.fetch_cost, inst.cap, inc, horizon,
+                           n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+                           order_seed=inst.order_seed)
+
+    for _ in range(warmup):
+        call()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        r = call()
+    dt = (time.perf_counter() - t0) / steps
+    out = {"ms_per_replan": dt * 1e3, "includes_pcie": True,
+           "shift": "50% routing shift", "horizon": horizon,
+           "adopt": r.adopt, "incumbent_objective": r.incumbent_objective,
+           "proposal_objective": r.proposal_objective,
+           "materialization_cost": r.materialization_cost}
+    gain = r.proposal_objective - r.incumbent_objective
+    if gain > 0:
+        out["break_even_epochs"] = r.materialization_cost // gain + 1
+    gold_path = os.path.join(ROOT, "tests", "golden", "replans.json")
+    if os.path.exists(gold_path):
+        with open(gold_path) as fh:
+            gold = json.load(fh).get(f"{inst.name}-shift50")
+        if gold:
+            out["parity_vs_golden"] = (
+                r.adopt == gold["adopt"]
+                and r.proposal_objective == gold["proposal_objective"]
+                and r.incumbent_objective == gold["incumbent_objective"]
+                and r.materialization_cost == gold["materialization_cost"])
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +172,8 @@ def main():
                     help="requester-side variant of the workload (each "
                          "requester's fetch cost taken from one source) "
                          "planned with the comparator safeguards")
+    ap.add_argument("--no-replan", action="store_true",
+                    help="skip the re-planning leg")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device (counter "
                          "calibration) and exit")
@@ -251,6 +298,10 @@ def main():
            if args.safeguards else {}),
         "paper_context": PAPER_CONTEXT,
     }
+    if not args.no_replan and not args.safeguards:
+        log("[bench] re-planning leg")
+        out["replan"] = replan_leg(B, W, inst, max(1, min(args.steps, 3)),
+                                   min(args.warmup, 1))
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         threads = max(1, min(8, os.cpu_count() or 1))

@@ -643,6 +643,9 @@ int ppo_replan(int32_t n, int32_t m, const int32_t *parent, const int64_t *deman
     int rc = validate(n, m, parent, demand, recompute_cost, fetch_cost, cap);
     if (rc != PPO_OK)
         return rc;
+    for (size_t x = 0; x < (size_t)m * n; x++)
+        if (incumbent[x] > 1)
+            return PPO_E_ARG;  /* a placement is a 0/1 matrix */
     uint8_t *prop = malloc((size_t)m * n);
     if (!prop)
         return PPO_E_NOMEM;

@@ -161,3 +161,12 @@ def test_equality_keeps_the_incumbent():
             one.materialization_cost) == (10, 0, 10)
     assert not one.adopt
     assert oracle.replan(parent, lam, w, f, cap, inc, 2).adopt
+
+
+def test_non_binary_incumbent_is_rejected():
+    inst = W.make_workload("tiny")
+    inc = np.zeros((inst.m, inst.n), np.uint8)
+    inc[1, 3] = 2
+    with pytest.raises(oracle.OracleError):
+        oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, 1)
