@@ -82,12 +82,13 @@ struct DevBuf {
 struct TreeLayout {
   int32_t n = 0;
   std::vector<int32_t> order, nextpos;
-  // the backtrack's skip chains inside 32-row windows [32w, 32w + 32):
-  // chain[q] has bit r set for every row 32w + r of q, next(q), next(next(q)),
-  // ... that lies in q's window; exitr[q] is the first row of that sequence
-  // past the window (>= n: past the end)
-  std::vector<uint32_t> chain;
-  std::vector<int32_t> exitr;
+  // the backtrack's skip chains inside 32-row windows [32w, 32w + 32), as
+  // pairs ce[2q] = chain mask, ce[2q + 1] = exit row: the mask has bit r set
+  // for every row 32w + r of q, next(q), next(next(q)), ... that lies in q's
+  // window; the exit row is the first row of that sequence past the window
+  // (>= n: past the end).  Padded with empty rows (mask 0, exit n) through
+  // one 512-row block past the last full block.
+  std::vector<uint32_t> ce;
   // per padded DP step: leaf flag (next(i) = i+1), the LDS slot the row is
   // stored to (-1: a sink row), and the slot holding the next step's skip
   // operand (-1: the zero row, or the next step is a leaf)
@@ -139,14 +140,15 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
     t.nextpos[q] = q + size[q];
     if (t.order[q] != q) t.identity = false;
   }
-  t.chain.assign(n, 0);
-  t.exitr.assign(n, 0);
+  const size_t ce_rows = ((size_t)n + kCeBlock - 1) / kCeBlock * kCeBlock + kCeBlock;
+  t.ce.assign(2 * ce_rows, 0);
+  for (size_t q = n; q < ce_rows; ++q) t.ce[2 * q + 1] = (uint32_t)n;
   for (int32_t q = n - 1; q >= 0; --q) {
     const int32_t wend = std::min<int32_t>((q / 32 + 1) * 32, n);
     const int32_t nq = t.nextpos[q];  // > q
     const bool inside = nq < wend;
-    t.chain[q] = (1u << (q % 32)) | (inside ? t.chain[nq] : 0u);
-    t.exitr[q] = inside ? t.exitr[nq] : nq;
+    t.ce[2 * q] = (1u << (q % 32)) | (inside ? t.ce[2 * nq] : 0u);
+    t.ce[2 * q + 1] = inside ? t.ce[2 * nq + 1] : (uint32_t)nq;
   }
   // DP metadata.  Rows are 1-based positions i; nx(i) = next(i); row i is
   // produced at padded step pad + n - i.  A row r = next(a) with r != a+1
@@ -303,7 +305,7 @@ struct pp_ctx {
   int device = 0;
   hipStream_t own = nullptr;
   // problem, preorder layout
-  DevBuf lam, w, f, nextpos, chain, exitr, meta, order;
+  DevBuf lam, w, f, nextpos, ce, meta, order;
   // uploads for host-pointer entry points (caller order)
   DevBuf up_lam, up_w, up_f, up_u8;
   // per-slot state
@@ -313,7 +315,7 @@ struct pp_ctx {
   std::vector<uint32_t> meta_host;  // source of the last metadata upload
   std::vector<hipEvent_t> events;
   ~pp_ctx() {
-    for (DevBuf* b : {&lam, &w, &f, &nextpos, &chain, &exitr, &meta, &order, &up_lam, &up_w,
+    for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
                       &ring, &cs, &partial, &flag})
       b->release();
@@ -637,8 +639,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   d.w = c->w.as<int64_t>();
   d.f = c->f.as<int64_t>();
   d.nextpos = c->nextpos.as<int32_t>();
-  d.chain = c->chain.as<uint32_t>();
-  d.exitr = c->exitr.as<int32_t>();
+  d.ce = c->ce.as<uint32_t>();
   // widest single launch: every start's update at once
   int64_t stage64 = 0;
   {
@@ -875,13 +876,12 @@ pp_ctx* thread_ctx(int& rc) {
 int upload_tree(pp_ctx* c, const TreeLayout& t, hipStream_t st) {
   const size_t n = (size_t)t.n;
   PP_TRY(c->nextpos.ensure(n * 4));
-  PP_TRY(c->chain.ensure(n * 4));
-  PP_TRY(c->exitr.ensure(n * 4));
+  PP_TRY(c->ce.ensure(t.ce.size() * 4));
   PP_TRY(c->order.ensure(n * 4));
   PP_HIP(hipMemcpyAsync(c->nextpos.p, t.nextpos.data(), n * 4,
                         hipMemcpyHostToDevice, st));
-  PP_HIP(hipMemcpyAsync(c->chain.p, t.chain.data(), n * 4, hipMemcpyHostToDevice, st));
-  PP_HIP(hipMemcpyAsync(c->exitr.p, t.exitr.data(), n * 4, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->ce.p, t.ce.data(), t.ce.size() * 4, hipMemcpyHostToDevice,
+                        st));
 
   PP_HIP(hipMemcpyAsync(c->order.p, t.order.data(), n * 4, hipMemcpyHostToDevice, st));
   return PP_OK;
@@ -1270,8 +1270,7 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     d.m = 1;
     d.npad = npad_of(n);
     d.nextpos = c->nextpos.as<int32_t>();
-    d.chain = c->chain.as<uint32_t>();
-    d.exitr = c->exitr.as<int32_t>();
+    d.ce = c->ce.as<uint32_t>();
     const int32_t slots_lds = t.slots;
     const int cells = choose_cells((kp + 63) / 64, c->device, slots_lds);
     PP_TRY(ensure_slots(c, d, 1, kp, cells));

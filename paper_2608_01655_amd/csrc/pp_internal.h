@@ -40,6 +40,8 @@ constexpr int kMaxSlots = 254;
 // to a multiple of it with leading dummy steps (leaf, profit 0), so step s
 // of the tree is padded step s + pad, pad = nsteps - n.
 constexpr int kDpBatch = 32;
+// Rows per block of the backtrack's staged chain table (16 windows of 32).
+constexpr int kCeBlock = 512;
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
 // Profit of a worker update: the exact marginal of Eq. 7, or one of the
@@ -80,9 +82,11 @@ struct DevState {
   const int64_t* w;         // [m][n]     recompute cost, preorder
   const int64_t* f;         // [m][m][n]  fetch cost [src][dst][pos]
   const int32_t* nextpos;   // [n]        0-based first position after subtree
-  const uint32_t* chain;    // [n]        backtrack skip chain of q in its
-                            //            32-row window (bit per row)
-  const int32_t* exitr;     // [n]        first row of that chain past the window
+  const uint32_t* ce;       // [nce][2]   backtrack skip chain of q in its
+                            //            32-row window (bit per row), and the
+                            //            first row of that chain past the
+                            //            window; nce = n rounded up to
+                            //            kCeBlock, plus kCeBlock empty rows
   const uint32_t* meta;     // [nsteps][4] per-step DP metadata
   uint8_t* tgt;             // [slots][m][n] placement, preorder
   int64_t* v1;              // [slots][m][n] best holder saving

@@ -801,128 +801,214 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
 // Row sets of 32 consecutive rows (windows) are staged in LDS: for window k
 // and lane l, the chain mask and exit row of row q_lo + 32k + (l mod 32) at
 // ace + 256k (exit at +4), and lane l's choice word of cell c at
-// aw + 256(Ck + c).  Each pass over window wk loads those, then finds the
-// takes: the next take is the lowest set bit of (word of cell rem & chain
-// mask of q); it is recorded (bit of tm), the walk moves to the row after
-// it and to cell rem-1.  Without a set bit the walk leaves the window at
-// the chain's exit row.  When the window changes, tm goes to lane wk of tw
-// and is cleared.  The walk returns when q reaches n, when rem wraps below
-// zero (it leaves the stage), or when q leaves the super-window (wk >= 16).
-// On entry wk < 16, q lies in window wk, rem >= 0 and q < n.  Every pass
-// raises q, so each window takes at most 32 passes.
-#define PP_WALK_SW(LOADW, COLWORD)                               \
-  "10:\n\t"                                                      \
-  "s_lshl_b32 %[off], %[wk], 8\n\t"                              \
+// aw + 256(Ck + c).  In window wk the walk reads those into registers, then
+// finds the takes: the next take is the lowest set bit of (word of cell rem
+// & chain mask of q); it is recorded (bit of tm), the walk moves to the row
+// after it and to cell rem-1.  Without a set bit the walk leaves the window
+// at the chain's exit row.  When the window changes, tm goes to lane wk of
+// tw and is cleared.  The walk returns when q reaches n, when rem wraps
+// below zero (it leaves the stage), or when q leaves the super-window
+// (wk >= 16).  On entry wk < 16, q lies in window wk, rem >= 0 and q < n.
+// Every pass raises q, so each window takes at most 32 passes.
+//
+// Nearly every window change goes to the next window, so two register sets
+// alternate: while the walk uses one (labels 11-19), the other already
+// holds window wk + 1 (labels 21-29); a move to the next window switches
+// sets and starts reading window wk + 2 into the one just left, and only
+// another move (a long skip) waits for LDS.  The lane-select operand of
+// v_writelane is m0 (one scalar operand besides the value); m0 is saved and
+// restored around the walk.
+#define PP_WALK_CE(S, IDX)                                       \
+  "s_lshl_b32 %[off], %[" IDX "], 8\n\t"                         \
   "v_add_u32_e32 %[va], %[off], %[ace]\n\t"                      \
-  "ds_read_b32 %[ch], %[va]\n\t"                                 \
-  "ds_read_b32 %[ex], %[va] offset:4\n\t"                        \
-  LOADW                                                          \
+  "ds_read_b32 %[ch" S "], %[va]\n\t"                            \
+  "ds_read_b32 %[ex" S "], %[va] offset:4\n\t"
+// window wk + 1, or window 15 when wk is the last one (never walked then)
+#define PP_WALK_NEXT                                             \
+  "s_add_u32 %[nx], %[wk], 1\n\t"                                \
+  "s_min_u32 %[nx], %[nx], 15\n\t"
+#define PP_WALK_ROW                                              \
   "s_lshl_b32 %[wlo], %[wk], 5\n\t"                              \
   "s_add_u32 %[wlo], %[wlo], %[qlo]\n\t"                         \
-  "s_sub_u32 %[r], %[q], %[wlo]\n\t"                             \
-  "s_waitcnt lgkmcnt(0)\n\t"                                     \
-  COLWORD                                                        \
-  "v_readlane_b32 %[m], %[ch], %[r]\n\t"                         \
-  "11:\n\t"                                                      \
+  "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+// takes inside the window of set S; leaves q at the row after the window's
+// walk (label T+2 / T+3 are the take-exit and no-take exits)
+#define PP_WALK_TAKES(S, T, COLW)                                \
+  COLW                                                           \
+  "v_readlane_b32 %[m], %[ch" S "], %[r]\n\t"                    \
+  T "1:\n\t"                                                     \
   "s_and_b32 %[m], %[m], %[w]\n\t"                               \
-  "s_cbranch_scc0 13f\n\t"                                       \
+  "s_cbranch_scc0 " T "3f\n\t"                                   \
   "s_ff1_i32_b32 %[t], %[m]\n\t"                                 \
   "s_bitset1_b32 %[tm], %[t]\n\t"                                \
   "s_add_u32 %[r], %[t], 1\n\t"                                  \
   "s_sub_u32 %[rem], %[rem], 1\n\t"                              \
-  "s_cbranch_scc1 12f\n\t"                                       \
-  COLWORD                                                        \
-  "v_readlane_b32 %[m], %[ch], %[r]\n\t"                         \
+  "s_cbranch_scc1 " T "2f\n\t"                                   \
+  COLW                                                           \
+  "v_readlane_b32 %[m], %[ch" S "], %[r]\n\t"                    \
   "s_cmp_lg_u32 %[r], 32\n\t"                                    \
-  "s_cbranch_scc1 11b\n\t"                                       \
-  "12:\n\t"                                                      \
+  "s_cbranch_scc1 " T "1b\n\t"                                   \
+  T "2:\n\t"                                                     \
   "s_add_u32 %[q], %[wlo], %[r]\n\t"                             \
-  "s_branch 14f\n\t"                                             \
-  "13:\n\t"                                                      \
-  "v_readlane_b32 %[q], %[ex], %[r]\n\t"                         \
-  "14:\n\t"                                                      \
+  "s_branch " T "4f\n\t"                                         \
+  T "3:\n\t"                                                     \
+  "v_readlane_b32 %[q], %[ex" S "], %[r]\n\t"                    \
+  T "4:\n\t"                                                     \
   "s_cmp_ge_u32 %[q], %[n]\n\t"                                  \
-  "s_cbranch_scc1 19f\n\t"                                       \
+  "s_cbranch_scc1 99f\n\t"                                       \
   "s_sub_u32 %[r], %[q], %[qlo]\n\t"                             \
   "s_lshr_b32 %[r], %[r], 5\n\t"                                 \
   "s_cmp_eq_u32 %[r], %[wk]\n\t"                                 \
-  "s_cbranch_scc1 15f\n\t"                                       \
+  "s_cbranch_scc1 " T "5f\n\t"                                   \
   "s_mov_b32 m0, %[wk]\n\t"                                      \
-  "v_writelane_b32 %[tw], %[tm], m0\n\t"                        \
+  "v_writelane_b32 %[tw], %[tm], m0\n\t"                         \
   "s_mov_b32 %[tm], 0\n\t"                                       \
+  "s_add_u32 %[t], %[wk], 1\n\t"                                 \
   "s_mov_b32 %[wk], %[r]\n\t"                                    \
-  "15:\n\t"                                                      \
   "s_cmp_lt_i32 %[rem], 0\n\t"                                   \
-  "s_cbranch_scc1 19f\n\t"                                       \
-  "s_cmp_lt_u32 %[wk], 16\n\t"                                   \
-  "s_cbranch_scc1 10b\n\t"                                       \
-  "19:"
+  "s_cbranch_scc1 99f\n\t"                                       \
+  "s_cmp_ge_u32 %[wk], 16\n\t"                                   \
+  "s_cbranch_scc1 99f\n\t"                                       \
+  "s_cmp_eq_u32 %[wk], %[t]\n\t"                                 \
+  "s_cbranch_scc0 10b\n\t"                                       \
+  "s_branch " T "6f\n\t"                                         \
+  T "5:\n\t"                                                     \
+  "s_cmp_lt_i32 %[rem], 0\n\t"                                   \
+  "s_cbranch_scc1 99f\n\t"                                       \
+  "s_branch 10b\n\t"                                             \
+  T "6:\n\t"
+
+// LDW(S, IDX): read window IDX's choice words into set S; COLW(S): the word
+// of cell rem from set S into w
+#define PP_WALK_SW(LDW, COLW)                                    \
+  "s_mov_b32 %[sm0], m0\n\t"                                     \
+  "10:\n\t"                                                      \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
+  PP_WALK_CE("P", "wk")                                          \
+  LDW("P", "wk")                                                 \
+  PP_WALK_NEXT                                                   \
+  PP_WALK_CE("N", "nx")                                          \
+  LDW("N", "nx")                                                 \
+  PP_WALK_ROW                                                    \
+  "s_waitcnt lgkmcnt(" PP_WALK_NREAD ")\n\t"                     \
+  "30:\n\t"                                                      \
+  PP_WALK_TAKES("P", "1", COLW("P"))                             \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
+  PP_WALK_NEXT                                                   \
+  PP_WALK_CE("P", "nx")                                          \
+  LDW("P", "nx")                                                 \
+  PP_WALK_ROW                                                    \
+  PP_WALK_TAKES("N", "2", COLW("N"))                             \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
+  PP_WALK_NEXT                                                   \
+  PP_WALK_CE("N", "nx")                                          \
+  LDW("N", "nx")                                                 \
+  PP_WALK_ROW                                                    \
+  "s_branch 30b\n\t"                                             \
+  "99:\n\t"                                                      \
+  "s_mov_b32 m0, %[sm0]"
 
 #define PP_WALK_OPERANDS                                                          \
   [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [wk] "+s"(wk), [tw] "+v"(tw),      \
       [r] "=&s"(r), [m] "=&s"(m), [w] "=&s"(w), [t] "=&s"(t), [off] "=&s"(off),   \
-      [wlo] "=&s"(wlo), [va] "=&v"(va), [ch] "=&v"(ch), [ex] "=&v"(ex)
+      [wlo] "=&s"(wlo), [nx] "=&s"(nx), [sm0] "=&s"(sm0), [va] "=&v"(va),         \
+      [chP] "=&v"(chP), [exP] "=&v"(exP), [chN] "=&v"(chN), [exN] "=&v"(exN),     \
+      [vb] "=&v"(vb)
+#define PP_WALK_INPUTS \
+  [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
+
+#define PP_LDW1(S, IDX)                                          \
+  "s_lshl_b32 %[offw], %[" IDX "], 8\n\t"                        \
+  "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"                      \
+  "ds_read_b32 %[w" S "0], %[vb]\n\t"
+#define PP_COLW1(S) "v_readlane_b32 %[w], %[w" S "0], %[rem]\n\t"
 
 __device__ __forceinline__ void walk_sw_c1(uint32_t& q, uint32_t& rem, uint32_t& tm,
                                            uint32_t& wk, uint32_t& tw, uint32_t qlo,
                                            uint32_t n, uint32_t ace, uint32_t aw) {
-  uint32_t r, m, w, t, off, wlo, va, ch, ex, vb, wc0;
-  asm volatile(PP_WALK_SW("v_add_u32_e32 %[vb], %[off], %[aw]\n\t"
-                          "ds_read_b32 %[wc0], %[vb]\n\t",
-                          "v_readlane_b32 %[w], %[wc0], %[rem]\n\t")
-               : PP_WALK_OPERANDS, [vb] "=&v"(vb), [wc0] "=&v"(wc0)
-               : [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
-               : "scc", "m0");
+  uint32_t r, m, w, t, off, wlo, nx, sm0, va, chP, exP, chN, exN, vb, offw, wP0, wN0;
+#define PP_WALK_NREAD "3"
+  asm volatile(PP_WALK_SW(PP_LDW1, PP_COLW1)
+               : PP_WALK_OPERANDS, [offw] "=&s"(offw), [wP0] "=&v"(wP0), [wN0] "=&v"(wN0)
+               : PP_WALK_INPUTS
+               : "scc");
+#undef PP_WALK_NREAD
 }
 
 // two and four cells per lane: cell rem is lane rem/C of word rem mod C
+#define PP_LDW2(S, IDX)                                          \
+  "s_lshl_b32 %[offw], %[" IDX "], 9\n\t"                        \
+  "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"                      \
+  "ds_read_b32 %[w" S "0], %[vb]\n\t"                            \
+  "ds_read_b32 %[w" S "1], %[vb] offset:256\n\t"
+#define PP_COLW2(S)                                              \
+  "s_lshr_b32 %[ln], %[rem], 1\n\t"                              \
+  "v_readlane_b32 %[w], %[w" S "0], %[ln]\n\t"                   \
+  "v_readlane_b32 %[w1], %[w" S "1], %[ln]\n\t"                  \
+  "s_bitcmp1_b32 %[rem], 0\n\t"                                  \
+  "s_cselect_b32 %[w], %[w1], %[w]\n\t"
+
 __device__ __forceinline__ void walk_sw_c2(uint32_t& q, uint32_t& rem, uint32_t& tm,
                                            uint32_t& wk, uint32_t& tw, uint32_t qlo,
                                            uint32_t n, uint32_t ace, uint32_t aw) {
-  uint32_t r, m, w, t, off, wlo, va, ch, ex, vb, wc0, wc1, ln, w1, offw;
-  asm volatile(PP_WALK_SW("s_lshl_b32 %[offw], %[wk], 9\n\t"
-                          "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"
-                          "ds_read_b32 %[wc0], %[vb]\n\t"
-                          "ds_read_b32 %[wc1], %[vb] offset:256\n\t",
-                          "s_lshr_b32 %[ln], %[rem], 1\n\t"
-                          "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
-                          "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
-                          "s_bitcmp1_b32 %[rem], 0\n\t"
-                          "s_cselect_b32 %[w], %[w1], %[w]\n\t")
-               : PP_WALK_OPERANDS, [vb] "=&v"(vb), [wc0] "=&v"(wc0), [wc1] "=&v"(wc1),
-                 [ln] "=&s"(ln), [w1] "=&s"(w1), [offw] "=&s"(offw)
-               : [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
-               : "scc", "m0");
+  uint32_t r, m, w, t, off, wlo, nx, sm0, va, chP, exP, chN, exN, vb, offw, ln, w1;
+  uint32_t wP0, wP1, wN0, wN1;
+#define PP_WALK_NREAD "4"
+  asm volatile(PP_WALK_SW(PP_LDW2, PP_COLW2)
+               : PP_WALK_OPERANDS, [offw] "=&s"(offw), [ln] "=&s"(ln), [w1] "=&s"(w1),
+                 [wP0] "=&v"(wP0), [wP1] "=&v"(wP1), [wN0] "=&v"(wN0), [wN1] "=&v"(wN1)
+               : PP_WALK_INPUTS
+               : "scc");
+#undef PP_WALK_NREAD
 }
+
+#define PP_LDW4(S, IDX)                                          \
+  "s_lshl_b32 %[offw], %[" IDX "], 10\n\t"                       \
+  "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"                      \
+  "ds_read_b32 %[w" S "0], %[vb]\n\t"                            \
+  "ds_read_b32 %[w" S "1], %[vb] offset:256\n\t"                 \
+  "ds_read_b32 %[w" S "2], %[vb] offset:512\n\t"                 \
+  "ds_read_b32 %[w" S "3], %[vb] offset:768\n\t"
+#define PP_COLW4(S)                                              \
+  "s_lshr_b32 %[ln], %[rem], 2\n\t"                              \
+  "v_readlane_b32 %[w], %[w" S "0], %[ln]\n\t"                   \
+  "v_readlane_b32 %[w1], %[w" S "1], %[ln]\n\t"                  \
+  "v_readlane_b32 %[w2], %[w" S "2], %[ln]\n\t"                  \
+  "v_readlane_b32 %[w3], %[w" S "3], %[ln]\n\t"                  \
+  "s_bitcmp1_b32 %[rem], 1\n\t"                                  \
+  "s_cselect_b32 %[w], %[w2], %[w]\n\t"                          \
+  "s_cselect_b32 %[w1], %[w3], %[w1]\n\t"                        \
+  "s_bitcmp1_b32 %[rem], 0\n\t"                                  \
+  "s_cselect_b32 %[w], %[w1], %[w]\n\t"
 
 __device__ __forceinline__ void walk_sw_c4(uint32_t& q, uint32_t& rem, uint32_t& tm,
                                            uint32_t& wk, uint32_t& tw, uint32_t qlo,
                                            uint32_t n, uint32_t ace, uint32_t aw) {
-  uint32_t r, m, w, t, off, wlo, va, ch, ex, vb, wc0, wc1, wc2, wc3, ln, w1, w2, w3, offw;
-  asm volatile(PP_WALK_SW("s_lshl_b32 %[offw], %[wk], 10\n\t"
-                          "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"
-                          "ds_read_b32 %[wc0], %[vb]\n\t"
-                          "ds_read_b32 %[wc1], %[vb] offset:256\n\t"
-                          "ds_read_b32 %[wc2], %[vb] offset:512\n\t"
-                          "ds_read_b32 %[wc3], %[vb] offset:768\n\t",
-                          "s_lshr_b32 %[ln], %[rem], 2\n\t"
-                          "v_readlane_b32 %[w], %[wc0], %[ln]\n\t"
-                          "v_readlane_b32 %[w1], %[wc1], %[ln]\n\t"
-                          "v_readlane_b32 %[w2], %[wc2], %[ln]\n\t"
-                          "v_readlane_b32 %[w3], %[wc3], %[ln]\n\t"
-                          "s_bitcmp1_b32 %[rem], 1\n\t"
-                          "s_cselect_b32 %[w], %[w2], %[w]\n\t"
-                          "s_cselect_b32 %[w1], %[w3], %[w1]\n\t"
-                          "s_bitcmp1_b32 %[rem], 0\n\t"
-                          "s_cselect_b32 %[w], %[w1], %[w]\n\t")
-               : PP_WALK_OPERANDS, [vb] "=&v"(vb), [wc0] "=&v"(wc0), [wc1] "=&v"(wc1),
-                 [wc2] "=&v"(wc2), [wc3] "=&v"(wc3), [ln] "=&s"(ln), [w1] "=&s"(w1),
-                 [w2] "=&s"(w2), [w3] "=&s"(w3), [offw] "=&s"(offw)
-               : [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
-               : "scc", "m0");
+  uint32_t r, m, w, t, off, wlo, nx, sm0, va, chP, exP, chN, exN, vb, offw, ln, w1, w2, w3;
+  uint32_t wP0, wP1, wP2, wP3, wN0, wN1, wN2, wN3;
+#define PP_WALK_NREAD "6"
+  asm volatile(PP_WALK_SW(PP_LDW4, PP_COLW4)
+               : PP_WALK_OPERANDS, [offw] "=&s"(offw), [ln] "=&s"(ln), [w1] "=&s"(w1),
+                 [w2] "=&s"(w2), [w3] "=&s"(w3), [wP0] "=&v"(wP0), [wP1] "=&v"(wP1),
+                 [wP2] "=&v"(wP2), [wP3] "=&v"(wP3), [wN0] "=&v"(wN0), [wN1] "=&v"(wN1),
+                 [wN2] "=&v"(wN2), [wN3] "=&v"(wN3)
+               : PP_WALK_INPUTS
+               : "scc");
+#undef PP_WALK_NREAD
 }
 #undef PP_WALK_OPERANDS
+#undef PP_WALK_INPUTS
 #undef PP_WALK_SW
+#undef PP_WALK_TAKES
+#undef PP_WALK_ROW
+#undef PP_WALK_NEXT
+#undef PP_WALK_CE
+#undef PP_LDW1
+#undef PP_COLW1
+#undef PP_LDW2
+#undef PP_COLW2
+#undef PP_LDW4
+#undef PP_COLW4
 
 // Acceptance (greedy: always; refinement: DP value > incumbent value, which
 // by Proposition 1 is G(T_-h, T'_h) > G(T)) and, when accepted, the walk
@@ -937,10 +1023,11 @@ __device__ __forceinline__ void walk_sw_c4(uint32_t& q, uint32_t& rem, uint32_t&
 // & mask), and without one the walk leaves the window at the sequence's
 // precomputed exit row: the scalar walk advances per take, not per row.
 // Rows are staged in super-windows of 512: the words of the current stage
-// and the masks and exit rows of the 512 rows go to LDS, and the next
-// super-window of the same stage is loaded from memory into registers while
-// this one is walked (rows only increase along the walk).  When j leaves
-// the stage, the words are reloaded for the stage below.  Taken rows are
+// and the masks and exit rows of the 512 rows go to LDS.  While one is
+// walked, two successors are loaded from memory into registers: the next
+// super-window of the same stage (rows only increase along the walk) and
+// the same super-window of the stage below (j only decreases, and leaves
+// the stage after at most 64C takes).  Taken rows are
 // gathered per window (lane k of tw: window k of the super-window) and
 // written as a bitmap when the walk leaves the super-window.
 template <int C>
@@ -949,12 +1036,12 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   constexpr int kWin = kDpBatch;        // rows per choice word
   constexpr int kSwWin = 16;            // windows per super-window
   constexpr int kSw = kWin * kSwWin;    // rows per super-window
-  constexpr int kNx = kSw / kWave;      // chain / exit registers per lane
-  constexpr int kW = C * kSwWin;        // choice-word registers per lane
+  static_assert(kSw == kCeBlock, "the chain table is padded per super-window");
+  constexpr int kW = C * 4;             // 16-byte word loads per lane
   constexpr int kStage = kWave * C;     // cells per stage
   static_assert(kWin == 32 && kSwWin == 16, "the scalar walk's window layout");
-  __shared__ uint32_t s_words[kSwWin][C][kWave];
-  __shared__ uint32_t s_ce[kSw][2];  // chain mask, exit row
+  __shared__ __attribute__((aligned(16))) uint32_t s_words[kSwWin][C][kWave];
+  __shared__ __attribute__((aligned(16))) uint32_t s_ce[kSw][2];  // chain mask, exit row
   const int ci = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t slot = set.slot[ci];
@@ -981,38 +1068,41 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   const int64_t cstride = 2 * (int64_t)d.npad;
   const uint32_t* bw = (const uint32_t*)d.bits + slot * d.stages * (int64_t)C * cstride;
 
-  // window wq = rows [32 wq, 32 wq + 32) = sweep batch nwin-1-wq.  Rows
-  // past the end are never walked; their loads are clamped into range.
-  auto load_words = [&](int sw, int g, uint32_t (&w)[kW]) {
-    const uint32_t* base = bw + (int64_t)g * C * cstride + lane;
+  // Window k of super-window sw is sweep batch nwin-1-(16 sw + k), so the
+  // 16 windows are 16 consecutive batches: 64 lanes x 4 KB per cell, read
+  // as four 16-byte loads per lane (load i, lane l: batch blo + 4i + l/16 =
+  // window 15 - 4i - l/16, columns 4(l mod 16) .. +3).  Windows past the
+  // last row are never walked; their loads are clamped into range.
+  auto load_words = [&](int sw, int g, pp_u32x4 (&w)[kW]) {
+    const int blo = nwin - kSwWin - sw * kSwWin;
+    const uint32_t* base = bw + (int64_t)g * C * cstride + 4 * (lane % 16);
 #pragma unroll
-    for (int k = 0; k < kSwWin; ++k) {
-      const int b = max(nwin - 1 - (sw * kSwWin + k), 0);
+    for (int i = 0; i < 4; ++i) {
+      const int b = max(blo + 4 * i + lane / 16, 0);
 #pragma unroll
-      for (int c = 0; c < C; ++c) w[c * kSwWin + k] = base[c * cstride + (int64_t)b * kWave];
+      for (int c = 0; c < C; ++c)
+        w[c * 4 + i] = *(const pp_u32x4*)(base + c * cstride + (int64_t)b * kWave);
     }
   };
-  auto load_chain = [&](int sw, uint32_t (&ch)[kNx], int (&ex)[kNx]) {
+  // chain masks and exit rows of the super-window's 512 rows (the host pads
+  // the table with empty rows through one super-window past the end)
+  auto load_chain = [&](int sw, pp_u32x4 (&ce)[4]) {
+    const pp_u32x4* src = (const pp_u32x4*)d.ce + (int64_t)sw * (kSw / 2);
 #pragma unroll
-    for (int t = 0; t < kNx; ++t) {
-      // rows past the end: no take, and the walk leaves at row n
-      const int q = sw * kSw + t * kWave + lane;
-      ch[t] = q < n ? d.chain[q] : 0u;
-      ex[t] = q < n ? d.exitr[q] : n;
+    for (int i = 0; i < 4; ++i) ce[i] = src[i * kWave + lane];
+  };
+  auto words_to_lds = [&](const pp_u32x4 (&w)[kW]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = kSwWin - 1 - (4 * i + lane / 16);
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+        *(pp_u32x4*)&s_words[k][c][4 * (lane % 16)] = w[c * 4 + i];
     }
   };
-  auto words_to_lds = [&](const uint32_t (&w)[kW]) {
+  auto chain_to_lds = [&](const pp_u32x4 (&ce)[4]) {
 #pragma unroll
-    for (int k = 0; k < kSwWin; ++k)
-#pragma unroll
-      for (int c = 0; c < C; ++c) s_words[k][c][lane] = w[c * kSwWin + k];
-  };
-  auto chain_to_lds = [&](const uint32_t (&ch)[kNx], const int (&ex)[kNx]) {
-#pragma unroll
-    for (int t = 0; t < kNx; ++t) {
-      s_ce[t * kWave + lane][0] = ch[t];
-      s_ce[t * kWave + lane][1] = (uint32_t)ex[t];
-    }
+    for (int i = 0; i < 4; ++i) ((pp_u32x4*)&s_ce[0][0])[i * kWave + lane] = ce[i];
   };
   // LDS addresses the walk reads from: lane l's row (l mod 32) of window 0
   // and lane l's word of window 0, cell 0
@@ -1027,19 +1117,20 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   int q = 0, j = kp;
   int g = (j - 1) / kStage;
   int sw = 0;
-  uint32_t wb[kW];
-  uint32_t cb[kNx];
-  int eb[kNx];
+  pp_u32x4 wb[kW];  // next super-window, same stage
+  pp_u32x4 wd[kW];  // same super-window, stage below
+  pp_u32x4 cb[4];
   load_words(0, g, wb);
-  load_chain(0, cb, eb);
+  load_chain(0, cb);
   words_to_lds(wb);
-  chain_to_lds(cb, eb);
+  chain_to_lds(cb);
   __syncthreads();
   uint32_t tw = 0, tm = 0;
   for (;;) {
-    // the next super-window of this stage, in flight while this one is walked
+    // both successors, in flight while this super-window is walked
     load_words(sw + 1, g, wb);
-    load_chain(sw + 1, cb, eb);
+    if (g > 0) load_words(sw, g - 1, wd);
+    load_chain(sw + 1, cb);
     const int jlo = g * kStage + 1;
     uint32_t uq = (uint32_t)q, urem = (uint32_t)(j - jlo);
     uint32_t wk = (uint32_t)(q - sw * kSw) / kWin;
@@ -1064,18 +1155,24 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
       store_takes(sw, tw);  // the last window's takes are in tw already
       tw = 0;
     }
+    bool below = false;
     if (g_n == g && sw_n == sw + 1) {
       // the prefetched super-window
     } else if (g_n == g) {
       load_words(sw_n, g_n, wb);
-      load_chain(sw_n, cb, eb);
+      load_chain(sw_n, cb);
+    } else if (sw_n == sw) {
+      below = true;  // the prefetched stage below
     } else {
       load_words(sw_n, g_n, wb);
-      if (sw_n != sw) load_chain(sw_n, cb, eb);
+      load_chain(sw_n, cb);
     }
     __syncthreads();
-    words_to_lds(wb);
-    if (sw_n != sw) chain_to_lds(cb, eb);
+    if (below)
+      words_to_lds(wd);
+    else
+      words_to_lds(wb);
+    if (sw_n != sw) chain_to_lds(cb);
     __syncthreads();
     sw = sw_n;
     g = g_n;
