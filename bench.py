@@ -93,6 +93,26 @@ def copy_probe(mib):
     return 0 if ok else 1
 
 
+def host_description():
+    """CPU model, logical CPUs and memory of the machine the bench runs on."""
+    model, mem_kib = None, None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+        with open("/proc/meminfo") as fh:
+            for line in fh:
+                if line.startswith("MemTotal"):
+                    mem_kib = int(line.split()[1])
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "host_cpus": os.cpu_count(),
+            "mem_gib": round(mem_kib / 2 ** 20, 1) if mem_kib else None}
+
+
 def cpu_baseline(inst, cells_per_plan, threads):
     """The oracle as it stands, on a bounded sample of the same workload:
     the standalone pass and the greedy pass of every start (no refinement
@@ -114,7 +134,7 @@ def cpu_baseline(inst, cells_per_plan, threads):
                    f"{inst.n_starts} starts ({res.updates} worker updates, "
                    f"{res.dp_cells:.3e} DP cells) in {dt:.1f} s; plans/s = "
                    f"cells/s / cells of one full plan"),
-        "host_cpus": os.cpu_count(),
+        **host_description(),
     }
 
 
@@ -174,6 +194,8 @@ def main():
                          "planned with the comparator safeguards")
     ap.add_argument("--no-replan", action="store_true",
                     help="skip the re-planning leg")
+    ap.add_argument("--no-host-plan", action="store_true",
+                    help="skip the timing of the host-array entry point")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device (counter "
                          "calibration) and exit")
@@ -231,13 +253,15 @@ def main():
         log(f"[bench] warmup {i}: objective {p.objective}")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    plans = []
+    plans, marks = [], []
     for i in range(args.steps):
         plans.append(step(B.PP_F_TIME_KERNELS))
+        marks.append(time.perf_counter())  # the call returns after its stream drained
         log(f"[bench] step {i}: objective {plans[-1].objective} "
             f"dp {plans[-1].dp_kernel_ms:.1f} ms")
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    step_ms = sorted((b - a) * 1e3 for a, b in zip([t0] + marks[:-1], marks))
     p = plans[-1]
     objectives = {q.objective for q in plans}
     gold_ok = None
@@ -255,6 +279,7 @@ def main():
     bytes_per_launch = cells * args.steps * BYTES_PER_CELL / launches
     avg_launch_s = dp_ms / launches / 1e3
     achieved = bytes_per_launch / avg_launch_s / 1e9
+    traffic = measured_traffic(inst.name)
     out = {
         "metric": METRIC,
         "value": plans_per_s,
@@ -266,6 +291,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": dt / args.steps * 1e3,
+        "ms_per_step_median": step_ms[len(step_ms) // 2],
+        "ms_per_step_min": step_ms[0],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -285,7 +312,10 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": measured_traffic(inst.name),
+            "traffic": traffic,
+            # the same launches against the bytes the counters saw move
+            "measured_frac": (traffic / avg_launch_s / 1e9 / HBM_PEAK_GBS
+                              if traffic else None),
             "bytes_per_cell": BYTES_PER_CELL,
             "dp_launches_per_plan": launches // args.steps,
             "avg_launch_ms": avg_launch_s * 1e3,
@@ -298,6 +328,19 @@ def main():
            if args.safeguards else {}),
         "paper_context": PAPER_CONTEXT,
     }
+    # the host-array entry point on the same inputs: PCIe copies of the
+    # inputs and the placement inside the call
+    host_ms = []
+    for _ in range(0 if args.no_host_plan else 2):
+        t1 = time.perf_counter()
+        hp = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
+                       inst.fetch_cost, inst.cap, n_starts=inst.n_starts,
+                       max_rounds=inst.max_rounds, order_seed=inst.order_seed,
+                       flags=plan_flags)
+        host_ms.append((time.perf_counter() - t1) * 1e3)
+    if host_ms:
+        out["host_pp_plan_ms"] = min(host_ms)
+        out["host_pp_plan_same_objective"] = hp.objective == p.objective
     if not args.no_replan and not args.safeguards:
         log("[bench] re-planning leg")
         out["replan"] = replan_leg(B, W, inst, max(1, min(args.steps, 3)),
