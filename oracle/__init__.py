@@ -27,8 +27,11 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(LIB) or \
             os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
+        # no contraction of a*b + c into one rounding: the real-valued
+        # entry points round every product and sum as written
         subprocess.run(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra",
-                        "-shared", "-fPIC", "-pthread", "-o", tmp, SRC],
+                        "-ffp-contract=off", "-shared", "-fPIC", "-pthread",
+                        "-o", tmp, SRC],
                        check=True)
         os.replace(tmp, LIB)
     return LIB
@@ -58,6 +61,12 @@ def lib() -> ctypes.CDLL:
         L.ppo_plan.argtypes = [i32, i32, P, P, P, P, P, i32, i32, u64, P, u32,
                                i32, P, P, P, P, P, P, P, P, P]
         L.ppo_requester_side.argtypes = [i32, i32, P]
+        f64 = ctypes.c_double
+        L.ppo_rooted_dp_f64.argtypes = [i32, P, P, i32, P, P]
+        L.ppo_marginal_f64.argtypes = [i32, i32, P, P, P, P, i32, P]
+        L.ppo_objective_f64.argtypes = [i32, i32, P, P, P, P, P]
+        L.ppo_plan_f64.argtypes = [i32, i32, P, P, P, P, P, f64, i32, i32, u64,
+                                   P, u32, P, P, P, P, P, P, P, P]
         L.ppo_candidates.argtypes = [i32, i32, P, P, P, P, P, P, P]
         L.ppo_materialization_cost.argtypes = [i32, i32, P, P, P, P, P]
         L.ppo_replan.argtypes = [i32, i32, P, P, P, P, P, P, i64, i32, i32,
@@ -283,3 +292,92 @@ def plan_instance(inst, **kw) -> PlanResult:
     args.update(kw)
     return plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
                 inst.cap, **args)
+
+
+# ------------------------------------------------------ real-valued costs
+
+def rooted_dp_f64(parent, profit, k):
+    """Eq. 9 on doubles (reading R24)."""
+    parent = _c(parent, np.int32)
+    profit = _c(profit, np.float64)
+    n = parent.shape[0]
+    sel = np.zeros(n, np.uint8)
+    val = np.zeros(1, np.float64)
+    _check(lib().ppo_rooted_dp_f64(n, _p(parent), _p(profit), int(k), _p(sel),
+                                   _p(val)))
+    return sel, float(val[0])
+
+
+def marginal_f64(demand, recompute_cost, fetch_cost, target, h):
+    """Eq. 7 on doubles, requester terms summed in increasing m."""
+    demand = _c(demand, np.float64)
+    w = _c(recompute_cost, np.float64)
+    f = _c(fetch_cost, np.float64)
+    target = _c(target, np.uint8)
+    m, n = demand.shape
+    prof = np.zeros(n, np.float64)
+    _check(lib().ppo_marginal_f64(n, m, _p(demand), _p(w), _p(f), _p(target),
+                                  int(h), _p(prof)))
+    return prof
+
+
+def objective_f64(demand, recompute_cost, fetch_cost, target) -> float:
+    """Eq. 6 on doubles, b outer, m inner."""
+    demand = _c(demand, np.float64)
+    w = _c(recompute_cost, np.float64)
+    f = _c(fetch_cost, np.float64)
+    target = _c(target, np.uint8)
+    m, n = demand.shape
+    out = np.zeros(1, np.float64)
+    _check(lib().ppo_objective_f64(n, m, _p(demand), _p(w), _p(f), _p(target),
+                                   _p(out)))
+    return float(out[0])
+
+
+@dataclass
+class PlanF64Result:
+    target: np.ndarray          # uint8 [m][n]
+    objective: float
+    standalone: np.ndarray      # float64 [m]
+    orders: np.ndarray          # int32 [S][m]
+    start_objective: np.ndarray  # float64 [S]
+    start_sweeps: np.ndarray
+    start_accepts: np.ndarray
+    best_start: int
+    updates: int
+    dp_cells: int
+
+
+def plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,
+             n_starts=1, max_rounds=0, order_seed=0, orders_in=None, flags=0
+             ) -> PlanF64Result:
+    """Algorithm 1 on real-valued costs with refinement tolerance epsilon
+    (reading R24)."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.float64)
+    w = _c(recompute_cost, np.float64)
+    f = _c(fetch_cost, np.float64)
+    cap = _c(cap, np.int32)
+    m, n = demand.shape
+    S = num_starts(m, n_starts)
+    if orders_in is not None:
+        orders_in = _c(orders_in, np.int32)
+    tgt = np.zeros((m, n), np.uint8)
+    obj = np.zeros(1, np.float64)
+    st = np.zeros(m, np.float64)
+    ords = np.zeros((S, m), np.int32)
+    so = np.zeros(S, np.float64)
+    ss = np.zeros(S, np.int32)
+    sa = np.zeros(S, np.int32)
+    info = np.zeros(4, np.int64)
+    _check(lib().ppo_plan_f64(n, m, _p(parent), _p(demand), _p(w), _p(f),
+                              _p(cap), float(epsilon), int(n_starts),
+                              int(max_rounds),
+                              ctypes.c_uint64(order_seed & (2**64 - 1)),
+                              _p(orders_in), int(flags), _p(tgt), _p(obj),
+                              _p(st), _p(ords), _p(so), _p(ss), _p(sa),
+                              _p(info)))
+    return PlanF64Result(target=tgt, objective=float(obj[0]), standalone=st,
+                         orders=ords, start_objective=so, start_sweeps=ss,
+                         start_accepts=sa, best_start=int(info[0]),
+                         updates=int(info[1]), dp_cells=int(info[2]))

@@ -19,6 +19,8 @@
  *   - epoch re-planning: adopt a re-optimized plan
  *     only if the horizon saving exceeds the one-
  *     time cost of materializing new chunks         Sec. IV-D; Sec. V-A (break-even requests)
+ *   - the same planner on real-valued costs with the
+ *     refinement tolerance epsilon                  Sec. IV-C, Algorithm 1 (REQUIRE: tolerance)
  *
  * Readings of points the paper leaves open (numbered as in the design notes):
  *   R1  DP ties: take b_i only if strictly better; skip wins ties.
@@ -54,6 +56,13 @@
  *   R22 the horizon H counts epochs; the re-optimized plan T' is adopted
  *       iff H * (G(T') - G(T)) > that cost (exact 128-bit comparison), G
  *       evaluated under the refreshed inputs.
+ *   R24 real-valued costs (the _f64 entry points): IEEE double arithmetic,
+ *       each product Lambda * x rounded before it is added (no fused
+ *       multiply-add); p_h(b) sums its requester terms in increasing m and
+ *       G(T) sums over b outer, m inner; the DP takes b_i only if
+ *       t > s; a refinement replacement is accepted iff
+ *       G(T_-h, T'_h) > G(T) + epsilon, both G evaluated from scratch;
+ *       starts compare G exactly (earliest start on equal values).
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -1000,5 +1009,384 @@ int ppo_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
 out:
     free(order); free(nextpos); free(orders); free(standalone); free(tgts);
     free(obj); free(sw); free(ac); free(rcs); free(cands);
+    return rc;
+}
+
+/* ------------------------------------------------ real-valued costs -- */
+
+/* The same definitions on IEEE doubles (R24).  Costs must be finite and
+ * non-negative.  Written out separately from the integer path so that each
+ * reads as its equation. */
+
+static double maxd(double a, double b) { return a > b ? a : b; }
+
+static int finite_nonneg(double x) { return x >= 0.0 && x <= 1.7976931348623157e308; }
+
+static int validate_f64(int32_t n, int32_t m, const int32_t *parent,
+                        const double *lam, const double *w, const double *f,
+                        const int32_t *cap)
+{
+    if (n < 1 || m < 1 || m > 255 || !parent || !lam || !w || !f || !cap)
+        return PPO_E_ARG;
+    for (int32_t v = 0; v < n; v++)
+        if (parent[v] < -1 || parent[v] >= n || parent[v] == v)
+            return PPO_E_TREE;
+    size_t mn = (size_t)m * n;
+    for (size_t x = 0; x < mn; x++)
+        if (!finite_nonneg(lam[x]) || !finite_nonneg(w[x]))
+            return PPO_E_RANGE;
+    for (size_t x = 0; x < mn * (size_t)m; x++)
+        if (!finite_nonneg(f[x]))
+            return PPO_E_RANGE;
+    for (int32_t r = 0; r < m; r++)
+        if (cap[r] < 0)
+            return PPO_E_RANGE;
+    return PPO_OK;
+}
+
+/* Eq. (5) */
+static double q_save_f64(int32_t n, int32_t m, const double *w, const double *f,
+                         int32_t h, int32_t req, int32_t b)
+{
+    double wm = w[(size_t)req * n + b];
+    if (h == req)
+        return wm;
+    double d = wm - f[((size_t)h * m + req) * n + b];
+    return maxd(d, 0.0);
+}
+
+/* Eq. (6), b outer, m inner */
+static double objective_f64(int32_t n, int32_t m, const double *lam,
+                            const double *w, const double *f, const uint8_t *tgt)
+{
+    double g = 0.0;
+    for (int32_t b = 0; b < n; b++)
+        for (int32_t r = 0; r < m; r++) {
+            double best = 0.0;
+            for (int32_t h = 0; h < m; h++)
+                if (tgt[(size_t)h * n + b])
+                    best = maxd(best, q_save_f64(n, m, w, f, h, r, b));
+            double term = lam[(size_t)r * n + b] * best;
+            g += term;
+        }
+    return g;
+}
+
+/* Eq. (7), requester terms in increasing m */
+static void marginal_f64(int32_t n, int32_t m, const double *lam,
+                         const double *w, const double *f, const uint8_t *tgt,
+                         int32_t h, double *profit)
+{
+    for (int32_t b = 0; b < n; b++) {
+        double p = 0.0;
+        for (int32_t r = 0; r < m; r++) {
+            double v = 0.0;
+            for (int32_t l = 0; l < m; l++)
+                if (l != h && tgt[(size_t)l * n + b])
+                    v = maxd(v, q_save_f64(n, m, w, f, l, r, b));
+            double gap = q_save_f64(n, m, w, f, h, r, b) - v;
+            double term = lam[(size_t)r * n + b] * maxd(gap, 0.0);
+            p += term;
+        }
+        profit[b] = p;
+    }
+}
+
+/* Eq. (9) on doubles: the full table, take only if strictly better */
+static int rooted_dp_pos_f64(int32_t n, const int32_t *nextpos,
+                             const double *profit_pos, int32_t k,
+                             uint8_t *sel_pos, double *value)
+{
+    int64_t kk = k < n ? k : n;
+    memset(sel_pos, 0, (size_t)n);
+    if (kk <= 0) {
+        *value = 0.0;
+        return PPO_OK;
+    }
+    size_t W = (size_t)kk + 1;
+    double *D = calloc(((size_t)n + 2) * W, sizeof(double));
+    if (!D)
+        return PPO_E_NOMEM;
+#define CELL(i, j) D[(size_t)(i) * W + (size_t)(j)]
+    for (int64_t i = n; i >= 1; i--) {
+        int64_t nx = (int64_t)nextpos[i - 1] + 1;
+        double p = profit_pos[i - 1];
+        for (int64_t j = 1; j <= kk; j++) {
+            double s = CELL(nx, j);
+            double t = p + CELL(i + 1, j - 1);
+            CELL(i, j) = t > s ? t : s;
+        }
+    }
+    *value = CELL(1, kk);
+    int64_t i = 1, j = kk;
+    while (i <= n && j > 0) {
+        int64_t nx = (int64_t)nextpos[i - 1] + 1;
+        double s = CELL(nx, j);
+        double t = profit_pos[i - 1] + CELL(i + 1, j - 1);
+        if (t > s) {
+            sel_pos[i - 1] = 1;
+            i += 1;
+            j -= 1;
+        } else {
+            i = nx;
+        }
+    }
+#undef CELL
+    free(D);
+    return PPO_OK;
+}
+
+int ppo_rooted_dp_f64(int32_t n, const int32_t *parent, const double *profit,
+                      int32_t k, uint8_t *sel, double *value)
+{
+    if (n < 1 || !parent || !profit || !sel || !value || k < 0)
+        return PPO_E_ARG;
+    for (int32_t v = 0; v < n; v++)
+        if (!finite_nonneg(profit[v]))
+            return PPO_E_RANGE;
+    int32_t *order = malloc((size_t)n * sizeof(int32_t));
+    int32_t *nextpos = malloc((size_t)n * sizeof(int32_t));
+    double *pp = malloc((size_t)n * sizeof(double));
+    uint8_t *sp = malloc((size_t)n);
+    int rc = PPO_E_NOMEM;
+    if (!order || !nextpos || !pp || !sp)
+        goto out;
+    rc = preorder(n, parent, order, nextpos);
+    if (rc != PPO_OK)
+        goto out;
+    for (int32_t i = 0; i < n; i++)
+        pp[i] = profit[order[i]];
+    rc = rooted_dp_pos_f64(n, nextpos, pp, k, sp, value);
+    if (rc == PPO_OK)
+        for (int32_t i = 0; i < n; i++)
+            sel[order[i]] = sp[i];
+out:
+    free(order); free(nextpos); free(pp); free(sp);
+    return rc;
+}
+
+int ppo_marginal_f64(int32_t n, int32_t m, const double *demand,
+                     const double *recompute_cost, const double *fetch_cost,
+                     const uint8_t *target, int32_t h, double *profit)
+{
+    if (n < 1 || m < 1 || h < 0 || h >= m || !demand || !recompute_cost ||
+        !fetch_cost || !target || !profit)
+        return PPO_E_ARG;
+    marginal_f64(n, m, demand, recompute_cost, fetch_cost, target, h, profit);
+    return PPO_OK;
+}
+
+int ppo_objective_f64(int32_t n, int32_t m, const double *demand,
+                      const double *recompute_cost, const double *fetch_cost,
+                      const uint8_t *target, double *objective)
+{
+    if (n < 1 || m < 1 || !demand || !recompute_cost || !fetch_cost ||
+        !target || !objective)
+        return PPO_E_ARG;
+    *objective = objective_f64(n, m, demand, recompute_cost, fetch_cost, target);
+    return PPO_OK;
+}
+
+typedef struct {
+    int32_t n, m;
+    const double *lam, *w, *f;
+    const int32_t *cap;
+    const int32_t *order, *nextpos;
+    int32_t max_rounds;
+    uint32_t flags;
+    double eps;
+} plan_in_f64;
+
+static int worker_update_f64(const plan_in_f64 *in, const uint8_t *tgt,
+                             int32_t h, double *profit, double *pp,
+                             uint8_t *sp, uint8_t *cand, double *dpval)
+{
+    int32_t n = in->n;
+    marginal_f64(n, in->m, in->lam, in->w, in->f, tgt, h, profit);
+    for (int32_t i = 0; i < n; i++)
+        pp[i] = profit[in->order[i]];
+    int rc = rooted_dp_pos_f64(n, in->nextpos, pp, in->cap[h], sp, dpval);
+    if (rc != PPO_OK)
+        return rc;
+    for (int32_t i = 0; i < n; i++)
+        cand[in->order[i]] = sp[i];
+    return PPO_OK;
+}
+
+/* Algorithm 1, one start, with the tolerance epsilon of the refinement test */
+static int run_start_f64(const plan_in_f64 *in, const int32_t *pi,
+                         uint8_t *tgt, double *obj, int32_t *sweeps,
+                         int32_t *accepts)
+{
+    int32_t n = in->n, m = in->m;
+    double *profit = malloc((size_t)n * sizeof(double));
+    double *pp = malloc((size_t)n * sizeof(double));
+    uint8_t *sp = malloc((size_t)n);
+    uint8_t *cand = malloc((size_t)n);
+    uint8_t *old = malloc((size_t)n);
+    int rc = PPO_E_NOMEM;
+    if (!profit || !pp || !sp || !cand || !old)
+        goto out;
+    memset(tgt, 0, (size_t)m * n);
+    double v;
+    for (int32_t a = 0; a < m; a++) {
+        int32_t h = pi[a];
+        rc = worker_update_f64(in, tgt, h, profit, pp, sp, cand, &v);
+        if (rc != PPO_OK)
+            goto out;
+        memcpy(tgt + (size_t)h * n, cand, (size_t)n);
+    }
+    int32_t r = 0, acc = 0;
+    if (!(in->flags & PPO_F_NO_REFINE)) {
+        int improved;
+        do {
+            improved = 0;
+            for (int32_t a = 0; a < m; a++) {
+                int32_t h = pi[a];
+                double g_old = objective_f64(n, m, in->lam, in->w, in->f, tgt);
+                uint8_t *th = tgt + (size_t)h * n;
+                memcpy(old, th, (size_t)n);
+                memset(th, 0, (size_t)n);
+                rc = worker_update_f64(in, tgt, h, profit, pp, sp, cand, &v);
+                if (rc != PPO_OK)
+                    goto out;
+                memcpy(th, cand, (size_t)n);
+                double g_new = objective_f64(n, m, in->lam, in->w, in->f, tgt);
+                if (g_new > g_old + in->eps) {
+                    improved = 1;
+                    acc++;
+                } else {
+                    memcpy(th, old, (size_t)n);
+                }
+            }
+            r++;
+        } while (improved && !(in->max_rounds > 0 && r == in->max_rounds));
+    }
+    *obj = objective_f64(n, m, in->lam, in->w, in->f, tgt);
+    *sweeps = r;
+    *accepts = acc;
+    rc = PPO_OK;
+out:
+    free(profit); free(pp); free(sp); free(cand); free(old);
+    return rc;
+}
+
+/* The planner on real-valued costs (R24), one start after another.
+ * Arguments as ppo_plan, with double inputs and outputs, the tolerance
+ * `epsilon` (finite, >= 0) and info[4] = {returned start, updates, DP
+ * cells, S}.  The comparator safeguards are not offered here. */
+int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
+                 const double *demand, const double *recompute_cost,
+                 const double *fetch_cost, const int32_t *cap, double epsilon,
+                 int32_t n_starts, int32_t max_rounds, uint64_t order_seed,
+                 const int32_t *orders_in, uint32_t flags, uint8_t *target,
+                 double *objective, double *standalone_out,
+                 int32_t *orders_out, double *start_objective,
+                 int32_t *start_sweeps, int32_t *start_accepts, int64_t *info)
+{
+    int rc = validate_f64(n, m, parent, demand, recompute_cost, fetch_cost, cap);
+    if (rc != PPO_OK)
+        return rc;
+    if (n_starts < 0 || max_rounds < 0 || !target || !objective ||
+        !finite_nonneg(epsilon) || (flags & PPO_F_SAFEGUARDS))
+        return PPO_E_ARG;
+    int32_t S = ppo_num_starts(m, n_starts);
+    if (orders_in) {
+        if (n_starts < 1)
+            return PPO_E_ARG;
+        for (int32_t s = 0; s < S; s++) {
+            uint8_t seen[256] = {0};
+            for (int32_t a = 0; a < m; a++) {
+                int32_t h = orders_in[(size_t)s * m + a];
+                if (h < 0 || h >= m || seen[h])
+                    return PPO_E_ARG;
+                seen[h] = 1;
+            }
+        }
+    }
+    int32_t *order = malloc((size_t)n * sizeof(int32_t));
+    int32_t *nextpos = malloc((size_t)n * sizeof(int32_t));
+    int32_t *orders = malloc((size_t)S * m * sizeof(int32_t));
+    double *standalone = malloc((size_t)m * sizeof(double));
+    int64_t *rank = malloc((size_t)m * sizeof(int64_t));
+    uint8_t *tgts = malloc((size_t)S * m * n);
+    double *obj = malloc((size_t)S * sizeof(double));
+    int32_t *sw = malloc((size_t)S * sizeof(int32_t));
+    int32_t *ac = malloc((size_t)S * sizeof(int32_t));
+    double *profit = malloc((size_t)n * sizeof(double));
+    double *pp = malloc((size_t)n * sizeof(double));
+    uint8_t *sp = malloc((size_t)n);
+    uint8_t *cand = malloc((size_t)n);
+    uint8_t *empty = calloc((size_t)m * n, 1);
+    rc = PPO_E_NOMEM;
+    if (!order || !nextpos || !orders || !standalone || !rank || !tgts ||
+        !obj || !sw || !ac || !profit || !pp || !sp || !cand || !empty)
+        goto out;
+    rc = preorder(n, parent, order, nextpos);
+    if (rc != PPO_OK)
+        goto out;
+    plan_in_f64 in = {n, m, demand, recompute_cost, fetch_cost, cap, order,
+                      nextpos, max_rounds, flags, epsilon};
+    for (int32_t h = 0; h < m; h++) {  /* R6 */
+        rc = worker_update_f64(&in, empty, h, profit, pp, sp, cand,
+                               &standalone[h]);
+        if (rc != PPO_OK)
+            goto out;
+    }
+    if (orders_in) {
+        memcpy(orders, orders_in, (size_t)S * m * sizeof(int32_t));
+    } else {
+        /* order 0 sorts by score: give equal scores equal integer keys */
+        for (int32_t h = 0; h < m; h++) {
+            rank[h] = 0;
+            for (int32_t l = 0; l < m; l++)
+                if (standalone[l] < standalone[h])
+                    rank[h]++;
+        }
+        rc = ppo_orders(m, n_starts, order_seed, rank, orders);
+        if (rc != PPO_OK)
+            goto out;
+    }
+    for (int32_t s = 0; s < S; s++) {
+        rc = run_start_f64(&in, orders + (size_t)s * m, tgts + (size_t)s * m * n,
+                           &obj[s], &sw[s], &ac[s]);
+        if (rc != PPO_OK)
+            goto out;
+    }
+    int32_t best = 0;
+    for (int32_t s = 1; s < S; s++)
+        if (obj[s] > obj[best])
+            best = s;
+    memcpy(target, tgts + (size_t)best * m * n, (size_t)m * n);
+    *objective = obj[best];
+    int64_t updates = m, cells = 0;
+    for (int32_t h = 0; h < m; h++)
+        cells += (int64_t)n * (cap[h] < n ? cap[h] : n);
+    int64_t cells_per_pass = cells;
+    for (int32_t s = 0; s < S; s++) {
+        updates += (int64_t)m * (1 + sw[s]);
+        cells += cells_per_pass * (1 + sw[s]);
+    }
+    if (standalone_out)
+        memcpy(standalone_out, standalone, (size_t)m * sizeof(double));
+    if (orders_out)
+        memcpy(orders_out, orders, (size_t)S * m * sizeof(int32_t));
+    if (start_objective)
+        memcpy(start_objective, obj, (size_t)S * sizeof(double));
+    if (start_sweeps)
+        memcpy(start_sweeps, sw, (size_t)S * sizeof(int32_t));
+    if (start_accepts)
+        memcpy(start_accepts, ac, (size_t)S * sizeof(int32_t));
+    if (info) {
+        info[0] = best;
+        info[1] = updates;
+        info[2] = cells;
+        info[3] = S;
+    }
+    rc = PPO_OK;
+out:
+    free(order); free(nextpos); free(orders); free(standalone); free(rank);
+    free(tgts); free(obj); free(sw); free(ac); free(profit); free(pp); free(sp);
+    free(cand); free(empty);
     return rc;
 }
