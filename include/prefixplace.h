@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 4
+#define PP_ABI_VERSION 5
 
 enum {
     PP_OK = 0,
@@ -149,6 +149,44 @@ int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
             const int32_t *cap, const pp_options *opt, uint8_t *target,
             int64_t *objective, pp_stats *stats);
 
+/* Real-valued costs (the paper's own domain: demand in requests per epoch,
+ * costs in milliseconds) with the refinement tolerance epsilon of Algorithm 1
+ * (Sec. IV-C): a refinement replacement is accepted only if it raises G by
+ * more than epsilon.  Every value is an IEEE double; inputs must be finite
+ * and >= 0 (PP_E_RANGE otherwise), epsilon finite and >= 0 (PP_E_ARG).
+ * The arithmetic is the integer path's, in doubles: each product
+ * Lambda * x is rounded before it is added, p_h(b) adds its requester terms
+ * in increasing m, the DP takes b_i only if p + D[i+1][j-1] > D[next(i)][j],
+ * and a replacement that leaves the worker's set unchanged is never counted
+ * as an improvement.  The acceptance test uses Proposition 1 (DP value >
+ * incumbent value + epsilon); objectives are summed in a fixed order, so a
+ * placement always gets the same value.  PP_F_SAFEGUARDS is not offered
+ * here (PP_E_UNSUPPORTED).  Statistics as pp_stats, with double objectives
+ * and standalone scores. */
+typedef struct {
+    int32_t best_start;
+    int32_t n_starts;
+    int64_t updates;
+    int64_t dp_cells;
+    double *start_objective;   /* [S] or NULL */
+    int32_t *start_sweeps;     /* [S] or NULL */
+    int32_t *start_accepts;    /* [S] or NULL */
+    double *standalone;        /* [m] or NULL */
+    int32_t *orders;           /* [S][m] or NULL */
+    double dp_kernel_ms;
+    int32_t dp_launches;
+} pp_stats_f64;
+
+/* pp_plan on real-valued host arrays (layouts as pp_plan). */
+int pp_plan_f64(int32_t n, int32_t m, const int32_t *parent, const double *demand,
+                const double *recompute_cost, const double *fetch_cost,
+                const int32_t *cap, double epsilon, const pp_options *opt,
+                uint8_t *target, double *objective, pp_stats_f64 *stats);
+
+/* pp_rooted_dp on real-valued profits (finite, >= 0). */
+int pp_rooted_dp_f64(int32_t n, const int32_t *parent, const double *profit,
+                     int32_t k, uint8_t *selected, double *value);
+
 /* Epoch re-planning (Sec. IV-D): when demand or routing changes, plan the
  * refreshed inputs (as pp_plan, same options), evaluate the incumbent under
  * them, and adopt the new plan only if the saving predicted over the horizon
@@ -225,6 +263,14 @@ int pp_plan_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
                    const int64_t *fetch_dev, const int32_t *cap,
                    const pp_options *opt, uint8_t *target_dev,
                    int64_t *objective, pp_stats *stats, void *hip_stream);
+
+/* pp_plan_device on real-valued device arrays (layouts as pp_plan_device;
+ * the value checks run on the device). */
+int pp_plan_f64_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
+                       const double *demand_dev, const double *recompute_dev,
+                       const double *fetch_dev, const int32_t *cap, double epsilon,
+                       const pp_options *opt, uint8_t *target_dev, double *objective,
+                       pp_stats_f64 *stats, void *hip_stream);
 
 /* Host only, for inspection and CPU-side checks of the DP sweep's step
  * schedule: for the tree `parent` and `cells` (1, 2 or 4) DP cells per

@@ -40,6 +40,15 @@ class pp_stats(ctypes.Structure):
                 ("safeguard_objective", ctypes.c_int64 * 3)]
 
 
+class pp_stats_f64(ctypes.Structure):
+    _fields_ = [("best_start", ctypes.c_int32), ("n_starts", ctypes.c_int32),
+                ("updates", ctypes.c_int64), ("dp_cells", ctypes.c_int64),
+                ("start_objective", _P), ("start_sweeps", _P),
+                ("start_accepts", _P), ("standalone", _P), ("orders", _P),
+                ("dp_kernel_ms", ctypes.c_double),
+                ("dp_launches", ctypes.c_int32)]
+
+
 class pp_replan_info(ctypes.Structure):
     _fields_ = [("adopt", ctypes.c_int32), ("incumbent_objective", ctypes.c_int64),
                 ("proposal_objective", ctypes.c_int64),
@@ -80,6 +89,11 @@ def lib() -> ctypes.CDLL:
         L.pp_plan.argtypes = [i32, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P]
         L.pp_replan.argtypes = [i32, i32, _P, _P, _P, _P, _P, _P, i64, _P, _P,
                                 _P, _P, _P]
+        f64 = ctypes.c_double
+        L.pp_plan_f64.argtypes = [i32, i32, _P, _P, _P, _P, _P, f64, _P, _P, _P, _P]
+        L.pp_plan_f64_device.argtypes = [_P, i32, i32, _P, _P, _P, _P, _P, f64, _P,
+                                         _P, _P, _P, _P]
+        L.pp_rooted_dp_f64.argtypes = [i32, _P, _P, i32, _P, _P]
         L.pp_rooted_dp.argtypes = [i32, _P, _P, i32, _P, _P]
         L.pp_marginal.argtypes = [i32, i32, _P, _P, _P, _P, i32, _P, _P]
         L.pp_objective.argtypes = [i32, i32, _P, _P, _P, _P, _P]
@@ -91,7 +105,8 @@ def lib() -> ctypes.CDLL:
         L.pp_ctx_destroy.restype = None
         L.pp_plan_device.argtypes = [_P, i32, i32, _P, _P, _P, _P, _P, _P, _P,
                                      _P, _P, _P]
-        for f in (L.pp_plan, L.pp_replan, L.pp_rooted_dp, L.pp_marginal, L.pp_objective,
+        for f in (L.pp_plan, L.pp_replan, L.pp_plan_f64, L.pp_plan_f64_device,
+                  L.pp_rooted_dp_f64, L.pp_rooted_dp, L.pp_marginal, L.pp_objective,
                   L.pp_orders, L.pp_ctx_create, L.pp_plan_device):
             f.restype = ctypes.c_int
         _lib = L
@@ -233,6 +248,58 @@ def pp_replan(parent, demand, recompute_cost, fetch_cost, cap, incumbent,
                   plan=_plan_from(st, arrs, prop, info.proposal_objective))
 
 
+def _options_f64(m, n_starts, max_rounds, order_seed, orders, flags):
+    o, _, _, keep = _options(m, n_starts, max_rounds, order_seed, orders, flags)
+    S = pp_num_starts(m, n_starts)
+    st = pp_stats_f64()
+    arrs = dict(start_objective=np.zeros(S, np.float64),
+                start_sweeps=np.zeros(S, np.int32),
+                start_accepts=np.zeros(S, np.int32),
+                standalone=np.zeros(m, np.float64),
+                orders=np.zeros((S, m), np.int32))
+    for k, v in arrs.items():
+        setattr(st, k, v.ctypes.data)
+    return o, st, arrs, keep
+
+
+def _plan_f64_from(st, arrs, target, objective):
+    return Plan(target=target, objective=float(objective), best_start=st.best_start,
+                n_starts=st.n_starts, updates=st.updates, dp_cells=st.dp_cells,
+                dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches, **arrs)
+
+
+def pp_plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,
+                n_starts=8, max_rounds=0, order_seed=0, orders=None, flags=0) -> Plan:
+    """Real-valued host-array planner (see pp_plan_f64 in
+    include/prefixplace.h); objectives are floats."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.float64)
+    w = _c(recompute_cost, np.float64)
+    f = _c(fetch_cost, np.float64)
+    cap = _c(cap, np.int32)
+    m, n = demand.shape
+    o, st, arrs, keep = _options_f64(m, n_starts, max_rounds, order_seed, orders,
+                                     flags)
+    tgt = np.zeros((m, n), np.uint8)
+    obj = ctypes.c_double(0.0)
+    _check(lib().pp_plan_f64(n, m, _p(parent), _p(demand), _p(w), _p(f), _p(cap),
+                             float(epsilon), ctypes.byref(o), _p(tgt),
+                             ctypes.byref(obj), ctypes.byref(st)))
+    del keep
+    return _plan_f64_from(st, arrs, tgt, obj.value)
+
+
+def pp_rooted_dp_f64(parent, profit, k):
+    parent = _c(parent, np.int32)
+    profit = _c(profit, np.float64)
+    n = parent.shape[0]
+    sel = np.zeros(n, np.uint8)
+    val = ctypes.c_double(0.0)
+    _check(lib().pp_rooted_dp_f64(n, _p(parent), _p(profit), int(k), _p(sel),
+                                  ctypes.byref(val)))
+    return sel, val.value
+
+
 def pp_rooted_dp(parent, profit, k):
     parent = _c(parent, np.int32)
     profit = _c(profit, np.int64)
@@ -308,6 +375,39 @@ class Context:
             self.close()
         except Exception:
             pass
+
+    def pp_plan_f64_device(self, parent, demand_dev, recompute_dev, fetch_dev,
+                           cap, target_dev, *, epsilon=0.0, n_starts=8,
+                           max_rounds=0, order_seed=0, orders=None, flags=0,
+                           stream=None) -> Plan:
+        """Real-valued plan on torch device tensors (float64 [m][n],
+        float64 [m][n], float64 [m][m][n]); writes uint8 [m][n] into
+        `target_dev`."""
+        import torch
+
+        for t, dt in ((demand_dev, torch.float64), (recompute_dev, torch.float64),
+                      (fetch_dev, torch.float64), (target_dev, torch.uint8)):
+            if not t.is_cuda or t.dtype != dt or not t.is_contiguous():
+                raise ValueError("device tensors must be contiguous, on the "
+                                 "GPU, with the documented dtypes")
+        parent = _c(parent, np.int32)
+        cap = _c(cap, np.int32)
+        m, n = demand_dev.shape
+        if tuple(fetch_dev.shape) != (m, m, n) or tuple(target_dev.shape) != (m, n) \
+                or tuple(recompute_dev.shape) != (m, n) or parent.shape[0] != n \
+                or cap.shape[0] != m:
+            raise ValueError("shape mismatch")
+        o, st, arrs, keep = _options_f64(m, n_starts, max_rounds, order_seed,
+                                         orders, flags)
+        obj = ctypes.c_double(0.0)
+        s = stream if stream is not None else torch.cuda.current_stream()
+        _check(lib().pp_plan_f64_device(
+            self._h, n, m, _p(parent), demand_dev.data_ptr(),
+            recompute_dev.data_ptr(), fetch_dev.data_ptr(), _p(cap),
+            float(epsilon), ctypes.byref(o), target_dev.data_ptr(),
+            ctypes.byref(obj), ctypes.byref(st), ctypes.c_void_p(s.cuda_stream)))
+        del keep
+        return _plan_f64_from(st, arrs, target_dev, obj.value)
 
     def pp_plan_device(self, parent, demand_dev, recompute_dev, fetch_dev, cap,
                        target_dev, *, n_starts=8, max_rounds=0, order_seed=0,

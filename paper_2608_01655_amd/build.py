@@ -15,8 +15,11 @@ BUILD_DIR = os.path.join(PKG, "_build")
 
 ARCH = "gfx950"
 # Packed-FP32 selection is disabled for all device code (no packed f32 math
-# is used here; this keeps the compiler from forming it).
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# is used here; this keeps the compiler from forming it).  No contraction of
+# a * b + c into one rounding: the real-valued path rounds every product and
+# sum as written.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-ffp-contract=off"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
 
 

@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <climits>
 #include <cstdlib>
+#include <cfloat>
 #include <cstring>
 #include <memory>
 #include <new>
@@ -310,14 +311,14 @@ struct pp_ctx {
   DevBuf up_lam, up_w, up_f, up_u8;
   // per-slot state
   DevBuf tgt, v1, v2, h1, profit, sel, bits, ring, cs;
-  DevBuf partial, flag;
+  DevBuf partial, flag, fpart;
   uint32_t epoch = 0;
   std::vector<uint32_t> meta_host;  // source of the last metadata upload
   std::vector<hipEvent_t> events;
   ~pp_ctx() {
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
-                      &ring, &cs, &partial, &flag})
+                      &ring, &cs, &partial, &flag, &fpart})
       b->release();
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (own) (void)hipStreamDestroy(own);
@@ -452,7 +453,7 @@ struct Engine {
     PP_HIP(launch_gains(set, d, st));
     PP_TRY(dp(set, 1));
     PP_HIP(launch_backtrack(set, d, mode, st));
-    PP_HIP(launch_commit(set, d, st));
+    PP_HIP(launch_commit(set, d, mode, st));
     return PP_OK;
   }
 };
@@ -569,7 +570,7 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
     PP_HIP(launch_gains(set, d, st, kGainsLocalDedup));
     PP_TRY(e.dp(set, 1));
     PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
-    PP_HIP(launch_commit(set, d, st));
+    PP_HIP(launch_commit(set, d, kModeGreedy, st));
   }
   {
     std::vector<int32_t> z(3, 0);
@@ -603,9 +604,12 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
 }
 
 // Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
+// Real-valued costs (f64): every value is the bit pattern of a non-negative
+// double, so the comparisons below (orders, best start) hold unchanged.
 int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
              const pp_options& o, bool fmax_ok, hipStream_t st,
-             PlanResult& res, int32_t extra_slots = 0) {
+             PlanResult& res, int32_t extra_slots = 0, bool f64 = false,
+             double eps = 0.0) {
   const int32_t n = t.n;
   const int32_t S = num_starts(m, o.n_starts);
   res.S = S;
@@ -656,6 +660,13 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
                                       std::to_string(e.slots_lds) + " rows)");
   e.fmax = fmax_ok && env_int("PP_DP_NO_FMAX", 0) == 0;
   PP_TRY(ensure_slots(c, d, slots, kmax, cells));
+  if (f64) {
+    d.f64 = 1;
+    d.eps = eps;
+    d.fpart_stride = fpart_blocks(n, m);
+    PP_TRY(c->fpart.ensure((size_t)slots * d.fpart_stride * 8));
+    d.fpart = c->fpart.as<double>();
+  }
   PP_TRY(upload_meta(c, t, cells, st));
   d.meta = c->meta.as<uint32_t>();  // upload_meta may have (re)allocated it
 
@@ -831,6 +842,28 @@ int check_values(int32_t n, int32_t m, const int64_t* lam, const int64_t* w,
   return PP_OK;
 }
 
+// Real-valued inputs: finite and non-negative (NaN fails every comparison).
+bool finite_nonneg(double x) { return x >= 0.0 && x <= DBL_MAX; }
+
+int check_values_f64(int32_t n, int32_t m, const double* lam, const double* w,
+                     const double* f) {
+  const size_t mn = (size_t)m * n;
+  for (size_t x = 0; x < mn; ++x)
+    if (!finite_nonneg(lam[x]) || !finite_nonneg(w[x]))
+      return fail(PP_E_RANGE, "demand and recompute cost must be finite and >= 0");
+  for (size_t x = 0; x < mn * (size_t)m; ++x)
+    if (!finite_nonneg(f[x]))
+      return fail(PP_E_RANGE, "fetch cost must be finite and >= 0");
+  return PP_OK;
+}
+
+int check_f64_options(const pp_options& o, double eps) {
+  if (!finite_nonneg(eps)) return fail(PP_E_ARG, "epsilon must be finite and >= 0");
+  if (o.flags & PP_F_SAFEGUARDS)
+    return fail(PP_E_UNSUPPORTED, "the comparator safeguards take integer costs");
+  return PP_OK;
+}
+
 // Every marginal, DP value and objective is at most sum Lambda*w; below
 // 2^62 the sweep may take its maximum with v_max_f64 on the bit patterns.
 constexpr unsigned __int128 kFmaxBound = (unsigned __int128)1 << 62;
@@ -954,6 +987,33 @@ void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = r.sg_obj[q];
   (void)m;
+}
+
+double bits_f64(int64_t v) {
+  double d;
+  std::memcpy(&d, &v, sizeof d);
+  return d;
+}
+
+void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
+  if (!stats) return;
+  stats->best_start = r.best;
+  stats->n_starts = r.S;
+  stats->updates = r.updates;
+  stats->dp_cells = r.cells;
+  if (stats->start_objective)
+    for (size_t s = 0; s < r.start_obj.size(); ++s)
+      stats->start_objective[s] = bits_f64(r.start_obj[s]);
+  if (stats->start_sweeps)
+    std::copy(r.sweeps.begin(), r.sweeps.end(), stats->start_sweeps);
+  if (stats->start_accepts)
+    std::copy(r.accepts.begin(), r.accepts.end(), stats->start_accepts);
+  if (stats->standalone)
+    for (size_t h = 0; h < r.standalone.size(); ++h)
+      stats->standalone[h] = bits_f64(r.standalone[h]);
+  if (stats->orders) std::copy(r.orders.begin(), r.orders.end(), stats->orders);
+  stats->dp_kernel_ms = r.dp_ms;
+  stats->dp_launches = r.dp_launches;
 }
 
 template <class F>
@@ -1133,6 +1193,95 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
   });
 }
 
+int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
+                       const double* demand_dev, const double* recompute_dev,
+                       const double* fetch_dev, const int32_t* cap, double epsilon,
+                       const pp_options* opt, uint8_t* target_dev, double* objective,
+                       pp_stats_f64* stats, void* hip_stream) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (!ctx) return fail(PP_E_ARG, "null ctx");
+    PP_TRY(check_common(n, m, parent, demand_dev, recompute_dev, fetch_dev));
+    if (!cap || !target_dev || !objective) return fail(PP_E_ARG, "null pointer argument");
+    const pp_options o = opt ? *opt : default_options();
+    PP_TRY(check_options(m, o));
+    PP_TRY(check_f64_options(o, epsilon));
+    for (int32_t h = 0; h < m; ++h)
+      if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    PP_TRY(select_device(ctx));
+    hipStream_t st = (hipStream_t)hip_stream;
+    PP_TRY(ctx->flag.ensure(64));
+    PP_HIP(hipMemsetAsync(ctx->flag.p, 0, 4, st));
+    PP_HIP(launch_validate_f64(demand_dev, recompute_dev, fetch_dev, n, m,
+                               ctx->flag.as<int32_t>(), st));
+    int32_t bad = 0;
+    PP_HIP(hipMemcpyAsync(&bad, ctx->flag.p, 4, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    if (bad) return fail(PP_E_RANGE, "demand and costs must be finite and >= 0");
+    PP_TRY(upload_tree(ctx, t, st));
+    PP_TRY(layout_inputs(ctx, t, m, (const int64_t*)demand_dev,
+                         (const int64_t*)recompute_dev, (const int64_t*)fetch_dev, st));
+    PlanResult r;
+    PP_TRY(run_plan(ctx, t, m, cap, o, false, st, r, 0, true, epsilon));
+    const size_t mn = (size_t)m * n;
+    PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
+                             target_dev, m, n, ctx->order.as<int32_t>(), st));
+    PP_HIP(hipStreamSynchronize(st));
+    *objective = bits_f64(r.win_obj);
+    fill_stats_f64(stats, r);
+    return PP_OK;
+  });
+}
+
+int pp_plan_f64(int32_t n, int32_t m, const int32_t* parent, const double* demand,
+                const double* recompute_cost, const double* fetch_cost,
+                const int32_t* cap, double epsilon, const pp_options* opt,
+                uint8_t* target, double* objective, pp_stats_f64* stats) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
+    if (!cap || !target || !objective) return fail(PP_E_ARG, "null pointer argument");
+    const pp_options o = opt ? *opt : default_options();
+    PP_TRY(check_options(m, o));
+    PP_TRY(check_f64_options(o, epsilon));
+    for (int32_t h = 0; h < m; ++h)
+      if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
+    PP_TRY(check_values_f64(n, m, demand, recompute_cost, fetch_cost));
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    int rc = PP_OK;
+    pp_ctx* c = thread_ctx(rc);
+    if (!c) return rc;
+    hipStream_t st = c->own;
+    const size_t mn = (size_t)m * n;
+    PP_TRY(c->up_lam.ensure(mn * 8));
+    PP_TRY(c->up_w.ensure(mn * 8));
+    PP_TRY(c->up_f.ensure(mn * m * 8));
+    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
+    PP_TRY(upload_tree(c, t, st));
+    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
+                         c->up_f.as<int64_t>(), st));
+    PlanResult r;
+    PP_TRY(run_plan(c, t, m, cap, o, false, st, r, 0, true, epsilon));
+    std::vector<uint8_t> pre(mn);
+    PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
+                          mn, hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    for (int32_t h = 0; h < m; ++h)
+      for (int32_t q = 0; q < n; ++q)
+        target[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
+    *objective = bits_f64(r.win_obj);
+    fill_stats_f64(stats, r);
+    return PP_OK;
+  });
+}
+
 int pp_replan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
               const int64_t* recompute_cost, const int64_t* fetch_cost,
               const int32_t* cap, const uint8_t* incumbent, int64_t horizon,
@@ -1237,21 +1386,28 @@ int pp_replan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand
   });
 }
 
-int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
-                 int32_t k, uint8_t* selected, int64_t* value) {
+static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v,
+                          int32_t k, uint8_t* selected, int64_t* value, bool f64) {
   g_err.clear();
   return guarded([&]() -> int {
     if (n < 1) return fail(PP_E_ARG, "n must be >= 1");
-    if (!parent || !profit || !selected || !value)
+    if (!parent || !profit_v || !selected || !value)
       return fail(PP_E_ARG, "null pointer argument");
     if (k < 0) return fail(PP_E_RANGE, "negative capacity");
+    const int64_t* profit = (const int64_t*)profit_v;
     unsigned __int128 tot = 0;
-    for (int32_t b = 0; b < n; ++b) {
-      if (profit[b] < 0) return fail(PP_E_RANGE, "negative profit");
-      tot += (uint64_t)profit[b];
+    if (f64) {
+      for (int32_t b = 0; b < n; ++b)
+        if (!finite_nonneg(((const double*)profit_v)[b]))
+          return fail(PP_E_RANGE, "profits must be finite and >= 0");
+    } else {
+      for (int32_t b = 0; b < n; ++b) {
+        if (profit[b] < 0) return fail(PP_E_RANGE, "negative profit");
+        tot += (uint64_t)profit[b];
+      }
+      if (tot > (unsigned __int128)INT64_MAX)
+        return fail(PP_E_OVERFLOW, "sum of profits exceeds INT64_MAX");
     }
-    if (tot > (unsigned __int128)INT64_MAX)
-      return fail(PP_E_OVERFLOW, "sum of profits exceeds INT64_MAX");
     TreeLayout t;
     PP_TRY(build_tree(n, parent, t));
     const int32_t kp = std::min(k, n);
@@ -1271,6 +1427,7 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     d.npad = npad_of(n);
     d.nextpos = c->nextpos.as<int32_t>();
     d.ce = c->ce.as<uint32_t>();
+    d.f64 = f64 ? 1 : 0;
     const int32_t slots_lds = t.slots;
     const int cells = choose_cells((kp + 63) / 64, c->device, slots_lds);
     PP_TRY(ensure_slots(c, d, 1, kp, cells));
@@ -1305,6 +1462,23 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
     *value = out.dpval;
     return PP_OK;
   });
+}
+
+int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
+                 int32_t k, uint8_t* selected, int64_t* value) {
+  return rooted_dp_impl(n, parent, profit, k, selected, value, false);
+}
+
+int pp_rooted_dp_f64(int32_t n, const int32_t* parent, const double* profit,
+                     int32_t k, uint8_t* selected, double* value) {
+  if (!value) {
+    g_err.clear();
+    return fail(PP_E_ARG, "null pointer argument");
+  }
+  int64_t v = 0;
+  const int rc = rooted_dp_impl(n, parent, profit, k, selected, &v, true);
+  if (rc == PP_OK) *value = bits_f64(v);
+  return rc;
 }
 
 // pp_marginal / pp_objective: chunks need no tree, so positions = ids.

@@ -63,6 +63,8 @@ struct ChainState {
   int32_t improved;  // some update of the current sweep was accepted
   int32_t accepts;   // accepted refinement replacements so far
   int32_t status;    // nonzero: a device-side wait gave up
+  int32_t changed;   // real-valued refinement: the accepted selection
+                     // differs from the incumbent set (counted once)
 };
 
 // The chains of one launch, passed by value as a kernel argument.
@@ -103,6 +105,13 @@ struct DevState {
   ChainState* cs;           // [slots]
   int32_t stages;           // stage stride of bits / ring
   int32_t cells;            // cells per lane of the DP sweep
+  // Real-valued costs: every value array (lam, w, f, v1, v2, profit, the
+  // ring and the ChainState values) then holds IEEE doubles, all finite
+  // and non-negative, so their bit patterns order like the values.
+  int32_t f64;
+  double eps;               // refinement tolerance (real-valued costs)
+  double* fpart;            // [slots][fpart_stride] per-block partial sums
+  int32_t fpart_stride;     //   summed in a fixed order (real-valued costs)
 };
 
 // Host-side launchers (pp_kernels.hip).  All enqueue on `st`.
@@ -118,6 +127,12 @@ hipError_t launch_validate(const int64_t* lam, const int64_t* w,
                            const int64_t* f, int32_t n, int32_t m,
                            uint64_t* partial, int32_t* neg, int32_t* nblocks,
                            hipStream_t st);
+// real-valued inputs: *bad = 1 if any value is negative, NaN or infinite
+hipError_t launch_validate_f64(const double* lam, const double* w,
+                               const double* f, int32_t n, int32_t m,
+                               int32_t* bad, hipStream_t st);
+// per-block partial sums of k_gains and k_objective for real-valued costs
+int32_t fpart_blocks(int32_t n, int32_t m);
 hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
                              int clear_tgt, hipStream_t st);
 hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
@@ -136,7 +151,8 @@ hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      int fmax, hipStream_t st);
 hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
                             hipStream_t st);
-hipError_t launch_commit(const ChainSet& set, const DevState& d, hipStream_t st);
+hipError_t launch_commit(const ChainSet& set, const DevState& d, int mode,
+                         hipStream_t st);
 hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
                               hipStream_t st);
 hipError_t launch_objective(const ChainSet& set, const DevState& d,

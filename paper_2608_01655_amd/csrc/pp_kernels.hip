@@ -17,6 +17,7 @@
 //
 // Integers only (int64 values, int32 indices); no floating point anywhere.
 
+#include <algorithm>
 #include <utility>
 
 #include "pp_internal.h"
@@ -31,13 +32,22 @@ __device__ __forceinline__ int64_t imax(int64_t a, int64_t b) {
   return a > b ? a : b;
 }
 
+// Real-valued costs travel as the bit patterns of IEEE doubles.
+__device__ __forceinline__ double as_f(int64_t v) { return __builtin_bit_cast(double, v); }
+__device__ __forceinline__ int64_t as_i(double v) { return __builtin_bit_cast(int64_t, v); }
+__device__ __forceinline__ double dpos(double v) { return v > 0.0 ? v : 0.0; }
+
 // Eq. 5: saving of requester `r` when its copy of chunk `i` comes from
-// holder `h` (fetch plane is [src][dst][pos]).
+// holder `h` (fetch plane is [src][dst][pos]).  For real-valued costs the
+// result is the bit pattern of a non-negative double, which compares like
+// the value.
 __device__ __forceinline__ int64_t saving(const DevState& d, int h, int r,
                                           int64_t i) {
   const int64_t wr = d.w[(int64_t)r * d.n + i];
   if (h == r) return wr;
-  return imax(wr - d.f[((int64_t)h * d.m + r) * d.n + i], 0);
+  const int64_t fv = d.f[((int64_t)h * d.m + r) * d.n + i];
+  if (d.f64) return as_i(dpos(as_f(wr) - as_f(fv)));
+  return imax(wr - fv, 0);
 }
 
 // Top-2 holder state of chunk i for every requester, from slot s's
@@ -103,6 +113,31 @@ __device__ int64_t block_sum(int64_t v) {
     for (int k = 0; k < (int)(blockDim.x / kWave); ++k) t += part[k];
   __syncthreads();
   return t;
+}
+
+// Sum of v over the block in a fixed order (shuffles within each wave, then
+// the waves in order); the result is in thread 0.
+__device__ double block_sum_f64(double v) {
+  __shared__ double part[256 / kWave];
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, kWave);
+  const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+  if (lane == 0) part[wv] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (threadIdx.x == 0)
+    for (int k = 0; k < (int)(blockDim.x / kWave); ++k) t += part[k];
+  __syncthreads();
+  return t;
+}
+
+// Sum of a[0..count) by one wave in a fixed order (lane-strided partial
+// sums, then a shuffle tree); every lane gets the result.
+__device__ double wave_sum_f64(const double* a, int count) {
+  const int lane = threadIdx.x % kWave;
+  double v = 0.0;
+  for (int q = lane; q < count; q += kWave) v += a[q];
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, kWave);
+  return __shfl(v, 0, kWave);
 }
 
 // ------------------------------------------------------------ helpers ---
@@ -177,6 +212,25 @@ __global__ void k_validate(const int64_t* __restrict__ lam, const int64_t* __res
 
 // Reset chain slots: empty placement (optional), zero holder state and
 // chain scalars.
+// Real-valued inputs: any negative, NaN or infinite value sets *bad.
+__global__ void k_validate_f64(const double* __restrict__ lam,
+                               const double* __restrict__ w,
+                               const double* __restrict__ f, int64_t mn,
+                               int64_t mmn, int32_t* bad) {
+  bool b = false;
+  const int64_t step = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mmn; x += step) {
+    const double fv = f[x];
+    b |= !(fv >= 0.0 && fv <= 1.7976931348623157e308);
+    if (x < mn) {
+      const double a = lam[x], c = w[x];
+      b |= !(a >= 0.0 && a <= 1.7976931348623157e308);
+      b |= !(c >= 0.0 && c <= 1.7976931348623157e308);
+    }
+  }
+  if (__syncthreads_or(b) && threadIdx.x == 0) atomicOr(bad, 1);
+}
+
 __global__ void k_init_slots(ChainSet set, DevState d, int clear_tgt) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
@@ -239,6 +293,26 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
     d.profit[s * n + i] = p;
     return;
   }
+  if (d.f64) {
+    // Eq. 7 on doubles: requester terms added in increasing r, each product
+    // rounded on its own; the incumbent value as per-block partial sums
+    double p = 0.0;
+    bool in_th = false;
+    if (i < n) {
+      for (int r = 0; r < d.m; ++r) {
+        const int64_t o = s * mn + (int64_t)r * n + i;
+        const double vmh = as_f((d.h1[o] == h) ? d.v2[o] : d.v1[o]);
+        const double L = as_f(d.lam[(int64_t)r * n + i]);
+        const double term = L * dpos(as_f(saving(d, h, r, i)) - vmh);
+        p = p + term;
+      }
+      d.profit[s * n + i] = as_i(p);
+      in_th = d.tgt[s * mn + (int64_t)h * n + i] != 0;
+    }
+    const double sh = block_sum_f64(in_th ? p : 0.0);
+    if (threadIdx.x == 0) d.fpart[s * d.fpart_stride + blockIdx.x] = sh;
+    return;
+  }
   int64_t p = 0, g = 0, held = 0;
   if (i < n) {
     for (int r = 0; r < d.m; ++r) {
@@ -262,15 +336,32 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
 // ------------------------------------------------------------ DP sweep --
 
 // acc * 2 + (t > sk): the lane's choice bit of this step shifted into its
-// 32-step word (the compare's lane mask is the add's carry-in).
+// 32-step word (the compare's lane mask is the add's carry-in).  F64: the
+// values are doubles.
+template <bool F64>
 __device__ __forceinline__ uint32_t shift_in_gt(int64_t t, int64_t sk,
                                                 uint32_t acc) {
   uint32_t r;
-  asm("v_cmp_gt_i64 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
-      : "=v"(r)
-      : "v"(t), "v"(sk), "v"(acc)
-      : "vcc");
+  if constexpr (F64)
+    asm("v_cmp_gt_f64 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
+        : "=v"(r)
+        : "v"(as_f(t)), "v"(as_f(sk)), "v"(acc)
+        : "vcc");
+  else
+    asm("v_cmp_gt_i64 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
+        : "=v"(r)
+        : "v"(t), "v"(sk), "v"(acc)
+        : "vcc");
   return r;
+}
+
+// a + b on integers, or on the doubles the bit patterns encode
+template <bool F64>
+__device__ __forceinline__ int64_t vadd(int64_t a, int64_t b) {
+  if constexpr (F64)
+    return as_i(as_f(a) + as_f(b));
+  else
+    return a + b;
 }
 
 // Take operands of a DP row: lanes 1..63 get r + v of lane l-1 (a 64-bit
@@ -279,8 +370,8 @@ __device__ __forceinline__ uint32_t shift_in_gt(int64_t t, int64_t sk,
 // two wait states after the VALU write of that VGPR: take_after_bit puts
 // the previous step's choice bit (t_prev > sk_prev, shifted into acc; two
 // instructions) in front of the shift, take_first pads with s_nop.
-__device__ __forceinline__ int64_t take_after_bit(int64_t r, int64_t v, int64_t t_prev,
-                                                  int64_t sk_prev, uint32_t& acc) {
+__device__ __forceinline__ int64_t take_after_bit_i64(int64_t r, int64_t v, int64_t t_prev,
+                                                      int64_t sk_prev, uint32_t& acc) {
   const pp_int2 rv = split64(r), vv = split64(v);
   pp_int2 t;
   asm("v_cmp_gt_i64 vcc, %3, %4\n\t"
@@ -293,7 +384,7 @@ __device__ __forceinline__ int64_t take_after_bit(int64_t r, int64_t v, int64_t 
   return join64(t);
 }
 
-__device__ __forceinline__ int64_t take_first(int64_t r, int64_t v) {
+__device__ __forceinline__ int64_t take_first_i64(int64_t r, int64_t v) {
   const pp_int2 rv = split64(r), vv = split64(v);
   pp_int2 t;
   asm("s_nop 1\n\t"
@@ -303,6 +394,18 @@ __device__ __forceinline__ int64_t take_first(int64_t r, int64_t v) {
       : "v"(vv.x), "v"(vv.y), "v"(rv.x), "v"(rv.y)
       : "vcc");
   return join64(t);
+}
+
+// Real-valued costs: v_add_f64 has no DPP form, so the left lane's 64-bit
+// value is moved across first (two DPP moves, wave_shr:1, zero for lane 0
+// by bound_ctrl) and added as doubles; lane 0 then gets r + 0.0 = r (r is a
+// non-negative double).  The compiler inserts the DPP wait states.
+__device__ __forceinline__ int64_t take_f64(int64_t r, int64_t v) {
+  const pp_int2 vv = split64(v);
+  pp_int2 sh;
+  sh.x = __builtin_amdgcn_update_dpp(0, vv.x, 0x138, 0xf, 0xf, true);
+  sh.y = __builtin_amdgcn_update_dpp(0, vv.y, 0x138, 0xf, 0xf, true);
+  return as_i(as_f(r) + as_f(join64(sh)));
 }
 
 // LDS byte address of a row cell: base + 8 * (low or high 16-bit half of w),
@@ -402,7 +505,7 @@ constexpr size_t dp_ctl_bytes() {
          2 * C * kWave * sizeof(uint32_t) + 16;
 }
 
-template <int C, bool FMAX>
+template <int C, bool FMAX, bool F64>
 __global__ void __launch_bounds__(2 * kWave)
 k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
      int store_bits, int32_t slots) {
@@ -518,7 +621,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         v.leaf = mv.z;
         StepView* dst = recs + ((b % 2) * (kBatch + 1) + lane) * 2;
         dst[0] = v;
-        v.r = pv + bnd;  // no overflow: a feasible set's value
+        v.r = vadd<F64>(pv, bnd);  // no overflow: a feasible set's value
         dst[1] = v;
       }
     };
@@ -709,14 +812,18 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       int64_t t[C], sk[C], y[C];
       // cell 0's take operand comes from the left lane (lane 0: r0 already
       // holds it); the previous step's choice bits go in first
-      if constexpr (u == 0)
-        t[0] = take_first(r0, x[C - 1]);
-      else
-        t[0] = take_after_bit(r0, x[C - 1], tp[0], skp[0], acc[0]);
+      if constexpr (F64) {
+        if constexpr (u > 0) acc[0] = shift_in_gt<true>(tp[0], skp[0], acc[0]);
+        t[0] = take_f64(r0, x[C - 1]);
+      } else if constexpr (u == 0) {
+        t[0] = take_first_i64(r0, x[C - 1]);
+      } else {
+        t[0] = take_after_bit_i64(r0, x[C - 1], tp[0], skp[0], acc[0]);
+      }
 #pragma unroll
       for (int c = 1; c < C; ++c) {
-        if constexpr (u > 0) acc[c] = shift_in_gt(tp[c], skp[c], acc[c]);
-        t[c] = pv[u % kRq] + x[c - 1];
+        if constexpr (u > 0) acc[c] = shift_in_gt<F64>(tp[c], skp[c], acc[c]);
+        t[c] = vadd<F64>(pv[u % kRq], x[c - 1]);
       }
 #pragma unroll
       for (int c = 0; c < C; ++c) {
@@ -754,7 +861,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     unroll_steps(step, std::make_integer_sequence<int, kBatch>{});
     // choice bits of the batch's last step
 #pragma unroll
-    for (int c = 0; c < C; ++c) acc[c] = shift_in_gt(tp[c], skp[c], acc[c]);
+    for (int c = 0; c < C; ++c) acc[c] = shift_in_gt<F64>(tp[c], skp[c], acc[c]);
     // hand the batch's outputs to the I/O wave
 #pragma unroll
     for (int c = 0; c < C; ++c) outb[(buf * C + c) * kWave + lane] = acc[c];
@@ -1048,14 +1155,34 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   const int kp = set.kprime[ci];
   const int n = d.n;
   ChainState* st = d.cs + slot;
-  const int64_t dpval = st->dpval, inc = st->inc;
-  const bool accept = (mode == kModeGreedy) || (dpval > inc);
-  if (lane == 0) {
-    st->accept = accept ? 1 : 0;
-    st->inc = 0;
-    if (mode == kModeRefine && accept) {
-      st->improved = 1;
-      st->accepts += 1;
+  const int64_t dpval = st->dpval;
+  bool accept;
+  if (d.f64) {
+    // G(T_-h, T'_h) > G(T) + eps with Proposition 1: DP value > incumbent
+    // value + eps; the incumbent value is summed from k_gains' per-block
+    // partials in a fixed order.  A replacement is counted (improved,
+    // accepts) by k_commit only if it changes the set, so that rounding
+    // alone never accepts the incumbent set again.
+    accept = true;
+    if (mode != kModeGreedy) {
+      const double inc = wave_sum_f64(d.fpart + slot * d.fpart_stride,
+                                      (n + 255) / 256);
+      accept = as_f(dpval) > inc + d.eps;
+    }
+    if (lane == 0) {
+      st->accept = accept ? 1 : 0;
+      st->changed = 0;
+    }
+  } else {
+    const int64_t inc = st->inc;
+    accept = (mode == kModeGreedy) || (dpval > inc);
+    if (lane == 0) {
+      st->accept = accept ? 1 : 0;
+      st->inc = 0;
+      if (mode == kModeRefine && accept) {
+        st->improved = 1;
+        st->accepts += 1;
+      }
     }
   }
   if (!accept) return;
@@ -1189,7 +1316,8 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
 // the new selection, and the new membership is written after a barrier.
 constexpr int kCommitThreads = 256;
 
-__global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevState d) {
+__global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevState d,
+                                                            int mode) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
   if (!d.cs[s].accept) return;
@@ -1209,6 +1337,12 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
     changed = nv != th[i];
   }
   if (!__syncthreads_or(changed)) return;
+  if (d.f64 && mode == kModeRefine && threadIdx.x == 0 &&
+      atomicExch(&d.cs[s].changed, 1) == 0) {
+    // the first block that sees a change counts the replacement
+    d.cs[s].improved = 1;
+    d.cs[s].accepts += 1;
+  }
   if (changed) {
     const int64_t wr = d.w[(int64_t)r * n + i];
     int64_t b1 = 0, b2 = 0;
@@ -1217,7 +1351,9 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
     for (int l = 0; l < m; ++l) {
       const bool held = (l == h) ? nv != 0 : t[(int64_t)l * n + i] != 0;
       const int64_t fv = (l == r) ? 0 : d.f[((int64_t)l * m + r) * n + i];
-      const int64_t q = (l == r) ? wr : imax(wr - fv, 0);
+      const int64_t q = (l == r) ? wr
+                        : d.f64 ? as_i(dpos(as_f(wr) - as_f(fv)))
+                                : imax(wr - fv, 0);
       if (held) {
         if (hb == kNoHolder || q > b1) {
           b2 = (hb == kNoHolder) ? b2 : b1;
@@ -1309,11 +1445,24 @@ __global__ void k_reset_round(ChainSet set, DevState d) {
 
 // ----------------------------------------------------------- objective --
 
-// F_pair(T) = sum_{m,b} Lambda_m(b) * v1_m(b)   (Eq. 6)
+// F_pair(T) = sum_{m,b} Lambda_m(b) * v1_m(b)   (Eq. 6).  Real-valued
+// costs: per-block partial sums, added by k_objective_final in a fixed
+// order (the same placement always gets the same value).
 __global__ void __launch_bounds__(256) k_objective(ChainSet set, DevState d) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
   const int64_t mn = (int64_t)d.m * d.n;
+  if (d.f64) {
+    double a = 0.0;
+    for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+         x += (int64_t)gridDim.x * blockDim.x) {
+      const double term = as_f(d.lam[x]) * as_f(d.v1[s * mn + x]);
+      a = a + term;
+    }
+    const double t = block_sum_f64(a);
+    if (threadIdx.x == 0) d.fpart[s * d.fpart_stride + blockIdx.x] = t;
+    return;
+  }
   int64_t acc = 0;
   for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
        x += (int64_t)gridDim.x * blockDim.x)
@@ -1321,6 +1470,12 @@ __global__ void __launch_bounds__(256) k_objective(ChainSet set, DevState d) {
   const int64_t t = block_sum(acc);
   if (threadIdx.x == 0 && t)
     atomicAdd((unsigned long long*)&d.cs[s].obj, (unsigned long long)t);
+}
+
+__global__ void k_objective_final(ChainSet set, DevState d, int32_t nblocks) {
+  const int64_t s = set.slot[blockIdx.x];
+  const double g = wave_sum_f64(d.fpart + s * d.fpart_stride, nblocks);
+  if (threadIdx.x == 0) d.cs[s].obj = as_i(g);
 }
 
 inline dim3 grid1(int64_t work, int bs, int rows) {
@@ -1372,6 +1527,24 @@ hipError_t launch_validate(const int64_t* lam, const int64_t* w,
   hipLaunchKernelGGL(k_validate, dim3((unsigned)b), dim3(256), 0, st, lam, w,
                      f, mn, mmn, partial, neg);
   return hipGetLastError();
+}
+
+hipError_t launch_validate_f64(const double* lam, const double* w,
+                               const double* f, int32_t n, int32_t m,
+                               int32_t* bad, hipStream_t st) {
+  const int64_t mn = (int64_t)m * n, mmn = mn * m;
+  int64_t b = (mmn + 255) / 256;
+  if (b > 2048) b = 2048;
+  hipLaunchKernelGGL(k_validate_f64, dim3((unsigned)b), dim3(256), 0, st, lam, w, f,
+                     mn, mmn, bad);
+  return hipGetLastError();
+}
+
+int32_t fpart_blocks(int32_t n, int32_t m) {
+  // k_gains: one block per 256 chunks; k_objective: up to 1024 blocks
+  const int64_t gains = ((int64_t)n + 255) / 256;
+  const int64_t obj = std::min<int64_t>(((int64_t)m * n + 255) / 256, 1024);
+  return (int32_t)std::max<int64_t>(std::max(gains, obj), 1);
 }
 
 hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
@@ -1431,13 +1604,13 @@ size_t dp_lds_bytes(int cells, int32_t slots_lds) {
   return ctl + (size_t)(slots_lds + 1 + dp_sink_rows(cells)) * dp_row_stride(cells);
 }
 
-template <int C, bool FMAX>
+template <int C, bool FMAX, bool F64 = false>
 static hipError_t dp_launch_c(const ChainSet& set, const DevState& d,
                               uint32_t epoch, uint32_t spin_limit,
                               int store_bits, int32_t slots_lds,
                               hipStream_t st) {
   const size_t lds = dp_lds_bytes(C, slots_lds);
-  hipLaunchKernelGGL((k_dp<C, FMAX>), dim3((unsigned)set.base[set.count]),
+  hipLaunchKernelGGL((k_dp<C, FMAX, F64>), dim3((unsigned)set.base[set.count]),
                      dim3(2 * kWave), lds, st, set, d, epoch, spin_limit,
                      store_bits, slots_lds);
   return hipGetLastError();
@@ -1446,6 +1619,15 @@ static hipError_t dp_launch_c(const ChainSet& set, const DevState& d,
 hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      uint32_t spin_limit, int store_bits, int32_t slots_lds,
                      int fmax, hipStream_t st) {
+  if (d.f64) {
+    // doubles: v_max_f64 is the plain maximum
+    switch (d.cells) {
+      case 1: return dp_launch_c<1, true, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+      case 2: return dp_launch_c<2, true, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+      case 4: return dp_launch_c<4, true, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (d.cells * 2 + (fmax ? 1 : 0)) {
     case 2: return dp_launch_c<1, false>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
     case 3: return dp_launch_c<1, true>(set, d, epoch, spin_limit, store_bits, slots_lds, st);
@@ -1458,16 +1640,28 @@ hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
 }
 
 int dp_resident_blocks(int cells, int32_t slots_lds, int device) {
-  int per_cu = 0, cus = 0;
+  int per_cu = 0, per_cu_f = 0, cus = 0;
   const size_t lds = dp_lds_bytes(cells, slots_lds);
-  hipError_t e = hipErrorInvalidValue;
+  hipError_t e = hipErrorInvalidValue, e2 = hipErrorInvalidValue;
+  // the integer and the real-valued variants; the smaller residency holds
+  // for both
   switch (cells) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1, false>, 2 * kWave, lds); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2, false>, 2 * kWave, lds); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4, false>, 2 * kWave, lds); break;
+    case 1:
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<1, false, false>, 2 * kWave, lds);
+      e2 = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_f, k_dp<1, true, true>, 2 * kWave, lds);
+      break;
+    case 2:
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<2, false, false>, 2 * kWave, lds);
+      e2 = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_f, k_dp<2, true, true>, 2 * kWave, lds);
+      break;
+    case 4:
+      e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_dp<4, false, false>, 2 * kWave, lds);
+      e2 = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_f, k_dp<4, true, true>, 2 * kWave, lds);
+      break;
     default: return 0;
   }
-  if (e != hipSuccess) return 0;
+  if (e != hipSuccess || e2 != hipSuccess) return 0;
+  per_cu = std::min(per_cu, per_cu_f);
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
     return 0;
   return per_cu * cus;
@@ -1484,9 +1678,10 @@ hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
   return hipGetLastError();
 }
 
-hipError_t launch_commit(const ChainSet& set, const DevState& d, hipStream_t st) {
+hipError_t launch_commit(const ChainSet& set, const DevState& d, int mode,
+                         hipStream_t st) {
   hipLaunchKernelGGL(k_commit, grid1(d.n, kCommitThreads / d.m, set.count),
-                     dim3(kCommitThreads), 0, st, set, d);
+                     dim3(kCommitThreads), 0, st, set, d, mode);
   return hipGetLastError();
 }
 
@@ -1503,6 +1698,10 @@ hipError_t launch_objective(const ChainSet& set, const DevState& d,
   if (b > 1024) b = 1024;
   hipLaunchKernelGGL(k_objective, dim3((unsigned)b, set.count), dim3(256), 0,
                      st, set, d);
+  if (d.f64) {
+    hipLaunchKernelGGL(k_objective_final, dim3(set.count), dim3(kWave), 0, st,
+                       set, d, (int32_t)b);
+  }
   return hipGetLastError();
 }
 

@@ -335,6 +335,22 @@ def prefix_incumbent(n: int, cap: np.ndarray) -> np.ndarray:
     return inc
 
 
+def real_valued(inst: "Instance", seed: int, jitter: float = 0.25) -> tuple:
+    """The workload in the paper's own units, as doubles: demand in requests
+    per epoch scaled by a per-entry factor U[1 - jitter, 1 + jitter], and
+    recompute and fetch costs in milliseconds (microseconds / 1000), each
+    scaled by its own factor from the same range.  Returns (demand,
+    recompute_cost, fetch_cost); the diagonal of the fetch plane stays 0."""
+    rng = np.random.default_rng(seed)
+    lo, hi = 1.0 - jitter, 1.0 + jitter
+    lam = inst.demand * rng.uniform(lo, hi, size=inst.demand.shape)
+    w = inst.recompute_cost / 1000.0 * rng.uniform(lo, hi, size=inst.recompute_cost.shape)
+    f = inst.fetch_cost / 1000.0 * rng.uniform(lo, hi, size=inst.fetch_cost.shape)
+    for i in range(inst.m):
+        f[i, i, :] = 0.0
+    return lam, w, f
+
+
 # --------------------------------------------------------------------------
 # The five benchmark workloads
 # --------------------------------------------------------------------------

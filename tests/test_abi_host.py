@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(L):
     assert len(names) >= 11
     for name in names:
         assert hasattr(L, name), name
-    assert B.pp_abi_version() == 4
+    assert B.pp_abi_version() == 5
 
 
 def _validate(inst, **kw):
@@ -155,3 +155,29 @@ def test_replan_validation(L):
                      z.ctypes.data_as(P), z.ctypes.data_as(P), 1, None,
                      z.ctypes.data_as(P), None, None, None)
     assert rc == B.PP_E_ARG  # info is required
+
+
+def test_real_valued_validation(L):
+    inst = W.make_workload("tiny")
+    lam, w, f = (inst.demand.astype(float), inst.recompute_cost.astype(float),
+                 inst.fetch_cost.astype(float))
+
+    def call(lam=lam, w=w, f=f, eps=0.0, flags=B.PP_F_VALIDATE_ONLY):
+        return B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps,
+                             flags=flags)
+
+    p = call()
+    assert p.target.sum() == 0
+    for bad in (np.nan, np.inf, -0.5):
+        l2 = lam.copy()
+        l2[1, 2] = bad
+        _expect(B.PP_E_RANGE, lambda: call(lam=l2))
+        f2 = f.copy()
+        f2[0, 1, 3] = bad
+        _expect(B.PP_E_RANGE, lambda: call(f=f2))
+    _expect(B.PP_E_ARG, lambda: call(eps=-1.0))
+    _expect(B.PP_E_ARG, lambda: call(eps=np.nan))
+    _expect(B.PP_E_UNSUPPORTED,
+            lambda: call(flags=B.PP_F_VALIDATE_ONLY | B.PP_F_SAFEGUARDS))
+    _expect(B.PP_E_RANGE, lambda: B.pp_rooted_dp_f64(inst.parent,
+                                                     np.full(inst.n, -1.0), 3))
