@@ -6,7 +6,9 @@ refinement until no sweep improves, best start) of the tree50k workload
 source-dependent fetch costs) through the device-resident C-ABI entry point,
 inputs already in HBM.  Prints one JSON line.  After the timed region a
 re-planning leg (a 50% routing shift of the same workload, through the
-host-array entry point) adds a "replan" object; --no-replan skips it.
+host-array entry point) adds a "replan" object, and a real-valued leg (the
+same workload in requests and milliseconds, as doubles) an "f64" object;
+--no-replan and --no-f64 skip them.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
@@ -181,6 +183,58 @@ def replan_leg(B, W, inst, steps, warmup):
     return out
 
 
+def f64_leg(B, W, inst, ctx, steps, warmup):
+    """The same workload in the paper's own units, as doubles (requests per
+    epoch and milliseconds, each entry jittered), planned through the
+    real-valued device entry point with epsilon = 1e-9 of sum(demand *
+    recompute cost); inputs already in HBM."""
+    import numpy as np
+    import torch
+
+    lam, w, f = W.real_valued(inst, 1)
+    eps = 1e-9 * float(np.sum(lam * w))
+    dev = torch.device("cuda:0")
+    tl = torch.from_numpy(lam).to(dev)
+    tw = torch.from_numpy(w).to(dev)
+    tf = torch.from_numpy(f).to(dev)
+    tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+
+    def call(flags=0):
+        return ctx.pp_plan_f64_device(inst.parent, tl, tw, tf, inst.cap, tgt,
+                                      epsilon=eps, n_starts=inst.n_starts,
+                                      max_rounds=inst.max_rounds,
+                                      order_seed=inst.order_seed, flags=flags)
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plans = [call(B.PP_F_TIME_KERNELS) for _ in range(steps)]
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    p = plans[-1]
+    dp_ms = sum(q.dp_kernel_ms for q in plans)
+    launches = sum(q.dp_launches for q in plans)
+    out = {"plans_per_s": 1.0 / dt, "ms_per_plan": dt * 1e3,
+           "dp_avg_launch_ms": dp_ms / launches,
+           "dp_launches_per_plan": launches // steps,
+           "dp_cells_per_s_in_kernel": p.dp_cells * steps / (dp_ms / 1e3),
+           "objective": p.objective, "epsilon": eps,
+           "sweeps_per_start": p.start_sweeps.tolist(),
+           "units": "requests/epoch and ms, per-entry jitter U[0.75, 1.25]"}
+    gold_path = os.path.join(ROOT, "tests", "golden", "plans_f64.json")
+    if os.path.exists(gold_path):
+        with open(gold_path) as fh:
+            gold = json.load(fh).get(inst.name)
+        if gold:
+            out["parity_vs_golden"] = all(
+                q.best_start == gold["best_start"]
+                and q.start_sweeps.tolist() == gold["start_sweeps"]
+                and abs(q.objective - float.fromhex(gold["objective"]))
+                <= 1e-12 * abs(q.objective) for q in plans)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -196,6 +250,8 @@ def main():
                     help="skip the re-planning leg")
     ap.add_argument("--no-host-plan", action="store_true",
                     help="skip the timing of the host-array entry point")
+    ap.add_argument("--no-f64", action="store_true",
+                    help="skip the real-valued leg")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device (counter "
                          "calibration) and exit")
@@ -345,6 +401,10 @@ def main():
         log("[bench] re-planning leg")
         out["replan"] = replan_leg(B, W, inst, max(1, min(args.steps, 3)),
                                    min(args.warmup, 1))
+    if not args.no_f64 and not args.safeguards:
+        log("[bench] real-valued leg")
+        out["f64"] = f64_leg(B, W, inst, ctx, max(1, min(args.steps, 3)),
+                             min(args.warmup, 1))
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         threads = max(1, min(8, os.cpu_count() or 1))

@@ -150,3 +150,60 @@ def test_device_entry_rag10k_real_valued(oracle_mod):
     ctx.close()
     o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
     _same_real(first, o)
+
+
+def test_cells_per_lane_do_not_change_the_result(oracle_mod):
+    """One, two or four DP cells per lane: the same real-valued plan, equal
+    to the oracle's."""
+    inst = W.make_workload("tree2k")
+    lam, w, f = W.real_valued(inst, 2)
+    eps = 1e-9 * float(np.sum(lam * w))
+    kw = dict(n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+              order_seed=inst.order_seed)
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
+    for cells in ("1", "2", "4"):
+        os.environ["PP_DP_CELLS"] = cells
+        try:
+            g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
+        finally:
+            del os.environ["PP_DP_CELLS"]
+        _same_real(g, o)
+
+
+def test_tree50k_real_valued_golden():
+    """The 50,000-chunk, 16-worker benchmark tree in the paper's units, at
+    the benchmark's start settings, through the device entry point, against
+    the oracle's stored real-valued plan."""
+    import torch
+
+    with open(os.path.join(os.path.dirname(GOLDEN), "plans_f64.json")) as fh:
+        gold = json.load(fh)["tree50k"]
+    inst = W.make_workload("tree50k")
+    lam, w, f = W.real_valued(inst, 1)
+    digest = hashlib.sha256(lam.tobytes() + w.tobytes() + f.tobytes()).hexdigest()
+    assert digest == gold["inputs_sha256"]
+    eps = float.fromhex(gold["epsilon"])
+    dev = torch.device("cuda:0")
+    tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+    ctx = B.Context(0)
+    p = ctx.pp_plan_f64_device(inst.parent, torch.from_numpy(lam).to(dev),
+                               torch.from_numpy(w).to(dev),
+                               torch.from_numpy(f).to(dev), inst.cap, tgt,
+                               epsilon=eps, n_starts=inst.n_starts,
+                               max_rounds=inst.max_rounds,
+                               order_seed=inst.order_seed)
+    target = tgt.cpu().numpy()
+    ctx.close()
+    assert p.standalone.tolist() == [float.fromhex(x) for x in gold["standalone"]]
+    assert p.orders.tolist() == gold["orders"]
+    assert p.start_sweeps.tolist() == gold["start_sweeps"]
+    assert p.start_accepts.tolist() == gold["start_accepts"]
+    assert p.best_start == gold["best_start"]
+    assert (p.updates, p.dp_cells) == (gold["updates"], gold["dp_cells"])
+    np.testing.assert_allclose(p.start_objective,
+                               [float.fromhex(x) for x in gold["start_objective"]],
+                               rtol=1e-12)
+    assert p.objective == pytest.approx(float.fromhex(gold["objective"]), rel=1e-12)
+    rows = [hashlib.sha256(np.ascontiguousarray(target[h]).tobytes()).hexdigest()
+            for h in range(inst.m)]
+    assert rows == gold["target_row_sha256"]
