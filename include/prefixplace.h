@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 5
+#define PP_ABI_VERSION 6
 
 enum {
     PP_OK = 0,
@@ -160,9 +160,10 @@ int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
  * and a replacement that leaves the worker's set unchanged is never counted
  * as an improvement.  The acceptance test uses Proposition 1 (DP value >
  * incumbent value + epsilon); objectives are summed in a fixed order, so a
- * placement always gets the same value.  PP_F_SAFEGUARDS is not offered
- * here (PP_E_UNSUPPORTED).  Statistics as pp_stats, with double objectives
- * and standalone scores. */
+ * placement always gets the same value.  PP_F_SAFEGUARDS adds the comparator
+ * candidates for requester-side costs (fetch costs equal as values over
+ * every source; -0.0 counts as 0.0) with the integer path's formulas in
+ * doubles.  Statistics as pp_stats, with double objectives and scores. */
 typedef struct {
     int32_t best_start;
     int32_t n_starts;
@@ -175,6 +176,8 @@ typedef struct {
     int32_t *orders;           /* [S][m] or NULL */
     double dp_kernel_ms;
     int32_t dp_launches;
+    int32_t safeguards_run;
+    double safeguard_objective[3];
 } pp_stats_f64;
 
 /* pp_plan on real-valued host arrays (layouts as pp_plan). */

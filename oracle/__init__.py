@@ -66,7 +66,7 @@ def lib() -> ctypes.CDLL:
         L.ppo_marginal_f64.argtypes = [i32, i32, P, P, P, P, i32, P]
         L.ppo_objective_f64.argtypes = [i32, i32, P, P, P, P, P]
         L.ppo_plan_f64.argtypes = [i32, i32, P, P, P, P, P, f64, i32, i32, u64,
-                                   P, u32, P, P, P, P, P, P, P, P]
+                                   P, u32, P, P, P, P, P, P, P, P, P]
         L.ppo_candidates.argtypes = [i32, i32, P, P, P, P, P, P, P]
         L.ppo_materialization_cost.argtypes = [i32, i32, P, P, P, P, P]
         L.ppo_replan.argtypes = [i32, i32, P, P, P, P, P, P, i64, i32, i32,
@@ -346,6 +346,8 @@ class PlanF64Result:
     best_start: int
     updates: int
     dp_cells: int
+    safeguards_run: bool = False
+    safeguard_objective: tuple = (0.0, 0.0, 0.0)
 
 
 def plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,
@@ -369,15 +371,18 @@ def plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,
     so = np.zeros(S, np.float64)
     ss = np.zeros(S, np.int32)
     sa = np.zeros(S, np.int32)
-    info = np.zeros(4, np.int64)
+    info = np.zeros(5, np.int64)
+    sgo = np.zeros(3, np.float64)
     _check(lib().ppo_plan_f64(n, m, _p(parent), _p(demand), _p(w), _p(f),
                               _p(cap), float(epsilon), int(n_starts),
                               int(max_rounds),
                               ctypes.c_uint64(order_seed & (2**64 - 1)),
                               _p(orders_in), int(flags), _p(tgt), _p(obj),
                               _p(st), _p(ords), _p(so), _p(ss), _p(sa),
-                              _p(info)))
+                              _p(info), _p(sgo)))
     return PlanF64Result(target=tgt, objective=float(obj[0]), standalone=st,
                          orders=ords, start_objective=so, start_sweeps=ss,
                          start_accepts=sa, best_start=int(info[0]),
-                         updates=int(info[1]), dp_cells=int(info[2]))
+                         updates=int(info[1]), dp_cells=int(info[2]),
+                         safeguards_run=bool(info[4]),
+                         safeguard_objective=tuple(float(x) for x in sgo))

@@ -62,7 +62,8 @@
  *       G(T) sums over b outer, m inner; the DP takes b_i only if
  *       t > s; a refinement replacement is accepted iff
  *       G(T_-h, T'_h) > G(T) + epsilon, both G evaluated from scratch;
- *       starts compare G exactly (earliest start on equal values).
+ *       starts compare G exactly (earliest start on equal values); the
+ *       comparator candidates use R18-R20 with value equality of doubles.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -1271,10 +1272,84 @@ out:
     return rc;
 }
 
+/* R18 on doubles: fetch_cost[src][dst][b] equal (as values) over src != dst */
+static int requester_side_f64(int32_t n, int32_t m, const double *fetch_cost)
+{
+    for (int32_t dst = 0; dst < m; dst++) {
+        int32_t first = dst == 0 ? 1 : 0;
+        for (int32_t src = first + 1; src < m; src++) {
+            if (src == dst)
+                continue;
+            for (int32_t b = 0; b < n; b++)
+                if (fetch_cost[((size_t)src * m + dst) * n + b] !=
+                    fetch_cost[((size_t)first * m + dst) * n + b])
+                    return 0;
+        }
+    }
+    return 1;
+}
+
+/* The comparator placements (R19) on doubles, with the integer path's
+ * formulas: Independent p = Lambda_h * w_h, Popularity p = Lambda_h,
+ * LocalDedup p = a + [b not in U] * Lambda_h * [w_h - f_h]_+ with
+ * a = Lambda_h * min(w_h, f_h) (M = 1: Lambda_h * w_h). */
+static int candidates_f64(int32_t n, int32_t m, const int32_t *order,
+                          const int32_t *nextpos, const double *demand,
+                          const double *recompute_cost, const double *fetch_cost,
+                          const int32_t *cap, uint8_t *targets, double *objs)
+{
+    double *pp = malloc((size_t)n * sizeof(double));
+    uint8_t *sp = malloc((size_t)n);
+    int rc = PPO_E_NOMEM;
+    if (!pp || !sp)
+        goto out;
+    memset(targets, 0, (size_t)3 * m * n);
+    for (int32_t c = 0; c < 3; c++) {
+        uint8_t *tg = targets + (size_t)c * m * n;
+        for (int32_t h = 0; h < m; h++) {
+            const double *lam = demand + (size_t)h * n;
+            const double *w = recompute_cost + (size_t)h * n;
+            int32_t src = h == 0 ? 1 : 0;
+            const double *f = m > 1 ? fetch_cost + ((size_t)src * m + h) * n : NULL;
+            for (int32_t i = 0; i < n; i++) {
+                int32_t b = order[i];
+                double p;
+                if (c == 0) {
+                    p = lam[b] * w[b];
+                } else if (c == 1) {
+                    p = lam[b];
+                } else if (!f) {
+                    p = lam[b] * w[b];
+                } else {
+                    int covered = 0;
+                    for (int32_t l = 0; l < h; l++)
+                        covered |= tg[(size_t)l * n + b];
+                    double a = lam[b] * (w[b] < f[b] ? w[b] : f[b]);
+                    double own = lam[b] * maxd(w[b] - f[b], 0.0);
+                    p = covered ? a : a + own;
+                }
+                pp[i] = p;
+            }
+            double v;
+            rc = rooted_dp_pos_f64(n, nextpos, pp, cap[h], sp, &v);
+            if (rc != PPO_OK)
+                goto out;
+            for (int32_t i = 0; i < n; i++)
+                tg[(size_t)h * n + order[i]] = sp[i];
+        }
+        objs[c] = objective_f64(n, m, demand, recompute_cost, fetch_cost, tg);
+    }
+    rc = PPO_OK;
+out:
+    free(pp); free(sp);
+    return rc;
+}
+
 /* The planner on real-valued costs (R24), one start after another.
  * Arguments as ppo_plan, with double inputs and outputs, the tolerance
- * `epsilon` (finite, >= 0) and info[4] = {returned start, updates, DP
- * cells, S}.  The comparator safeguards are not offered here. */
+ * `epsilon` (finite, >= 0), info[5] = {returned candidate (start s, or
+ * S + c for safeguard c), updates, DP cells, S, safeguards run} and
+ * safeguard_obj[3] (0 if not run). */
 int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
                  const double *demand, const double *recompute_cost,
                  const double *fetch_cost, const int32_t *cap, double epsilon,
@@ -1282,13 +1357,14 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
                  const int32_t *orders_in, uint32_t flags, uint8_t *target,
                  double *objective, double *standalone_out,
                  int32_t *orders_out, double *start_objective,
-                 int32_t *start_sweeps, int32_t *start_accepts, int64_t *info)
+                 int32_t *start_sweeps, int32_t *start_accepts, int64_t *info,
+                 double *safeguard_obj)
 {
     int rc = validate_f64(n, m, parent, demand, recompute_cost, fetch_cost, cap);
     if (rc != PPO_OK)
         return rc;
     if (n_starts < 0 || max_rounds < 0 || !target || !objective ||
-        !finite_nonneg(epsilon) || (flags & PPO_F_SAFEGUARDS))
+        !finite_nonneg(epsilon))
         return PPO_E_ARG;
     int32_t S = ppo_num_starts(m, n_starts);
     if (orders_in) {
@@ -1310,7 +1386,7 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
     double *standalone = malloc((size_t)m * sizeof(double));
     int64_t *rank = malloc((size_t)m * sizeof(int64_t));
     uint8_t *tgts = malloc((size_t)S * m * n);
-    double *obj = malloc((size_t)S * sizeof(double));
+    double *obj = calloc((size_t)S, sizeof(double));
     int32_t *sw = malloc((size_t)S * sizeof(int32_t));
     int32_t *ac = malloc((size_t)S * sizeof(int32_t));
     double *profit = malloc((size_t)n * sizeof(double));
@@ -1318,6 +1394,7 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
     uint8_t *sp = malloc((size_t)n);
     uint8_t *cand = malloc((size_t)n);
     uint8_t *empty = calloc((size_t)m * n, 1);
+    uint8_t *cands = NULL;
     rc = PPO_E_NOMEM;
     if (!order || !nextpos || !orders || !standalone || !rank || !tgts ||
         !obj || !sw || !ac || !profit || !pp || !sp || !cand || !empty)
@@ -1357,8 +1434,29 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
     for (int32_t s = 1; s < S; s++)
         if (obj[s] > obj[best])
             best = s;
-    memcpy(target, tgts + (size_t)best * m * n, (size_t)m * n);
-    *objective = obj[best];
+    const uint8_t *won = tgts + (size_t)best * m * n;
+    double won_obj = obj[best];
+    double sg_obj[3] = {0.0, 0.0, 0.0};
+    int sg_run = 0;
+    if ((flags & PPO_F_SAFEGUARDS) && requester_side_f64(n, m, fetch_cost)) {
+        cands = malloc((size_t)3 * m * n);
+        rc = PPO_E_NOMEM;
+        if (!cands)
+            goto out;
+        rc = candidates_f64(n, m, order, nextpos, demand, recompute_cost,
+                            fetch_cost, cap, cands, sg_obj);
+        if (rc != PPO_OK)
+            goto out;
+        sg_run = 1;
+        for (int32_t c = 0; c < 3; c++)  /* R20 */
+            if (sg_obj[c] > won_obj) {
+                won_obj = sg_obj[c];
+                won = cands + (size_t)c * m * n;
+                best = S + c;
+            }
+    }
+    memcpy(target, won, (size_t)m * n);
+    *objective = won_obj;
     int64_t updates = m, cells = 0;
     for (int32_t h = 0; h < m; h++)
         cells += (int64_t)n * (cap[h] < n ? cap[h] : n);
@@ -1377,16 +1475,23 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
         memcpy(start_sweeps, sw, (size_t)S * sizeof(int32_t));
     if (start_accepts)
         memcpy(start_accepts, ac, (size_t)S * sizeof(int32_t));
+    if (sg_run) {
+        updates += 3 * (int64_t)m;
+        cells += 3 * cells_per_pass;
+    }
     if (info) {
         info[0] = best;
         info[1] = updates;
         info[2] = cells;
         info[3] = S;
+        info[4] = sg_run;
     }
+    if (safeguard_obj)
+        memcpy(safeguard_obj, sg_obj, sizeof sg_obj);
     rc = PPO_OK;
 out:
     free(order); free(nextpos); free(orders); free(standalone); free(rank);
     free(tgts); free(obj); free(sw); free(ac); free(profit); free(pp); free(sp);
-    free(cand); free(empty);
+    free(cand); free(empty); free(cands);
     return rc;
 }

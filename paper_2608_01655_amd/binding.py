@@ -46,7 +46,9 @@ class pp_stats_f64(ctypes.Structure):
                 ("start_objective", _P), ("start_sweeps", _P),
                 ("start_accepts", _P), ("standalone", _P), ("orders", _P),
                 ("dp_kernel_ms", ctypes.c_double),
-                ("dp_launches", ctypes.c_int32)]
+                ("dp_launches", ctypes.c_int32),
+                ("safeguards_run", ctypes.c_int32),
+                ("safeguard_objective", ctypes.c_double * 3)]
 
 
 class pp_replan_info(ctypes.Structure):
@@ -265,7 +267,10 @@ def _options_f64(m, n_starts, max_rounds, order_seed, orders, flags):
 def _plan_f64_from(st, arrs, target, objective):
     return Plan(target=target, objective=float(objective), best_start=st.best_start,
                 n_starts=st.n_starts, updates=st.updates, dp_cells=st.dp_cells,
-                dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches, **arrs)
+                dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches,
+                safeguards_run=bool(st.safeguards_run),
+                safeguard_objective=tuple(float(x) for x in st.safeguard_objective),
+                **arrs)
 
 
 def pp_plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,

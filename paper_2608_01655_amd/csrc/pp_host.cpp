@@ -857,10 +857,8 @@ int check_values_f64(int32_t n, int32_t m, const double* lam, const double* w,
   return PP_OK;
 }
 
-int check_f64_options(const pp_options& o, double eps) {
+int check_f64_options(double eps) {
   if (!finite_nonneg(eps)) return fail(PP_E_ARG, "epsilon must be finite and >= 0");
-  if (o.flags & PP_F_SAFEGUARDS)
-    return fail(PP_E_UNSUPPORTED, "the comparator safeguards take integer costs");
   return PP_OK;
 }
 
@@ -1014,6 +1012,8 @@ void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
   if (stats->orders) std::copy(r.orders.begin(), r.orders.end(), stats->orders);
   stats->dp_kernel_ms = r.dp_ms;
   stats->dp_launches = r.dp_launches;
+  stats->safeguards_run = r.sg_run ? 1 : 0;
+  for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = bits_f64(r.sg_obj[q]);
 }
 
 template <class F>
@@ -1205,7 +1205,7 @@ int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     if (!cap || !target_dev || !objective) return fail(PP_E_ARG, "null pointer argument");
     const pp_options o = opt ? *opt : default_options();
     PP_TRY(check_options(m, o));
-    PP_TRY(check_f64_options(o, epsilon));
+    PP_TRY(check_f64_options(epsilon));
     for (int32_t h = 0; h < m; ++h)
       if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
     TreeLayout t;
@@ -1246,7 +1246,7 @@ int pp_plan_f64(int32_t n, int32_t m, const int32_t* parent, const double* deman
     if (!cap || !target || !objective) return fail(PP_E_ARG, "null pointer argument");
     const pp_options o = opt ? *opt : default_options();
     PP_TRY(check_options(m, o));
-    PP_TRY(check_f64_options(o, epsilon));
+    PP_TRY(check_f64_options(epsilon));
     for (int32_t h = 0; h < m; ++h)
       if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
     PP_TRY(check_values_f64(n, m, demand, recompute_cost, fetch_cost));

@@ -142,11 +142,17 @@ __device__ double wave_sum_f64(const double* a, int count) {
 
 // ------------------------------------------------------------ helpers ---
 
+// Values into preorder positions.  The bit pattern of -0.0 (INT64_MIN,
+// never a valid integer input) becomes +0.0, so that real-valued inputs
+// compare and order by their bit patterns.
 __global__ void k_gather(const int64_t* __restrict__ src, int64_t* __restrict__ dst,
                          int32_t n, const int32_t* __restrict__ order) {
   const int64_t row = blockIdx.y;
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) dst[row * n + i] = src[row * n + order[i]];
+  if (i < n) {
+    const int64_t v = src[row * n + order[i]];
+    dst[row * n + i] = v == INT64_MIN ? 0 : v;
+  }
 }
 
 __global__ void k_gather_u8(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
@@ -271,6 +277,30 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
   const int64_t n = d.n;
   const int64_t mn = (int64_t)d.m * n;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (gmode != kGainsMarginal && d.f64) {
+    // the comparator profits on doubles, with the integer path's formulas
+    if (i >= n) return;
+    const double L = as_f(d.lam[(int64_t)h * n + i]), Wv = as_f(d.w[(int64_t)h * n + i]);
+    double p;
+    if (gmode == kGainsIndependent) {
+      p = L * Wv;
+    } else if (gmode == kGainsPopularity) {
+      p = L;
+    } else if (d.m == 1) {
+      p = L * Wv;
+    } else {
+      const int src = h == 0 ? 1 : 0;
+      const double F = as_f(d.f[((int64_t)src * d.m + h) * n + i]);
+      bool covered = false;
+      for (int l = 0; l < d.m; ++l)
+        if (l != h && d.tgt[s * mn + (int64_t)l * n + i]) covered = true;
+      const double a = L * (Wv < F ? Wv : F);
+      const double own = L * dpos(Wv - F);
+      p = covered ? a : a + own;
+    }
+    d.profit[s * n + i] = as_i(p);
+    return;
+  }
   if (gmode != kGainsMarginal) {
     if (i >= n) return;
     const int64_t L = d.lam[(int64_t)h * n + i], Wv = d.w[(int64_t)h * n + i];

@@ -207,3 +207,56 @@ def test_tree50k_real_valued_golden():
     rows = [hashlib.sha256(np.ascontiguousarray(target[h]).tobytes()).hexdigest()
             for h in range(inst.m)]
     assert rows == gold["target_row_sha256"]
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_safeguards_f64_random(oracle_mod, seed):
+    """Comparator safeguards on real requester-side costs (one fetch cost
+    per requester and chunk, the same from every source)."""
+    rng = np.random.default_rng(950 + seed)
+    m = int(rng.integers(1, 6))
+    n = int(rng.integers(1, 260))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, n + 2])),
+                             source_dependent=False)
+    lam, w, f = W.real_valued(inst, seed, jitter=0.5)
+    # one factor per requester and chunk keeps the costs requester-side
+    f = np.broadcast_to(f.max(axis=0)[None], f.shape).copy()
+    for i in range(m):
+        f[i, i] = 0.0
+    if seed % 4 == 0 and m > 2:
+        f[1, 2][f[1, 2] == 0.0] = -0.0  # equal as values to +0.0
+    eps = 1e-9 * (float(np.sum(lam * w)) + 1.0)
+    flags = B.PP_F_SAFEGUARDS | (B.PP_F_NO_REFINE if seed % 2 else 0)
+    kw = dict(n_starts=int(rng.integers(1, 4)), max_rounds=int(rng.integers(0, 3)),
+              flags=flags)
+    g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
+    assert o.safeguards_run and g.safeguards_run
+    np.testing.assert_allclose(g.safeguard_objective, o.safeguard_objective,
+                               rtol=1e-12)
+    _same_real(g, o)
+
+
+def test_safeguards_f64_winning_candidates(oracle_mod):
+    """Instances where a comparator beats a single greedy start."""
+    found = 0
+    for seed in range(3000):
+        rng = np.random.default_rng(20000 + seed)
+        m = int(rng.integers(2, 4))
+        inst = W.random_instance(int(rng.integers(3, 12)), m, rng, kmax=5,
+                                 source_dependent=False, value_range=20)
+        lam, w, f = W.real_valued(inst, seed, jitter=0.3)
+        f = np.broadcast_to(f.max(axis=0)[None], f.shape).copy()
+        for i in range(m):
+            f[i, i] = 0.0
+        kw = dict(n_starts=1, flags=B.PP_F_SAFEGUARDS | B.PP_F_NO_REFINE,
+                  epsilon=1e-9)
+        o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+        if o.best_start < 1:
+            continue
+        g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+        _same_real(g, o)
+        found += 1
+        if found == 6:
+            break
+    assert found > 0

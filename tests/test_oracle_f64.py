@@ -247,5 +247,54 @@ def test_invalid_real_inputs_are_rejected():
             oracle.plan_f64(parent, lam, w, f2, cap)
     with pytest.raises(oracle.OracleError):
         oracle.plan_f64(parent, lam, w, f, cap, epsilon=-1.0)
-    with pytest.raises(oracle.OracleError):
-        oracle.plan_f64(parent, lam, w, f, cap, flags=oracle.F_SAFEGUARDS)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_safeguards_on_integer_valued_doubles_match_integer(seed):
+    """Requester-side inputs with the comparator safeguards: the real-valued
+    planner on integer-valued doubles reproduces the integer planner's
+    candidates and choice exactly (all sums exact)."""
+    rng = np.random.default_rng(600 + seed)
+    m = int(rng.integers(1, 5))
+    n = int(rng.integers(1, 80))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 20, n + 2])),
+                             source_dependent=False,
+                             value_range=int(rng.choice([5, 100])))
+    flags = oracle.F_SAFEGUARDS | (oracle.F_NO_REFINE if seed % 2 else 0)
+    a = oracle.plan(inst.parent, inst.demand, inst.recompute_cost,
+                    inst.fetch_cost, inst.cap, n_starts=1, flags=flags)
+    b = oracle.plan_f64(inst.parent, inst.demand.astype(float),
+                        inst.recompute_cost.astype(float),
+                        inst.fetch_cost.astype(float), inst.cap, n_starts=1,
+                        flags=flags)
+    assert a.safeguards_run and b.safeguards_run
+    assert b.safeguard_objective == tuple(float(x) for x in a.safeguard_objective)
+    assert (b.best_start, b.updates, b.dp_cells) == (a.best_start, a.updates, a.dp_cells)
+    assert b.objective == float(a.objective)
+    np.testing.assert_array_equal(b.target, a.target)
+
+
+def test_safeguards_real_values_and_signed_zero():
+    """On real requester-side costs the candidates run, the returned plan is
+    the argmax of the starts and the candidates, and a fetch plane whose
+    sources differ only by the sign of a zero still counts as
+    requester-side."""
+    parent, lam, w, f, cap = real_instance(5, n_max=40, m_max=3,
+                                           source_dependent=False)
+    m = lam.shape[0]
+    f[f == f.min()] = 0.0
+    if m > 2:
+        g = f.copy()
+        g[1, 2][g[1, 2] == 0.0] = -0.0  # -0.0 == 0.0 as values
+        f = g
+    plain = oracle.plan_f64(parent, lam, w, f, cap, n_starts=1)
+    sg = oracle.plan_f64(parent, lam, w, f, cap, n_starts=1,
+                         flags=oracle.F_SAFEGUARDS)
+    assert sg.safeguards_run
+    assert sg.objective == max([plain.objective] + list(sg.safeguard_objective))
+    src = f.copy()
+    if m > 2:
+        src[0, m - 1, 0] += 1.0  # one source differs: not requester-side
+        nd = oracle.plan_f64(parent, lam, w, src, cap, n_starts=1,
+                             flags=oracle.F_SAFEGUARDS)
+        assert not nd.safeguards_run
