@@ -180,3 +180,26 @@ def test_real_valued_validation(L):
     call(flags=B.PP_F_VALIDATE_ONLY | B.PP_F_SAFEGUARDS)  # offered
     _expect(B.PP_E_RANGE, lambda: B.pp_rooted_dp_f64(inst.parent,
                                                      np.full(inst.n, -1.0), 3))
+
+
+def _caterpillar(depth):
+    """Spine 0..depth-1 plus one leaf per spine node; the spine child has the
+    smaller id, so every leaf's row stays pending while the spine below it
+    is swept (one pending skip target per level)."""
+    parent = [-1] + list(range(0, depth - 1)) + list(range(0, depth))
+    return np.array(parent, np.int32)
+
+
+def test_pending_skip_rows_limit(L):
+    for depth, ok in ((250, True), (300, False)):
+        parent = _caterpillar(depth)
+        n = parent.shape[0]
+        lam = np.ones((1, n), np.int64)
+        w = np.ones((1, n), np.int64)
+        f = np.zeros((1, 1, n), np.int64)
+        call = lambda: B.pp_plan(parent, lam, w, f, np.array([5], np.int32),
+                                 n_starts=1, flags=B.PP_F_VALIDATE_ONLY)
+        if ok:
+            call()
+        else:
+            _expect(B.PP_E_UNSUPPORTED, call)

@@ -170,3 +170,30 @@ def test_stall_guard_reports_device_error(monkeypatch):
     p = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost,
                   inst.fetch_cost, inst.cap, n_starts=2)
     assert p.objective == ref.objective
+
+
+def test_plan_maximum_workers(oracle_mod):
+    """255 workers (the maximum): the standalone pass and every update span
+    several launches of at most 64 chains."""
+    rng = np.random.default_rng(255)
+    inst = W.random_instance(30, 255, rng, kmax=6, value_range=50)
+    g, o = _plan_both(oracle_mod, inst, n_starts=2, max_rounds=1)
+    _same(g, o)
+
+
+def test_plan_deep_caterpillar(oracle_mod):
+    """A 250-level spine with a side leaf per level, each pending while the
+    spine below it is swept (250 LDS slots)."""
+    depth = 250
+    parent = np.array([-1] + list(range(0, depth - 1)) + list(range(0, depth)),
+                      np.int32)
+    n = parent.shape[0]
+    rng = np.random.default_rng(9)
+    m = 3
+    lam = rng.integers(0, 20, size=(m, n)).astype(np.int64)
+    w = rng.integers(0, 20, size=(m, n)).astype(np.int64)
+    f = rng.integers(0, 20, size=(m, m, n)).astype(np.int64)
+    cap = np.array([40, 120, n], np.int32)
+    g = B.pp_plan(parent, lam, w, f, cap, n_starts=2, max_rounds=0)
+    o = oracle_mod.plan(parent, lam, w, f, cap, n_starts=2, max_rounds=0)
+    _same(g, o)
