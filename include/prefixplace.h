@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 6
+#define PP_ABI_VERSION 7
 
 enum {
     PP_OK = 0,
@@ -221,6 +221,25 @@ int pp_replan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand
               const int32_t *cap, const uint8_t *incumbent, int64_t horizon,
               const pp_options *opt, uint8_t *target, uint8_t *proposal,
               pp_replan_info *info, pp_stats *stats);
+
+/* pp_replan on real-valued costs: the planner of pp_plan_f64 (tolerance
+ * epsilon), the same rule with a real horizon (finite, >= 0):
+ * adopt iff horizon * (G(T') - G(T)) > cost, evaluated in doubles (the
+ * cost is a sum of doubles in a fixed order; a decision within rounding of
+ * its threshold can differ from another evaluation order).  Errors as
+ * pp_plan_f64 and pp_replan. */
+typedef struct {
+    int32_t adopt;
+    double incumbent_objective;
+    double proposal_objective;
+    double materialization_cost;
+} pp_replan_info_f64;
+
+int pp_replan_f64(int32_t n, int32_t m, const int32_t *parent, const double *demand,
+                  const double *recompute_cost, const double *fetch_cost,
+                  const int32_t *cap, const uint8_t *incumbent, double horizon,
+                  double epsilon, const pp_options *opt, uint8_t *target,
+                  uint8_t *proposal, pp_replan_info_f64 *info, pp_stats_f64 *stats);
 
 /* One exact rooted-tree solve (Eq. 9, Theorem 1) on the GPU.
  *   parent [n] host, profit [n] host (>= 0, sum <= INT64_MAX), k >= 0;

@@ -67,6 +67,8 @@ def lib() -> ctypes.CDLL:
         L.ppo_objective_f64.argtypes = [i32, i32, P, P, P, P, P]
         L.ppo_plan_f64.argtypes = [i32, i32, P, P, P, P, P, f64, i32, i32, u64,
                                    P, u32, P, P, P, P, P, P, P, P, P]
+        L.ppo_replan_f64.argtypes = [i32, i32, P, P, P, P, P, P, f64, f64, i32,
+                                     i32, u64, u32, P, P, P, P]
         L.ppo_candidates.argtypes = [i32, i32, P, P, P, P, P, P, P]
         L.ppo_materialization_cost.argtypes = [i32, i32, P, P, P, P, P]
         L.ppo_replan.argtypes = [i32, i32, P, P, P, P, P, P, i64, i32, i32,
@@ -386,3 +388,39 @@ def plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,
                          updates=int(info[1]), dp_cells=int(info[2]),
                          safeguards_run=bool(info[4]),
                          safeguard_objective=tuple(float(x) for x in sgo))
+
+
+@dataclass
+class ReplanF64Result:
+    target: np.ndarray
+    proposal: np.ndarray
+    adopt: bool
+    incumbent_objective: float
+    proposal_objective: float
+    materialization_cost: float
+
+
+def replan_f64(parent, demand, recompute_cost, fetch_cost, cap, incumbent,
+               horizon, *, epsilon=0.0, n_starts=1, max_rounds=0, order_seed=0,
+               flags=0) -> ReplanF64Result:
+    """Epoch re-planning on real-valued costs (readings R21, R22, R24)."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.float64)
+    w = _c(recompute_cost, np.float64)
+    f = _c(fetch_cost, np.float64)
+    cap = _c(cap, np.int32)
+    inc = _c(incumbent, np.uint8)
+    m, n = demand.shape
+    tgt = np.zeros((m, n), np.uint8)
+    prop = np.zeros((m, n), np.uint8)
+    adopt = np.zeros(1, np.int32)
+    res = np.zeros(3, np.float64)
+    _check(lib().ppo_replan_f64(n, m, _p(parent), _p(demand), _p(w), _p(f),
+                                _p(cap), _p(inc), float(horizon), float(epsilon),
+                                int(n_starts), int(max_rounds),
+                                ctypes.c_uint64(order_seed & (2**64 - 1)),
+                                int(flags), _p(tgt), _p(prop), _p(adopt), _p(res)))
+    return ReplanF64Result(target=tgt, proposal=prop, adopt=bool(adopt[0]),
+                           incumbent_objective=float(res[0]),
+                           proposal_objective=float(res[1]),
+                           materialization_cost=float(res[2]))

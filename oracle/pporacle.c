@@ -1495,3 +1495,72 @@ out:
     free(cand); free(empty); free(cands);
     return rc;
 }
+
+/* R21/R22 on doubles: the one-time cost summed over (m, b) in order, and
+ * adoption iff horizon * (G(T') - G(T)) > cost. */
+static double materialization_cost_f64(int32_t n, int32_t m, const double *w,
+                                       const double *f, const uint8_t *incumbent,
+                                       const uint8_t *proposal)
+{
+    double total = 0.0;
+    for (int32_t r = 0; r < m; r++)
+        for (int32_t b = 0; b < n; b++) {
+            if (!proposal[(size_t)r * n + b] || incumbent[(size_t)r * n + b])
+                continue;
+            double c = w[(size_t)r * n + b];
+            for (int32_t h = 0; h < m; h++)
+                if (h != r && incumbent[(size_t)h * n + b]) {
+                    double fh = f[((size_t)h * m + r) * n + b];
+                    if (fh < c)
+                        c = fh;
+                }
+            total += c;
+        }
+    return total;
+}
+
+/* Epoch re-planning on real-valued costs: arguments as ppo_replan, with
+ * double inputs, a real horizon (finite, >= 0) and the tolerance epsilon of
+ * the planner; result[3] = {G(incumbent), G(proposal), cost}, *adopt. */
+int ppo_replan_f64(int32_t n, int32_t m, const int32_t *parent,
+                   const double *demand, const double *recompute_cost,
+                   const double *fetch_cost, const int32_t *cap,
+                   const uint8_t *incumbent, double horizon, double epsilon,
+                   int32_t n_starts, int32_t max_rounds, uint64_t order_seed,
+                   uint32_t flags, uint8_t *target, uint8_t *proposal,
+                   int32_t *adopt, double *result)
+{
+    if (!incumbent || !target || !result || !adopt || !finite_nonneg(horizon))
+        return PPO_E_ARG;
+    int rc = validate_f64(n, m, parent, demand, recompute_cost, fetch_cost, cap);
+    if (rc != PPO_OK)
+        return rc;
+    for (size_t x = 0; x < (size_t)m * n; x++)
+        if (incumbent[x] > 1)
+            return PPO_E_ARG;
+    uint8_t *prop = malloc((size_t)m * n);
+    if (!prop)
+        return PPO_E_NOMEM;
+    double g_new;
+    rc = ppo_plan_f64(n, m, parent, demand, recompute_cost, fetch_cost, cap,
+                      epsilon, n_starts, max_rounds, order_seed, NULL, flags,
+                      prop, &g_new, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
+    if (rc != PPO_OK) {
+        free(prop);
+        return rc;
+    }
+    double g_inc = objective_f64(n, m, demand, recompute_cost, fetch_cost,
+                                 incumbent);
+    double cost = materialization_cost_f64(n, m, recompute_cost, fetch_cost,
+                                           incumbent, prop);
+    int a = horizon * (g_new - g_inc) > cost;
+    memcpy(target, a ? prop : incumbent, (size_t)m * n);
+    if (proposal)
+        memcpy(proposal, prop, (size_t)m * n);
+    *adopt = a;
+    result[0] = g_inc;
+    result[1] = g_new;
+    result[2] = cost;
+    free(prop);
+    return PPO_OK;
+}

@@ -57,6 +57,12 @@ class pp_replan_info(ctypes.Structure):
                 ("materialization_cost", ctypes.c_int64)]
 
 
+class pp_replan_info_f64(ctypes.Structure):
+    _fields_ = [("adopt", ctypes.c_int32), ("incumbent_objective", ctypes.c_double),
+                ("proposal_objective", ctypes.c_double),
+                ("materialization_cost", ctypes.c_double)]
+
+
 class PPError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"prefixplace error {code}: {msg}")
@@ -96,6 +102,8 @@ def lib() -> ctypes.CDLL:
         L.pp_plan_f64_device.argtypes = [_P, i32, i32, _P, _P, _P, _P, _P, f64, _P,
                                          _P, _P, _P, _P]
         L.pp_rooted_dp_f64.argtypes = [i32, _P, _P, i32, _P, _P]
+        L.pp_replan_f64.argtypes = [i32, i32, _P, _P, _P, _P, _P, _P, f64, f64,
+                                    _P, _P, _P, _P, _P]
         L.pp_rooted_dp.argtypes = [i32, _P, _P, i32, _P, _P]
         L.pp_marginal.argtypes = [i32, i32, _P, _P, _P, _P, i32, _P, _P]
         L.pp_objective.argtypes = [i32, i32, _P, _P, _P, _P, _P]
@@ -107,7 +115,8 @@ def lib() -> ctypes.CDLL:
         L.pp_ctx_destroy.restype = None
         L.pp_plan_device.argtypes = [_P, i32, i32, _P, _P, _P, _P, _P, _P, _P,
                                      _P, _P, _P]
-        for f in (L.pp_plan, L.pp_replan, L.pp_plan_f64, L.pp_plan_f64_device,
+        for f in (L.pp_plan, L.pp_replan, L.pp_replan_f64, L.pp_plan_f64,
+                  L.pp_plan_f64_device,
                   L.pp_rooted_dp_f64, L.pp_rooted_dp, L.pp_marginal, L.pp_objective,
                   L.pp_orders, L.pp_ctx_create, L.pp_plan_device):
             f.restype = ctypes.c_int
@@ -292,6 +301,37 @@ def pp_plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,
                              ctypes.byref(obj), ctypes.byref(st)))
     del keep
     return _plan_f64_from(st, arrs, tgt, obj.value)
+
+
+def pp_replan_f64(parent, demand, recompute_cost, fetch_cost, cap, incumbent,
+                  horizon, *, epsilon=0.0, n_starts=8, max_rounds=0, order_seed=0,
+                  orders=None, flags=0) -> Replan:
+    """Real-valued epoch re-planning (see pp_replan_f64 in
+    include/prefixplace.h)."""
+    parent = _c(parent, np.int32)
+    demand = _c(demand, np.float64)
+    w = _c(recompute_cost, np.float64)
+    f = _c(fetch_cost, np.float64)
+    cap = _c(cap, np.int32)
+    inc = _c(incumbent, np.uint8)
+    m, n = demand.shape
+    if inc.shape != (m, n):
+        raise ValueError(f"incumbent shape {inc.shape} != {(m, n)}")
+    o, st, arrs, keep = _options_f64(m, n_starts, max_rounds, order_seed, orders,
+                                     flags)
+    tgt = np.zeros((m, n), np.uint8)
+    prop = np.zeros((m, n), np.uint8)
+    info = pp_replan_info_f64()
+    _check(lib().pp_replan_f64(n, m, _p(parent), _p(demand), _p(w), _p(f),
+                               _p(cap), _p(inc), float(horizon), float(epsilon),
+                               ctypes.byref(o), _p(tgt), _p(prop),
+                               ctypes.byref(info), ctypes.byref(st)))
+    del keep
+    return Replan(target=tgt, proposal=prop, adopt=bool(info.adopt),
+                  incumbent_objective=float(info.incumbent_objective),
+                  proposal_objective=float(info.proposal_objective),
+                  materialization_cost=float(info.materialization_cost),
+                  plan=_plan_f64_from(st, arrs, prop, info.proposal_objective))
 
 
 def pp_rooted_dp_f64(parent, profit, k):

@@ -1464,6 +1464,105 @@ static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v
   });
 }
 
+int pp_replan_f64(int32_t n, int32_t m, const int32_t* parent, const double* demand,
+                  const double* recompute_cost, const double* fetch_cost,
+                  const int32_t* cap, const uint8_t* incumbent, double horizon,
+                  double epsilon, const pp_options* opt, uint8_t* target,
+                  uint8_t* proposal, pp_replan_info_f64* info, pp_stats_f64* stats) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
+    if (!cap || !incumbent || !target || !info)
+      return fail(PP_E_ARG, "null pointer argument");
+    if (!finite_nonneg(horizon)) return fail(PP_E_ARG, "horizon must be finite and >= 0");
+    const pp_options o = opt ? *opt : default_options();
+    PP_TRY(check_options(m, o));
+    PP_TRY(check_f64_options(epsilon));
+    for (int32_t h = 0; h < m; ++h)
+      if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
+    const size_t mn = (size_t)m * n;
+    for (size_t x = 0; x < mn; ++x)
+      if (incumbent[x] > 1) return fail(PP_E_ARG, "incumbent entries must be 0 or 1");
+    PP_TRY(check_values_f64(n, m, demand, recompute_cost, fetch_cost));
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    int rc = PP_OK;
+    pp_ctx* c = thread_ctx(rc);
+    if (!c) return rc;
+    hipStream_t st = c->own;
+    PP_TRY(c->up_lam.ensure(mn * 8));
+    PP_TRY(c->up_w.ensure(mn * 8));
+    PP_TRY(c->up_f.ensure(mn * m * 8));
+    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
+    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
+    PP_TRY(upload_tree(c, t, st));
+    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
+                         c->up_f.as<int64_t>(), st));
+    PlanResult r;
+    PP_TRY(run_plan(c, t, m, cap, o, false, st, r, 1, true, epsilon));
+    DevState d{};
+    d.n = n;
+    d.m = m;
+    d.npad = npad_of(n);
+    d.lam = c->lam.as<int64_t>();
+    d.w = c->w.as<int64_t>();
+    d.f = c->f.as<int64_t>();
+    d.tgt = c->tgt.as<uint8_t>();
+    d.v1 = c->v1.as<int64_t>();
+    d.v2 = c->v2.as<int64_t>();
+    d.h1 = c->h1.as<uint8_t>();
+    d.cs = c->cs.as<ChainState>();
+    d.f64 = 1;
+    d.eps = epsilon;
+    d.fpart_stride = fpart_blocks(n, m);
+    d.fpart = c->fpart.as<double>();
+    const int32_t xs = r.extra_slot;
+    std::vector<uint8_t> pre(mn);
+    for (int32_t h = 0; h < m; ++h)
+      for (int32_t q = 0; q < n; ++q)
+        pre[(size_t)h * n + q] = incumbent[(size_t)h * n + t.order[q]];
+    PP_HIP(hipMemcpyAsync(d.tgt + (size_t)xs * mn, pre.data(), mn,
+                          hipMemcpyHostToDevice, st));
+    const std::vector<int32_t> one = {xs}, zero = {0};
+    const ChainSet inc_set = chain_set(one, zero, zero, 0, 1);
+    PP_HIP(launch_init_slots(inc_set, d, 0, st));
+    PP_HIP(launch_holder_build(inc_set, d, st));
+    PP_HIP(launch_objective(inc_set, d, st));
+    PP_TRY(c->partial.ensure(1024 * 16));
+    int32_t nb = 0;
+    PP_HIP(launch_mat_cost(d, xs, r.win_slot, c->partial.p, &nb, st));
+    std::vector<double> part(nb);
+    ChainState inc_cs{};
+    PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, 8 * (size_t)nb,
+                          hipMemcpyDeviceToHost, st));
+    PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState),
+                          hipMemcpyDeviceToHost, st));
+    std::vector<uint8_t> prop_pre(mn);
+    PP_HIP(hipMemcpyAsync(prop_pre.data(), d.tgt + (size_t)r.win_slot * mn, mn,
+                          hipMemcpyDeviceToHost, st));
+    PP_HIP(hipStreamSynchronize(st));
+    double cost = 0.0;
+    for (double v : part) cost += v;
+    const double g_inc = bits_f64(inc_cs.obj), g_new = bits_f64(r.win_obj);
+    const bool adopt = horizon * (g_new - g_inc) > cost;
+    for (int32_t h = 0; h < m; ++h)
+      for (int32_t q = 0; q < n; ++q) {
+        const size_t id = (size_t)h * n + t.order[q];
+        const uint8_t v = prop_pre[(size_t)h * n + q];
+        if (proposal) proposal[id] = v;
+        target[id] = adopt ? v : incumbent[id];
+      }
+    info->adopt = adopt ? 1 : 0;
+    info->incumbent_objective = g_inc;
+    info->proposal_objective = g_new;
+    info->materialization_cost = cost;
+    fill_stats_f64(stats, r);
+    return PP_OK;
+  });
+}
+
 int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
                  int32_t k, uint8_t* selected, int64_t* value) {
   return rooted_dp_impl(n, parent, profit, k, selected, value, false);

@@ -1443,6 +1443,27 @@ __global__ void __launch_bounds__(256) k_mat_cost(DevState d, int64_t inc, int64
   const int64_t n = d.n, mn = (int64_t)d.m * n;
   const uint8_t* ti = d.tgt + inc * mn;
   const uint8_t* tp = d.tgt + prop * mn;
+  if (d.f64) {
+    // the same minimum on bit patterns (non-negative doubles order like
+    // them); per-block sums of doubles in a fixed order
+    double a = 0.0;
+    for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+         x += (int64_t)gridDim.x * blockDim.x) {
+      if (!tp[x] || ti[x]) continue;
+      const int r = (int)(x / n);
+      const int64_t i = x % n;
+      int64_t c = d.w[x];
+      for (int h = 0; h < d.m; ++h)
+        if (h != r && ti[(int64_t)h * n + i]) {
+          const int64_t fh = d.f[((int64_t)h * d.m + r) * n + i];
+          if (fh < c) c = fh;
+        }
+      a += as_f(c);
+    }
+    const double t = block_sum_f64(a);
+    if (threadIdx.x == 0) ((double*)partial)[blockIdx.x] = t;
+    return;
+  }
   unsigned __int128 acc = 0;
   for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
        x += (int64_t)gridDim.x * blockDim.x) {

@@ -147,3 +147,50 @@ def test_replan_tree50k_golden():
             for h in range(inst.m)]
     assert rows == gold["proposal_row_sha256"]
     np.testing.assert_array_equal(g.target, g.proposal if g.adopt else inc)
+
+
+# ---------------------------------------------------------- real-valued costs
+
+def _same_f64(g, o):
+    assert g.adopt == o.adopt
+    assert g.incumbent_objective == pytest.approx(o.incumbent_objective, rel=1e-12)
+    assert g.proposal_objective == pytest.approx(o.proposal_objective, rel=1e-12)
+    assert g.materialization_cost == pytest.approx(o.materialization_cost,
+                                                   rel=1e-12, abs=0.0)
+    np.testing.assert_array_equal(g.proposal, o.proposal)
+    np.testing.assert_array_equal(g.target, o.target)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_replan_f64_random(oracle_mod, seed):
+    rng = np.random.default_rng(1700 + seed)
+    m = int(rng.integers(1, 6))
+    n = int(rng.integers(1, 260))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, n + 2])),
+                             source_dependent=bool(seed % 3))
+    lam, w, f = W.real_valued(inst, seed, jitter=0.5)
+    inc = (rng.random((m, n)) < rng.choice([0.0, 0.1, 0.5, 1.0])).astype(np.uint8)
+    horizon = float(rng.choice([0.0, 0.37, 7.0, 1e6]))
+    eps = 1e-9 * (float(np.sum(lam * w)) + 1.0)
+    kw = dict(epsilon=eps, n_starts=int(rng.integers(1, 4)),
+              max_rounds=int(rng.integers(0, 3)),
+              order_seed=int(rng.integers(0, 2 ** 62)))
+    g = B.pp_replan_f64(inst.parent, lam, w, f, inst.cap, inc, horizon, **kw)
+    o = oracle_mod.replan_f64(inst.parent, lam, w, f, inst.cap, inc, horizon, **kw)
+    _same_f64(g, o)
+
+
+def test_replan_f64_tree2k_routing_shift(oracle_mod):
+    inst = W.make_workload("tree2k")
+    lam, w, f = W.real_valued(inst, 4)
+    eps = 1e-9 * float(np.sum(lam * w))
+    kw = dict(epsilon=eps, n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+              order_seed=inst.order_seed)
+    old = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+    shifted = np.roll(lam, 1, axis=0)  # every request routed to the next worker
+    for horizon in (0.5, 100.0, 1e6):
+        g = B.pp_replan_f64(inst.parent, shifted, w, f, inst.cap, old.target,
+                            horizon, **kw)
+        o = oracle_mod.replan_f64(inst.parent, shifted, w, f, inst.cap, old.target,
+                                  horizon, **kw)
+        _same_f64(g, o)

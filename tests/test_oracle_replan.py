@@ -10,6 +10,8 @@ that already holds the chunk), and the decision (reading R22) is re-derived
 with Python integers.
 """
 
+import math
+
 import numpy as np
 import pytest
 
@@ -170,3 +172,49 @@ def test_non_binary_incumbent_is_rejected():
     with pytest.raises(oracle.OracleError):
         oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
                       inst.fetch_cost, inst.cap, inc, 1)
+
+
+# --------------------------------------------------------- real-valued costs
+
+@pytest.mark.parametrize("seed", range(20))
+def test_f64_replan_on_integer_values_matches_integer(seed):
+    """Integer-valued doubles: every sum is exact, so the real-valued rule
+    reproduces the integer one."""
+    inst, inc, rng = random_case(300 + seed)
+    H = int(rng.choice([0, 1, 3, 50]))
+    a = oracle.replan(inst.parent, inst.demand, inst.recompute_cost,
+                      inst.fetch_cost, inst.cap, inc, H, n_starts=2, max_rounds=1)
+    b = oracle.replan_f64(inst.parent, inst.demand.astype(float),
+                          inst.recompute_cost.astype(float),
+                          inst.fetch_cost.astype(float), inst.cap, inc, float(H),
+                          n_starts=2, max_rounds=1)
+    assert b.adopt == a.adopt
+    assert (b.incumbent_objective, b.proposal_objective, b.materialization_cost) == \
+        (float(a.incumbent_objective), float(a.proposal_objective),
+         float(a.materialization_cost))
+    np.testing.assert_array_equal(b.target, a.target)
+    np.testing.assert_array_equal(b.proposal, a.proposal)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_f64_replan_definition_on_reals(seed):
+    inst, inc, rng = random_case(400 + seed)
+    lam, w, f = W.real_valued(inst, seed, jitter=0.5)
+    H = float(rng.choice([0.0, 0.5, 3.0, 1e6]))
+    r = oracle.replan_f64(inst.parent, lam, w, f, inst.cap, inc, H, epsilon=1e-9,
+                          n_starts=2, max_rounds=1)
+    plan = oracle.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=1e-9,
+                           n_starts=2, max_rounds=1)
+    np.testing.assert_array_equal(r.proposal, plan.target)
+    assert r.proposal_objective == plan.objective
+    assert r.incumbent_objective == oracle.objective_f64(lam, w, f, inc)
+    m, n = w.shape
+    terms = [min([float(w[q][b])] + [float(f[h][q][b]) for h in range(m)
+                                     if h != q and inc[h][b]])
+             for q in range(m) for b in range(n)
+             if plan.target[q][b] and not inc[q][b]]
+    want = math.fsum(terms)
+    assert r.materialization_cost == pytest.approx(want, rel=1e-12, abs=0.0)
+    assert r.adopt == (H * (r.proposal_objective - r.incumbent_objective) >
+                       r.materialization_cost)
+    np.testing.assert_array_equal(r.target, plan.target if r.adopt else inc)
