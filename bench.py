@@ -218,7 +218,8 @@ def f64_leg(B, W, inst, ctx, steps, warmup):
     out = {"plans_per_s": 1.0 / dt, "ms_per_plan": dt * 1e3,
            "dp_avg_launch_ms": dp_ms / launches,
            "dp_launches_per_plan": launches // steps,
-           "dp_cells_per_s_in_kernel": p.dp_cells * steps / (dp_ms / 1e3),
+           "dp_cells_per_s_in_kernel":
+               sum(q.dp_cells_executed for q in plans) / (dp_ms / 1e3),
            "objective": p.objective, "epsilon": eps,
            "sweeps_per_start": p.start_sweeps.tolist(),
            "units": "requests/epoch and ms, per-entry jitter U[0.75, 1.25]"}
@@ -382,9 +383,12 @@ def main():
     cells = p.dp_cells
     plans_per_s = args.steps / dt
     cells_per_s = cells * args.steps / dt
+    # cells the sweeps actually processed (refinement updates of workers
+    # whose inputs did not change are resolved without a sweep)
+    exec_cells = sum(q.dp_cells_executed for q in plans)
     dp_ms = sum(q.dp_kernel_ms for q in plans)
     launches = sum(q.dp_launches for q in plans)
-    bytes_per_launch = cells * args.steps * BYTES_PER_CELL / launches
+    bytes_per_launch = exec_cells * BYTES_PER_CELL / launches
     avg_launch_s = dp_ms / launches / 1e3
     achieved = bytes_per_launch / avg_launch_s / 1e9
     traffic = measured_traffic(inst.name)
@@ -393,8 +397,12 @@ def main():
         "value": plans_per_s,
         "unit": "plans/s",
         "dp_cells_per_s": cells_per_s,
-        "dp_cells_per_s_frac_hbm_roofline": cells_per_s * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
-        "plans_per_s_frac_hbm_roofline": cells_per_s * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
+        "dp_cells_executed_per_s": exec_cells / dt,
+        # model fraction on the cells actually swept
+        "dp_cells_per_s_frac_hbm_roofline":
+            exec_cells / dt * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
+        "plans_per_s_frac_hbm_roofline":
+            exec_cells / dt * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -411,6 +419,7 @@ def main():
             "k": [int(x) for x in sorted(set(inst.cap.tolist()))],
             "starts": inst.n_starts, "max_rounds": inst.max_rounds,
             "updates_per_plan": p.updates, "dp_cells_per_plan": cells,
+            "dp_cells_executed_per_plan": exec_cells // args.steps,
             "sweeps_per_start": p.start_sweeps.tolist(),
         },
         "roofline": {
@@ -427,7 +436,7 @@ def main():
             "bytes_per_cell": BYTES_PER_CELL,
             "dp_launches_per_plan": launches // args.steps,
             "avg_launch_ms": avg_launch_s * 1e3,
-            "dp_cells_per_s_in_kernel": cells * args.steps / (dp_ms / 1e3),
+            "dp_cells_per_s_in_kernel": exec_cells / (dp_ms / 1e3),
             "dp_share_of_plan_time": dp_ms / 1e3 / dt,
         },
         "parity_vs_golden": gold_ok,

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 7
+#define PP_ABI_VERSION 8
 
 enum {
     PP_OK = 0,
@@ -106,8 +106,8 @@ typedef struct {
                                   (0 Independent, 1 Popularity, 2 LocalDedup)
                                   is returned */
     int32_t n_starts;          /* out: number of starts run */
-    int64_t updates;           /* out: worker updates executed (standalone +
-                                  greedy + every sweep) */
+    int64_t updates;           /* out: worker updates of Algorithm 1
+                                  (standalone + greedy + every sweep) */
     int64_t dp_cells;          /* out: sum over updates of n * min(k_h, n) */
     int64_t *start_objective;  /* out [S]: objective of each start */
     int32_t *start_sweeps;     /* out [S]: refinement sweeps per start */
@@ -121,6 +121,13 @@ typedef struct {
                                   evaluated (requester-side costs) */
     int64_t safeguard_objective[3]; /* out: their objectives (Independent,
                                   Popularity, LocalDedup), 0 if not run */
+    int64_t dp_cells_executed; /* out: DP cells actually swept.  A refinement
+                                  update of a worker whose inputs have not
+                                  changed since its last sweep (no other
+                                  worker's set changed) would find the same
+                                  set and reject it; it is resolved as
+                                  rejected without a sweep, so this can be
+                                  below dp_cells.  Results are unaffected. */
 } pp_stats;
 
 /* Number of starts the options select (see pp_options.n_starts). */
@@ -178,6 +185,7 @@ typedef struct {
     int32_t dp_launches;
     int32_t safeguards_run;
     double safeguard_objective[3];
+    int64_t dp_cells_executed;   /* as in pp_stats */
 } pp_stats_f64;
 
 /* pp_plan on real-valued host arrays (layouts as pp_plan). */

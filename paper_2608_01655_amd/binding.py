@@ -37,7 +37,8 @@ class pp_stats(ctypes.Structure):
                 ("dp_kernel_ms", ctypes.c_double),
                 ("dp_launches", ctypes.c_int32),
                 ("safeguards_run", ctypes.c_int32),
-                ("safeguard_objective", ctypes.c_int64 * 3)]
+                ("safeguard_objective", ctypes.c_int64 * 3),
+                ("dp_cells_executed", ctypes.c_int64)]
 
 
 class pp_stats_f64(ctypes.Structure):
@@ -48,7 +49,8 @@ class pp_stats_f64(ctypes.Structure):
                 ("dp_kernel_ms", ctypes.c_double),
                 ("dp_launches", ctypes.c_int32),
                 ("safeguards_run", ctypes.c_int32),
-                ("safeguard_objective", ctypes.c_double * 3)]
+                ("safeguard_objective", ctypes.c_double * 3),
+                ("dp_cells_executed", ctypes.c_int64)]
 
 
 class pp_replan_info(ctypes.Structure):
@@ -166,6 +168,7 @@ class Plan:
     dp_launches: int
     safeguards_run: bool = False
     safeguard_objective: tuple = (0, 0, 0)
+    dp_cells_executed: int = 0
 
 
 def _options(m, n_starts, max_rounds, order_seed, orders, flags):
@@ -196,7 +199,7 @@ def _plan_from(st, arrs, target, objective):
                 dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches,
                 safeguards_run=bool(st.safeguards_run),
                 safeguard_objective=tuple(int(x) for x in st.safeguard_objective),
-                **arrs)
+                dp_cells_executed=st.dp_cells_executed, **arrs)
 
 
 def pp_plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=8,
@@ -279,7 +282,7 @@ def _plan_f64_from(st, arrs, target, objective):
                 dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches,
                 safeguards_run=bool(st.safeguards_run),
                 safeguard_objective=tuple(float(x) for x in st.safeguard_objective),
-                **arrs)
+                dp_cells_executed=st.dp_cells_executed, **arrs)
 
 
 def pp_plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,

@@ -450,7 +450,7 @@ struct Engine {
   // every chain of `set`.
   int update(const ChainSet& set, int mode) {
     if (set.count == 0) return PP_OK;
-    PP_HIP(launch_gains(set, d, st));
+    PP_HIP(launch_gains(set, d, st, kGainsMarginal, mode == kModeRefine ? 1 : 0));
     PP_TRY(dp(set, 1));
     PP_HIP(launch_backtrack(set, d, mode, st));
     PP_HIP(launch_commit(set, d, mode, st));
@@ -503,6 +503,7 @@ struct PlanResult {
   bool sg_run = false;         // safeguard candidates evaluated
   int64_t sg_obj[3] = {0, 0, 0};
   int32_t extra_slot = -1;     // first slot reserved for the caller
+  int64_t skipped_cells = 0;   // cells of updates resolved without a sweep
   int64_t updates = 0, cells = 0;
   double dp_ms = 0.0;
   int32_t dp_launches = 0;
@@ -775,6 +776,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
       if (fin[s - lo].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
       res.start_obj[s] = fin[s - lo].obj;
       res.accepts[s] = fin[s - lo].accepts;
+      res.skipped_cells += fin[s - lo].skipped_cells;
     }
   }
   res.best = 0;
@@ -984,6 +986,7 @@ void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
   stats->dp_launches = r.dp_launches;
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = r.sg_obj[q];
+  stats->dp_cells_executed = r.cells - r.skipped_cells;
   (void)m;
 }
 
@@ -1014,6 +1017,7 @@ void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
   stats->dp_launches = r.dp_launches;
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = bits_f64(r.sg_obj[q]);
+  stats->dp_cells_executed = r.cells - r.skipped_cells;
 }
 
 template <class F>

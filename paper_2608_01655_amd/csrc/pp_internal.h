@@ -65,6 +65,15 @@ struct ChainState {
   int32_t status;    // nonzero: a device-side wait gave up
   int32_t changed;   // real-valued refinement: the accepted selection
                      // differs from the incumbent set (counted once)
+  // Refinement updates whose inputs are unchanged: bit h of dirty is set
+  // when another worker's set changes and cleared when worker h's DP runs.
+  // A refinement update of a clean worker would rebuild the same profits,
+  // find the same set and reject it, so it is resolved as rejected without
+  // the sweep (skip = 1 for the current update).
+  int32_t skip;
+  int32_t skips;           // updates resolved that way
+  int64_t skipped_cells;   // their n * k' DP cells
+  uint32_t dirty[8];       // one bit per worker (m <= 255)
 };
 
 // The chains of one launch, passed by value as a kernel argument.
@@ -137,8 +146,10 @@ hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
                              int clear_tgt, hipStream_t st);
 hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
                                hipStream_t st);
+// may_skip: refinement updates, which resolve a clean worker's update
+// without a sweep (see ChainState::dirty)
 hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st,
-                        int gmode = kGainsMarginal);
+                        int gmode = kGainsMarginal, int may_skip = 0);
 hipError_t launch_assemble(const ChainSet& set, const DevState& d, int32_t dst,
                            hipStream_t st);
 hipError_t launch_requester_check(const int64_t* f, int32_t n, int32_t m,

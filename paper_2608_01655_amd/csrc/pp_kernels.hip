@@ -270,13 +270,28 @@ __global__ void k_holder_build(ChainSet set, DevState d) {
 // LocalDedup p = a_h(b) + 1{b not held by another worker} Lambda_h
 // [w_h - f_h]_+ (a_h = Lambda_h min(w_h, f_h), Eq. 2; f_h the common fetch
 // cost of requester h; with one worker p = Lambda_h w_h).
-__global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmode) {
+__global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmode,
+                                               int may_skip) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
   const int h = set.worker[ci];
   const int64_t n = d.n;
   const int64_t mn = (int64_t)d.m * n;
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  {
+    // a refinement update of a worker whose inputs have not changed since
+    // its last sweep: resolved as rejected, no gains, sweep or walk
+    const bool clean = may_skip && gmode == kGainsMarginal &&
+                       ((d.cs[s].dirty[h >> 5] >> (h & 31)) & 1u) == 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      d.cs[s].skip = clean ? 1 : 0;
+      if (clean) {
+        d.cs[s].skips += 1;
+        d.cs[s].skipped_cells += n * set.kprime[ci];
+      }
+    }
+    if (clean) return;
+  }
   if (gmode != kGainsMarginal && d.f64) {
     // the comparator profits on doubles, with the integer path's formulas
     if (i >= n) return;
@@ -580,6 +595,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   int ci = 0;
   while (ci + 1 < set.count && set.base[ci + 1] <= blk) ++ci;
   const int64_t slot = set.slot[ci];
+  if (d.cs[slot].skip) return;  // the update is resolved without a sweep
   const int kp = set.kprime[ci];
   const int g = blk - set.base[ci];
   const int G = set.base[ci + 1] - set.base[ci];
@@ -1185,6 +1201,17 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   const int kp = set.kprime[ci];
   const int n = d.n;
   ChainState* st = d.cs + slot;
+  if (st->skip) {
+    if (lane == 0) {
+      st->accept = 0;
+      st->inc = 0;
+    }
+    return;
+  }
+  if (lane == 0) {  // worker h's DP ran: its inputs are current again
+    const int h = set.worker[ci];
+    st->dirty[h >> 5] &= ~(1u << (h & 31));
+  }
   const int64_t dpval = st->dpval;
   bool accept;
   if (d.f64) {
@@ -1367,6 +1394,12 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
     changed = nv != th[i];
   }
   if (!__syncthreads_or(changed)) return;
+  if (threadIdx.x == 0) {
+    // every other worker's marginals change with worker h's set
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      atomicOr(&d.cs[s].dirty[q], q == (h >> 5) ? ~(1u << (h & 31)) : ~0u);
+  }
   if (d.f64 && mode == kModeRefine && threadIdx.x == 0 &&
       atomicExch(&d.cs[s].changed, 1) == 0) {
     // the first block that sees a change counts the replacement
@@ -1616,9 +1649,9 @@ hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
 }
 
 hipError_t launch_gains(const ChainSet& set, const DevState& d, hipStream_t st,
-                        int gmode) {
+                        int gmode, int may_skip) {
   hipLaunchKernelGGL(k_gains, grid1(d.n, 256, set.count), dim3(256), 0, st,
-                     set, d, gmode);
+                     set, d, gmode, may_skip);
   return hipGetLastError();
 }
 

@@ -197,3 +197,16 @@ def test_plan_deep_caterpillar(oracle_mod):
     g = B.pp_plan(parent, lam, w, f, cap, n_starts=2, max_rounds=0)
     o = oracle_mod.plan(parent, lam, w, f, cap, n_starts=2, max_rounds=0)
     _same(g, o)
+
+
+def test_unchanged_workers_skip_their_sweep(oracle_mod):
+    """Refinement updates of workers whose inputs have not changed are
+    resolved without a sweep: fewer cells swept, identical plan."""
+    inst = W.make_workload("tree2k")
+    g, o = _plan_both(oracle_mod, inst)
+    _same(g, o)
+    assert g.dp_cells_executed < g.dp_cells
+    nr = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                   inst.cap, n_starts=inst.n_starts, order_seed=inst.order_seed,
+                   flags=B.PP_F_NO_REFINE)
+    assert nr.dp_cells_executed == nr.dp_cells
