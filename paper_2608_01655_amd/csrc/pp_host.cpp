@@ -1020,6 +1020,116 @@ void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
   stats->dp_cells_executed = r.cells - r.skipped_cells;
 }
 
+// Host-array inputs (caller ids, 8-byte values) to the context's preorder
+// layout: upload, tree tables, gather.
+int upload_host_inputs(pp_ctx* c, const TreeLayout& t, int32_t m, const void* demand,
+                       const void* recompute_cost, const void* fetch_cost,
+                       hipStream_t st) {
+  const size_t mn = (size_t)m * t.n;
+  PP_TRY(c->up_lam.ensure(mn * 8));
+  PP_TRY(c->up_w.ensure(mn * 8));
+  PP_TRY(c->up_f.ensure(mn * m * 8));
+  PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
+  PP_TRY(upload_tree(c, t, st));
+  return layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
+                       c->up_f.as<int64_t>(), st);
+}
+
+// Slot `slot`'s placement (preorder) to host memory in caller ids.
+int placement_to_host(pp_ctx* c, const TreeLayout& t, int32_t m, int32_t slot,
+                      uint8_t* out, hipStream_t st) {
+  const size_t n = (size_t)t.n, mn = (size_t)m * n;
+  std::vector<uint8_t> pre(mn);
+  PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)slot * mn, mn,
+                        hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  for (int32_t h = 0; h < m; ++h)
+    for (size_t q = 0; q < n; ++q) out[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
+  return PP_OK;
+}
+
+// Re-planning, after run_plan with one spare slot: the incumbent (caller
+// ids) into that slot, its objective under the refreshed inputs (Eq. 6) and
+// the one-time cost of the proposal's new (worker, chunk) pairs, summed
+// exactly (integers) or in a fixed order (doubles).
+struct ReplanEval {
+  int64_t g_inc = 0;              // objective bits
+  unsigned __int128 cost = 0;     // integer costs
+  double cost_f64 = 0.0;          // real-valued costs
+};
+
+int replan_evaluate(pp_ctx* c, const TreeLayout& t, int32_t m, const PlanResult& r,
+                    const uint8_t* incumbent, bool f64, double eps, hipStream_t st,
+                    ReplanEval& ev) {
+  const int32_t n = t.n;
+  const size_t mn = (size_t)m * n;
+  DevState d{};
+  d.n = n;
+  d.m = m;
+  d.npad = npad_of(n);
+  d.lam = c->lam.as<int64_t>();
+  d.w = c->w.as<int64_t>();
+  d.f = c->f.as<int64_t>();
+  d.tgt = c->tgt.as<uint8_t>();
+  d.v1 = c->v1.as<int64_t>();
+  d.v2 = c->v2.as<int64_t>();
+  d.h1 = c->h1.as<uint8_t>();
+  d.cs = c->cs.as<ChainState>();
+  if (f64) {
+    d.f64 = 1;
+    d.eps = eps;
+    d.fpart_stride = fpart_blocks(n, m);
+    d.fpart = c->fpart.as<double>();
+  }
+  const int32_t xs = r.extra_slot;
+  std::vector<uint8_t> pre(mn);
+  for (int32_t h = 0; h < m; ++h)
+    for (int32_t q = 0; q < n; ++q)
+      pre[(size_t)h * n + q] = incumbent[(size_t)h * n + t.order[q]];
+  PP_HIP(hipMemcpyAsync(d.tgt + (size_t)xs * mn, pre.data(), mn,
+                        hipMemcpyHostToDevice, st));
+  const std::vector<int32_t> one = {xs}, zero = {0};
+  const ChainSet inc_set = chain_set(one, zero, zero, 0, 1);
+  PP_HIP(launch_init_slots(inc_set, d, 0, st));
+  PP_HIP(launch_holder_build(inc_set, d, st));
+  PP_HIP(launch_objective(inc_set, d, st));
+  PP_TRY(c->partial.ensure(1024 * 16));
+  int32_t nb = 0;
+  PP_HIP(launch_mat_cost(d, xs, r.win_slot, c->partial.p, &nb, st));
+  std::vector<unsigned char> part((size_t)nb * 16);
+  ChainState inc_cs{};
+  PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, part.size(), hipMemcpyDeviceToHost, st));
+  PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState), hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
+  ev.g_inc = inc_cs.obj;
+  for (int32_t b = 0; b < nb; ++b) {
+    if (f64) {
+      double v;
+      std::memcpy(&v, part.data() + 8 * (size_t)b, 8);
+      ev.cost_f64 += v;
+    } else {
+      unsigned __int128 v;
+      std::memcpy(&v, part.data() + 16 * (size_t)b, 16);
+      ev.cost += v;
+    }
+  }
+  return PP_OK;
+}
+
+// target := proposal if adopted, else the incumbent; proposal optional.
+int replan_outputs(pp_ctx* c, const TreeLayout& t, int32_t m, const PlanResult& r,
+                   const uint8_t* incumbent, bool adopt, uint8_t* target,
+                   uint8_t* proposal, hipStream_t st) {
+  const size_t mn = (size_t)m * t.n;
+  std::vector<uint8_t> prop(mn);
+  PP_TRY(placement_to_host(c, t, m, r.win_slot, prop.data(), st));
+  if (proposal) std::memcpy(proposal, prop.data(), mn);
+  std::memcpy(target, adopt ? prop.data() : incumbent, mn);
+  return PP_OK;
+}
+
 template <class F>
 int guarded(F&& fn) {
   try {
@@ -1172,25 +1282,10 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
     pp_ctx* c = thread_ctx(rc);
     if (!c) return rc;
     hipStream_t st = c->own;
-    const size_t mn = (size_t)m * n;
-    PP_TRY(c->up_lam.ensure(mn * 8));
-    PP_TRY(c->up_w.ensure(mn * 8));
-    PP_TRY(c->up_f.ensure(mn * m * 8));
-    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
-    PP_TRY(upload_tree(c, t, st));
-    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
-                         c->up_f.as<int64_t>(), st));
+    PP_TRY(upload_host_inputs(c, t, m, demand, recompute_cost, fetch_cost, st));
     PlanResult r;
     PP_TRY(run_plan(c, t, m, cap, o, tot < kFmaxBound, st, r));
-    std::vector<uint8_t> pre(mn);
-    PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
-                          mn, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
-    for (int32_t h = 0; h < m; ++h)
-      for (int32_t q = 0; q < n; ++q)
-        target[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
+    PP_TRY(placement_to_host(c, t, m, r.win_slot, target, st));
     *objective = r.win_obj;
     fill_stats(stats, r, m);
     return PP_OK;
@@ -1261,25 +1356,10 @@ int pp_plan_f64(int32_t n, int32_t m, const int32_t* parent, const double* deman
     pp_ctx* c = thread_ctx(rc);
     if (!c) return rc;
     hipStream_t st = c->own;
-    const size_t mn = (size_t)m * n;
-    PP_TRY(c->up_lam.ensure(mn * 8));
-    PP_TRY(c->up_w.ensure(mn * 8));
-    PP_TRY(c->up_f.ensure(mn * m * 8));
-    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
-    PP_TRY(upload_tree(c, t, st));
-    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
-                         c->up_f.as<int64_t>(), st));
+    PP_TRY(upload_host_inputs(c, t, m, demand, recompute_cost, fetch_cost, st));
     PlanResult r;
     PP_TRY(run_plan(c, t, m, cap, o, false, st, r, 0, true, epsilon));
-    std::vector<uint8_t> pre(mn);
-    PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
-                          mn, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
-    for (int32_t h = 0; h < m; ++h)
-      for (int32_t q = 0; q < n; ++q)
-        target[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
+    PP_TRY(placement_to_host(c, t, m, r.win_slot, target, st));
     *objective = bits_f64(r.win_obj);
     fill_stats_f64(stats, r);
     return PP_OK;
@@ -1313,74 +1393,21 @@ int pp_replan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand
     pp_ctx* c = thread_ctx(rc);
     if (!c) return rc;
     hipStream_t st = c->own;
-    PP_TRY(c->up_lam.ensure(mn * 8));
-    PP_TRY(c->up_w.ensure(mn * 8));
-    PP_TRY(c->up_f.ensure(mn * m * 8));
-    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
-    PP_TRY(upload_tree(c, t, st));
-    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
-                         c->up_f.as<int64_t>(), st));
+    PP_TRY(upload_host_inputs(c, t, m, demand, recompute_cost, fetch_cost, st));
     // the proposal: Algorithm 1 on the refreshed inputs, one slot spare
     PlanResult r;
     PP_TRY(run_plan(c, t, m, cap, o, tot < kFmaxBound, st, r, 1));
-    DevState d{};
-    d.n = n;
-    d.m = m;
-    d.npad = npad_of(n);
-    d.lam = c->lam.as<int64_t>();
-    d.w = c->w.as<int64_t>();
-    d.f = c->f.as<int64_t>();
-    d.tgt = c->tgt.as<uint8_t>();
-    d.v1 = c->v1.as<int64_t>();
-    d.v2 = c->v2.as<int64_t>();
-    d.h1 = c->h1.as<uint8_t>();
-    d.cs = c->cs.as<ChainState>();
-    // the incumbent, in preorder positions, into the spare slot; its
-    // objective under the refreshed inputs (Eq. 6)
-    const int32_t xs = r.extra_slot;
-    std::vector<uint8_t> pre(mn);
-    for (int32_t h = 0; h < m; ++h)
-      for (int32_t q = 0; q < n; ++q)
-        pre[(size_t)h * n + q] = incumbent[(size_t)h * n + t.order[q]];
-    PP_HIP(hipMemcpyAsync(d.tgt + (size_t)xs * mn, pre.data(), mn,
-                          hipMemcpyHostToDevice, st));
-    const std::vector<int32_t> one = {xs}, zero = {0};
-    const ChainSet inc_set = chain_set(one, zero, zero, 0, 1);
-    PP_HIP(launch_init_slots(inc_set, d, 0, st));
-    PP_HIP(launch_holder_build(inc_set, d, st));
-    PP_HIP(launch_objective(inc_set, d, st));
-    // one-time cost of the proposal's new (worker, chunk) pairs
-    PP_TRY(c->partial.ensure(1024 * 16));
-    int32_t nb = 0;
-    PP_HIP(launch_mat_cost(d, xs, r.win_slot, c->partial.p, &nb, st));
-    std::vector<unsigned __int128> part(nb);
-    ChainState inc_cs{};
-    PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, 16 * (size_t)nb,
-                          hipMemcpyDeviceToHost, st));
-    PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState),
-                          hipMemcpyDeviceToHost, st));
-    std::vector<uint8_t> prop_pre(mn);
-    PP_HIP(hipMemcpyAsync(prop_pre.data(), d.tgt + (size_t)r.win_slot * mn, mn,
-                          hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
-    unsigned __int128 cost = 0;
-    for (unsigned __int128 v : part) cost += v;
+    ReplanEval ev;
+    PP_TRY(replan_evaluate(c, t, m, r, incumbent, false, 0.0, st, ev));
+    const unsigned __int128 cost = ev.cost;
     if (cost > (unsigned __int128)INT64_MAX)
       return fail(PP_E_OVERFLOW, "materialization cost exceeds INT64_MAX");
     // adopt iff horizon * (G(T') - G(T)) > cost, exactly
-    const int64_t g_inc = inc_cs.obj, g_new = r.win_obj;
+    const int64_t g_inc = ev.g_inc, g_new = r.win_obj;
     bool adopt = false;
     if (g_new > g_inc)
       adopt = (unsigned __int128)(uint64_t)(g_new - g_inc) * (uint64_t)horizon > cost;
-    for (int32_t h = 0; h < m; ++h)
-      for (int32_t q = 0; q < n; ++q) {
-        const size_t id = (size_t)h * n + t.order[q];
-        const uint8_t v = prop_pre[(size_t)h * n + q];
-        if (proposal) proposal[id] = v;
-        target[id] = adopt ? v : incumbent[id];
-      }
+    PP_TRY(replan_outputs(c, t, m, r, incumbent, adopt, target, proposal, st));
     info->adopt = adopt ? 1 : 0;
     info->incumbent_objective = g_inc;
     info->proposal_objective = g_new;
@@ -1495,69 +1522,15 @@ int pp_replan_f64(int32_t n, int32_t m, const int32_t* parent, const double* dem
     pp_ctx* c = thread_ctx(rc);
     if (!c) return rc;
     hipStream_t st = c->own;
-    PP_TRY(c->up_lam.ensure(mn * 8));
-    PP_TRY(c->up_w.ensure(mn * 8));
-    PP_TRY(c->up_f.ensure(mn * m * 8));
-    PP_HIP(hipMemcpyAsync(c->up_lam.p, demand, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_w.p, recompute_cost, mn * 8, hipMemcpyHostToDevice, st));
-    PP_HIP(hipMemcpyAsync(c->up_f.p, fetch_cost, mn * m * 8, hipMemcpyHostToDevice, st));
-    PP_TRY(upload_tree(c, t, st));
-    PP_TRY(layout_inputs(c, t, m, c->up_lam.as<int64_t>(), c->up_w.as<int64_t>(),
-                         c->up_f.as<int64_t>(), st));
+    PP_TRY(upload_host_inputs(c, t, m, demand, recompute_cost, fetch_cost, st));
     PlanResult r;
     PP_TRY(run_plan(c, t, m, cap, o, false, st, r, 1, true, epsilon));
-    DevState d{};
-    d.n = n;
-    d.m = m;
-    d.npad = npad_of(n);
-    d.lam = c->lam.as<int64_t>();
-    d.w = c->w.as<int64_t>();
-    d.f = c->f.as<int64_t>();
-    d.tgt = c->tgt.as<uint8_t>();
-    d.v1 = c->v1.as<int64_t>();
-    d.v2 = c->v2.as<int64_t>();
-    d.h1 = c->h1.as<uint8_t>();
-    d.cs = c->cs.as<ChainState>();
-    d.f64 = 1;
-    d.eps = epsilon;
-    d.fpart_stride = fpart_blocks(n, m);
-    d.fpart = c->fpart.as<double>();
-    const int32_t xs = r.extra_slot;
-    std::vector<uint8_t> pre(mn);
-    for (int32_t h = 0; h < m; ++h)
-      for (int32_t q = 0; q < n; ++q)
-        pre[(size_t)h * n + q] = incumbent[(size_t)h * n + t.order[q]];
-    PP_HIP(hipMemcpyAsync(d.tgt + (size_t)xs * mn, pre.data(), mn,
-                          hipMemcpyHostToDevice, st));
-    const std::vector<int32_t> one = {xs}, zero = {0};
-    const ChainSet inc_set = chain_set(one, zero, zero, 0, 1);
-    PP_HIP(launch_init_slots(inc_set, d, 0, st));
-    PP_HIP(launch_holder_build(inc_set, d, st));
-    PP_HIP(launch_objective(inc_set, d, st));
-    PP_TRY(c->partial.ensure(1024 * 16));
-    int32_t nb = 0;
-    PP_HIP(launch_mat_cost(d, xs, r.win_slot, c->partial.p, &nb, st));
-    std::vector<double> part(nb);
-    ChainState inc_cs{};
-    PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, 8 * (size_t)nb,
-                          hipMemcpyDeviceToHost, st));
-    PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState),
-                          hipMemcpyDeviceToHost, st));
-    std::vector<uint8_t> prop_pre(mn);
-    PP_HIP(hipMemcpyAsync(prop_pre.data(), d.tgt + (size_t)r.win_slot * mn, mn,
-                          hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
-    double cost = 0.0;
-    for (double v : part) cost += v;
-    const double g_inc = bits_f64(inc_cs.obj), g_new = bits_f64(r.win_obj);
+    ReplanEval ev;
+    PP_TRY(replan_evaluate(c, t, m, r, incumbent, true, epsilon, st, ev));
+    const double cost = ev.cost_f64;
+    const double g_inc = bits_f64(ev.g_inc), g_new = bits_f64(r.win_obj);
     const bool adopt = horizon * (g_new - g_inc) > cost;
-    for (int32_t h = 0; h < m; ++h)
-      for (int32_t q = 0; q < n; ++q) {
-        const size_t id = (size_t)h * n + t.order[q];
-        const uint8_t v = prop_pre[(size_t)h * n + q];
-        if (proposal) proposal[id] = v;
-        target[id] = adopt ? v : incumbent[id];
-      }
+    PP_TRY(replan_outputs(c, t, m, r, incumbent, adopt, target, proposal, st));
     info->adopt = adopt ? 1 : 0;
     info->incumbent_objective = g_inc;
     info->proposal_objective = g_new;
