@@ -689,10 +689,13 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     if (lane == 0) sync[kDone] = 0;
     bool ok;
     {
+      // the records' other inputs first: they do not wait on the ring
+      const int64_t p0 = profit_at(lane);
+      const uint4 m0 = meta_at(lane);
       uint64_t w0, w1;
       ring_load(0, w0, w1);
       ok = ring_wait(0, w0, w1);
-      stage(0, profit_at(lane), w0, w1, meta_at(lane));
+      stage(0, p0, w0, w1, m0);
     }
     // inputs of batch b+1, loaded during batch b-1 (ring words two batches
     // ahead; the validation waits only on loads)
