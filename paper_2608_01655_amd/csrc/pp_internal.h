@@ -66,7 +66,8 @@ struct ChainState {
   int32_t changed;   // real-valued refinement: the accepted selection
                      // differs from the incumbent set (counted once)
   // Refinement updates whose inputs are unchanged: bit h of dirty is set
-  // when another worker's set changes and cleared when worker h's DP runs.
+  // when another worker's replacement is adopted (its set may change) and
+  // cleared when worker h's DP runs.
   // A refinement update of a clean worker would rebuild the same profits,
   // find the same set and reject it, so it is resolved as rejected without
   // the sweep (skip = 1 for the current update).

@@ -1246,6 +1246,14 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     }
   }
   if (!accept) return;
+  if (lane == 0) {
+    // every other worker's marginals change with worker h's set (an
+    // accepted real-valued replacement may leave the set as it was: then
+    // the marks only cost those workers a sweep)
+    const int h = set.worker[ci];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
+  }
   const int nwords = d.npad / 32;
   uint32_t* selw = d.sel + slot * nwords;
   for (int q = lane; q < nwords; q += kWave) selw[q] = 0;
@@ -1369,11 +1377,16 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
 // -------------------------------------------------------------- commit --
 
 // Adopt T'_h where accepted: write the new membership and refresh the top-2
-// holder state of every chunk whose membership changed (O(M^2) each).  A
-// block holds kCommitThreads / M chunks times M requesters (requester-major,
-// so each requester's loads are contiguous); each thread rebuilds one
-// requester's top-2 over all holders, taking worker h's membership from
-// the new selection, and the new membership is written after a barrier.
+// holder state of every chunk whose membership changed.  A block holds
+// kCommitThreads / M chunks times M requesters (requester-major, so each
+// requester's loads are contiguous); each thread updates one requester's
+// top-2, and the new membership is written after a barrier.  Only worker
+// h's membership changes, so the new state follows from the old one and
+// h's saving q_h: when h joins, q_h is inserted (top-2 values of the
+// multiset, lowest holder id among the maxima); when h leaves and was
+// neither the best holder nor tied with the second value (q_h < v2), the
+// state is unchanged.  Otherwise (h leaves as h1, or with q_h == v2) the
+// thread rebuilds the top-2 over all holders, O(M).
 constexpr int kCommitThreads = 256;
 
 __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevState d,
@@ -1397,30 +1410,54 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
     changed = nv != th[i];
   }
   if (!__syncthreads_or(changed)) return;
-  if (threadIdx.x == 0) {
-    // every other worker's marginals change with worker h's set
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-      atomicOr(&d.cs[s].dirty[q], q == (h >> 5) ? ~(1u << (h & 31)) : ~0u);
-  }
   if (d.f64 && mode == kModeRefine && threadIdx.x == 0 &&
+      __hip_atomic_load(&d.cs[s].changed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0 &&
       atomicExch(&d.cs[s].changed, 1) == 0) {
-    // the first block that sees a change counts the replacement
+    // the first block that sees a change counts the replacement (the plain
+    // load keeps the other blocks off the atomic)
     d.cs[s].improved = 1;
     d.cs[s].accepts += 1;
   }
   if (changed) {
+    const int64_t o = s * mn + (int64_t)r * n + i;
     const int64_t wr = d.w[(int64_t)r * n + i];
-    int64_t b1 = 0, b2 = 0;
-    int hb = kNoHolder;
+    auto q_of = [&](int l) -> int64_t {
+      if (l == r) return wr;
+      const int64_t fv = d.f[((int64_t)l * m + r) * n + i];
+      return d.f64 ? as_i(dpos(as_f(wr) - as_f(fv))) : imax(wr - fv, 0);
+    };
+    const int64_t qh = q_of(h);
+    int64_t b1 = d.v1[o], b2 = d.v2[o];
+    int hb = d.h1[o];
+    // savings are non-negative (doubles: finite, +0 for none), so their
+    // bit patterns compare like the values
+    bool rebuild = false;
+    if (nv) {
+      if (hb == kNoHolder) {
+        b1 = qh;
+        b2 = 0;
+        hb = h;
+      } else if (qh > b1) {
+        b2 = b1;
+        b1 = qh;
+        hb = h;
+      } else if (qh == b1) {
+        b2 = b1;
+        hb = h < hb ? h : hb;
+      } else if (qh > b2) {
+        b2 = qh;
+      }
+    } else {
+      rebuild = hb == h || qh >= b2;
+    }
+    if (rebuild) {
+      b1 = 0;
+      b2 = 0;
+      hb = kNoHolder;
 #pragma unroll 8
-    for (int l = 0; l < m; ++l) {
-      const bool held = (l == h) ? nv != 0 : t[(int64_t)l * n + i] != 0;
-      const int64_t fv = (l == r) ? 0 : d.f[((int64_t)l * m + r) * n + i];
-      const int64_t q = (l == r) ? wr
-                        : d.f64 ? as_i(dpos(as_f(wr) - as_f(fv)))
-                                : imax(wr - fv, 0);
-      if (held) {
+      for (int l = 0; l < m; ++l) {
+        if (l == h || t[(int64_t)l * n + i] == 0) continue;
+        const int64_t q = q_of(l);
         if (hb == kNoHolder || q > b1) {
           b2 = (hb == kNoHolder) ? b2 : b1;
           b1 = q;
@@ -1430,7 +1467,6 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
         }
       }
     }
-    const int64_t o = s * mn + (int64_t)r * n + i;
     d.v1[o] = b1;
     d.v2[o] = b2;
     d.h1[o] = (uint8_t)hb;
