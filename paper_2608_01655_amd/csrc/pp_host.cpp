@@ -17,8 +17,6 @@
 #include <memory>
 #include <new>
 #include <string>
-#include <map>
-#include <set>
 #include <vector>
 
 using namespace pp;
@@ -84,11 +82,12 @@ struct TreeLayout {
   int32_t n = 0;
   std::vector<int32_t> order, nextpos;
   // the backtrack's skip chains inside 32-row windows [32w, 32w + 32), as
-  // pairs ce[2q] = chain mask, ce[2q + 1] = exit row: the mask has bit r set
-  // for every row 32w + r of q, next(q), next(next(q)), ... that lies in q's
-  // window; the exit row is the first row of that sequence past the window
-  // (>= n: past the end).  Padded with empty rows (mask 0, exit n) through
-  // one 512-row block past the last full block.
+  // ce[4q] = chain mask, ce[4q + 1] = exit row, ce[4q + 2] = the exit row's
+  // own chain mask, ce[4q + 3] = 0: the mask has bit r set for every row
+  // 32w + r of q, next(q), next(next(q)), ... that lies in q's window; the
+  // exit row is the first row of that sequence past the window (kCeEnd if
+  // that is past the last row, with mask 0).  Padded with empty rows (mask
+  // 0, exit kCeEnd) through one 512-row block past the last full block.
   std::vector<uint32_t> ce;
   // per padded DP step: leaf flag (next(i) = i+1), the LDS slot the row is
   // stored to (-1: a sink row), and the slot holding the next step's skip
@@ -142,14 +141,21 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
     if (t.order[q] != q) t.identity = false;
   }
   const size_t ce_rows = ((size_t)n + kCeBlock - 1) / kCeBlock * kCeBlock + kCeBlock;
-  t.ce.assign(2 * ce_rows, 0);
-  for (size_t q = n; q < ce_rows; ++q) t.ce[2 * q + 1] = (uint32_t)n;
+  t.ce.assign(4 * ce_rows, 0);
+  for (size_t q = n; q < ce_rows; ++q) t.ce[4 * q + 1] = kCeEnd;
   for (int32_t q = n - 1; q >= 0; --q) {
     const int32_t wend = std::min<int32_t>((q / 32 + 1) * 32, n);
     const int32_t nq = t.nextpos[q];  // > q
-    const bool inside = nq < wend;
-    t.ce[2 * q] = (1u << (q % 32)) | (inside ? t.ce[2 * nq] : 0u);
-    t.ce[2 * q + 1] = inside ? t.ce[2 * nq + 1] : (uint32_t)nq;
+    uint32_t* e = &t.ce[4 * (size_t)q];
+    if (nq < wend) {  // the chain continues inside the window
+      e[0] = (1u << (q % 32)) | t.ce[4 * (size_t)nq];
+      e[1] = t.ce[4 * (size_t)nq + 1];
+      e[2] = t.ce[4 * (size_t)nq + 2];
+    } else {
+      e[0] = 1u << (q % 32);
+      e[1] = nq < n ? (uint32_t)nq : kCeEnd;
+      e[2] = nq < n ? t.ce[4 * (size_t)nq] : 0u;
+    }
   }
   // DP metadata.  Rows are 1-based positions i; nx(i) = next(i); row i is
   // produced at padded step pad + n - i.  A row r = next(a) with r != a+1
@@ -172,15 +178,35 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
   t.leaf.assign(nsteps, 1);
   t.store.assign(nsteps, -1);
   t.src.assign(nsteps, -1);
-  // free slots (lowest first) and slots waiting for their release step
-  std::set<int32_t> free_slots;
-  std::multimap<int32_t, int32_t> releases;  // step -> slot
+  // Free slots as a bitmap (the lowest is taken first), and slots waiting
+  // for their release step: a release is due at most kDpGatherMax - 1 steps
+  // ahead, so it waits in the bitmap of its step modulo kDpGatherMax.
+  static_assert(kMaxSlots <= 256, "slot bitmaps");
+  struct Slots {
+    uint64_t w[4] = {0, 0, 0, 0};
+    void set(int32_t k) { w[k >> 6] |= 1ull << (k & 63); }
+    bool any() const { return (w[0] | w[1] | w[2] | w[3]) != 0; }
+    int32_t take_lowest() {
+      for (int q = 0; q < 4; ++q)
+        if (w[q]) {
+          const int b = __builtin_ctzll(w[q]);
+          w[q] &= w[q] - 1;
+          return q * 64 + b;
+        }
+      return -1;
+    }
+    void absorb(Slots& o) {
+      for (int q = 0; q < 4; ++q) {
+        w[q] |= o.w[q];
+        o.w[q] = 0;
+      }
+    }
+  };
+  Slots free_slots, releases[kDpGatherMax];
   int32_t high = 0;
   for (int32_t i = n; i >= 1; --i) {
     const int32_t s = pad + n - i;  // padded step of row i
-    for (auto it = releases.begin(); it != releases.end() && it->first <= s;
-         it = releases.erase(it))
-      free_slots.insert(it->second);
+    free_slots.absorb(releases[s % kDpGatherMax]);
     const int32_t r = nx(i);
     t.leaf[s] = (r == i + 1) ? 1 : 0;
     if (far(i, r) && last_user[r] == i) {
@@ -188,17 +214,16 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
       // group
       const int32_t sr = pad + n - r;
       const int32_t after_gather = (sr / kDpGatherMax + 1) * kDpGatherMax;
-      const int32_t at = std::max(s, after_gather);
+      const int32_t at = std::max(s, after_gather);  // < s + kDpGatherMax
       if (at <= s)
-        free_slots.insert(slot_of[r]);
+        free_slots.set(slot_of[r]);
       else
-        releases.emplace(at, slot_of[r]);
+        releases[at % kDpGatherMax].set(slot_of[r]);
     }
     if (last_user[i] != INT32_MAX) {
       int32_t k;
-      if (!free_slots.empty()) {
-        k = *free_slots.begin();
-        free_slots.erase(free_slots.begin());
+      if (free_slots.any()) {
+        k = free_slots.take_lowest();
       } else {
         if (high >= kMaxSlots)
           return fail(PP_E_UNSUPPORTED,
@@ -459,11 +484,13 @@ struct Engine {
 };
 
 // Cells per lane for a launch whose chains need `total_stage_cells_c1`
-// stages at one cell per lane.  A stage is one wave; alone on its SIMD its
-// row step takes about 61 / 77 / 125 ns at 1 / 2 / 4 cells per lane (it is
-// bound by the wave's instruction issue).  When stages outnumber SIMDs they
-// share the SIMDs' vector units, so the estimate is scaled by the waves per
-// SIMD (about three quarters of a step's instructions are vector ops).
+// stages at one cell per lane.  A stage's compute wave, alone on its SIMD,
+// takes about 37 ns per row step at one cell per lane (bound by the wave's
+// instruction issue); the weights below (45 / 61 / 96 at 1 / 2 / 4 cells
+// per lane) are relative row-step costs of the sweep at each width.  When
+// compute waves outnumber SIMDs they share the SIMDs' vector units, so the
+// estimate is scaled by the waves per SIMD (about three quarters of a
+// step's instructions are vector ops).
 // Only widths whose stages all fit on the device at once are considered; if
 // none fits, the width with the most resident blocks is used and launches
 // are split.

@@ -42,6 +42,9 @@ constexpr int kMaxSlots = 254;
 constexpr int kDpBatch = 32;
 // Rows per block of the backtrack's staged chain table (16 windows of 32).
 constexpr int kCeBlock = 512;
+// Exit row of a backtrack skip chain that leaves the last row: larger than
+// any row of any super-window the walk can be in.
+constexpr uint32_t kCeEnd = 0x7FFFFFFFu;
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
 // Profit of a worker update: the exact marginal of Eq. 7, or one of the
@@ -94,11 +97,14 @@ struct DevState {
   const int64_t* w;         // [m][n]     recompute cost, preorder
   const int64_t* f;         // [m][m][n]  fetch cost [src][dst][pos]
   const int32_t* nextpos;   // [n]        0-based first position after subtree
-  const uint32_t* ce;       // [nce][2]   backtrack skip chain of q in its
-                            //            32-row window (bit per row), and the
+  const uint32_t* ce;       // [nce][4]   backtrack skip chain of q in its
+                            //            32-row window (bit per row), the
                             //            first row of that chain past the
-                            //            window; nce = n rounded up to
-                            //            kCeBlock, plus kCeBlock empty rows
+                            //            window (kCeEnd: past the last
+                            //            row), that row's own chain mask (0
+                            //            for kCeEnd) and 0; nce = n rounded
+                            //            up to kCeBlock, plus kCeBlock empty
+                            //            rows (mask 0, exit kCeEnd)
   const uint32_t* meta;     // [nsteps][4] per-step DP metadata
   uint8_t* tgt;             // [slots][m][n] placement, preorder
   int64_t* v1;              // [slots][m][n] best holder saving

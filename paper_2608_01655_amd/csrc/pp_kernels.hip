@@ -955,9 +955,11 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
 
 // The backtrack walk through one staged super-window, in scalar code.
 // Row sets of 32 consecutive rows (windows) are staged in LDS: for window k
-// and lane l, the chain mask and exit row of row q_lo + 32k + (l mod 32) at
-// ace + 256k (exit at +4), and lane l's choice word of cell c at
-// aw + 256(Ck + c).  In window wk the walk reads those into registers, then
+// and lane l, the 16-byte table row of row q_lo + 32k + (l mod 32) at
+// ace + 512k (chain mask, exit row at +4, the exit row's chain mask at +8),
+// and lane l's choice word of cell c at aw + 256(Ck + c).  Exit rows past
+// the last row are kCeEnd.  In window wk the walk reads those into
+// registers, then
 // finds the takes: the next take is the lowest set bit of (word of cell rem
 // & chain mask of q); it is recorded (bit of tm), the walk moves to the row
 // after it and to cell rem-1.  Without a set bit the walk leaves the window
@@ -967,6 +969,7 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
 // (wk >= 16).  On entry wk < 16, q lies in window wk, rem >= 0 and q < n.
 // Every pass raises q, so each window takes at most 32 passes.
 //
+// Two and four cells per lane (one cell per lane: walk_sw_c1 below).
 // Nearly every window change goes to the next window, so two register sets
 // alternate: while the walk uses one (labels 11-19), the other already
 // holds window wk + 1 (labels 21-29); a move to the next window switches
@@ -975,7 +978,7 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
 // v_writelane is m0 (one scalar operand besides the value); m0 is saved and
 // restored around the walk.
 #define PP_WALK_CE(S, IDX)                                       \
-  "s_lshl_b32 %[off], %[" IDX "], 8\n\t"                         \
+  "s_lshl_b32 %[off], %[" IDX "], 9\n\t"                         \
   "v_add_u32_e32 %[va], %[off], %[ace]\n\t"                      \
   "ds_read_b32 %[ch" S "], %[va]\n\t"                            \
   "ds_read_b32 %[ex" S "], %[va] offset:4\n\t"
@@ -1062,6 +1065,7 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
   PP_WALK_ROW                                                    \
   "s_branch 30b\n\t"                                             \
   "99:\n\t"                                                      \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
   "s_mov_b32 m0, %[sm0]"
 
 #define PP_WALK_OPERANDS                                                          \
@@ -1073,23 +1077,135 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
 #define PP_WALK_INPUTS \
   [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
 
-#define PP_LDW1(S, IDX)                                          \
-  "s_lshl_b32 %[offw], %[" IDX "], 8\n\t"                        \
-  "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"                      \
-  "ds_read_b32 %[w" S "0], %[vb]\n\t"
-#define PP_COLW1(S) "v_readlane_b32 %[w], %[w" S "0], %[rem]\n\t"
+// One cell per lane: the walk keeps the two window sets in fixed registers
+// (v48-v51: table rows of set P's window -- chain mask, exit row, the exit
+// row's chain mask --, v56: its choice words; v52-v55 and v57: set N), so
+// one 16-byte LDS read fetches a lane's table row.  A take is the lowest
+// set bit of (mask of row r & word of column rem); both lookups of the next
+// take are issued before the take's own bookkeeping.  A window is left
+// either after a take at its last row (next window, row 0) or, with no
+// take, at the exit row, whose chain mask comes with the row just left; in
+// both cases the next window is usually the one already in the other set,
+// and the walk continues there after one pair of lane reads.  Exit rows
+// past the last row are kCeEnd, so they leave the super-window like any
+// row beyond it.  Every pass raises the row, so the walk ends.
+#define PP_W1_LOAD(CE, WD, IDX)                                  \
+  "s_lshl_b32 %[off], %[" IDX "], 9\n\t"                         \
+  "v_add_u32_e32 %[va], %[off], %[ace]\n\t"                      \
+  "ds_read_b128 " CE ", %[va]\n\t"                               \
+  "s_lshl_b32 %[off], %[" IDX "], 8\n\t"                         \
+  "v_add_u32_e32 %[vb], %[off], %[aw]\n\t"                       \
+  "ds_read_b32 " WD ", %[vb]\n\t"
+// window wk + 1 (or 15 past the last one, never walked) into a set
+#define PP_W1_NEXT(CE, WD)                                       \
+  "s_add_u32 %[nx], %[wk], 1\n\t"                                \
+  "s_min_u32 %[nx], %[nx], 15\n\t"                               \
+  PP_W1_LOAD(CE, WD, "nx")
+// Takes inside the window of set S (labels T1-T4); O is the other set.
+// On entry m = chain mask of row r, w = word of column rem, and nx =
+// min(wk + 1, 15), the window the other set holds (an exit row in window 16
+// therefore leaves the super-window).
+#define PP_W1_SET(T, CE, CM, CX, CXM, WS, OCM, OWS, OT, DIR)     \
+  T "1:\n\t"                                                     \
+  "s_and_b32 %[t], %[m], %[w]\n\t"                               \
+  "s_cbranch_scc0 " T "3f\n\t"                                   \
+  "s_ff1_i32_b32 %[t], %[t]\n\t"                                 \
+  "s_add_u32 %[r], %[t], 1\n\t"                                  \
+  "s_bitset1_b32 %[tm], %[t]\n\t"                                \
+  "s_sub_u32 %[rem], %[rem], 1\n\t"                              \
+  "v_readlane_b32 %[m], " CM ", %[r]\n\t"                        \
+  "v_readlane_b32 %[w], " WS ", %[rem]\n\t"                      \
+  "s_cbranch_scc1 " T "4f\n\t"                                   \
+  "s_cmp_lg_u32 %[r], 32\n\t"                                    \
+  "s_cbranch_scc1 " T "1b\n\t"                                   \
+  /* a take at the last row: the next window, row 0 */           \
+  "s_mov_b32 m0, %[wk]\n\t"                                      \
+  "v_writelane_b32 %[tw], %[tm], m0\n\t"                         \
+  "s_mov_b32 %[tm], 0\n\t"                                       \
+  "s_add_u32 %[wk], %[wk], 1\n\t"                                \
+  "s_add_u32 %[wlo], %[wlo], 32\n\t"                             \
+  "s_cmp_ge_u32 %[wk], 16\n\t"                                   \
+  "s_cbranch_scc1 97f\n\t"                                       \
+  "s_mov_b32 %[r], 0\n\t"                                        \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
+  "v_readlane_b32 %[m], " OCM ", 0\n\t"                          \
+  "v_readlane_b32 %[w], " OWS ", %[rem]\n\t"                     \
+  PP_W1_NEXT(CE, WS)                                             \
+  "s_branch " OT "1" DIR "\n\t"                                  \
+  /* no take: the exit row and its chain mask */                 \
+  T "3:\n\t"                                                     \
+  "v_readlane_b32 %[q], " CX ", %[r]\n\t"                        \
+  "v_readlane_b32 %[m], " CXM ", %[r]\n\t"                       \
+  "s_mov_b32 m0, %[wk]\n\t"                                      \
+  "v_writelane_b32 %[tw], %[tm], m0\n\t"                         \
+  "s_mov_b32 %[tm], 0\n\t"                                       \
+  "s_sub_u32 %[wk], %[q], %[qlo]\n\t"                            \
+  "s_lshr_b32 %[wk], %[wk], 5\n\t"                               \
+  /* nx = min(wk + 1, 15) of the window left: the other set's */  \
+  "s_cmp_lg_u32 %[wk], %[nx]\n\t"                                \
+  "s_cbranch_scc1 15f\n\t"                                       \
+  "s_add_u32 %[wlo], %[wlo], 32\n\t"                             \
+  "s_sub_u32 %[r], %[q], %[wlo]\n\t"                             \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
+  "v_readlane_b32 %[w], " OWS ", %[rem]\n\t"                     \
+  PP_W1_NEXT(CE, WS)                                             \
+  "s_branch " OT "1" DIR "\n\t"                                  \
+  /* the take used the stage's first column: leave the stage */  \
+  T "4:\n\t"                                                     \
+  "s_add_u32 %[q], %[wlo], %[r]\n\t"                             \
+  "s_cmp_lg_u32 %[r], 32\n\t"                                    \
+  "s_cbranch_scc1 99f\n\t"                                       \
+  "s_mov_b32 m0, %[wk]\n\t"                                      \
+  "v_writelane_b32 %[tw], %[tm], m0\n\t"                         \
+  "s_mov_b32 %[tm], 0\n\t"                                       \
+  "s_add_u32 %[wk], %[wk], 1\n\t"                                \
+  "s_branch 99f\n\t"
 
 __device__ __forceinline__ void walk_sw_c1(uint32_t& q, uint32_t& rem, uint32_t& tm,
                                            uint32_t& wk, uint32_t& tw, uint32_t qlo,
-                                           uint32_t n, uint32_t ace, uint32_t aw) {
-  uint32_t r, m, w, t, off, wlo, nx, sm0, va, chP, exP, chN, exN, vb, offw, wP0, wN0;
-#define PP_WALK_NREAD "3"
-  asm volatile(PP_WALK_SW(PP_LDW1, PP_COLW1)
-               : PP_WALK_OPERANDS, [offw] "=&s"(offw), [wP0] "=&v"(wP0), [wN0] "=&v"(wN0)
-               : PP_WALK_INPUTS
-               : "scc");
-#undef PP_WALK_NREAD
+                                           uint32_t ace, uint32_t aw) {
+  uint32_t r, m, w, t, off, wlo, nx, sm0, va, vb;
+  asm volatile(
+      "s_mov_b32 %[sm0], m0\n\t"
+      // (re)load: window wk into set P, wk + 1 into set N; row r of wk
+      "10:\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
+      PP_W1_LOAD("v[48:51]", "v56", "wk")
+      "s_add_u32 %[nx], %[wk], 1\n\t"
+      "s_min_u32 %[nx], %[nx], 15\n\t"
+      PP_W1_LOAD("v[52:55]", "v57", "nx")
+      "s_lshl_b32 %[wlo], %[wk], 5\n\t"
+      "s_add_u32 %[wlo], %[wlo], %[qlo]\n\t"
+      "s_sub_u32 %[r], %[q], %[wlo]\n\t"
+      "s_waitcnt lgkmcnt(2)\n\t"
+      "v_readlane_b32 %[m], v48, %[r]\n\t"
+      "v_readlane_b32 %[w], v56, %[rem]\n\t"
+      "s_branch 11f\n\t"
+      PP_W1_SET("1", "v[48:51]", "v48", "v49", "v50", "v56", "v52", "v57", "2", "f")
+      PP_W1_SET("2", "v[52:55]", "v52", "v53", "v54", "v57", "v48", "v56", "1", "b")
+      // the exit row is not in the next window: leave the super-window, or
+      // reload both sets around it
+      "15:\n\t"
+      "s_cmp_ge_u32 %[wk], 16\n\t"
+      "s_cbranch_scc1 99f\n\t"
+      "s_branch 10b\n\t"
+      // a take at the super-window's last row
+      "97:\n\t"
+      "s_mov_b32 %[q], %[wlo]\n\t"
+      // no LDS read may still be landing in a register the compiler reuses
+      "99:\n\t"
+      "s_waitcnt lgkmcnt(0)\n\t"
+      "s_mov_b32 m0, %[sm0]"
+      : [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [wk] "+s"(wk), [tw] "+v"(tw),
+        [r] "=&s"(r), [m] "=&s"(m), [w] "=&s"(w), [t] "=&s"(t), [off] "=&s"(off),
+        [wlo] "=&s"(wlo), [nx] "=&s"(nx), [sm0] "=&s"(sm0), [va] "=&v"(va), [vb] "=&v"(vb)
+      : [qlo] "s"(qlo), [ace] "v"(ace), [aw] "v"(aw)
+      : "scc", "memory", "v48", "v49", "v50", "v51", "v52", "v53", "v54", "v55", "v56",
+        "v57");
 }
+#undef PP_W1_SET
+#undef PP_W1_NEXT
+#undef PP_W1_LOAD
 
 // two and four cells per lane: cell rem is lane rem/C of word rem mod C
 #define PP_LDW2(S, IDX)                                          \
@@ -1159,8 +1275,6 @@ __device__ __forceinline__ void walk_sw_c4(uint32_t& q, uint32_t& rem, uint32_t&
 #undef PP_WALK_ROW
 #undef PP_WALK_NEXT
 #undef PP_WALK_CE
-#undef PP_LDW1
-#undef PP_COLW1
 #undef PP_LDW2
 #undef PP_COLW2
 #undef PP_LDW4
@@ -1197,7 +1311,8 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   constexpr int kStage = kWave * C;     // cells per stage
   static_assert(kWin == 32 && kSwWin == 16, "the scalar walk's window layout");
   __shared__ __attribute__((aligned(16))) uint32_t s_words[kSwWin][C][kWave];
-  __shared__ __attribute__((aligned(16))) uint32_t s_ce[kSw][2];  // chain mask, exit row
+  // chain mask, exit row, the exit row's chain mask, 0
+  __shared__ __attribute__((aligned(16))) uint32_t s_ce[kSw][4];
   const int ci = blockIdx.x;
   const int lane = threadIdx.x;
   const int64_t slot = set.slot[ci];
@@ -1279,12 +1394,13 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
         w[c * 4 + i] = *(const pp_u32x4*)(base + c * cstride + (int64_t)b * kWave);
     }
   };
-  // chain masks and exit rows of the super-window's 512 rows (the host pads
-  // the table with empty rows through one super-window past the end)
-  auto load_chain = [&](int sw, pp_u32x4 (&ce)[4]) {
-    const pp_u32x4* src = (const pp_u32x4*)d.ce + (int64_t)sw * (kSw / 2);
+  // table rows of the super-window's 512 rows, one 16-byte row per load
+  // (the host pads the table with empty rows through one super-window past
+  // the end)
+  auto load_chain = [&](int sw, pp_u32x4 (&ce)[8]) {
+    const pp_u32x4* src = (const pp_u32x4*)d.ce + (int64_t)sw * kSw;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ce[i] = src[i * kWave + lane];
+    for (int i = 0; i < 8; ++i) ce[i] = src[i * kWave + lane];
   };
   auto words_to_lds = [&](const pp_u32x4 (&w)[kW]) {
 #pragma unroll
@@ -1295,9 +1411,9 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
         *(pp_u32x4*)&s_words[k][c][4 * (lane % 16)] = w[c * 4 + i];
     }
   };
-  auto chain_to_lds = [&](const pp_u32x4 (&ce)[4]) {
+  auto chain_to_lds = [&](const pp_u32x4 (&ce)[8]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ((pp_u32x4*)&s_ce[0][0])[i * kWave + lane] = ce[i];
+    for (int i = 0; i < 8; ++i) ((pp_u32x4*)&s_ce[0][0])[i * kWave + lane] = ce[i];
   };
   // LDS addresses the walk reads from: lane l's row (l mod 32) of window 0
   // and lane l's word of window 0, cell 0
@@ -1314,7 +1430,7 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   int sw = 0;
   pp_u32x4 wb[kW];  // next super-window, same stage
   pp_u32x4 wd[kW];  // same super-window, stage below
-  pp_u32x4 cb[4];
+  pp_u32x4 cb[8];
   load_words(0, g, wb);
   load_chain(0, cb);
   words_to_lds(wb);
@@ -1330,7 +1446,7 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     uint32_t uq = (uint32_t)q, urem = (uint32_t)(j - jlo);
     uint32_t wk = (uint32_t)(q - sw * kSw) / kWin;
     if constexpr (C == 1) {
-      walk_sw_c1(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
+      walk_sw_c1(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), ace, aw);
     } else if constexpr (C == 2) {
       walk_sw_c2(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
     } else {
