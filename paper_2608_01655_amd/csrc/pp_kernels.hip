@@ -1133,9 +1133,13 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
   PP_W1_NEXT(CE, WS)                                             \
   "s_branch " OT "1" DIR "\n\t"                                  \
   /* no take: the exit row and its chain mask */                 \
+  /* (the other set's word of column rem is read before it is */ \
+  /* known to be the window: unused otherwise) */                 \
   T "3:\n\t"                                                     \
+  "s_waitcnt lgkmcnt(0)\n\t"                                     \
   "v_readlane_b32 %[q], " CX ", %[r]\n\t"                        \
   "v_readlane_b32 %[m], " CXM ", %[r]\n\t"                       \
+  "v_readlane_b32 %[w], " OWS ", %[rem]\n\t"                     \
   "s_mov_b32 m0, %[wk]\n\t"                                      \
   "v_writelane_b32 %[tw], %[tm], m0\n\t"                         \
   "s_mov_b32 %[tm], 0\n\t"                                       \
@@ -1146,8 +1150,6 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
   "s_cbranch_scc1 15f\n\t"                                       \
   "s_add_u32 %[wlo], %[wlo], 32\n\t"                             \
   "s_sub_u32 %[r], %[q], %[wlo]\n\t"                             \
-  "s_waitcnt lgkmcnt(0)\n\t"                                     \
-  "v_readlane_b32 %[w], " OWS ", %[rem]\n\t"                     \
   PP_W1_NEXT(CE, WS)                                             \
   "s_branch " OT "1" DIR "\n\t"                                  \
   /* the take used the stage's first column: leave the stage */  \
