@@ -69,6 +69,22 @@ def test_rooted_dp_shapes(oracle_mod):
             _dp_case(oracle_mod, parent, profit, k)
 
 
+@pytest.mark.parametrize("n", [511, 512, 513, 1023, 1024, 1025, 1553, 2065])
+def test_rooted_dp_super_window_edges(oracle_mod, n):
+    """The backtrack stages rows in blocks of 512 (16 windows of 32): sizes
+    at and around those boundaries, sparse profits so that the walk skips
+    whole subtrees across window and block boundaries, and budgets that end
+    the walk inside a block, at a stage edge or past the last row."""
+    rng = np.random.default_rng(5000 + n)
+    for p_root in (0.0, 0.01, 0.2):
+        parent = W.random_forest(n, rng, p_root=p_root)
+        for density in (0.05, 0.5):
+            profit = (rng.integers(1, 1000, size=n) *
+                      (rng.random(n) < density)).astype(np.int64)
+            for k in (64, 65, 300, n // 2, n, n + 1):
+                _dp_case(oracle_mod, parent, profit, k)
+
+
 def test_rooted_dp_all_zero_and_huge(oracle_mod):
     rng = np.random.default_rng(3)
     parent = W.random_forest(500, rng)
