@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 8
+#define PP_ABI_VERSION 9
 
 enum {
     PP_OK = 0,
@@ -320,6 +320,27 @@ int pp_plan_f64_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
  * first step's node is a leaf. */
 int pp_sweep_layout(int32_t n, const int32_t *parent, int32_t cells,
                     uint32_t *meta, int32_t *nsteps, int32_t *slots);
+
+/* Exit row in pp_backtrack_table for a skip sequence that runs past the
+ * last row. */
+#define PP_BT_END 0x7FFFFFFFu
+
+/* Host only, for inspection and CPU-side checks of the backtrack's skip
+ * table (Theorem 1's walk from (1, k'): a take moves to row i+1, a skip to
+ * next(i)).  Rows are 0-based preorder positions, grouped in windows of 32
+ * (rows 32w .. 32w+31).  For row q < n, with S(q) = q, next(q),
+ * next(next(q)), ... (next(q) = first position after q's subtree):
+ *   word 0 = mask of S(q) inside q's window, bit (r mod 32) for each row r
+ *            of S(q) below min(32(w+1), n);
+ *   word 1 = the first row of S(q) at or past that bound if it is < n, else
+ *            PP_BT_END;
+ *   word 2 = word 0 of that row (0 for PP_BT_END);
+ *   word 3 = 0.
+ * Rows n .. rows-1 are padding: {0, PP_BT_END, 0, 0}; rows = n rounded up to
+ * a multiple of 512, plus 512.  `table` (4 * rows words) may be NULL to
+ * query `rows`.  Errors as for pp_sweep_layout. */
+int pp_backtrack_table(int32_t n, const int32_t *parent, uint32_t *table,
+                       int64_t *rows);
 
 /* Description of the last error on the calling thread; valid until the
  * next pp_* call on that thread. */

@@ -112,6 +112,8 @@ def lib() -> ctypes.CDLL:
         L.pp_orders.argtypes = [i32, i32, u64, _P, _P]
         L.pp_sweep_layout.argtypes = [i32, _P, i32, _P, _P, _P]
         L.pp_sweep_layout.restype = ctypes.c_int
+        L.pp_backtrack_table.argtypes = [i32, _P, _P, _P]
+        L.pp_backtrack_table.restype = ctypes.c_int
         L.pp_ctx_create.argtypes = [ctypes.POINTER(_P), ctypes.c_int]
         L.pp_ctx_destroy.argtypes = [_P]
         L.pp_ctx_destroy.restype = None
@@ -404,6 +406,21 @@ def pp_sweep_layout(parent, cells):
     _check(lib().pp_sweep_layout(n, _p(parent), int(cells), _p(meta),
                                  ctypes.byref(ns), ctypes.byref(sl)))
     return meta, sl.value
+
+
+PP_BT_END = 0x7FFFFFFF
+
+
+def pp_backtrack_table(parent):
+    """The backtrack's per-row skip table of a tree, [rows][4] uint32
+    (host only; see pp_backtrack_table in include/prefixplace.h)."""
+    parent = _c(parent, np.int32)
+    n = parent.shape[0]
+    rows = ctypes.c_int64(0)
+    _check(lib().pp_backtrack_table(n, _p(parent), None, ctypes.byref(rows)))
+    table = np.zeros((rows.value, 4), np.uint32)
+    _check(lib().pp_backtrack_table(n, _p(parent), _p(table), ctypes.byref(rows)))
+    return table
 
 
 class Context:

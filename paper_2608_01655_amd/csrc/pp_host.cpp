@@ -1212,6 +1212,21 @@ int pp_sweep_layout(int32_t n, const int32_t* parent, int32_t cells,
   });
 }
 
+static_assert(kCeEnd == PP_BT_END, "one end marker for the backtrack table");
+
+int pp_backtrack_table(int32_t n, const int32_t* parent, uint32_t* table,
+                       int64_t* rows) {
+  g_err.clear();
+  return guarded([&]() -> int {
+    if (n < 1 || !parent || !rows) return fail(PP_E_ARG, "bad arguments to pp_backtrack_table");
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    if (table) std::copy(t.ce.begin(), t.ce.end(), table);
+    *rows = (int64_t)(t.ce.size() / 4);
+    return PP_OK;
+  });
+}
+
 int pp_ctx_create(pp_ctx** ctx, int device) {
   g_err.clear();
   if (!ctx) return fail(PP_E_ARG, "null ctx");

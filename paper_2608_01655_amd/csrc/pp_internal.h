@@ -44,7 +44,7 @@ constexpr int kDpBatch = 32;
 constexpr int kCeBlock = 512;
 // Exit row of a backtrack skip chain that leaves the last row: larger than
 // any row of any super-window the walk can be in.
-constexpr uint32_t kCeEnd = 0x7FFFFFFFu;
+constexpr uint32_t kCeEnd = 0x7FFFFFFFu;  // = PP_BT_END of the public header
 
 enum Mode : int32_t { kModeStandalone = 0, kModeGreedy = 1, kModeRefine = 2 };
 // Profit of a worker update: the exact marginal of Eq. 7, or one of the
