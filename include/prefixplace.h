@@ -16,9 +16,12 @@
  * order-diverse starts (Sec. IV-C, Algorithm 1).
  *
  * Conventions shared by every entry point
- *   - Integers only: demand is requests per epoch, costs are integer
- *     microseconds, every value/objective is int64 (request * us).  Results
- *     are exact and deterministic.
+ *   - Values: the integer entry points take demand in requests per epoch
+ *     and costs in integer microseconds, and every value/objective is int64
+ *     (request * us), exact.  The *_f64 entry points take finite,
+ *     non-negative IEEE doubles in any consistent units and a refinement
+ *     tolerance epsilon >= 0; their sums are taken in a fixed order, so
+ *     results are deterministic.
  *   - Node ids are the caller's labels 0..n-1.  parent[v] = -1 attaches v to
  *     the implicit no-cost dummy root (Sec. III-A), so forests are allowed.
  *   - Host arrays are C-contiguous, caller-owned, read or written only during
@@ -31,8 +34,9 @@
  *       better), so among optimal sets the one whose 0/1 vector in canonical
  *       preorder (roots, then children, by increasing id) is
  *       lexicographically smallest is returned;
- *       a refinement replacement is accepted only if it strictly raises the
- *       objective (integer costs: tolerance 0);
+ *       a refinement replacement is accepted only if it raises the
+ *       objective strictly (integer costs) or by more than epsilon (the
+ *       *_f64 entry points);
  *       ties between starts go to the lowest start index.
  *   - Start orders: start 0 sorts workers by standalone score (the optimum
  *     of the worker's own rooted-tree problem against an empty placement)
