@@ -7,15 +7,18 @@
 //                top-2 holder state, plus the incumbent's value for the
 //                strict-improvement test (Sec. IV-C)
 //   k_dp<C>      the rooted-tree DP sweep of Eq. 9 (Theorem 1), pipelined
-//                over the capacity axis: one wave64 "stage" owns 64*C
-//                consecutive cells j; rows are swept n..1 with no barrier
+//                over the capacity axis: one stage (a compute wave and an
+//                I/O wave) owns 64*C consecutive cells j; rows are swept
+//                n..1 with no barrier
 //   k_backtrack  the acceptance decision and the backtrack (Theorem 1's
 //                "at most n states"), one wave per chain
 //   k_commit     adopt T'_h and refresh the top-2 holder state on the chunks
 //                whose membership changed
 // plus the objective F_pair (Eq. 6) and small layout helpers.
 //
-// Integers only (int64 values, int32 indices); no floating point anywhere.
+// Values are int64 (integer costs) or, for real-valued costs, the bit
+// patterns of finite non-negative doubles in the same 64-bit slots (the
+// F64 template flag of k_dp, DevState::f64 elsewhere); indices are int32.
 
 #include <algorithm>
 #include <utility>
