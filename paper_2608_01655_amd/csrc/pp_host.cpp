@@ -397,6 +397,7 @@ ChainSet chain_set(const std::vector<int32_t>& slots,
   s.count = (int32_t)(hi - lo);
   for (size_t k = lo; k < hi; ++k) {
     s.slot[k - lo] = slots[k];
+    s.src[k - lo] = slots[k];
     s.worker[k - lo] = workers[k];
     s.kprime[k - lo] = kprime[k];
   }
@@ -451,6 +452,7 @@ struct Engine {
         const int32_t g = (in.kprime[k] + cellsw - 1) / cellsw;
         if (s.count > 0 && blocks + g > resident) break;
         s.slot[s.count] = in.slot[k];
+        s.src[s.count] = in.src[k];
         s.worker[s.count] = in.worker[k];
         s.kprime[s.count] = in.kprime[k];
         s.base[s.count] = blocks;
@@ -531,6 +533,7 @@ struct PlanResult {
   int64_t sg_obj[3] = {0, 0, 0};
   int32_t extra_slot = -1;     // first slot reserved for the caller
   int64_t skipped_cells = 0;   // cells of updates resolved without a sweep
+  int64_t spec_cells = 0;      // cells swept by discarded speculative updates
   int64_t updates = 0, cells = 0;
   double dp_ms = 0.0;
   int32_t dp_launches = 0;
@@ -634,6 +637,199 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
 // Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
 // Real-valued costs (f64): every value is the bit pattern of a non-negative
 // double, so the comparisons below (orders, best start) hold unchanged.
+// Coordinate refinement (Algorithm 1's sweeps) of the starts `starts`,
+// after their greedy pass.  Each start keeps its own position and sweep.
+// The host mirrors every start's stale-input marks (ChainState::dirty, the
+// same rules as the kernels: a worker's sweep clears its bit, an adopted
+// replacement sets every other worker's) and passes over positions whose
+// update is resolved as rejected without a sweep (a clean worker, or
+// k = 0) at no cost.  Each launch then holds every active start's next
+// update that needs a sweep, in the start's own slot, and fills the rest of
+// `budget` with speculative updates: later positions of the same sweep of
+// a start, in spare slots, computed against the start's current placement,
+// which is the placement each of them sees in Algorithm 1's order as long
+// as every earlier one is rejected.  The first accepted update of a start
+// is adopted and committed; the positions after it are looked at again in
+// the next launch.  Results are those of the sequential sweeps.
+int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_base,
+                  int32_t budget, int32_t m, const std::vector<int32_t>& kp,
+                  int32_t max_rounds, PlanResult& res) {
+  DevState& d = e.d;
+  const int32_t A = (int32_t)starts.size();
+  for (int32_t q = 1; q < A; ++q)
+    if (starts[q] != starts[0] + q) return fail(PP_E_DEVICE, "internal: start slots");
+  struct St {
+    int32_t s, pos;
+    bool improved, done;
+    uint32_t dirty[8];
+    bool is_dirty(int32_t h) const { return (dirty[h >> 5] >> (h & 31)) & 1u; }
+    void mark_ran(int32_t h) { dirty[h >> 5] &= ~(1u << (h & 31)); }
+    void mark_adopted(int32_t h) {
+      for (int q = 0; q < 8; ++q) dirty[q] = ~0u;
+      mark_ran(h);
+    }
+  };
+  std::vector<St> st(A);
+  {
+    std::vector<ChainState> cs0(A);
+    PP_HIP(hipMemcpyAsync(cs0.data(), d.cs + starts[0], sizeof(ChainState) * A,
+                          hipMemcpyDeviceToHost, e.st));
+    PP_HIP(hipStreamSynchronize(e.st));
+    for (int32_t q = 0; q < A; ++q) {
+      if (cs0[q].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+      st[q].s = starts[q];
+      st[q].pos = 0;
+      st[q].improved = false;
+      st[q].done = false;
+      std::memcpy(st[q].dirty, cs0[q].dirty, sizeof st[q].dirty);
+    }
+    std::vector<int32_t> z(A, 0);
+    PP_HIP(launch_reset_round(chain_set(starts, z, z, 0, A), d, e.st));
+  }
+  auto worker_at = [&](const St& x, int32_t a) { return res.orders[(size_t)x.s * m + a]; };
+  auto resolved_free = [&](const St& x, int32_t a) {
+    const int32_t h = worker_at(x, a);
+    return kp[h] == 0 || !x.is_dirty(h);
+  };
+  auto free_cells = [&](const St& x, int32_t a) {
+    return (int64_t)d.n * kp[worker_at(x, a)];  // 0 for k = 0
+  };
+  struct Item {
+    int32_t q, slot, worker, pos;
+  };
+  for (;;) {
+    // each start's next update that needs a sweep; sweep ends
+    for (int32_t q = 0; q < A; ++q) {
+      St& x = st[q];
+      while (!x.done) {
+        if (x.pos == m) {
+          res.sweeps[x.s] += 1;
+          bool improved = x.improved;
+          if (d.f64) {
+            // real-valued costs: k_commit counts a replacement only if it
+            // changes the set
+            ChainState c;
+            PP_HIP(hipMemcpyAsync(&c, d.cs + x.s, sizeof c, hipMemcpyDeviceToHost, e.st));
+            PP_HIP(hipStreamSynchronize(e.st));
+            improved = c.improved != 0;
+          }
+          const bool capped = max_rounds > 0 && res.sweeps[x.s] >= max_rounds;
+          if (!improved || capped) {
+            x.done = true;
+            break;
+          }
+          x.pos = 0;
+          x.improved = false;
+          const std::vector<int32_t> one = {x.s}, z = {0};
+          PP_HIP(launch_reset_round(chain_set(one, z, z, 0, 1), d, e.st));
+          continue;
+        }
+        if (!resolved_free(x, x.pos)) break;
+        res.skipped_cells += free_cells(x, x.pos);
+        ++x.pos;
+      }
+    }
+    std::vector<Item> items;
+    std::vector<int32_t> scan(A, m);
+    for (int32_t q = 0; q < A; ++q)
+      if (!st[q].done) {
+        items.push_back({q, st[q].s, worker_at(st[q], st[q].pos), st[q].pos});
+        scan[q] = st[q].pos + 1;
+      }
+    if (items.empty()) return PP_OK;
+    // speculative updates: at most `budget` updates in all, one spare slot
+    // each (budget - 1 spare slots exist)
+    int32_t spares = 0;
+    auto room = [&]() { return (int32_t)items.size() < budget && spares < budget - 1; };
+    for (bool grew = true; grew && room();) {
+      grew = false;
+      for (int32_t q = 0; q < A && room(); ++q) {
+        if (st[q].done) continue;
+        int32_t a = scan[q];
+        while (a < m && resolved_free(st[q], a)) ++a;
+        if (a < m) {
+          items.push_back({q, spare_base + spares++, worker_at(st[q], a), a});
+          grew = true;
+        }
+        scan[q] = a < m ? a + 1 : m;
+      }
+    }
+    std::stable_sort(items.begin(), items.end(),
+                     [](const Item& u, const Item& v) { return u.q < v.q; });
+    ChainSet set;
+    std::memset(&set, 0, sizeof set);
+    set.count = (int32_t)items.size();
+    for (int32_t k = 0; k < set.count; ++k) {
+      set.slot[k] = items[k].slot;
+      set.src[k] = st[items[k].q].s;
+      set.worker[k] = items[k].worker;
+      set.kprime[k] = kp[items[k].worker];
+    }
+    PP_HIP(launch_gains(set, d, e.st, kGainsMarginal, 1));
+    PP_TRY(e.dp(set, 1));
+    PP_HIP(launch_backtrack(set, d, kModeRefine, e.st));
+    // the launch's results: the starts' slots (consecutive) and the spare
+    // slots, in two copies
+    std::vector<ChainState> own(A), spare(spares > 0 ? spares : 1);
+    PP_HIP(hipMemcpyAsync(own.data(), d.cs + starts[0], sizeof(ChainState) * A,
+                          hipMemcpyDeviceToHost, e.st));
+    if (spares > 0)
+      PP_HIP(hipMemcpyAsync(spare.data(), d.cs + spare_base, sizeof(ChainState) * spares,
+                            hipMemcpyDeviceToHost, e.st));
+    PP_HIP(hipStreamSynchronize(e.st));
+    std::vector<ChainState> cs(items.size());
+    for (size_t k = 0; k < items.size(); ++k)
+      cs[k] = items[k].slot >= spare_base ? spare[items[k].slot - spare_base]
+                                          : own[items[k].slot - starts[0]];
+    // decisions, in each start's order
+    std::vector<int32_t> csl, cwk, ckp;
+    size_t k = 0;
+    for (int32_t q = 0; q < A; ++q) {
+      St& x = st[q];
+      uint32_t ran[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      const Item* take = nullptr;
+      int32_t last = x.pos - 1;  // last position resolved in this launch
+      for (; k < items.size() && items[k].q == q; ++k) {
+        const Item& it = items[k];
+        const ChainState& c = cs[k];
+        if (c.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+        if (take) {  // computed against a placement that has changed
+          if (!c.skip) res.spec_cells += (int64_t)d.n * kp[it.worker];
+          continue;
+        }
+        // positions passed over on the way are resolved as rejected
+        for (int32_t a = last + 1; a < it.pos; ++a) res.skipped_cells += free_cells(x, a);
+        if (c.skip) res.skipped_cells += (int64_t)d.n * kp[it.worker];
+        last = it.pos;
+        if (c.accept) {
+          take = &it;
+          x.improved = true;
+          x.mark_adopted(it.worker);
+        } else {
+          x.mark_ran(it.worker);
+          if (it.slot != x.s) ran[it.worker >> 5] |= 1u << (it.worker & 31);
+        }
+      }
+      if (x.done) continue;
+      x.pos = last + 1;
+      bool any_ran = false;
+      for (uint32_t b : ran) any_ran = any_ran || b != 0;
+      // (an update in the start's own slot is backtracked and marked by
+      // k_backtrack itself)
+      if ((take && take->slot != x.s) || (!take && any_ran))
+        PP_HIP(launch_adopt(d, x.s, take ? take->slot : -1, take ? take->worker : 0, ran,
+                            e.st));
+      if (take) {
+        csl.push_back(x.s);
+        cwk.push_back(take->worker);
+        ckp.push_back(kp[take->worker]);
+      }
+    }
+    if (!csl.empty())
+      PP_HIP(launch_commit(chain_set(csl, cwk, ckp, 0, csl.size()), d, kModeRefine, e.st));
+  }
+}
+
 int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
              const pp_options& o, bool fmax_ok, hipStream_t st,
              PlanResult& res, int32_t extra_slots = 0, bool f64 = false,
@@ -654,7 +850,11 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   // and LocalDedup candidates, and slots 0..m-1 serve as scratch chains
   const bool sg_asked = (o.flags & PP_F_SAFEGUARDS) != 0;
   const int32_t slot_b = std::max(m, S);
-  const int32_t slots = slot_b + (sg_asked ? 4 : 0) + extra_slots;
+  // speculative refinement (few active starts): up to kSpecChains updates
+  // of one start per launch, all but the first in spare slots at the end
+  const int32_t spec_chains = env_int("PP_NO_SPEC", 0) ? 1 : kSpecChains;  // updates per launch
+  const int32_t spare_base = slot_b + (sg_asked ? 4 : 0) + extra_slots;
+  const int32_t slots = spare_base + (spec_chains > 1 ? spec_chains - 1 : 0);
   res.extra_slot = extra_slots > 0 ? slot_b + (sg_asked ? 4 : 0) : -1;
   Engine e;
   e.c = c;
@@ -746,7 +946,9 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     std::vector<int32_t> active;
     for (int32_t s = lo; s < hi; ++s) active.push_back(s);
     {
-      std::vector<int32_t> sl(active), wk(active.size(), 0), kk(active.size(), 0);
+      std::vector<int32_t> sl(active);
+      for (int32_t q = spare_base; q < slots; ++q) sl.push_back(q);
+      std::vector<int32_t> wk(sl.size(), 0), kk(sl.size(), 0);
       PP_HIP(launch_init_slots(chain_set(sl, wk, kk, 0, sl.size()), d, 1, st));
     }
     auto position_set = [&](const std::vector<int32_t>& act, int32_t a) {
@@ -762,31 +964,8 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     };
     for (int32_t a = 0; a < m; ++a)
       PP_TRY(e.update(position_set(active, a), kModeGreedy));
-    if (!(o.flags & PP_F_NO_REFINE)) {
-      while (!active.empty()) {
-        {
-          std::vector<int32_t> wk(active.size(), 0), kk(active.size(), 0);
-          PP_HIP(launch_reset_round(chain_set(active, wk, kk, 0, active.size()),
-                                    d, st));
-        }
-        for (int32_t a = 0; a < m; ++a)
-          PP_TRY(e.update(position_set(active, a), kModeRefine));
-        std::vector<ChainState> cur(active.size());
-        for (size_t q = 0; q < active.size(); ++q)
-          PP_HIP(hipMemcpyAsync(&cur[q], d.cs + active[q], sizeof(ChainState),
-                                hipMemcpyDeviceToHost, st));
-        PP_HIP(hipStreamSynchronize(st));
-        std::vector<int32_t> next;
-        for (size_t q = 0; q < active.size(); ++q) {
-          const int32_t s = active[q];
-          if (cur[q].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
-          res.sweeps[s] += 1;
-          const bool capped = o.max_rounds > 0 && res.sweeps[s] >= o.max_rounds;
-          if (cur[q].improved && !capped) next.push_back(s);
-        }
-        active.swap(next);
-      }
-    }
+    if (!(o.flags & PP_F_NO_REFINE))
+      PP_TRY(refine_starts(e, active, spare_base, spec_chains, m, kp, o.max_rounds, res));
     std::vector<int32_t> sl, wk, kk;
     for (int32_t s = lo; s < hi; ++s) {
       sl.push_back(s);
@@ -1013,7 +1192,7 @@ void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
   stats->dp_launches = r.dp_launches;
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = r.sg_obj[q];
-  stats->dp_cells_executed = r.cells - r.skipped_cells;
+  stats->dp_cells_executed = r.cells - r.skipped_cells + r.spec_cells;
   (void)m;
 }
 
@@ -1044,7 +1223,7 @@ void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
   stats->dp_launches = r.dp_launches;
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = bits_f64(r.sg_obj[q]);
-  stats->dp_cells_executed = r.cells - r.skipped_cells;
+  stats->dp_cells_executed = r.cells - r.skipped_cells + r.spec_cells;
 }
 
 // Host-array inputs (caller ids, 8-byte values) to the context's preorder

@@ -9,6 +9,9 @@ namespace pp {
 
 // Chains (one worker update each) handled by a single launch.
 constexpr int kMaxChains = 64;
+// Updates per launch in a speculative refinement sweep (all active starts
+// together; a start's speculative updates beyond the first use spare slots).
+constexpr int kSpecChains = 8;
 // "no holder" marker of the top-1 holder state (workers are < 255).
 constexpr uint8_t kNoHolder = 255;
 
@@ -84,6 +87,9 @@ struct ChainState {
 struct ChainSet {
   int32_t count;
   int32_t slot[kMaxChains];    // state slot of the chain
+  int32_t src[kMaxChains];     // slot whose placement k_gains reads (the
+                               // chain's own slot, except for a speculative
+                               // update computed in a spare slot)
   int32_t worker[kMaxChains];  // worker h being updated
   int32_t kprime[kMaxChains];  // min(k_h, n)
   int32_t base[kMaxChains + 1];  // DP: first block of each chain's stages
@@ -169,6 +175,13 @@ hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
                      int fmax, hipStream_t st);
 hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
                             hipStream_t st);
+// Speculative refinement: the updates of consecutive positions of one
+// start run together in spare slots; the first accepted one (position
+// `take`, in spare slot `from`, or none: from = -1) is adopted into the
+// start's slot `s`, whose stale-input marks lose the bits in `ran` (workers
+// whose sweep ran against the unchanged placement).
+hipError_t launch_adopt(const DevState& d, int32_t s, int32_t from, int32_t worker,
+                        const uint32_t (&ran)[8], hipStream_t st);
 hipError_t launch_commit(const ChainSet& set, const DevState& d, int mode,
                          hipStream_t st);
 hipError_t launch_reset_round(const ChainSet& set, const DevState& d,

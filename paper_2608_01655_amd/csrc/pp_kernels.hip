@@ -276,7 +276,8 @@ __global__ void k_holder_build(ChainSet set, DevState d) {
 __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmode,
                                                int may_skip) {
   const int ci = blockIdx.y;
-  const int64_t s = set.slot[ci];
+  const int64_t s = set.slot[ci];   // the update's own state: profit, sums
+  const int64_t ps = set.src[ci];   // the placement it is computed against
   const int h = set.worker[ci];
   const int64_t n = d.n;
   const int64_t mn = (int64_t)d.m * n;
@@ -285,7 +286,7 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
     // a refinement update of a worker whose inputs have not changed since
     // its last sweep: resolved as rejected, no gains, sweep or walk
     const bool clean = may_skip && gmode == kGainsMarginal &&
-                       ((d.cs[s].dirty[h >> 5] >> (h & 31)) & 1u) == 0;
+                       ((d.cs[ps].dirty[h >> 5] >> (h & 31)) & 1u) == 0;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       d.cs[s].skip = clean ? 1 : 0;
       if (clean) {
@@ -311,7 +312,7 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
       const double F = as_f(d.f[((int64_t)src * d.m + h) * n + i]);
       bool covered = false;
       for (int l = 0; l < d.m; ++l)
-        if (l != h && d.tgt[s * mn + (int64_t)l * n + i]) covered = true;
+        if (l != h && d.tgt[ps * mn + (int64_t)l * n + i]) covered = true;
       const double a = L * (Wv < F ? Wv : F);
       const double own = L * dpos(Wv - F);
       p = covered ? a : a + own;
@@ -334,7 +335,7 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
       const int64_t F = d.f[((int64_t)src * d.m + h) * n + i];
       bool covered = false;
       for (int l = 0; l < d.m; ++l)
-        if (l != h && d.tgt[s * mn + (int64_t)l * n + i]) covered = true;
+        if (l != h && d.tgt[ps * mn + (int64_t)l * n + i]) covered = true;
       const int64_t a = L * (Wv < F ? Wv : F);
       p = covered ? a : a + L * imax(Wv - F, 0);
     }
@@ -348,14 +349,14 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
     bool in_th = false;
     if (i < n) {
       for (int r = 0; r < d.m; ++r) {
-        const int64_t o = s * mn + (int64_t)r * n + i;
+        const int64_t o = ps * mn + (int64_t)r * n + i;
         const double vmh = as_f((d.h1[o] == h) ? d.v2[o] : d.v1[o]);
         const double L = as_f(d.lam[(int64_t)r * n + i]);
         const double term = L * dpos(as_f(saving(d, h, r, i)) - vmh);
         p = p + term;
       }
       d.profit[s * n + i] = as_i(p);
-      in_th = d.tgt[s * mn + (int64_t)h * n + i] != 0;
+      in_th = d.tgt[ps * mn + (int64_t)h * n + i] != 0;
     }
     const double sh = block_sum_f64(in_th ? p : 0.0);
     if (threadIdx.x == 0) d.fpart[s * d.fpart_stride + blockIdx.x] = sh;
@@ -364,14 +365,14 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
   int64_t p = 0, g = 0, held = 0;
   if (i < n) {
     for (int r = 0; r < d.m; ++r) {
-      const int64_t o = s * mn + (int64_t)r * n + i;
+      const int64_t o = ps * mn + (int64_t)r * n + i;
       const int64_t vmh = (d.h1[o] == h) ? d.v2[o] : d.v1[o];
       const int64_t L = d.lam[(int64_t)r * n + i];
       p += L * imax(saving(d, h, r, i) - vmh, 0);
       g += L * vmh;
     }
     d.profit[s * n + i] = p;
-    held = d.tgt[s * mn + (int64_t)h * n + i] ? p : 0;
+    held = d.tgt[ps * mn + (int64_t)h * n + i] ? p : 0;
   }
   const int64_t sh = block_sum(held);
   const int64_t sg = block_sum(g);
@@ -1596,6 +1597,46 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
   if (changed && r == 0) th[i] = nv;
 }
 
+// Speculative refinement, after the decision: the workers in `ran` swept
+// against the start's unchanged placement (their inputs are current); if a
+// later position was accepted in spare slot `from`, slot s takes its
+// selection and acceptance as k_backtrack leaves them for an update run in
+// slot s itself, so that k_commit can adopt it there.
+struct Bits8 {
+  uint32_t w[8];
+};
+
+__global__ void __launch_bounds__(256) k_adopt(DevState d, int32_t s, int32_t from,
+                                               int32_t h, Bits8 ran) {
+  ChainState* st = d.cs + s;
+  if (from >= 0) {
+    const int nwords = d.npad / 32;
+    const uint32_t* src = d.sel + (int64_t)from * nwords;
+    uint32_t* dst = d.sel + (int64_t)s * nwords;
+    for (int q = threadIdx.x; q < nwords; q += blockDim.x) dst[q] = src[q];
+  }
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) st->dirty[q] &= ~ran.w[q];
+    if (from >= 0) {
+      const ChainState& fs = d.cs[from];
+      st->accept = 1;
+      st->inc = 0;
+      st->dpval = fs.dpval;
+      if (d.f64) {
+        st->changed = 0;  // k_commit counts the replacement if the set changes
+      } else {
+        st->improved = 1;
+        st->accepts += 1;
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
+      st->dirty[h >> 5] &= ~(1u << (h & 31));
+    }
+  }
+}
+
 // Row h of slot `dst`'s placement := the backtracked selection of chain
 // (slot, h), for every chain of the set (the per-worker comparator
 // candidates are solved in scratch slots and assembled here).
@@ -1919,6 +1960,14 @@ hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
     case 4: hipLaunchKernelGGL(k_backtrack<4>, dim3(set.count), dim3(kWave), 0, st, set, d, mode); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_adopt(const DevState& d, int32_t s, int32_t from, int32_t worker,
+                        const uint32_t (&ran)[8], hipStream_t st) {
+  Bits8 b;
+  for (int q = 0; q < 8; ++q) b.w[q] = ran[q];
+  hipLaunchKernelGGL(k_adopt, dim3(1), dim3(256), 0, st, d, s, from, worker, b);
   return hipGetLastError();
 }
 

@@ -199,9 +199,11 @@ def test_plan_deep_caterpillar(oracle_mod):
     _same(g, o)
 
 
-def test_unchanged_workers_skip_their_sweep(oracle_mod):
+def test_unchanged_workers_skip_their_sweep(oracle_mod, monkeypatch):
     """Refinement updates of workers whose inputs have not changed are
-    resolved without a sweep: fewer cells swept, identical plan."""
+    resolved without a sweep: fewer cells swept, identical plan (without
+    speculative sweeps, whose discarded updates add swept cells)."""
+    monkeypatch.setenv("PP_NO_SPEC", "1")
     inst = W.make_workload("tree2k")
     g, o = _plan_both(oracle_mod, inst)
     _same(g, o)
@@ -210,3 +212,26 @@ def test_unchanged_workers_skip_their_sweep(oracle_mod):
                    inst.cap, n_starts=inst.n_starts, order_seed=inst.order_seed,
                    flags=B.PP_F_NO_REFINE)
     assert nr.dp_cells_executed == nr.dp_cells
+
+
+@pytest.mark.parametrize("name,starts", [("tree2k", 1), ("tree2k", 2), ("rag10k", 3),
+                                         ("tiny", 1), ("tree2k", 5)])
+def test_speculative_sweeps(oracle_mod, monkeypatch, name, starts):
+    """Refinement runs each start at its own position, passes over updates
+    resolved without a sweep on the host, and fills each launch with
+    speculative updates of later positions (the first accepted one is
+    adopted, the rest computed again).  Same plan and statistics as without
+    speculation and as the oracle; fewer DP launches."""
+    inst = W.make_workload(name)
+    args = dict(n_starts=starts, max_rounds=0, order_seed=inst.order_seed)
+    g = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                  inst.cap, flags=B.PP_F_TIME_KERNELS, **args)
+    monkeypatch.setenv("PP_NO_SPEC", "1")
+    q = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                  inst.cap, flags=B.PP_F_TIME_KERNELS, **args)
+    o = oracle_mod.plan_instance(inst, threads=8, **args)
+    _same(g, o)
+    _same(q, o)
+    assert g.updates == q.updates and g.dp_cells == q.dp_cells
+    if starts <= 4 and name != "tiny":
+        assert g.dp_launches < q.dp_launches
