@@ -652,8 +652,8 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
 // is adopted and committed; the positions after it are looked at again in
 // the next launch.  Results are those of the sequential sweeps.
 int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_base,
-                  int32_t budget, int32_t m, const std::vector<int32_t>& kp,
-                  int32_t max_rounds, PlanResult& res) {
+                  int32_t budget, int32_t block_budget, int32_t m,
+                  const std::vector<int32_t>& kp, int32_t max_rounds, PlanResult& res) {
   DevState& d = e.d;
   const int32_t A = (int32_t)starts.size();
   for (int32_t q = 1; q < A; ++q)
@@ -737,8 +737,13 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
         scan[q] = st[q].pos + 1;
       }
     if (items.empty()) return PP_OK;
-    // speculative updates: at most `budget` updates in all, one spare slot
-    // each (budget - 1 spare slots exist)
+    // speculative updates: at most `budget` updates in all (one spare slot
+    // each; budget - 1 spare slots exist) and, beyond the starts' own
+    // updates, at most `block_budget` DP stage blocks in the launch
+    const int32_t cellsw = 64 * d.cells;
+    auto blocks_of = [&](int32_t h) { return (kp[h] + cellsw - 1) / cellsw; };
+    int32_t blocks = 0;
+    for (const Item& it : items) blocks += blocks_of(it.worker);
     int32_t spares = 0;
     auto room = [&]() { return (int32_t)items.size() < budget && spares < budget - 1; };
     for (bool grew = true; grew && room();) {
@@ -747,7 +752,12 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
         if (st[q].done) continue;
         int32_t a = scan[q];
         while (a < m && resolved_free(st[q], a)) ++a;
+        if (a < m && blocks + blocks_of(worker_at(st[q], a)) > block_budget) {
+          scan[q] = m;  // this start's next update does not fit any more
+          continue;
+        }
         if (a < m) {
+          blocks += blocks_of(worker_at(st[q], a));
           items.push_back({q, spare_base + spares++, worker_at(st[q], a), a});
           grew = true;
         }
@@ -852,7 +862,19 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   const int32_t slot_b = std::max(m, S);
   // speculative refinement (few active starts): up to kSpecChains updates
   // of one start per launch, all but the first in spare slots at the end
-  const int32_t spec_chains = env_int("PP_NO_SPEC", 0) ? 1 : kSpecChains;  // updates per launch
+  const int32_t spec_chains =  // updates per refinement launch
+      env_int("PP_NO_SPEC", 0) ? 1
+                               : std::max(1, std::min(kMaxChains, env_int("PP_SPEC_CHAINS",
+                                                                          kSpecChains)));
+  // stage blocks a speculative launch may fill: two per compute unit
+  int32_t spec_blocks = 512;
+  {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device) ==
+            hipSuccess && cus > 0)
+      spec_blocks = 2 * cus;
+    spec_blocks = env_int("PP_SPEC_BLOCKS", spec_blocks);
+  }
   const int32_t spare_base = slot_b + (sg_asked ? 4 : 0) + extra_slots;
   const int32_t slots = spare_base + (spec_chains > 1 ? spec_chains - 1 : 0);
   res.extra_slot = extra_slots > 0 ? slot_b + (sg_asked ? 4 : 0) : -1;
@@ -965,7 +987,8 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     for (int32_t a = 0; a < m; ++a)
       PP_TRY(e.update(position_set(active, a), kModeGreedy));
     if (!(o.flags & PP_F_NO_REFINE))
-      PP_TRY(refine_starts(e, active, spare_base, spec_chains, m, kp, o.max_rounds, res));
+      PP_TRY(refine_starts(e, active, spare_base, spec_chains, spec_blocks, m, kp,
+                           o.max_rounds, res));
     std::vector<int32_t> sl, wk, kk;
     for (int32_t s = lo; s < hi; ++s) {
       sl.push_back(s);

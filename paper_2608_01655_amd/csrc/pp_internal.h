@@ -11,7 +11,7 @@ namespace pp {
 constexpr int kMaxChains = 64;
 // Updates per launch in a speculative refinement sweep (all active starts
 // together; a start's speculative updates beyond the first use spare slots).
-constexpr int kSpecChains = 8;
+constexpr int kSpecChains = 16;
 // "no holder" marker of the top-1 holder state (workers are < 255).
 constexpr uint8_t kNoHolder = 255;
 
