@@ -131,7 +131,12 @@ typedef struct {
                                   worker's set changed) would find the same
                                   set and reject it; it is resolved as
                                   rejected without a sweep, so this can be
-                                  below dp_cells.  Results are unaffected. */
+                                  below dp_cells.  Speculative refinement
+                                  updates (later positions of a start swept
+                                  in the same launch, valid only if the
+                                  earlier ones are rejected) that are
+                                  discarded add their cells, so it can also
+                                  exceed dp_cells.  Results are unaffected. */
 } pp_stats;
 
 /* Number of starts the options select (see pp_options.n_starts). */
