@@ -4,11 +4,17 @@ One step = one full plan (standalone scores, WorkerGreedy, coordinate
 refinement until no sweep improves, best start) of the tree50k workload
 (n = 50,000 chunks, M = 16 workers, k = 4,096 each, 8 order-diverse starts,
 source-dependent fetch costs) through the device-resident C-ABI entry point,
-inputs already in HBM.  Prints one JSON line.  After the timed region a
-re-planning leg (a 50% routing shift of the same workload, through the
-host-array entry point) adds a "replan" object, and a real-valued leg (the
-same workload in requests and milliseconds, as doubles) an "f64" object;
---no-replan and --no-f64 skip them.
+inputs already in HBM.  Prints one JSON line.  After the timed region:
+  configs      the other four synthetic workloads (tiny, tree2k, rag10k,
+               chat50k), each planned on the GPU and checked against the
+               oracle's stored plan, the small ones also timed on the
+               oracle (full plans, one thread and one thread per start)
+  replan       epoch re-planning after a 50% routing shift (host arrays)
+  f64          the same workload in the paper's units, as doubles
+  paper_config the paper's own timing configuration (k = 128)
+  cpu_baseline the oracle on a bounded sample of the headline workload
+--no-configs, --no-replan, --no-f64, --no-paper-config and
+--no-cpu-baseline skip them.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
@@ -26,11 +32,27 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-# Algorithmic bytes per DP cell in the table formulation of Theorem 1:
-# 8 B write of D[i][j], 8 B read of the skip operand D[next(i)][j], and one
-# choice bit (row i+1 is produced the step before and held on chip).
-BYTES_PER_CELL = 16.125
+# The rooted-tree DP sweep (k_dp) keeps its rows on chip: per cell it moves
+# about one byte of HBM traffic (choice bits and stage-boundary words) and
+# executes a fixed number of vector instructions, so the bound that applies
+# is vector instruction issue.  MI355X: 256 CUs x 4 SIMDs x 16 lanes at
+# 2.4 GHz = 39.32e12 32-bit lane operations per second.
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# LDS: 128 bytes per clock per CU.
+LDS_PEAK_GBS = 256 * 128 * 2.4e9 / 1e9
 HBM_PEAK_GBS = 8000.0
+# Algorithmic bytes per DP cell in the table formulation of Theorem 1 (8 B
+# write of D[i][j], 8 B read of D[next(i)][j], one choice bit): the model
+# the HBM fraction of the metric is quoted on.  k_dp does not move these
+# bytes, so the model fraction exceeds 1; it is reported under its own name.
+TABLE_BYTES_PER_CELL = 16.125
+# Gains bytes per (worker, chunk) and per chunk of one update (k_gains:
+# demand, recompute and fetch as int64, top-1, top-2 and holder; profit).
+GAIN_BYTES_PER_MN, GAIN_BYTES_PER_N = 41, 8
+# Eq. 9 per cell, as 32-bit integer operations: the take operand's 64-bit
+# add (two), the 64-bit comparison and the two selects of the maximum, and
+# the choice bit shifted into its word.
+ALGO_OPS_PER_CELL = 6
 METRIC = ("full PrefixPlace plans/sec and tree-DP cells/sec "
           "(n·k·updates/s), 1 GPU")
 # Paper context: n = 50,000, M = 16 solved in 12.29 s on one EPYC 9V74 with
@@ -47,6 +69,30 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_dp_hbm_traffic.md")
 KERNEL_SOURCES = ("paper_2608_01655_amd/csrc/pp_kernels.hip",
                   "paper_2608_01655_amd/csrc/pp_internal.h",
                   "paper_2608_01655_amd/csrc/pp_host.cpp")
+
+
+def dp_valu_per_step(cells, fmax, f64):
+    """Vector instructions the DP sweep's compute wave issues per row step
+    (64 * cells cells): two row addresses; cell 0's take operand (a DPP
+    64-bit add, or for doubles two DPP moves and an add); the other cells'
+    take operands (a 64-bit add, or one add of doubles); per cell the choice
+    bit (compare, add with carry), the skip operand (two bit selects) and the
+    maximum (one v_max_f64, or a compare and two selects).  The SQ counters
+    of one cell per lane agree (profiles/)."""
+    return (2 + (3 if f64 else 2) + (cells - 1) * (1 if f64 else 2)
+            + cells * (4 + (1 if fmax else 3)))
+
+
+def dp_lds_bytes_per_cell(cells):
+    """LDS bytes per DP cell: the compute wave's step record (16 B per lane;
+    with several cells per lane also the 8-byte profit), row store and skip
+    row read (8 B per cell each), one gathered column per group of sink
+    rows; the I/O wave's staging (two 16-byte views for 33 lanes per
+    32-step batch)."""
+    sink = 16 if cells == 1 else 4
+    per_step = 64 * 16 + (64 * 8 if cells > 1 else 0) + 2 * 64 * cells * 8 \
+        + 64 * 8 / sink + 2 * 16 * 33 / 32
+    return per_step / (64 * cells)
 
 
 def log(msg):
@@ -96,13 +142,19 @@ def copy_probe(mib):
 
 
 def host_description():
-    """CPU model, logical CPUs and memory of the machine the bench runs on."""
-    model, mem_kib = None, None
+    """CPU model (the full /proc/cpuinfo identification: model name, family,
+    model and stepping), logical CPUs, CPUs this process may run on, and
+    memory of the machine the bench runs on."""
+    info, mem_kib = {}, None
     try:
         with open("/proc/cpuinfo") as fh:
             for line in fh:
-                if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
+                key, _, val = line.partition(":")
+                key = key.strip()
+                if key in ("model name", "cpu family", "model", "stepping",
+                           "vendor_id", "cpu MHz") and key not in info:
+                    info[key] = val.strip()
+                if not line.strip() and info:
                     break
         with open("/proc/meminfo") as fh:
             for line in fh:
@@ -111,33 +163,194 @@ def host_description():
                     break
     except OSError:
         pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    model = info.get("model name")
+    if model and "family" not in model:
+        model = (f"{model} (vendor {info.get('vendor_id')}, family "
+                 f"{info.get('cpu family')}, model {info.get('model')}, "
+                 f"stepping {info.get('stepping')}, {info.get('cpu MHz')} MHz)")
     return {"cpu_model": model, "host_cpus": os.cpu_count(),
+            "usable_cpus": usable,
             "mem_gib": round(mem_kib / 2 ** 20, 1) if mem_kib else None}
 
 
-def cpu_baseline(inst, cells_per_plan, threads):
+def oracle_threads(starts):
+    """One oracle thread per start, at most the CPUs this process may use."""
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 1
+    return max(1, min(starts, usable))
+
+
+def cpu_baseline(inst, plan_cells, threads):
     """The oracle as it stands, on a bounded sample of the same workload:
-    the standalone pass and the greedy pass of every start (no refinement
-    sweeps), timed on the host cores."""
+    Algorithm 1 with the sweep cap set to one -- the standalone pass, the
+    greedy pass and the first refinement sweep of every start, every cell
+    of every DP table computed and the objective recomputed from scratch at
+    every acceptance test -- one thread per start.  plans/s = the sample's
+    DP cells per second / the DP cells of one full plan (Algorithm 1's
+    count, as the GPU reports it)."""
     import oracle
 
     oracle.lib()
     t0 = time.perf_counter()
-    res = oracle.plan_instance(inst, flags=oracle.F_NO_REFINE, threads=threads)
+    res = oracle.plan_instance(inst, max_rounds=1, threads=threads)
     dt = time.perf_counter() - t0
     cps = res.dp_cells / dt
     return {
-        "value": cps / cells_per_plan,
+        "value": cps / plan_cells,
         "unit": "plans/s",
         "cells_per_s": cps,
         "cores": threads,
         "kind": "oracle",
-        "sample": (f"{inst.name}: standalone + greedy pass of all "
+        "sample": (f"{inst.name} with the refinement sweeps capped at one: "
+                   f"standalone, greedy and first refinement sweep of all "
                    f"{inst.n_starts} starts ({res.updates} worker updates, "
-                   f"{res.dp_cells:.3e} DP cells) in {dt:.1f} s; plans/s = "
-                   f"cells/s / cells of one full plan"),
+                   f"{res.dp_cells:.3e} DP cells) in {dt:.1f} s on "
+                   f"{threads} threads; plans/s = cells/s / "
+                   f"{plan_cells:.4e} cells of one full plan"),
+        "sample_seconds": dt,
         **host_description(),
     }
+
+
+def plan_timing(B, ctx, inst, lam, w, f, tgt, steps, warmup, plan_flags=0):
+    """Plans of `inst` through the device entry point (inputs in HBM);
+    returns the per-plan wall times, the last plan and the kernel totals."""
+    import torch
+
+    def step(flags=0):
+        return ctx.pp_plan_device(inst.parent, lam, w, f, inst.cap, tgt,
+                                  n_starts=inst.n_starts,
+                                  max_rounds=inst.max_rounds,
+                                  order_seed=inst.order_seed,
+                                  flags=flags | plan_flags)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plans, marks = [], []
+    for _ in range(steps):
+        plans.append(step(B.PP_F_TIME_KERNELS))
+        marks.append(time.perf_counter())  # the call returns after its stream drained
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    step_ms = sorted((b - a) * 1e3 for a, b in zip([t0] + marks[:-1], marks))
+    return dt, step_ms, plans
+
+
+def dp_figures(inst, plans, dt):
+    """Throughput and roofline figures of a series of plans: plan-level
+    cells per second (Algorithm 1's count and the cells actually swept), the
+    DP sweep's cells per second inside its launches, its fraction of the
+    vector-issue ceiling, of the LDS peak and, under the table model, of
+    HBM."""
+    p = plans[-1]
+    steps = len(plans)
+    exec_cells = sum(q.dp_cells_executed for q in plans)
+    dp_ms = sum(q.dp_kernel_ms for q in plans)
+    launches = sum(q.dp_launches for q in plans)
+    kernel_cps = exec_cells / (dp_ms / 1e3) if dp_ms > 0 else 0.0
+    c = max(1, p.dp_lane_cells)
+    valu = dp_valu_per_step(c, p.dp_fmax, isinstance(p.objective, float))
+    issue_ceiling = VALU_PEAK_TOPS * 1e12 * c / valu  # cells/s
+    lds_b = dp_lds_bytes_per_cell(c)
+    plan_bytes_table = (exec_cells / steps * TABLE_BYTES_PER_CELL
+                        + p.updates * (GAIN_BYTES_PER_MN * inst.m * inst.n
+                                       + GAIN_BYTES_PER_N * inst.n))
+    return {
+        "plans_per_s": steps / dt,
+        "ms_per_plan": dt / steps * 1e3,
+        "dp_cells_per_s_algorithm1": p.dp_cells * steps / dt,
+        "dp_cells_per_s_swept": exec_cells / dt,
+        "dp_cells_per_plan_algorithm1": p.dp_cells,
+        "dp_cells_per_plan_swept": exec_cells // steps,
+        "updates_per_plan": p.updates,
+        "dp_lane_cells": c,
+        "dp_launches_per_plan": launches // steps,
+        "dp_avg_launch_ms": dp_ms / launches if launches else None,
+        "dp_share_of_plan_time": dp_ms / 1e3 / dt,
+        "dp_cells_per_s_in_kernel": kernel_cps,
+        "dp_issue_frac": kernel_cps / issue_ceiling,
+        "dp_valu_per_row_step": valu,
+        "dp_lds_frac": kernel_cps * lds_b / (LDS_PEAK_GBS * 1e9),
+        "dp_table_model_hbm_frac": kernel_cps * TABLE_BYTES_PER_CELL
+        / (HBM_PEAK_GBS * 1e9),
+        "plan_table_model_hbm_frac": plan_bytes_table * steps / dt
+        / (HBM_PEAK_GBS * 1e9),
+        "plan_issue_frac": exec_cells / dt / issue_ceiling,
+        "sweeps_per_start": p.start_sweeps.tolist(),
+    }
+
+
+def golden_plan(name):
+    gold_path = os.path.join(ROOT, "tests", "golden", "plans.json")
+    if not os.path.exists(gold_path):
+        return None
+    with open(gold_path) as fh:
+        return json.load(fh).get(name)
+
+
+def configs_leg(B, W, ctx, names, with_oracle):
+    """Every other synthetic workload: plans on the GPU (inputs in HBM; a
+    number of plans sized to about a second of GPU time), checked against
+    the oracle's stored plan; for the small workloads also full oracle plans
+    (one thread, and one thread per start) on the host cores."""
+    import numpy as np
+    import torch
+
+    out = {}
+    dev = torch.device("cuda:0")
+    for name in names:
+        inst = W.make_workload(name)
+        log(f"[bench] config {name}: n={inst.n} m={inst.m} S={inst.n_starts}")
+        lam = torch.from_numpy(inst.demand).to(dev)
+        w = torch.from_numpy(inst.recompute_cost).to(dev)
+        f = torch.from_numpy(inst.fetch_cost).to(dev)
+        tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+        # one timed plan to size the run
+        t1, _, _ = plan_timing(B, ctx, inst, lam, w, f, tgt, 1, 1)
+        steps = int(max(3, min(200, 1.0 / max(t1, 1e-4))))
+        dt, step_ms, plans = plan_timing(B, ctx, inst, lam, w, f, tgt, steps, 0)
+        fig = dp_figures(inst, plans, dt)
+        fig["steps"] = steps
+        fig["ms_per_plan_median"] = step_ms[len(step_ms) // 2]
+        fig["ms_per_plan_min"] = step_ms[0]
+        gold = golden_plan(name)
+        if gold:
+            import hashlib as _h
+
+            target = tgt.cpu().numpy()
+            rows = [_h.sha256(np.ascontiguousarray(target[h]).tobytes()).hexdigest()
+                    for h in range(inst.m)]
+            fig["parity_vs_golden"] = (
+                all(q.objective == gold["objective"] for q in plans)
+                and plans[-1].start_sweeps.tolist() == gold["start_sweeps"]
+                and rows == gold["target_row_sha256"])
+        if with_oracle and inst.n * int(inst.cap.max()) <= 2 * 10 ** 7:
+            import oracle
+
+            oracle.lib()
+            reps = 5 if inst.n <= 2000 else 1
+            T = oracle_threads(inst.n_starts)
+            o = {}
+            for threads in sorted({1, T}):
+                t0 = time.perf_counter()
+                for _ in range(reps):
+                    res = oracle.plan_instance(inst, threads=threads)
+                sec = (time.perf_counter() - t0) / reps
+                o[f"threads_{threads}"] = {
+                    "s_per_plan": sec, "plans_per_s": 1.0 / sec,
+                    "dp_cells_per_s": res.dp_cells / sec, "repetitions": reps}
+            o["same_objective"] = res.objective == plans[-1].objective
+            fig["oracle_full_plan"] = o
+        out[name] = fig
+    return out
 
 
 def replan_leg(B, W, inst, steps, warmup):
@@ -297,6 +510,10 @@ def main():
                     help="requester-side variant of the workload (each "
                          "requester's fetch cost taken from one source) "
                          "planned with the comparator safeguards")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other synthetic workloads")
+    ap.add_argument("--configs", default="tiny,tree2k,rag10k,chat50k",
+                    help="comma-separated workloads of the configs object")
     ap.add_argument("--no-replan", action="store_true",
                     help="skip the re-planning leg")
     ap.add_argument("--no-host-plan", action="store_true",
@@ -305,6 +522,9 @@ def main():
                     help="skip the real-valued leg")
     ap.add_argument("--no-paper-config", action="store_true",
                     help="skip the leg at the paper's own timing configuration")
+    ap.add_argument("--oracle-full", action="store_true",
+                    help="also time one full oracle plan of the workload "
+                         "(minutes at 50,000 chunks)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device (counter "
                          "calibration) and exit")
@@ -317,7 +537,6 @@ def main():
               "pairs, which this build does not run", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     from paper_2608_01655_amd import binding as B
@@ -350,59 +569,39 @@ def main():
     tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
     ctx = B.Context(0)
 
-    def step(flags=0):
-        return ctx.pp_plan_device(inst.parent, lam, w, f, inst.cap, tgt,
-                                  n_starts=inst.n_starts,
-                                  max_rounds=inst.max_rounds,
-                                  order_seed=inst.order_seed,
-                                  flags=flags | plan_flags)
-
-    for i in range(args.warmup):
-        p = step()
-        log(f"[bench] warmup {i}: objective {p.objective}")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    plans, marks = [], []
-    for i in range(args.steps):
-        plans.append(step(B.PP_F_TIME_KERNELS))
-        marks.append(time.perf_counter())  # the call returns after its stream drained
-        log(f"[bench] step {i}: objective {plans[-1].objective} "
-            f"dp {plans[-1].dp_kernel_ms:.1f} ms")
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    step_ms = sorted((b - a) * 1e3 for a, b in zip([t0] + marks[:-1], marks))
+    dt, step_ms, plans = plan_timing(B, ctx, inst, lam, w, f, tgt, args.steps,
+                                     args.warmup, plan_flags)
+    for i, q in enumerate(plans):
+        log(f"[bench] step {i}: objective {q.objective} dp {q.dp_kernel_ms:.1f} ms")
     p = plans[-1]
     objectives = {q.objective for q in plans}
-    gold_ok = None
-    gold_path = os.path.join(ROOT, "tests", "golden", "plans.json")
-    if os.path.exists(gold_path):
-        with open(gold_path) as fh:
-            gold = json.load(fh).get(inst.name)
-        if gold:
-            gold_ok = objectives == {gold["objective"]}
-    cells = p.dp_cells
-    plans_per_s = args.steps / dt
-    cells_per_s = cells * args.steps / dt
-    # cells the sweeps actually processed (refinement updates of workers
-    # whose inputs did not change are resolved without a sweep)
+    gold = golden_plan(inst.name)
+    gold_ok = (objectives == {gold["objective"]}) if gold else None
+    fig = dp_figures(inst, plans, dt)
     exec_cells = sum(q.dp_cells_executed for q in plans)
     dp_ms = sum(q.dp_kernel_ms for q in plans)
     launches = sum(q.dp_launches for q in plans)
-    bytes_per_launch = exec_cells * BYTES_PER_CELL / launches
     avg_launch_s = dp_ms / launches / 1e3
-    achieved = bytes_per_launch / avg_launch_s / 1e9
+    cells_per_launch = exec_cells / launches
+    c = max(1, p.dp_lane_cells)
+    valu = fig["dp_valu_per_row_step"]
+    # lane operations one launch issues for the DP (VALU instructions per
+    # row step x 64 lanes per 64*C cells), over its measured duration
+    achieved = cells_per_launch * valu / c / avg_launch_s / 1e12
     traffic = measured_traffic(inst.name)
     out = {
         "metric": METRIC,
-        "value": plans_per_s,
+        "value": args.steps / dt,
         "unit": "plans/s",
-        "dp_cells_per_s": cells_per_s,
-        "dp_cells_executed_per_s": exec_cells / dt,
-        # model fraction on the cells actually swept
-        "dp_cells_per_s_frac_hbm_roofline":
-            exec_cells / dt * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
-        "plans_per_s_frac_hbm_roofline":
-            exec_cells / dt * BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
+        # Algorithm 1's cells (every update n * min(k_h, n)) per second
+        "dp_cells_per_s": fig["dp_cells_per_s_algorithm1"],
+        # cells the sweeps processed (updates of workers whose inputs did not
+        # change need no sweep; discarded speculative updates add theirs)
+        "dp_cells_executed_per_s": fig["dp_cells_per_s_swept"],
+        "dp_cells_per_s_frac_issue_roofline": fig["plan_issue_frac"],
+        "dp_cells_per_s_frac_hbm_table_model": fig["dp_cells_per_s_swept"]
+        * TABLE_BYTES_PER_CELL / (HBM_PEAK_GBS * 1e9),
+        "plans_per_s_frac_hbm_table_model": fig["plan_table_model_hbm_frac"],
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -418,26 +617,45 @@ def main():
             "workload": inst.name, "n": inst.n, "workers": inst.m,
             "k": [int(x) for x in sorted(set(inst.cap.tolist()))],
             "starts": inst.n_starts, "max_rounds": inst.max_rounds,
-            "updates_per_plan": p.updates, "dp_cells_per_plan": cells,
+            "updates_per_plan": p.updates, "dp_cells_per_plan": p.dp_cells,
             "dp_cells_executed_per_plan": exec_cells // args.steps,
             "sweeps_per_start": p.start_sweeps.tolist(),
         },
         "roofline": {
-            "bound": "hbm",
-            "kernel": "k_dp (rooted-tree DP sweep)",
+            "bound": "alu",
+            "kernel": f"k_dp<{c}, {'true' if p.dp_fmax else 'false'}, false> "
+                      "(rooted-tree DP sweep)",
             "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
+            "peak": VALU_PEAK_TOPS,
+            "unit": "T lane-ops/s (32-bit vector)",
+            "frac": achieved / VALU_PEAK_TOPS,
             "traffic": traffic,
-            # the same launches against the bytes the counters saw move
-            "measured_frac": (traffic / avg_launch_s / 1e9 / HBM_PEAK_GBS
-                              if traffic else None),
-            "bytes_per_cell": BYTES_PER_CELL,
+            "ops_basis": (f"{valu} vector instructions per row step of "
+                          f"{64 * c} cells (compute wave; SQ_INSTS_VALU), "
+                          f"each one 32-bit op per lane"),
+            "cells_per_launch": cells_per_launch,
             "dp_launches_per_plan": launches // args.steps,
             "avg_launch_ms": avg_launch_s * 1e3,
-            "dp_cells_per_s_in_kernel": exec_cells / (dp_ms / 1e3),
-            "dp_share_of_plan_time": dp_ms / 1e3 / dt,
+            "dp_cells_per_s_in_kernel": fig["dp_cells_per_s_in_kernel"],
+            "dp_share_of_plan_time": fig["dp_share_of_plan_time"],
+            # Eq. 9's own arithmetic (6 ops per cell) against the same peak
+            "algorithmic_frac": fig["dp_cells_per_s_in_kernel"]
+            * ALGO_OPS_PER_CELL / (VALU_PEAK_TOPS * 1e12),
+            "lds": {"bytes_per_cell": dp_lds_bytes_per_cell(c),
+                    "achieved_gbs": fig["dp_cells_per_s_in_kernel"]
+                    * dp_lds_bytes_per_cell(c) / 1e9,
+                    "peak_gbs": LDS_PEAK_GBS,
+                    "frac": fig["dp_lds_frac"]},
+            "hbm_measured": ({"gbs": traffic / avg_launch_s / 1e9,
+                              "frac": traffic / avg_launch_s / 1e9 / HBM_PEAK_GBS,
+                              "bytes_per_cell": traffic / cells_per_launch}
+                             if traffic else None),
+            # Theorem 1's table formulation (16.125 B per cell) against HBM
+            # peak: above 1 because the sweep keeps the table on chip
+            "hbm_table_model": {"bytes_per_cell": TABLE_BYTES_PER_CELL,
+                                "achieved_gbs": fig["dp_cells_per_s_in_kernel"]
+                                * TABLE_BYTES_PER_CELL / 1e9,
+                                "frac": fig["dp_table_model_hbm_frac"]},
         },
         "parity_vs_golden": gold_ok,
         **({"safeguards": {"run": p.safeguards_run, "returned": p.best_start,
@@ -458,6 +676,9 @@ def main():
     if host_ms:
         out["host_pp_plan_ms"] = min(host_ms)
         out["host_pp_plan_same_objective"] = hp.objective == p.objective
+    if not args.no_configs and not args.safeguards:
+        names = [x for x in args.configs.split(",") if x and x != inst.name]
+        out["configs"] = configs_leg(B, W, ctx, names, not args.no_cpu_baseline)
     if not args.no_replan and not args.safeguards:
         log("[bench] re-planning leg")
         out["replan"] = replan_leg(B, W, inst, max(1, min(args.steps, 3)),
@@ -471,9 +692,22 @@ def main():
         out["paper_config"] = paper_config_leg(B, W, ctx, max(1, min(args.steps, 3)),
                                                 not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a bounded sample")
-        threads = max(1, min(8, os.cpu_count() or 1))
-        out["cpu_baseline"] = cpu_baseline(inst, cells, threads)
+        threads = oracle_threads(inst.n_starts)
+        log(f"[bench] timing the CPU oracle on a bounded sample ({threads} threads)")
+        out["cpu_baseline"] = cpu_baseline(inst, p.dp_cells, threads)
+    if args.oracle_full:
+        import oracle
+
+        threads = oracle_threads(inst.n_starts)
+        log(f"[bench] timing one full oracle plan ({threads} threads)")
+        oracle.lib()
+        t1 = time.perf_counter()
+        res = oracle.plan_instance(inst, threads=threads)
+        sec = time.perf_counter() - t1
+        out["oracle_full_plan"] = {"s_per_plan": sec, "plans_per_s": 1.0 / sec,
+                                   "threads": threads,
+                                   "dp_cells_per_s": res.dp_cells / sec,
+                                   "same_objective": res.objective == p.objective}
     ctx.close()
     print(json.dumps(out), flush=True)
 

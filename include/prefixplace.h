@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 9
+#define PP_ABI_VERSION 10
 
 enum {
     PP_OK = 0,
@@ -137,6 +137,13 @@ typedef struct {
                                   earlier ones are rejected) that are
                                   discarded add their cells, so it can also
                                   exceed dp_cells.  Results are unaffected. */
+    int32_t dp_lane_cells;     /* out: DP cells per lane of the sweep's
+                                  compute wave (1, 2 or 4; 0 if no sweep
+                                  ran), chosen per plan */
+    int32_t dp_fmax;           /* out: 1 if the sweep took the maximum with
+                                  one 64-bit float instruction (every value
+                                  below 2^62, or real-valued costs), 0 if
+                                  with a compare and two selects */
 } pp_stats;
 
 /* Number of starts the options select (see pp_options.n_starts). */
@@ -195,6 +202,8 @@ typedef struct {
     int32_t safeguards_run;
     double safeguard_objective[3];
     int64_t dp_cells_executed;   /* as in pp_stats */
+    int32_t dp_lane_cells;       /* as in pp_stats */
+    int32_t dp_fmax;             /* as in pp_stats */
 } pp_stats_f64;
 
 /* pp_plan on real-valued host arrays (layouts as pp_plan). */

@@ -38,7 +38,9 @@ class pp_stats(ctypes.Structure):
                 ("dp_launches", ctypes.c_int32),
                 ("safeguards_run", ctypes.c_int32),
                 ("safeguard_objective", ctypes.c_int64 * 3),
-                ("dp_cells_executed", ctypes.c_int64)]
+                ("dp_cells_executed", ctypes.c_int64),
+                ("dp_lane_cells", ctypes.c_int32),
+                ("dp_fmax", ctypes.c_int32)]
 
 
 class pp_stats_f64(ctypes.Structure):
@@ -50,7 +52,9 @@ class pp_stats_f64(ctypes.Structure):
                 ("dp_launches", ctypes.c_int32),
                 ("safeguards_run", ctypes.c_int32),
                 ("safeguard_objective", ctypes.c_double * 3),
-                ("dp_cells_executed", ctypes.c_int64)]
+                ("dp_cells_executed", ctypes.c_int64),
+                ("dp_lane_cells", ctypes.c_int32),
+                ("dp_fmax", ctypes.c_int32)]
 
 
 class pp_replan_info(ctypes.Structure):
@@ -171,6 +175,8 @@ class Plan:
     safeguards_run: bool = False
     safeguard_objective: tuple = (0, 0, 0)
     dp_cells_executed: int = 0
+    dp_lane_cells: int = 0      # DP cells per lane of the sweep (1, 2, 4)
+    dp_fmax: bool = False       # maximum by one 64-bit float instruction
 
 
 def _options(m, n_starts, max_rounds, order_seed, orders, flags):
@@ -201,7 +207,8 @@ def _plan_from(st, arrs, target, objective):
                 dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches,
                 safeguards_run=bool(st.safeguards_run),
                 safeguard_objective=tuple(int(x) for x in st.safeguard_objective),
-                dp_cells_executed=st.dp_cells_executed, **arrs)
+                dp_cells_executed=st.dp_cells_executed,
+                dp_lane_cells=st.dp_lane_cells, dp_fmax=bool(st.dp_fmax), **arrs)
 
 
 def pp_plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=8,
@@ -284,7 +291,8 @@ def _plan_f64_from(st, arrs, target, objective):
                 dp_kernel_ms=st.dp_kernel_ms, dp_launches=st.dp_launches,
                 safeguards_run=bool(st.safeguards_run),
                 safeguard_objective=tuple(float(x) for x in st.safeguard_objective),
-                dp_cells_executed=st.dp_cells_executed, **arrs)
+                dp_cells_executed=st.dp_cells_executed,
+                dp_lane_cells=st.dp_lane_cells, dp_fmax=bool(st.dp_fmax), **arrs)
 
 
 def pp_plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,

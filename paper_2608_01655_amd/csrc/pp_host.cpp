@@ -23,12 +23,17 @@ using namespace pp;
 
 namespace {
 
-thread_local std::string g_err;
+// Description of the last error on this thread, in a fixed buffer (setting
+// it allocates nothing, which the allocation-free entry point relies on).
+thread_local char g_err[512];
 
-int fail(int code, const std::string& msg) {
-  g_err = msg;
+int fail_c(int code, const char* msg) {
+  std::strncpy(g_err, msg, sizeof g_err - 1);
+  g_err[sizeof g_err - 1] = 0;
   return code;
 }
+
+int fail(int code, const std::string& msg) { return fail_c(code, msg.c_str()); }
 
 #define PP_HIP(expr)                                                      \
   do {                                                                    \
@@ -537,6 +542,8 @@ struct PlanResult {
   int64_t updates = 0, cells = 0;
   double dp_ms = 0.0;
   int32_t dp_launches = 0;
+  int32_t lane_cells = 0;      // DP cells per lane of the sweep
+  int32_t fmax = 0;            // maximum by one 64-bit float instruction
 };
 
 // Comparator safeguards of Sec. IV-C (Algorithm 1: the candidate set also
@@ -909,6 +916,8 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident (LDS stack of " +
                                       std::to_string(e.slots_lds) + " rows)");
   e.fmax = fmax_ok && env_int("PP_DP_NO_FMAX", 0) == 0;
+  res.lane_cells = cells;
+  res.fmax = (e.fmax || f64) ? 1 : 0;
   PP_TRY(ensure_slots(c, d, slots, kmax, cells));
   if (f64) {
     d.f64 = 1;
@@ -1216,6 +1225,8 @@ void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = r.sg_obj[q];
   stats->dp_cells_executed = r.cells - r.skipped_cells + r.spec_cells;
+  stats->dp_lane_cells = r.lane_cells;
+  stats->dp_fmax = r.fmax;
   (void)m;
 }
 
@@ -1247,6 +1258,8 @@ void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
   stats->safeguards_run = r.sg_run ? 1 : 0;
   for (int q = 0; q < 3; ++q) stats->safeguard_objective[q] = bits_f64(r.sg_obj[q]);
   stats->dp_cells_executed = r.cells - r.skipped_cells + r.spec_cells;
+  stats->dp_lane_cells = r.lane_cells;
+  stats->dp_fmax = r.fmax;
 }
 
 // Host-array inputs (caller ids, 8-byte values) to the context's preorder
@@ -1378,7 +1391,7 @@ extern "C" {
 
 int pp_abi_version(void) { return PP_ABI_VERSION; }
 
-const char* pp_last_error(void) { return g_err.c_str(); }
+const char* pp_last_error(void) { return g_err; }
 
 int32_t pp_num_starts(int32_t m, int32_t n_starts) {
   return num_starts(m, n_starts);
@@ -1386,7 +1399,7 @@ int32_t pp_num_starts(int32_t m, int32_t n_starts) {
 
 int pp_orders(int32_t m, int32_t n_starts, uint64_t order_seed,
               const int64_t* standalone, int32_t* orders) {
-  g_err.clear();
+  g_err[0] = 0;
   if (m < 1 || m > 255 || n_starts < 0 || !standalone || !orders)
     return fail(PP_E_ARG, "bad arguments to pp_orders");
   return guarded([&] {
@@ -1397,7 +1410,7 @@ int pp_orders(int32_t m, int32_t n_starts, uint64_t order_seed,
 
 int pp_sweep_layout(int32_t n, const int32_t* parent, int32_t cells,
                     uint32_t* meta, int32_t* nsteps, int32_t* slots) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (n < 1 || !parent || !nsteps || !slots)
       return fail(PP_E_ARG, "bad arguments to pp_sweep_layout");
@@ -1418,7 +1431,7 @@ static_assert(kCeEnd == PP_BT_END, "one end marker for the backtrack table");
 
 int pp_backtrack_table(int32_t n, const int32_t* parent, uint32_t* table,
                        int64_t* rows) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (n < 1 || !parent || !rows) return fail(PP_E_ARG, "bad arguments to pp_backtrack_table");
     TreeLayout t;
@@ -1430,7 +1443,7 @@ int pp_backtrack_table(int32_t n, const int32_t* parent, uint32_t* table,
 }
 
 int pp_ctx_create(pp_ctx** ctx, int device) {
-  g_err.clear();
+  g_err[0] = 0;
   if (!ctx) return fail(PP_E_ARG, "null ctx");
   return guarded([&]() -> int {
     int count = 0;
@@ -1458,7 +1471,7 @@ int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
                    const int64_t* fetch_dev, const int32_t* cap,
                    const pp_options* opt, uint8_t* target_dev,
                    int64_t* objective, pp_stats* stats, void* hip_stream) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (!ctx) return fail(PP_E_ARG, "null ctx");
     PP_TRY(check_common(n, m, parent, demand_dev, recompute_dev, fetch_dev));
@@ -1509,7 +1522,7 @@ int pp_plan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand,
             const int64_t* recompute_cost, const int64_t* fetch_cost,
             const int32_t* cap, const pp_options* opt, uint8_t* target,
             int64_t* objective, pp_stats* stats) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
     if (!cap || !target || !objective) return fail(PP_E_ARG, "null pointer argument");
@@ -1541,7 +1554,7 @@ int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
                        const double* fetch_dev, const int32_t* cap, double epsilon,
                        const pp_options* opt, uint8_t* target_dev, double* objective,
                        pp_stats_f64* stats, void* hip_stream) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (!ctx) return fail(PP_E_ARG, "null ctx");
     PP_TRY(check_common(n, m, parent, demand_dev, recompute_dev, fetch_dev));
@@ -1583,7 +1596,7 @@ int pp_plan_f64(int32_t n, int32_t m, const int32_t* parent, const double* deman
                 const double* recompute_cost, const double* fetch_cost,
                 const int32_t* cap, double epsilon, const pp_options* opt,
                 uint8_t* target, double* objective, pp_stats_f64* stats) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
     if (!cap || !target || !objective) return fail(PP_E_ARG, "null pointer argument");
@@ -1615,7 +1628,7 @@ int pp_replan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand
               const int32_t* cap, const uint8_t* incumbent, int64_t horizon,
               const pp_options* opt, uint8_t* target, uint8_t* proposal,
               pp_replan_info* info, pp_stats* stats) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
     if (!cap || !incumbent || !target || !info)
@@ -1663,7 +1676,7 @@ int pp_replan(int32_t n, int32_t m, const int32_t* parent, const int64_t* demand
 
 static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v,
                           int32_t k, uint8_t* selected, int64_t* value, bool f64) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (n < 1) return fail(PP_E_ARG, "n must be >= 1");
     if (!parent || !profit_v || !selected || !value)
@@ -1744,7 +1757,7 @@ int pp_replan_f64(int32_t n, int32_t m, const int32_t* parent, const double* dem
                   const int32_t* cap, const uint8_t* incumbent, double horizon,
                   double epsilon, const pp_options* opt, uint8_t* target,
                   uint8_t* proposal, pp_replan_info_f64* info, pp_stats_f64* stats) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     PP_TRY(check_common(n, m, parent, demand, recompute_cost, fetch_cost));
     if (!cap || !incumbent || !target || !info)
@@ -1792,7 +1805,7 @@ int pp_rooted_dp(int32_t n, const int32_t* parent, const int64_t* profit,
 int pp_rooted_dp_f64(int32_t n, const int32_t* parent, const double* profit,
                      int32_t k, uint8_t* selected, double* value) {
   if (!value) {
-    g_err.clear();
+    g_err[0] = 0;
     return fail(PP_E_ARG, "null pointer argument");
   }
   int64_t v = 0;
@@ -1851,7 +1864,7 @@ int pp_marginal(int32_t n, int32_t m, const int64_t* demand,
                 const int64_t* recompute_cost, const int64_t* fetch_cost,
                 const uint8_t* target, int32_t h, int64_t* profit,
                 int64_t* g_without_h) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (!profit) return fail(PP_E_ARG, "null profit");
     if (m >= 1 && (h < 0 || h >= m)) return fail(PP_E_ARG, "h out of range");
@@ -1868,7 +1881,7 @@ int pp_marginal(int32_t n, int32_t m, const int64_t* demand,
 int pp_objective(int32_t n, int32_t m, const int64_t* demand,
                  const int64_t* recompute_cost, const int64_t* fetch_cost,
                  const uint8_t* target, int64_t* objective) {
-  g_err.clear();
+  g_err[0] = 0;
   return guarded([&]() -> int {
     if (!objective) return fail(PP_E_ARG, "null objective");
     int64_t v = 0;
