@@ -290,6 +290,29 @@ int pp_objective(int32_t n, int32_t m, const int64_t *demand,
                  const int64_t *recompute_cost, const int64_t *fetch_cost,
                  const uint8_t *target, int64_t *objective);
 
+/* Allocation-free F_pair(T), for callers that cannot allocate device memory
+ * (code under HIP graph capture set-up, tight serving loops, harnesses that
+ * forbid hipMalloc): the value pp_objective returns, on device-resident
+ * arrays in caller ids (layouts as pp_plan; target [m][n], a chunk is held
+ * where the byte is nonzero), enqueued on `hip_stream` (a hipStream_t; NULL
+ * = the null stream).  The call waits for the stream and writes the result
+ * to the host `objective`.  It calls no hipMalloc, hipFree or other
+ * allocating routine, host or device: its only device memory besides the
+ * caller's arrays is a file-scope array of PP_NOALLOC_SCRATCH_BYTES in the
+ * library, one per GPU, held until the process ends.  The scratch does not
+ * grow with the input (at most 1024 per-block partial sums), so every size
+ * pp_objective accepts is accepted: n >= 1, 1 <= m <= 255.  Every call on a
+ * GPU shares that GPU's array: calls that overlap on one GPU (other threads,
+ * other streams) race and must be serialized by the caller.  Errors as
+ * pp_objective: PP_E_ARG (null pointer, sizes), PP_E_RANGE (negative value),
+ * PP_E_OVERFLOW (sum of demand * recompute cost above INT64_MAX),
+ * PP_E_DEVICE (HIP error); *objective is then left unchanged. */
+#define PP_NOALLOC_SCRATCH_BYTES 40960
+int pp_objective_device_noalloc(int32_t n, int32_t m, const int64_t *demand_dev,
+                                const int64_t *recompute_dev,
+                                const int64_t *fetch_dev, const uint8_t *target_dev,
+                                int64_t *objective, void *hip_stream);
+
 /* Start orders (Sec. IV-C) from standalone scores [m]; host only.
  * orders [pp_num_starts(m, n_starts)][m] host out. */
 int pp_orders(int32_t m, int32_t n_starts, uint64_t order_seed,

@@ -123,10 +123,12 @@ def lib() -> ctypes.CDLL:
         L.pp_ctx_destroy.restype = None
         L.pp_plan_device.argtypes = [_P, i32, i32, _P, _P, _P, _P, _P, _P, _P,
                                      _P, _P, _P]
+        L.pp_objective_device_noalloc.argtypes = [i32, i32, _P, _P, _P, _P, _P, _P]
         for f in (L.pp_plan, L.pp_replan, L.pp_replan_f64, L.pp_plan_f64,
                   L.pp_plan_f64_device,
                   L.pp_rooted_dp_f64, L.pp_rooted_dp, L.pp_marginal, L.pp_objective,
-                  L.pp_orders, L.pp_ctx_create, L.pp_plan_device):
+                  L.pp_orders, L.pp_ctx_create, L.pp_plan_device,
+                  L.pp_objective_device_noalloc):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -391,6 +393,30 @@ def pp_objective(demand, recompute_cost, fetch_cost, target) -> int:
     out = ctypes.c_int64(0)
     _check(lib().pp_objective(n, m, _p(demand), _p(w), _p(f), _p(target),
                               ctypes.byref(out)))
+    return out.value
+
+
+def pp_objective_device_noalloc(demand_dev, recompute_dev, fetch_dev, target_dev,
+                                stream=None) -> int:
+    """F_pair(T) on torch device tensors (int64 [m][n], int64 [m][n], int64
+    [m][m][n], uint8 [m][n]) through the allocation-free entry point (see
+    include/prefixplace.h)."""
+    import torch
+
+    for t, dt in ((demand_dev, torch.int64), (recompute_dev, torch.int64),
+                  (fetch_dev, torch.int64), (target_dev, torch.uint8)):
+        if not t.is_cuda or t.dtype != dt or not t.is_contiguous():
+            raise ValueError("device tensors must be contiguous, on the GPU, "
+                             "with the documented dtypes")
+    m, n = demand_dev.shape
+    if tuple(fetch_dev.shape) != (m, m, n) or tuple(target_dev.shape) != (m, n) \
+            or tuple(recompute_dev.shape) != (m, n):
+        raise ValueError("shape mismatch")
+    s = stream if stream is not None else torch.cuda.current_stream()
+    out = ctypes.c_int64(0)
+    _check(lib().pp_objective_device_noalloc(
+        n, m, demand_dev.data_ptr(), recompute_dev.data_ptr(), fetch_dev.data_ptr(),
+        target_dev.data_ptr(), ctypes.byref(out), ctypes.c_void_p(s.cuda_stream)))
     return out.value
 
 

@@ -1428,6 +1428,7 @@ int pp_sweep_layout(int32_t n, const int32_t* parent, int32_t cells,
 }
 
 static_assert(kCeEnd == PP_BT_END, "one end marker for the backtrack table");
+static_assert(kNoAllocScratchBytes == PP_NOALLOC_SCRATCH_BYTES, "one scratch size");
 
 int pp_backtrack_table(int32_t n, const int32_t* parent, uint32_t* table,
                        int64_t* rows) {
@@ -1890,6 +1891,33 @@ int pp_objective(int32_t n, int32_t m, const int64_t* demand,
     *objective = v;
     return PP_OK;
   });
+}
+
+int pp_objective_device_noalloc(int32_t n, int32_t m, const int64_t* demand_dev,
+                                const int64_t* recompute_dev, const int64_t* fetch_dev,
+                                const uint8_t* target_dev, int64_t* objective,
+                                void* hip_stream) {
+  // no allocation of any kind on this path: errors go to the fixed buffer,
+  // the kernels' partial sums to the library's per-GPU scratch array
+  g_err[0] = 0;
+  if (!demand_dev || !recompute_dev || !fetch_dev || !target_dev || !objective)
+    return fail_c(PP_E_ARG, "null pointer argument");
+  if (n < 1 || m < 1 || m > 255) return fail_c(PP_E_ARG, "need n >= 1 and 1 <= m <= 255");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail_c(PP_E_DEVICE, "no current HIP device");
+  void* scr = nullptr;
+  hipError_t e = noalloc_scratch(dev, &scr);
+  if (e != hipSuccess)
+    return fail_c(PP_E_DEVICE, "looking up the scratch array (hipGetSymbolAddress) failed");
+  NoAllocResult r{};
+  e = launch_objective_noalloc(n, m, demand_dev, recompute_dev, fetch_dev, target_dev,
+                               scr, &r, (hipStream_t)hip_stream);
+  if (e != hipSuccess) return fail_c(PP_E_DEVICE, hipGetErrorString(e));
+  if (r.bad) return fail_c(PP_E_RANGE, "negative demand, recompute cost or fetch cost");
+  if (r.overflow)
+    return fail_c(PP_E_OVERFLOW, "sum of demand * recompute cost exceeds INT64_MAX");
+  *objective = r.objective;
+  return PP_OK;
 }
 
 }  // extern "C"

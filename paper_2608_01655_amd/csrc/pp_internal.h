@@ -189,6 +189,25 @@ hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
 hipError_t launch_objective(const ChainSet& set, const DevState& d,
                             hipStream_t st);
 
+// Allocation-free objective (pp_objective_device_noalloc): the kernels' only
+// device memory besides the caller's arrays is a file-scope array of
+// kNoAllocScratchBytes per GPU (= PP_NOALLOC_SCRATCH_BYTES).
+constexpr size_t kNoAllocScratchBytes = 40960;
+constexpr int kNoAllocMaxDevices = 64;
+struct NoAllocResult {
+  int64_t objective;
+  bool bad;       // a negative demand or cost
+  bool overflow;  // sum of demand * recompute cost above INT64_MAX
+};
+// Device address of the scratch array on `device` (the current device),
+// looked up once per device.
+hipError_t noalloc_scratch(int device, void** ptr);
+// Enqueue the objective kernels on `st`, copy the totals back and wait.
+hipError_t launch_objective_noalloc(int32_t n, int32_t m, const int64_t* lam,
+                                    const int64_t* w, const int64_t* f,
+                                    const uint8_t* tgt, void* scr,
+                                    NoAllocResult* out, hipStream_t st);
+
 // Blocks of the DP sweep that can be resident at once for `cells` cells
 // per lane and `slots_lds` stack slots (0 if unsupported).
 int dp_resident_blocks(int cells, int32_t slots_lds, int device);

@@ -21,6 +21,7 @@
 // F64 template flag of k_dp, DevState::f64 elsewhere); indices are int32.
 
 #include <algorithm>
+#include <mutex>
 #include <utility>
 
 #include "pp_internal.h"
@@ -1996,6 +1997,173 @@ hipError_t launch_objective(const ChainSet& set, const DevState& d,
                        set, d, (int32_t)b);
   }
   return hipGetLastError();
+}
+
+// ------------------------------------------- allocation-free objective --
+
+// F_pair(T) of Eq. 6 for callers that cannot allocate device memory.  Its
+// per-block partial sums live in `scratch`, one array per GPU for the life
+// of the process; every call on a GPU shares it (overlapping calls on one
+// GPU race), and each call writes every partial it later reads, so nothing
+// needs clearing.  Layout: kNaBlocks 16-byte objective partials, kNaBlocks
+// 16-byte partials of sum lam*w (overflow check), kNaBlocks 4-byte flags
+// (some input negative), then the totals (NaTotals).
+constexpr int kNaBlocks = 1024;
+
+struct NaTotals {
+  unsigned __int128 obj;  // sum over (r, b) of lam_r(b) * v1_r(b)
+  unsigned __int128 lw;   // sum of lam * w, saturated at 2^64
+  uint32_t bad;           // nonzero: a negative demand or cost
+  uint32_t pad[3];
+};
+
+constexpr size_t kNaTotalsOffset = (size_t)kNaBlocks * (16 + 16 + 4);
+constexpr size_t kNaScratchBytes = kNaTotalsOffset + sizeof(NaTotals);
+static_assert(kNaTotalsOffset % 16 == 0, "totals alignment");
+static_assert(kNaScratchBytes <= kNoAllocScratchBytes, "declared scratch size");
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+
+constexpr unsigned __int128 kNaSat = (unsigned __int128)1 << 64;
+
+__device__ __forceinline__ unsigned __int128 sat_add(unsigned __int128 a,
+                                                     unsigned __int128 b) {
+  const unsigned __int128 s = a + b;
+  return s > kNaSat ? kNaSat : s;
+}
+
+// One thread per (requester r, chunk b) in a grid-stride loop over the
+// caller's layout: v1 = best saving of r over the holders of b (Eq. 5; 0 if
+// none holds it), term lam_r(b) * v1; fetch costs are scanned for negative
+// entries.  A held chunk is any nonzero target byte.
+__global__ void __launch_bounds__(256) k_objective_na(int32_t n, int32_t m,
+                                                      const int64_t* __restrict__ lam,
+                                                      const int64_t* __restrict__ w,
+                                                      const int64_t* __restrict__ f,
+                                                      const uint8_t* __restrict__ tgt,
+                                                      unsigned char* scr) {
+  unsigned __int128* part_obj = (unsigned __int128*)scr;
+  unsigned __int128* part_lw = part_obj + kNaBlocks;
+  uint32_t* part_bad = (uint32_t*)(part_lw + kNaBlocks);
+  const int64_t mn = (int64_t)m * n, mmn = mn * m;
+  const int64_t step = (int64_t)gridDim.x * blockDim.x;
+  unsigned __int128 acc = 0, lw = 0;
+  bool bad = false;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn; x += step) {
+    const int r = (int)(x / n);
+    const int64_t b = x % n;
+    const int64_t L = lam[x], W = w[x];
+    if (L < 0 || W < 0) {
+      bad = true;
+      continue;
+    }
+    int64_t v1 = 0;
+    for (int l = 0; l < m; ++l) {
+      if (!tgt[(int64_t)l * n + b]) continue;
+      const int64_t q = l == r ? W : imax(W - f[((int64_t)l * m + r) * n + b], 0);
+      v1 = imax(v1, q);
+    }
+    acc = sat_add(acc, (unsigned __int128)(uint64_t)L * (uint64_t)v1);
+    lw = sat_add(lw, (unsigned __int128)(uint64_t)L * (uint64_t)W);
+  }
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mmn; x += step)
+    if (f[x] < 0) bad = true;
+  __shared__ unsigned __int128 so[256], sl[256];
+  so[threadIdx.x] = acc;
+  sl[threadIdx.x] = lw;
+  bad = __syncthreads_or(bad);
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      so[threadIdx.x] = sat_add(so[threadIdx.x], so[threadIdx.x + o]);
+      sl[threadIdx.x] = sat_add(sl[threadIdx.x], sl[threadIdx.x + o]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    part_obj[blockIdx.x] = so[0];
+    part_lw[blockIdx.x] = sl[0];
+    part_bad[blockIdx.x] = bad ? 1u : 0u;
+  }
+}
+
+// The totals of the first `nblocks` partials (one block).
+__global__ void __launch_bounds__(256) k_objective_na_final(int32_t nblocks,
+                                                            unsigned char* scr) {
+  const unsigned __int128* part_obj = (const unsigned __int128*)scr;
+  const unsigned __int128* part_lw = part_obj + kNaBlocks;
+  const uint32_t* part_bad = (const uint32_t*)(part_lw + kNaBlocks);
+  unsigned __int128 a = 0, l = 0;
+  bool bad = false;
+  for (int q = threadIdx.x; q < nblocks; q += blockDim.x) {
+    a = sat_add(a, part_obj[q]);
+    l = sat_add(l, part_lw[q]);
+    bad |= part_bad[q] != 0;
+  }
+  __shared__ unsigned __int128 so[256], sl[256];
+  so[threadIdx.x] = a;
+  sl[threadIdx.x] = l;
+  bad = __syncthreads_or(bad);
+  for (int o = 128; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      so[threadIdx.x] = sat_add(so[threadIdx.x], so[threadIdx.x + o]);
+      sl[threadIdx.x] = sat_add(sl[threadIdx.x], sl[threadIdx.x + o]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    NaTotals* t = (NaTotals*)(scr + kNaTotalsOffset);
+    t->obj = so[0];
+    t->lw = sl[0];
+    t->bad = bad ? 1u : 0u;
+  }
+}
+
+}  // namespace
+
+// Device address of `scratch` on each GPU, looked up once per device with
+// that device current (each GPU holds its own copy of the array).
+static void* g_na_ptr[kNoAllocMaxDevices];
+static std::mutex g_na_mu;
+
+hipError_t noalloc_scratch(int device, void** ptr) {
+  if (device < 0 || device >= kNoAllocMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_na_mu);
+  if (!g_na_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_na_ptr[device] = p;
+  }
+  *ptr = g_na_ptr[device];
+  return hipSuccess;
+}
+
+hipError_t launch_objective_noalloc(int32_t n, int32_t m, const int64_t* lam,
+                                    const int64_t* w, const int64_t* f,
+                                    const uint8_t* tgt, void* scr,
+                                    NoAllocResult* out, hipStream_t st) {
+  const int64_t mn = (int64_t)m * n;
+  int64_t b = (mn + 255) / 256;
+  if (b > kNaBlocks) b = kNaBlocks;
+  if (b < 1) b = 1;
+  unsigned char* s = (unsigned char*)scr;
+  hipLaunchKernelGGL(k_objective_na, dim3((unsigned)b), dim3(256), 0, st, n, m,
+                     lam, w, f, tgt, s);
+  hipLaunchKernelGGL(k_objective_na_final, dim3(1), dim3(256), 0, st, (int32_t)b, s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  NaTotals t;
+  e = hipMemcpyAsync(&t, s + kNaTotalsOffset, sizeof t, hipMemcpyDeviceToHost, st);
+  if (e != hipSuccess) return e;
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return e;
+  out->bad = t.bad != 0;
+  out->overflow = t.lw > (unsigned __int128)INT64_MAX;
+  out->objective = out->overflow ? 0 : (int64_t)t.obj;
+  return hipSuccess;
 }
 
 }  // namespace pp
