@@ -58,12 +58,19 @@
  *       evaluated under the refreshed inputs.
  *   R24 real-valued costs (the _f64 entry points): IEEE double arithmetic,
  *       each product Lambda * x rounded before it is added (no fused
- *       multiply-add); p_h(b) sums its requester terms in increasing m and
- *       G(T) sums over b outer, m inner; the DP takes b_i only if
- *       t > s; a refinement replacement is accepted iff
- *       G(T_-h, T'_h) > G(T) + epsilon, both G evaluated from scratch;
- *       starts compare G exactly (earliest start on equal values); the
- *       comparator candidates use R18-R20 with value equality of doubles.
+ *       multiply-add); p_h(b) sums its requester terms in increasing m; the
+ *       DP takes b_i only if t > s; the comparator candidates use R18-R20
+ *       with value equality of doubles.
+ *   R26 G(T) on real-valued costs is the exact sum of its rounded terms
+ *       Lambda_m(b) * max(...) (a sum of doubles has one exact value, while
+ *       a floating-point sum depends on its order, which the paper does not
+ *       fix): a refinement replacement is accepted iff the exact
+ *       G(T_-h, T'_h) exceeds the exact G(T) + epsilon, both evaluated from
+ *       scratch; starts and comparator candidates compare exact values
+ *       (earliest on equal values); a reported objective is the exact value
+ *       rounded to the nearest double (ties to even).  Re-planning rounds
+ *       the exact G(T') - G(T) and the exact one-time cost to doubles and
+ *       decides horizon * (G(T') - G(T)) > cost on those doubles.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -1056,11 +1063,132 @@ static double q_save_f64(int32_t n, int32_t m, const double *w, const double *f,
     return maxd(d, 0.0);
 }
 
-/* Eq. (6), b outer, m inner */
-static double objective_f64(int32_t n, int32_t m, const double *lam,
-                            const double *w, const double *f, const uint8_t *tgt)
+/* Exact sums of non-negative doubles (R26).  Every finite double x >= 0 is
+ * an integer multiple of 2^-1074, so a sum of them is an integer in those
+ * units; it is kept as a plain little-endian array of 32-bit limbs (72
+ * limbs hold 2^2304 units, far above any sum of finite doubles). */
+#define EX_LIMBS 72
+typedef struct {
+    uint32_t w[EX_LIMBS];
+} exact_t;
+
+static void ex_zero(exact_t *a) { memset(a->w, 0, sizeof a->w); }
+
+/* a += v * 2^(32 * limb), v < 2^96 given as three 32-bit words */
+static void ex_add_at(exact_t *a, int limb, uint64_t lo64, uint32_t hi32)
 {
-    double g = 0.0;
+    uint64_t carry = 0;
+    uint32_t part[3] = {(uint32_t)lo64, (uint32_t)(lo64 >> 32), hi32};
+    for (int i = limb; i < EX_LIMBS; i++) {
+        uint64_t add = i - limb < 3 ? part[i - limb] : 0;
+        if (i - limb >= 3 && carry == 0)
+            break;
+        uint64_t t = (uint64_t)a->w[i] + add + carry;
+        a->w[i] = (uint32_t)t;
+        carry = t >> 32;
+    }
+}
+
+/* a += x, x finite and >= 0: x = mant * 2^(pos - 1074) with the 53-bit
+ * mantissa (implicit bit included for normal numbers) */
+static void ex_add_double(exact_t *a, double x)
+{
+    uint64_t bits;
+    memcpy(&bits, &x, sizeof bits);
+    int e = (int)(bits >> 52);
+    uint64_t mant = bits & ((1ull << 52) - 1);
+    int pos = 0;
+    if (e > 0) {
+        mant |= 1ull << 52;
+        pos = e - 1;
+    }
+    if (mant == 0)
+        return;
+    int limb = pos / 32, sh = pos % 32;
+    /* mant << sh < 2^85: low 64 bits and the bits above */
+    uint64_t lo = sh ? mant << sh : mant;
+    uint32_t hi = sh ? (uint32_t)(mant >> (64 - sh)) : 0;
+    ex_add_at(a, limb, lo, hi);
+}
+
+static void ex_add(exact_t *a, const exact_t *b)
+{
+    uint64_t carry = 0;
+    for (int i = 0; i < EX_LIMBS; i++) {
+        uint64_t t = (uint64_t)a->w[i] + b->w[i] + carry;
+        a->w[i] = (uint32_t)t;
+        carry = t >> 32;
+    }
+}
+
+/* a - b for a >= b */
+static void ex_sub(exact_t *d, const exact_t *a, const exact_t *b)
+{
+    int64_t borrow = 0;
+    for (int i = 0; i < EX_LIMBS; i++) {
+        int64_t t = (int64_t)a->w[i] - b->w[i] - borrow;
+        borrow = t < 0;
+        d->w[i] = (uint32_t)(t + (borrow ? (int64_t)1 << 32 : 0));
+    }
+}
+
+static int ex_cmp(const exact_t *a, const exact_t *b)
+{
+    for (int i = EX_LIMBS - 1; i >= 0; i--)
+        if (a->w[i] != b->w[i])
+            return a->w[i] < b->w[i] ? -1 : 1;
+    return 0;
+}
+
+static int ex_bit(const exact_t *a, int k) { return (a->w[k / 32] >> (k % 32)) & 1u; }
+
+/* the nearest double to a (ties to even); +infinity beyond the largest */
+static double ex_round(const exact_t *a)
+{
+    int top = -1;
+    for (int k = 32 * EX_LIMBS - 1; k >= 0; k--)
+        if (ex_bit(a, k)) {
+            top = k;
+            break;
+        }
+    uint64_t bits;
+    if (top < 53) {
+        /* below 2^53 units the value is exact: a denormal, or the smallest
+         * normal binade, whose encoding is the unit count itself */
+        bits = 0;
+        for (int k = top; k >= 0; k--)
+            bits = bits << 1 | (uint64_t)ex_bit(a, k);
+    } else {
+        uint64_t m53 = 0;
+        for (int k = top; k > top - 53; k--)
+            m53 = m53 << 1 | (uint64_t)ex_bit(a, k);
+        int half = ex_bit(a, top - 53), sticky = 0;
+        for (int k = top - 54; k >= 0 && !sticky; k--)
+            sticky = ex_bit(a, k);
+        if (half && (sticky || (m53 & 1))) {
+            m53++;
+            if (m53 == 1ull << 53) {
+                m53 >>= 1;
+                top++;
+            }
+        }
+        int64_t expo = (int64_t)top - 51; /* value = m53 / 2^52 * 2^(top - 1074) */
+        if (expo >= 2047)
+            bits = 0x7FFull << 52;
+        else
+            bits = (uint64_t)expo << 52 | (m53 & ((1ull << 52) - 1));
+    }
+    double x;
+    memcpy(&x, &bits, sizeof x);
+    return x;
+}
+
+/* Eq. (6) exactly: the sum over (b, m) of the rounded terms (R26) */
+static void objective_exact(int32_t n, int32_t m, const double *lam,
+                            const double *w, const double *f, const uint8_t *tgt,
+                            exact_t *g)
+{
+    ex_zero(g);
     for (int32_t b = 0; b < n; b++)
         for (int32_t r = 0; r < m; r++) {
             double best = 0.0;
@@ -1068,9 +1196,16 @@ static double objective_f64(int32_t n, int32_t m, const double *lam,
                 if (tgt[(size_t)h * n + b])
                     best = maxd(best, q_save_f64(n, m, w, f, h, r, b));
             double term = lam[(size_t)r * n + b] * best;
-            g += term;
+            ex_add_double(g, term);
         }
-    return g;
+}
+
+static double objective_f64(int32_t n, int32_t m, const double *lam,
+                            const double *w, const double *f, const uint8_t *tgt)
+{
+    exact_t g;
+    objective_exact(n, m, lam, w, f, tgt, &g);
+    return ex_round(&g);
 }
 
 /* Eq. (7), requester terms in increasing m */
@@ -1216,7 +1351,7 @@ static int worker_update_f64(const plan_in_f64 *in, const uint8_t *tgt,
 
 /* Algorithm 1, one start, with the tolerance epsilon of the refinement test */
 static int run_start_f64(const plan_in_f64 *in, const int32_t *pi,
-                         uint8_t *tgt, double *obj, int32_t *sweeps,
+                         uint8_t *tgt, exact_t *obj, int32_t *sweeps,
                          int32_t *accepts)
 {
     int32_t n = in->n, m = in->m;
@@ -1244,7 +1379,8 @@ static int run_start_f64(const plan_in_f64 *in, const int32_t *pi,
             improved = 0;
             for (int32_t a = 0; a < m; a++) {
                 int32_t h = pi[a];
-                double g_old = objective_f64(n, m, in->lam, in->w, in->f, tgt);
+                exact_t g_old, g_new, bar;
+                objective_exact(n, m, in->lam, in->w, in->f, tgt, &g_old);
                 uint8_t *th = tgt + (size_t)h * n;
                 memcpy(old, th, (size_t)n);
                 memset(th, 0, (size_t)n);
@@ -1252,8 +1388,11 @@ static int run_start_f64(const plan_in_f64 *in, const int32_t *pi,
                 if (rc != PPO_OK)
                     goto out;
                 memcpy(th, cand, (size_t)n);
-                double g_new = objective_f64(n, m, in->lam, in->w, in->f, tgt);
-                if (g_new > g_old + in->eps) {
+                objective_exact(n, m, in->lam, in->w, in->f, tgt, &g_new);
+                ex_zero(&bar);  /* G(T) + epsilon, exactly */
+                ex_add_double(&bar, in->eps);
+                ex_add(&bar, &g_old);
+                if (ex_cmp(&g_new, &bar) > 0) {
                     improved = 1;
                     acc++;
                 } else {
@@ -1263,7 +1402,7 @@ static int run_start_f64(const plan_in_f64 *in, const int32_t *pi,
             r++;
         } while (improved && !(in->max_rounds > 0 && r == in->max_rounds));
     }
-    *obj = objective_f64(n, m, in->lam, in->w, in->f, tgt);
+    objective_exact(n, m, in->lam, in->w, in->f, tgt, obj);
     *sweeps = r;
     *accepts = acc;
     rc = PPO_OK;
@@ -1296,7 +1435,7 @@ static int requester_side_f64(int32_t n, int32_t m, const double *fetch_cost)
 static int candidates_f64(int32_t n, int32_t m, const int32_t *order,
                           const int32_t *nextpos, const double *demand,
                           const double *recompute_cost, const double *fetch_cost,
-                          const int32_t *cap, uint8_t *targets, double *objs)
+                          const int32_t *cap, uint8_t *targets, exact_t *objs)
 {
     double *pp = malloc((size_t)n * sizeof(double));
     uint8_t *sp = malloc((size_t)n);
@@ -1337,7 +1476,7 @@ static int candidates_f64(int32_t n, int32_t m, const int32_t *order,
             for (int32_t i = 0; i < n; i++)
                 tg[(size_t)h * n + order[i]] = sp[i];
         }
-        objs[c] = objective_f64(n, m, demand, recompute_cost, fetch_cost, tg);
+        objective_exact(n, m, demand, recompute_cost, fetch_cost, tg, &objs[c]);
     }
     rc = PPO_OK;
 out:
@@ -1386,7 +1525,7 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
     double *standalone = malloc((size_t)m * sizeof(double));
     int64_t *rank = malloc((size_t)m * sizeof(int64_t));
     uint8_t *tgts = malloc((size_t)S * m * n);
-    double *obj = calloc((size_t)S, sizeof(double));
+    exact_t *obj = calloc((size_t)S, sizeof(exact_t));
     int32_t *sw = malloc((size_t)S * sizeof(int32_t));
     int32_t *ac = malloc((size_t)S * sizeof(int32_t));
     double *profit = malloc((size_t)n * sizeof(double));
@@ -1430,12 +1569,13 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
         if (rc != PPO_OK)
             goto out;
     }
-    int32_t best = 0;
+    int32_t best = 0;  /* R10, R26: exact values, earliest start on ties */
     for (int32_t s = 1; s < S; s++)
-        if (obj[s] > obj[best])
+        if (ex_cmp(&obj[s], &obj[best]) > 0)
             best = s;
     const uint8_t *won = tgts + (size_t)best * m * n;
-    double won_obj = obj[best];
+    exact_t won_obj = obj[best];
+    exact_t sg_ex[3];
     double sg_obj[3] = {0.0, 0.0, 0.0};
     int sg_run = 0;
     if ((flags & PPO_F_SAFEGUARDS) && requester_side_f64(n, m, fetch_cost)) {
@@ -1444,19 +1584,21 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
         if (!cands)
             goto out;
         rc = candidates_f64(n, m, order, nextpos, demand, recompute_cost,
-                            fetch_cost, cap, cands, sg_obj);
+                            fetch_cost, cap, cands, sg_ex);
         if (rc != PPO_OK)
             goto out;
         sg_run = 1;
-        for (int32_t c = 0; c < 3; c++)  /* R20 */
-            if (sg_obj[c] > won_obj) {
-                won_obj = sg_obj[c];
+        for (int32_t c = 0; c < 3; c++) {  /* R20 */
+            sg_obj[c] = ex_round(&sg_ex[c]);
+            if (ex_cmp(&sg_ex[c], &won_obj) > 0) {
+                won_obj = sg_ex[c];
                 won = cands + (size_t)c * m * n;
                 best = S + c;
             }
+        }
     }
     memcpy(target, won, (size_t)m * n);
-    *objective = won_obj;
+    *objective = ex_round(&won_obj);
     int64_t updates = m, cells = 0;
     for (int32_t h = 0; h < m; h++)
         cells += (int64_t)n * (cap[h] < n ? cap[h] : n);
@@ -1470,7 +1612,8 @@ int ppo_plan_f64(int32_t n, int32_t m, const int32_t *parent,
     if (orders_out)
         memcpy(orders_out, orders, (size_t)S * m * sizeof(int32_t));
     if (start_objective)
-        memcpy(start_objective, obj, (size_t)S * sizeof(double));
+        for (int32_t s = 0; s < S; s++)
+            start_objective[s] = ex_round(&obj[s]);
     if (start_sweeps)
         memcpy(start_sweeps, sw, (size_t)S * sizeof(int32_t));
     if (start_accepts)
@@ -1496,13 +1639,13 @@ out:
     return rc;
 }
 
-/* R21/R22 on doubles: the one-time cost summed over (m, b) in order, and
- * adoption iff horizon * (G(T') - G(T)) > cost. */
-static double materialization_cost_f64(int32_t n, int32_t m, const double *w,
+/* R21/R22 on doubles: the one-time cost, summed exactly (R26); adoption
+ * iff horizon * (G(T') - G(T)) > cost on the rounded exact values. */
+static void materialization_cost_exact(int32_t n, int32_t m, const double *w,
                                        const double *f, const uint8_t *incumbent,
-                                       const uint8_t *proposal)
+                                       const uint8_t *proposal, exact_t *total)
 {
-    double total = 0.0;
+    ex_zero(total);
     for (int32_t r = 0; r < m; r++)
         for (int32_t b = 0; b < n; b++) {
             if (!proposal[(size_t)r * n + b] || incumbent[(size_t)r * n + b])
@@ -1514,9 +1657,8 @@ static double materialization_cost_f64(int32_t n, int32_t m, const double *w,
                     if (fh < c)
                         c = fh;
                 }
-            total += c;
+            ex_add_double(total, c);
         }
-    return total;
 }
 
 /* Epoch re-planning on real-valued costs: arguments as ppo_replan, with
@@ -1549,11 +1691,22 @@ int ppo_replan_f64(int32_t n, int32_t m, const int32_t *parent,
         free(prop);
         return rc;
     }
-    double g_inc = objective_f64(n, m, demand, recompute_cost, fetch_cost,
-                                 incumbent);
-    double cost = materialization_cost_f64(n, m, recompute_cost, fetch_cost,
-                                           incumbent, prop);
-    int a = horizon * (g_new - g_inc) > cost;
+    exact_t e_inc, e_new, e_cost, diff;
+    objective_exact(n, m, demand, recompute_cost, fetch_cost, incumbent, &e_inc);
+    objective_exact(n, m, demand, recompute_cost, fetch_cost, prop, &e_new);
+    materialization_cost_exact(n, m, recompute_cost, fetch_cost, incumbent, prop,
+                               &e_cost);
+    double gain;  /* G(T') - G(T), exact, then rounded */
+    if (ex_cmp(&e_new, &e_inc) >= 0) {
+        ex_sub(&diff, &e_new, &e_inc);
+        gain = ex_round(&diff);
+    } else {
+        ex_sub(&diff, &e_inc, &e_new);
+        gain = -ex_round(&diff);
+    }
+    double g_inc = ex_round(&e_inc);
+    double cost = ex_round(&e_cost);
+    int a = horizon * gain > cost;
     memcpy(target, a ? prop : incumbent, (size_t)m * n);
     if (proposal)
         memcpy(proposal, prop, (size_t)m * n);

@@ -10,10 +10,18 @@ the exhaustive optimum within rounding, the objective must match Eq. 6
 evaluated with NumPy, Proposition 1's exact-gain identity must hold within
 rounding, every fixed-order greedy start must reach half the exhaustive joint
 optimum (Theorem 3), and the tolerance must gate refinement as stated.
+
+Reading R26 (G is the exact sum of its rounded terms) is pinned by Python's
+math.fsum, which returns the correctly rounded exact sum of its inputs, by
+rounding edge cases (ties to even, denormals, overflow), and by an
+independent driver of Algorithm 1 that evaluates G with exact rationals
+(fractions.Fraction) and must make every acceptance decision the oracle
+makes, including the cases where two rounded sums would disagree.
 """
 
 import itertools
 import math
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -107,6 +115,129 @@ def test_objective_matches_eq6(seed):
     tgt = (rng.random(lam.shape) < 0.4).astype(np.uint8)
     got = oracle.objective_f64(lam, w, f, tgt)
     assert got == pytest.approx(objective_numpy(lam, w, f, tgt), rel=1e-12)
+
+
+def eq6_terms(lam, w, f, tgt):
+    """The rounded terms lam_m(b) * max over holders h of q_{m<-h}(b) (Eq. 5,
+    Eq. 6; 0 where nobody holds b), as NumPy computes them."""
+    m, n = lam.shape
+    best = np.zeros((m, n))
+    for h in range(m):
+        for r in range(m):
+            q = w[r] if h == r else np.maximum(w[r] - f[h, r], 0.0)
+            best[r] = np.where(tgt[h] != 0, np.maximum(best[r], q), best[r])
+    return (lam * best).ravel()
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_objective_is_the_correctly_rounded_exact_sum(seed):
+    """R26: G is the exact sum of the rounded terms, rounded once: it equals
+    math.fsum of the same terms bit for bit, at every magnitude."""
+    parent, lam, w, f, cap = real_instance(9000 + seed, n_max=200, m_max=5)
+    rng = np.random.default_rng(seed)
+    if seed % 4 == 1:  # terms spread over many binades
+        lam = lam * np.exp2(rng.integers(-60, 60, size=lam.shape))
+    if seed % 4 == 2:  # denormal and tiny terms only
+        lam = lam * 2.0 ** -1070
+    if seed % 4 == 3:  # a few huge terms among small ones
+        lam[:, :3] *= 2.0 ** 900
+    tgt = (rng.random(lam.shape) < 0.5).astype(np.uint8)
+    got = oracle.objective_f64(lam, w, f, tgt)
+    assert got == math.fsum(eq6_terms(lam, w, f, tgt))
+
+
+def _one_chunk_sum(values):
+    """A one-chunk instance whose terms are exactly `values`: every worker
+    holds the chunk, demand 1, so requester r's term is its own w_r."""
+    m = len(values)
+    lam = np.ones((m, 1))
+    w = np.array(values, dtype=np.float64).reshape(m, 1)
+    f = np.zeros((m, m, 1))
+    return oracle.objective_f64(lam, w, f, np.ones((m, 1), np.uint8))
+
+
+def test_exact_sum_rounding_edges():
+    u = 2.0 ** -53
+    assert _one_chunk_sum([1.0, u]) == 1.0                 # tie: to even
+    assert _one_chunk_sum([1.0 + 2 * u, u]) == 1.0 + 4 * u  # tie: to even (up)
+    assert _one_chunk_sum([1.0, u, 2.0 ** -200]) == 1.0 + 2 * u  # just above the tie
+    assert _one_chunk_sum([1.0] + [2.0 ** -60] * 200) == math.fsum([1.0] + [2.0 ** -60] * 200)
+    tiny = 5e-324
+    assert _one_chunk_sum([tiny] * 7) == 7 * tiny           # denormal, exact
+    assert _one_chunk_sum([2.0 ** -1022 - tiny, tiny]) == 2.0 ** -1022  # into the normals
+    big = 1.7976931348623157e308
+    assert _one_chunk_sum([big, big]) == math.inf          # beyond the largest double
+    # half an ulp (2^970) above the largest double is a tie, and its odd
+    # mantissa rounds up, past the largest; less than that rounds down
+    assert _one_chunk_sum([big, 2.0 ** 970]) == math.inf
+    assert _one_chunk_sum([big, 2.0 ** 970 - 2.0 ** 917]) == big
+    assert _one_chunk_sum([big, 2.0 ** 969]) == big
+    assert _one_chunk_sum([0.0, 0.0]) == 0.0
+    vals = [3.0 ** k * 2.0 ** -30 for k in range(40)] + [1e-300, 1e300, -0.0 + 0.0]
+    assert _one_chunk_sum(vals) == math.fsum(vals)
+
+
+def _exact_g(lam, w, f, tgt):
+    return sum((Fraction(float(x)) for x in eq6_terms(lam, w, f, tgt)), Fraction(0))
+
+
+def _algorithm1_exact(parent, lam, w, f, cap, order, eps, max_rounds=0):
+    """Algorithm 1 for one start order, every acceptance decided on exact
+    rationals: the exact G of the placement with worker h's set replaced
+    must exceed the exact G of the current placement plus epsilon.  The
+    update itself (marginals, rooted-tree DP) is the oracle's, pinned above."""
+    m, n = lam.shape
+    tgt = np.zeros((m, n), np.uint8)
+    for h in order:
+        p = oracle.marginal_f64(lam, w, f, tgt, h)
+        tgt[h] = oracle.rooted_dp_f64(parent, p, int(cap[h]))[0]
+    sweeps = accepts = ties = 0
+    while True:
+        improved = False
+        for h in order:
+            g_old = _exact_g(lam, w, f, tgt)
+            old = tgt[h].copy()
+            tgt[h] = 0
+            p = oracle.marginal_f64(lam, w, f, tgt, h)
+            tgt[h] = oracle.rooted_dp_f64(parent, p, int(cap[h]))[0]
+            g_new = _exact_g(lam, w, f, tgt)
+            if g_new > g_old + Fraction(eps):
+                improved = True
+                accepts += 1
+            else:
+                if g_new == g_old and not np.array_equal(old, tgt[h]):
+                    ties += 1  # a different set of exactly equal value
+                tgt[h] = old
+        sweeps += 1
+        if not improved or (max_rounds and sweeps == max_rounds):
+            break
+    return tgt, sweeps, accepts, float(_exact_g(lam, w, f, tgt)), ties
+
+
+def test_acceptance_matches_exact_rational_driver():
+    """Every decision equals the exact-rational one, at epsilon = 0 (where
+    replacements of equal value must be rejected whatever the rounding of
+    two sums would say) and at a small epsilon; some cases hit such ties."""
+    ties = 0
+    for seed in range(60):
+        rng = np.random.default_rng(800 + seed)
+        m = int(rng.integers(2, 6))
+        n = int(rng.integers(5, 120))
+        inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, n + 2])),
+                                 source_dependent=bool(seed % 4))
+        lam, w, f = W.real_valued(inst, seed, jitter=0.5)
+        order = [int(x) for x in rng.permutation(m)]
+        eps = 0.0 if seed % 3 else 1e-7 * float(np.sum(lam * w))
+        tgt, sweeps, accepts, obj, t = _algorithm1_exact(
+            inst.parent, lam, w, f, inst.cap, order, eps)
+        ties += t
+        r = oracle.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps,
+                            n_starts=1, orders_in=np.array([order], np.int32))
+        assert r.start_sweeps.tolist() == [sweeps]
+        assert r.start_accepts.tolist() == [accepts]
+        np.testing.assert_array_equal(r.target, tgt)
+        assert r.objective == obj
+    assert ties > 0
 
 
 @pytest.mark.parametrize("seed", range(30))
