@@ -444,8 +444,7 @@ def f64_leg(B, W, inst, ctx, steps, warmup):
             out["parity_vs_golden"] = all(
                 q.best_start == gold["best_start"]
                 and q.start_sweeps.tolist() == gold["start_sweeps"]
-                and abs(q.objective - float.fromhex(gold["objective"]))
-                <= 1e-12 * abs(q.objective) for q in plans)
+                and q.objective == float.fromhex(gold["objective"]) for q in plans)
     return out
 
 
@@ -495,7 +494,7 @@ def paper_config_leg(B, W, ctx, steps, with_oracle):
         out["oracle_s_per_plan_1_thread"] = time.perf_counter() - t1
         out["same_as_oracle"] = (
             bool(np.array_equal(o.target, tgt.cpu().numpy()))
-            and abs(o.objective - p.objective) <= 1e-12 * abs(o.objective))
+            and o.objective == p.objective)
     return out
 
 

@@ -20,8 +20,9 @@
  *     and costs in integer microseconds, and every value/objective is int64
  *     (request * us), exact.  The *_f64 entry points take finite,
  *     non-negative IEEE doubles in any consistent units and a refinement
- *     tolerance epsilon >= 0; their sums are taken in a fixed order, so
- *     results are deterministic.
+ *     tolerance epsilon >= 0; every objective value they compare is the
+ *     exact sum of its rounded terms, so no result depends on an order of
+ *     summation.
  *   - Node ids are the caller's labels 0..n-1.  parent[v] = -1 attaches v to
  *     the implicit no-cost dummy root (Sec. III-A), so forests are allowed.
  *   - Host arrays are C-contiguous, caller-owned, read or written only during
@@ -180,10 +181,14 @@ int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
  * The arithmetic is the integer path's, in doubles: each product
  * Lambda * x is rounded before it is added, p_h(b) adds its requester terms
  * in increasing m, the DP takes b_i only if p + D[i+1][j-1] > D[next(i)][j],
- * and a replacement that leaves the worker's set unchanged is never counted
- * as an improvement.  The acceptance test uses Proposition 1 (DP value >
- * incumbent value + epsilon); objectives are summed in a fixed order, so a
- * placement always gets the same value.  PP_F_SAFEGUARDS adds the comparator
+ * and G = F_pair is the exact sum of its rounded terms Lambda_m(b) *
+ * max(...) (every finite double is a multiple of 2^-1074, so the sum is kept
+ * as an exact integer of those units): a refinement replacement is accepted
+ * iff the exact G with it exceeds the exact G(T) + epsilon (so one of
+ * exactly equal value, e.g. differing only by chunks of zero marginal value,
+ * is never accepted, also at epsilon = 0); starts and comparator candidates
+ * compare exact values; reported objectives are the exact values rounded to
+ * the nearest double.  PP_F_SAFEGUARDS adds the comparator
  * candidates for requester-side costs (fetch costs equal as values over
  * every source; -0.0 counts as 0.0) with the integer path's formulas in
  * doubles.  Statistics as pp_stats, with double objectives and scores. */
@@ -250,10 +255,10 @@ int pp_replan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand
 
 /* pp_replan on real-valued costs: the planner of pp_plan_f64 (tolerance
  * epsilon), the same rule with a real horizon (finite, >= 0):
- * adopt iff horizon * (G(T') - G(T)) > cost, evaluated in doubles (the
- * cost is a sum of doubles in a fixed order; a decision within rounding of
- * its threshold can differ from another evaluation order).  Errors as
- * pp_plan_f64 and pp_replan. */
+ * adopt iff horizon * (G(T') - G(T)) > cost, where G(T') - G(T) and the
+ * cost are exact sums each rounded once to the nearest double, and the
+ * product and comparison are evaluated in doubles.  Errors as pp_plan_f64
+ * and pp_replan. */
 typedef struct {
     int32_t adopt;
     double incumbent_objective;

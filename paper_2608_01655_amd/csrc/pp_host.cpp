@@ -341,14 +341,14 @@ struct pp_ctx {
   DevBuf up_lam, up_w, up_f, up_u8;
   // per-slot state
   DevBuf tgt, v1, v2, h1, profit, sel, bits, ring, cs;
-  DevBuf partial, flag, fpart;
+  DevBuf partial, flag, gx, gxp;
   uint32_t epoch = 0;
   std::vector<uint32_t> meta_host;  // source of the last metadata upload
   std::vector<hipEvent_t> events;
   ~pp_ctx() {
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
-                      &ring, &cs, &partial, &flag, &fpart})
+                      &ring, &cs, &partial, &flag, &gx, &gxp})
       b->release();
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (own) (void)hipStreamDestroy(own);
@@ -391,6 +391,29 @@ int ensure_slots(pp_ctx* c, DevState& d, int32_t slots, int32_t kmax,
   d.cs = c->cs.as<ChainState>();
   d.stages = stages;
   d.cells = cells;
+  return PP_OK;
+}
+
+// Real-valued costs: exact objective values per slot and the per-block
+// partials of one launch of up to kMaxChains chains.
+int ensure_exact(pp_ctx* c, DevState& d, int32_t slots) {
+  d.gx_blocks = gexact_blocks(d.n, d.m);
+  PP_TRY(c->gx.ensure((size_t)slots * 2 * kExLimbs * 4));
+  PP_TRY(c->gxp.ensure((size_t)kMaxChains * d.gx_blocks * kExLimbs * 8));
+  d.gx = c->gx.as<uint32_t>();
+  d.gxp = c->gxp.as<uint64_t>();
+  return PP_OK;
+}
+
+// Exact objective values of `count` consecutive slots from `first`.
+int read_exact(const DevState& d, int32_t first, int32_t count, hipStream_t st,
+               std::vector<uint32_t>& out) {
+  out.assign((size_t)count * kExLimbs, 0);
+  for (int32_t q = 0; q < count; ++q)
+    PP_HIP(hipMemcpyAsync(out.data() + (size_t)q * kExLimbs,
+                          d.gx + (size_t)(first + q) * 2 * kExLimbs, kExLimbs * 4,
+                          hipMemcpyDeviceToHost, st));
+  PP_HIP(hipStreamSynchronize(st));
   return PP_OK;
 }
 
@@ -485,6 +508,7 @@ struct Engine {
     PP_HIP(launch_gains(set, d, st, kGainsMarginal, mode == kModeRefine ? 1 : 0));
     PP_TRY(dp(set, 1));
     PP_HIP(launch_backtrack(set, d, mode, st));
+    if (d.f64) PP_HIP(launch_gexact(set, d, mode, st));  // exact G and the decision
     PP_HIP(launch_commit(set, d, mode, st));
     return PP_OK;
   }
@@ -544,6 +568,9 @@ struct PlanResult {
   int32_t dp_launches = 0;
   int32_t lane_cells = 0;      // DP cells per lane of the sweep
   int32_t fmax = 0;            // maximum by one 64-bit float instruction
+  // real-valued costs: exact objective values of the starts and of the
+  // returned placement (kExLimbs limbs each)
+  std::vector<uint32_t> start_gx, win_gx;
 };
 
 // Comparator safeguards of Sec. IV-C (Algorithm 1: the candidate set also
@@ -570,6 +597,10 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
   // keep the best start's placement out of the scratch slots
   PP_HIP(hipMemcpyAsync(d.tgt + (size_t)slot_b * mn, d.tgt + (size_t)res.win_slot * mn,
                         mn, hipMemcpyDeviceToDevice, st));
+  if (d.f64)
+    PP_HIP(hipMemcpyAsync(d.gx + (size_t)slot_b * 2 * kExLimbs,
+                          d.gx + (size_t)res.win_slot * 2 * kExLimbs, 2 * kExLimbs * 4,
+                          hipMemcpyDeviceToDevice, st));
   res.win_slot = slot_b;
   std::vector<int32_t> cand_slot = {slot_b + 1, slot_b + 2, slot_b + 3};
   {
@@ -608,6 +639,7 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
     PP_HIP(launch_gains(set, d, st, kGainsLocalDedup));
     PP_TRY(e.dp(set, 1));
     PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
+    if (d.f64) PP_HIP(launch_gexact(set, d, kModeGreedy, st));  // adopts T'_h
     PP_HIP(launch_commit(set, d, kModeGreedy, st));
   }
   {
@@ -628,12 +660,19 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
   for (const ChainState& x : scr)
     if (x.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
   res.sg_run = true;
+  std::vector<uint32_t> cgx;
+  if (d.f64) PP_TRY(read_exact(d, cand_slot[0], 3, st, cgx));
   for (int q = 0; q < 3; ++q) {
     res.sg_obj[q] = fin[q].obj;
-    if (fin[q].obj > res.win_obj) {
+    // real-valued costs compare exact values
+    const bool better = d.f64 ? ex_cmp(&cgx[(size_t)q * kExLimbs], res.win_gx.data()) > 0
+                              : fin[q].obj > res.win_obj;
+    if (better) {
       res.win_obj = fin[q].obj;
       res.win_slot = cand_slot[q];
       res.best = res.S + q;
+      if (d.f64) res.win_gx.assign(cgx.begin() + (size_t)q * kExLimbs,
+                                   cgx.begin() + (size_t)(q + 1) * kExLimbs);
     }
   }
   res.updates += 3 * (int64_t)m;
@@ -711,15 +750,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
       while (!x.done) {
         if (x.pos == m) {
           res.sweeps[x.s] += 1;
-          bool improved = x.improved;
-          if (d.f64) {
-            // real-valued costs: k_commit counts a replacement only if it
-            // changes the set
-            ChainState c;
-            PP_HIP(hipMemcpyAsync(&c, d.cs + x.s, sizeof c, hipMemcpyDeviceToHost, e.st));
-            PP_HIP(hipStreamSynchronize(e.st));
-            improved = c.improved != 0;
-          }
+          const bool improved = x.improved;
           const bool capped = max_rounds > 0 && res.sweeps[x.s] >= max_rounds;
           if (!improved || capped) {
             x.done = true;
@@ -785,6 +816,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
     PP_HIP(launch_gains(set, d, e.st, kGainsMarginal, 1));
     PP_TRY(e.dp(set, 1));
     PP_HIP(launch_backtrack(set, d, kModeRefine, e.st));
+    if (d.f64) PP_HIP(launch_gexact(set, d, kModeRefine, e.st));
     // the launch's results: the starts' slots (consecutive) and the spare
     // slots, in two copies
     std::vector<ChainState> own(A), spare(spares > 0 ? spares : 1);
@@ -922,9 +954,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   if (f64) {
     d.f64 = 1;
     d.eps = eps;
-    d.fpart_stride = fpart_blocks(n, m);
-    PP_TRY(c->fpart.ensure((size_t)slots * d.fpart_stride * 8));
-    d.fpart = c->fpart.as<double>();
+    PP_TRY(ensure_exact(c, d, slots));
   }
   PP_TRY(upload_meta(c, t, cells, st));
   d.meta = c->meta.as<uint32_t>();  // upload_meta may have (re)allocated it
@@ -1018,8 +1048,19 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     }
   }
   res.best = 0;
-  for (int32_t s = 1; s < S; ++s)
-    if (res.start_obj[s] > res.start_obj[res.best]) res.best = s;
+  if (f64) {
+    // real-valued costs: starts compare exact objective values
+    PP_TRY(read_exact(d, 0, S, st, res.start_gx));
+    for (int32_t s = 1; s < S; ++s)
+      if (ex_cmp(&res.start_gx[(size_t)s * kExLimbs],
+                 &res.start_gx[(size_t)res.best * kExLimbs]) > 0)
+        res.best = s;
+    res.win_gx.assign(res.start_gx.begin() + (size_t)res.best * kExLimbs,
+                      res.start_gx.begin() + (size_t)(res.best + 1) * kExLimbs);
+  } else {
+    for (int32_t s = 1; s < S; ++s)
+      if (res.start_obj[s] > res.start_obj[res.best]) res.best = s;
+  }
   res.win_slot = res.best;
   res.win_obj = res.start_obj[res.best];
   res.updates = m;
@@ -1299,7 +1340,10 @@ int placement_to_host(pp_ctx* c, const TreeLayout& t, int32_t m, int32_t slot,
 struct ReplanEval {
   int64_t g_inc = 0;              // objective bits
   unsigned __int128 cost = 0;     // integer costs
-  double cost_f64 = 0.0;          // real-valued costs
+  // real-valued costs: the exact cost and the exact G(T') - G(T), each
+  // rounded to the nearest double
+  double cost_f64 = 0.0;
+  double gain_f64 = 0.0;
 };
 
 int replan_evaluate(pp_ctx* c, const TreeLayout& t, int32_t m, const PlanResult& r,
@@ -1322,8 +1366,9 @@ int replan_evaluate(pp_ctx* c, const TreeLayout& t, int32_t m, const PlanResult&
   if (f64) {
     d.f64 = 1;
     d.eps = eps;
-    d.fpart_stride = fpart_blocks(n, m);
-    d.fpart = c->fpart.as<double>();
+    d.gx_blocks = gexact_blocks(n, m);
+    d.gx = c->gx.as<uint32_t>();
+    d.gxp = c->gxp.as<uint64_t>();
   }
   const int32_t xs = r.extra_slot;
   std::vector<uint8_t> pre(mn);
@@ -1337,25 +1382,48 @@ int replan_evaluate(pp_ctx* c, const TreeLayout& t, int32_t m, const PlanResult&
   PP_HIP(launch_init_slots(inc_set, d, 0, st));
   PP_HIP(launch_holder_build(inc_set, d, st));
   PP_HIP(launch_objective(inc_set, d, st));
-  PP_TRY(c->partial.ensure(1024 * 16));
+  const size_t part_bytes = f64 ? (size_t)kExLimbs * 8 : 16;
+  PP_TRY(c->partial.ensure(1024 * part_bytes));
   int32_t nb = 0;
   PP_HIP(launch_mat_cost(d, xs, r.win_slot, c->partial.p, &nb, st));
-  std::vector<unsigned char> part((size_t)nb * 16);
+  std::vector<unsigned char> part((size_t)nb * part_bytes);
   ChainState inc_cs{};
   PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, part.size(), hipMemcpyDeviceToHost, st));
   PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState), hipMemcpyDeviceToHost, st));
   PP_HIP(hipStreamSynchronize(st));
   ev.g_inc = inc_cs.obj;
-  for (int32_t b = 0; b < nb; ++b) {
-    if (f64) {
-      double v;
-      std::memcpy(&v, part.data() + 8 * (size_t)b, 8);
-      ev.cost_f64 += v;
-    } else {
+  if (!f64) {
+    for (int32_t b = 0; b < nb; ++b) {
       unsigned __int128 v;
       std::memcpy(&v, part.data() + 16 * (size_t)b, 16);
       ev.cost += v;
     }
+    return PP_OK;
+  }
+  // the exact cost: the blocks' lazy limbs, summed and carried
+  std::vector<uint32_t> cost(kExLimbs);
+  unsigned __int128 carry = 0;
+  for (int q = 0; q < kExLimbs; ++q) {
+    unsigned __int128 v = carry;
+    for (int32_t b = 0; b < nb; ++b) {
+      uint64_t x;
+      std::memcpy(&x, part.data() + ((size_t)b * kExLimbs + q) * 8, 8);
+      v += x;
+    }
+    cost[q] = (uint32_t)v;
+    carry = v >> 32;
+  }
+  ev.cost_f64 = bits_f64((int64_t)ex_round_bits(cost.data()));
+  // G(T') - G(T), exact, then rounded
+  std::vector<uint32_t> ginc, diff(kExLimbs);
+  PP_TRY(read_exact(d, xs, 1, st, ginc));
+  const uint32_t* gw = r.win_gx.data();
+  if (ex_cmp(gw, ginc.data()) >= 0) {
+    ex_sub(diff.data(), gw, ginc.data());
+    ev.gain_f64 = bits_f64((int64_t)ex_round_bits(diff.data()));
+  } else {
+    ex_sub(diff.data(), ginc.data(), gw);
+    ev.gain_f64 = -bits_f64((int64_t)ex_round_bits(diff.data()));
   }
   return PP_OK;
 }
@@ -1787,7 +1855,7 @@ int pp_replan_f64(int32_t n, int32_t m, const int32_t* parent, const double* dem
     PP_TRY(replan_evaluate(c, t, m, r, incumbent, true, epsilon, st, ev));
     const double cost = ev.cost_f64;
     const double g_inc = bits_f64(ev.g_inc), g_new = bits_f64(r.win_obj);
-    const bool adopt = horizon * (g_new - g_inc) > cost;
+    const bool adopt = horizon * ev.gain_f64 > cost;
     PP_TRY(replan_outputs(c, t, m, r, incumbent, adopt, target, proposal, st));
     info->adopt = adopt ? 1 : 0;
     info->incumbent_objective = g_inc;

@@ -59,6 +59,101 @@ enum GainsMode : int32_t {
   kGainsLocalDedup = 3
 };
 
+// Exact sums of real-valued objective terms.  A finite double x >= 0 is an
+// integer number of units of 2^-1074; a sum of such terms is kept exactly as
+// kExLimbs little-endian 32-bit limbs of that integer (2^2304 units, far
+// above any sum of finite doubles), so it does not depend on the order of
+// the additions.  Device accumulators are "lazy": 64-bit limbs that each
+// collect 32-bit chunks and are carried once at the end.
+constexpr int kExLimbs = 72;
+
+// Where a term lands: x = mant * 2^pos units, split into 32-bit chunks at
+// limbs limb, limb+1, limb+2 (chunk 2 < 2^21).  Returns false for x = 0.
+__host__ __device__ inline bool ex_chunks(double x, int& limb, uint32_t& c0, uint32_t& c1,
+                                          uint32_t& c2) {
+  const uint64_t bits = __builtin_bit_cast(uint64_t, x);
+  const int e = (int)(bits >> 52);
+  uint64_t mant = bits & ((1ull << 52) - 1);
+  int pos = 0;
+  if (e > 0) {
+    mant |= 1ull << 52;
+    pos = e - 1;
+  }
+  if (mant == 0) return false;
+  limb = pos >> 5;
+  const int sh = pos & 31;
+  const uint64_t lo = mant << sh;
+  c0 = (uint32_t)lo;
+  c1 = (uint32_t)(lo >> 32);
+  c2 = sh ? (uint32_t)(mant >> (64 - sh)) : 0u;
+  return true;
+}
+
+// a += x exactly (canonical limbs, carries propagated).
+__host__ __device__ inline void ex_add_double(uint32_t* a, double x) {
+  int limb;
+  uint32_t c[3];
+  if (!ex_chunks(x, limb, c[0], c[1], c[2])) return;
+  uint64_t carry = 0;
+  for (int q = limb; q < kExLimbs; ++q) {
+    const uint64_t add = q - limb < 3 ? c[q - limb] : 0u;
+    if (q - limb >= 3 && carry == 0) break;
+    const uint64_t t = (uint64_t)a[q] + add + carry;
+    a[q] = (uint32_t)t;
+    carry = t >> 32;
+  }
+}
+
+// -1, 0, 1 as a < b, a == b, a > b.
+__host__ __device__ inline int ex_cmp(const uint32_t* a, const uint32_t* b) {
+  for (int q = kExLimbs - 1; q >= 0; --q)
+    if (a[q] != b[q]) return a[q] < b[q] ? -1 : 1;
+  return 0;
+}
+
+// d = a - b for a >= b.
+__host__ __device__ inline void ex_sub(uint32_t* d, const uint32_t* a, const uint32_t* b) {
+  uint32_t borrow = 0;
+  for (int q = 0; q < kExLimbs; ++q) {
+    const uint64_t t = (uint64_t)a[q] - b[q] - borrow;
+    d[q] = (uint32_t)t;
+    borrow = (uint32_t)(t >> 63);
+  }
+}
+
+// Bit pattern of the double nearest to a (ties to even; +inf beyond the
+// largest finite double).
+__host__ __device__ inline uint64_t ex_round_bits(const uint32_t* a) {
+  int hi = kExLimbs - 1;
+  while (hi >= 0 && a[hi] == 0) --hi;
+  if (hi < 0) return 0;
+  const int top = 32 * hi + 31 - __builtin_clz(a[hi]);  // highest set bit
+  // bits [lo, top] of a as an integer (lo >= 0), at most 64 of them
+  auto window = [&](int lo) -> uint64_t {
+    uint64_t v = 0;
+    for (int k = top; k >= lo; --k) v = v << 1 | ((a[k >> 5] >> (k & 31)) & 1u);
+    return v;
+  };
+  if (top < 53) return window(0);  // exact: a denormal or the first binade
+  uint64_t m = window(top - 52);   // 53 bits
+  const int rb = top - 53;         // rounding bit
+  const bool half = (a[rb >> 5] >> (rb & 31)) & 1u;
+  bool sticky = false;
+  for (int k = 0; k < (rb >> 5) && !sticky; ++k) sticky = a[k] != 0;
+  if (!sticky) sticky = (a[rb >> 5] & ((1u << (rb & 31)) - 1u)) != 0;
+  int t = top;
+  if (half && (sticky || (m & 1))) {
+    ++m;
+    if (m == (1ull << 53)) {
+      m >>= 1;
+      ++t;
+    }
+  }
+  const int64_t expo = (int64_t)t - 51;  // the value is m / 2^52 * 2^(t - 1074)
+  if (expo >= 2047) return 0x7FFull << 52;
+  return (uint64_t)expo << 52 | (m & ((1ull << 52) - 1));
+}
+
 // Scalars of one chain slot, updated on the device.
 struct ChainState {
   int64_t dpval;     // D[1][k'] of the last DP sweep
@@ -69,8 +164,12 @@ struct ChainState {
   int32_t improved;  // some update of the current sweep was accepted
   int32_t accepts;   // accepted refinement replacements so far
   int32_t status;    // nonzero: a device-side wait gave up
-  int32_t changed;   // real-valued refinement: the accepted selection
-                     // differs from the incumbent set (counted once)
+  // Real-valued refinement: the update was rejected before its walk (its
+  // DP value is below the incumbent's value + eps by more than any
+  // rounding of the two sums can account for), so no exact G is needed.
+  int32_t rejected;
+  int64_t wsum;      // real-valued: sum over (r, b) of Lambda * w (the
+                     // scale of that rounding bound), double bits
   // Refinement updates whose inputs are unchanged: bit h of dirty is set
   // when another worker's replacement is adopted (its set may change) and
   // cleared when worker h's DP runs.
@@ -132,8 +231,12 @@ struct DevState {
   // and non-negative, so their bit patterns order like the values.
   int32_t f64;
   double eps;               // refinement tolerance (real-valued costs)
-  double* fpart;            // [slots][fpart_stride] per-block partial sums
-  int32_t fpart_stride;     //   summed in a fixed order (real-valued costs)
+  // Exact objective values (real-valued costs): gx[slot][0] = G of the
+  // slot's placement, gx[slot][1] = G with the slot's last update adopted;
+  // gxp = lazy per-block partial sums, [chain][gx_blocks][kExLimbs].
+  uint32_t* gx;
+  uint64_t* gxp;
+  int32_t gx_blocks;
 };
 
 // Host-side launchers (pp_kernels.hip).  All enqueue on `st`.
@@ -153,8 +256,15 @@ hipError_t launch_validate(const int64_t* lam, const int64_t* w,
 hipError_t launch_validate_f64(const double* lam, const double* w,
                                const double* f, int32_t n, int32_t m,
                                int32_t* bad, hipStream_t st);
-// per-block partial sums of k_gains and k_objective for real-valued costs
-int32_t fpart_blocks(int32_t n, int32_t m);
+// Exact objective sums (real-valued costs): blocks per chain of k_gexact
+// (128, or enough that no block sums more than 2^30 terms; m * n < 2^39).
+constexpr int kGexactBlocks = 512;
+int32_t gexact_blocks(int32_t n, int32_t m);
+// mode kModeGreedy / kModeRefine: G of each update's placement (worker h's
+// set replaced by its backtracked selection) and the acceptance decision;
+// any other mode: G of each slot's own placement (gx[slot][0], cs.obj).
+hipError_t launch_gexact(const ChainSet& set, const DevState& d, int mode,
+                         hipStream_t st);
 hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
                              int clear_tgt, hipStream_t st);
 hipError_t launch_holder_build(const ChainSet& set, const DevState& d,
@@ -167,7 +277,8 @@ hipError_t launch_assemble(const ChainSet& set, const DevState& d, int32_t dst,
                            hipStream_t st);
 hipError_t launch_requester_check(const int64_t* f, int32_t n, int32_t m,
                                   int32_t* mismatch, hipStream_t st);
-// partial: at least 1024 16-byte exact sums; *nblocks receives the count
+// partial: at least 1024 exact sums (integer costs: 16 bytes each;
+// real-valued: kExLimbs lazy 64-bit limbs each); *nblocks receives the count
 hipError_t launch_mat_cost(const DevState& d, int32_t inc, int32_t prop,
                            void* partial, int32_t* nblocks, hipStream_t st);
 hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,

@@ -119,8 +119,7 @@ __device__ int64_t block_sum(int64_t v) {
   return t;
 }
 
-// Sum of v over the block in a fixed order (shuffles within each wave, then
-// the waves in order); the result is in thread 0.
+// Sum of a double over a 256-thread block (any order), in thread 0.
 __device__ double block_sum_f64(double v) {
   __shared__ double part[256 / kWave];
   for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, kWave);
@@ -134,14 +133,43 @@ __device__ double block_sum_f64(double v) {
   return t;
 }
 
-// Sum of a[0..count) by one wave in a fixed order (lane-strided partial
-// sums, then a shuffle tree); every lane gets the result.
-__device__ double wave_sum_f64(const double* a, int count) {
-  const int lane = threadIdx.x % kWave;
-  double v = 0.0;
-  for (int q = lane; q < count; q += kWave) v += a[q];
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_down(v, o, kWave);
-  return __shfl(v, 0, kWave);
+// Lazy exact accumulation of non-negative doubles into kExLimbs 64-bit
+// limbs in LDS (each limb collects 32-bit chunks; the carries are taken
+// when the block's partial is written).  A thread first adds its terms into
+// a window of four limbs in registers, anchored one limb below its first
+// term (the terms of one sum are mostly of similar size); a term outside the
+// window goes to LDS at once, the window at the end (flush).
+struct ExWindow {
+  int base = -1;
+  unsigned long long r0 = 0, r1 = 0, r2 = 0, r3 = 0;
+};
+
+__device__ __forceinline__ void ex_accumulate(unsigned long long* acc, ExWindow& win,
+                                              double x) {
+  int limb;
+  uint32_t c0, c1, c2;
+  if (!ex_chunks(x, limb, c0, c1, c2)) return;
+  if (win.base < 0) win.base = limb > 0 ? limb - 1 : 0;
+  const int o = limb - win.base;
+  if (o == 0 || o == 1) {
+    const unsigned long long a0 = c0, a1 = c1, a2 = c2;
+    win.r0 += o == 0 ? a0 : 0ull;
+    win.r1 += o == 0 ? a1 : a0;
+    win.r2 += o == 0 ? a2 : a1;
+    win.r3 += o == 0 ? 0ull : a2;
+    return;
+  }
+  atomicAdd(acc + limb, (unsigned long long)c0);
+  if (c1) atomicAdd(acc + limb + 1, (unsigned long long)c1);
+  if (c2) atomicAdd(acc + limb + 2, (unsigned long long)c2);
+}
+
+__device__ __forceinline__ void ex_flush(unsigned long long* acc, const ExWindow& win) {
+  if (win.base < 0) return;
+  if (win.r0) atomicAdd(acc + win.base, win.r0);
+  if (win.r1) atomicAdd(acc + win.base + 1, win.r1);
+  if (win.r2) atomicAdd(acc + win.base + 2, win.r2);
+  if (win.r3) atomicAdd(acc + win.base + 3, win.r3);
 }
 
 // ------------------------------------------------------------ helpers ---
@@ -256,6 +284,8 @@ __global__ void k_init_slots(ChainSet set, DevState d, int clear_tgt) {
     ChainState z = {};
     d.cs[s] = z;
   }
+  if (d.gx && clear_tgt && blockIdx.x == 0)  // G of the empty placement
+    for (int q = threadIdx.x; q < 2 * kExLimbs; q += blockDim.x) d.gx[s * 2 * kExLimbs + q] = 0;
 }
 
 __global__ void k_holder_build(ChainSet set, DevState d) {
@@ -345,8 +375,11 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
   }
   if (d.f64) {
     // Eq. 7 on doubles: requester terms added in increasing r, each product
-    // rounded on its own; the incumbent value as per-block partial sums
-    double p = 0.0;
+    // rounded on its own.  The acceptance test evaluates G exactly (in
+    // k_gexact); the incumbent's value sum_{b in T_h} p_h(b) and the scale
+    // sum Lambda * w summed here (in any order) only let k_backtrack reject
+    // an update early when no rounding could make it acceptable.
+    double p = 0.0, wl = 0.0;
     bool in_th = false;
     if (i < n) {
       for (int r = 0; r < d.m; ++r) {
@@ -355,12 +388,17 @@ __global__ void __launch_bounds__(256) k_gains(ChainSet set, DevState d, int gmo
         const double L = as_f(d.lam[(int64_t)r * n + i]);
         const double term = L * dpos(as_f(saving(d, h, r, i)) - vmh);
         p = p + term;
+        wl = wl + L * as_f(d.w[(int64_t)r * n + i]);
       }
       d.profit[s * n + i] = as_i(p);
       in_th = d.tgt[ps * mn + (int64_t)h * n + i] != 0;
     }
     const double sh = block_sum_f64(in_th ? p : 0.0);
-    if (threadIdx.x == 0) d.fpart[s * d.fpart_stride + blockIdx.x] = sh;
+    const double sw = block_sum_f64(wl);
+    if (threadIdx.x == 0) {
+      if (sh != 0.0) atomicAdd((double*)&d.cs[s].inc, sh);
+      if (sw != 0.0) atomicAdd((double*)&d.cs[s].wsum, sw);
+    }
     return;
   }
   int64_t p = 0, g = 0, held = 0;
@@ -1340,21 +1378,37 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   const int64_t dpval = st->dpval;
   bool accept;
   if (d.f64) {
-    // G(T_-h, T'_h) > G(T) + eps with Proposition 1: DP value > incumbent
-    // value + eps; the incumbent value is summed from k_gains' per-block
-    // partials in a fixed order.  A replacement is counted (improved,
-    // accepts) by k_commit only if it changes the set, so that rounding
-    // alone never accepts the incumbent set again.
-    accept = true;
-    if (mode != kModeGreedy) {
-      const double inc = wave_sum_f64(d.fpart + slot * d.fpart_stride,
-                                      (n + 255) / 256);
-      accept = as_f(dpval) > inc + d.eps;
+    // Real-valued costs: the decision, on the exact G of the placement with
+    // T'_h against the exact G(T) + eps (Algorithm 1's test evaluated from
+    // scratch), is k_gexact_final's, which also sets the acceptance marks.
+    // A refinement update is rejected here, without its walk, when its DP
+    // value stays below the incumbent's value + eps by more than E, a bound
+    // on how far the rounded sums can be from that exact difference of G
+    // (Proposition 1): each marginal is within (M + 4) u W_b of the exact
+    // difference of its chunk's rounded terms (u = 2^-53, W_b = sum over
+    // requesters of Lambda * w), each of the two sums of at most k' of them
+    // adds k' u of its total, and denormal terms add at most 2^-1074 per
+    // rounding.
+    const double dv = as_f(dpval), inc = as_f(st->inc), wsum = as_f(st->wsum);
+    bool early = false;
+    if (mode == kModeRefine) {
+      const double u = 0x1p-53;
+      const double e = 1.25 * (d.m + 8.0 + 2.0 * kp) * u * wsum + 2.0 * u * d.eps +
+                       (double)n * (d.m + 4.0) * 0x1p-1070;
+      early = dv + e < inc + d.eps;
     }
     if (lane == 0) {
-      st->accept = accept ? 1 : 0;
-      st->changed = 0;
+      st->accept = 0;
+      st->inc = 0;
+      st->wsum = 0;
+      st->rejected = early ? 1 : 0;
     }
+    if (early) return;
+    const int nwords = d.npad / 32;
+    uint32_t* selw = d.sel + slot * nwords;
+    for (int q = lane; q < nwords; q += kWave) selw[q] = 0;
+    if (kp <= 0) return;
+    accept = true;
   } else {
     const int64_t inc = st->inc;
     accept = (mode == kModeGreedy) || (dpval > inc);
@@ -1368,18 +1422,18 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     }
   }
   if (!accept) return;
-  if (lane == 0) {
-    // every other worker's marginals change with worker h's set (an
-    // accepted real-valued replacement may leave the set as it was: then
-    // the marks only cost those workers a sweep)
-    const int h = set.worker[ci];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
-  }
   const int nwords = d.npad / 32;
   uint32_t* selw = d.sel + slot * nwords;
-  for (int q = lane; q < nwords; q += kWave) selw[q] = 0;
-  if (kp <= 0) return;
+  if (!d.f64) {
+    if (lane == 0) {
+      // every other worker's marginals change with worker h's set
+      const int h = set.worker[ci];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
+    }
+    for (int q = lane; q < nwords; q += kWave) selw[q] = 0;
+    if (kp <= 0) return;
+  }
 
   const int nwin = (n + kWin - 1) / kWin;  // windows = sweep batches
   const int64_t cstride = 2 * (int64_t)d.npad;
@@ -1533,14 +1587,6 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
     changed = nv != th[i];
   }
   if (!__syncthreads_or(changed)) return;
-  if (d.f64 && mode == kModeRefine && threadIdx.x == 0 &&
-      __hip_atomic_load(&d.cs[s].changed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0 &&
-      atomicExch(&d.cs[s].changed, 1) == 0) {
-    // the first block that sees a change counts the replacement (the plain
-    // load keeps the other blocks off the atomic)
-    d.cs[s].improved = 1;
-    d.cs[s].accepts += 1;
-  }
   if (changed) {
     const int64_t o = s * mn + (int64_t)r * n + i;
     const int64_t wr = d.w[(int64_t)r * n + i];
@@ -1615,6 +1661,11 @@ __global__ void __launch_bounds__(256) k_adopt(DevState d, int32_t s, int32_t fr
     const uint32_t* src = d.sel + (int64_t)from * nwords;
     uint32_t* dst = d.sel + (int64_t)s * nwords;
     for (int q = threadIdx.x; q < nwords; q += blockDim.x) dst[q] = src[q];
+    if (d.f64) {
+      // the exact G with the adopted replacement becomes the start's G
+      for (int q = threadIdx.x; q < kExLimbs; q += blockDim.x)
+        d.gx[(s * 2) * kExLimbs + q] = d.gx[((int64_t)from * 2 + 1) * kExLimbs + q];
+    }
   }
   if (threadIdx.x == 0) {
 #pragma unroll
@@ -1624,12 +1675,8 @@ __global__ void __launch_bounds__(256) k_adopt(DevState d, int32_t s, int32_t fr
       st->accept = 1;
       st->inc = 0;
       st->dpval = fs.dpval;
-      if (d.f64) {
-        st->changed = 0;  // k_commit counts the replacement if the set changes
-      } else {
-        st->improved = 1;
-        st->accepts += 1;
-      }
+      st->improved = 1;
+      st->accepts += 1;
 #pragma unroll
       for (int q = 0; q < 8; ++q)
         st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
@@ -1680,8 +1727,12 @@ __global__ void __launch_bounds__(256) k_mat_cost(DevState d, int64_t inc, int64
   const uint8_t* tp = d.tgt + prop * mn;
   if (d.f64) {
     // the same minimum on bit patterns (non-negative doubles order like
-    // them); per-block sums of doubles in a fixed order
-    double a = 0.0;
+    // them); the cost summed exactly, lazy per-block partials of kExLimbs
+    // 64-bit limbs
+    __shared__ unsigned long long acc[kExLimbs];
+    for (int q = threadIdx.x; q < kExLimbs; q += blockDim.x) acc[q] = 0;
+    __syncthreads();
+    ExWindow win;
     for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
          x += (int64_t)gridDim.x * blockDim.x) {
       if (!tp[x] || ti[x]) continue;
@@ -1693,10 +1744,12 @@ __global__ void __launch_bounds__(256) k_mat_cost(DevState d, int64_t inc, int64
           const int64_t fh = d.f[((int64_t)h * d.m + r) * n + i];
           if (fh < c) c = fh;
         }
-      a += as_f(c);
+      ex_accumulate(acc, win, as_f(c));
     }
-    const double t = block_sum_f64(a);
-    if (threadIdx.x == 0) ((double*)partial)[blockIdx.x] = t;
+    ex_flush(acc, win);
+    __syncthreads();
+    uint64_t* out = (uint64_t*)partial + (int64_t)blockIdx.x * kExLimbs;
+    for (int q = threadIdx.x; q < kExLimbs; q += blockDim.x) out[q] = acc[q];
     return;
   }
   unsigned __int128 acc = 0;
@@ -1731,24 +1784,11 @@ __global__ void k_reset_round(ChainSet set, DevState d) {
 
 // ----------------------------------------------------------- objective --
 
-// F_pair(T) = sum_{m,b} Lambda_m(b) * v1_m(b)   (Eq. 6).  Real-valued
-// costs: per-block partial sums, added by k_objective_final in a fixed
-// order (the same placement always gets the same value).
+// F_pair(T) = sum_{m,b} Lambda_m(b) * v1_m(b)   (Eq. 6), integer costs.
 __global__ void __launch_bounds__(256) k_objective(ChainSet set, DevState d) {
   const int ci = blockIdx.y;
   const int64_t s = set.slot[ci];
   const int64_t mn = (int64_t)d.m * d.n;
-  if (d.f64) {
-    double a = 0.0;
-    for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
-         x += (int64_t)gridDim.x * blockDim.x) {
-      const double term = as_f(d.lam[x]) * as_f(d.v1[s * mn + x]);
-      a = a + term;
-    }
-    const double t = block_sum_f64(a);
-    if (threadIdx.x == 0) d.fpart[s * d.fpart_stride + blockIdx.x] = t;
-    return;
-  }
   int64_t acc = 0;
   for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
        x += (int64_t)gridDim.x * blockDim.x)
@@ -1758,10 +1798,130 @@ __global__ void __launch_bounds__(256) k_objective(ChainSet set, DevState d) {
     atomicAdd((unsigned long long*)&d.cs[s].obj, (unsigned long long)t);
 }
 
-__global__ void k_objective_final(ChainSet set, DevState d, int32_t nblocks) {
-  const int64_t s = set.slot[blockIdx.x];
-  const double g = wave_sum_f64(d.fpart + s * d.fpart_stride, nblocks);
-  if (threadIdx.x == 0) d.cs[s].obj = as_i(g);
+// Real-valued costs: G (Eq. 6) as the exact sum of its rounded terms, so
+// that every comparison of objectives is independent of summation order.
+// replace = 0: the slot's own placement, terms Lambda_r(b) * v1_r(b).
+// replace = 1: the update's placement, worker h's set replaced by the
+// backtracked selection T'_h: terms Lambda_r(b) * max(v_r^{(-h)}(b),
+// [b in T'_h] q_{r<-h}(b)), v^{(-h)} from the source slot's top-2 holder
+// state (the same values the oracle's maximum over holders gives).
+// Per-block lazy partial sums go to d.gxp.
+__global__ void __launch_bounds__(256) k_gexact(ChainSet set, DevState d, int replace) {
+  const int ci = blockIdx.y;
+  const int64_t s = set.slot[ci];
+  if (replace && (d.cs[s].skip || d.cs[s].rejected)) return;  // already rejected
+  __shared__ unsigned long long acc[kExLimbs];
+  for (int q = threadIdx.x; q < kExLimbs; q += blockDim.x) acc[q] = 0;
+  __syncthreads();
+  const int64_t ps = set.src[ci];
+  const int h = set.worker[ci];
+  const int64_t n = d.n, mn = (int64_t)d.m * n;
+  const uint32_t* selw = d.sel + s * (d.npad / 32);
+  ExWindow win;
+  for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mn;
+       x += (int64_t)gridDim.x * blockDim.x) {
+    double best;
+    if (replace) {
+      const int r = (int)(x / n);
+      const int64_t i = x - (int64_t)r * n;
+      const int64_t o = ps * mn + x;
+      best = as_f((d.h1[o] == h) ? d.v2[o] : d.v1[o]);
+      if ((selw[i >> 5] >> (i & 31)) & 1u) {
+        const double q = as_f(saving(d, h, r, i));
+        best = q > best ? q : best;
+      }
+    } else {
+      best = as_f(d.v1[s * mn + x]);
+    }
+    ex_accumulate(acc, win, as_f(d.lam[x]) * best);
+  }
+  ex_flush(acc, win);
+  __syncthreads();
+  if (threadIdx.x == 0) {  // carry the block's limbs: each below 2^32 after
+    unsigned long long carry = 0;
+    for (int q = 0; q < kExLimbs; ++q) {
+      const unsigned long long v = acc[q] + carry;
+      acc[q] = v & 0xFFFFFFFFull;
+      carry = v >> 32;
+    }
+  }
+  __syncthreads();
+  uint64_t* part = d.gxp + ((int64_t)ci * d.gx_blocks + blockIdx.x) * kExLimbs;
+  for (int q = threadIdx.x; q < kExLimbs; q += blockDim.x) part[q] = acc[q];
+}
+
+// One block per chain: the exact G from k_gexact's partials (carried into
+// canonical limbs), then
+//   kModeGreedy: the update is adopted: gx[slot][0] = G, acceptance marks;
+//   kModeRefine: Algorithm 1's test, exact G(T_-h, T'_h) > exact G(T) +
+//                eps with G(T) that of the source slot; on acceptance the
+//                replacement is counted, the other workers' inputs marked
+//                stale, and (in the start's own slot) G(T) updated;
+//   otherwise:   the slot's objective, gx[slot][0] = G and its nearest
+//                double in cs.obj.
+// gx[slot][1] always receives G.
+__global__ void __launch_bounds__(256) k_gexact_final(ChainSet set, DevState d, int mode,
+                                                      int nblocks) {
+  const int ci = blockIdx.x;
+  const int64_t s = set.slot[ci];
+  const bool update = mode == kModeGreedy || mode == kModeRefine;
+  if (update && (d.cs[s].skip || d.cs[s].rejected)) return;
+  // the blocks' partials are carried limbs (each below 2^32), so a limb's
+  // sum over at most kGexactBlocks of them stays below 2^41
+  __shared__ unsigned long long tot[kExLimbs];
+  __shared__ uint32_t g[kExLimbs];
+  for (int q = threadIdx.x; q < kExLimbs; q += blockDim.x) tot[q] = 0;
+  __syncthreads();
+  const uint64_t* part = d.gxp + (int64_t)ci * d.gx_blocks * kExLimbs;
+  const int count = nblocks * kExLimbs;
+  constexpr int kUnroll = 4;  // loads in flight per thread
+  for (int x0 = threadIdx.x; x0 < count; x0 += kUnroll * blockDim.x) {
+    uint64_t v[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const int x = x0 + k * blockDim.x;
+      v[k] = x < count ? part[x] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k)
+      if (v[k]) atomicAdd(&tot[(x0 + k * blockDim.x) % kExLimbs], (unsigned long long)v[k]);
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  unsigned long long carry = 0;
+  for (int q = 0; q < kExLimbs; ++q) {
+    const unsigned long long v = tot[q] + carry;
+    g[q] = (uint32_t)v;
+    carry = v >> 32;
+  }
+  uint32_t* cur = d.gx + (s * 2) * kExLimbs;
+  uint32_t* nxt = d.gx + (s * 2 + 1) * kExLimbs;
+  for (int q = 0; q < kExLimbs; ++q) nxt[q] = g[q];
+  ChainState* st = d.cs + s;
+  if (!update) {
+    for (int q = 0; q < kExLimbs; ++q) cur[q] = g[q];
+    st->obj = (int64_t)ex_round_bits(g);
+    return;
+  }
+  const int64_t ps = set.src[ci];
+  bool accept = true;
+  if (mode == kModeRefine) {
+    uint32_t bar[kExLimbs];
+    const uint32_t* gs = d.gx + (ps * 2) * kExLimbs;
+    for (int q = 0; q < kExLimbs; ++q) bar[q] = gs[q];
+    ex_add_double(bar, d.eps);
+    accept = ex_cmp(g, bar) > 0;
+  }
+  st->accept = accept ? 1 : 0;
+  if (!accept) return;
+  if (mode == kModeRefine) {
+    st->improved = 1;
+    st->accepts += 1;
+  }
+  const int h = set.worker[ci];
+  for (int q = 0; q < 8; ++q) st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
+  if (s == ps)
+    for (int q = 0; q < kExLimbs; ++q) cur[q] = g[q];
 }
 
 inline dim3 grid1(int64_t work, int bs, int rows) {
@@ -1824,13 +1984,6 @@ hipError_t launch_validate_f64(const double* lam, const double* w,
   hipLaunchKernelGGL(k_validate_f64, dim3((unsigned)b), dim3(256), 0, st, lam, w, f,
                      mn, mmn, bad);
   return hipGetLastError();
-}
-
-int32_t fpart_blocks(int32_t n, int32_t m) {
-  // k_gains: one block per 256 chunks; k_objective: up to 1024 blocks
-  const int64_t gains = ((int64_t)n + 255) / 256;
-  const int64_t obj = std::min<int64_t>(((int64_t)m * n + 255) / 256, 1024);
-  return (int32_t)std::max<int64_t>(std::max(gains, obj), 1);
 }
 
 hipError_t launch_init_slots(const ChainSet& set, const DevState& d,
@@ -1987,15 +2140,35 @@ hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
 
 hipError_t launch_objective(const ChainSet& set, const DevState& d,
                             hipStream_t st) {
+  if (d.f64) return launch_gexact(set, d, -1, st);
   int64_t mn = (int64_t)d.m * d.n;
   int64_t b = (mn + 255) / 256;
   if (b > 1024) b = 1024;
   hipLaunchKernelGGL(k_objective, dim3((unsigned)b, set.count), dim3(256), 0,
                      st, set, d);
-  if (d.f64) {
-    hipLaunchKernelGGL(k_objective_final, dim3(set.count), dim3(kWave), 0, st,
-                       set, d, (int32_t)b);
-  }
+  return hipGetLastError();
+}
+
+int32_t gexact_blocks(int32_t n, int32_t m) {
+  // 128 blocks per chain, more only where a block would otherwise sum more
+  // than 2^30 terms (its lazy 64-bit limbs take at most one 32-bit chunk
+  // per term); never more than one block per 256 terms
+  const int64_t mn = (int64_t)m * n;
+  const int64_t need = (mn + (1ll << 30) - 1) >> 30;
+  const int64_t b = std::min<int64_t>((mn + 255) / 256, std::max<int64_t>(128, need));
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(b, kGexactBlocks));
+}
+
+hipError_t launch_gexact(const ChainSet& set, const DevState& d, int mode,
+                         hipStream_t st) {
+  if (set.count == 0) return hipSuccess;
+  const int32_t b = gexact_blocks(d.n, d.m);
+  if (b > d.gx_blocks) return hipErrorInvalidValue;
+  const int replace = (mode == kModeGreedy || mode == kModeRefine) ? 1 : 0;
+  hipLaunchKernelGGL(k_gexact, dim3((unsigned)b, set.count), dim3(256), 0, st, set, d,
+                     replace);
+  hipLaunchKernelGGL(k_gexact_final, dim3(set.count), dim3(256), 0, st, set, d, mode,
+                     (int)b);
   return hipGetLastError();
 }
 

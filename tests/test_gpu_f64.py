@@ -3,11 +3,12 @@ the refinement tolerance epsilon) against the CPU oracle.
 
 On integer-valued doubles every sum is exact, so the GPU must reproduce the
 integer planner bit for bit -- checked on all five benchmark workloads at
-full size against the oracle's stored plans.  On real values the profits,
-DP values, standalone scores, orders, sweep and accept counts and placements
-are bit-exact; objectives are sums taken in a different order on the GPU, so
-they agree to a relative 1e-12.  The tolerance is chosen far above rounding
-so that no acceptance decision sits within rounding of its threshold.
+full size against the oracle's stored plans.  On real values everything is
+bit-exact too: profits, DP values, standalone scores, orders, sweep and
+accept counts, placements, and the objectives, which both sides evaluate as
+the exact sum of their rounded terms (reading R26), so that no decision
+depends on a summation order -- also at epsilon = 0, where a replacement of
+exactly equal value must be rejected.
 """
 
 import hashlib
@@ -37,10 +38,10 @@ def _same_real(g, o):
     np.testing.assert_array_equal(g.orders, o.orders)
     np.testing.assert_array_equal(g.start_sweeps, o.start_sweeps)
     np.testing.assert_array_equal(g.start_accepts, o.start_accepts)
-    np.testing.assert_allclose(g.start_objective, o.start_objective, rtol=1e-12)
+    np.testing.assert_array_equal(g.start_objective, o.start_objective)
     assert g.best_start == o.best_start
     assert g.updates == o.updates and g.dp_cells == o.dp_cells
-    assert g.objective == pytest.approx(o.objective, rel=1e-12)
+    assert g.objective == o.objective
     np.testing.assert_array_equal(g.target, o.target)
 
 
@@ -78,18 +79,56 @@ def test_plan_f64_random_reals(oracle_mod, seed):
     _same_real(g, o)
 
 
-def test_plan_f64_zero_tolerance_terminates(oracle_mod):
-    """epsilon = 0 on real values: a replacement that reproduces the worker's
-    set is never counted, so refinement stops; the result is a valid plan."""
-    rng = np.random.default_rng(17)
-    inst = W.random_instance(400, 5, rng, kmax=60)
-    lam, w, f = W.real_valued(inst, 3, jitter=0.5)
-    g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=0.0, n_starts=3)
-    assert g.objective == pytest.approx(
-        oracle_mod.objective_f64(lam, w, f, g.target), rel=1e-12)
-    greedy = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, n_starts=3,
-                           flags=B.PP_F_NO_REFINE)
-    assert np.all(g.start_objective >= greedy.start_objective * (1 - 1e-12))
+def _valid_local_optimum(oracle_mod, parent, lam, w, f, cap, target):
+    """Every row parent-closed and within capacity, and no worker's exact
+    replacement (its marginals against the others, the rooted-tree DP)
+    raises the exact objective: the placement refinement stops at."""
+    from fractions import Fraction
+
+    m, n = lam.shape
+    for h in range(m):
+        row = target[h]
+        assert int(row.sum()) <= min(int(cap[h]), n)
+        for v in np.flatnonzero(row):
+            assert parent[v] < 0 or row[parent[v]], f"worker {h}: parent of {v} missing"
+
+    def exact_g(t):
+        best = np.zeros((m, n))
+        for hh in range(m):
+            for r in range(m):
+                q = w[r] if hh == r else np.maximum(w[r] - f[hh, r], 0.0)
+                best[r] = np.where(t[hh] != 0, np.maximum(best[r], q), best[r])
+        return sum((Fraction(float(x)) for x in (lam * best).ravel()), Fraction(0))
+
+    g = exact_g(target)
+    for h in range(m):
+        t = target.copy()
+        t[h] = 0
+        p = oracle_mod.marginal_f64(lam, w, f, t, h)
+        t[h] = oracle_mod.rooted_dp_f64(parent, p, int(cap[h]))[0]
+        assert exact_g(t) <= g
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_plan_f64_zero_tolerance_matches_oracle(oracle_mod, seed):
+    """epsilon = 0 on real values (Algorithm 1's strict test with no slack):
+    bit-exact against the oracle, including the replacements that differ
+    from the worker's set only by chunks of zero marginal value -- exactly
+    the same objective, to be rejected whatever two rounded sums would say
+    -- and the result is a valid local optimum."""
+    rng = np.random.default_rng(800 + seed)
+    m = int(rng.integers(2, 6))
+    n = int(rng.integers(5, 200))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, n + 2])),
+                             source_dependent=bool(seed % 4))
+    lam, w, f = W.real_valued(inst, seed, jitter=0.5)
+    kw = dict(n_starts=int(rng.integers(1, 4)), max_rounds=0,
+              order_seed=int(rng.integers(0, 2 ** 62)))
+    g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=0.0, **kw)
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=0.0, **kw)
+    _same_real(g, o)
+    if seed % 4 == 0:
+        _valid_local_optimum(oracle_mod, inst.parent, lam, w, f, inst.cap, g.target)
 
 
 def _golden(name):
@@ -200,10 +239,8 @@ def test_tree50k_real_valued_golden():
     assert p.start_accepts.tolist() == gold["start_accepts"]
     assert p.best_start == gold["best_start"]
     assert (p.updates, p.dp_cells) == (gold["updates"], gold["dp_cells"])
-    np.testing.assert_allclose(p.start_objective,
-                               [float.fromhex(x) for x in gold["start_objective"]],
-                               rtol=1e-12)
-    assert p.objective == pytest.approx(float.fromhex(gold["objective"]), rel=1e-12)
+    assert p.start_objective.tolist() == [float.fromhex(x) for x in gold["start_objective"]]
+    assert p.objective == float.fromhex(gold["objective"])
     rows = [hashlib.sha256(np.ascontiguousarray(target[h]).tobytes()).hexdigest()
             for h in range(inst.m)]
     assert rows == gold["target_row_sha256"]
@@ -232,8 +269,7 @@ def test_safeguards_f64_random(oracle_mod, seed):
     g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
     o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
     assert o.safeguards_run and g.safeguards_run
-    np.testing.assert_allclose(g.safeguard_objective, o.safeguard_objective,
-                               rtol=1e-12)
+    assert g.safeguard_objective == o.safeguard_objective
     _same_real(g, o)
 
 

@@ -152,11 +152,12 @@ def test_replan_tree50k_golden():
 # ---------------------------------------------------------- real-valued costs
 
 def _same_f64(g, o):
+    """Objectives and the cost are exact sums rounded once (reading R26):
+    bit for bit on both sides."""
     assert g.adopt == o.adopt
-    assert g.incumbent_objective == pytest.approx(o.incumbent_objective, rel=1e-12)
-    assert g.proposal_objective == pytest.approx(o.proposal_objective, rel=1e-12)
-    assert g.materialization_cost == pytest.approx(o.materialization_cost,
-                                                   rel=1e-12, abs=0.0)
+    assert g.incumbent_objective == o.incumbent_objective
+    assert g.proposal_objective == o.proposal_objective
+    assert g.materialization_cost == o.materialization_cost
     np.testing.assert_array_equal(g.proposal, o.proposal)
     np.testing.assert_array_equal(g.target, o.target)
 
