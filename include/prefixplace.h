@@ -223,8 +223,8 @@ int pp_rooted_dp_f64(int32_t n, const int32_t *parent, const double *profit,
 
 /* Epoch re-planning (Sec. IV-D): when demand or routing changes, plan the
  * refreshed inputs (as pp_plan, same options), evaluate the incumbent under
- * them, and adopt the new plan only if the saving predicted over the horizon
- * exceeds the one-time cost of materializing the newly assigned chunks:
+ * them, and switch to the new plan only when its gain per epoch over the
+ * horizon pays for copying in the chunks it newly assigns:
  *   adopt  iff  horizon * (G(T') - G(T)) > sum over (m, b) with b in T'_m
  *               and not in T_m of c_m(b),
  *   c_m(b) = min(w_m(b), min over workers h != m holding b in the

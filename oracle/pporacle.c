@@ -16,9 +16,9 @@
  *     order-diverse starts, best-candidate return   Sec. IV-B/IV-C, Theorem 3, Algorithm 1 (PrefixPlace)
  *   - comparator safeguards for requester-side
  *     costs (Independent, Popularity, LocalDedup)   Sec. IV-C, Algorithm 1; Sec. V-A (comparators)
- *   - epoch re-planning: adopt a re-optimized plan
- *     only if the horizon saving exceeds the one-
- *     time cost of materializing new chunks         Sec. IV-D; Sec. V-A (break-even requests)
+ *   - epoch re-planning: switch to a fresh plan when
+ *     its gain over the horizon pays for copying in
+ *     the chunks it newly assigns                   Sec. IV-D; Sec. V-A (break-even requests)
  *   - the same planner on real-valued costs with the
  *     refinement tolerance epsilon                  Sec. IV-C, Algorithm 1 (REQUIRE: tolerance)
  *

@@ -40,9 +40,10 @@ def test_rooted_dp_random(oracle_mod, seed):
     _dp_case(oracle_mod, parent, profit, k)
 
 
-@pytest.mark.parametrize("cells", [1, 2, 4, 8])
+@pytest.mark.parametrize("cells", [1, 2, 4])
 def test_rooted_dp_each_lane_width(oracle_mod, cells, monkeypatch):
-    """Every compiled cells-per-lane variant of the sweep."""
+    """Every compiled cells-per-lane variant of the sweep (1, 2 and 4 cells
+    per lane, forced through PP_DP_CELLS)."""
     monkeypatch.setenv("PP_DP_CELLS", str(cells))
     rng = np.random.default_rng(100 + cells)
     for n, k in ((1, 1), (70, 69), (3000, 1000), (2500, 2500)):

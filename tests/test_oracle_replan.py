@@ -1,8 +1,8 @@
-"""Oracle pins of the epoch re-planning rule (Sec. IV-D: evaluate the
-incumbent and a re-optimized plan under refreshed demand; adopt the new plan
-only if the saving predicted over the horizon exceeds the one-time cost of
-materializing newly assigned chunks; Sec. V-A defines break-even as that
-cost divided by the per-request gain).  CPU only.
+"""Oracle pins of the epoch re-planning rule (Sec. IV-D; break-even as in
+Sec. V-A): under refreshed demand both the incumbent placement and a freshly
+optimized one are evaluated, and the fresh one replaces the incumbent only
+when its gain per epoch, times the horizon, pays for copying in the chunks
+it newly assigns.  CPU only.
 
 The one-time cost is rebuilt here from its definition (reading R21: each new
 (worker, chunk) pays the cheaper of recomputation and a fetch from a worker
