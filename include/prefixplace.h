@@ -164,10 +164,13 @@ int32_t pp_num_starts(int32_t m, int32_t n_starts);
  *                            parent-closed with at most cap[m] ones
  *   objective                host out: F_pair(T) in request * us
  *   stats                    NULL or statistics
- * Limits: the DP sweep keeps pending skip-target rows in LDS slots; their
- * number (at most the tree depth; 14 and 17 on the 50,000-chunk benchmark
- * trees) must not exceed 254, and the rows must fit one compute unit's LDS
- * (up to 254 slots fit at one cell per lane), else PP_E_UNSUPPORTED. */
+ * Limits: the DP sweep keeps pending skip-target rows in LDS slots (their
+ * number is at most the tree depth; 14 and 17 on the 50,000-chunk benchmark
+ * trees).  Up to 254 stay in LDS; a deeper tree that branches along long
+ * chains has its long-lived pending rows spilled to device memory and
+ * restored ahead of their reads (pp_sweep_spills), so any depth is
+ * accepted; PP_E_UNSUPPORTED only if even then more than 254 LDS rows would
+ * be needed at once, or the rows do not fit one compute unit's LDS. */
 int pp_plan(int32_t n, int32_t m, const int32_t *parent, const int64_t *demand,
             const int64_t *recompute_cost, const int64_t *fetch_cost,
             const int32_t *cap, const pp_options *opt, uint8_t *target,
@@ -366,6 +369,31 @@ int pp_plan_f64_device(pp_ctx *ctx, int32_t n, int32_t m, const int32_t *parent,
  * first step's node is a leaf. */
 int pp_sweep_layout(int32_t n, const int32_t *parent, int32_t cells,
                     uint32_t *meta, int32_t *nsteps, int32_t *slots);
+
+/* Host only, for CPU-side checks of the DP sweep on deep trees.  The sweep
+ * keeps each pending skip row (a row that a later non-leaf row reads as its
+ * D[next(i)][*]) in an LDS slot; when a tree has more of them pending at
+ * once than the slots hold (deep trees that branch along long chains), the
+ * rows first read kSpillGap = 3 or more sweep batches (of 32 steps) after
+ * their store are spilled: stored to a temporary slot as usual, copied to
+ * device memory by the stage's I/O wave once their batch is done (and
+ * before it stages the batch after next), and copied back into a restore
+ * slot when it stages each later batch that reads them.  Writes nbatches
+ * (padded steps / 32), nspill (spill rows per stage; 0 = nothing spilled,
+ * then the lists are empty and the offsets zero), n_out and n_in (list
+ * entries); each of out_off, spill_out, in_off, spill_in may be NULL.
+ * out_off [nbatches + 1]: batch b copies out the entries
+ *   spill_out[2e], spill_out[2e + 1] = (LDS slot, spill index) for
+ *   e in [out_off[b], out_off[b + 1]);
+ * in_off [nbatches + 1]: batch b is staged after copying in the entries
+ *   spill_in[2e], spill_in[2e + 1] = (LDS slot, spill index) for
+ *   e in [in_off[b], in_off[b + 1]).
+ * The step metadata of pp_sweep_layout already names the temporary and
+ * restore slots.  Errors as pp_sweep_layout, PP_E_UNSUPPORTED if the
+ * pending rows exceed 254 LDS rows even with spilling. */
+int pp_sweep_spills(int32_t n, const int32_t *parent, int32_t *nbatches, int32_t *nspill,
+                    int32_t *n_out, int32_t *n_in, int32_t *out_off, int32_t *spill_out,
+                    int32_t *in_off, int32_t *spill_in);
 
 /* Exit row in pp_backtrack_table for a skip sequence that runs past the
  * last row. */

@@ -116,6 +116,8 @@ def lib() -> ctypes.CDLL:
         L.pp_orders.argtypes = [i32, i32, u64, _P, _P]
         L.pp_sweep_layout.argtypes = [i32, _P, i32, _P, _P, _P]
         L.pp_sweep_layout.restype = ctypes.c_int
+        L.pp_sweep_spills.argtypes = [i32, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+        L.pp_sweep_spills.restype = ctypes.c_int
         L.pp_backtrack_table.argtypes = [i32, _P, _P, _P]
         L.pp_backtrack_table.restype = ctypes.c_int
         L.pp_ctx_create.argtypes = [ctypes.POINTER(_P), ctypes.c_int]
@@ -440,6 +442,27 @@ def pp_sweep_layout(parent, cells):
     _check(lib().pp_sweep_layout(n, _p(parent), int(cells), _p(meta),
                                  ctypes.byref(ns), ctypes.byref(sl)))
     return meta, sl.value
+
+
+def pp_sweep_spills(parent):
+    """Spill schedule of the DP sweep for a deep tree (host only): returns
+    (nspill, out lists, in lists), each list one int32 [k][2] array of
+    (LDS slot, spill index) per sweep batch."""
+    parent = _c(parent, np.int32)
+    n = parent.shape[0]
+    nb, ns, no, ni = (ctypes.c_int32(0) for _ in range(4))
+    _check(lib().pp_sweep_spills(n, _p(parent), ctypes.byref(nb), ctypes.byref(ns),
+                                 ctypes.byref(no), ctypes.byref(ni), None, None, None, None))
+    out_off = np.zeros(nb.value + 1, np.int32)
+    in_off = np.zeros(nb.value + 1, np.int32)
+    outs = np.zeros((max(no.value, 1), 2), np.int32)
+    ins = np.zeros((max(ni.value, 1), 2), np.int32)
+    _check(lib().pp_sweep_spills(n, _p(parent), ctypes.byref(nb), ctypes.byref(ns),
+                                 ctypes.byref(no), ctypes.byref(ni), _p(out_off), _p(outs),
+                                 _p(in_off), _p(ins)))
+    per_out = [outs[out_off[b]:out_off[b + 1]] for b in range(nb.value)]
+    per_in = [ins[in_off[b]:in_off[b + 1]] for b in range(nb.value)]
+    return ns.value, per_out, per_in
 
 
 PP_BT_END = 0x7FFFFFFF

@@ -16,7 +16,9 @@
 #include <cstring>
 #include <memory>
 #include <new>
+#include <queue>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 using namespace pp;
@@ -101,7 +103,19 @@ struct TreeLayout {
   std::vector<int32_t> store, src;
   int32_t slots = 0;    // LDS stack rows the sweep needs
   bool identity = true; // caller ids are already in preorder
+  // Trees with more pending skip rows than the LDS slots hold (deep trees
+  // that branch along long chains): rows whose first read comes at least
+  // kSpillGap batches after their store are spilled to device memory.  Per
+  // sweep batch b, spill_out[out_off[b] .. out_off[b+1]) lists (LDS slot,
+  // spill index) pairs that the I/O wave copies out once batch b is done,
+  // and spill_in[in_off[b] .. in_off[b+1]) the (LDS slot, spill index) pairs
+  // it copies back in when it stages batch b.  nspill = 0: no spilling.
+  std::vector<int32_t> out_off, spill_out, in_off, spill_in;
+  int32_t nspill = 0;
 };
+
+int layout_sweep(TreeLayout& t);
+int layout_sweep_spilled(TreeLayout& t, int32_t pad, int32_t nsteps);
 
 int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
   for (int32_t v = 0; v < n; ++v) {
@@ -162,15 +176,20 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
       e[2] = nq < n ? t.ce[4 * (size_t)nq] : 0u;
     }
   }
-  // DP metadata.  Rows are 1-based positions i; nx(i) = next(i); row i is
-  // produced at padded step pad + n - i.  A row r = next(a) with r != a+1
-  // (a is no leaf) and r != n+1 is a far target: it is stored to an LDS
-  // slot at its own step, and a reader a reads it right after the store two
-  // steps before its own.  Every other row is stored to a sink row (step
-  // mod the sink row count).  Every few steps (the sink row count, at most
-  // kDpGatherMax) the stage gathers its last cell column from the rows those
-  // steps were stored to, so a slot becomes free after its last reader (the
-  // smallest a) has read it and after the gather of its group.
+  return layout_sweep(t);
+}
+
+// DP metadata.  Rows are 1-based positions i; nx(i) = next(i); row i is
+// produced at padded step pad + n - i.  A row r = next(a) with r != a+1
+// (a is no leaf) and r != n+1 is a far target: it is stored to an LDS
+// slot at its own step, and a reader a reads it right after the store two
+// steps before its own.  Every other row is stored to a sink row (step
+// mod the sink row count).  Every few steps (the sink row count, at most
+// kDpGatherMax) the stage gathers its last cell column from the rows those
+// steps were stored to, so a slot becomes free after its last reader (the
+// smallest a) has read it and after the gather of its group.
+int layout_sweep(TreeLayout& t) {
+  const int32_t n = t.n;
   auto nx = [&](int32_t i) { return t.nextpos[i - 1] + 1; };
   auto far = [&](int32_t a, int32_t r) { return r != a + 1 && r != n + 1; };
   std::vector<int32_t> last_user(n + 2, INT32_MAX), slot_of(n + 2, -1);
@@ -183,6 +202,11 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
   t.leaf.assign(nsteps, 1);
   t.store.assign(nsteps, -1);
   t.src.assign(nsteps, -1);
+  t.out_off.clear();
+  t.spill_out.clear();
+  t.in_off.clear();
+  t.spill_in.clear();
+  t.nspill = 0;
   // Free slots as a bitmap (the lowest is taken first), and slots waiting
   // for their release step: a release is due at most kDpGatherMax - 1 steps
   // ahead, so it waits in the bitmap of its step modulo kDpGatherMax.
@@ -209,7 +233,8 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
   };
   Slots free_slots, releases[kDpGatherMax];
   int32_t high = 0;
-  for (int32_t i = n; i >= 1; --i) {
+  bool overflow = false;
+  for (int32_t i = n; i >= 1 && !overflow; --i) {
     const int32_t s = pad + n - i;  // padded step of row i
     free_slots.absorb(releases[s % kDpGatherMax]);
     const int32_t r = nx(i);
@@ -230,9 +255,10 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
       if (free_slots.any()) {
         k = free_slots.take_lowest();
       } else {
-        if (high >= kMaxSlots)
-          return fail(PP_E_UNSUPPORTED,
-                      "tree needs more than 254 pending subtree boundaries");
+        if (high >= kMaxSlots) {
+          overflow = true;
+          break;
+        }
         k = high++;
       }
       slot_of[i] = k;
@@ -246,7 +272,174 @@ int build_tree(int32_t n, const int32_t* parent, TreeLayout& t) {
       }
     }
   }
-  t.slots = high;
+  if (!overflow) {
+    t.slots = high;
+    return PP_OK;
+  }
+  return layout_sweep_spilled(t, pad, nsteps);
+}
+
+// The sweep's slots when the pending skip rows do not fit the LDS slots.
+// A far target with a read issued kSpillGap or more batches after its store
+// is spilled: the compute wave stores it to a temporary slot as usual, which
+// also serves the reads issued in the batches before that; the I/O wave
+// copies it to device memory once its batch is done (and before it stages
+// the batch after next, so the slot is free again two batches on), and
+// copies it back into a restore slot when it stages each later batch that
+// issues a read of it (at the earliest once the batch two before is done,
+// so the restore slot must be free from the start of the batch before).
+// The compute wave's schedule is unchanged.  Slots and spill indices are
+// assigned by greedy interval colouring (lowest free index first) of their
+// lifetimes, half-open step intervals for slots and batch intervals for
+// spill indices.
+int layout_sweep_spilled(TreeLayout& t, int32_t pad, int32_t nsteps) {
+  const int32_t n = t.n;
+  const int32_t nb = nsteps / kDpBatch;
+  auto nx = [&](int32_t i) { return t.nextpos[i - 1] + 1; };
+  auto far = [&](int32_t a, int32_t r) { return r != a + 1 && r != n + 1; };
+  auto step_of = [&](int32_t i) { return pad + n - i; };
+  auto gather_end = [](int32_t sr) { return (sr / kDpGatherMax + 1) * kDpGatherMax; };
+  // a read of row r = next(a) is issued at step (step of a) - 2; its slot
+  // is recorded in src[(step of a) - 1]
+  std::vector<int32_t> is_target(n + 2, 0), last_early(n + 2, -1), last_issue(n + 2, -1);
+  std::vector<uint8_t> spilled(n + 2, 0);
+  for (int32_t a = n; a >= 1; --a) {
+    const int32_t r = nx(a);
+    if (!far(a, r)) continue;
+    const int32_t is = step_of(a) - 2, br = step_of(r) / kDpBatch;
+    is_target[r] = 1;
+    last_issue[r] = std::max(last_issue[r], is);
+    if (is / kDpBatch < br + kSpillGap)
+      last_early[r] = std::max(last_early[r], is);
+    else
+      spilled[r] = 1;
+  }
+  struct Iv {
+    int32_t lo, hi;  // live steps [lo, hi)
+    int32_t row, batch;
+    bool restore;
+  };
+  std::vector<Iv> iv;
+  std::unordered_map<int64_t, size_t> restore_of;  // (row, batch) -> interval
+  for (int32_t r = 1; r <= n; ++r) {
+    if (!is_target[r]) continue;
+    const int32_t sr = step_of(r), br = sr / kDpBatch;
+    int32_t hi = std::max(gather_end(sr), last_early[r] + 2);  // the early readers' steps
+    if (spilled[r]) hi = std::max(hi, (br + 2) * kDpBatch);
+    iv.push_back({sr, hi, r, br, false});
+  }
+  for (int32_t a = n; a >= 1; --a) {
+    const int32_t r = nx(a);
+    if (!far(a, r) || !spilled[r]) continue;
+    const int32_t is = step_of(a) - 2, b = is / kDpBatch;
+    if (b < step_of(r) / kDpBatch + kSpillGap) continue;  // served by the temporary slot
+    const int64_t key = (int64_t)r * nb + b;
+    auto it = restore_of.find(key);
+    if (it != restore_of.end()) {
+      iv[it->second].hi = std::max(iv[it->second].hi, is + 1);
+    } else {
+      restore_of[key] = iv.size();
+      iv.push_back({(b - 1) * kDpBatch, is + 1, r, b, true});
+    }
+  }
+  std::vector<size_t> ord(iv.size());
+  for (size_t k = 0; k < iv.size(); ++k) ord[k] = k;
+  std::stable_sort(ord.begin(), ord.end(),
+                   [&](size_t u, size_t v) { return iv[u].lo < iv[v].lo; });
+  // interval colouring over at most kMaxSlots slots
+  std::vector<int32_t> slot(iv.size(), -1), busy_until;
+  for (size_t k : ord) {
+    int32_t best = -1;
+    for (size_t q = 0; q < busy_until.size(); ++q)
+      if (busy_until[q] <= iv[k].lo) {
+        best = (int32_t)q;
+        break;
+      }
+    if (best < 0) {
+      if ((int32_t)busy_until.size() >= kMaxSlots)
+        return fail(PP_E_UNSUPPORTED,
+                    "tree needs more than 254 LDS rows for its pending skip rows "
+                    "even with spilling");
+      best = (int32_t)busy_until.size();
+      busy_until.push_back(0);
+    }
+    busy_until[best] = iv[k].hi;
+    slot[k] = best;
+  }
+  t.slots = (int32_t)busy_until.size();
+  // spill indices, live from the store's batch to the last read's batch
+  std::vector<int32_t> spill_idx(n + 2, -1);
+  {
+    std::vector<int32_t> rows;
+    for (int32_t r = n; r >= 1; --r)  // increasing store step
+      if (spilled[r]) rows.push_back(r);
+    using Busy = std::pair<int32_t, int32_t>;  // (last batch, index)
+    std::priority_queue<Busy, std::vector<Busy>, std::greater<Busy>> busy;
+    std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> freed;
+    int32_t count = 0;
+    for (int32_t r : rows) {
+      const int32_t lo = step_of(r) / kDpBatch;
+      while (!busy.empty() && busy.top().first < lo) {
+        freed.push(busy.top().second);
+        busy.pop();
+      }
+      int32_t k;
+      if (!freed.empty()) {
+        k = freed.top();
+        freed.pop();
+      } else {
+        k = count++;
+      }
+      busy.push({last_issue[r] / kDpBatch, k});
+      spill_idx[r] = k;
+    }
+    t.nspill = count;
+  }
+  // the step schedule and the per-batch copy lists
+  std::vector<int32_t> row_slot(n + 2, -1);
+  std::vector<std::vector<std::pair<int32_t, int32_t>>> outs(nb), ins(nb);
+  for (size_t k = 0; k < iv.size(); ++k) {
+    const Iv& v = iv[k];
+    if (v.restore) {
+      ins[v.batch].push_back({slot[k], spill_idx[v.row]});
+    } else {
+      row_slot[v.row] = slot[k];
+      if (spilled[v.row]) outs[v.batch].push_back({slot[k], spill_idx[v.row]});
+    }
+  }
+  for (int32_t i = n; i >= 1; --i) {
+    const int32_t s = step_of(i);
+    const int32_t r = nx(i);
+    t.leaf[s] = (r == i + 1) ? 1 : 0;
+    if (is_target[i]) t.store[s] = row_slot[i];
+    if (i > 1) {
+      const int32_t r2 = nx(i - 1);
+      if (far(i - 1, r2)) {
+        const int32_t b = (s - 1) / kDpBatch;  // batch issuing this read
+        int32_t k = row_slot[r2];
+        if (spilled[r2] && b >= step_of(r2) / kDpBatch + kSpillGap) {
+          auto it = restore_of.find((int64_t)r2 * nb + b);
+          k = it == restore_of.end() ? -1 : slot[it->second];
+        }
+        if (k < 0) return fail(PP_E_DEVICE, "internal: far row without a slot");
+        t.src[s] = k;
+      }
+    }
+  }
+  t.out_off.assign(nb + 1, 0);
+  t.in_off.assign(nb + 1, 0);
+  for (int32_t b = 0; b < nb; ++b) {
+    for (const auto& e : outs[b]) {
+      t.spill_out.push_back(e.first);
+      t.spill_out.push_back(e.second);
+    }
+    for (const auto& e : ins[b]) {
+      t.spill_in.push_back(e.first);
+      t.spill_in.push_back(e.second);
+    }
+    t.out_off[b + 1] = (int32_t)t.spill_out.size() / 2;
+    t.in_off[b + 1] = (int32_t)t.spill_in.size() / 2;
+  }
   return PP_OK;
 }
 
@@ -269,6 +462,8 @@ std::vector<uint32_t> encode_meta(const TreeLayout& t, int cells) {
 }
 
 int upload_meta(pp_ctx* c, const TreeLayout& t, int cells, hipStream_t st);
+int upload_spills(pp_ctx* c, const TreeLayout& t, DevState& d, int32_t slots,
+                  hipStream_t st);
 
 // ------------------------------------------------------------- orders ---
 
@@ -342,13 +537,14 @@ struct pp_ctx {
   // per-slot state
   DevBuf tgt, v1, v2, h1, profit, sel, bits, ring, cs;
   DevBuf partial, flag, gx, gxp;
+  DevBuf sp_lists, spill;  // spilled skip rows of deep trees
   uint32_t epoch = 0;
   std::vector<uint32_t> meta_host;  // source of the last metadata upload
   std::vector<hipEvent_t> events;
   ~pp_ctx() {
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
-                      &ring, &cs, &partial, &flag, &gx, &gxp})
+                      &ring, &cs, &partial, &flag, &gx, &gxp, &sp_lists, &spill})
       b->release();
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (own) (void)hipStreamDestroy(own);
@@ -958,6 +1154,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   }
   PP_TRY(upload_meta(c, t, cells, st));
   d.meta = c->meta.as<uint32_t>();  // upload_meta may have (re)allocated it
+  PP_TRY(upload_spills(c, t, d, slots, st));
 
   // --- standalone scores: each worker against the empty placement
   res.standalone.assign(m, 0);
@@ -1219,6 +1416,33 @@ int check_meta(const TreeLayout& t, const std::vector<uint32_t>& meta,
         (meta[q + 2] != 0u && meta[q + 2] != 0xFFFFFFFFu) || meta[q + 3] != 0u)
       return fail(PP_E_DEVICE, "internal: DP step metadata out of range");
   }
+  return PP_OK;
+}
+
+// Deep trees: the sweep's spill lists and the spilled rows' device memory
+// for `slots` chain slots of d.stages stages at d.cells cells per lane.
+int upload_spills(pp_ctx* c, const TreeLayout& t, DevState& d, int32_t slots,
+                  hipStream_t st) {
+  d.nspill = t.nspill;
+  d.sp_out_off = d.sp_out = d.sp_in_off = d.sp_in = nullptr;
+  d.spill = nullptr;
+  if (t.nspill == 0) return PP_OK;
+  const size_t a = t.out_off.size(), b = t.spill_out.size(), c2 = t.in_off.size(),
+               e = t.spill_in.size();
+  PP_TRY(c->sp_lists.ensure((a + b + c2 + e) * 4));
+  int32_t* base = c->sp_lists.as<int32_t>();
+  PP_HIP(hipMemcpyAsync(base, t.out_off.data(), a * 4, hipMemcpyHostToDevice, st));
+  if (b) PP_HIP(hipMemcpyAsync(base + a, t.spill_out.data(), b * 4, hipMemcpyHostToDevice, st));
+  PP_HIP(hipMemcpyAsync(base + a + b, t.in_off.data(), c2 * 4, hipMemcpyHostToDevice, st));
+  if (e)
+    PP_HIP(hipMemcpyAsync(base + a + b + c2, t.spill_in.data(), e * 4, hipMemcpyHostToDevice,
+                          st));
+  d.sp_out_off = base;
+  d.sp_out = base + a;
+  d.sp_in_off = base + a + b;
+  d.sp_in = base + a + b + c2;
+  PP_TRY(c->spill.ensure((size_t)slots * d.stages * t.nspill * 64 * d.cells * 8));
+  d.spill = c->spill.as<uint64_t>();
   return PP_OK;
 }
 
@@ -1497,6 +1721,33 @@ int pp_sweep_layout(int32_t n, const int32_t* parent, int32_t cells,
 
 static_assert(kCeEnd == PP_BT_END, "one end marker for the backtrack table");
 static_assert(kNoAllocScratchBytes == PP_NOALLOC_SCRATCH_BYTES, "one scratch size");
+
+int pp_sweep_spills(int32_t n, const int32_t* parent, int32_t* nbatches, int32_t* nspill,
+                    int32_t* n_out, int32_t* n_in, int32_t* out_off, int32_t* spill_out,
+                    int32_t* in_off, int32_t* spill_in) {
+  g_err[0] = 0;
+  return guarded([&]() -> int {
+    if (n < 1 || !parent || !nbatches || !nspill || !n_out || !n_in)
+      return fail(PP_E_ARG, "null pointer or n < 1");
+    TreeLayout t;
+    PP_TRY(build_tree(n, parent, t));
+    const int32_t nb = (int32_t)(t.leaf.size() / kDpBatch);
+    *nbatches = nb;
+    *nspill = t.nspill;
+    *n_out = (int32_t)t.spill_out.size() / 2;
+    *n_in = (int32_t)t.spill_in.size() / 2;
+    if (t.nspill == 0) {
+      if (out_off) std::fill(out_off, out_off + nb + 1, 0);
+      if (in_off) std::fill(in_off, in_off + nb + 1, 0);
+      return PP_OK;
+    }
+    if (out_off) std::copy(t.out_off.begin(), t.out_off.end(), out_off);
+    if (in_off) std::copy(t.in_off.begin(), t.in_off.end(), in_off);
+    if (spill_out) std::copy(t.spill_out.begin(), t.spill_out.end(), spill_out);
+    if (spill_in) std::copy(t.spill_in.begin(), t.spill_in.end(), spill_in);
+    return PP_OK;
+  });
+}
 
 int pp_backtrack_table(int32_t n, const int32_t* parent, uint32_t* table,
                        int64_t* rows) {
@@ -1790,6 +2041,7 @@ static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v
     PP_TRY(ensure_slots(c, d, 1, kp, cells));
     PP_TRY(upload_meta(c, t, cells, st));
     d.meta = c->meta.as<uint32_t>();  // upload_meta may have (re)allocated it
+    PP_TRY(upload_spills(c, t, d, 1, st));
     PP_TRY(c->up_lam.ensure((size_t)n * 8));
     PP_HIP(hipMemcpyAsync(c->up_lam.p, profit, (size_t)n * 8, hipMemcpyHostToDevice, st));
     PP_HIP(launch_gather(c->up_lam.as<int64_t>(), d.profit, 1, n,

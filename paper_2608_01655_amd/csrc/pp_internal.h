@@ -39,6 +39,9 @@ constexpr int dp_sink_rows(int cells) { return cells == 1 ? 16 : 4; }
 // rows falls in different banks.
 constexpr int64_t dp_row_stride(int cells) { return (int64_t)cells * 64 * 8 + 8; }
 constexpr int kMaxSlots = 254;
+// Deep trees whose pending skip rows exceed the LDS slots spill the rows
+// first read at least this many sweep batches after their store.
+constexpr int kSpillGap = 3;
 // The sweep runs steps in batches of kDpBatch; the step count is padded up
 // to a multiple of it with leading dummy steps (leaf, profit 0), so step s
 // of the tree is padded step s + pad, pad = nsteps - n.
@@ -223,6 +226,17 @@ struct DevState {
                             //   word 64*b + l = lane l's cell over sweep
                             //   batch b, bit 31-u = step 32*b + u
   uint64_t* ring;           // [slots][stages][n][2] stage boundary values
+  // Spilled skip rows (deep trees only; nspill = 0 otherwise): per sweep
+  // batch b, sp_out[2e], sp_out[2e+1] for e in [sp_out_off[b],
+  // sp_out_off[b+1]) = (temporary LDS slot, spill index) copied out once the
+  // batch is done; sp_in likewise (restore LDS slot, spill index) copied in
+  // when the batch is staged; spill = [slots][stages][nspill][64 * cells].
+  const int32_t* sp_out_off;
+  const int32_t* sp_out;
+  const int32_t* sp_in_off;
+  const int32_t* sp_in;
+  uint64_t* spill;
+  int32_t nspill;
   ChainState* cs;           // [slots]
   int32_t stages;           // stage stride of bits / ring
   int32_t cells;            // cells per lane of the DP sweep

@@ -701,7 +701,39 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     auto meta_at = [&](int t) -> uint4 {
       return (lane <= kBatch && t < nsteps) ? meta[t] : make_uint4(0u, 0u, 0u, 0u);
     };
+    // Spilled skip rows (deep trees): this stage's rows in device memory,
+    // one 64*C-value row per spill index, lane l holding cells l + 64c.
+    const bool spilling = d.nspill > 0;
+    uint64_t* spill_rows =
+        spilling ? d.spill + (slot * d.stages + g) * (int64_t)d.nspill * (kWave * C) : nullptr;
+    auto lds_cell = [&](int32_t row_slot, int c) -> int64_t* {
+      return (int64_t*)(rows + (int64_t)row_slot * kStride + c * kWave * 8 + lane * 8);
+    };
+    // copy-in of the rows that batch b reads from a restore slot, before
+    // its records are published (a lane's relaxed agent-scope accesses to
+    // one address stay in program order, so it reads what it spilled)
+    auto spill_in = [&](int b) {
+      for (int32_t e = d.sp_in_off[b]; e < d.sp_in_off[b + 1]; ++e) {
+        const int32_t rs = d.sp_in[2 * e], x = d.sp_in[2 * e + 1];
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+          *lds_cell(rs, c) =
+              (int64_t)ld_agent(spill_rows + (int64_t)x * (kWave * C) + c * kWave + lane);
+      }
+    };
+    // copy-out of the spilled rows batch b stored to temporary slots, once
+    // the batch is done (before the batch after next is staged)
+    auto spill_out = [&](int b) {
+      for (int32_t e = d.sp_out_off[b]; e < d.sp_out_off[b + 1]; ++e) {
+        const int32_t ts = d.sp_out[2 * e], x = d.sp_out[2 * e + 1];
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+          st_agent(spill_rows + (int64_t)x * (kWave * C) + c * kWave + lane,
+                   (uint64_t)*lds_cell(ts, c));
+      }
+    };
     auto stage = [&](int b, int64_t pv, uint64_t w0, uint64_t w1, uint4 mv) {
+      if (spilling) spill_in(b);
       if (lane <= kBatch) {
         const int64_t bnd = (int64_t)((w1 << 32) | (w0 & 0xFFFFFFFFull));
         StepView v;
@@ -728,6 +760,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
         st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
       }
+      if (spilling) spill_out(b);
     };
     if (lane == 0) sync[kDone] = 0;
     bool ok;
@@ -767,7 +800,9 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
         ++nstore;
         progress = true;
       }
-      if (nstage < nb && done >= nstage - 1) {
+      // (spilling: batch nstage-2's rows are copied out before batch
+      // nstage, which may overwrite their temporary slots, is staged)
+      if (nstage < nb && done >= nstage - 1 && (!spilling || nstore >= nstage - 1)) {
         if (ring_ok(a0, a1)) {
           stage(nstage, pa, a0, a1, ma);
           sync_set(kStaged, nstage + 1);

@@ -439,12 +439,43 @@ def random_forest(n: int, rng: np.random.Generator, p_root: float = 0.15,
     return out
 
 
+def caterpillar(depth: int) -> np.ndarray:
+    """Spine 0..depth-1 and one leaf per spine node (ids depth..2 depth-1);
+    the spine child has the smaller id, so in canonical preorder every
+    leaf follows the rest of the spine below its node (depth - 1 subtree
+    boundaries pending at once in the DP sweep)."""
+    return np.array([-1] + list(range(0, depth - 1)) + list(range(0, depth)),
+                    dtype=np.int32)
+
+
+def regenerated_conversation(n: int, rng: np.random.Generator) -> np.ndarray:
+    """A long multi-turn conversation (a chain of n // 2 turns) whose turns
+    were regenerated: the other nodes hang off uniformly random turns, one
+    at a time or as short chains of their own (each next node continues the
+    previous branch with probability 1/2).  Branch ids are larger than the
+    chain's, so a branch follows the rest of the conversation in preorder
+    and hundreds of subtree boundaries are pending at once."""
+    chain = n // 2
+    parent = [-1] + list(range(0, chain - 1))
+    for v in range(chain, n):
+        if v > chain and rng.random() < 0.5:
+            parent.append(v - 1)
+        else:
+            parent.append(int(rng.integers(0, chain)))
+    return np.array(parent, dtype=np.int32)
+
+
 def random_instance(n: int, m: int, rng: np.random.Generator, *,
                     kmax: int | None = None, source_dependent: bool = True,
                     value_range: int = 50, zero_frac: float = 0.2,
-                    shuffle: bool = True) -> Instance:
-    """Small random planner input with many ties (small integer ranges)."""
-    parent = random_forest(n, rng, shuffle=shuffle)
+                    shuffle: bool = True, parent: np.ndarray | None = None) -> Instance:
+    """Small random planner input with many ties (small integer ranges), on
+    a random forest or on the given tree."""
+    if parent is None:
+        parent = random_forest(n, rng, shuffle=shuffle)
+    else:
+        parent = np.asarray(parent, dtype=np.int32)
+        n = parent.shape[0]
     demand = rng.integers(0, value_range, size=(m, n)).astype(np.int64)
     demand[rng.random((m, n)) < zero_frac] = 0
     w = rng.integers(0, value_range, size=(m, n)).astype(np.int64)

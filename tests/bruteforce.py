@@ -22,14 +22,13 @@ def canonical_preorder(parent) -> list[int]:
     for v in range(n):
         kids[int(parent[v])].append(v)
     out: list[int] = []
-
-    def visit(v):
+    # depth first with an explicit stack (trees can be thousands deep):
+    # children pushed in decreasing id are popped in increasing id
+    stack = sorted(kids[-1], reverse=True)
+    while stack:
+        v = stack.pop()
         out.append(v)
-        for c in sorted(kids[v]):
-            visit(c)
-
-    for r in sorted(kids[-1]):
-        visit(r)
+        stack.extend(sorted(kids[v], reverse=True))
     return out
 
 

@@ -190,16 +190,18 @@ def _caterpillar(depth):
     return np.array(parent, np.int32)
 
 
-def test_pending_skip_rows_limit(L):
-    for depth, ok in ((250, True), (300, False)):
+def test_pending_skip_rows_beyond_the_lds_slots(L):
+    """Up to 254 pending skip rows stay in LDS slots; deeper trees spill the
+    long-lived ones to device memory instead of failing."""
+    for depth, spills in ((250, False), (300, True), (1000, True), (5000, True)):
         parent = _caterpillar(depth)
         n = parent.shape[0]
         lam = np.ones((1, n), np.int64)
         w = np.ones((1, n), np.int64)
         f = np.zeros((1, 1, n), np.int64)
-        call = lambda: B.pp_plan(parent, lam, w, f, np.array([5], np.int32),
-                                 n_starts=1, flags=B.PP_F_VALIDATE_ONLY)
-        if ok:
-            call()
-        else:
-            _expect(B.PP_E_UNSUPPORTED, call)
+        B.pp_plan(parent, lam, w, f, np.array([5], np.int32), n_starts=1,
+                  flags=B.PP_F_VALIDATE_ONLY)
+        meta, slots = B.pp_sweep_layout(parent, 1)
+        nspill = B.pp_sweep_spills(parent)[0]
+        assert (nspill > 0) == spills
+        assert slots <= 254 and (not spills or slots < 100)

@@ -29,6 +29,8 @@ BATCH = 32
 
 def replay(parent, profit, k, cells):
     meta, slots = B.pp_sweep_layout(parent, cells)
+    nspill, outs, ins = B.pp_sweep_spills(parent)
+    spill = {}                                   # spill index -> row values
     n = len(parent)
     kk = min(k, n)
     order = bf.canonical_preorder(parent)
@@ -44,6 +46,19 @@ def replay(parent, profit, k, cells):
     bits = np.zeros((nsteps, kk + 1), dtype=bool)
     group = []                                   # (row, value) of this group
     for s in range(nsteps):
+        if s % BATCH == 0 and nspill:
+            # at a batch boundary B: the copy-outs of batch B-2 at the latest
+            # (they precede the staging of batch B), the copy-ins of batch
+            # B+1 at the earliest (once batch B-1 is done)
+            b = s // BATCH
+            if b >= 2:
+                for ts, sx in outs[b - 2]:
+                    spill[int(sx)] = rows[int(ts)].copy()
+            for bb in ([0, 1] if b == 0 else [b + 1]):
+                if bb < len(ins):
+                    for rs, sx in ins[bb]:
+                        assert int(rs) != zero
+                        rows[int(rs)] = spill[int(sx)].copy()
         st, pf, m2, m3 = (int(v) for v in meta[s])
         assert m2 in (0, 0xFFFFFFFF) and m3 == 0
         leaf = m2 != 0
@@ -129,10 +144,56 @@ def test_replayed_schedule_deep_and_wide(oracle_mod):
             np.testing.assert_array_equal(sel, osel)
 
 
+caterpillar = W.caterpillar
+conversation_tree = W.regenerated_conversation
+
+
+@pytest.mark.parametrize("depth", [256, 300, 700])
+def test_replayed_schedule_with_spilled_rows(oracle_mod, depth):
+    """More pending skip rows than the LDS slots hold: long-lived rows are
+    spilled to device memory and restored; the replay, with every copy-out at
+    its latest and every copy-in at its earliest time, must still give the
+    oracle's optimum and set."""
+    parent = caterpillar(depth)
+    nspill, outs, ins = B.pp_sweep_spills(parent)
+    assert nspill > 0
+    meta, slots = B.pp_sweep_layout(parent, 1)
+    assert slots < 254
+    rng = np.random.default_rng(depth)
+    n = parent.shape[0]
+    for k in (1, 64, 300, n):
+        profit = rng.integers(0, 30, size=n)
+        for cells in (1, 2):
+            val, sel = replay(parent, profit, k, cells)
+            osel, oval = oracle_mod.rooted_dp(parent, profit, k)
+            assert val == oval
+            np.testing.assert_array_equal(sel, osel)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_replayed_schedule_branching_chains(oracle_mod, seed):
+    rng = np.random.default_rng(77 + seed)
+    parent = conversation_tree(int(rng.integers(1500, 4000)), rng)
+    assert B.pp_sweep_spills(parent)[0] > 0
+    perm = rng.permutation(parent.shape[0]) if seed % 2 else None
+    if perm is not None:  # relabel: the schedule follows the canonical preorder
+        inv = np.empty_like(perm)
+        inv[perm] = np.arange(perm.shape[0])
+        parent = np.array([-1 if parent[perm[v]] < 0 else inv[parent[perm[v]]]
+                           for v in range(parent.shape[0])], np.int32)
+    profit = rng.integers(0, 1000, size=parent.shape[0])
+    k = int(rng.choice([100, 1000]))
+    val, sel = replay(parent, profit, k, 1)
+    osel, oval = oracle_mod.rooted_dp(parent, profit, k)
+    assert val == oval
+    np.testing.assert_array_equal(sel, osel)
+
+
 def test_layout_of_benchmark_trees():
     """Stack depth of the benchmark trees stays small (LDS-resident)."""
     for name, limit in (("tree50k", 20), ("chat50k", 24), ("rag10k", 16)):
         inst = W.make_workload(name)
         meta, slots = B.pp_sweep_layout(inst.parent, 2)
         assert slots <= limit
+        assert B.pp_sweep_spills(inst.parent)[0] == 0  # nothing spilled
         assert meta.shape[0] == (inst.n + 31) // 32 * 32
