@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define PP_ABI_VERSION 10
+#define PP_ABI_VERSION 11
 
 enum {
     PP_OK = 0,
@@ -145,6 +145,14 @@ typedef struct {
                                   one 64-bit float instruction (every value
                                   below 2^62, or real-valued costs), 0 if
                                   with a compare and two selects */
+    int32_t dp_restarts;       /* out: times the plan was run again because a
+                                  DP sweep stage gave up a bounded wait for
+                                  its neighbour (the sweep's stages must be
+                                  resident at once; other work on the GPU
+                                  can crowd them out): each run uses fewer
+                                  stage blocks per launch and longer waits;
+                                  after 2 the call fails with PP_E_DEVICE.
+                                  Results are unaffected. */
 } pp_stats;
 
 /* Number of starts the options select (see pp_options.n_starts). */
@@ -212,6 +220,7 @@ typedef struct {
     int64_t dp_cells_executed;   /* as in pp_stats */
     int32_t dp_lane_cells;       /* as in pp_stats */
     int32_t dp_fmax;             /* as in pp_stats */
+    int32_t dp_restarts;         /* as in pp_stats */
 } pp_stats_f64;
 
 /* pp_plan on real-valued host arrays (layouts as pp_plan). */

@@ -40,7 +40,8 @@ class pp_stats(ctypes.Structure):
                 ("safeguard_objective", ctypes.c_int64 * 3),
                 ("dp_cells_executed", ctypes.c_int64),
                 ("dp_lane_cells", ctypes.c_int32),
-                ("dp_fmax", ctypes.c_int32)]
+                ("dp_fmax", ctypes.c_int32),
+                ("dp_restarts", ctypes.c_int32)]
 
 
 class pp_stats_f64(ctypes.Structure):
@@ -54,7 +55,8 @@ class pp_stats_f64(ctypes.Structure):
                 ("safeguard_objective", ctypes.c_double * 3),
                 ("dp_cells_executed", ctypes.c_int64),
                 ("dp_lane_cells", ctypes.c_int32),
-                ("dp_fmax", ctypes.c_int32)]
+                ("dp_fmax", ctypes.c_int32),
+                ("dp_restarts", ctypes.c_int32)]
 
 
 class pp_replan_info(ctypes.Structure):
@@ -181,6 +183,7 @@ class Plan:
     dp_cells_executed: int = 0
     dp_lane_cells: int = 0      # DP cells per lane of the sweep (1, 2, 4)
     dp_fmax: bool = False       # maximum by one 64-bit float instruction
+    dp_restarts: int = 0        # plan runs repeated after a stalled sweep
 
 
 def _options(m, n_starts, max_rounds, order_seed, orders, flags):
@@ -212,7 +215,8 @@ def _plan_from(st, arrs, target, objective):
                 safeguards_run=bool(st.safeguards_run),
                 safeguard_objective=tuple(int(x) for x in st.safeguard_objective),
                 dp_cells_executed=st.dp_cells_executed,
-                dp_lane_cells=st.dp_lane_cells, dp_fmax=bool(st.dp_fmax), **arrs)
+                dp_lane_cells=st.dp_lane_cells, dp_fmax=bool(st.dp_fmax),
+                dp_restarts=st.dp_restarts, **arrs)
 
 
 def pp_plan(parent, demand, recompute_cost, fetch_cost, cap, *, n_starts=8,
@@ -296,7 +300,8 @@ def _plan_f64_from(st, arrs, target, objective):
                 safeguards_run=bool(st.safeguards_run),
                 safeguard_objective=tuple(float(x) for x in st.safeguard_objective),
                 dp_cells_executed=st.dp_cells_executed,
-                dp_lane_cells=st.dp_lane_cells, dp_fmax=bool(st.dp_fmax), **arrs)
+                dp_lane_cells=st.dp_lane_cells, dp_fmax=bool(st.dp_fmax),
+                dp_restarts=st.dp_restarts, **arrs)
 
 
 def pp_plan_f64(parent, demand, recompute_cost, fetch_cost, cap, *, epsilon=0.0,

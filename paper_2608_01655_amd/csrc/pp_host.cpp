@@ -37,6 +37,18 @@ int fail_c(int code, const char* msg) {
 
 int fail(int code, const std::string& msg) { return fail_c(code, msg.c_str()); }
 
+// A DP sweep stage gave up a bounded wait (its stages were not all resident
+// at once, e.g. with other work on the GPU): the plan is run again with
+// fewer stages per launch and a longer wait, up to kStallRetries times.
+thread_local bool g_stall = false;
+constexpr int kStallRetries = 2;
+constexpr uint32_t kDefaultSpin = 1u << 22;
+
+int stall_fail() {
+  g_stall = true;
+  return fail_c(PP_E_DEVICE, "DP pipeline wait gave up (stages not co-resident)");
+}
+
 #define PP_HIP(expr)                                                      \
   do {                                                                    \
     hipError_t e_ = (expr);                                               \
@@ -762,6 +774,7 @@ struct PlanResult {
   int64_t updates = 0, cells = 0;
   double dp_ms = 0.0;
   int32_t dp_launches = 0;
+  int32_t restarts = 0;        // plan runs repeated after a DP sweep stalled
   int32_t lane_cells = 0;      // DP cells per lane of the sweep
   int32_t fmax = 0;            // maximum by one 64-bit float instruction
   // real-valued costs: exact objective values of the starts and of the
@@ -852,9 +865,9 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
                         hipMemcpyDeviceToHost, st));
   PP_HIP(hipStreamSynchronize(st));
   for (const ChainState& x : fin)
-    if (x.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+    if (x.status) return stall_fail();
   for (const ChainState& x : scr)
-    if (x.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+    if (x.status) return stall_fail();
   res.sg_run = true;
   std::vector<uint32_t> cgx;
   if (d.f64) PP_TRY(read_exact(d, cand_slot[0], 3, st, cgx));
@@ -918,7 +931,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
                           hipMemcpyDeviceToHost, e.st));
     PP_HIP(hipStreamSynchronize(e.st));
     for (int32_t q = 0; q < A; ++q) {
-      if (cs0[q].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+      if (cs0[q].status) return stall_fail();
       st[q].s = starts[q];
       st[q].pos = 0;
       st[q].improved = false;
@@ -1037,7 +1050,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
       for (; k < items.size() && items[k].q == q; ++k) {
         const Item& it = items[k];
         const ChainState& c = cs[k];
-        if (c.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+        if (c.status) return stall_fail();
         if (take) {  // computed against a placement that has changed
           if (!c.skip) res.spec_cells += (int64_t)d.n * kp[it.worker];
           continue;
@@ -1075,10 +1088,41 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
   }
 }
 
+int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
+                  const pp_options& o, bool fmax_ok, hipStream_t st, PlanResult& res,
+                  int32_t extra_slots, bool f64, double eps, int attempt);
+
+// Algorithm 1 on the context's inputs, run again (identical results: the
+// plan is deterministic) if a DP sweep stalled.
 int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
              const pp_options& o, bool fmax_ok, hipStream_t st,
              PlanResult& res, int32_t extra_slots = 0, bool f64 = false,
              double eps = 0.0) {
+  for (int attempt = 0;; ++attempt) {
+    g_stall = false;
+    res = PlanResult{};
+    const int rc = run_plan_once(c, t, m, cap, o, fmax_ok, st, res, extra_slots, f64, eps,
+                                 attempt);
+    res.restarts = attempt;
+    if (rc == PP_OK || !g_stall || attempt >= kStallRetries) return rc;
+    PP_HIP(hipStreamSynchronize(st));
+  }
+}
+
+// Spin limit of the DP sweep's bounded waits: PP_SPIN_LIMIT (a test hook)
+// on the first attempt, then at least the default, four times longer per
+// further attempt.
+uint32_t spin_limit_for(int attempt) {
+  const uint32_t base = (uint32_t)env_int("PP_SPIN_LIMIT", (int)kDefaultSpin);
+  if (attempt == 0) return base;
+  uint64_t v = std::max(base, kDefaultSpin);
+  for (int a = 1; a < attempt; ++a) v *= 4;
+  return (uint32_t)std::min<uint64_t>(v, 1u << 30);
+}
+
+int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
+                  const pp_options& o, bool fmax_ok, hipStream_t st, PlanResult& res,
+                  int32_t extra_slots, bool f64, double eps, int attempt) {
   const int32_t n = t.n;
   const int32_t S = num_starts(m, o.n_starts);
   res.S = S;
@@ -1117,7 +1161,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   e.c = c;
   e.st = st;
   e.slots_lds = t.slots;
-  e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 22);
+  e.spin_limit = spin_limit_for(attempt);
   e.timer.on = (o.flags & PP_F_TIME_KERNELS) != 0;
   DevState& d = e.d;
   d = DevState{};
@@ -1140,6 +1184,11 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   const int cells = choose_cells((int32_t)std::min<int64_t>(stage64, INT32_MAX),
                                  c->device, e.slots_lds);
   e.resident = dp_resident_blocks(cells, e.slots_lds, c->device);
+  if (attempt > 0 && e.resident > 0) {
+    // fewer stage blocks per launch, but every chain's stages in one
+    const int32_t chain = (kmax + 64 * cells - 1) / (64 * cells);
+    e.resident = std::max(chain, e.resident >> attempt);
+  }
   if (e.resident <= 0)
     return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident (LDS stack of " +
                                       std::to_string(e.slots_lds) + " rows)");
@@ -1183,7 +1232,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
                         hipMemcpyDeviceToHost, st));
   PP_HIP(hipStreamSynchronize(st));
   for (int32_t h = 0; h < m; ++h) {
-    if (hs[h].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+    if (hs[h].status) return stall_fail();
     res.standalone[h] = kp[h] > 0 ? hs[h].dpval : 0;
   }
 
@@ -1238,7 +1287,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
                           hipMemcpyDeviceToHost, st));
     PP_HIP(hipStreamSynchronize(st));
     for (int32_t s = lo; s < hi; ++s) {
-      if (fin[s - lo].status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+      if (fin[s - lo].status) return stall_fail();
       res.start_obj[s] = fin[s - lo].obj;
       res.accepts[s] = fin[s - lo].accepts;
       res.skipped_cells += fin[s - lo].skipped_cells;
@@ -1492,6 +1541,7 @@ void fill_stats(pp_stats* stats, const PlanResult& r, int32_t m) {
   stats->dp_cells_executed = r.cells - r.skipped_cells + r.spec_cells;
   stats->dp_lane_cells = r.lane_cells;
   stats->dp_fmax = r.fmax;
+  stats->dp_restarts = r.restarts;
   (void)m;
 }
 
@@ -1525,6 +1575,7 @@ void fill_stats_f64(pp_stats_f64* stats, const PlanResult& r) {
   stats->dp_cells_executed = r.cells - r.skipped_cells + r.spec_cells;
   stats->dp_lane_cells = r.lane_cells;
   stats->dp_fmax = r.fmax;
+  stats->dp_restarts = r.restarts;
 }
 
 // Host-array inputs (caller ids, 8-byte values) to the context's preorder
@@ -2054,19 +2105,22 @@ static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v
     e.st = st;
     e.slots_lds = slots_lds;
     e.resident = dp_resident_blocks(cells, slots_lds, c->device);
-    e.spin_limit = (uint32_t)env_int("PP_SPIN_LIMIT", 1 << 22);
     e.fmax = tot < kFmaxBound && env_int("PP_DP_NO_FMAX", 0) == 0;
     if (e.resident <= 0) return fail(PP_E_UNSUPPORTED, "DP sweep cannot be resident");
-    ChainState z{};
-    PP_HIP(hipMemcpyAsync(d.cs, &z, sizeof z, hipMemcpyHostToDevice, st));
-    PP_TRY(e.dp(set, 1));
-    PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
     std::vector<uint32_t> pre(d.npad / 32);
     ChainState out{};
-    PP_HIP(hipMemcpyAsync(pre.data(), d.sel, pre.size() * 4, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
-    if (out.status) return fail(PP_E_DEVICE, "DP pipeline wait gave up");
+    for (int attempt = 0;; ++attempt) {  // again, with a longer wait, if it stalled
+      e.spin_limit = spin_limit_for(attempt);
+      ChainState z{};
+      PP_HIP(hipMemcpyAsync(d.cs, &z, sizeof z, hipMemcpyHostToDevice, st));
+      PP_TRY(e.dp(set, 1));
+      PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
+      PP_HIP(hipMemcpyAsync(pre.data(), d.sel, pre.size() * 4, hipMemcpyDeviceToHost, st));
+      PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
+      PP_HIP(hipStreamSynchronize(st));
+      if (!out.status) break;
+      if (attempt >= kStallRetries) return stall_fail();
+    }
     for (int32_t q = 0; q < n; ++q) selected[t.order[q]] = (pre[q / 32] >> (q % 32)) & 1u;
     *value = out.dpval;
     return PP_OK;

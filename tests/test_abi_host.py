@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(L):
     assert len(names) >= 11
     for name in names:
         assert hasattr(L, name), name
-    assert B.pp_abi_version() == 10
+    assert B.pp_abi_version() == 11
 
 
 def _validate(inst, **kw):

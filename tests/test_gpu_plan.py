@@ -235,3 +235,27 @@ def test_speculative_sweeps(oracle_mod, monkeypatch, name, starts):
     assert g.updates == q.updates and g.dp_cells == q.dp_cells
     if starts <= 4 and name != "tiny":
         assert g.dp_launches < q.dp_launches
+
+
+def test_stalled_sweep_is_run_again(oracle_mod, monkeypatch):
+    """A DP sweep whose stage gives up its bounded wait for the neighbouring
+    stage (forced from the host with a one-poll spin limit, so every kernel
+    still exits normally) makes the library run the plan again with fewer
+    stage blocks per launch and the default wait: the same plan as the
+    oracle, with the restart reported."""
+    inst = W.make_workload("tree2k")
+    monkeypatch.setenv("PP_SPIN_LIMIT", "1")
+    p = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                  inst.cap, n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+                  order_seed=inst.order_seed)
+    assert p.dp_restarts >= 1
+    o = oracle_mod.plan_instance(inst)
+    assert p.objective == o.objective
+    np.testing.assert_array_equal(p.target, o.target)
+    rng = np.random.default_rng(5)
+    parent = W.random_forest(3000, rng)
+    profit = rng.integers(0, 1000, size=3000).astype(np.int64)
+    sel, val = B.pp_rooted_dp(parent, profit, 900)
+    osel, oval = oracle_mod.rooted_dp(parent, profit, 900)
+    assert val == oval
+    np.testing.assert_array_equal(sel, osel)
