@@ -585,12 +585,19 @@ __device__ __forceinline__ void unroll_steps(F&& f, std::integer_sequence<int, U
   (f(IC<U>{}), ...);
 }
 
+// Stage-ring values of a batch in the LDS output buffer: one per lane at
+// one cell per lane (lanes < kBatch carry a step's; every lane stores, see
+// k_dp), else one per step.
+template <int C>
+constexpr int dp_outv_stride() {
+  return C == 1 ? kWave : kBatch;
+}
+
 // LDS bytes of the sweep's control area: two record buffers, two output
-// buffers (stage-ring values, one per lane of which lanes < kBatch carry a
-// step's, and choice words of a batch) and a flag word.
+// buffers (stage-ring values and choice words of a batch) and a flag word.
 template <int C>
 constexpr size_t dp_ctl_bytes() {
-  return 2 * (kBatch + 1) * 2 * sizeof(StepView) + 2 * kWave * sizeof(int64_t) +
+  return 2 * (kBatch + 1) * 2 * sizeof(StepView) + 2 * dp_outv_stride<C>() * sizeof(int64_t) +
          2 * C * kWave * sizeof(uint32_t) + 16;
 }
 
@@ -605,8 +612,9 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // control area first (small immediate offsets), then the rows: the slots,
   // the zero row and the sink rows
   StepView* recs = (StepView*)lds;                             // [2][kBatch + 1][2]
-  int64_t* outv = (int64_t*)(recs + 2 * (kBatch + 1) * 2);     // [2][64]
-  uint32_t* outb = (uint32_t*)(outv + 2 * kWave);              // [2][C][64]
+  constexpr int kOutv = dp_outv_stride<C>();
+  int64_t* outv = (int64_t*)(recs + 2 * (kBatch + 1) * 2);     // [2][kOutv]
+  uint32_t* outb = (uint32_t*)(outv + 2 * kOutv);              // [2][C][64]
   // Hand-off between the waves through two LDS counters: sync[kStaged] =
   // batches whose records are staged (-1: the I/O wave gave up), sync[kDone]
   // = batches the compute wave has finished (their outputs are in LDS and
@@ -756,7 +764,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
           bits[c * cstride + wi] = outb[((b % 2) * C + c) * kWave + lane];
       }
       if (produce && lane < kBatch) {
-        const uint64_t bo = (uint64_t)outv[(b % 2) * kWave + lane];
+        const uint64_t bo = (uint64_t)outv[(b % 2) * kOutv + lane];
         const int idx = b * kBatch + lane;
         st_agent(ring_out + 2 * (int64_t)idx, tag | (bo & 0xFFFFFFFFull));
         st_agent(ring_out + 2 * (int64_t)idx + 1, tag | (bo >> 32));
@@ -888,24 +896,31 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   rec_load(0, 2);
 
   // gather: lane u < kBatch reads the last cell of the row step u of a
-  // batch was stored to, in groups of kProd steps; a batch's values are
-  // handed to the I/O wave a few steps into the next batch (or after the
-  // last one), when the last group's read has landed without a wait
-  int64_t gath[kBatch / kProd];
+  // batch was stored to, in groups of kProd steps.  At one cell per lane a
+  // batch's values are handed to the I/O wave a few steps into the next
+  // batch (or after the last one), when the last group's read has landed
+  // without a wait; wider rows (eight groups to select from) hand off at
+  // the end of the batch, which measures faster there.
+  constexpr bool kDefer = C == 1;
+  constexpr int kGroups = kBatch / kProd;
+  int64_t gath_kept[kDefer ? kGroups : 1];  // carried into the next batch
 #pragma unroll
-  for (int q = 0; q < kBatch / kProd; ++q) gath[q] = 0;
-  // the stage-ring values of the batch before (output buffer obuf) to LDS
+  for (int q = 0; q < (kDefer ? kGroups : 1); ++q) gath_kept[q] = 0;
+  // a batch's stage-ring values (lane u: step u's) to output buffer obuf
   // and the finished-batch count to `done`
-  auto hand_off = [&](int obuf, int done) {
-    int64_t v = gath[0];
-#pragma unroll
-    for (int q = 1; q < kBatch / kProd; ++q)
-      if (lane >= q * kProd) v = gath[q];
-    outv[obuf * kWave + lane] = v;
+  auto hand_off = [&](int64_t v, int obuf, int done) {
+    if (kDefer || lane < kBatch) outv[obuf * kOutv + lane] = v;
     sync_set(kDone, done);
   };
+  auto select_groups = [&](const int64_t (&g)[kDefer ? kGroups : 1]) {
+    int64_t v = g[0];
+#pragma unroll
+    for (int q = 1; q < (kDefer ? kGroups : 1); ++q)
+      if (lane >= q * kProd) v = g[q];
+    return v;
+  };
   constexpr int kHandOff = 2;  // step of the next batch that hands off
-  static_assert(kHandOff + 1 < kProd, "hand-off before the next gather");
+  static_assert(!kDefer || kHandOff + 1 < kProd, "hand-off before the next gather");
 
   // one batch; `buf` (b % 2, a compile-time constant) selects the record
   // and output buffers.  Returns false if the I/O wave gave up.
@@ -934,12 +949,21 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       }
     }
     const StepView* rec = recs + buf * (kBatch + 1) * 2;
-    // gather addresses: lane u < kBatch, step u's rows word (read by every
-    // lane: lanes >= kBatch read words inside the control area, and use 0)
-    const uint32_t gath_rw = rec[2 * lane].rows;
-    const uint32_t gath_w = lane < kBatch ? gath_rw : 0u;
+    // gather addresses: lane u < kBatch, step u's rows word (at one cell
+    // per lane read by every lane: lanes >= kBatch read words inside the
+    // control area, and use 0)
+    uint32_t gath_w = 0;
+    if constexpr (kDefer) {
+      const uint32_t gath_rw = rec[2 * lane].rows;
+      gath_w = lane < kBatch ? gath_rw : 0u;
+    } else {
+      gath_w = lane < kBatch ? rec[2 * lane].rows : 0u;
+    }
     const uint32_t gath_base = lane_base - lane * 8 + kLastCell;
     uint32_t gath_a = 0;
+    // wider rows: each group's values are folded into gath_v one group
+    // later (the read has landed by then), so no group array is kept
+    int64_t gath_v = 0, gath_p = 0;
     auto step = [&](auto uc) {
       constexpr int u = decltype(uc)::value;
       if constexpr (u + 3 < kBatch) {
@@ -997,10 +1021,17 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       }
       // the previous batch's ring values and count (batch 0: the count
       // stays 0 and buffer 1 gets values that batch 1 overwrites)
-      if constexpr (u == kHandOff) hand_off(1 - buf, b);
+      if constexpr (kDefer && u == kHandOff) hand_off(select_groups(gath_kept), 1 - buf, b);
       if constexpr (u % kProd == kProd - 1) {
+        constexpr int q = u / kProd;
         if constexpr (u == kProd - 1) gath_a = lds_row_lo(gath_w, gath_base);
-        gath[u / kProd] = *lds_at(gath_a);
+        if constexpr (kDefer) {
+          gath_kept[q] = *lds_at(gath_a);
+        } else {
+          if constexpr (q == 1) gath_v = gath_p;
+          if constexpr (q > 1) gath_v = lane >= (q - 1) * kProd ? gath_p : gath_v;
+          gath_p = *lds_at(gath_a);
+        }
       }
 #pragma unroll
       for (int c = 0; c < C; ++c) {
@@ -1013,9 +1044,11 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     // choice bits of the batch's last step
 #pragma unroll
     for (int c = 0; c < C; ++c) acc[c] = shift_in_gt<F64>(tp[c], skp[c], acc[c]);
-    // the batch's choice words; its ring values follow in the next batch
+    // the batch's choice words (and, unless deferred, its ring values)
 #pragma unroll
     for (int c = 0; c < C; ++c) outb[(buf * C + c) * kWave + lane] = acc[c];
+    if constexpr (!kDefer)
+      hand_off(lane >= (kGroups - 1) * kProd ? gath_p : gath_v, buf, b + 1);
     return true;
   };
   bool ok = true;
@@ -1027,7 +1060,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     sync_set(kDone, -1);
     return;
   }
-  hand_off((nb - 1) % 2, nb);
+  if constexpr (kDefer) hand_off(select_groups(gath_kept), (nb - 1) % 2, nb);
   // D[1][k'] sits in stage (k'-1)/(64C), lane ((k'-1) mod 64C)/C, cell c.
   const int jj = kp - 1;
   if (jj / (kWave * C) == g) {
