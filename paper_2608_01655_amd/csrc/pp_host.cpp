@@ -553,7 +553,12 @@ struct pp_ctx {
   uint32_t epoch = 0;
   std::vector<uint32_t> meta_host;  // source of the last metadata upload
   std::vector<hipEvent_t> events;
+  // pinned host copy of the chain states read back after each refinement
+  // launch (a direct device-to-host copy)
+  ChainState* cs_pin = nullptr;
+  size_t cs_pin_n = 0;
   ~pp_ctx() {
+    if (cs_pin) (void)hipHostFree(cs_pin);
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
                       &ring, &cs, &partial, &flag, &gx, &gxp, &sp_lists, &spill})
@@ -568,6 +573,28 @@ namespace {
 int select_device(pp_ctx* c) {
   PP_HIP(hipSetDevice(c->device));
   return PP_OK;
+}
+
+// At least `count` pinned chain states in c->cs_pin.
+int ensure_cs_pin(pp_ctx* c, size_t count) {
+  if (c->cs_pin_n >= count) return PP_OK;
+  if (c->cs_pin) PP_HIP(hipHostFree(c->cs_pin));
+  c->cs_pin = nullptr;
+  c->cs_pin_n = 0;
+  PP_HIP(hipHostMalloc((void**)&c->cs_pin, count * sizeof(ChainState), hipHostMallocDefault));
+  c->cs_pin_n = count;
+  return PP_OK;
+}
+
+// Waits for `st` by polling: after each refinement launch the host decides
+// the next launch from the chain states, so the wake-up delay of a
+// blocking wait would leave the device idle.
+int poll_stream(hipStream_t st) {
+  for (;;) {
+    const hipError_t q = hipStreamQuery(st);
+    if (q == hipSuccess) return PP_OK;
+    if (q != hipErrorNotReady) PP_HIP(q);
+  }
 }
 
 int npad_of(int32_t n) { return (n + 63) / 64 * 64; }
@@ -1027,14 +1054,16 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
     PP_HIP(launch_backtrack(set, d, kModeRefine, e.st));
     if (d.f64) PP_HIP(launch_gexact(set, d, kModeRefine, e.st));
     // the launch's results: the starts' slots (consecutive) and the spare
-    // slots, in two copies
-    std::vector<ChainState> own(A), spare(spares > 0 ? spares : 1);
-    PP_HIP(hipMemcpyAsync(own.data(), d.cs + starts[0], sizeof(ChainState) * A,
+    // slots, in two copies (to pinned memory: starts, then spares)
+    PP_TRY(ensure_cs_pin(e.c, (size_t)A + (size_t)spares));
+    ChainState* own = e.c->cs_pin;
+    ChainState* spare = e.c->cs_pin + A;
+    PP_HIP(hipMemcpyAsync(own, d.cs + starts[0], sizeof(ChainState) * A,
                           hipMemcpyDeviceToHost, e.st));
     if (spares > 0)
-      PP_HIP(hipMemcpyAsync(spare.data(), d.cs + spare_base, sizeof(ChainState) * spares,
+      PP_HIP(hipMemcpyAsync(spare, d.cs + spare_base, sizeof(ChainState) * spares,
                             hipMemcpyDeviceToHost, e.st));
-    PP_HIP(hipStreamSynchronize(e.st));
+    PP_TRY(poll_stream(e.st));
     std::vector<ChainState> cs(items.size());
     for (size_t k = 0; k < items.size(); ++k)
       cs[k] = items[k].slot >= spare_base ? spare[items[k].slot - spare_base]
