@@ -864,6 +864,9 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // row step u was stored to
   constexpr int kLastCell = (C - 1) * kWave * 8 + (kWave - 1) * 8;
   barrier();
+  // The compute wave issues ahead of other waves on its SIMD (another
+  // block's I/O wave shares it at two blocks per compute unit).
+  __builtin_amdgcn_s_setprio(2);
 
   // LDS address of this lane's cell 0 in row offset 0 (rows are addressed
   // as this plus a row's byte offset)
