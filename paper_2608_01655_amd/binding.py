@@ -87,7 +87,7 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(
                 f"{LIB_PATH} is missing: build it with "
-                "`python -c 'import __graft_entry__ as g; g.build()'`")
+                "`python -m paper_2608_01655_amd.build`")
         # PyTorch-ROCm ships its own HIP runtime (same SONAME as the system
         # one, but its libraries ask for it under another file name).  Load
         # torch first so this library binds to that same runtime instead of
