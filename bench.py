@@ -74,24 +74,24 @@ KERNEL_SOURCES = ("paper_2608_01655_amd/csrc/pp_kernels.hip",
 def dp_valu_per_step(cells, fmax, f64):
     """Vector instructions the DP sweep's compute wave issues per row step
     (64 * cells cells): two row addresses; cell 0's take operand (a DPP
-    64-bit add, or for doubles two DPP moves and an add); the other cells'
-    take operands (a 64-bit add, or one add of doubles); per cell the choice
-    bit (compare, add with carry), the skip operand (two bit selects) and the
-    maximum (one v_max_f64, or a compare and two selects).  The SQ counters
-    of one cell per lane agree (profiles/)."""
-    return (2 + (3 if f64 else 2) + (cells - 1) * (1 if f64 else 2)
+    64-bit add, or for doubles two DPP moves and an add); with several
+    cells per lane the profit moved into lane 0 (two DPP moves) and the
+    other cells' take operands (one 64-bit add each); per cell the choice
+    bit (compare, add with carry), the skip operand (two bit selects) and
+    the maximum (one v_max_f64, or a compare and two selects).  The SQ
+    counters of one cell per lane and the compiled code of every width
+    agree (profiles/)."""
+    return (2 + (3 if f64 else 2) + (2 + (cells - 1) if cells > 1 else 0)
             + cells * (4 + (1 if fmax else 3)))
 
 
 def dp_lds_bytes_per_cell(cells):
-    """LDS bytes per DP cell: the compute wave's step record (16 B per lane;
-    with several cells per lane also the 8-byte profit), row store and skip
-    row read (8 B per cell each), one gathered column per group of sink
-    rows; the I/O wave's staging (two 16-byte views for 33 lanes per
-    32-step batch)."""
+    """LDS bytes per DP cell: the compute wave's step record (16 B per
+    lane), row store and skip row read (8 B per cell each), one gathered
+    column per group of sink rows; the I/O wave's staging (two 16-byte views
+    for 33 lanes per 32-step batch)."""
     sink = 16 if cells == 1 else 4
-    per_step = 64 * 16 + (64 * 8 if cells > 1 else 0) + 2 * 64 * cells * 8 \
-        + 64 * 8 / sink + 2 * 16 * 33 / 32
+    per_step = 64 * 16 + 2 * 64 * cells * 8 + 64 * 8 / sink + 2 * 16 * 33 / 32
     return per_step / (64 * cells)
 
 

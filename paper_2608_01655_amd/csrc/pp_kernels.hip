@@ -558,12 +558,11 @@ __device__ __forceinline__ int64_t max_nonneg_f64(int64_t a, int64_t b) {
 // leaf, rows stay all-zero).  Per batch the I/O wave stages each step's
 // record -- profit (plus the boundary value for lane 0), the packed row
 // offsets and the leaf mask -- in LDS, read back by the compute wave with
-// one load per step (and, for C > 1, a broadcast load of p).  The two
-// waves meet at one barrier per batch.  Each lane shifts its cells'
-// choice bits into one 32-bit word per cell per batch (bit 31-u = step u),
-// stored with one coalesced store per cell; the stage ring output also
-// leaves with one store per batch.  No per-row launch, barrier or HBM row
-// traffic.
+// one load per step.  The waves hand batches over through two LDS counters
+// (no barrier in the batch loop).  Each lane shifts its cells' choice bits
+// into one 32-bit word per cell per batch (bit 31-u = step u), stored with
+// one coalesced store per cell; the stage ring output also leaves with one
+// store per batch.  No per-row launch, barrier or HBM row traffic.
 constexpr int kBatch = kDpBatch;
 
 // A step's record in two 16-byte views: lanes 1..63 read view 0, lane 0
@@ -878,20 +877,16 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // Records of steps u..u+3 in flight, in a ring of kRq register sets that
   // runs across batches (kRq divides kBatch): a batch's record kBatch is
   // the next batch's record 0, and records 1 and 2 of the next batch are
-  // read from its buffer after the staged count, a few steps ahead.  Wider
-  // rows also read p for cells 1..C-1 (lane 0's view holds p plus the
-  // boundary value).
+  // read from its buffer after the staged count, a few steps ahead.
   constexpr int kRq = 4;
   static_assert(kBatch % kRq == 0, "record ring");
   pp_u32x4 rv[kRq];
-  int64_t pv[kRq];
   int staged_v;  // the staged count as loaded (made uniform where checked)
   auto view_of = [&](int buf) {
     return (const char*)(recs + buf * (kBatch + 1) * 2) + (lane == 0 ? sizeof(StepView) : 0);
   };
   auto rec_load = [&](int buf, int t) {
     rv[t % kRq] = *(const pp_u32x4*)(view_of(buf) + 2 * sizeof(StepView) * t);
-    if constexpr (C > 1) pv[t % kRq] = recs[(buf * (kBatch + 1) + t) * 2].r;
   };
   staged_v = sync_load(kStaged);  // 1, or -1 if staging batch 0 failed
   rec_load(0, 0);
@@ -995,10 +990,19 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       } else {
         t[0] = take_after_bit_i64(r0, x[C - 1], tp[0], skp[0], acc[0]);
       }
+      // cells 1..C-1 add p itself, which lanes 1..63 hold; lane 0 (whose
+      // view adds the boundary value) takes lane 1's by DPP wave_shl:1,
+      // and lane 63, which has no right neighbour, keeps its own
+      if constexpr (C > 1) {
+        pp_int2 pq;
+        pq.x = __builtin_amdgcn_update_dpp((int)r.x, (int)r.x, 0x130, 0xf, 0xf, false);
+        pq.y = __builtin_amdgcn_update_dpp((int)r.y, (int)r.y, 0x130, 0xf, 0xf, false);
+        const int64_t pl = join64(pq);
 #pragma unroll
-      for (int c = 1; c < C; ++c) {
-        if constexpr (u > 0) acc[c] = shift_in_gt<F64>(tp[c], skp[c], acc[c]);
-        t[c] = vadd<F64>(pv[u % kRq], x[c - 1]);
+        for (int c = 1; c < C; ++c) {
+          if constexpr (u > 0) acc[c] = shift_in_gt<F64>(tp[c], skp[c], acc[c]);
+          t[c] = vadd<F64>(pl, x[c - 1]);
+        }
       }
 #pragma unroll
       for (int c = 0; c < C; ++c) {
