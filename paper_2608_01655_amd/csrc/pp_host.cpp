@@ -548,6 +548,7 @@ struct pp_ctx {
   DevBuf up_lam, up_w, up_f, up_u8;
   // per-slot state
   DevBuf tgt, v1, v2, h1, profit, sel, bits, ring, cs;
+  DevBuf sel0;  // standalone selections, [m][npad/32] (greedy position 0)
   DevBuf partial, flag, gx, gxp;
   DevBuf sp_lists, spill;  // spilled skip rows of deep trees
   uint32_t epoch = 0;
@@ -560,7 +561,7 @@ struct pp_ctx {
   ~pp_ctx() {
     if (cs_pin) (void)hipHostFree(cs_pin);
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
-                      &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &bits,
+                      &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &sel0, &bits,
                       &ring, &cs, &partial, &flag, &gx, &gxp, &sp_lists, &spill})
       b->release();
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
@@ -733,6 +734,16 @@ struct Engine {
                        st));
       PP_TRY(timer_mark(c, timer, false, st));
     }
+    return PP_OK;
+  }
+
+  // Greedy position 0 of every chain of `set`: the standalone solve of its
+  // worker (its selection saved in sel0), adopted and committed.
+  int take_standalone(const ChainSet& set, const uint32_t* sel0) {
+    if (set.count == 0) return PP_OK;
+    PP_HIP(launch_take_standalone(set, d, sel0, st));
+    if (d.f64) PP_HIP(launch_gexact(set, d, kModeGreedy, st));  // exact G, marks
+    PP_HIP(launch_commit(set, d, kModeGreedy, st));
     return PP_OK;
   }
 
@@ -1255,8 +1266,19 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
         wk2.push_back(wk[q]);
         kk2.push_back(kk[q]);
       }
-    if (!sl2.empty()) PP_TRY(e.dp(chain_set(sl2, wk2, kk2, 0, sl2.size()), 0));
+    if (!sl2.empty()) {
+      // the choice bits and the walk too: every start's first greedy update
+      // is the standalone solve of its first worker
+      const ChainSet s2 = chain_set(sl2, wk2, kk2, 0, sl2.size());
+      PP_TRY(e.dp(s2, 1));
+      PP_HIP(launch_backtrack(s2, d, kModeGreedy, st));
+    }
   }
+  // the standalone selections (slots 0..m-1) outlive the starts' use of
+  // those slots
+  const size_t sel_bytes = (size_t)m * (d.npad / 32) * sizeof(uint32_t);
+  PP_TRY(c->sel0.ensure(sel_bytes));
+  PP_HIP(hipMemcpyAsync(c->sel0.p, d.sel, sel_bytes, hipMemcpyDeviceToDevice, st));
   PP_HIP(hipMemcpyAsync(hs.data(), d.cs, sizeof(ChainState) * m,
                         hipMemcpyDeviceToHost, st));
   PP_HIP(hipStreamSynchronize(st));
@@ -1298,7 +1320,12 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
       }
       return chain_set(sl, wk, kk, 0, sl.size());
     };
-    for (int32_t a = 0; a < m; ++a)
+    {
+      const ChainSet first = position_set(active, 0);
+      PP_TRY(e.take_standalone(first, c->sel0.as<uint32_t>()));
+      for (int32_t q = 0; q < first.count; ++q) res.skipped_cells += (int64_t)n * first.kprime[q];
+    }
+    for (int32_t a = 1; a < m; ++a)
       PP_TRY(e.update(position_set(active, a), kModeGreedy));
     if (!(o.flags & PP_F_NO_REFINE))
       PP_TRY(refine_starts(e, active, spare_base, spec_chains, spec_blocks, m, kp,

@@ -307,6 +307,10 @@ hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
 // whose sweep ran against the unchanged placement).
 hipError_t launch_adopt(const DevState& d, int32_t s, int32_t from, int32_t worker,
                         const uint32_t (&ran)[8], hipStream_t st);
+// Greedy position 0: each chain adopts the standalone selection of its
+// worker (row `worker` of sel0, [m][npad/32]) as its walk would have.
+hipError_t launch_take_standalone(const ChainSet& set, const DevState& d,
+                                 const uint32_t* sel0, hipStream_t st);
 hipError_t launch_commit(const ChainSet& set, const DevState& d, int mode,
                          hipStream_t st);
 hipError_t launch_reset_round(const ChainSet& set, const DevState& d,

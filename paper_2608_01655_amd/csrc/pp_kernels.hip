@@ -1779,6 +1779,36 @@ __global__ void __launch_bounds__(256) k_adopt(DevState d, int32_t s, int32_t fr
   }
 }
 
+// The first greedy update of a start (position 0, every worker's set
+// empty) is the standalone solve of its worker (same profits, same DP), so
+// it adopts that solve's selection, saved in `sel0` (row h: worker h),
+// instead of sweeping again; the marks are those the walk would set (the
+// real-valued decision and its marks follow in k_gexact_final).
+__global__ void __launch_bounds__(256) k_take_standalone(ChainSet set, DevState d,
+                                                         const uint32_t* __restrict__ sel0) {
+  const int ci = blockIdx.x;
+  const int64_t s = set.slot[ci];
+  const int h = set.worker[ci];
+  const int nwords = d.npad / 32;
+  const uint32_t* src = sel0 + (int64_t)h * nwords;
+  uint32_t* dst = d.sel + s * nwords;
+  for (int q = threadIdx.x; q < nwords; q += blockDim.x) dst[q] = src[q];
+  if (threadIdx.x == 0) {
+    ChainState* st = d.cs + s;
+    st->dirty[h >> 5] &= ~(1u << (h & 31));
+    st->inc = 0;
+    if (d.f64) {
+      st->accept = 0;
+      st->wsum = 0;
+      st->rejected = 0;
+    } else {
+      st->accept = 1;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
+    }
+  }
+}
+
 // Row h of slot `dst`'s placement := the backtracked selection of chain
 // (slot, h), for every chain of the set (the per-worker comparator
 // candidates are solved in scratch slots and assembled here).
@@ -2216,6 +2246,13 @@ hipError_t launch_adopt(const DevState& d, int32_t s, int32_t from, int32_t work
   Bits8 b;
   for (int q = 0; q < 8; ++q) b.w[q] = ran[q];
   hipLaunchKernelGGL(k_adopt, dim3(1), dim3(256), 0, st, d, s, from, worker, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_take_standalone(const ChainSet& set, const DevState& d,
+                                 const uint32_t* sel0, hipStream_t st) {
+  if (set.count == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_take_standalone, dim3(set.count), dim3(256), 0, st, set, d, sel0);
   return hipGetLastError();
 }
 
