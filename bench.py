@@ -448,21 +448,16 @@ def f64_leg(B, W, inst, ctx, steps, warmup):
     return out
 
 
-def paper_config_leg(B, W, ctx, steps, with_oracle):
-    """The configuration of the paper's own timing (n = 50,000, M = 16,
-    k = 128 per worker): the tree50k tree and demand with every capacity
-    set to 128, in requests per epoch and milliseconds as doubles, 8
-    starts, refinement to convergence, through the real-valued device entry
-    point.  The paper reports 12.29 s per plan on one EPYC 9V74 for its own
-    inputs of this size; the CPU oracle (one thread, the full DP table) is
-    timed on the same inputs as a second point of reference."""
-    import dataclasses
-
+def _runtime_point(B, W, ctx, inst, steps, with_oracle):
+    """One of the paper's solver-runtime configurations: the instance in
+    requests per epoch and milliseconds as doubles (epsilon = 1e-9 of the
+    sum of demand x recompute cost), planned through the real-valued device
+    entry point with the instance's start set and refinement to
+    convergence; with `with_oracle`, the CPU oracle (one thread, the full DP
+    table) on the same inputs."""
     import numpy as np
     import torch
 
-    inst = W.make_workload("tree50k")
-    inst = dataclasses.replace(inst, cap=np.full(inst.m, 128, np.int32))
     lam, w, f = W.real_valued(inst, 1)
     eps = 1e-9 * float(np.sum(lam * w))
     dev = torch.device("cuda:0")
@@ -479,12 +474,8 @@ def paper_config_leg(B, W, ctx, steps, with_oracle):
         p = ctx.pp_plan_f64_device(inst.parent, tl, tw, tf, inst.cap, tgt, **kw)
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / steps
-    out = {"workload": "tree50k tree and demand, k = 128 for all 16 workers, "
-                       "real-valued (requests, ms)",
-           "ms_per_plan": dt * 1e3, "updates_per_plan": p.updates,
-           "sweeps_per_start": p.start_sweeps.tolist(), "objective": p.objective,
-           "paper_s_per_plan": 12.29, "paper_hardware": "one EPYC 9V74",
-           "ratio_paper_time_to_this": 12.29 / dt}
+    out = {"ms_per_plan": dt * 1e3, "starts": int(p.n_starts), "updates_per_plan": p.updates,
+           "sweeps_per_start": p.start_sweeps.tolist(), "objective": p.objective}
     if with_oracle:
         import oracle
 
@@ -495,6 +486,38 @@ def paper_config_leg(B, W, ctx, steps, with_oracle):
         out["same_as_oracle"] = (
             bool(np.array_equal(o.target, tgt.cpu().numpy()))
             and o.objective == p.objective)
+    return out, dt
+
+
+def paper_config_leg(B, W, ctx, steps, with_oracle):
+    """The configurations of the paper's own solver timing (k = 128 per
+    worker): n = 50,000 with M = 16 -- the tree50k tree and demand with every
+    capacity set to 128, 8 starts -- and n = 10,000 with M = 4, 8 and 16 --
+    the RAG-shaped tree and demand of rag10k split over M workers, the
+    paper's default start set (every order for M = 4) -- all real-valued,
+    refinement to convergence.  The paper reports 12.29 s and 0.41, 1.12,
+    2.35 s per plan on one EPYC 9V74 for its own inputs of these sizes
+    (context: other inputs and hardware); the CPU oracle (one thread) is
+    timed on the same inputs as a second point of reference."""
+    import dataclasses
+
+    import numpy as np
+
+    inst = W.make_workload("tree50k")
+    inst = dataclasses.replace(inst, cap=np.full(inst.m, 128, np.int32))
+    pt, dt = _runtime_point(B, W, ctx, inst, steps, with_oracle)
+    out = {"workload": "tree50k tree and demand, k = 128 for all 16 workers, "
+                       "real-valued (requests, ms)",
+           **pt, "paper_s_per_plan": 12.29, "paper_hardware": "one EPYC 9V74",
+           "ratio_paper_time_to_this": 12.29 / dt}
+    points = []
+    for m, paper_s in ((4, 0.41), (8, 1.12), (16, 2.35)):
+        pt, dt = _runtime_point(B, W, ctx, W.runtime_instance(m), max(steps, 3), with_oracle)
+        points.append({"n": 10_000, "workers": m, "k": 128, **pt, "paper_s_per_plan": paper_s,
+                       "ratio_paper_time_to_this": paper_s / dt})
+    out["n10k_points"] = points
+    out["n10k_workload"] = ("rag10k tree and demand split over M workers, k = 128, "
+                            "the paper's default start set, real-valued (requests, ms)")
     return out
 
 

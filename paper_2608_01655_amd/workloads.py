@@ -417,6 +417,27 @@ def make_workload(name: str) -> Instance:
                     depth=depth)
 
 
+def runtime_instance(m: int, seed: int = 11) -> Instance:
+    """The shape of the paper's solver-runtime measurements at n = 10,000
+    (Sec. V, solver runtime: k = 128 per worker, M = 4, 8 or 16): the
+    RAG-shaped tree and demand of `rag10k` (40 templates, Zipf 0.9 over the
+    leaves, 10^7 requests) split over m workers with the cyclic hardware
+    factors and source-dependent fetch costs over U[1.5, 25] Gb/s; the
+    paper's default start set (`n_starts = 0`: every order for m <= 5, else
+    8 starts) and refinement to convergence.  The same tree for every m."""
+    rng = np.random.default_rng(seed)
+    parent, _ = _relabel_preorder(rag_tree(10_000, 40, rng))
+    n = parent.shape[0]
+    depth = _depths(parent)
+    rng_m = np.random.default_rng(seed * 100 + m)
+    demand = zipf_leaf_demand(parent, m, 0.9, 10 ** 7, rng_m)
+    w = depth_linear_recompute(depth, H10_CYCLE[np.arange(m) % 3])
+    f = pairwise_fetch(m, n, 1.5, 25.0, rng_m)
+    return Instance(name=f"runtime10k_m{m}", parent=parent, demand=demand, recompute_cost=w,
+                    fetch_cost=f, cap=np.full(m, 128, dtype=np.int32), n_starts=0,
+                    max_rounds=0, order_seed=seed, depth=depth)
+
+
 # --------------------------------------------------------------------------
 # Small random instances for property and parity tests
 # --------------------------------------------------------------------------

@@ -78,3 +78,20 @@ def test_routing_shift_and_popularity_perturbation():
             assert np.all(pert[:, p] >= pert[:, v])
     zero = W.perturb_popularity(inst.parent, lam, 0.0, rng)
     np.testing.assert_array_equal(zero, lam)
+
+
+def test_runtime_instances_share_the_tree():
+    """The n = 10,000, k = 128 runtime configurations: one RAG-shaped tree
+    for M = 4, 8 and 16, demand aggregated along prefix paths with the same
+    total, the paper's default start set."""
+    insts = [W.runtime_instance(m) for m in (4, 8, 16)]
+    for inst, m in zip(insts, (4, 8, 16)):
+        assert inst.n == 10_000 and inst.m == m
+        np.testing.assert_array_equal(inst.parent, insts[0].parent)
+        assert inst.cap.tolist() == [128] * m and inst.n_starts == 0
+        assert int(inst.demand[:, 0].sum()) == 10 ** 7
+        assert inst.fetch_cost.shape == (m, m, inst.n)
+        for v in range(1, inst.n):
+            p = inst.parent[v]
+            if p >= 0:
+                assert np.all(inst.demand[:, p] >= inst.demand[:, v])
