@@ -296,3 +296,21 @@ def test_safeguards_f64_winning_candidates(oracle_mod):
         if found == 6:
             break
     assert found > 0
+
+
+@pytest.mark.parametrize("m", [4, 8])
+def test_paper_runtime_configuration_matches_oracle(oracle_mod, m):
+    """The paper's solver-runtime configuration at n = 10,000 (k = 128, the
+    paper's default start set: all 24 orders at M = 4, 8 starts at M = 8;
+    the bench checks M = 16 the same way),
+    real-valued, refinement to convergence: the plan the bench times is the
+    oracle's, bit for bit."""
+    inst = W.runtime_instance(m)
+    lam, w, f = W.real_valued(inst, 1)
+    eps = 1e-9 * float(np.sum(lam * w))
+    kw = dict(epsilon=eps, n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+              order_seed=inst.order_seed)
+    g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+    _same_real(g, o)
+    assert g.n_starts == (24 if m == 4 else 8)
