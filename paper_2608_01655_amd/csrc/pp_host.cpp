@@ -1179,12 +1179,6 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   // and LocalDedup candidates, and slots 0..m-1 serve as scratch chains
   const bool sg_asked = (o.flags & PP_F_SAFEGUARDS) != 0;
   const int32_t slot_b = std::max(m, S);
-  // speculative refinement (few active starts): up to kSpecChains updates
-  // of one start per launch, all but the first in spare slots at the end
-  const int32_t spec_chains =  // updates per refinement launch
-      env_int("PP_NO_SPEC", 0) ? 1
-                               : std::max(1, std::min(kMaxChains, env_int("PP_SPEC_CHAINS",
-                                                                          kSpecChains)));
   // stage blocks a speculative launch may fill: two per compute unit
   int32_t spec_blocks = 512;
   {
@@ -1194,6 +1188,19 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
       spec_blocks = 2 * cus;
     spec_blocks = env_int("PP_SPEC_BLOCKS", spec_blocks);
   }
+  // speculative refinement: up to kSpecChains updates per launch (each
+  // start's next one and later positions of the same sweep, all but the
+  // first of a start in spare slots at the end); twice as many where that
+  // many chains of the widest capacity (stages at one cell per lane) fit
+  // the launch's stage blocks -- small capacities, whose launches take the
+  // same time with more chains
+  const int32_t wide_stages = std::max(1, (kmax + 63) / 64);
+  const int32_t spec_default =
+      2 * kSpecChains * wide_stages <= spec_blocks ? 2 * kSpecChains : kSpecChains;
+  const int32_t spec_chains =  // updates per refinement launch
+      env_int("PP_NO_SPEC", 0) ? 1
+                               : std::max(1, std::min(kMaxChains, env_int("PP_SPEC_CHAINS",
+                                                                          spec_default)));
   const int32_t spare_base = slot_b + (sg_asked ? 4 : 0) + extra_slots;
   const int32_t slots = spare_base + (spec_chains > 1 ? spec_chains - 1 : 0);
   res.extra_slot = extra_slots > 0 ? slot_b + (sg_asked ? 4 : 0) : -1;
