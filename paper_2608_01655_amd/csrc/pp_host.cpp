@@ -989,6 +989,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
   };
   struct Item {
     int32_t q, slot, worker, pos;
+    bool next;  // a position of the start's next sweep
   };
   for (;;) {
     // each start's next update that needs a sweep; sweep ends
@@ -1015,11 +1016,17 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
       }
     }
     std::vector<Item> items;
-    std::vector<int32_t> scan(A, m);
+    std::vector<int32_t> scan(A, m), wscan(A, 0);
+    // A start whose sweep has accepted a replacement sweeps again unless the
+    // cap stops it, so once every later position of this sweep is in the
+    // launch or resolved without a sweep, positions of the next sweep can be
+    // speculated too (valid if everything before them is rejected).
+    std::vector<char> can_wrap(A, 0);
     for (int32_t q = 0; q < A; ++q)
       if (!st[q].done) {
-        items.push_back({q, st[q].s, worker_at(st[q], st[q].pos), st[q].pos});
+        items.push_back({q, st[q].s, worker_at(st[q], st[q].pos), st[q].pos, false});
         scan[q] = st[q].pos + 1;
+        can_wrap[q] = st[q].improved && (max_rounds == 0 || res.sweeps[st[q].s] + 1 < max_rounds);
       }
     if (items.empty()) return PP_OK;
     // speculative updates: at most `budget` updates in all (one spare slot
@@ -1031,6 +1038,14 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
     for (const Item& it : items) blocks += blocks_of(it.worker);
     int32_t spares = 0;
     auto room = [&]() { return (int32_t)items.size() < budget && spares < budget - 1; };
+    // a position b < pos of the next sweep needs a sweep there (if nothing
+    // is adopted before it) iff its worker is stale now: the workers of
+    // positions >= pos run in this launch or are unchanged since their last
+    // sweep
+    auto next_needs_sweep = [&](const St& x, int32_t b) {
+      const int32_t h = worker_at(x, b);
+      return kp[h] > 0 && x.is_dirty(h);
+    };
     for (bool grew = true; grew && room();) {
       grew = false;
       for (int32_t q = 0; q < A && room(); ++q) {
@@ -1039,14 +1054,28 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
         while (a < m && resolved_free(st[q], a)) ++a;
         if (a < m && blocks + blocks_of(worker_at(st[q], a)) > block_budget) {
           scan[q] = m;  // this start's next update does not fit any more
+          can_wrap[q] = 0;
           continue;
         }
         if (a < m) {
           blocks += blocks_of(worker_at(st[q], a));
-          items.push_back({q, spare_base + spares++, worker_at(st[q], a), a});
+          items.push_back({q, spare_base + spares++, worker_at(st[q], a), a, false});
+          scan[q] = a + 1;
           grew = true;
+          continue;
         }
-        scan[q] = a < m ? a + 1 : m;
+        scan[q] = m;
+        if (!can_wrap[q]) continue;
+        int32_t b = wscan[q];
+        while (b < st[q].pos && !next_needs_sweep(st[q], b)) ++b;
+        if (b >= st[q].pos || blocks + blocks_of(worker_at(st[q], b)) > block_budget) {
+          can_wrap[q] = 0;
+          continue;
+        }
+        blocks += blocks_of(worker_at(st[q], b));
+        items.push_back({q, spare_base + spares++, worker_at(st[q], b), b, true});
+        wscan[q] = b + 1;
+        grew = true;
       }
     }
     std::stable_sort(items.begin(), items.end(),
@@ -1087,6 +1116,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
       uint32_t ran[8] = {0, 0, 0, 0, 0, 0, 0, 0};
       const Item* take = nullptr;
       int32_t last = x.pos - 1;  // last position resolved in this launch
+      bool in_next = false;
       for (; k < items.size() && items[k].q == q; ++k) {
         const Item& it = items[k];
         const ChainState& c = cs[k];
@@ -1094,6 +1124,17 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
         if (take) {  // computed against a placement that has changed
           if (!c.skip) res.spec_cells += (int64_t)d.n * kp[it.worker];
           continue;
+        }
+        if (it.next && !in_next) {
+          // every position left in this sweep was rejected: the sweep ends
+          // (it accepted earlier, so the next one follows)
+          for (int32_t a = last + 1; a < m; ++a) res.skipped_cells += free_cells(x, a);
+          res.sweeps[x.s] += 1;
+          x.improved = false;
+          const std::vector<int32_t> one = {x.s}, z = {0};
+          PP_HIP(launch_reset_round(chain_set(one, z, z, 0, 1), d, e.st));
+          last = -1;
+          in_next = true;
         }
         // positions passed over on the way are resolved as rejected
         for (int32_t a = last + 1; a < it.pos; ++a) res.skipped_cells += free_cells(x, a);

@@ -314,3 +314,18 @@ def test_paper_runtime_configuration_matches_oracle(oracle_mod, m):
     o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
     _same_real(g, o)
     assert g.n_starts == (24 if m == 4 else 8)
+
+
+@pytest.mark.parametrize("chains,rounds", [(3, 2), (5, 0)])
+def test_f64_speculation_into_the_next_sweep(oracle_mod, monkeypatch, chains, rounds):
+    """Real-valued refinement with a few updates per launch, so that
+    speculation reaches into starts' next sweeps at several points, with
+    and without a sweep cap: the oracle's plan, bit for bit."""
+    inst = W.runtime_instance(4)
+    lam, w, f = W.real_valued(inst, 2)
+    eps = 1e-9 * float(np.sum(lam * w))
+    kw = dict(epsilon=eps, n_starts=6, max_rounds=rounds, order_seed=inst.order_seed)
+    monkeypatch.setenv("PP_SPEC_CHAINS", str(chains))
+    g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
+    _same_real(g, o)

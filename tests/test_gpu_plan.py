@@ -242,6 +242,24 @@ def test_speculative_sweeps(oracle_mod, monkeypatch, name, starts):
         assert g.dp_launches < q.dp_launches
 
 
+@pytest.mark.parametrize("chains,rounds", [(2, 0), (3, 2), (6, 3), (6, 0), (64, 2), (64, 0)])
+def test_speculation_into_the_next_sweep(oracle_mod, monkeypatch, chains, rounds):
+    """A start whose sweep has accepted an update and whose remaining
+    positions all fit the launch speculates positions of its next sweep
+    (those whose workers are stale) unless the sweep cap ends it there:
+    with a few or many updates per launch and with and without a cap, the
+    plan and its statistics are the oracle's."""
+    inst = W.make_workload("tree2k")
+    args = dict(n_starts=2, max_rounds=rounds, order_seed=inst.order_seed)
+    monkeypatch.setenv("PP_SPEC_CHAINS", str(chains))
+    g = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                  inst.cap, **args)
+    o = oracle_mod.plan_instance(inst, threads=8, **args)
+    _same(g, o)
+    if rounds == 0:
+        assert max(g.start_sweeps) >= 2
+
+
 def test_stalled_sweep_is_run_again(oracle_mod, monkeypatch):
     """A DP sweep whose stage gives up its bounded wait for the neighbouring
     stage (forced from the host with a one-poll spin limit, so every kernel
