@@ -558,8 +558,14 @@ struct pp_ctx {
   // launch (a direct device-to-host copy)
   ChainState* cs_pin = nullptr;
   size_t cs_pin_n = 0;
+  // pinned staging of the tree tables uploaded per call (copies from
+  // pageable memory would each wait for the stream); filled front to back,
+  // reused after a device synchronization
+  uint8_t* stage = nullptr;
+  size_t stage_cap = 0, stage_used = 0;
   ~pp_ctx() {
     if (cs_pin) (void)hipHostFree(cs_pin);
+    if (stage) (void)hipHostFree(stage);
     for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &sel0, &bits,
                       &ring, &cs, &partial, &flag, &gx, &gxp, &sp_lists, &spill})
@@ -584,6 +590,30 @@ int ensure_cs_pin(pp_ctx* c, size_t count) {
   c->cs_pin_n = 0;
   PP_HIP(hipHostMalloc((void**)&c->cs_pin, count * sizeof(ChainState), hipHostMallocDefault));
   c->cs_pin_n = count;
+  return PP_OK;
+}
+
+// Host-to-device copy of `bytes` at `src` (which the caller may reuse at
+// once) through the context's pinned staging buffer.
+int stage_h2d(pp_ctx* c, void* dst, const void* src, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return PP_OK;
+  const size_t need = (bytes + 255) & ~(size_t)255;
+  if (c->stage_used + need > c->stage_cap) {
+    // every copy out of the buffer has completed before it is written again
+    PP_HIP(hipDeviceSynchronize());
+    c->stage_used = 0;
+    if (need > c->stage_cap) {
+      const size_t cap = std::max({need * 4, c->stage_cap * 2, (size_t)1 << 20});
+      if (c->stage) PP_HIP(hipHostFree(c->stage));
+      c->stage = nullptr;
+      c->stage_cap = 0;
+      PP_HIP(hipHostMalloc((void**)&c->stage, cap, hipHostMallocDefault));
+      c->stage_cap = cap;
+    }
+  }
+  std::memcpy(c->stage + c->stage_used, src, bytes);
+  PP_HIP(hipMemcpyAsync(dst, c->stage + c->stage_used, bytes, hipMemcpyHostToDevice, st));
+  c->stage_used += need;
   return PP_OK;
 }
 
@@ -976,8 +1006,6 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
       st[q].done = false;
       std::memcpy(st[q].dirty, cs0[q].dirty, sizeof st[q].dirty);
     }
-    std::vector<int32_t> z(A, 0);
-    PP_HIP(launch_reset_round(chain_set(starts, z, z, 0, A), d, e.st));
   }
   auto worker_at = [&](const St& x, int32_t a) { return res.orders[(size_t)x.s * m + a]; };
   auto resolved_free = [&](const St& x, int32_t a) {
@@ -1006,8 +1034,6 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
           }
           x.pos = 0;
           x.improved = false;
-          const std::vector<int32_t> one = {x.s}, z = {0};
-          PP_HIP(launch_reset_round(chain_set(one, z, z, 0, 1), d, e.st));
           continue;
         }
         if (!resolved_free(x, x.pos)) break;
@@ -1093,16 +1119,15 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
     PP_TRY(e.dp(set, 1));
     PP_HIP(launch_backtrack(set, d, kModeRefine, e.st));
     if (d.f64) PP_HIP(launch_gexact(set, d, kModeRefine, e.st));
-    // the launch's results: the starts' slots (consecutive) and the spare
-    // slots, in two copies (to pinned memory: starts, then spares)
-    PP_TRY(ensure_cs_pin(e.c, (size_t)A + (size_t)spares));
+    // the launch's results, to pinned memory in one copy: the starts' slots
+    // (consecutive) through the last spare slot used (the slots between
+    // them come along unread)
+    const size_t span = spares > 0 ? (size_t)(spare_base + spares - starts[0]) : (size_t)A;
+    PP_TRY(ensure_cs_pin(e.c, span));
     ChainState* own = e.c->cs_pin;
-    ChainState* spare = e.c->cs_pin + A;
-    PP_HIP(hipMemcpyAsync(own, d.cs + starts[0], sizeof(ChainState) * A,
+    ChainState* spare = e.c->cs_pin + (spare_base - starts[0]);
+    PP_HIP(hipMemcpyAsync(own, d.cs + starts[0], sizeof(ChainState) * span,
                           hipMemcpyDeviceToHost, e.st));
-    if (spares > 0)
-      PP_HIP(hipMemcpyAsync(spare, d.cs + spare_base, sizeof(ChainState) * spares,
-                            hipMemcpyDeviceToHost, e.st));
     PP_TRY(poll_stream(e.st));
     std::vector<ChainState> cs(items.size());
     for (size_t k = 0; k < items.size(); ++k)
@@ -1110,6 +1135,8 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
                                           : own[items[k].slot - starts[0]];
     // decisions, in each start's order
     std::vector<int32_t> csl, cwk, ckp;
+    AdoptSet ad;
+    ad.count = 0;
     size_t k = 0;
     for (int32_t q = 0; q < A; ++q) {
       St& x = st[q];
@@ -1131,8 +1158,6 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
           for (int32_t a = last + 1; a < m; ++a) res.skipped_cells += free_cells(x, a);
           res.sweeps[x.s] += 1;
           x.improved = false;
-          const std::vector<int32_t> one = {x.s}, z = {0};
-          PP_HIP(launch_reset_round(chain_set(one, z, z, 0, 1), d, e.st));
           last = -1;
           in_next = true;
         }
@@ -1155,15 +1180,20 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
       for (uint32_t b : ran) any_ran = any_ran || b != 0;
       // (an update in the start's own slot is backtracked and marked by
       // k_backtrack itself)
-      if ((take && take->slot != x.s) || (!take && any_ran))
-        PP_HIP(launch_adopt(d, x.s, take ? take->slot : -1, take ? take->worker : 0, ran,
-                            e.st));
+      if ((take && take->slot != x.s) || (!take && any_ran)) {
+        const int32_t q2 = ad.count++;
+        ad.slot[q2] = x.s;
+        ad.from[q2] = take ? take->slot : -1;
+        ad.worker[q2] = take ? take->worker : 0;
+        std::memcpy(ad.ran[q2], ran, sizeof ran);
+      }
       if (take) {
         csl.push_back(x.s);
         cwk.push_back(take->worker);
         ckp.push_back(kp[take->worker]);
       }
     }
+    PP_HIP(launch_adopt(ad, d, e.st));
     if (!csl.empty())
       PP_HIP(launch_commit(chain_set(csl, cwk, ckp, 0, csl.size()), d, kModeRefine, e.st));
   }
@@ -1540,12 +1570,9 @@ int upload_tree(pp_ctx* c, const TreeLayout& t, hipStream_t st) {
   PP_TRY(c->nextpos.ensure(n * 4));
   PP_TRY(c->ce.ensure(t.ce.size() * 4));
   PP_TRY(c->order.ensure(n * 4));
-  PP_HIP(hipMemcpyAsync(c->nextpos.p, t.nextpos.data(), n * 4,
-                        hipMemcpyHostToDevice, st));
-  PP_HIP(hipMemcpyAsync(c->ce.p, t.ce.data(), t.ce.size() * 4, hipMemcpyHostToDevice,
-                        st));
-
-  PP_HIP(hipMemcpyAsync(c->order.p, t.order.data(), n * 4, hipMemcpyHostToDevice, st));
+  PP_TRY(stage_h2d(c, c->nextpos.p, t.nextpos.data(), n * 4, st));
+  PP_TRY(stage_h2d(c, c->ce.p, t.ce.data(), t.ce.size() * 4, st));
+  PP_TRY(stage_h2d(c, c->order.p, t.order.data(), n * 4, st));
   return PP_OK;
 }
 
@@ -1584,12 +1611,10 @@ int upload_spills(pp_ctx* c, const TreeLayout& t, DevState& d, int32_t slots,
                e = t.spill_in.size();
   PP_TRY(c->sp_lists.ensure((a + b + c2 + e) * 4));
   int32_t* base = c->sp_lists.as<int32_t>();
-  PP_HIP(hipMemcpyAsync(base, t.out_off.data(), a * 4, hipMemcpyHostToDevice, st));
-  if (b) PP_HIP(hipMemcpyAsync(base + a, t.spill_out.data(), b * 4, hipMemcpyHostToDevice, st));
-  PP_HIP(hipMemcpyAsync(base + a + b, t.in_off.data(), c2 * 4, hipMemcpyHostToDevice, st));
-  if (e)
-    PP_HIP(hipMemcpyAsync(base + a + b + c2, t.spill_in.data(), e * 4, hipMemcpyHostToDevice,
-                          st));
+  PP_TRY(stage_h2d(c, base, t.out_off.data(), a * 4, st));
+  PP_TRY(stage_h2d(c, base + a, t.spill_out.data(), b * 4, st));
+  PP_TRY(stage_h2d(c, base + a + b, t.in_off.data(), c2 * 4, st));
+  PP_TRY(stage_h2d(c, base + a + b + c2, t.spill_in.data(), e * 4, st));
   d.sp_out_off = base;
   d.sp_out = base + a;
   d.sp_in_off = base + a + b;
@@ -1603,8 +1628,7 @@ int upload_meta(pp_ctx* c, const TreeLayout& t, int cells, hipStream_t st) {
   c->meta_host = encode_meta(t, cells);
   PP_TRY(check_meta(t, c->meta_host, cells));
   PP_TRY(c->meta.ensure(c->meta_host.size() * 4));
-  PP_HIP(hipMemcpyAsync(c->meta.p, c->meta_host.data(), c->meta_host.size() * 4,
-                        hipMemcpyHostToDevice, st));
+  PP_TRY(stage_h2d(c, c->meta.p, c->meta_host.data(), c->meta_host.size() * 4, st));
   return PP_OK;
 }
 

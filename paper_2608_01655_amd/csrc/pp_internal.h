@@ -164,7 +164,6 @@ struct ChainState {
   int64_t gwo;       // G(T_-h): objective with T_h emptied
   int64_t obj;       // objective of the chain's placement
   int32_t accept;    // last update adopted its DP result
-  int32_t improved;  // some update of the current sweep was accepted
   int32_t accepts;   // accepted refinement replacements so far
   int32_t status;    // nonzero: a device-side wait gave up
   // Real-valued refinement: the update was rejected before its walk (its
@@ -195,6 +194,16 @@ struct ChainSet {
   int32_t worker[kMaxChains];  // worker h being updated
   int32_t kprime[kMaxChains];  // min(k_h, n)
   int32_t base[kMaxChains + 1];  // DP: first block of each chain's stages
+};
+
+// Adoptions after a speculative refinement launch, one per start, passed
+// by value as a kernel argument.
+struct AdoptSet {
+  int32_t count;
+  int32_t slot[kMaxChains];    // the start's slot
+  int32_t from[kMaxChains];    // spare slot of the accepted update, or -1
+  int32_t worker[kMaxChains];  // its worker (from >= 0)
+  uint32_t ran[kMaxChains][8]; // workers swept against the unchanged placement
 };
 
 // Device-resident problem and per-slot state of a context.
@@ -252,6 +261,9 @@ struct DevState {
   uint64_t* gxp;
   int32_t gx_blocks;
 };
+// kernel arguments stay within the 4 KB that every launch path accepts
+static_assert(sizeof(AdoptSet) + sizeof(DevState) <= 4096, "k_adopt arguments");
+static_assert(sizeof(ChainSet) + sizeof(DevState) + 64 <= 4096, "ChainSet kernel arguments");
 
 // Host-side launchers (pp_kernels.hip).  All enqueue on `st`.
 hipError_t launch_gather(const int64_t* src, int64_t* dst, int32_t rows,
@@ -301,20 +313,17 @@ hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
 hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
                             hipStream_t st);
 // Speculative refinement: the updates of consecutive positions of one
-// start run together in spare slots; the first accepted one (position
-// `take`, in spare slot `from`, or none: from = -1) is adopted into the
-// start's slot `s`, whose stale-input marks lose the bits in `ran` (workers
-// whose sweep ran against the unchanged placement).
-hipError_t launch_adopt(const DevState& d, int32_t s, int32_t from, int32_t worker,
-                        const uint32_t (&ran)[8], hipStream_t st);
+// start run together in spare slots; per start, the first accepted one (in
+// spare slot `from`, or none: from = -1) is adopted into the start's slot,
+// whose stale-input marks lose the bits in `ran` (workers whose sweep ran
+// against the unchanged placement).  One launch for every start.
+hipError_t launch_adopt(const AdoptSet& set, const DevState& d, hipStream_t st);
 // Greedy position 0: each chain adopts the standalone selection of its
 // worker (row `worker` of sel0, [m][npad/32]) as its walk would have.
 hipError_t launch_take_standalone(const ChainSet& set, const DevState& d,
                                  const uint32_t* sel0, hipStream_t st);
 hipError_t launch_commit(const ChainSet& set, const DevState& d, int mode,
                          hipStream_t st);
-hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
-                              hipStream_t st);
 hipError_t launch_objective(const ChainSet& set, const DevState& d,
                             hipStream_t st);
 

@@ -21,8 +21,10 @@
 // F64 template flag of k_dp, DevState::f64 elsewhere); indices are int32.
 
 #include <algorithm>
+#include <array>
 #include <mutex>
 #include <utility>
+#include <vector>
 
 #include "pp_internal.h"
 
@@ -1509,10 +1511,7 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     if (lane == 0) {
       st->accept = accept ? 1 : 0;
       st->inc = 0;
-      if (mode == kModeRefine && accept) {
-        st->improved = 1;
-        st->accepts += 1;
-      }
+      if (mode == kModeRefine && accept) st->accepts += 1;
     }
   }
   if (!accept) return;
@@ -1738,17 +1737,15 @@ __global__ void __launch_bounds__(kCommitThreads) k_commit(ChainSet set, DevStat
   if (changed && r == 0) th[i] = nv;
 }
 
-// Speculative refinement, after the decision: the workers in `ran` swept
-// against the start's unchanged placement (their inputs are current); if a
-// later position was accepted in spare slot `from`, slot s takes its
-// selection and acceptance as k_backtrack leaves them for an update run in
-// slot s itself, so that k_commit can adopt it there.
-struct Bits8 {
-  uint32_t w[8];
-};
-
-__global__ void __launch_bounds__(256) k_adopt(DevState d, int32_t s, int32_t from,
-                                               int32_t h, Bits8 ran) {
+// Speculative refinement, after the decisions (one block per start): the
+// workers in `ran` swept against the start's unchanged placement (their
+// inputs are current); if a later position was accepted in spare slot
+// `from`, slot s takes its selection and acceptance as k_backtrack leaves
+// them for an update run in slot s itself, so that k_commit can adopt it
+// there.
+__global__ void __launch_bounds__(256) k_adopt(AdoptSet set, DevState d) {
+  const int ci = blockIdx.x;
+  const int32_t s = set.slot[ci], from = set.from[ci], h = set.worker[ci];
   ChainState* st = d.cs + s;
   if (from >= 0) {
     const int nwords = d.npad / 32;
@@ -1763,13 +1760,12 @@ __global__ void __launch_bounds__(256) k_adopt(DevState d, int32_t s, int32_t fr
   }
   if (threadIdx.x == 0) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) st->dirty[q] &= ~ran.w[q];
+    for (int q = 0; q < 8; ++q) st->dirty[q] &= ~set.ran[ci][q];
     if (from >= 0) {
       const ChainState& fs = d.cs[from];
       st->accept = 1;
       st->inc = 0;
       st->dpval = fs.dpval;
-      st->improved = 1;
       st->accepts += 1;
 #pragma unroll
       for (int q = 0; q < 8; ++q)
@@ -1898,12 +1894,6 @@ __global__ void __launch_bounds__(256) k_mat_cost(DevState d, int64_t inc, int64
     __syncthreads();
   }
   if (threadIdx.x == 0) partial[blockIdx.x] = part[0];
-}
-
-// Start of a refinement sweep: no replacement accepted yet.
-__global__ void k_reset_round(ChainSet set, DevState d) {
-  const int ci = threadIdx.x;
-  if (ci < set.count) d.cs[set.slot[ci]].improved = 0;
 }
 
 // ----------------------------------------------------------- objective --
@@ -2038,10 +2028,7 @@ __global__ void __launch_bounds__(256) k_gexact_final(ChainSet set, DevState d, 
   }
   st->accept = accept ? 1 : 0;
   if (!accept) return;
-  if (mode == kModeRefine) {
-    st->improved = 1;
-    st->accepts += 1;
-  }
+  if (mode == kModeRefine) st->accepts += 1;
   const int h = set.worker[ci];
   for (int q = 0; q < 8; ++q) st->dirty[q] |= q == (h >> 5) ? ~(1u << (h & 31)) : ~0u;
   if (s == ps)
@@ -2202,7 +2189,31 @@ hipError_t launch_dp(const ChainSet& set, const DevState& d, uint32_t epoch,
   }
 }
 
+namespace {
+int dp_resident_blocks_query(int cells, int32_t slots_lds, int device);
+}
+
+// Stage blocks of the sweep that fit the device at once (occupancy queries,
+// remembered per width, LDS stack height and device).
 int dp_resident_blocks(int cells, int32_t slots_lds, int device) {
+  static std::mutex mu;
+  static std::vector<std::pair<std::array<int, 3>, int>> known;
+  const std::array<int, 3> key = {cells, (int)slots_lds, device};
+  {
+    std::lock_guard<std::mutex> g(mu);
+    for (const auto& kv : known)
+      if (kv.first == key) return kv.second;
+  }
+  const int v = dp_resident_blocks_query(cells, slots_lds, device);
+  if (v > 0) {
+    std::lock_guard<std::mutex> g(mu);
+    known.emplace_back(key, v);
+  }
+  return v;
+}
+
+namespace {
+int dp_resident_blocks_query(int cells, int32_t slots_lds, int device) {
   int per_cu = 0, per_cu_f = 0, cus = 0;
   const size_t lds = dp_lds_bytes(cells, slots_lds);
   hipError_t e = hipErrorInvalidValue, e2 = hipErrorInvalidValue;
@@ -2229,6 +2240,7 @@ int dp_resident_blocks(int cells, int32_t slots_lds, int device) {
     return 0;
   return per_cu * cus;
 }
+}  // namespace
 
 hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
                             hipStream_t st) {
@@ -2241,11 +2253,9 @@ hipError_t launch_backtrack(const ChainSet& set, const DevState& d, int mode,
   return hipGetLastError();
 }
 
-hipError_t launch_adopt(const DevState& d, int32_t s, int32_t from, int32_t worker,
-                        const uint32_t (&ran)[8], hipStream_t st) {
-  Bits8 b;
-  for (int q = 0; q < 8; ++q) b.w[q] = ran[q];
-  hipLaunchKernelGGL(k_adopt, dim3(1), dim3(256), 0, st, d, s, from, worker, b);
+hipError_t launch_adopt(const AdoptSet& set, const DevState& d, hipStream_t st) {
+  if (set.count == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_adopt, dim3(set.count), dim3(256), 0, st, set, d);
   return hipGetLastError();
 }
 
@@ -2260,12 +2270,6 @@ hipError_t launch_commit(const ChainSet& set, const DevState& d, int mode,
                          hipStream_t st) {
   hipLaunchKernelGGL(k_commit, grid1(d.n, kCommitThreads / d.m, set.count),
                      dim3(kCommitThreads), 0, st, set, d, mode);
-  return hipGetLastError();
-}
-
-hipError_t launch_reset_round(const ChainSet& set, const DevState& d,
-                              hipStream_t st) {
-  hipLaunchKernelGGL(k_reset_round, dim3(1), dim3(kMaxChains), 0, st, set, d);
   return hipGetLastError();
 }
 
