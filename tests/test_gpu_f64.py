@@ -329,3 +329,22 @@ def test_f64_speculation_into_the_next_sweep(oracle_mod, monkeypatch, chains, ro
     g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
     o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, **kw)
     _same_real(g, o)
+
+
+@pytest.mark.parametrize("seed", range(15))
+def test_plan_f64_random_launch_budgets(oracle_mod, monkeypatch, seed):
+    """Real-valued random plans with 2 to 64 updates per refinement launch:
+    the oracle's plan, bit for bit."""
+    rng = np.random.default_rng(6100 + seed)
+    m = int(rng.integers(1, 7))
+    n = int(rng.integers(1, 300))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, n + 2])),
+                             source_dependent=bool(seed % 3))
+    lam, w, f = W.real_valued(inst, seed, jitter=0.5)
+    kw = dict(n_starts=int(rng.integers(0, 6)), max_rounds=int(rng.integers(0, 4)),
+              order_seed=int(rng.integers(0, 2 ** 62)))
+    eps = 1e-9 * (float(np.sum(lam * w)) + 1.0)
+    monkeypatch.setenv("PP_SPEC_CHAINS", str(int(rng.choice([2, 3, 5, 64]))))
+    g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
+    _same_real(g, o)

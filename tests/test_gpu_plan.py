@@ -62,6 +62,26 @@ def test_plan_random(oracle_mod, seed):
     _same(g, o)
 
 
+@pytest.mark.parametrize("seed", range(30))
+def test_plan_random_launch_budgets(oracle_mod, monkeypatch, seed):
+    """Random small plans with 2 to 64 updates per refinement launch (so
+    that speculation, within a sweep and into the next, stops at every
+    kind of boundary: launch budget, sweep cap, workers without capacity,
+    a single worker) and a few stage blocks per launch: the oracle's plan."""
+    rng = np.random.default_rng(5000 + seed)
+    m = int(rng.integers(1, 9))
+    n = int(rng.integers(1, 400))
+    inst = W.random_instance(n, m, rng, kmax=int(rng.choice([3, 40, 200, n + 2])),
+                             source_dependent=bool(seed % 3),
+                             value_range=int(rng.choice([5, 100, 10 ** 5])))
+    monkeypatch.setenv("PP_SPEC_CHAINS", str(int(rng.choice([2, 3, 5, 9, 64]))))
+    monkeypatch.setenv("PP_SPEC_BLOCKS", str(int(rng.choice([1, 3, 8, 512]))))
+    g, o = _plan_both(oracle_mod, inst, n_starts=int(rng.integers(0, 7)),
+                      max_rounds=int(rng.integers(0, 4)),
+                      order_seed=int(rng.integers(0, 2 ** 62)))
+    _same(g, o)
+
+
 def test_plan_flags_and_explicit_orders(oracle_mod):
     rng = np.random.default_rng(11)
     inst = W.random_instance(150, 4, rng, kmax=60)
