@@ -617,9 +617,10 @@ int stage_h2d(pp_ctx* c, void* dst, const void* src, size_t bytes, hipStream_t s
   return PP_OK;
 }
 
-// Waits for `st` by polling: after each refinement launch the host decides
-// the next launch from the chain states, so the wake-up delay of a
-// blocking wait would leave the device idle.
+// Waits for `st` by polling (every wait of the library): the host decides
+// the next launches from what it reads back (after each refinement launch,
+// the chain states), so the wake-up delay of a blocking wait would leave
+// the device idle, and for small trees it is a large part of a call.
 int poll_stream(hipStream_t st) {
   for (;;) {
     const hipError_t q = hipStreamQuery(st);
@@ -679,7 +680,7 @@ int read_exact(const DevState& d, int32_t first, int32_t count, hipStream_t st,
     PP_HIP(hipMemcpyAsync(out.data() + (size_t)q * kExLimbs,
                           d.gx + (size_t)(first + q) * 2 * kExLimbs, kExLimbs * 4,
                           hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   return PP_OK;
 }
 
@@ -869,7 +870,7 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
   PP_HIP(launch_requester_check(d.f, d.n, m, c->flag.as<int32_t>(), st));
   int32_t mismatch = 0;
   PP_HIP(hipMemcpyAsync(&mismatch, c->flag.p, 4, hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   if (mismatch) return PP_OK;  // source-dependent costs: no comparators
   // keep the best start's placement out of the scratch slots
   PP_HIP(hipMemcpyAsync(d.tgt + (size_t)slot_b * mn, d.tgt + (size_t)res.win_slot * mn,
@@ -926,12 +927,12 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
   std::vector<ChainState> fin(3);
   PP_HIP(hipMemcpyAsync(fin.data(), d.cs + cand_slot[0], sizeof(ChainState) * 3,
                         hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   // the scratch chains' status words, in case a DP wait gave up
   std::vector<ChainState> scr(m);
   PP_HIP(hipMemcpyAsync(scr.data(), d.cs, sizeof(ChainState) * m,
                         hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   for (const ChainState& x : fin)
     if (x.status) return stall_fail();
   for (const ChainState& x : scr)
@@ -997,7 +998,7 @@ int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_b
     std::vector<ChainState> cs0(A);
     PP_HIP(hipMemcpyAsync(cs0.data(), d.cs + starts[0], sizeof(ChainState) * A,
                           hipMemcpyDeviceToHost, e.st));
-    PP_HIP(hipStreamSynchronize(e.st));
+    PP_TRY(poll_stream(e.st));
     for (int32_t q = 0; q < A; ++q) {
       if (cs0[q].status) return stall_fail();
       st[q].s = starts[q];
@@ -1216,7 +1217,7 @@ int run_plan(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
                                  attempt);
     res.restarts = attempt;
     if (rc == PP_OK || !g_stall || attempt >= kStallRetries) return rc;
-    PP_HIP(hipStreamSynchronize(st));
+    PP_TRY(poll_stream(st));
   }
 }
 
@@ -1359,7 +1360,7 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   PP_HIP(hipMemcpyAsync(c->sel0.p, d.sel, sel_bytes, hipMemcpyDeviceToDevice, st));
   PP_HIP(hipMemcpyAsync(hs.data(), d.cs, sizeof(ChainState) * m,
                         hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   for (int32_t h = 0; h < m; ++h) {
     if (hs[h].status) return stall_fail();
     res.standalone[h] = kp[h] > 0 ? hs[h].dpval : 0;
@@ -1419,7 +1420,7 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     std::vector<ChainState> fin(hi - lo);
     PP_HIP(hipMemcpyAsync(fin.data(), d.cs + lo, sizeof(ChainState) * (hi - lo),
                           hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
+    PP_TRY(poll_stream(st));
     for (int32_t s = lo; s < hi; ++s) {
       if (fin[s - lo].status) return stall_fail();
       res.start_obj[s] = fin[s - lo].obj;
@@ -1730,7 +1731,7 @@ int placement_to_host(pp_ctx* c, const TreeLayout& t, int32_t m, int32_t slot,
   std::vector<uint8_t> pre(mn);
   PP_HIP(hipMemcpyAsync(pre.data(), c->tgt.as<uint8_t>() + (size_t)slot * mn, mn,
                         hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   for (int32_t h = 0; h < m; ++h)
     for (size_t q = 0; q < n; ++q) out[(size_t)h * n + t.order[q]] = pre[(size_t)h * n + q];
   return PP_OK;
@@ -1793,7 +1794,7 @@ int replan_evaluate(pp_ctx* c, const TreeLayout& t, int32_t m, const PlanResult&
   ChainState inc_cs{};
   PP_HIP(hipMemcpyAsync(part.data(), c->partial.p, part.size(), hipMemcpyDeviceToHost, st));
   PP_HIP(hipMemcpyAsync(&inc_cs, d.cs + xs, sizeof(ChainState), hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   ev.g_inc = inc_cs.obj;
   if (!f64) {
     for (int32_t b = 0; b < nb; ++b) {
@@ -1996,7 +1997,7 @@ int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     int32_t neg = 0;
     PP_HIP(hipMemcpyAsync(part.data(), ctx->partial.p, 8 * nb, hipMemcpyDeviceToHost, st));
     PP_HIP(hipMemcpyAsync(&neg, ctx->flag.p, 4, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
+    PP_TRY(poll_stream(st));
     if (neg) return fail(PP_E_RANGE, "negative demand or cost");
     unsigned __int128 tot = 0;
     for (uint64_t v : part) tot += v;
@@ -2010,7 +2011,7 @@ int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     const size_t mn = (size_t)m * n;
     PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
                              target_dev, m, n, ctx->order.as<int32_t>(), st));
-    PP_HIP(hipStreamSynchronize(st));
+    PP_TRY(poll_stream(st));
     *objective = r.win_obj;
     fill_stats(stats, r, m);
     return PP_OK;
@@ -2074,7 +2075,7 @@ int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
                                ctx->flag.as<int32_t>(), st));
     int32_t bad = 0;
     PP_HIP(hipMemcpyAsync(&bad, ctx->flag.p, 4, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipStreamSynchronize(st));
+    PP_TRY(poll_stream(st));
     if (bad) return fail(PP_E_RANGE, "demand and costs must be finite and >= 0");
     PP_TRY(upload_tree(ctx, t, st));
     PP_TRY(layout_inputs(ctx, t, m, (const int64_t*)demand_dev,
@@ -2084,7 +2085,7 @@ int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     const size_t mn = (size_t)m * n;
     PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
                              target_dev, m, n, ctx->order.as<int32_t>(), st));
-    PP_HIP(hipStreamSynchronize(st));
+    PP_TRY(poll_stream(st));
     *objective = bits_f64(r.win_obj);
     fill_stats_f64(stats, r);
     return PP_OK;
@@ -2245,7 +2246,7 @@ static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v
       PP_HIP(launch_backtrack(set, d, kModeGreedy, st));
       PP_HIP(hipMemcpyAsync(pre.data(), d.sel, pre.size() * 4, hipMemcpyDeviceToHost, st));
       PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
-      PP_HIP(hipStreamSynchronize(st));
+      PP_TRY(poll_stream(st));
       if (!out.status) break;
       if (attempt >= kStallRetries) return stall_fail();
     }
@@ -2357,7 +2358,7 @@ static int marginal_or_objective(int32_t n, int32_t m, const int64_t* demand,
     PP_HIP(launch_objective(set, d, st));
   }
   PP_HIP(hipMemcpyAsync(&out, d.cs, sizeof out, hipMemcpyDeviceToHost, st));
-  PP_HIP(hipStreamSynchronize(st));
+  PP_TRY(poll_stream(st));
   if (gwo) *gwo = out.gwo;
   if (objective) *objective = out.obj;
   return PP_OK;
