@@ -543,7 +543,13 @@ struct pp_ctx {
   int device = 0;
   hipStream_t own = nullptr;
   // problem, preorder layout
-  DevBuf lam, w, f, nextpos, ce, meta, order;
+  DevBuf lam, w, f, meta;
+  // tree tables in one allocation (one upload): next positions, preorder
+  // (position -> caller id) and the backtrack's skip-chain table
+  DevBuf tree;
+  int32_t* nextpos = nullptr;
+  int32_t* order = nullptr;
+  uint32_t* ce = nullptr;
   // uploads for host-pointer entry points (caller order)
   DevBuf up_lam, up_w, up_f, up_u8;
   // per-slot state
@@ -553,11 +559,13 @@ struct pp_ctx {
   DevBuf sp_lists, spill;  // spilled skip rows of deep trees
   uint32_t epoch = 0;
   std::vector<uint32_t> meta_host;  // source of the last metadata upload
+  std::vector<uint8_t> tree_host;   // and of the last tree tables
   std::vector<hipEvent_t> events;
   // pinned host copy of the chain states read back after each refinement
   // launch (a direct device-to-host copy)
   ChainState* cs_pin = nullptr;
   size_t cs_pin_n = 0;
+  uint64_t* val_pin = nullptr;  // pinned read-back of the input checks
   // pinned staging of the tree tables uploaded per call (copies from
   // pageable memory would each wait for the stream); filled front to back,
   // reused after a device synchronization
@@ -566,7 +574,8 @@ struct pp_ctx {
   ~pp_ctx() {
     if (cs_pin) (void)hipHostFree(cs_pin);
     if (stage) (void)hipHostFree(stage);
-    for (DevBuf* b : {&lam, &w, &f, &nextpos, &ce, &meta, &order, &up_lam, &up_w,
+    if (val_pin) (void)hipHostFree(val_pin);
+    for (DevBuf* b : {&lam, &w, &f, &tree, &meta, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &sel0, &bits,
                       &ring, &cs, &partial, &flag, &gx, &gxp, &sp_lists, &spill})
       b->release();
@@ -590,6 +599,13 @@ int ensure_cs_pin(pp_ctx* c, size_t count) {
   c->cs_pin_n = 0;
   PP_HIP(hipHostMalloc((void**)&c->cs_pin, count * sizeof(ChainState), hipHostMallocDefault));
   c->cs_pin_n = count;
+  return PP_OK;
+}
+
+int ensure_val_pin(pp_ctx* c) {
+  if (!c->val_pin)
+    PP_HIP(hipHostMalloc((void**)&c->val_pin, 2 * kValidateBlocks * sizeof(uint64_t),
+                         hipHostMallocDefault));
   return PP_OK;
 }
 
@@ -1290,8 +1306,8 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   d.lam = c->lam.as<int64_t>();
   d.w = c->w.as<int64_t>();
   d.f = c->f.as<int64_t>();
-  d.nextpos = c->nextpos.as<int32_t>();
-  d.ce = c->ce.as<uint32_t>();
+  d.nextpos = c->nextpos;
+  d.ce = c->ce;
   // widest single launch: every start's update at once
   int64_t stage64 = 0;
   {
@@ -1568,13 +1584,17 @@ pp_ctx* thread_ctx(int& rc) {
 // Upload the tree layout and (already gathered or identity) inputs.
 int upload_tree(pp_ctx* c, const TreeLayout& t, hipStream_t st) {
   const size_t n = (size_t)t.n;
-  PP_TRY(c->nextpos.ensure(n * 4));
-  PP_TRY(c->ce.ensure(t.ce.size() * 4));
-  PP_TRY(c->order.ensure(n * 4));
-  PP_TRY(stage_h2d(c, c->nextpos.p, t.nextpos.data(), n * 4, st));
-  PP_TRY(stage_h2d(c, c->ce.p, t.ce.data(), t.ce.size() * 4, st));
-  PP_TRY(stage_h2d(c, c->order.p, t.order.data(), n * 4, st));
-  return PP_OK;
+  const size_t a = (n * 4 + 255) & ~(size_t)255, ceb = t.ce.size() * 4;
+  std::vector<uint8_t>& h = c->tree_host;
+  h.assign(2 * a + ceb, 0);
+  std::memcpy(h.data(), t.nextpos.data(), n * 4);
+  std::memcpy(h.data() + a, t.order.data(), n * 4);
+  std::memcpy(h.data() + 2 * a, t.ce.data(), ceb);
+  PP_TRY(c->tree.ensure(h.size()));
+  c->nextpos = c->tree.as<int32_t>();
+  c->order = (int32_t*)(c->tree.as<uint8_t>() + a);
+  c->ce = (uint32_t*)(c->tree.as<uint8_t>() + 2 * a);
+  return stage_h2d(c, c->tree.p, h.data(), h.size(), st);
 }
 
 // Every LDS row the metadata names must lie inside the sweep's LDS layout.
@@ -1641,10 +1661,9 @@ int layout_inputs(pp_ctx* c, const TreeLayout& t, int32_t m,
   PP_TRY(c->lam.ensure(m * n * 8));
   PP_TRY(c->w.ensure(m * n * 8));
   PP_TRY(c->f.ensure((size_t)m * m * n * 8));
-  const int32_t* ord = c->order.as<int32_t>();
-  PP_HIP(launch_gather(lam, c->lam.as<int64_t>(), m, t.n, ord, st));
-  PP_HIP(launch_gather(w, c->w.as<int64_t>(), m, t.n, ord, st));
-  PP_HIP(launch_gather(f, c->f.as<int64_t>(), m * m, t.n, ord, st));
+  const int32_t* ord = c->order;
+  PP_HIP(launch_gather_inputs(lam, w, f, c->lam.as<int64_t>(), c->w.as<int64_t>(),
+                              c->f.as<int64_t>(), m, t.n, ord, st));
   return PP_OK;
 }
 
@@ -1981,36 +2000,40 @@ int pp_plan_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     for (int32_t h = 0; h < m; ++h)
       if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
     TreeLayout t;
-    PP_TRY(build_tree(n, parent, t));
-    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    if (o.flags & PP_F_VALIDATE_ONLY) return build_tree(n, parent, t);
     PP_TRY(select_device(ctx));
     hipStream_t st = (hipStream_t)hip_stream;
-    // value checks on the device: negatives, and sum of lam*w added exactly
-    PP_TRY(ctx->partial.ensure(1024 * 8));
-    PP_TRY(ctx->flag.ensure(64));
-    PP_HIP(hipMemsetAsync(ctx->flag.p, 0, 4, st));
+    // value checks on the device (negatives, and the sum of lam*w added
+    // exactly), while the host builds the tree tables
+    PP_TRY(ctx->partial.ensure(2 * kValidateBlocks * 8));
+    PP_TRY(ensure_val_pin(ctx));
     int32_t nb = 0;
     PP_HIP(launch_validate(demand_dev, recompute_dev, fetch_dev, n, m,
-                           ctx->partial.as<uint64_t>(), ctx->flag.as<int32_t>(),
-                           &nb, st));
-    std::vector<uint64_t> part(nb);
-    int32_t neg = 0;
-    PP_HIP(hipMemcpyAsync(part.data(), ctx->partial.p, 8 * nb, hipMemcpyDeviceToHost, st));
-    PP_HIP(hipMemcpyAsync(&neg, ctx->flag.p, 4, hipMemcpyDeviceToHost, st));
-    PP_TRY(poll_stream(st));
-    if (neg) return fail(PP_E_RANGE, "negative demand or cost");
-    unsigned __int128 tot = 0;
-    for (uint64_t v : part) tot += v;
-    if (tot > (unsigned __int128)INT64_MAX)
-      return fail(PP_E_OVERFLOW, "sum of demand * recompute cost exceeds INT64_MAX");
+                           ctx->partial.as<uint64_t>(), &nb, st));
+    PP_HIP(hipMemcpyAsync(ctx->val_pin, ctx->partial.p, 16 * (size_t)nb,
+                          hipMemcpyDeviceToHost, st));
+    const int trc = build_tree(n, parent, t);
+    if (trc != PP_OK) {
+      PP_TRY(poll_stream(st));
+      return trc;
+    }
+    // the layout does not depend on the checks' outcome
     PP_TRY(upload_tree(ctx, t, st));
     PP_TRY(layout_inputs(ctx, t, m, demand_dev, recompute_dev, fetch_dev, st));
+    PP_TRY(poll_stream(st));
+    unsigned __int128 tot = 0;
+    for (int32_t b = 0; b < nb; ++b) {
+      if (ctx->val_pin[nb + b]) return fail(PP_E_RANGE, "negative demand or cost");
+      tot += ctx->val_pin[b];
+    }
+    if (tot > (unsigned __int128)INT64_MAX)
+      return fail(PP_E_OVERFLOW, "sum of demand * recompute cost exceeds INT64_MAX");
     PlanResult r;
     PP_TRY(run_plan(ctx, t, m, cap, o, tot < kFmaxBound, st, r));
     // best start's placement back to caller ids
     const size_t mn = (size_t)m * n;
     PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
-                             target_dev, m, n, ctx->order.as<int32_t>(), st));
+                             target_dev, m, n, ctx->order, st));
     PP_TRY(poll_stream(st));
     *objective = r.win_obj;
     fill_stats(stats, r, m);
@@ -2084,7 +2107,7 @@ int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     PP_TRY(run_plan(ctx, t, m, cap, o, false, st, r, 0, true, epsilon));
     const size_t mn = (size_t)m * n;
     PP_HIP(launch_scatter_u8(ctx->tgt.as<uint8_t>() + (size_t)r.win_slot * mn,
-                             target_dev, m, n, ctx->order.as<int32_t>(), st));
+                             target_dev, m, n, ctx->order, st));
     PP_TRY(poll_stream(st));
     *objective = bits_f64(r.win_obj);
     fill_stats_f64(stats, r);
@@ -2213,8 +2236,8 @@ static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v
     d.n = n;
     d.m = 1;
     d.npad = npad_of(n);
-    d.nextpos = c->nextpos.as<int32_t>();
-    d.ce = c->ce.as<uint32_t>();
+    d.nextpos = c->nextpos;
+    d.ce = c->ce;
     d.f64 = f64 ? 1 : 0;
     const int32_t slots_lds = t.slots;
     const int cells = choose_cells((kp + 63) / 64, c->device, slots_lds);
@@ -2225,7 +2248,7 @@ static int rooted_dp_impl(int32_t n, const int32_t* parent, const void* profit_v
     PP_TRY(c->up_lam.ensure((size_t)n * 8));
     PP_HIP(hipMemcpyAsync(c->up_lam.p, profit, (size_t)n * 8, hipMemcpyHostToDevice, st));
     PP_HIP(launch_gather(c->up_lam.as<int64_t>(), d.profit, 1, n,
-                         c->order.as<int32_t>(), st));
+                         c->order, st));
     std::vector<int32_t> sl{0}, wk{0}, kk{kp};
     ChainSet set = chain_set(sl, wk, kk, 0, 1);
     Engine e;

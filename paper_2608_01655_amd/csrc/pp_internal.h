@@ -268,16 +268,23 @@ static_assert(sizeof(ChainSet) + sizeof(DevState) + 64 <= 4096, "ChainSet kernel
 // Host-side launchers (pp_kernels.hip).  All enqueue on `st`.
 hipError_t launch_gather(const int64_t* src, int64_t* dst, int32_t rows,
                          int32_t n, const int32_t* order, hipStream_t st);
+// lam, w ([m][n]) and f ([m][m][n]) gathered to preorder in one launch
+hipError_t launch_gather_inputs(const int64_t* lam, const int64_t* w, const int64_t* f,
+                                int64_t* dlam, int64_t* dw, int64_t* df, int32_t m,
+                                int32_t n, const int32_t* order, hipStream_t st);
 hipError_t launch_gather_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
                             int32_t n, const int32_t* order, hipStream_t st);
 hipError_t launch_scatter_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
                              int32_t n, const int32_t* order, hipStream_t st);
 hipError_t launch_scatter_i64(const int64_t* src, int64_t* dst, int32_t n,
                               const int32_t* order, hipStream_t st);
+// integer inputs, *nblocks (<= kValidateBlocks) blocks: partial[b] = block
+// b's sum of lam*w (UINT64_MAX if it exceeds INT64_MAX), partial[nblocks +
+// b] = 1 if block b saw a negative value, else 0
+constexpr int kValidateBlocks = 1024;
 hipError_t launch_validate(const int64_t* lam, const int64_t* w,
                            const int64_t* f, int32_t n, int32_t m,
-                           uint64_t* partial, int32_t* neg, int32_t* nblocks,
-                           hipStream_t st);
+                           uint64_t* partial, int32_t* nblocks, hipStream_t st);
 // real-valued inputs: *bad = 1 if any value is negative, NaN or infinite
 hipError_t launch_validate_f64(const double* lam, const double* w,
                                const double* f, int32_t n, int32_t m,

@@ -189,6 +189,31 @@ __global__ void k_gather(const int64_t* __restrict__ src, int64_t* __restrict__ 
   }
 }
 
+// The three inputs in one launch: rows [0, m) of lam, then of w, then the
+// m*m rows of f.
+__global__ void k_gather_inputs(const int64_t* __restrict__ lam, const int64_t* __restrict__ w,
+                                const int64_t* __restrict__ f, int64_t* __restrict__ dlam,
+                                int64_t* __restrict__ dw, int64_t* __restrict__ df, int32_t m,
+                                int32_t n, const int32_t* __restrict__ order) {
+  int64_t row = blockIdx.y;
+  const int64_t* src = lam;
+  int64_t* dst = dlam;
+  if (row >= 2 * m) {
+    row -= 2 * m;
+    src = f;
+    dst = df;
+  } else if (row >= m) {
+    row -= m;
+    src = w;
+    dst = dw;
+  }
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    const int64_t v = src[row * n + order[i]];
+    dst[row * n + i] = v == INT64_MIN ? 0 : v;
+  }
+}
+
 __global__ void k_gather_u8(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
                             int32_t n, const int32_t* __restrict__ order) {
   const int64_t row = blockIdx.y;
@@ -214,7 +239,7 @@ __global__ void k_scatter_i64(const int64_t* __restrict__ src, int64_t* __restri
 // the host to add exactly.
 __global__ void k_validate(const int64_t* __restrict__ lam, const int64_t* __restrict__ w,
                            const int64_t* __restrict__ f, int64_t mn, int64_t mmn,
-                           uint64_t* partial, int32_t* neg) {
+                           uint64_t* partial) {
   uint64_t acc = 0;
   bool ovf = false, bad = false;
   for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mmn;
@@ -234,7 +259,10 @@ __global__ void k_validate(const int64_t* __restrict__ lam, const int64_t* __res
         acc += prod;
     }
   }
-  if (bad) atomicOr(neg, 1);
+  // this block's flag: partial[gridDim.x + block] (every block writes its
+  // own, so nothing needs clearing first)
+  const int any_bad = __syncthreads_or(bad ? 1 : 0);
+  if (threadIdx.x == 0) partial[gridDim.x + blockIdx.x] = any_bad ? 1 : 0;
   // block sum with saturation: each term is <= INT64_MAX, so two fit u64
   __shared__ uint64_t part[256];
   part[threadIdx.x] = ovf ? UINT64_MAX : acc;
@@ -2052,6 +2080,14 @@ hipError_t launch_gather(const int64_t* src, int64_t* dst, int32_t rows,
   return hipGetLastError();
 }
 
+hipError_t launch_gather_inputs(const int64_t* lam, const int64_t* w, const int64_t* f,
+                                int64_t* dlam, int64_t* dw, int64_t* df, int32_t m,
+                                int32_t n, const int32_t* order, hipStream_t st) {
+  hipLaunchKernelGGL(k_gather_inputs, grid1(n, 256, 2 * m + m * m), dim3(256), 0, st, lam,
+                     w, f, dlam, dw, df, m, n, order);
+  return hipGetLastError();
+}
+
 hipError_t launch_gather_u8(const uint8_t* src, uint8_t* dst, int32_t rows,
                             int32_t n, const int32_t* order, hipStream_t st) {
   hipLaunchKernelGGL(k_gather_u8, grid1(n, 256, rows), dim3(256), 0, st, src,
@@ -2075,14 +2111,13 @@ hipError_t launch_scatter_i64(const int64_t* src, int64_t* dst, int32_t n,
 
 hipError_t launch_validate(const int64_t* lam, const int64_t* w,
                            const int64_t* f, int32_t n, int32_t m,
-                           uint64_t* partial, int32_t* neg, int32_t* nblocks,
-                           hipStream_t st) {
+                           uint64_t* partial, int32_t* nblocks, hipStream_t st) {
   const int64_t mn = (int64_t)m * n, mmn = mn * m;
   int64_t b = (mmn + 255) / 256;
-  if (b > 1024) b = 1024;
+  if (b > kValidateBlocks) b = kValidateBlocks;
   *nblocks = (int32_t)b;
   hipLaunchKernelGGL(k_validate, dim3((unsigned)b), dim3(256), 0, st, lam, w,
-                     f, mn, mmn, partial, neg);
+                     f, mn, mmn, partial);
   return hipGetLastError();
 }
 
