@@ -567,13 +567,19 @@ struct pp_ctx {
   size_t cs_pin_n = 0;
   uint64_t* val_pin = nullptr;  // pinned read-back of the input checks
   // pinned staging of the tree tables uploaded per call (copies from
-  // pageable memory would each wait for the stream); filled front to back,
-  // reused after a device synchronization
+  // pageable memory would each wait for the stream); filled front to back
+  // and reused once the copies out of it have completed: stage_ev is
+  // recorded on stage_st after the latest copy, and every earlier copy not
+  // known to be complete is on that stream too
   uint8_t* stage = nullptr;
   size_t stage_cap = 0, stage_used = 0;
+  hipEvent_t stage_ev = nullptr;
+  hipStream_t stage_st = nullptr;
+  bool stage_pending = false;
   ~pp_ctx() {
     if (cs_pin) (void)hipHostFree(cs_pin);
     if (stage) (void)hipHostFree(stage);
+    if (stage_ev) (void)hipEventDestroy(stage_ev);
     if (val_pin) (void)hipHostFree(val_pin);
     for (DevBuf* b : {&lam, &w, &f, &tree, &meta, &up_lam, &up_w,
                       &up_f, &up_u8, &tgt, &v1, &v2, &h1, &profit, &sel, &sel0, &bits,
@@ -614,9 +620,14 @@ int ensure_val_pin(pp_ctx* c) {
 int stage_h2d(pp_ctx* c, void* dst, const void* src, size_t bytes, hipStream_t st) {
   if (bytes == 0) return PP_OK;
   const size_t need = (bytes + 255) & ~(size_t)255;
+  // copies on another stream, or a full buffer: wait for the copies out of
+  // it, then fill it from the front
+  if (c->stage_pending && (c->stage_st != st || c->stage_used + need > c->stage_cap)) {
+    PP_HIP(hipEventSynchronize(c->stage_ev));
+    c->stage_pending = false;
+    c->stage_used = 0;
+  }
   if (c->stage_used + need > c->stage_cap) {
-    // every copy out of the buffer has completed before it is written again
-    PP_HIP(hipDeviceSynchronize());
     c->stage_used = 0;
     if (need > c->stage_cap) {
       const size_t cap = std::max({need * 4, c->stage_cap * 2, (size_t)1 << 20});
@@ -630,6 +641,10 @@ int stage_h2d(pp_ctx* c, void* dst, const void* src, size_t bytes, hipStream_t s
   std::memcpy(c->stage + c->stage_used, src, bytes);
   PP_HIP(hipMemcpyAsync(dst, c->stage + c->stage_used, bytes, hipMemcpyHostToDevice, st));
   c->stage_used += need;
+  if (!c->stage_ev) PP_HIP(hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming));
+  PP_HIP(hipEventRecord(c->stage_ev, st));
+  c->stage_st = st;
+  c->stage_pending = true;
   return PP_OK;
 }
 

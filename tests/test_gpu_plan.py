@@ -156,6 +156,37 @@ def test_plan_device_path_golden(name):
     ctx.close()
 
 
+def test_context_on_alternating_streams():
+    """One context used on two streams in turn, for trees of different
+    sizes (the staged tree-table uploads switch streams, wrap and grow):
+    every plan is the stored one."""
+    import torch
+
+    dev = torch.device("cuda:0")
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    cases = []
+    for name in ("tree2k", "tiny", "rag10k"):
+        inst = W.make_workload(name)
+        t = [torch.from_numpy(a).to(dev) for a in (inst.demand, inst.recompute_cost,
+                                                   inst.fetch_cost)]
+        cases.append((inst, _golden(name), t))
+    torch.cuda.synchronize()
+    ctx = B.Context(0)
+    # (workload, stream): switches, and three rag10k plans in a row on one
+    # stream (more than the staging buffer's first size)
+    for ci, si in ((0, 0), (1, 1), (2, 0), (2, 0), (2, 0), (0, 1), (1, 1)):
+        inst, gold, (lam, w, f) = cases[ci]
+        st = streams[si]
+        with torch.cuda.stream(st):
+            tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+            p = ctx.pp_plan_device(inst.parent, lam, w, f, inst.cap, tgt,
+                                   n_starts=inst.n_starts, max_rounds=inst.max_rounds,
+                                   order_seed=inst.order_seed, stream=st)
+        st.synchronize()
+        _check_golden(inst, gold, p, tgt.cpu().numpy())
+    ctx.close()
+
+
 def test_plan_is_deterministic():
     inst = W.make_workload("tree2k")
     a = B.pp_plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
