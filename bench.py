@@ -556,7 +556,7 @@ def main():
     if args.gpus != 1:
         print("bench.py runs on exactly one GPU: the planner's starts would "
               "shard across GPUs with one exchange of (objective, start) "
-              "pairs, which this build does not run", file=sys.stderr)
+              "pairs, which this implementation does not run", file=sys.stderr)
         sys.exit(2)
 
     import torch
