@@ -1124,127 +1124,20 @@ extern "C" __device__ int pp_writelane_i32(int val, int lane, int old) __asm(
 // Row sets of 32 consecutive rows (windows) are staged in LDS: for window k
 // and lane l, the 16-byte table row of row q_lo + 32k + (l mod 32) at
 // ace + 512k (chain mask, exit row at +4, the exit row's chain mask at +8),
-// and lane l's choice word of cell c at aw + 256(Ck + c).  Exit rows past
-// the last row are kCeEnd.  In window wk the walk reads those into
-// registers, then
-// finds the takes: the next take is the lowest set bit of (word of cell rem
-// & chain mask of q); it is recorded (bit of tm), the walk moves to the row
-// after it and to cell rem-1.  Without a set bit the walk leaves the window
-// at the chain's exit row.  When the window changes, tm goes to lane wk of
-// tw and is cleared.  The walk returns when q reaches n, when rem wraps
-// below zero (it leaves the stage), or when q leaves the super-window
-// (wk >= 16).  On entry wk < 16, q lies in window wk, rem >= 0 and q < n.
-// Every pass raises q, so each window takes at most 32 passes.
+// and the choice word of column l of the 64 columns the pass walks (a plane:
+// a stage of one cell per lane, or a quarter or half of a wider one) at
+// aw + 256k.  Exit rows past the last row are kCeEnd.  In window wk the walk
+// reads those into registers, then finds the takes: the next take is the
+// lowest set bit of (word of column rem & chain mask of q); it is recorded
+// (bit of tm), the walk moves to the row after it and to column rem-1.
+// Without a set bit the walk leaves the window at the chain's exit row.
+// When the window changes, tm goes to lane wk of tw and is cleared.  The
+// walk returns when rem wraps below zero (it leaves the plane) or when q
+// leaves the super-window (wk >= 16; rows past the last one do).  On entry
+// wk < 16, q lies in window wk, 0 <= rem < 64 and q < n.  Every pass raises
+// q, so each window takes at most 32 passes.
 //
-// Two and four cells per lane (one cell per lane: walk_sw_c1 below).
-// Nearly every window change goes to the next window, so two register sets
-// alternate: while the walk uses one (labels 11-19), the other already
-// holds window wk + 1 (labels 21-29); a move to the next window switches
-// sets and starts reading window wk + 2 into the one just left, and only
-// another move (a long skip) waits for LDS.  The lane-select operand of
-// v_writelane is m0 (one scalar operand besides the value); m0 is saved and
-// restored around the walk.
-#define PP_WALK_CE(S, IDX)                                       \
-  "s_lshl_b32 %[off], %[" IDX "], 9\n\t"                         \
-  "v_add_u32_e32 %[va], %[off], %[ace]\n\t"                      \
-  "ds_read_b32 %[ch" S "], %[va]\n\t"                            \
-  "ds_read_b32 %[ex" S "], %[va] offset:4\n\t"
-// window wk + 1, or window 15 when wk is the last one (never walked then)
-#define PP_WALK_NEXT                                             \
-  "s_add_u32 %[nx], %[wk], 1\n\t"                                \
-  "s_min_u32 %[nx], %[nx], 15\n\t"
-#define PP_WALK_ROW                                              \
-  "s_lshl_b32 %[wlo], %[wk], 5\n\t"                              \
-  "s_add_u32 %[wlo], %[wlo], %[qlo]\n\t"                         \
-  "s_sub_u32 %[r], %[q], %[wlo]\n\t"
-// takes inside the window of set S; leaves q at the row after the window's
-// walk (label T+2 / T+3 are the take-exit and no-take exits)
-#define PP_WALK_TAKES(S, T, COLW)                                \
-  COLW                                                           \
-  "v_readlane_b32 %[m], %[ch" S "], %[r]\n\t"                    \
-  T "1:\n\t"                                                     \
-  "s_and_b32 %[m], %[m], %[w]\n\t"                               \
-  "s_cbranch_scc0 " T "3f\n\t"                                   \
-  "s_ff1_i32_b32 %[t], %[m]\n\t"                                 \
-  "s_bitset1_b32 %[tm], %[t]\n\t"                                \
-  "s_add_u32 %[r], %[t], 1\n\t"                                  \
-  "s_sub_u32 %[rem], %[rem], 1\n\t"                              \
-  "s_cbranch_scc1 " T "2f\n\t"                                   \
-  COLW                                                           \
-  "v_readlane_b32 %[m], %[ch" S "], %[r]\n\t"                    \
-  "s_cmp_lg_u32 %[r], 32\n\t"                                    \
-  "s_cbranch_scc1 " T "1b\n\t"                                   \
-  T "2:\n\t"                                                     \
-  "s_add_u32 %[q], %[wlo], %[r]\n\t"                             \
-  "s_branch " T "4f\n\t"                                         \
-  T "3:\n\t"                                                     \
-  "v_readlane_b32 %[q], %[ex" S "], %[r]\n\t"                    \
-  T "4:\n\t"                                                     \
-  "s_cmp_ge_u32 %[q], %[n]\n\t"                                  \
-  "s_cbranch_scc1 99f\n\t"                                       \
-  "s_sub_u32 %[r], %[q], %[qlo]\n\t"                             \
-  "s_lshr_b32 %[r], %[r], 5\n\t"                                 \
-  "s_cmp_eq_u32 %[r], %[wk]\n\t"                                 \
-  "s_cbranch_scc1 " T "5f\n\t"                                   \
-  "s_mov_b32 m0, %[wk]\n\t"                                      \
-  "v_writelane_b32 %[tw], %[tm], m0\n\t"                         \
-  "s_mov_b32 %[tm], 0\n\t"                                       \
-  "s_add_u32 %[t], %[wk], 1\n\t"                                 \
-  "s_mov_b32 %[wk], %[r]\n\t"                                    \
-  "s_cmp_lt_i32 %[rem], 0\n\t"                                   \
-  "s_cbranch_scc1 99f\n\t"                                       \
-  "s_cmp_ge_u32 %[wk], 16\n\t"                                   \
-  "s_cbranch_scc1 99f\n\t"                                       \
-  "s_cmp_eq_u32 %[wk], %[t]\n\t"                                 \
-  "s_cbranch_scc0 10b\n\t"                                       \
-  "s_branch " T "6f\n\t"                                         \
-  T "5:\n\t"                                                     \
-  "s_cmp_lt_i32 %[rem], 0\n\t"                                   \
-  "s_cbranch_scc1 99f\n\t"                                       \
-  "s_branch 10b\n\t"                                             \
-  T "6:\n\t"
-
-// LDW(S, IDX): read window IDX's choice words into set S; COLW(S): the word
-// of cell rem from set S into w
-#define PP_WALK_SW(LDW, COLW)                                    \
-  "s_mov_b32 %[sm0], m0\n\t"                                     \
-  "10:\n\t"                                                      \
-  "s_waitcnt lgkmcnt(0)\n\t"                                     \
-  PP_WALK_CE("P", "wk")                                          \
-  LDW("P", "wk")                                                 \
-  PP_WALK_NEXT                                                   \
-  PP_WALK_CE("N", "nx")                                          \
-  LDW("N", "nx")                                                 \
-  PP_WALK_ROW                                                    \
-  "s_waitcnt lgkmcnt(" PP_WALK_NREAD ")\n\t"                     \
-  "30:\n\t"                                                      \
-  PP_WALK_TAKES("P", "1", COLW("P"))                             \
-  "s_waitcnt lgkmcnt(0)\n\t"                                     \
-  PP_WALK_NEXT                                                   \
-  PP_WALK_CE("P", "nx")                                          \
-  LDW("P", "nx")                                                 \
-  PP_WALK_ROW                                                    \
-  PP_WALK_TAKES("N", "2", COLW("N"))                             \
-  "s_waitcnt lgkmcnt(0)\n\t"                                     \
-  PP_WALK_NEXT                                                   \
-  PP_WALK_CE("N", "nx")                                          \
-  LDW("N", "nx")                                                 \
-  PP_WALK_ROW                                                    \
-  "s_branch 30b\n\t"                                             \
-  "99:\n\t"                                                      \
-  "s_waitcnt lgkmcnt(0)\n\t"                                     \
-  "s_mov_b32 m0, %[sm0]"
-
-#define PP_WALK_OPERANDS                                                          \
-  [q] "+s"(q), [rem] "+s"(rem), [tm] "+s"(tm), [wk] "+s"(wk), [tw] "+v"(tw),      \
-      [r] "=&s"(r), [m] "=&s"(m), [w] "=&s"(w), [t] "=&s"(t), [off] "=&s"(off),   \
-      [wlo] "=&s"(wlo), [nx] "=&s"(nx), [sm0] "=&s"(sm0), [va] "=&v"(va),         \
-      [chP] "=&v"(chP), [exP] "=&v"(exP), [chN] "=&v"(chN), [exN] "=&v"(exN),     \
-      [vb] "=&v"(vb)
-#define PP_WALK_INPUTS \
-  [qlo] "s"(qlo), [n] "s"(n), [ace] "v"(ace), [aw] "v"(aw)
-
-// One cell per lane: the walk keeps the two window sets in fixed registers
+// The walk keeps the two window sets in fixed registers
 // (v48-v51: table rows of set P's window -- chain mask, exit row, the exit
 // row's chain mask --, v56: its choice words; v52-v55 and v57: set N), so
 // one 16-byte LDS read fetches a lane's table row.  A take is the lowest
@@ -1376,78 +1269,6 @@ __device__ __forceinline__ void walk_sw_c1(uint32_t& q, uint32_t& rem, uint32_t&
 #undef PP_W1_NEXT
 #undef PP_W1_LOAD
 
-// two and four cells per lane: cell rem is lane rem/C of word rem mod C
-#define PP_LDW2(S, IDX)                                          \
-  "s_lshl_b32 %[offw], %[" IDX "], 9\n\t"                        \
-  "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"                      \
-  "ds_read_b32 %[w" S "0], %[vb]\n\t"                            \
-  "ds_read_b32 %[w" S "1], %[vb] offset:256\n\t"
-#define PP_COLW2(S)                                              \
-  "s_lshr_b32 %[ln], %[rem], 1\n\t"                              \
-  "v_readlane_b32 %[w], %[w" S "0], %[ln]\n\t"                   \
-  "v_readlane_b32 %[w1], %[w" S "1], %[ln]\n\t"                  \
-  "s_bitcmp1_b32 %[rem], 0\n\t"                                  \
-  "s_cselect_b32 %[w], %[w1], %[w]\n\t"
-
-__device__ __forceinline__ void walk_sw_c2(uint32_t& q, uint32_t& rem, uint32_t& tm,
-                                           uint32_t& wk, uint32_t& tw, uint32_t qlo,
-                                           uint32_t n, uint32_t ace, uint32_t aw) {
-  uint32_t r, m, w, t, off, wlo, nx, sm0, va, chP, exP, chN, exN, vb, offw, ln, w1;
-  uint32_t wP0, wP1, wN0, wN1;
-#define PP_WALK_NREAD "4"
-  asm volatile(PP_WALK_SW(PP_LDW2, PP_COLW2)
-               : PP_WALK_OPERANDS, [offw] "=&s"(offw), [ln] "=&s"(ln), [w1] "=&s"(w1),
-                 [wP0] "=&v"(wP0), [wP1] "=&v"(wP1), [wN0] "=&v"(wN0), [wN1] "=&v"(wN1)
-               : PP_WALK_INPUTS
-               : "scc");
-#undef PP_WALK_NREAD
-}
-
-#define PP_LDW4(S, IDX)                                          \
-  "s_lshl_b32 %[offw], %[" IDX "], 10\n\t"                       \
-  "v_add_u32_e32 %[vb], %[offw], %[aw]\n\t"                      \
-  "ds_read_b32 %[w" S "0], %[vb]\n\t"                            \
-  "ds_read_b32 %[w" S "1], %[vb] offset:256\n\t"                 \
-  "ds_read_b32 %[w" S "2], %[vb] offset:512\n\t"                 \
-  "ds_read_b32 %[w" S "3], %[vb] offset:768\n\t"
-#define PP_COLW4(S)                                              \
-  "s_lshr_b32 %[ln], %[rem], 2\n\t"                              \
-  "v_readlane_b32 %[w], %[w" S "0], %[ln]\n\t"                   \
-  "v_readlane_b32 %[w1], %[w" S "1], %[ln]\n\t"                  \
-  "v_readlane_b32 %[w2], %[w" S "2], %[ln]\n\t"                  \
-  "v_readlane_b32 %[w3], %[w" S "3], %[ln]\n\t"                  \
-  "s_bitcmp1_b32 %[rem], 1\n\t"                                  \
-  "s_cselect_b32 %[w], %[w2], %[w]\n\t"                          \
-  "s_cselect_b32 %[w1], %[w3], %[w1]\n\t"                        \
-  "s_bitcmp1_b32 %[rem], 0\n\t"                                  \
-  "s_cselect_b32 %[w], %[w1], %[w]\n\t"
-
-__device__ __forceinline__ void walk_sw_c4(uint32_t& q, uint32_t& rem, uint32_t& tm,
-                                           uint32_t& wk, uint32_t& tw, uint32_t qlo,
-                                           uint32_t n, uint32_t ace, uint32_t aw) {
-  uint32_t r, m, w, t, off, wlo, nx, sm0, va, chP, exP, chN, exN, vb, offw, ln, w1, w2, w3;
-  uint32_t wP0, wP1, wP2, wP3, wN0, wN1, wN2, wN3;
-#define PP_WALK_NREAD "6"
-  asm volatile(PP_WALK_SW(PP_LDW4, PP_COLW4)
-               : PP_WALK_OPERANDS, [offw] "=&s"(offw), [ln] "=&s"(ln), [w1] "=&s"(w1),
-                 [w2] "=&s"(w2), [w3] "=&s"(w3), [wP0] "=&v"(wP0), [wP1] "=&v"(wP1),
-                 [wP2] "=&v"(wP2), [wP3] "=&v"(wP3), [wN0] "=&v"(wN0), [wN1] "=&v"(wN1),
-                 [wN2] "=&v"(wN2), [wN3] "=&v"(wN3)
-               : PP_WALK_INPUTS
-               : "scc");
-#undef PP_WALK_NREAD
-}
-#undef PP_WALK_OPERANDS
-#undef PP_WALK_INPUTS
-#undef PP_WALK_SW
-#undef PP_WALK_TAKES
-#undef PP_WALK_ROW
-#undef PP_WALK_NEXT
-#undef PP_WALK_CE
-#undef PP_LDW2
-#undef PP_COLW2
-#undef PP_LDW4
-#undef PP_COLW4
 
 // Acceptance (greedy: always; refinement: DP value > incumbent value, which
 // by Proposition 1 is G(T_-h, T'_h) > G(T)) and, when accepted, the walk
@@ -1477,9 +1298,10 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   constexpr int kSw = kWin * kSwWin;    // rows per super-window
   static_assert(kSw == kCeBlock, "the chain table is padded per super-window");
   constexpr int kW = C * 4;             // 16-byte word loads per lane
-  constexpr int kStage = kWave * C;     // cells per stage
   static_assert(kWin == 32 && kSwWin == 16, "the scalar walk's window layout");
-  __shared__ __attribute__((aligned(16))) uint32_t s_words[kSwWin][C][kWave];
+  // choice words by plane (64 consecutive columns of the stage), window and
+  // column within the plane
+  __shared__ __attribute__((aligned(16))) uint32_t s_words[C][kSwWin][kWave];
   // chain mask, exit row, the exit row's chain mask, 0
   __shared__ __attribute__((aligned(16))) uint32_t s_ce[kSw][4];
   const int ci = blockIdx.x;
@@ -1584,13 +1406,23 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
 #pragma unroll
     for (int i = 0; i < 8; ++i) ce[i] = src[i * kWave + lane];
   };
+  // (a load holds sweep lanes 4(l mod 16) .. +3 of one cell c; sweep lane
+  // u's cell c is column uC + c of the stage)
   auto words_to_lds = [&](const pp_u32x4 (&w)[kW]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int k = kSwWin - 1 - (4 * i + lane / 16);
+      if constexpr (C == 1) {
+        *(pp_u32x4*)&s_words[0][k][4 * (lane % 16)] = w[i];
+      } else {
 #pragma unroll
-      for (int c = 0; c < C; ++c)
-        *(pp_u32x4*)&s_words[k][c][4 * (lane % 16)] = w[c * 4 + i];
+        for (int c = 0; c < C; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int col = (4 * (lane % 16) + e) * C + c;
+            s_words[col / kWave][k][col % kWave] = w[c * 4 + i][e];
+          }
+      }
     }
   };
   auto chain_to_lds = [&](const pp_u32x4 (&ce)[8]) {
@@ -1598,9 +1430,10 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     for (int i = 0; i < 8; ++i) ((pp_u32x4*)&s_ce[0][0])[i * kWave + lane] = ce[i];
   };
   // LDS addresses the walk reads from: lane l's row (l mod 32) of window 0
-  // and lane l's word of window 0, cell 0
+  // and the word of column l of window 0 in plane 0 (plane p: + p * kPlane)
   const uint32_t ace = (uint32_t)(size_t)(__attribute__((address_space(3))) uint32_t*)&s_ce[lane % kWin][0];
   const uint32_t aw = (uint32_t)(size_t)(__attribute__((address_space(3))) uint32_t*)&s_words[0][0][lane];
+  constexpr uint32_t kPlane = kSwWin * kWave * sizeof(uint32_t);
   // this super-window's take masks to the bitmap
   auto store_takes = [&](int sw, uint32_t tw) {
     const int idx = sw * kSwWin + lane;
@@ -1608,7 +1441,8 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   };
 
   int q = 0, j = kp;
-  int g = (j - 1) / kStage;
+  int pl = (j - 1) / kWave;  // plane of column j (64 columns each)
+  int g = pl / C;            // its stage
   int sw = 0;
   pp_u32x4 wb[kW];  // next super-window, same stage
   pp_u32x4 wd[kW];  // same super-window, stage below
@@ -1618,32 +1452,37 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
   words_to_lds(wb);
   chain_to_lds(cb);
   __syncthreads();
+  static_assert(C == 1 || C == 2 || C == 4, "one, two or four cells per lane");
   uint32_t tw = 0, tm = 0;
   for (;;) {
     // both successors, in flight while this super-window is walked
     load_words(sw + 1, g, wb);
     if (g > 0) load_words(sw, g - 1, wd);
     load_chain(sw + 1, cb);
-    const int jlo = g * kStage + 1;
-    uint32_t uq = (uint32_t)q, urem = (uint32_t)(j - jlo);
-    uint32_t wk = (uint32_t)(q - sw * kSw) / kWin;
-    if constexpr (C == 1) {
-      walk_sw_c1(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), ace, aw);
-    } else if constexpr (C == 2) {
-      walk_sw_c2(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
-    } else {
-      static_assert(C == 4, "one, two or four cells per lane");
-      walk_sw_c4(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), (uint32_t)n, ace, aw);
+    int sw_n = sw, pl_n = pl;
+    bool done = false;
+    for (;;) {  // the planes of stage g walked inside super-window sw
+      const int jlo = pl * kWave + 1;
+      uint32_t uq = (uint32_t)q, urem = (uint32_t)(j - jlo);
+      uint32_t wk = (uint32_t)(q - sw * kSw) / kWin;
+      walk_sw_c1(uq, urem, tm, wk, tw, (uint32_t)(sw * kSw), ace,
+                 aw + (uint32_t)(pl % C) * kPlane);
+      q = (int)uq;
+      j = jlo + (int)urem;
+      if (q >= n || j == 0) {
+        if (wk < (uint32_t)kSwWin) tw = (uint32_t)pp_writelane_i32((int)tm, (int)wk, (int)tw);
+        store_takes(sw, tw);
+        done = true;
+        break;
+      }
+      // the walk left the plane or the super-window
+      sw_n = q / kSw;
+      pl_n = (j - 1) / kWave;
+      if (C == 1 || sw_n != sw || pl_n / C != g) break;
+      pl = pl_n;  // the next plane of the stage: its words are staged already
     }
-    q = (int)uq;
-    j = jlo + (int)urem;
-    if (q >= n || j == 0) {
-      if (wk < (uint32_t)kSwWin) tw = (uint32_t)pp_writelane_i32((int)tm, (int)wk, (int)tw);
-      store_takes(sw, tw);
-      break;
-    }
-    // the walk left the stage or the super-window
-    const int sw_n = q / kSw, g_n = (j - 1) / kStage;
+    if (done) break;
+    const int g_n = pl_n / C;
     if (sw_n != sw) {
       store_takes(sw, tw);  // the last window's takes are in tw already
       tw = 0;
@@ -1669,6 +1508,7 @@ __global__ void __launch_bounds__(64) k_backtrack(ChainSet set, DevState d,
     __syncthreads();
     sw = sw_n;
     g = g_n;
+    pl = pl_n;
   }
 }
 
