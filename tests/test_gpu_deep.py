@@ -38,7 +38,7 @@ def test_trees_spill():
 
 
 @pytest.mark.parametrize("idx", range(len(TREES)))
-@pytest.mark.parametrize("cells", ["1", "2"])
+@pytest.mark.parametrize("cells", ["1", "2", "4"])
 def test_rooted_dp_deep(oracle_mod, idx, cells, monkeypatch):
     monkeypatch.setenv("PP_DP_CELLS", cells)
     name, parent = TREES[idx]
@@ -54,7 +54,10 @@ def test_rooted_dp_deep(oracle_mod, idx, cells, monkeypatch):
 
 
 @pytest.mark.parametrize("idx", range(len(TREES)))
-def test_plan_deep(oracle_mod, idx):
+@pytest.mark.parametrize("cells", [None, "2", "4"])
+def test_plan_deep(oracle_mod, idx, cells, monkeypatch):
+    if cells:
+        monkeypatch.setenv("PP_DP_CELLS", cells)
     name, parent = TREES[idx]
     rng = np.random.default_rng(900 + idx)
     inst = W.random_instance(0, 3, rng, kmax=300, parent=parent,
