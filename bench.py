@@ -544,6 +544,9 @@ def main():
                     help="skip the real-valued leg")
     ap.add_argument("--no-paper-config", action="store_true",
                     help="skip the leg at the paper's own timing configuration")
+    ap.add_argument("--paper-config-only", action="store_true",
+                    help="only the leg at the paper's own timing configuration "
+                         "(prints its object; for kernel traces of that leg)")
     ap.add_argument("--oracle-full", action="store_true",
                     help="also time one full oracle plan of the workload "
                          "(minutes at 50,000 chunks)")
@@ -568,6 +571,13 @@ def main():
         from paper_2608_01655_amd import build
 
         build.build()
+    if args.paper_config_only:
+        ctx = B.Context(0)
+        out = paper_config_leg(B, W, ctx, max(1, min(args.steps, 3)),
+                               not args.no_cpu_baseline)
+        ctx.close()
+        print(json.dumps({"paper_config": out}), flush=True)
+        return
     inst = W.make_workload(args.workload)
     plan_flags = 0
     if args.safeguards:

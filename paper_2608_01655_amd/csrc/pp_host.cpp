@@ -706,12 +706,15 @@ int ensure_exact(pp_ctx* c, DevState& d, int32_t slots) {
 // Exact objective values of `count` consecutive slots from `first`.
 int read_exact(const DevState& d, int32_t first, int32_t count, hipStream_t st,
                std::vector<uint32_t>& out) {
+  // slot s's G is gx[2s]: one copy of the slots' pairs, then every other
+  std::vector<uint32_t> pairs((size_t)count * 2 * kExLimbs);
+  PP_HIP(hipMemcpyAsync(pairs.data(), d.gx + (size_t)first * 2 * kExLimbs,
+                        pairs.size() * sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+  PP_TRY(poll_stream(st));
   out.assign((size_t)count * kExLimbs, 0);
   for (int32_t q = 0; q < count; ++q)
-    PP_HIP(hipMemcpyAsync(out.data() + (size_t)q * kExLimbs,
-                          d.gx + (size_t)(first + q) * 2 * kExLimbs, kExLimbs * 4,
-                          hipMemcpyDeviceToHost, st));
-  PP_TRY(poll_stream(st));
+    std::memcpy(out.data() + (size_t)q * kExLimbs, pairs.data() + (size_t)q * 2 * kExLimbs,
+                kExLimbs * sizeof(uint32_t));
   return PP_OK;
 }
 
@@ -2103,21 +2106,29 @@ int pp_plan_f64_device(pp_ctx* ctx, int32_t n, int32_t m, const int32_t* parent,
     for (int32_t h = 0; h < m; ++h)
       if (cap[h] < 0) return fail(PP_E_RANGE, "negative capacity");
     TreeLayout t;
-    PP_TRY(build_tree(n, parent, t));
-    if (o.flags & PP_F_VALIDATE_ONLY) return PP_OK;
+    if (o.flags & PP_F_VALIDATE_ONLY) return build_tree(n, parent, t);
     PP_TRY(select_device(ctx));
     hipStream_t st = (hipStream_t)hip_stream;
-    PP_TRY(ctx->flag.ensure(64));
-    PP_HIP(hipMemsetAsync(ctx->flag.p, 0, 4, st));
+    // value checks on the device while the host builds the tree tables
+    PP_TRY(ctx->partial.ensure(2 * kValidateBlocks * 8));
+    PP_TRY(ensure_val_pin(ctx));
+    int32_t nb = 0;
     PP_HIP(launch_validate_f64(demand_dev, recompute_dev, fetch_dev, n, m,
-                               ctx->flag.as<int32_t>(), st));
-    int32_t bad = 0;
-    PP_HIP(hipMemcpyAsync(&bad, ctx->flag.p, 4, hipMemcpyDeviceToHost, st));
-    PP_TRY(poll_stream(st));
-    if (bad) return fail(PP_E_RANGE, "demand and costs must be finite and >= 0");
+                               ctx->partial.as<uint64_t>(), &nb, st));
+    PP_HIP(hipMemcpyAsync(ctx->val_pin, ctx->partial.p, 8 * (size_t)nb,
+                          hipMemcpyDeviceToHost, st));
+    const int trc = build_tree(n, parent, t);
+    if (trc != PP_OK) {
+      PP_TRY(poll_stream(st));
+      return trc;
+    }
+    // the layout does not depend on the checks' outcome
     PP_TRY(upload_tree(ctx, t, st));
     PP_TRY(layout_inputs(ctx, t, m, (const int64_t*)demand_dev,
                          (const int64_t*)recompute_dev, (const int64_t*)fetch_dev, st));
+    PP_TRY(poll_stream(st));
+    for (int32_t b = 0; b < nb; ++b)
+      if (ctx->val_pin[b]) return fail(PP_E_RANGE, "demand and costs must be finite and >= 0");
     PlanResult r;
     PP_TRY(run_plan(ctx, t, m, cap, o, false, st, r, 0, true, epsilon));
     const size_t mn = (size_t)m * n;

@@ -285,10 +285,11 @@ constexpr int kValidateBlocks = 1024;
 hipError_t launch_validate(const int64_t* lam, const int64_t* w,
                            const int64_t* f, int32_t n, int32_t m,
                            uint64_t* partial, int32_t* nblocks, hipStream_t st);
-// real-valued inputs: *bad = 1 if any value is negative, NaN or infinite
+// real-valued inputs, *nblocks (<= 2 kValidateBlocks) blocks: flags[b] = 1
+// if block b saw a negative, NaN or infinite value, else 0
 hipError_t launch_validate_f64(const double* lam, const double* w,
                                const double* f, int32_t n, int32_t m,
-                               int32_t* bad, hipStream_t st);
+                               uint64_t* flags, int32_t* nblocks, hipStream_t st);
 // Exact objective sums (real-valued costs): blocks per chain of k_gexact
 // (128, or enough that no block sums more than 2^30 terms; m * n < 2^39).
 constexpr int kGexactBlocks = 512;

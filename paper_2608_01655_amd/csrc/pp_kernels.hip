@@ -284,7 +284,7 @@ __global__ void k_validate(const int64_t* __restrict__ lam, const int64_t* __res
 __global__ void k_validate_f64(const double* __restrict__ lam,
                                const double* __restrict__ w,
                                const double* __restrict__ f, int64_t mn,
-                               int64_t mmn, int32_t* bad) {
+                               int64_t mmn, uint64_t* flags) {
   bool b = false;
   const int64_t step = (int64_t)gridDim.x * blockDim.x;
   for (int64_t x = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; x < mmn; x += step) {
@@ -296,7 +296,9 @@ __global__ void k_validate_f64(const double* __restrict__ lam,
       b |= !(c >= 0.0 && c <= 1.7976931348623157e308);
     }
   }
-  if (__syncthreads_or(b) && threadIdx.x == 0) atomicOr(bad, 1);
+  // this block's flag (every block writes its own: nothing to clear first)
+  const int any = __syncthreads_or(b ? 1 : 0);
+  if (threadIdx.x == 0) flags[blockIdx.x] = any ? 1 : 0;
 }
 
 __global__ void k_init_slots(ChainSet set, DevState d, int clear_tgt) {
@@ -1963,12 +1965,13 @@ hipError_t launch_validate(const int64_t* lam, const int64_t* w,
 
 hipError_t launch_validate_f64(const double* lam, const double* w,
                                const double* f, int32_t n, int32_t m,
-                               int32_t* bad, hipStream_t st) {
+                               uint64_t* flags, int32_t* nblocks, hipStream_t st) {
   const int64_t mn = (int64_t)m * n, mmn = mn * m;
   int64_t b = (mmn + 255) / 256;
-  if (b > 2048) b = 2048;
+  if (b > 2 * kValidateBlocks) b = 2 * kValidateBlocks;
+  *nblocks = (int32_t)b;
   hipLaunchKernelGGL(k_validate_f64, dim3((unsigned)b), dim3(256), 0, st, lam, w, f,
-                     mn, mmn, bad);
+                     mn, mmn, flags);
   return hipGetLastError();
 }
 
