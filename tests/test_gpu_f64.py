@@ -348,3 +348,44 @@ def test_plan_f64_random_launch_budgets(oracle_mod, monkeypatch, seed):
     g = B.pp_plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
     o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, **kw)
     _same_real(g, o)
+
+
+def test_f64_device_entry_input_errors_then_a_valid_plan(oracle_mod):
+    """Real-valued device entry: a negative, NaN or infinite value in any of
+    the three inputs (late blocks of the check) is PP_E_RANGE, a cyclic
+    parent array PP_E_TREE; the same context then plans valid inputs as the
+    oracle does."""
+    import torch
+
+    rng = np.random.default_rng(32)
+    inst = W.random_instance(3000, 4, rng, kmax=200, shuffle=False)
+    lam, w, f = W.real_valued(inst, 4, jitter=0.5)
+    dev = torch.device("cuda:0")
+    ctx = B.Context(0)
+    tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+    eps = 1e-9 * (float(np.sum(lam * w)) + 1.0)
+
+    def run(a, b, c, parent=inst.parent):
+        t = [torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (a, b, c)]
+        return ctx.pp_plan_f64_device(parent, *t, inst.cap, tgt, epsilon=eps, n_starts=2,
+                                      order_seed=5)
+
+    for which, idx, val in ((0, (3, 2999), -1.0), (1, (2, 1777), float("nan")),
+                            (2, (3, 2, 2998), float("inf"))):
+        arrs = [lam.copy(), w.copy(), f.copy()]
+        arrs[which][idx] = val
+        with pytest.raises(B.PPError) as e:
+            run(*arrs)
+        assert e.value.code == B.PP_E_RANGE
+    cyc = inst.parent.copy(); cyc[0] = 5; cyc[5] = 0
+    with pytest.raises(B.PPError) as e:
+        run(lam, w, f, parent=cyc)
+    assert e.value.code == B.PP_E_TREE
+    import dataclasses
+
+    g = run(lam, w, f)
+    g = dataclasses.replace(g, target=tgt.cpu().numpy())
+    o = oracle_mod.plan_f64(inst.parent, lam, w, f, inst.cap, epsilon=eps, n_starts=2,
+                            order_seed=5)
+    _same_real(g, o)
+    ctx.close()

@@ -333,3 +333,45 @@ def test_stalled_sweep_is_run_again(oracle_mod, monkeypatch):
     osel, oval = oracle_mod.rooted_dp(parent, profit, 900)
     assert val == oval
     np.testing.assert_array_equal(sel, osel)
+
+
+def test_device_entry_input_errors_then_a_valid_plan(oracle_mod):
+    """The device entry's input checks run on the GPU while the host builds
+    the tree tables: a negative demand, recompute or fetch cost anywhere
+    (here in late blocks of the check) is PP_E_RANGE, a sum of demand *
+    recompute cost above INT64_MAX is PP_E_OVERFLOW, a cyclic parent array
+    is PP_E_TREE even when values are bad too; the same context then plans
+    valid inputs exactly as the oracle does."""
+    import torch
+
+    rng = np.random.default_rng(31)
+    inst = W.random_instance(3000, 4, rng, kmax=200, shuffle=False)
+    dev = torch.device("cuda:0")
+    ctx = B.Context(0)
+    tgt = torch.zeros((inst.m, inst.n), dtype=torch.uint8, device=dev)
+
+    def run(lam, w, f, parent=inst.parent):
+        t = [torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in (lam, w, f)]
+        return ctx.pp_plan_device(parent, *t, inst.cap, tgt, n_starts=2, order_seed=5)
+
+    cases = []
+    lam = inst.demand.copy(); lam[3, 2999] = -1; cases.append(((lam, inst.recompute_cost, inst.fetch_cost), B.PP_E_RANGE))
+    w = inst.recompute_cost.copy(); w[2, 1777] = -5; cases.append(((inst.demand, w, inst.fetch_cost), B.PP_E_RANGE))
+    f = inst.fetch_cost.copy(); f[3, 2, 2998] = -1; cases.append(((inst.demand, inst.recompute_cost, f), B.PP_E_RANGE))
+    big = inst.demand.copy(); big[0, :] = 2 ** 40
+    wb = inst.recompute_cost.copy(); wb[0, :] = 2 ** 40
+    cases.append(((big, wb, inst.fetch_cost), B.PP_E_OVERFLOW))
+    for args, code in cases:
+        with pytest.raises(B.PPError) as e:
+            run(*args)
+        assert e.value.code == code
+    cyc = inst.parent.copy(); cyc[0] = 5; cyc[5] = 0
+    with pytest.raises(B.PPError) as e:
+        run(cases[0][0][0], inst.recompute_cost, inst.fetch_cost, parent=cyc)
+    assert e.value.code == B.PP_E_TREE
+    g = run(inst.demand, inst.recompute_cost, inst.fetch_cost)
+    o = oracle_mod.plan(inst.parent, inst.demand, inst.recompute_cost, inst.fetch_cost,
+                        inst.cap, n_starts=2, order_seed=5)
+    assert g.objective == o.objective
+    np.testing.assert_array_equal(tgt.cpu().numpy(), o.target)
+    ctx.close()
