@@ -992,9 +992,6 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
   return PP_OK;
 }
 
-// Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
-// Real-valued costs (f64): every value is the bit pattern of a non-negative
-// double, so the comparisons below (orders, best start) hold unchanged.
 // Coordinate refinement (Algorithm 1's sweeps) of the starts `starts`,
 // after their greedy pass.  Each start keeps its own position and sweep.
 // The host mirrors every start's stale-input marks (ChainState::dirty, the
@@ -1008,7 +1005,9 @@ int run_safeguards(Engine& e, int32_t m, const std::vector<int32_t>& kp,
 // which is the placement each of them sees in Algorithm 1's order as long
 // as every earlier one is rejected.  The first accepted update of a start
 // is adopted and committed; the positions after it are looked at again in
-// the next launch.  Results are those of the sequential sweeps.
+// the next launch.  A start whose sweep has accepted an update goes on into
+// its next sweep the same way once the rest of the sweep is in the launch.
+// Results are those of the sequential sweeps.
 int refine_starts(Engine& e, const std::vector<int32_t>& starts, int32_t spare_base,
                   int32_t budget, int32_t block_budget, int32_t m,
                   const std::vector<int32_t>& kp, int32_t max_rounds, PlanResult& res) {
@@ -1266,6 +1265,9 @@ uint32_t spin_limit_for(int attempt) {
   return (uint32_t)std::min<uint64_t>(v, 1u << 30);
 }
 
+// Algorithm 1 on device-resident, preorder-laid-out inputs in `c`.
+// Real-valued costs (f64): every value is the bit pattern of a non-negative
+// double, so the comparisons below (orders, best start) hold unchanged.
 int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
                   const pp_options& o, bool fmax_ok, hipStream_t st, PlanResult& res,
                   int32_t extra_slots, bool f64, double eps, int attempt) {
