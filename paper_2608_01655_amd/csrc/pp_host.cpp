@@ -1287,13 +1287,16 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   // and LocalDedup candidates, and slots 0..m-1 serve as scratch chains
   const bool sg_asked = (o.flags & PP_F_SAFEGUARDS) != 0;
   const int32_t slot_b = std::max(m, S);
-  // stage blocks a speculative launch may fill: two per compute unit
-  int32_t spec_blocks = 512;
+  // stage blocks a speculative launch may fill: three per compute unit (the
+  // sweep gives each block's compute wave a SIMD of its own where the
+  // placement allows; a fourth block per unit slows every stage on it), and
+  // never more than fit the device at once
+  int32_t spec_blocks = 768;
   {
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device) ==
             hipSuccess && cus > 0)
-      spec_blocks = 2 * cus;
+      spec_blocks = 3 * cus;
     spec_blocks = env_int("PP_SPEC_BLOCKS", spec_blocks);
   }
   // speculative refinement: up to kSpecChains updates per launch (each
@@ -1443,7 +1446,8 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
     for (int32_t a = 1; a < m; ++a)
       PP_TRY(e.update(position_set(active, a), kModeGreedy));
     if (!(o.flags & PP_F_NO_REFINE))
-      PP_TRY(refine_starts(e, active, spare_base, spec_chains, spec_blocks, m, kp,
+      PP_TRY(refine_starts(e, active, spare_base, spec_chains,
+                           std::min(spec_blocks, e.resident), m, kp,
                            o.max_rounds, res));
     std::vector<int32_t> sl, wk, kk;
     for (int32_t s = lo; s < hi; ++s) {

@@ -625,12 +625,23 @@ constexpr int dp_outv_stride() {
 }
 
 // LDS bytes of the sweep's control area: two record buffers, two output
-// buffers (stage-ring values and choice words of a batch) and a flag word.
+// buffers (stage-ring values and choice words of a batch) and four flag
+// words (the two hand-off counters and the waves' role decision).
 template <int C>
 constexpr size_t dp_ctl_bytes() {
   return 2 * (kBatch + 1) * 2 * sizeof(StepView) + 2 * dp_outv_stride<C>() * sizeof(int64_t) +
          2 * C * kWave * sizeof(uint32_t) + 16;
 }
+
+// Compute waves per SIMD: bit s of g_simd_claims[cu] is set while a sweep's
+// compute wave runs on SIMD s of compute unit cu (a key made of the XCD,
+// shader engine, shader array and CU ids; each field is masked to its
+// width, so every key indexes the table).  One table per device, zero at
+// load; every wave that sets a bit clears it before it exits.
+constexpr int kSimdClaimKeys = 1 << 12;
+__device__ uint32_t g_simd_claims[kSimdClaimKeys];
+constexpr int kHwIdReg = (31 << 11) | 4;    // s_getreg: HW_ID, 32 bits
+constexpr int kXccIdReg = (31 << 11) | 20;  // s_getreg: XCC_ID, 32 bits
 
 template <int C, bool FMAX, bool F64>
 __global__ void __launch_bounds__(2 * kWave)
@@ -654,7 +665,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // place for a wave that reads the counter and then the data; compiler
   // fences keep that program order, and no wave waits on the LDS counter.
   int* sync = (int*)(outb + 2 * C * kWave);
-  constexpr int kStaged = 0, kDone = 1;
+  constexpr int kStaged = 0, kDone = 1, kRole = 2;
   // bound on the polls of one LDS wait (the partner wave's own waits are
   // bounded, so this is reached only if the hand-off itself breaks)
   constexpr uint32_t kLdsSpins = 1u << 24;
@@ -668,9 +679,10 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
       __hip_atomic_store(sync + t, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   };
   char* rows = (char*)lds + dp_ctl_bytes<C>();
-  // wave 0 computes the sweep; wave 1 does every global-memory access of
-  // the batch loop, so the compute wave never waits on a memory counter
-  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+  // one wave computes the sweep (role 0); the other does every global-memory
+  // access of the batch loop (role 1), so the compute wave never waits on a
+  // memory counter
+  const int hw_wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   const int lane = threadIdx.x % kWave;
   char* lane_bytes = rows + lane * 8;
   const int blk = blockIdx.x;
@@ -686,12 +698,47 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   const int nsteps = (n + kBatch - 1) / kBatch * kBatch;
   const int nb = nsteps / kBatch;
   const int pad = nsteps - n;  // leading dummy steps
-  // Barrier between the two waves (once, after set-up).  Only LDS is
-  // exchanged through it, so the fences order LDS alone.
+  // Barrier between the two waves.  Only LDS is exchanged through it, so
+  // the fences order LDS alone.
   auto barrier = [&]() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  };
+  // Roles.  The hardware puts the block's two waves on two SIMDs of its
+  // compute unit; with three or more blocks on one compute unit, two
+  // compute waves can share a SIMD, which runs both at about half pace and
+  // holds back both chains.  So the compute role goes to a wave whose SIMD
+  // no other compute wave has claimed: wave 0 if its SIMD is free, else
+  // wave 1 if its SIMD is, else wave 0 without a claim.  (Claiming both at
+  // once and giving one back was slower: the claim a block gives back can
+  // turn another block away from a SIMD that stays free.)
+  const uint32_t hw_id = __builtin_amdgcn_s_getreg(kHwIdReg);
+  const uint32_t cu_key = ((__builtin_amdgcn_s_getreg(kXccIdReg) & 0xFu) << 8) |
+                          (((hw_id >> 13) & 7u) << 5) | (((hw_id >> 12) & 1u) << 4) |
+                          ((hw_id >> 8) & 0xFu);
+  const uint32_t simd_bit = 1u << ((hw_id >> 4) & 3u);
+  uint32_t* const claim = g_simd_claims + cu_key;
+  auto try_claim = [&]() {
+    uint32_t old = 0;
+    if (lane == 0) old = atomicOr(claim, simd_bit);
+    return (__builtin_amdgcn_readfirstlane((int)old) & (int)simd_bit) == 0;
+  };
+  bool claimed = false;
+  if (hw_wave == 0) {
+    claimed = try_claim();
+    if (lane == 0) sync[kRole] = claimed ? 0 : -1;
+  }
+  barrier();
+  if (hw_wave == 1 && __builtin_amdgcn_readfirstlane(sync_load(kRole)) < 0) {
+    claimed = try_claim();
+    if (lane == 0) sync[kRole] = claimed ? 1 : 0;
+  }
+  barrier();
+  const int wave =
+      hw_wave == __builtin_amdgcn_readfirstlane(sync_load(kRole)) ? 0 : 1;
+  auto release_claim = [&]() {
+    if (claimed && lane == 0) atomicAnd(claim, ~simd_bit);
   };
 
   if (wave == 1) {
@@ -1095,6 +1142,7 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     ok = batch(IC<0>{}, b);
     if (ok && b + 1 < nb) ok = batch(IC<1>{}, b + 1);
   }
+  release_claim();
   if (!ok) {
     sync_set(kDone, -1);
     return;
