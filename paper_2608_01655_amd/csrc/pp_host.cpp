@@ -1341,6 +1341,12 @@ int run_plan_once(pp_ctx* c, const TreeLayout& t, int32_t m, const int32_t* cap,
   }
   const int cells = choose_cells((int32_t)std::min<int64_t>(stage64, INT32_MAX),
                                  c->device, e.slots_lds);
+  {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device) ==
+            hipSuccess && cus > 0)
+      d.role_max_blocks = 4 * cus;
+  }
   e.resident = dp_resident_blocks(cells, e.slots_lds, c->device);
   if (attempt > 0 && e.resident > 0) {
     // fewer stage blocks per launch, but every chain's stages in one

@@ -260,6 +260,10 @@ struct DevState {
   uint32_t* gx;
   uint64_t* gxp;
   int32_t gx_blocks;
+  // DP sweeps of at most this many stage blocks choose their waves' roles
+  // by SIMD (0: every sweep); beyond four blocks per compute unit some
+  // SIMDs carry two compute waves whatever the roles
+  int32_t role_max_blocks;
 };
 // kernel arguments stay within the 4 KB that every launch path accepts
 static_assert(sizeof(AdoptSet) + sizeof(DevState) <= 4096, "k_adopt arguments");

@@ -724,10 +724,11 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
     if (lane == 0) old = atomicOr(claim, simd_bit);
     return (__builtin_amdgcn_readfirstlane((int)old) & (int)simd_bit) == 0;
   };
+  const bool roles = d.role_max_blocks == 0 || set.base[set.count] <= d.role_max_blocks;
   bool claimed = false;
   if (hw_wave == 0) {
-    claimed = try_claim();
-    if (lane == 0) sync[kRole] = claimed ? 0 : -1;
+    if (roles) claimed = try_claim();
+    if (lane == 0) sync[kRole] = (claimed || !roles) ? 0 : -1;
   }
   barrier();
   if (hw_wave == 1 && __builtin_amdgcn_readfirstlane(sync_load(kRole)) < 0) {
