@@ -712,7 +712,9 @@ k_dp(ChainSet set, DevState d, uint32_t epoch, uint32_t spin_limit,
   // no other compute wave has claimed: wave 0 if its SIMD is free, else
   // wave 1 if its SIMD is, else wave 0 without a claim.  (Claiming both at
   // once and giving one back was slower: the claim a block gives back can
-  // turn another block away from a SIMD that stays free.)
+  // turn another block away from a SIMD that stays free.)  Launches of more
+  // than d.role_max_blocks blocks skip the claims: some SIMD carries two
+  // compute waves there whatever the roles.
   const uint32_t hw_id = __builtin_amdgcn_s_getreg(kHwIdReg);
   const uint32_t cu_key = ((__builtin_amdgcn_s_getreg(kXccIdReg) & 0xFu) << 8) |
                           (((hw_id >> 13) & 7u) << 5) | (((hw_id >> 12) & 1u) << 4) |
